@@ -1,0 +1,168 @@
+/*
+ * tq.h -- C ABI of the batched state-vector simulation library for MI355X.
+ *
+ * The library runs the circuit-execution hot path of TensorFlow Quantum
+ * (arXiv:2003.02989) on one AMD Instinct MI355X: batched state-vector
+ * simulation of parameterized circuits in complex64, Pauli-sum expectation
+ * values, bitstring sampling and adjoint-method gradients.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Circuits and Pauli sums arrive as flat little-endian blobs (format in
+ *    the description of tq_program_create / tq_observables_create).  A batch
+ *    may mix circuits of different structure and qubit count (the paper's
+ *    ops accept any batch of circuits, Sec. "Sampling and Expectation
+ *    Values").
+ *  - Qubit q of an n-qubit circuit is bit (n-1-q) of an amplitude index and
+ *    of a sampled bitstring: qubit 0 is the most significant bit.
+ *  - Every array argument of the compute calls is a DEVICE pointer owned by
+ *    the caller, and `stream` is a hipStream_t (NULL = the null stream).
+ *    Compute calls only enqueue work on `stream` and return without a host
+ *    synchronisation; inputs and outputs must stay alive until the caller
+ *    synchronises the stream.  Faults of enqueued kernels surface at that
+ *    synchronisation.
+ *  - All validation happens on the host, before anything is enqueued.  On an
+ *    error the outputs are untouched, the call returns a non-zero tq_status
+ *    and tq_last_error() returns a message (thread local).
+ *  - The library owns only its internal workspaces (intermediate states,
+ *    partial sums, fused gate matrices, sampler levels).  They are allocated
+ *    on the device that is current at the first compute call, cached in the
+ *    program handle and freed by tq_program_destroy.
+ *  - Calls on distinct program handles may run from different threads; one
+ *    handle must be used by one thread at a time, and concurrent calls on the
+ *    same handle on different streams race on its workspaces.
+ *  - No C++ exception crosses this boundary.
+ */
+#ifndef TQ_H
+#define TQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tq_program_s *tq_program;
+typedef struct tq_observables_s *tq_observables;
+
+typedef enum {
+    TQ_OK = 0,
+    TQ_E_INVALID = 1,     /* malformed blob or argument: bad magic/version, qubit out of range or repeated,
+                             symbol column >= S, observable qubit >= n_b, null pointer, negative size */
+    TQ_E_UNSUPPORTED = 2, /* unknown opcode, or a problem outside the library's limits (n > 32) */
+    TQ_E_NOMEM = 3,       /* a device workspace could not be allocated */
+    TQ_E_DEVICE = 4       /* a HIP runtime error; its text is in tq_last_error() */
+} tq_status;
+
+/* Planner options; a zero field selects the default.
+ *   max_tile_qubits: log2 of the amplitudes one workgroup stages in LDS per
+ *                    forward pass (default 12, allowed 8..13);
+ *   low_qubits:      contiguous low index bits every tile keeps, so that each
+ *                    wavefront reads runs of 2^low_qubits amplitudes
+ *                    (default 6, allowed 3..8);
+ *   fuse:            1 = fuse neighbouring gates into one matrix (default),
+ *                    -1 = apply every gate on its own. */
+typedef struct {
+    int32_t max_tile_qubits;
+    int32_t low_qubits;
+    int32_t fuse;
+    int32_t reserved;
+} tq_options;
+
+/* Parse, validate and plan a batch of B parameterized circuits over S symbols
+ * (host only; no device call).  Blob:
+ *     "TQP1" u32 version(=1) u32 B u32 S
+ *     per circuit: u32 n_qubits u32 n_gates
+ *       per gate:  u16 opcode u8 nq u8 np u32 qubit[nq]
+ *                  np x { i32 symbol (-1 = constant) f64 scale f64 offset }
+ *                  then 8 f64 for MATRIX1, 32 f64 for MATRIX2 (re, im, row major)
+ * A parameter resolves to eta = scale * symbol_values[b, symbol] + offset, the
+ * affine symbol maps of the paper's chain rule (Sec. "Parameter shift
+ * methods", eq. chain_rule); constants take eta = offset.
+ * Opcodes (Cirq's gate set as the paper uses it; pow gates G^t follow the
+ * phase convention G^t = e^{i pi t/2} (cos(pi t/2) I - i sin(pi t/2) G)):
+ *     1 H  2 X  3 Y  4 Z  5 RX(theta)  6 RY  7 RZ  8 XPOW(t)  9 YPOW  10 ZPOW
+ *     11 CZ  12 CNOT(control, target)  13 CZPOW(t)  14 CNOTPOW(t)  15 XXPOW(t)
+ *     16 YYPOW(t)  17 ZZPOW(t)  18 RZZ(gamma) = exp(-i gamma Z Z / 2)
+ *     19 SQRTX  20 SQRTY  21 SQRTW  22 FSIM(theta, phi)  23 MATRIX1
+ *     24 MATRIX2  25 SWAP
+ * A two-qubit gate on (a, b) uses the local index 2*bit(a) + bit(b).
+ * Circuits may have 0..32 qubits and any number of gates.  `opt` may be NULL.
+ * On success *out owns the parsed program; release it with
+ * tq_program_destroy. */
+tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *opt, tq_program *out);
+void tq_program_destroy(tq_program prog);
+
+/* Batch size, symbol count, largest qubit count, and (when not NULL) the
+ * qubit count of every circuit into qubits_per_circuit[B] (host memory). */
+tq_status tq_program_info(tq_program prog, int32_t *B, int32_t *S, int32_t *max_qubits,
+                          int32_t *qubits_per_circuit);
+
+/* Parse B x K Pauli sums h_{b,k} = sum_t c_t P_t (Sec. "Sampling and
+ * Expectations", eq. cost_lincomb).  Blob:
+ *     "TQO1" u32 version(=1) u32 B u32 K
+ *     per (b, k), row major: u32 T
+ *       per term: f64 coeff u32 n_factors n_factors x { u32 qubit u8 pauli (1=X 2=Y 3=Z) }
+ * An empty factor list is the identity term.  A qubit may appear once per
+ * term; qubit ranges are checked against a program when both are used. */
+tq_status tq_observables_create(const void *blob, size_t nbytes, tq_observables *out);
+void tq_observables_destroy(tq_observables obs);
+tq_status tq_observables_info(tq_observables obs, int32_t *B, int32_t *K);
+
+/* Final state of every circuit (the paper's state op, Sec. "TFQ
+ * architecture"): psi_b = W_G(eta_G) ... W_1(eta_1) |0...0>.
+ * symbol_values: float32 [B, S] row major (may be NULL when S = 0).
+ * states: complex64 [B, 2^max_qubits] (interleaved re, im); row b holds
+ * 2^{n_b} amplitudes followed by zeros. */
+tq_status tq_simulate_state(tq_program prog, const float *symbol_values, void *states, void *stream);
+
+/* Expectation values out[b, k] = <psi_b| h_{b,k} |psi_b> (Sec. "Sampling and
+ * Expectations", eq. qee_lincomb), float32 [B, K].  The imaginary part, zero
+ * for Hermitian h, is dropped. */
+tq_status tq_expectation(tq_program prog, const float *symbol_values, tq_observables obs, float *out,
+                         void *stream);
+
+/* n_shots bitstrings per circuit drawn from |psi_b,i|^2 (Sec. "Sampling and
+ * Expectation Values"), uint64 [B, n_shots], bitstring i packed with qubit q at
+ * bit n_b-1-q.  Rule (integer, order independent): p_i = re^2 + im^2 of the
+ * complex64 amplitude in float64, w_i = floor(p_i 2^62), W = sum_i w_i,
+ * u_k = SplitMix64 output number (b * n_shots + k) of the stream started at
+ * `seed`, r_k = floor(u_k W / 2^64), and shot k is the unique i with
+ * C_i <= r_k < C_i + w_i where C is the exclusive prefix sum of w.
+ * n_shots >= 0; a row with W = 0 yields all-zero bitstrings. */
+tq_status tq_sample(tq_program prog, const float *symbol_values, int64_t n_shots, uint64_t seed,
+                    uint64_t *out, void *stream);
+
+/* Adjoint-method gradient (Sec. "Adjoint Gradient Backpropagation in
+ * Simulations") of sum_k upstream[b,k] <h_{b,k}> with respect to every symbol
+ * value: with H_g = sum_k g_k h_k (Sec. "Autodifferentiation through hybrid
+ * quantum-classical backpropagation") it computes phi = H_g psi, then walks
+ * the gates backwards, psi <- W^dagger psi, grad += scale * 2 Re <phi| dW/deta
+ * |psi>, phi <- W^dagger phi.  A symbol used by several gates sums their
+ * contributions (eq. chain_rule).
+ * upstream: float32 [B, K]; grad: float32 [B, S] (overwritten);
+ * expectations: float32 [B, K] or NULL -- when given it also receives
+ * <h_{b,k}>, from the same forward pass. */
+tq_status tq_adjoint_grad(tq_program prog, const float *symbol_values, tq_observables obs,
+                          const float *upstream, float *grad, float *expectations, void *stream);
+
+/* Amplitudes <x_{b,m}|psi_b> at M bitstrings per circuit: bitstrings uint64
+ * [B, M] (each < 2^{n_b}, checked on the device: an out-of-range entry yields
+ * a zero amplitude), amps complex64 [B, M]. */
+tq_status tq_amplitudes(tq_program prog, const float *symbol_values, const uint64_t *bitstrings, int64_t M,
+                        void *amps, void *stream);
+
+/* The sampling rule of tq_sample applied to given states: complex64
+ * [B, 2^n] device array.  Deterministic and bit-exact for a given input. */
+tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
+                               uint64_t *out, void *stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *tq_last_error(void);
+const char *tq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TQ_H */

@@ -1,0 +1,143 @@
+// kernels.h -- argument blocks and launchers of the libtq kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "tq_internal.h"
+
+namespace tq {
+
+constexpr int kTermChunk = 256;  // terms whose partial sums one expectation sweep accumulates
+constexpr int kMaxLevels = 8;    // sampler levels (64-ary), enough for 2^48 amplitudes
+
+struct BuildArgs {
+    const BuildTask *tasks;
+    int task_begin, task_end;
+    const Member *members;
+    const GateDev *gates;
+    const int32_t *slot_sym;
+    const double *slot_scale, *slot_off;
+    int uniform, n_slots;
+    const double *explicit_mats;
+    const float *theta;
+    int S;
+    const int32_t *rows;
+    float2 *mats;
+    int64_t mat_stride;
+};
+
+struct PassArgs {
+    float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;
+    const float2 *mats;
+    int64_t mat_stride;
+    const PassOp *ops;
+    int nops;
+    TileGeom g;
+    int tiles_log2;
+    int wg_per_row;
+    int product_init;
+    int32_t init_mat[kMaxQubits];
+};
+
+struct ExpArgs {
+    const float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;
+    const TermDev *terms;
+    const int32_t *row_term_begin, *row_term_count;
+    TileGeom g;
+    int tiles_log2, wg_per_row;
+    double *partial;  // [nrows][wg_per_row][tmax]
+    int tmax;
+};
+
+struct ExpReduceArgs {
+    const int32_t *rows;
+    const TermDev *terms;
+    const int32_t *row_term_begin, *row_term_count;
+    const double *partial;
+    int wg_per_row, tmax, K;
+    float *out;
+};
+
+struct HArgs {
+    const float2 *psi;
+    float2 *phi;
+    int64_t row_stride;
+    const int32_t *rows;   // state rows
+    const int32_t *brows;  // batch index of each row (upstream)
+    const TermDev *terms;
+    const int32_t *row_term_begin, *row_term_count;
+    const float *upstream;
+    int K;
+    TileGeom g;
+    int tiles_log2, wg_per_row;
+};
+
+struct RevArgs {
+    float2 *psi, *phi;
+    int64_t row_stride;
+    const int32_t *rows;
+    const float2 *mats;
+    int64_t mat_stride;
+    const PassOp *ops;
+    int nops;
+    TileGeom g;
+    int tiles_log2, wg_per_row;
+    int store;
+    double *gpart;  // [nrows][wg_per_row][n_gslots]
+    int n_gslots, gbase, gcount;
+};
+
+struct GradReduceArgs {
+    const int32_t *rows;
+    const double *gpart;
+    int wg_per_row, n_gslots;
+    const int32_t *sym_begin, *sym_gslots, *gslot_slot;
+    const double *slot_scale;
+    int uniform, n_slots;
+    int S;
+    float *grad;
+};
+
+struct SampArgs {
+    const float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;   // state rows (NULL: the row index)
+    const int32_t *brows;  // batch index of each row (NULL: the row index)
+    uint64_t *levels;
+    int64_t row_level;  // entries per row
+    int nlev;           // stored levels 1..nlev; level nlev has at most 64 entries
+    int64_t count[kMaxLevels + 1];
+    int64_t off[kMaxLevels + 1];
+    int64_t n_shots;
+    uint64_t seed;
+    uint64_t *out;
+};
+
+struct GatherArgs {
+    const float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;   // state rows
+    const int32_t *brows;  // batch index of each row
+    int n;
+    const uint64_t *bits;
+    int64_t M;
+    float2 *out;
+};
+
+size_t pass_lds_bytes(const TileGeom &g, bool product_init);
+hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
+hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
+hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s);
+hipError_t launch_expect_reduce(const ExpReduceArgs &a, int nrows, hipStream_t s);
+hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s);
+hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s);
+hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s);
+hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s);
+hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s);
+hipError_t launch_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int nrows, int64_t from,
+                            int64_t to, hipStream_t s);
+
+} // namespace tq

@@ -1,0 +1,996 @@
+// kernels.hip -- HIP kernels of libtq for CDNA4 (gfx950), wave64.
+//
+// State vectors are complex64 (float2) rows of 2^n amplitudes in HBM.  Every
+// sweep over a state is a tile kernel: a 256-thread workgroup stages tiles of
+// 2^t amplitudes in LDS (t index bits = the `c` lowest bits, so that each
+// wavefront reads contiguous runs, plus `h` high bits), works on them and
+// writes them back.  Gate matrices are resolved from the symbol values and
+// pre-multiplied (fused) in float64 by a separate builder kernel and rounded
+// once to complex64.  All reductions are two-stage and fixed-order (no
+// floating-point atomics), so every output is bitwise reproducible.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace tq {
+
+// ------------------------------------------------------------ small helpers
+__device__ __forceinline__ float2 cmul(float2 a, float2 b)
+{
+    return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 cmul2(float2 m0, float2 a0, float2 m1, float2 a1)
+{
+    return make_float2(m0.x * a0.x - m0.y * a0.y + m1.x * a1.x - m1.y * a1.y,
+                       m0.x * a0.y + m0.y * a0.x + m1.x * a1.y + m1.y * a1.x);
+}
+// insert a zero bit at position k of p
+__device__ __forceinline__ uint32_t ins0(uint32_t p, int k) { return ((p >> k) << (k + 1)) | (p & ((1u << k) - 1)); }
+
+// deposit the low bits of v at the set bits of mask
+__device__ uint64_t pdep64(uint64_t v, uint64_t mask)
+{
+    uint64_t r = 0;
+    for (int k = 0; mask; k++) {
+        uint64_t low = mask & (~mask + 1);
+        if ((v >> k) & 1) r |= low;
+        mask ^= low;
+    }
+    return r;
+}
+
+__device__ __forceinline__ double wave_sum(double v)
+{
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// parity of popcount
+__device__ __forceinline__ int par64(uint64_t v) { return __popcll(v) & 1; }
+__device__ __forceinline__ int par32(uint32_t v) { return __popc(v) & 1; }
+
+// ---------------------------------------------------- gate matrices (fp64)
+// Closed forms of the opcode set, written from the gate definitions: for an
+// involutory generator G, G^t = (1+w)/2 I + (1-w)/2 G with w = e^{i pi t}
+// (the phase convention e^{i pi t/2}(cos(pi t/2) I - i sin(pi t/2) G)), and a
+// rotation exp(-i theta G / 2) = cos(theta/2) I - i sin(theta/2) G.
+struct cd {
+    double x, y;
+};
+__device__ __forceinline__ cd C(double x, double y) { return cd{x, y}; }
+__device__ __forceinline__ cd cdmul(cd a, cd b) { return cd{a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x}; }
+__device__ __forceinline__ cd cdadd(cd a, cd b) { return cd{a.x + b.x, a.y + b.y}; }
+__device__ __forceinline__ cd cdscale(cd a, double s) { return cd{a.x * s, a.y * s}; }
+
+// m: row-major d x d, zero-initialised by the caller
+__device__ int gate_matrix_dev(int op, const double *eta, const double *ex, int form, cd *m)
+{
+    const double r = 0.70710678118654752440;
+    double c, s;
+    switch (op) {
+    case OP_H: m[0] = C(r, 0); m[1] = C(r, 0); m[2] = C(r, 0); m[3] = C(-r, 0); return 2;
+    case OP_X: m[1] = C(1, 0); m[2] = C(1, 0); return 2;
+    case OP_Y: m[1] = C(0, -1); m[2] = C(0, 1); return 2;
+    case OP_Z: m[0] = C(1, 0); m[3] = C(-1, 0); return 2;
+    case OP_RX:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(c, 0); m[1] = C(0, -s); m[2] = C(0, -s); m[3] = C(c, 0); return 2;
+    case OP_RY:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(c, 0); m[1] = C(-s, 0); m[2] = C(s, 0); m[3] = C(c, 0); return 2;
+    case OP_RZ:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(c, -s); m[3] = C(c, s); return 2;
+    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_SQRTX: case OP_SQRTY: case OP_SQRTW: {
+        double t = (op == OP_SQRTX || op == OP_SQRTY || op == OP_SQRTW) ? 0.5 : eta[0];
+        sincospi(t, &s, &c);
+        cd a = C(0.5 * (1 + c), 0.5 * s);   // (1 + w) / 2
+        cd bq = C(0.5 * (1 - c), -0.5 * s); // (1 - w) / 2
+        if (op == OP_ZPOW) { m[0] = C(1, 0); m[3] = C(c, s); return 2; }
+        m[0] = a; m[3] = a;
+        if (op == OP_XPOW || op == OP_SQRTX) { m[1] = bq; m[2] = bq; }
+        else if (op == OP_YPOW || op == OP_SQRTY) { m[1] = cdmul(bq, C(0, -1)); m[2] = cdmul(bq, C(0, 1)); }
+        else { m[1] = cdmul(bq, C(r, -r)); m[2] = cdmul(bq, C(r, r)); } // W = [[0, e^{-i pi/4}], [e^{i pi/4}, 0]]
+        return 2;
+    }
+    case OP_CZ:
+        m[0] = m[5] = m[10] = C(1, 0); m[15] = C(-1, 0); return 4;
+    case OP_CZPOW:
+        sincospi(eta[0], &s, &c);
+        m[0] = m[5] = m[10] = C(1, 0); m[15] = C(c, s); return 4;
+    case OP_CNOT:
+        if (form == FORM_CBLOCK) { m[1] = m[2] = C(1, 0); return 2; }
+        m[0] = m[5] = C(1, 0); m[11] = m[14] = C(1, 0); return 4;
+    case OP_CNOTPOW: {
+        sincospi(eta[0], &s, &c);
+        cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
+        if (form == FORM_CBLOCK) { m[0] = m[3] = a; m[1] = m[2] = bq; return 2; }
+        m[0] = m[5] = C(1, 0); m[10] = m[15] = a; m[11] = m[14] = bq; return 4;
+    }
+    case OP_XXPOW: case OP_YYPOW: {
+        sincospi(eta[0], &s, &c);
+        cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
+        m[0] = m[5] = m[10] = m[15] = a;
+        if (op == OP_XXPOW) { m[3] = m[6] = m[9] = m[12] = bq; }
+        else { m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq; } // YY: -|11><00| - |00><11| + |10><01| + |01><10|
+        return 4;
+    }
+    case OP_ZZPOW:
+        sincospi(eta[0], &s, &c);
+        m[0] = m[15] = C(1, 0); m[5] = m[10] = C(c, s); return 4;
+    case OP_RZZ:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = m[15] = C(c, -s); m[5] = m[10] = C(c, s); return 4;
+    case OP_FSIM:
+        sincos(eta[0], &s, &c);
+        m[0] = C(1, 0); m[5] = m[10] = C(c, 0); m[6] = m[9] = C(0, -s);
+        sincos(eta[1], &s, &c);
+        m[15] = C(c, -s); return 4;
+    case OP_SWAP:
+        m[0] = m[6] = m[9] = m[15] = C(1, 0); return 4;
+    case OP_MATRIX1:
+        for (int i = 0; i < 4; i++) m[i] = C(ex[2 * i], ex[2 * i + 1]);
+        return 2;
+    case OP_MATRIX2:
+        for (int i = 0; i < 16; i++) m[i] = C(ex[2 * i], ex[2 * i + 1]);
+        return 4;
+    }
+    return 0;
+}
+
+// derivative with respect to parameter `which` (m zero-initialised)
+__device__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd *m)
+{
+    double c, s;
+    const double pi = 3.14159265358979323846;
+    switch (op) {
+    case OP_RX:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(-0.5 * s, 0); m[1] = C(0, -0.5 * c); m[2] = C(0, -0.5 * c); m[3] = C(-0.5 * s, 0); return 2;
+    case OP_RY:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(-0.5 * s, 0); m[1] = C(-0.5 * c, 0); m[2] = C(0.5 * c, 0); m[3] = C(-0.5 * s, 0); return 2;
+    case OP_RZ:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = C(-0.5 * s, -0.5 * c); m[3] = C(-0.5 * s, 0.5 * c); return 2;
+    case OP_RZZ:
+        sincos(eta[0] * 0.5, &s, &c);
+        m[0] = m[15] = C(-0.5 * s, -0.5 * c); m[5] = m[10] = C(-0.5 * s, 0.5 * c); return 4;
+    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW:
+    case OP_XXPOW: case OP_YYPOW: case OP_ZZPOW: {
+        // d/dt G^t = (i pi w / 2)(I - G), w = e^{i pi t}
+        sincospi(eta[0], &s, &c);
+        cd k = C(-0.5 * pi * s, 0.5 * pi * c);  // i pi w / 2
+        cd mk = cdscale(k, -1);
+        switch (op) {
+        case OP_XPOW: m[0] = m[3] = k; m[1] = m[2] = mk; return 2;
+        case OP_YPOW: m[0] = m[3] = k; m[1] = cdmul(mk, C(0, -1)); m[2] = cdmul(mk, C(0, 1)); return 2;
+        case OP_ZPOW: m[3] = cdscale(k, 2); return 2;
+        case OP_CZPOW: m[15] = cdscale(k, 2); return 4;
+        case OP_CNOTPOW:
+            if (form == FORM_CBLOCK) { m[0] = m[3] = k; m[1] = m[2] = mk; return 2; }
+            m[10] = m[15] = k; m[11] = m[14] = mk; return 4;
+        case OP_XXPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[6] = m[9] = m[12] = mk; return 4;
+        case OP_YYPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[12] = k; m[6] = m[9] = mk; return 4;
+        case OP_ZZPOW: m[5] = m[10] = cdscale(k, 2); return 4;
+        }
+        return 0;
+    }
+    case OP_FSIM:
+        if (which == 0) {
+            sincos(eta[0], &s, &c);
+            m[5] = m[10] = C(-s, 0); m[6] = m[9] = C(0, -c);
+        } else {
+            sincos(eta[1], &s, &c);
+            m[15] = C(-s, -c);  // -i e^{-i phi}
+        }
+        return 4;
+    }
+    return 0;
+}
+
+// permutation of a 4x4 two-qubit matrix for reversed qubit order (|ab> -> |ba>)
+__device__ void swap_qubits4(cd *m)
+{
+    const int pm[4] = {0, 2, 1, 3};
+    cd t[16];
+    for (int i = 0; i < 4; i++)
+        for (int j = 0; j < 4; j++) t[pm[i] * 4 + pm[j]] = m[i * 4 + j];
+    for (int i = 0; i < 16; i++) m[i] = t[i];
+}
+
+// --------------------------------------------------- matrix build kernel
+// One thread per (row, task): symbol resolution eta = scale*theta + offset
+// and the fused product / dagger / derivative in float64, stored complex64.
+__global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
+{
+    const int row = blockIdx.y;
+    const int ti = blockIdx.x * blockDim.x + threadIdx.x + a.task_begin;
+    if (ti >= a.task_end) return;
+    const BuildTask bt = a.tasks[ti];
+    const int b = a.rows[row];
+    const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots);
+    const double *off = a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots);
+    const float *theta = a.theta + (int64_t)b * a.S;
+    const int d = bt.dim;
+    cd acc[16], g[16];
+    for (int i = 0; i < 16; i++) acc[i] = C(0, 0);
+    for (int i = 0; i < d; i++) acc[i * d + i] = C(1, 0);
+    for (int mi = 0; mi < bt.mem_count; mi++) {
+        const Member mem = a.members[bt.mem_begin + mi];
+        const GateDev gd = a.gates[mem.gate];
+        double eta[2] = {0, 0};
+        for (int j = 0; j < gd.np; j++) {
+            int slot = gd.slot0 + j;
+            int sy = a.slot_sym[slot];
+            eta[j] = sy >= 0 ? scale[slot] * (double)theta[sy] + off[slot] : off[slot];
+        }
+        const double *ex = gd.explicit_ >= 0 ? a.explicit_mats + 32 * gd.explicit_ : nullptr;
+        for (int i = 0; i < 16; i++) g[i] = C(0, 0);
+        int gdim;
+        if (bt.kind == BT_DERIV) gdim = gate_deriv_dev(gd.op, eta, bt.which, mem.form, g);
+        else gdim = gate_matrix_dev(gd.op, eta, ex, mem.form, g);
+        if (gdim != d) continue;  // the planner never mixes dimensions
+        if (mem.swapped) swap_qubits4(g);
+        if (bt.kind == BT_DAGGER) {
+            for (int i = 0; i < d; i++)
+                for (int j = 0; j < d; j++) acc[i * d + j] = C(g[j * d + i].x, -g[j * d + i].y);
+        } else if (bt.kind == BT_DERIV) {
+            for (int i = 0; i < d * d; i++) acc[i] = g[i];
+        } else {
+            cd t[16];
+            for (int i = 0; i < d; i++)
+                for (int j = 0; j < d; j++) {
+                    cd sacc = C(0, 0);
+                    for (int k = 0; k < d; k++) sacc = cdadd(sacc, cdmul(g[i * d + k], acc[k * d + j]));
+                    t[i * d + j] = sacc;
+                }
+            for (int i = 0; i < d * d; i++) acc[i] = t[i];
+        }
+    }
+    float2 *out = a.mats + (int64_t)row * a.mat_stride + bt.out;
+    if (bt.diag) {
+        for (int i = 0; i < d; i++) out[i] = make_float2((float)acc[i * d + i].x, (float)acc[i * d + i].y);
+    } else {
+        for (int i = 0; i < d * d; i++) out[i] = make_float2((float)acc[i].x, (float)acc[i].y);
+    }
+}
+
+// ------------------------------------------------------------ tile access
+struct TileCtx {
+    const TileGeom *g;
+    const uint64_t *hi_off;  // LDS table: global offset of each high-bit combination
+    uint32_t lowmask;
+};
+
+__device__ __forceinline__ uint64_t tile_index(const TileCtx &tc, uint64_t fb, uint32_t l)
+{
+    return fb | (l & tc.lowmask) | tc.hi_off[l >> tc.g->c];
+}
+
+// copy a tile between HBM and LDS; two amplitudes per float4 when c >= 1
+template <bool kLoad>
+__device__ __forceinline__ void tile_copy(const TileCtx &tc, float2 *lds, float2 *row, uint64_t fb, int T)
+{
+    if (tc.g->c >= 1) {
+        for (int l = 2 * threadIdx.x; l < T; l += 2 * blockDim.x) {
+            float4 *p = reinterpret_cast<float4 *>(row + tile_index(tc, fb, l));
+            if (kLoad) {
+                float4 v = *p;
+                lds[l] = make_float2(v.x, v.y);
+                lds[l + 1] = make_float2(v.z, v.w);
+            } else {
+                *p = make_float4(lds[l].x, lds[l].y, lds[l + 1].x, lds[l + 1].y);
+            }
+        }
+    } else {
+        for (int l = threadIdx.x; l < T; l += blockDim.x) {
+            if (kLoad) lds[l] = row[tile_index(tc, fb, l)];
+            else row[tile_index(tc, fb, l)] = lds[l];
+        }
+    }
+}
+
+__device__ void build_hi_off(const TileGeom &g, uint64_t *hi_off)
+{
+    for (int j = threadIdx.x; j < (1 << g.h); j += blockDim.x) {
+        uint64_t o = 0;
+        for (int k = 0; k < g.h; k++)
+            if ((j >> k) & 1) o |= 1ull << g.hb[k];
+        hi_off[j] = o;
+    }
+}
+
+__device__ __forceinline__ int bit_of(uint8_t loc, uint8_t pos, uint32_t l, uint64_t fb)
+{
+    return loc != kFixed ? (int)((l >> loc) & 1) : (int)((fb >> pos) & 1);
+}
+
+// ------------------------------------------------------ forward tile ops
+__device__ void apply_op(const PassOp &op, const float2 *__restrict__ m, float2 *lds, int t, uint64_t fb)
+{
+    const uint32_t T = 1u << t;
+    const int tid = threadIdx.x, nt = blockDim.x;
+    if (op.kind == K_M1) {
+        const float2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+        const int tb = op.l0;
+        if (op.ctrl && op.l1 != kFixed) {
+            const int cb = op.l1;
+            const int lo = min(tb, cb), hi = max(tb, cb);
+            const uint32_t cv = (uint32_t)op.cval << cb;
+            for (uint32_t p = tid; p < T / 4; p += nt) {
+                uint32_t i = ins0(ins0(p, lo), hi) | cv, j = i | (1u << tb);
+                float2 a0 = lds[i], a1 = lds[j];
+                lds[i] = cmul2(m00, a0, m01, a1);
+                lds[j] = cmul2(m10, a0, m11, a1);
+            }
+            return;
+        }
+        if (op.ctrl && (int)((fb >> op.p1) & 1) != op.cval) return;
+        for (uint32_t p = tid; p < T / 2; p += nt) {
+            uint32_t i = ins0(p, tb), j = i | (1u << tb);
+            float2 a0 = lds[i], a1 = lds[j];
+            lds[i] = cmul2(m00, a0, m01, a1);
+            lds[j] = cmul2(m10, a0, m11, a1);
+        }
+    } else if (op.kind == K_M2) {
+        float2 mm[16];
+        for (int i = 0; i < 16; i++) mm[i] = m[i];
+        const int b0 = op.l0, b1 = op.l1;
+        const int lo = min(b0, b1), hi = max(b0, b1);
+        for (uint32_t p = tid; p < T / 4; p += nt) {
+            uint32_t i00 = ins0(ins0(p, lo), hi);
+            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
+            float2 v0 = lds[i00], v1 = lds[i01], v2 = lds[i10], v3 = lds[i11];
+            lds[i00] = cadd(cmul2(mm[0], v0, mm[1], v1), cmul2(mm[2], v2, mm[3], v3));
+            lds[i01] = cadd(cmul2(mm[4], v0, mm[5], v1), cmul2(mm[6], v2, mm[7], v3));
+            lds[i10] = cadd(cmul2(mm[8], v0, mm[9], v1), cmul2(mm[10], v2, mm[11], v3));
+            lds[i11] = cadd(cmul2(mm[12], v0, mm[13], v1), cmul2(mm[14], v2, mm[15], v3));
+        }
+    } else {  // diagonal K_D1 / K_D2
+        const bool two = op.kind == K_D2;
+        float2 d[4];
+        for (int i = 0; i < (two ? 4 : 2); i++) d[i] = m[i];
+        for (uint32_t l = tid; l < T; l += nt) {
+            int idx = bit_of(op.l0, op.p0, l, fb);
+            if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
+            lds[l] = cmul(d[idx], lds[l]);
+        }
+    }
+}
+
+// ------------------------------------------------------- forward pass
+__global__ __launch_bounds__(256) void k_pass(PassArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const TileGeom &g = a.g;
+    const int t = g.t;
+    const int T = 1 << t;
+    float2 *lds = reinterpret_cast<float2 *>(smem);
+    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
+    float2 *p1 = reinterpret_cast<float2 *>(hi_off + (1 << g.h));
+    const int a1 = t / 2;
+    float2 *p2 = p1 + (1 << a1);
+
+    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
+    const int b = a.rows[row];
+    float2 *st = a.state + (int64_t)b * a.row_stride;
+    const float2 *M = a.mats + (int64_t)row * a.mat_stride;
+    build_hi_off(g, hi_off);
+    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+
+    if (a.product_init) {
+        // per-qubit product-state vectors: column 0 of each init matrix
+        for (int j = threadIdx.x; j < (1 << a1) + (1 << (t - a1)); j += blockDim.x) {
+            const bool first = j < (1 << a1);
+            const int k0 = first ? 0 : a1, k1 = first ? a1 : t;
+            const int v = first ? j : j - (1 << a1);
+            float2 acc = make_float2(1.f, 0.f);
+            for (int k = k0; k < k1; k++) {
+                int pos = k < g.c ? k : g.hb[k - g.c];
+                int q = g.n - 1 - pos;
+                const float2 *im = M + a.init_mat[q];
+                acc = cmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
+            }
+            if (first) p1[v] = acc;
+            else p2[v] = acc;
+        }
+    }
+    __syncthreads();
+
+    const int64_t ntiles = (int64_t)1 << a.tiles_log2;
+    for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
+        const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
+        if (a.product_init) {
+            float2 f = make_float2(1.f, 0.f);
+            for (uint64_t fm = g.fixed_mask; fm; fm &= fm - 1) {
+                int pos = __ffsll((unsigned long long)fm) - 1;
+                const float2 *im = M + a.init_mat[g.n - 1 - pos];
+                f = cmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
+            }
+            for (int l = threadIdx.x; l < T; l += blockDim.x)
+                lds[l] = cmul(f, cmul(p1[l & ((1 << a1) - 1)], p2[l >> a1]));
+        } else {
+            tile_copy<true>(tc, lds, st, fb, T);
+        }
+        __syncthreads();
+        for (int oi = 0; oi < a.nops; oi++) {
+            const PassOp op = a.ops[oi];
+            apply_op(op, M + op.mat, lds, t, fb);
+            __syncthreads();
+        }
+        tile_copy<false>(tc, lds, st, fb, T);
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------- expectation partials
+// Term t on a tile with fixed bits fb:
+//   x == 0:   sum_l (-1)^{|g(l) & z|} |psi_l|^2
+//   x != 0:   pairs (i, j = i ^ x) with bit m(x) of i clear contribute
+//             2 Re(i^{ny} (-1)^{|j & z|} conj(psi_i) psi_j)
+// where m is the lowest set bit of x's in-tile part (partner in LDS) or, when
+// x flips fixed bits, of its out-of-tile part (partner tile in HBM, and only
+// tiles with that bit clear count the pair).
+__device__ __forceinline__ double re_iny(int ny, double s, float2 A)
+{
+    switch (ny & 3) {
+    case 0: return s * A.x;
+    case 1: return -s * A.y;
+    case 2: return -s * A.x;
+    default: return s * A.y;
+    }
+}
+
+__device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const float2 *lds, const float2 *row, uint64_t fb,
+                                int t)
+{
+    const uint32_t T = 1u << t;
+    const int tid = threadIdx.x, nt = blockDim.x;
+    double acc = 0;
+    if (tm.x == 0) {
+        const int zf = par64(fb & tm.z);
+        for (uint32_t l = tid; l < T; l += nt) {
+            float2 v = lds[l];
+            double pr = (double)v.x * v.x + (double)v.y * v.y;
+            acc += ((zf ^ par32(l & tm.zl)) ? -pr : pr);
+        }
+    } else if (tm.xout == 0) {
+        const int zf = par64(fb & tm.z);
+        const int mb = __ffs(tm.xl) - 1;
+        for (uint32_t p = tid; p < T / 2; p += nt) {
+            uint32_t i = ins0(p, mb), j = i ^ tm.xl;
+            float2 a = lds[i], c = lds[j];
+            float2 A = make_float2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);  // conj(a) c
+            double s = (zf ^ par32(j & tm.zl)) ? -2.0 : 2.0;
+            acc += re_iny(tm.ny, s, A);
+        }
+    } else {
+        const int mb = __ffsll((unsigned long long)tm.xout) - 1;
+        if ((fb >> mb) & 1) return 0.0;
+        const uint64_t fj = fb ^ tm.xout;
+        const int zf = par64(fj & tm.z);
+        for (uint32_t l = tid; l < T; l += nt) {
+            uint32_t lj = l ^ tm.xl;
+            float2 a = lds[l], c = row[tile_index(tc, fj, lj)];
+            float2 A = make_float2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);
+            double s = (zf ^ par32(lj & tm.zl)) ? -2.0 : 2.0;
+            acc += re_iny(tm.ny, s, A);
+        }
+    }
+    return acc;
+}
+
+__global__ __launch_bounds__(256) void k_expect(ExpArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const TileGeom &g = a.g;
+    const int t = g.t;
+    const int T = 1 << t;
+    float2 *lds = reinterpret_cast<float2 *>(smem);
+    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
+    double *acc = reinterpret_cast<double *>(hi_off + (1 << g.h));  // [4][kTermChunk]
+
+    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
+    const int b = a.rows[row];
+    const float2 *st = a.state + (int64_t)b * a.row_stride;
+    const TermDev *terms = a.terms + a.row_term_begin[row];
+    const int nterm = a.row_term_count[row];
+    build_hi_off(g, hi_off);
+    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+
+    for (int c0 = 0; c0 < nterm; c0 += kTermChunk) {
+        const int cn = min(kTermChunk, nterm - c0);
+        for (int j = threadIdx.x; j < 4 * kTermChunk; j += blockDim.x) acc[j] = 0;
+        __syncthreads();
+        const int64_t ntiles = (int64_t)1 << a.tiles_log2;
+        for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
+            const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
+            tile_copy<true>(tc, lds, const_cast<float2 *>(st), fb, T);
+            __syncthreads();
+            for (int k = 0; k < cn; k++) {
+                double v = wave_sum(term_tile_sum(terms[c0 + k], tc, lds, st, fb, t));
+                if (lane == 0) acc[wave * kTermChunk + k] += v;
+            }
+            __syncthreads();
+        }
+        double *out = a.partial + ((int64_t)row * a.wg_per_row + w) * a.tmax + c0;
+        for (int k = threadIdx.x; k < cn; k += blockDim.x)
+            out[k] = ((acc[k] + acc[kTermChunk + k]) + acc[2 * kTermChunk + k]) + acc[3 * kTermChunk + k];
+        __syncthreads();
+    }
+}
+
+// out[b, k] = sum over the row's terms of observable k: coeff * sum_w partial
+__global__ void k_expect_reduce(ExpReduceArgs a)
+{
+    const int row = blockIdx.x;
+    const int b = a.rows[row];
+    const TermDev *terms = a.terms + a.row_term_begin[row];
+    const int nterm = a.row_term_count[row];
+    const double *p = a.partial + (int64_t)row * a.wg_per_row * a.tmax;
+    for (int k = threadIdx.x; k < a.K; k += blockDim.x) {
+        double sum = 0;
+        for (int ti = 0; ti < nterm; ti++) {
+            if (terms[ti].k != k) continue;
+            double s = 0;
+            for (int w = 0; w < a.wg_per_row; w++) s += p[(int64_t)w * a.tmax + ti];
+            sum += terms[ti].coeff * s;
+        }
+        a.out[(int64_t)b * a.K + k] = (float)sum;
+    }
+}
+
+// --------------------------------------------------- phi = H_g psi
+// (P psi)[i] = i^{ny} (-1)^{|(i ^ x) & z|} psi[i ^ x]; the coefficient of term
+// t of observable k is upstream[b, k] * coeff_t.
+__global__ __launch_bounds__(256) void k_apply_h(HArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const TileGeom &g = a.g;
+    const int t = g.t;
+    const int T = 1 << t;
+    float2 *lds = reinterpret_cast<float2 *>(smem);
+    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
+    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
+    const int b = a.rows[row];
+    const float2 *ps = a.psi + (int64_t)b * a.row_stride;
+    float2 *ph = a.phi + (int64_t)b * a.row_stride;
+    const TermDev *terms = a.terms + a.row_term_begin[row];
+    const int nterm = a.row_term_count[row];
+    const float *up = a.upstream + (int64_t)a.brows[row] * a.K;
+    build_hi_off(g, hi_off);
+    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    __syncthreads();  // hi_off is read by every thread below
+    const int64_t ntiles = (int64_t)1 << a.tiles_log2;
+    for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
+        const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
+        tile_copy<true>(tc, lds, const_cast<float2 *>(ps), fb, T);
+        __syncthreads();
+        for (int l = threadIdx.x; l < T; l += blockDim.x) {
+            double ax = 0, ay = 0;
+            for (int k = 0; k < nterm; k++) {
+                const TermDev tm = terms[k];
+                const uint32_t lj = l ^ tm.xl;
+                const uint64_t fj = fb ^ tm.xout;
+                float2 v = tm.xout == 0 ? lds[lj] : ps[tile_index(tc, fj, lj)];
+                double cf = tm.coeff * (double)up[tm.k];
+                if (par64(fj & tm.z) ^ par32(lj & tm.zl)) cf = -cf;
+                double vx = v.x, vy = v.y;
+                switch (tm.ny & 3) {
+                case 0: ax += cf * vx; ay += cf * vy; break;
+                case 1: ax -= cf * vy; ay += cf * vx; break;
+                case 2: ax -= cf * vx; ay -= cf * vy; break;
+                default: ax += cf * vy; ay -= cf * vx; break;
+                }
+            }
+            ph[tile_index(tc, fb, l)] = make_float2((float)ax, (float)ay);
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------ reverse pass
+// psi and phi tiles side by side in LDS.  For each op (a reversed gate W):
+// psi <- W^dagger psi; for every symbolic parameter accumulate
+// Re <phi| dW/deta |psi>; phi <- W^dagger phi.
+__global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const TileGeom &g = a.g;
+    const int t = g.t;
+    const uint32_t T = 1u << t;
+    float2 *lp = reinterpret_cast<float2 *>(smem);
+    float2 *lf = lp + T;
+    uint64_t *hi_off = reinterpret_cast<uint64_t *>(lf + T);
+    double *acc = reinterpret_cast<double *>(hi_off + (1 << g.h));  // [4][gcount]
+
+    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
+    const int b = a.rows[row];
+    float2 *sp = a.psi + (int64_t)b * a.row_stride;
+    float2 *sf = a.phi + (int64_t)b * a.row_stride;
+    const float2 *M = a.mats + (int64_t)row * a.mat_stride;
+    build_hi_off(g, hi_off);
+    for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) acc[j] = 0;
+    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int wave = tid / 64, lane = tid % 64;
+    __syncthreads();
+
+    const int64_t ntiles = (int64_t)1 << a.tiles_log2;
+    for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
+        const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
+        tile_copy<true>(tc, lp, sp, fb, T);
+        tile_copy<true>(tc, lf, sf, fb, T);
+        __syncthreads();
+        for (int oi = 0; oi < a.nops; oi++) {
+            const PassOp op = a.ops[oi];
+            const float2 *m = M + op.mat;
+            double g0 = 0, g1 = 0;
+            if (op.kind == K_M1) {
+                const float2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+                float2 d0[4] = {}, d1[4] = {};
+                for (int i = 0; i < 4 && op.ngrad > 0; i++) d0[i] = M[op.dmat[0] + i];
+                for (int i = 0; i < 4 && op.ngrad > 1; i++) d1[i] = M[op.dmat[1] + i];
+                const int tb = op.l0;
+                bool active = true;
+                uint32_t count = T / 2;
+                int lo = tb, hi = tb, cb = -1;
+                uint32_t cv = 0;
+                if (op.ctrl) {
+                    if (op.l1 == kFixed) {
+                        active = (int)((fb >> op.p1) & 1) == op.cval;
+                    } else {
+                        cb = op.l1;
+                        lo = min(tb, cb);
+                        hi = max(tb, cb);
+                        cv = (uint32_t)op.cval << cb;
+                        count = T / 4;
+                    }
+                }
+                if (active) {
+                    for (uint32_t p = tid; p < count; p += nt) {
+                        uint32_t i = cb >= 0 ? (ins0(ins0(p, lo), hi) | cv) : ins0(p, tb);
+                        uint32_t j = i | (1u << tb);
+                        float2 a0 = lp[i], a1 = lp[j];
+                        float2 b0 = cmul2(m00, a0, m01, a1), b1 = cmul2(m10, a0, m11, a1);
+                        lp[i] = b0;
+                        lp[j] = b1;
+                        float2 f0 = lf[i], f1 = lf[j];
+                        if (op.ngrad > 0) {
+                            float2 e0 = cmul2(d0[0], b0, d0[1], b1), e1 = cmul2(d0[2], b0, d0[3], b1);
+                            g0 += (double)(f0.x * e0.x + f0.y * e0.y) + (double)(f1.x * e1.x + f1.y * e1.y);
+                        }
+                        if (op.ngrad > 1) {
+                            float2 e0 = cmul2(d1[0], b0, d1[1], b1), e1 = cmul2(d1[2], b0, d1[3], b1);
+                            g1 += (double)(f0.x * e0.x + f0.y * e0.y) + (double)(f1.x * e1.x + f1.y * e1.y);
+                        }
+                        lf[i] = cmul2(m00, f0, m01, f1);
+                        lf[j] = cmul2(m10, f0, m11, f1);
+                    }
+                }
+            } else if (op.kind == K_M2) {
+                float2 mm[16];
+                for (int i = 0; i < 16; i++) mm[i] = m[i];
+                const int b0 = op.l0, b1 = op.l1;
+                const int lo = min(b0, b1), hi = max(b0, b1);
+                for (uint32_t p = tid; p < T / 4; p += nt) {
+                    uint32_t ix[4];
+                    ix[0] = ins0(ins0(p, lo), hi);
+                    ix[1] = ix[0] | (1u << b1);
+                    ix[2] = ix[0] | (1u << b0);
+                    ix[3] = ix[1] | (1u << b0);
+                    float2 v[4], u[4], f[4];
+                    for (int r = 0; r < 4; r++) v[r] = lp[ix[r]];
+                    for (int r = 0; r < 4; r++)
+                        u[r] = cadd(cmul2(mm[4 * r], v[0], mm[4 * r + 1], v[1]),
+                                    cmul2(mm[4 * r + 2], v[2], mm[4 * r + 3], v[3]));
+                    for (int r = 0; r < 4; r++) lp[ix[r]] = u[r];
+                    for (int r = 0; r < 4; r++) f[r] = lf[ix[r]];
+                    for (int gq = 0; gq < op.ngrad; gq++) {
+                        const float2 *dm = M + op.dmat[gq];
+                        double s = 0;
+                        for (int r = 0; r < 4; r++) {
+                            float2 e = cadd(cmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
+                                            cmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3]));
+                            s += (double)(f[r].x * e.x + f[r].y * e.y);
+                        }
+                        if (gq == 0) g0 += s;
+                        else g1 += s;
+                    }
+                    for (int r = 0; r < 4; r++)
+                        lf[ix[r]] = cadd(cmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]),
+                                         cmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3]));
+                }
+            } else {
+                const bool two = op.kind == K_D2;
+                float2 d[4], dd0[4] = {}, dd1[4] = {};
+                for (int i = 0; i < (two ? 4 : 2); i++) {
+                    d[i] = m[i];
+                    if (op.ngrad > 0) dd0[i] = M[op.dmat[0] + i];
+                    if (op.ngrad > 1) dd1[i] = M[op.dmat[1] + i];
+                }
+                for (uint32_t l = tid; l < T; l += nt) {
+                    int idx = bit_of(op.l0, op.p0, l, fb);
+                    if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
+                    float2 u = cmul(d[idx], lp[l]);
+                    lp[l] = u;
+                    float2 f = lf[l];
+                    if (op.ngrad > 0) {
+                        float2 e = cmul(dd0[idx], u);
+                        g0 += (double)(f.x * e.x + f.y * e.y);
+                    }
+                    if (op.ngrad > 1) {
+                        float2 e = cmul(dd1[idx], u);
+                        g1 += (double)(f.x * e.x + f.y * e.y);
+                    }
+                    lf[l] = cmul(d[idx], f);
+                }
+            }
+            if (op.ngrad > 0) {
+                double v = wave_sum(g0);
+                if (lane == 0) acc[wave * a.gcount + (op.gslot[0] - a.gbase)] += v;
+            }
+            if (op.ngrad > 1) {
+                double v = wave_sum(g1);
+                if (lane == 0) acc[wave * a.gcount + (op.gslot[1] - a.gbase)] += v;
+            }
+            __syncthreads();
+        }
+        if (a.store) {
+            tile_copy<false>(tc, lp, sp, fb, T);
+            tile_copy<false>(tc, lf, sf, fb, T);
+        }
+        __syncthreads();
+    }
+    double *out = a.gpart + ((int64_t)row * a.wg_per_row + w) * a.n_gslots + a.gbase;
+    for (int j = tid; j < a.gcount; j += nt)
+        out[j] = ((acc[j] + acc[a.gcount + j]) + acc[2 * a.gcount + j]) + acc[3 * a.gcount + j];
+}
+
+// grad[b, s] = sum over gradient slots of s: 2 * scale * sum_w gpart
+__global__ void k_grad_reduce(GradReduceArgs a)
+{
+    const int row = blockIdx.x;
+    const int b = a.rows[row];
+    const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots);
+    const double *p = a.gpart + (int64_t)row * a.wg_per_row * a.n_gslots;
+    for (int s = threadIdx.x; s < a.S; s += blockDim.x) {
+        double sum = 0;
+        for (int k = a.sym_begin[s]; k < a.sym_begin[s + 1]; k++) {
+            int gs = a.sym_gslots[k];
+            double v = 0;
+            for (int w = 0; w < a.wg_per_row; w++) v += p[(int64_t)w * a.n_gslots + gs];
+            sum += 2.0 * scale[a.gslot_slot[gs]] * v;
+        }
+        a.grad[(int64_t)b * a.S + s] = (float)sum;
+    }
+}
+
+// ------------------------------------------------------------- sampling
+__device__ __forceinline__ uint64_t weight_of(float2 v)
+{
+    double re = v.x, im = v.y;
+    double p = re * re + im * im;
+    return (uint64_t)(p * 0x1p62);
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
+{
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// level 1: sum of the weights of each group of 64 amplitudes
+__global__ __launch_bounds__(256) void k_samp_l1(SampArgs a)
+{
+    const int row = blockIdx.y;
+    const int sr = a.rows ? a.rows[row] : row;
+    const int64_t grp = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (grp >= a.count[1]) return;
+    const int64_t i = grp * 64 + lane;
+    const float2 *st = a.state + (int64_t)sr * a.row_stride;
+    uint64_t wv = i < a.count[0] ? weight_of(st[i]) : 0;
+    wv = wave_sum_u64(wv);
+    if (lane == 0) a.levels[(int64_t)row * a.row_level + a.off[1] + grp] = wv;
+}
+
+// level k+1 from level k
+__global__ __launch_bounds__(256) void k_samp_up(SampArgs a, int k)
+{
+    const int row = blockIdx.y;
+    const int64_t grp = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (grp >= a.count[k + 1]) return;
+    const int64_t i = grp * 64 + lane;
+    const uint64_t *lv = a.levels + (int64_t)row * a.row_level;
+    uint64_t wv = i < a.count[k] ? lv[a.off[k] + i] : 0;
+    wv = wave_sum_u64(wv);
+    if (lane == 0) a.levels[(int64_t)row * a.row_level + a.off[k + 1] + grp] = wv;
+}
+
+// SplitMix64 (Steele, Lea, Flood 2014): output number `counter` of the stream
+// whose state starts at `seed`
+__device__ __forceinline__ uint64_t splitmix64(uint64_t seed, uint64_t counter)
+{
+    uint64_t z = seed + (counter + 1) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// one wavefront per shot: descend the levels, at each one locating the child
+// whose cumulative interval contains r by a wavefront prefix scan
+__global__ __launch_bounds__(256) void k_samp_shots(SampArgs a)
+{
+    const int row = blockIdx.y;
+    const int sr = a.rows ? a.rows[row] : row;
+    const int b = a.brows ? a.brows[row] : row;
+    const int64_t shot = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (shot >= a.n_shots) return;
+    const uint64_t *lv = a.levels + (int64_t)row * a.row_level;
+    const float2 *st = a.state + (int64_t)sr * a.row_stride;
+    const int top = a.nlev;
+    auto level_value = [&](int k, int64_t i) -> uint64_t {
+        if (i >= a.count[k]) return 0;
+        return k == 0 ? weight_of(st[i]) : lv[a.off[k] + i];
+    };
+    // total weight from the top level (at most 64 entries)
+    const uint64_t tv = level_value(top, lane);
+    const uint64_t W = wave_sum_u64(tv);
+    uint64_t *out = a.out + (int64_t)b * a.n_shots + shot;
+    if (W == 0) {
+        if (lane == 0) *out = 0;
+        return;
+    }
+    const uint64_t u = splitmix64(a.seed, (uint64_t)b * (uint64_t)a.n_shots + (uint64_t)shot);
+    uint64_t r = __umul64hi(u, W);
+    int64_t base = 0;  // index of the chosen entry at the current level
+    for (int k = top; k >= 0; k--) {
+        const uint64_t v = k == top ? tv : level_value(k, base * 64 + lane);
+        uint64_t incl = v;
+        for (int d = 1; d < 64; d <<= 1) {
+            uint64_t o = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += o;
+        }
+        const uint64_t hit = __ballot(incl > r);
+        // the children of the chosen entry sum to its value (> r), so some lane
+        // hits; the clamp only keeps indexing in range
+        const int sel = hit ? __ffsll((unsigned long long)hit) - 1 : 63;
+        const uint64_t before = __shfl(incl - v, sel, 64);
+        r -= before;
+        base = base * 64 + sel;
+    }
+    if (lane == 0) *out = (uint64_t)base;
+}
+
+// ------------------------------------------------------- gather, padding
+__global__ void k_gather(GatherArgs a)
+{
+    const int row = blockIdx.y;
+    const int b = a.brows[row];
+    const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (m >= a.M) return;
+    const uint64_t x = a.bits[(int64_t)b * a.M + m];
+    float2 v = make_float2(0.f, 0.f);
+    if ((x >> a.n) == 0) v = a.state[(int64_t)a.rows[row] * a.row_stride + (int64_t)x];
+    a.out[(int64_t)b * a.M + m] = v;
+}
+
+__global__ void k_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int64_t from, int64_t to)
+{
+    const int row = blockIdx.y;
+    const int64_t i = from + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < to) state[(int64_t)rows[row] * row_stride + i] = make_float2(0.f, 0.f);
+}
+
+// ------------------------------------------------------- launch wrappers
+namespace {
+template <class K> hipError_t set_lds(K kernel, size_t bytes)
+{
+    if (bytes <= 65536) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+} // namespace
+
+hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s)
+{
+    int n = a.task_end - a.task_begin;
+    if (n <= 0 || nrows <= 0) return hipSuccess;
+    dim3 grid((n + 255) / 256, nrows);
+    hipLaunchKernelGGL(k_build_mats, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+size_t pass_lds_bytes(const TileGeom &g, bool product_init)
+{
+    size_t b = sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h);
+    if (product_init) b += sizeof(float2) * (((size_t)1 << (g.t / 2)) + ((size_t)1 << (g.t - g.t / 2)));
+    return b;
+}
+
+hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s)
+{
+    size_t lds = pass_lds_bytes(a.g, a.product_init != 0);
+    hipError_t e = set_lds(k_pass, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_pass, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s)
+{
+    size_t lds = sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
+                 sizeof(double) * 4 * kTermChunk;
+    hipError_t e = set_lds(k_expect, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_expect, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_expect_reduce(const ExpReduceArgs &a, int nrows, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_expect_reduce, dim3(nrows), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s)
+{
+    size_t lds = sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h);
+    hipError_t e = set_lds(k_apply_h, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_apply_h, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s)
+{
+    size_t lds = 2 * sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
+                 sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
+    hipError_t e = set_lds(k_rev_pass, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_rev_pass, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_grad_reduce, dim3(nrows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s)
+{
+    if (nrows <= 0) return hipSuccess;
+    if (a.nlev >= 1) {
+        hipLaunchKernelGGL(k_samp_l1, dim3((unsigned)((a.count[1] + 3) / 4), nrows), dim3(256), 0, s, a);
+        for (int k = 1; k < a.nlev; k++)
+            hipLaunchKernelGGL(k_samp_up, dim3((unsigned)((a.count[k + 1] + 3) / 4), nrows), dim3(256), 0, s, a, k);
+    }
+    if (a.n_shots > 0)
+        hipLaunchKernelGGL(k_samp_shots, dim3((unsigned)((a.n_shots + 3) / 4), nrows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s)
+{
+    if (a.M <= 0 || nrows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_gather, dim3((unsigned)((a.M + 255) / 256), nrows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int nrows, int64_t from, int64_t to,
+                            hipStream_t s)
+{
+    if (to <= from || nrows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_zero_tail, dim3((unsigned)((to - from + 255) / 256), nrows), dim3(256), 0, s, state,
+                       row_stride, rows, from, to);
+    return hipGetLastError();
+}
+
+} // namespace tq

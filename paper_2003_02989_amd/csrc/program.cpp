@@ -1,0 +1,628 @@
+// program.cpp -- parsing, validation, structure dedupe and pass planning.
+//
+// Planning follows the idea behind the paper's gate fusion (Sec. "Gate Fusion
+// with qsim"): every application of a gate costs a sweep over all 2^n
+// amplitudes, so as many gates as possible are applied per sweep.  Here a
+// sweep is a "tile pass": each workgroup stages a tile of 2^t amplitudes in
+// LDS (t index bits: the lowest `low` bits, for coalesced HBM runs, plus
+// chosen high bits), applies every gate of the pass whose non-diagonal qubits
+// lie in the tile -- diagonal gates and control qubits may sit outside, their
+// bit is then constant over the tile -- and writes the tile back.  Inside a
+// pass, neighbouring gates on the same qubit set are pre-multiplied into one
+// matrix on the device.
+#include "program.h"
+
+#include <algorithm>
+#include <cstring>
+#include <map>
+
+#include "../../include/tq.h"
+
+namespace tq {
+
+namespace {
+
+struct Reader {
+    const uint8_t *p, *end;
+    bool bad = false;
+    template <class T> T get()
+    {
+        T v{};
+        if (end - p < (long)sizeof(T)) {
+            bad = true;
+            return v;
+        }
+        std::memcpy(&v, p, sizeof(T));
+        p += sizeof(T);
+        return v;
+    }
+};
+
+[[noreturn]] void fail(int status, const std::string &m) { throw Error{status, m}; }
+
+bool op_shape(int op, int &nq, int &np)
+{
+    switch (op) {
+    case OP_H: case OP_X: case OP_Y: case OP_Z: case OP_SQRTX: case OP_SQRTY: case OP_SQRTW: case OP_MATRIX1:
+        nq = 1; np = 0; return true;
+    case OP_RX: case OP_RY: case OP_RZ: case OP_XPOW: case OP_YPOW: case OP_ZPOW:
+        nq = 1; np = 1; return true;
+    case OP_CZ: case OP_CNOT: case OP_MATRIX2: case OP_SWAP:
+        nq = 2; np = 0; return true;
+    case OP_CZPOW: case OP_CNOTPOW: case OP_XXPOW: case OP_YYPOW: case OP_ZZPOW: case OP_RZZ:
+        nq = 2; np = 1; return true;
+    case OP_FSIM:
+        nq = 2; np = 2; return true;
+    default:
+        return false;
+    }
+}
+
+// Gate classes as the tile passes see them.
+enum Cls { C_1D, C_1M, C_CTRL, C_2D, C_2M };
+
+int classify(int op)
+{
+    switch (op) {
+    case OP_Z: case OP_RZ: case OP_ZPOW:
+        return C_1D;
+    case OP_CNOT: case OP_CNOTPOW:
+        return C_CTRL;
+    case OP_CZ: case OP_CZPOW: case OP_ZZPOW: case OP_RZZ:
+        return C_2D;
+    case OP_XXPOW: case OP_YYPOW: case OP_FSIM: case OP_MATRIX2: case OP_SWAP:
+        return C_2M;
+    default:
+        return C_1M;
+    }
+}
+
+// Qubits whose bit must be local to the tile (the non-diagonal ones).
+int targets(const Group &g, int gi, int *out)
+{
+    int cls = classify(g.gates[gi].op);
+    switch (cls) {
+    case C_1D: case C_2D: return 0;
+    case C_1M: out[0] = g.gate_q0[gi]; return 1;
+    case C_CTRL: out[0] = g.gate_q1[gi]; return 1;
+    default: out[0] = g.gate_q0[gi]; out[1] = g.gate_q1[gi]; return 2;
+    }
+}
+
+int qubits_of(const Group &g, int gi, int *out)
+{
+    out[0] = g.gate_q0[gi];
+    if (g.gates[gi].nq == 2) {
+        out[1] = g.gate_q1[gi];
+        return 2;
+    }
+    return 1;
+}
+
+struct Sched {
+    std::vector<int> bits;   // tile bit positions
+    std::vector<int> items;  // gate indices in application order
+};
+
+// Greedy pass scheduling.  A gate joins the current pass when none of its
+// qubits is blocked by an earlier deferred gate and its target bits fit in
+// the tile (choosing new tile bits while there is room); otherwise it is
+// deferred and blocks its qubits.  The free tile bits are then filled with
+// the targets of the earliest deferred gates and the scan is repeated with
+// the tile fixed, so that the pass takes every gate that became possible.
+std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n, int t, int c)
+{
+    std::vector<Sched> out;
+    if (n <= t) {
+        Sched s;
+        for (int b = 0; b < n; b++) s.bits.push_back(b);
+        s.items = items;
+        out.push_back(s);
+        return out;
+    }
+    auto pos = [n](int q) { return n - 1 - q; };
+    std::vector<int> remaining = items;
+    while (!remaining.empty()) {
+        std::vector<char> in_tile(n, 0);
+        int used = 0;
+        for (int b = 0; b < c; b++) in_tile[b] = 1, used++;
+        // phase 1: choose bits greedily in gate order
+        {
+            std::vector<char> blocked(n, 0);
+            for (int gi : remaining) {
+                int qs[2], ts[2];
+                int nq = qubits_of(g, gi, qs), nt = targets(g, gi, ts);
+                bool blk = false;
+                for (int j = 0; j < nq; j++) blk |= blocked[qs[j]] != 0;
+                int need = 0;
+                for (int j = 0; j < nt; j++) need += !in_tile[pos(ts[j])];
+                if (!blk && used + need <= t) {
+                    for (int j = 0; j < nt; j++)
+                        if (!in_tile[pos(ts[j])]) in_tile[pos(ts[j])] = 1, used++;
+                } else {
+                    for (int j = 0; j < nq; j++) blocked[qs[j]] = 1;
+                }
+            }
+        }
+        // phase 2: fill free bits with targets of deferred gates, in order
+        if (used < t) {
+            for (int gi : remaining) {
+                int ts[2];
+                int nt = targets(g, gi, ts);
+                for (int j = 0; j < nt && used < t; j++)
+                    if (!in_tile[pos(ts[j])]) in_tile[pos(ts[j])] = 1, used++;
+                if (used == t) break;
+            }
+            for (int b = n - 1; b >= 0 && used < t; b--)
+                if (!in_tile[b]) in_tile[b] = 1, used++;
+        }
+        // phase 3: schedule with the tile fixed
+        Sched s;
+        for (int b = 0; b < n; b++)
+            if (in_tile[b]) s.bits.push_back(b);
+        std::vector<int> deferred;
+        std::vector<char> blocked(n, 0);
+        for (int gi : remaining) {
+            int qs[2], ts[2];
+            int nq = qubits_of(g, gi, qs), nt = targets(g, gi, ts);
+            bool ok = true;
+            for (int j = 0; j < nq; j++) ok &= !blocked[qs[j]];
+            for (int j = 0; j < nt; j++) ok &= in_tile[pos(ts[j])] != 0;
+            if (ok) {
+                s.items.push_back(gi);
+            } else {
+                deferred.push_back(gi);
+                for (int j = 0; j < nq; j++) blocked[qs[j]] = 1;
+            }
+        }
+        if (s.items.empty()) fail(TQ_E_UNSUPPORTED, "planner made no progress");
+        out.push_back(std::move(s));
+        remaining.swap(deferred);
+    }
+    return out;
+}
+
+TileGeom geom_from_bits(int n, int c, const std::vector<int> &bits)
+{
+    TileGeom gm{};
+    gm.n = n;
+    gm.t = (int)bits.size();
+    gm.c = std::min(c, n);
+    if (gm.t <= gm.c) gm.c = gm.t;
+    gm.h = gm.t - gm.c;
+    uint64_t tile_mask = 0;
+    for (int b : bits) tile_mask |= 1ull << b;
+    for (int b = 0; b < gm.c; b++)
+        if (!((tile_mask >> b) & 1)) fail(TQ_E_UNSUPPORTED, "tile lacks a low bit");
+    int k = 0;
+    for (int b : bits)
+        if (b >= gm.c) gm.hb[k++] = (uint8_t)b;
+    uint64_t all = n >= 64 ? ~0ull : ((1ull << n) - 1);
+    gm.fixed_mask = all & ~tile_mask;
+    return gm;
+}
+
+uint8_t local_of(const TileGeom &gm, int pos)
+{
+    if (pos < gm.c) return (uint8_t)pos;
+    for (int k = 0; k < gm.h; k++)
+        if (gm.hb[k] == pos) return (uint8_t)(gm.c + k);
+    return kFixed;
+}
+
+struct Planner {
+    Group &g;
+    int32_t alloc(int entries)
+    {
+        int32_t o = g.mat_block;
+        g.mat_block += entries;
+        return o;
+    }
+    int add_task(uint8_t kind, int dim, bool diag, int which, const std::vector<Member> &mem)
+    {
+        BuildTask bt{};
+        bt.kind = kind;
+        bt.dim = (uint8_t)dim;
+        bt.diag = diag;
+        bt.which = (uint8_t)which;
+        bt.out = alloc(diag ? dim : dim * dim);
+        bt.mem_begin = (int32_t)g.members.size();
+        bt.mem_count = (int32_t)mem.size();
+        for (const auto &m : mem) g.members.push_back(m);
+        g.tasks.push_back(bt);
+        return (int)g.tasks.size() - 1;
+    }
+};
+
+PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
+{
+    PassOp op{};
+    int cls = classify(g.gates[gi].op);
+    int q0 = g.gate_q0[gi], q1 = g.gate_q1[gi];
+    auto pos = [n](int q) { return n - 1 - q; };
+    switch (cls) {
+    case C_1D: op.kind = K_D1; break;
+    case C_1M: op.kind = K_M1; break;
+    case C_CTRL: op.kind = K_M1; break;
+    case C_2D: op.kind = K_D2; break;
+    default: op.kind = K_M2; break;
+    }
+    if (cls == C_CTRL) {  // q0 field = target, q1 field = control
+        op.p0 = (uint8_t)pos(q1);
+        op.l0 = local_of(gm, op.p0);
+        op.p1 = (uint8_t)pos(q0);
+        op.l1 = local_of(gm, op.p1);
+        op.ctrl = 1;
+        op.cval = 1;
+    } else {
+        op.p0 = (uint8_t)pos(q0);
+        op.l0 = local_of(gm, op.p0);
+        if (g.gates[gi].nq == 2) {
+            op.p1 = (uint8_t)pos(q1);
+            op.l1 = local_of(gm, op.p1);
+        } else {
+            op.p1 = 0;
+            op.l1 = kFixed;
+        }
+    }
+    return op;
+}
+
+void plan_group(Group &g, const Options &opt, int S)
+{
+    const int n = g.n;
+    Planner P{g};
+    const int G = (int)g.gates.size();
+
+    // Product-state initialisation: the single-qubit gates a qubit sees
+    // before its first two-qubit gate act on |0> alone, so the first pass
+    // generates the product state instead of reading |0...0> and applying
+    // them.
+    std::vector<std::vector<int>> absorbed(n);
+    std::vector<char> entangled(n, 0), is_absorbed(G, 0);
+    for (int gi = 0; gi < G; gi++) {
+        if (g.gates[gi].nq == 1 && !entangled[g.gate_q0[gi]]) {
+            absorbed[g.gate_q0[gi]].push_back(gi);
+            is_absorbed[gi] = 1;
+        } else if (g.gates[gi].nq == 2) {
+            entangled[g.gate_q0[gi]] = entangled[g.gate_q1[gi]] = 1;
+        }
+    }
+    g.fwd_tasks.begin = (int)g.tasks.size();
+    for (int q = 0; q < kMaxQubits; q++) g.init_mat[q] = -1;
+    for (int q = 0; q < n; q++) {
+        std::vector<Member> mem;
+        for (int gi : absorbed[q]) mem.push_back(Member{gi, 0, FORM_FULL, {0, 0}});
+        int ti = P.add_task(BT_PRODUCT, 2, false, 0, mem);
+        g.init_mat[q] = g.tasks[ti].out;
+    }
+
+    // forward passes
+    std::vector<int> fitems;
+    for (int gi = 0; gi < G; gi++)
+        if (!is_absorbed[gi]) fitems.push_back(gi);
+    auto fs = schedule(g, fitems, n, opt.tile, opt.low);
+    if (fs.empty()) {  // nothing beyond the product state: one generating pass
+        Sched s;
+        for (int b = 0; b < std::min(n, opt.tile); b++) s.bits.push_back(b);
+        if (n > opt.tile)
+            for (int b = opt.low; (int)s.bits.size() < opt.tile; b++)
+                if (std::find(s.bits.begin(), s.bits.end(), b) == s.bits.end()) s.bits.push_back(b);
+        std::sort(s.bits.begin(), s.bits.end());
+        fs.push_back(s);
+    }
+    for (size_t pi = 0; pi < fs.size(); pi++) {
+        Pass ps;
+        ps.geom = geom_from_bits(n, opt.low, fs[pi].bits);
+        ps.product_init = pi == 0;
+        struct OpB {
+            PassOp op;
+            std::vector<Member> mem;
+            int qa, qb;  // qubit set; qb = -1 for one qubit, -2 for a controlled op
+        };
+        std::vector<OpB> ops;
+        std::vector<int> last(n, -1);  // last op touching each qubit
+        for (int gi : fs[pi].items) {
+            int cls = classify(g.gates[gi].op);
+            int q0 = g.gate_q0[gi], q1 = g.gate_q1[gi];
+            if (opt.fuse && (cls == C_1D || cls == C_1M)) {
+                int o = last[q0];
+                if (o >= 0 && ops[o].qb == -1 && ops[o].qa == q0) {
+                    ops[o].mem.push_back(Member{gi, 0, FORM_FULL, {0, 0}});
+                    if (cls == C_1M) ops[o].op.kind = K_M1;
+                    continue;
+                }
+            }
+            if (opt.fuse && (cls == C_2D || cls == C_2M)) {
+                int o = last[q0];
+                if (o >= 0 && last[q1] == o && ops[o].qb >= 0 &&
+                    ((ops[o].qa == q0 && ops[o].qb == q1) || (ops[o].qa == q1 && ops[o].qb == q0))) {
+                    ops[o].mem.push_back(Member{gi, (uint8_t)(ops[o].qa != q0), FORM_FULL, {0, 0}});
+                    if (cls == C_2M) ops[o].op.kind = K_M2;
+                    continue;
+                }
+            }
+            OpB ob;
+            ob.op = base_op(g, ps.geom, gi, n);
+            ob.mem.push_back(Member{gi, 0, (uint8_t)(cls == C_CTRL ? FORM_CBLOCK : FORM_FULL), {0, 0}});
+            ob.qa = cls == C_CTRL ? q1 : q0;
+            ob.qb = cls == C_CTRL ? -2 : (g.gates[gi].nq == 2 ? q1 : -1);
+            int oi = (int)ops.size();
+            ops.push_back(std::move(ob));
+            last[q0] = oi;
+            if (g.gates[gi].nq == 2) last[q1] = oi;
+        }
+        for (auto &ob : ops) {
+            bool diag = ob.op.kind == K_D1 || ob.op.kind == K_D2;
+            int dim = (ob.op.kind == K_M2 || ob.op.kind == K_D2) ? 4 : 2;
+            int ti = P.add_task(BT_PRODUCT, dim, diag, 0, ob.mem);
+            ob.op.mat = g.tasks[ti].out;
+            ps.ops.push_back(ob.op);
+        }
+        g.fwd.push_back(std::move(ps));
+    }
+    g.fwd_tasks.end = (int)g.tasks.size();
+
+    // reverse passes: every gate, last first, W^dagger and dW/deta per op;
+    // two states share the LDS, so the tile is one bit smaller at most 12
+    g.rev_tasks.begin = (int)g.tasks.size();
+    std::vector<int> ritems;
+    for (int gi = G - 1; gi >= 0; gi--) ritems.push_back(gi);
+    int trev = std::min(opt.tile, 12);
+    auto rs0 = schedule(g, ritems, n, trev, std::min(opt.low, trev - 2));
+    // the reverse kernel keeps per-wave accumulators of every gradient slot of
+    // a pass in LDS: split passes that would hold too many
+    std::vector<Sched> rs;
+    for (auto &s0 : rs0) {
+        Sched cur;
+        cur.bits = s0.bits;
+        int ng = 0;
+        for (int gi : s0.items) {
+            int k = 0;
+            for (int j = 0; j < g.gates[gi].np; j++) k += g.slot_sym[g.gates[gi].slot0 + j] >= 0;
+            if (ng + k > kMaxGradPerPass && !cur.items.empty()) {
+                rs.push_back(cur);
+                cur.items.clear();
+                ng = 0;
+            }
+            cur.items.push_back(gi);
+            ng += k;
+        }
+        if (!cur.items.empty() || rs.empty()) rs.push_back(cur);
+    }
+    for (auto &s : rs) {
+        Pass ps;
+        ps.geom = geom_from_bits(n, std::min(opt.low, trev - 2), s.bits);
+        for (int gi : s.items) {
+            int cls = classify(g.gates[gi].op);
+            PassOp op = base_op(g, ps.geom, gi, n);
+            bool diag = op.kind == K_D1 || op.kind == K_D2;
+            int dim = (op.kind == K_M2 || op.kind == K_D2) ? 4 : 2;
+            Member m{gi, 0, (uint8_t)(cls == C_CTRL ? FORM_CBLOCK : FORM_FULL), {0, 0}};
+            int ti = P.add_task(BT_DAGGER, dim, diag, 0, {m});
+            op.mat = g.tasks[ti].out;
+            op.ngrad = 0;
+            for (int j = 0; j < g.gates[gi].np; j++) {
+                int slot = g.gates[gi].slot0 + j;
+                if (g.slot_sym[slot] < 0) continue;
+                int di = P.add_task(BT_DERIV, dim, diag, j, {m});
+                op.dmat[op.ngrad] = g.tasks[di].out;
+                op.gslot[op.ngrad] = g.n_gslots++;
+                g.gslot_slot.push_back(slot);
+                op.ngrad++;
+            }
+            ps.ops.push_back(op);
+        }
+        g.rev.push_back(std::move(ps));
+    }
+    g.rev_tasks.end = (int)g.tasks.size();
+
+    // every dense op must find its target bits in the tile
+    for (const std::vector<Pass> *pv : {&g.fwd, &g.rev})
+        for (const Pass &ps : *pv)
+            for (const PassOp &op : ps.ops) {
+                bool ok = true;
+                if (op.kind == K_M1) ok = op.l0 < ps.geom.t && (!op.ctrl || op.l1 == kFixed || op.l1 < ps.geom.t);
+                if (op.kind == K_M2) ok = op.l0 < ps.geom.t && op.l1 < ps.geom.t && op.l0 != op.l1;
+                if (op.kind == K_D1 || op.kind == K_D2) ok = op.p0 < n && (op.kind == K_D1 || op.p1 < n);
+                if (!ok) fail(TQ_E_UNSUPPORTED, "internal planner error: op outside its tile");
+            }
+
+    // symbol -> gradient slots
+    g.sym_gslot_begin.assign(S + 1, 0);
+    for (int gs = 0; gs < g.n_gslots; gs++) g.sym_gslot_begin[g.slot_sym[g.gslot_slot[gs]] + 1]++;
+    for (int s = 0; s < S; s++) g.sym_gslot_begin[s + 1] += g.sym_gslot_begin[s];
+    g.sym_gslots.assign(g.n_gslots, 0);
+    std::vector<int> fill(g.sym_gslot_begin.begin(), g.sym_gslot_begin.end() - 1);
+    for (int gs = 0; gs < g.n_gslots; gs++) g.sym_gslots[fill[g.slot_sym[g.gslot_slot[gs]]]++] = gs;
+}
+
+} // namespace
+
+TileGeom expectation_geometry(int n, int t, int c, const std::vector<uint64_t> &xmasks)
+{
+    std::vector<int> bits;
+    if (n <= t) {
+        for (int b = 0; b < n; b++) bits.push_back(b);
+        return geom_from_bits(n, c, bits);
+    }
+    std::vector<int> count(n, 0);
+    for (uint64_t x : xmasks)
+        for (int b = 0; b < n; b++)
+            if ((x >> b) & 1) count[b]++;
+    for (int b = 0; b < c; b++) bits.push_back(b);
+    std::vector<int> rest;
+    for (int b = c; b < n; b++) rest.push_back(b);
+    std::stable_sort(rest.begin(), rest.end(), [&](int a, int b) { return count[a] > count[b]; });
+    for (int i = 0; (int)bits.size() < t; i++) bits.push_back(rest[i]);
+    std::sort(bits.begin(), bits.end());
+    return geom_from_bits(n, c, bits);
+}
+
+std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt)
+{
+    if (!blob) fail(TQ_E_INVALID, "program blob is NULL");
+    Reader r{(const uint8_t *)blob, (const uint8_t *)blob + nbytes};
+    if (nbytes < 16 || std::memcmp(blob, "TQP1", 4) != 0) fail(TQ_E_INVALID, "program blob: bad magic");
+    r.p += 4;
+    uint32_t ver = r.get<uint32_t>(), B = r.get<uint32_t>(), S = r.get<uint32_t>();
+    if (ver != 1) fail(TQ_E_INVALID, "program blob: unsupported version");
+    if (B > (1u << 24) || S > (1u << 24)) fail(TQ_E_INVALID, "program blob: batch or symbol count too large");
+    auto pd = std::make_unique<ProgramData>();
+    pd->B = (int)B;
+    pd->S = (int)S;
+    pd->opt = opt;
+    pd->circuits.resize(B);
+    for (uint32_t b = 0; b < B; b++) {
+        uint32_t n = r.get<uint32_t>(), ng = r.get<uint32_t>();
+        if (r.bad) fail(TQ_E_INVALID, "program blob: truncated circuit header");
+        if (n > (uint32_t)kMaxQubits)
+            fail(TQ_E_UNSUPPORTED, "circuit " + std::to_string(b) + " has more than 32 qubits");
+        if (ng > (1u << 24)) fail(TQ_E_INVALID, "program blob: gate count too large");
+        HCircuit &c = pd->circuits[b];
+        c.n = (int)n;
+        pd->nmax = std::max(pd->nmax, (int)n);
+        c.gates.resize(ng);
+        for (uint32_t i = 0; i < ng; i++) {
+            HGate &g = c.gates[i];
+            std::memset(&g, 0, sizeof g);
+            g.op = r.get<uint16_t>();
+            g.nq = r.get<uint8_t>();
+            g.np = r.get<uint8_t>();
+            if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+            int enq, enp;
+            if (!op_shape(g.op, enq, enp))
+                fail(TQ_E_UNSUPPORTED, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                           ": unknown opcode " + std::to_string(g.op));
+            if (enq != g.nq || enp != g.np)
+                fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                       ": qubit/parameter count does not match the opcode");
+            for (int j = 0; j < g.nq; j++) {
+                g.q[j] = r.get<uint32_t>();
+                if (!r.bad && g.q[j] >= n)
+                    fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                           ": qubit out of range");
+            }
+            if (g.nq == 2 && g.q[0] == g.q[1])
+                fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                       ": repeated qubit");
+            for (int j = 0; j < g.np; j++) {
+                g.sym[j] = r.get<int32_t>();
+                g.scale[j] = r.get<double>();
+                g.offset[j] = r.get<double>();
+                if (!r.bad && (g.sym[j] < -1 || g.sym[j] >= (int32_t)S))
+                    fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                           ": symbol column out of range");
+            }
+            int nm = g.op == OP_MATRIX1 ? 8 : g.op == OP_MATRIX2 ? 32 : 0;
+            for (int j = 0; j < nm; j++) g.mat[j] = r.get<double>();
+            if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+        }
+    }
+    if (r.p != r.end) fail(TQ_E_INVALID, "program blob: trailing bytes");
+
+    // structure dedupe: same qubit count, opcodes, qubits, symbol wiring and
+    // explicit matrices; scales and offsets may differ per row
+    std::map<std::string, int> key_to_group;
+    for (uint32_t b = 0; b < B; b++) {
+        const HCircuit &c = pd->circuits[b];
+        std::string key;
+        key.append((const char *)&c.n, sizeof c.n);
+        for (const HGate &g : c.gates) {
+            key.append((const char *)&g.op, 2);
+            key.append((const char *)g.q, 8);
+            key.append((const char *)g.sym, 8);
+            if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2) key.append((const char *)g.mat, sizeof g.mat);
+        }
+        auto it = key_to_group.find(key);
+        Group *grp;
+        if (it == key_to_group.end()) {
+            key_to_group[key] = (int)pd->groups.size();
+            pd->groups.push_back(std::make_unique<Group>());
+            grp = pd->groups.back().get();
+            grp->n = c.n;
+            for (const HGate &g : c.gates) {
+                GateDev gd{};
+                gd.op = g.op;
+                gd.nq = g.nq;
+                gd.np = g.np;
+                gd.slot0 = grp->n_slots;
+                gd.explicit_ = -1;
+                if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2) {
+                    gd.explicit_ = (int32_t)(grp->explicit_mats.size() / 32);
+                    grp->explicit_mats.insert(grp->explicit_mats.end(), g.mat, g.mat + 32);
+                }
+                for (int j = 0; j < g.np; j++) grp->slot_sym.push_back(g.sym[j]);
+                grp->n_slots += g.np;
+                grp->gates.push_back(gd);
+                grp->gate_q0.push_back((int32_t)g.q[0]);
+                grp->gate_q1.push_back(g.nq == 2 ? (int32_t)g.q[1] : -1);
+            }
+        } else {
+            grp = pd->groups[it->second].get();
+        }
+        grp->rows.push_back((int32_t)b);
+        for (const HGate &g : c.gates)
+            for (int j = 0; j < g.np; j++) {
+                grp->slot_scale.push_back(g.scale[j]);
+                grp->slot_off.push_back(g.offset[j]);
+            }
+    }
+    for (auto &gp : pd->groups) {
+        Group &g = *gp;
+        // rows that share every scale and offset keep one table row
+        bool uni = true;
+        size_t ns = (size_t)g.n_slots;
+        for (size_t r = 1; r < g.rows.size() && uni; r++)
+            uni = std::equal(g.slot_scale.begin(), g.slot_scale.begin() + ns, g.slot_scale.begin() + r * ns) &&
+                  std::equal(g.slot_off.begin(), g.slot_off.begin() + ns, g.slot_off.begin() + r * ns);
+        g.uniform_slots = uni;
+        if (uni) {
+            g.slot_scale.resize(ns);
+            g.slot_off.resize(ns);
+        }
+        plan_group(g, opt, (int)S);
+    }
+    return pd;
+}
+
+std::unique_ptr<ObsData> parse_observables(const void *blob, size_t nbytes)
+{
+    if (!blob) fail(TQ_E_INVALID, "observable blob is NULL");
+    Reader r{(const uint8_t *)blob, (const uint8_t *)blob + nbytes};
+    if (nbytes < 16 || std::memcmp(blob, "TQO1", 4) != 0) fail(TQ_E_INVALID, "observable blob: bad magic");
+    r.p += 4;
+    uint32_t ver = r.get<uint32_t>(), B = r.get<uint32_t>(), K = r.get<uint32_t>();
+    if (ver != 1) fail(TQ_E_INVALID, "observable blob: unsupported version");
+    if ((uint64_t)B * K > (1u << 26)) fail(TQ_E_INVALID, "observable blob: too many sums");
+    auto od = std::make_unique<ObsData>();
+    od->B = (int)B;
+    od->K = (int)K;
+    od->sums.resize((size_t)B * K);
+    for (auto &sum : od->sums) {
+        uint32_t T = r.get<uint32_t>();
+        if (r.bad || T > (1u << 24)) fail(TQ_E_INVALID, "observable blob: bad term count");
+        sum.resize(T);
+        for (auto &term : sum) {
+            term.coeff = r.get<double>();
+            uint32_t nf = r.get<uint32_t>();
+            if (r.bad || nf > (uint32_t)kMaxQubits) fail(TQ_E_INVALID, "observable blob: bad factor count");
+            uint64_t seen = 0;
+            for (uint32_t f = 0; f < nf; f++) {
+                uint32_t q = r.get<uint32_t>();
+                uint8_t p = r.get<uint8_t>();
+                if (r.bad) fail(TQ_E_INVALID, "observable blob: truncated term");
+                if (p < 1 || p > 3) fail(TQ_E_INVALID, "observable blob: Pauli code must be 1, 2 or 3");
+                if (q >= (uint32_t)kMaxQubits) fail(TQ_E_INVALID, "observable blob: qubit out of range");
+                if ((seen >> q) & 1) fail(TQ_E_INVALID, "observable blob: qubit repeated within a term");
+                seen |= 1ull << q;
+                term.factors.emplace_back(q, p);
+            }
+        }
+    }
+    if (r.bad) fail(TQ_E_INVALID, "observable blob: truncated");
+    if (r.p != r.end) fail(TQ_E_INVALID, "observable blob: trailing bytes");
+    return od;
+}
+
+} // namespace tq

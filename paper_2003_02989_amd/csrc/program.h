@@ -1,0 +1,100 @@
+// program.h -- host-side program representation: parsed circuits, structure
+// groups (circuits of the batch that share gates and symbol wiring) and the
+// pass plans the kernels execute.
+#pragma once
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "tq_internal.h"
+
+namespace tq {
+
+struct Error {
+    int status;
+    std::string msg;
+};
+
+struct Options {
+    int tile = 12;    // forward tile bits
+    int low = 6;      // contiguous low bits per tile
+    bool fuse = true;
+};
+
+struct HGate {
+    uint16_t op;
+    uint8_t nq, np;
+    uint32_t q[2];
+    int32_t sym[2];
+    double scale[2], offset[2];
+    double mat[32];
+};
+
+struct HCircuit {
+    int n = 0;
+    std::vector<HGate> gates;
+};
+
+struct Pass {
+    TileGeom geom;
+    std::vector<PassOp> ops;
+    bool product_init = false;
+};
+
+// Build-task ranges of a group: [begin, end) into Group::tasks.
+struct TaskRange {
+    int begin = 0, end = 0;
+};
+
+struct Group {
+    int n = 0;
+    std::vector<int32_t> rows;  // batch indices of the circuits in this group
+    std::vector<GateDev> gates;
+    std::vector<int32_t> gate_q0, gate_q1;
+    int n_slots = 0;
+    std::vector<int32_t> slot_sym;              // [n_slots]
+    std::vector<double> slot_scale, slot_off;   // [rows or 1][n_slots]
+    bool uniform_slots = true;
+    std::vector<double> explicit_mats;          // [n_explicit][32]
+
+    // plan
+    std::vector<BuildTask> tasks;
+    std::vector<Member> members;
+    TaskRange fwd_tasks, rev_tasks;
+    int32_t mat_block = 0;                      // complex entries per row
+    std::vector<Pass> fwd;
+    int32_t init_mat[kMaxQubits];               // per qubit: 2x2 product-init matrix
+    std::vector<Pass> rev;
+    int n_gslots = 0;
+    std::vector<int32_t> gslot_slot;            // gradient slot -> parameter slot
+    std::vector<int32_t> sym_gslot_begin;       // [S+1] CSR symbol -> gradient slots
+    std::vector<int32_t> sym_gslots;
+    TileGeom egeom;                             // tile geometry of expectation / H_g kernels
+};
+
+struct ProgramData {
+    int B = 0, S = 0, nmax = 0;
+    Options opt;
+    std::vector<HCircuit> circuits;
+    std::vector<std::unique_ptr<Group>> groups;
+};
+
+struct HTerm {
+    double coeff;
+    std::vector<std::pair<uint32_t, uint8_t>> factors;  // (qubit, pauli 1..3)
+};
+
+struct ObsData {
+    int B = 0, K = 0;
+    std::vector<std::vector<HTerm>> sums;  // [B*K]
+    uint64_t id = 0;
+};
+
+std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt);
+std::unique_ptr<ObsData> parse_observables(const void *blob, size_t nbytes);
+
+// Tile geometry for expectation-type kernels: low bits plus the bits most
+// often flipped by the terms' X/Y factors.
+TileGeom expectation_geometry(int n, int t, int c, const std::vector<uint64_t> &xmasks);
+
+} // namespace tq

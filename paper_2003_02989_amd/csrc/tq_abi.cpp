@@ -1,0 +1,712 @@
+// tq_abi.cpp -- the extern "C" entry points of libtq: validation, lazy
+// device upload of the plan, workspace management and the launch sequence of
+// each call.  Every call validates on the host first and then only enqueues
+// work on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "../../include/tq.h"
+#include "kernels.h"
+#include "program.h"
+
+using namespace tq;
+
+namespace {
+
+thread_local std::string g_err;
+
+[[noreturn]] void fail(int status, const std::string &m) { throw Error{status, m}; }
+
+void hip_check(hipError_t e, const char *what)
+{
+    if (e != hipSuccess) fail(TQ_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// A device allocation owned by a handle, grown on demand.
+struct DevBuf {
+    void *p = nullptr;
+    size_t bytes = 0;
+    void *ensure(size_t n)
+    {
+        if (n <= bytes && p) return p;
+        release();
+        if (n == 0) n = 256;
+        if (hipMalloc(&p, n) != hipSuccess) {
+            (void)hipGetLastError();
+            p = nullptr;
+            bytes = 0;
+            fail(TQ_E_NOMEM, "device allocation of " + std::to_string(n) + " bytes failed");
+        }
+        bytes = n;
+        return p;
+    }
+    void release()
+    {
+        if (p) (void)hipFree(p);
+        p = nullptr;
+        bytes = 0;
+    }
+};
+
+template <class T> T *upload(DevBuf &buf, const std::vector<T> &v)
+{
+    size_t n = std::max<size_t>(v.size() * sizeof(T), 16);
+    T *d = static_cast<T *>(buf.ensure(n));
+    if (!v.empty()) hip_check(hipMemcpy(d, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice), "hipMemcpy");
+    return d;
+}
+
+std::atomic<uint64_t> g_obs_counter{1};
+
+int wg_for(int nrows, int tiles_log2)
+{
+    // enough workgroups to cover the chip several times, never more than the tiles
+    int64_t tiles = (int64_t)1 << tiles_log2;
+    int64_t want = std::max<int64_t>(1, 4096 / std::max(nrows, 1));
+    return (int)std::min<int64_t>(tiles, want);
+}
+
+struct ObsGroupDev {
+    TileGeom geom;
+    int tmax = 0;
+    DevBuf terms, begin, count;
+};
+
+struct GroupDev {
+    DevBuf rows, ident, gates, slot_sym, scale, off, explicit_, tasks, members, fwd_ops, rev_ops, sym_begin,
+        sym_gslots, gslot_slot;
+    std::vector<int> fwd_op_off, rev_op_off;
+    size_t psi_off = 0;  // amplitude offset of this group's rows in the state workspaces
+    size_t mat_off = 0;  // offset in the matrix workspace
+};
+
+} // namespace
+
+struct tq_observables_s {
+    std::unique_ptr<ObsData> od;
+};
+
+struct tq_program_s {
+    std::unique_ptr<ProgramData> pd;
+    int device = -1;
+    std::vector<std::unique_ptr<GroupDev>> gdev;
+    DevBuf psi, phi, mats, partial, gpart, levels;
+    size_t psi_total = 0, mat_total = 0;
+    uint64_t obs_id = 0;
+    std::vector<std::unique_ptr<ObsGroupDev>> obs_dev;
+
+    ~tq_program_s()
+    {
+        for (auto &g : gdev) {
+            for (DevBuf *b : {&g->rows, &g->ident, &g->gates, &g->slot_sym, &g->scale, &g->off, &g->explicit_,
+                              &g->tasks, &g->members, &g->fwd_ops, &g->rev_ops, &g->sym_begin, &g->sym_gslots,
+                              &g->gslot_slot})
+                b->release();
+        }
+        for (auto &o : obs_dev) {
+            o->terms.release();
+            o->begin.release();
+            o->count.release();
+        }
+        for (DevBuf *b : {&psi, &phi, &mats, &partial, &gpart, &levels}) b->release();
+    }
+};
+
+namespace {
+
+template <class F> tq_status guarded(F &&f)
+{
+    try {
+        f();
+        g_err.clear();
+        return TQ_OK;
+    } catch (const Error &e) {
+        g_err = e.msg;
+        return (tq_status)e.status;
+    } catch (const std::bad_alloc &) {
+        g_err = "host allocation failed";
+        return TQ_E_NOMEM;
+    } catch (...) {
+        g_err = "internal error";
+        return TQ_E_DEVICE;
+    }
+}
+
+// Upload the plan to the current device on first use.
+void ensure_device(tq_program p)
+{
+    int dev = -1;
+    hip_check(hipGetDevice(&dev), "hipGetDevice");
+    if (p->device >= 0) {
+        if (dev != p->device) fail(TQ_E_INVALID, "program was first used on another device");
+        return;
+    }
+    ProgramData &pd = *p->pd;
+    size_t psi_total = 0, mat_total = 0;
+    for (auto &gp : pd.groups) {
+        const Group &g = *gp;
+        auto gd = std::make_unique<GroupDev>();
+        upload(gd->rows, g.rows);
+        std::vector<int32_t> ident(g.rows.size());
+        for (size_t i = 0; i < ident.size(); i++) ident[i] = (int32_t)i;
+        upload(gd->ident, ident);
+        upload(gd->gates, g.gates);
+        upload(gd->slot_sym, g.slot_sym);
+        upload(gd->scale, g.slot_scale);
+        upload(gd->off, g.slot_off);
+        upload(gd->explicit_, g.explicit_mats);
+        upload(gd->tasks, g.tasks);
+        upload(gd->members, g.members);
+        std::vector<PassOp> fo, ro;
+        for (const Pass &ps : g.fwd) {
+            gd->fwd_op_off.push_back((int)fo.size());
+            fo.insert(fo.end(), ps.ops.begin(), ps.ops.end());
+        }
+        for (const Pass &ps : g.rev) {
+            gd->rev_op_off.push_back((int)ro.size());
+            ro.insert(ro.end(), ps.ops.begin(), ps.ops.end());
+        }
+        upload(gd->fwd_ops, fo);
+        upload(gd->rev_ops, ro);
+        upload(gd->sym_begin, g.sym_gslot_begin);
+        upload(gd->sym_gslots, g.sym_gslots);
+        upload(gd->gslot_slot, g.gslot_slot);
+        gd->psi_off = psi_total;
+        // keep every group's rows 512-byte aligned for the vector tile loads
+        psi_total += ((g.rows.size() << g.n) + 63) & ~(size_t)63;
+        gd->mat_off = mat_total;
+        mat_total += g.rows.size() * (size_t)std::max(g.mat_block, 1);
+        p->gdev.push_back(std::move(gd));
+    }
+    p->psi_total = psi_total;
+    p->mat_total = mat_total;
+    p->device = dev;
+}
+
+float2 *psi_ws(tq_program p) { return (float2 *)p->psi.ensure(p->psi_total * sizeof(float2)); }
+float2 *phi_ws(tq_program p) { return (float2 *)p->phi.ensure(p->psi_total * sizeof(float2)); }
+float2 *mat_ws(tq_program p) { return (float2 *)p->mats.ensure(p->mat_total * sizeof(float2)); }
+
+// Symbol resolution + fused matrices for the task range [begin, end).
+void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    BuildArgs a{};
+    a.tasks = (const BuildTask *)gd.tasks.p;
+    a.task_begin = begin;
+    a.task_end = end;
+    a.members = (const Member *)gd.members.p;
+    a.gates = (const GateDev *)gd.gates.p;
+    a.slot_sym = (const int32_t *)gd.slot_sym.p;
+    a.slot_scale = (const double *)gd.scale.p;
+    a.slot_off = (const double *)gd.off.p;
+    a.uniform = g.uniform_slots;
+    a.n_slots = g.n_slots;
+    a.explicit_mats = (const double *)gd.explicit_.p;
+    a.theta = theta;
+    a.S = p->pd->S;
+    a.rows = (const int32_t *)gd.rows.p;
+    a.mats = mat_ws(p) + gd.mat_off;
+    a.mat_stride = std::max(g.mat_block, 1);
+    hip_check(launch_build(a, (int)g.rows.size(), s), "matrix build launch");
+}
+
+// Forward passes of group gi into `state` (row r of the group at
+// srows[r] * row_stride).
+void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const int32_t *srows, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    const int nrows = (int)g.rows.size();
+    for (size_t pi = 0; pi < g.fwd.size(); pi++) {
+        const Pass &ps = g.fwd[pi];
+        PassArgs a{};
+        a.state = state;
+        a.row_stride = row_stride;
+        a.rows = srows;
+        a.mats = mat_ws(p) + gd.mat_off;
+        a.mat_stride = std::max(g.mat_block, 1);
+        a.ops = (const PassOp *)gd.fwd_ops.p + gd.fwd_op_off[pi];
+        a.nops = (int)ps.ops.size();
+        a.g = ps.geom;
+        a.tiles_log2 = g.n - ps.geom.t;
+        a.wg_per_row = wg_for(nrows, a.tiles_log2);
+        a.product_init = ps.product_init;
+        for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
+        hip_check(launch_pass(a, nrows, s), "pass launch");
+    }
+}
+
+void check_obs_fit(tq_program p, tq_observables o)
+{
+    const ProgramData &pd = *p->pd;
+    const ObsData &od = *o->od;
+    if (od.B != pd.B) fail(TQ_E_INVALID, "observables batch size differs from the program's");
+    for (int b = 0; b < pd.B; b++)
+        for (int k = 0; k < od.K; k++)
+            for (const HTerm &t : od.sums[(size_t)b * od.K + k])
+                for (auto &f : t.factors)
+                    if ((int)f.first >= pd.circuits[b].n)
+                        fail(TQ_E_INVALID, "observable (" + std::to_string(b) + ", " + std::to_string(k) +
+                                               ") acts on a qubit the circuit does not have");
+}
+
+// Per-group term tables of an observables handle, in the group's
+// expectation tile geometry.
+void ensure_obs(tq_program p, tq_observables o)
+{
+    if (p->obs_id == o->od->id) return;
+    const ProgramData &pd = *p->pd;
+    const ObsData &od = *o->od;
+    std::vector<std::unique_ptr<ObsGroupDev>> out;
+    for (auto &gp : pd.groups) {
+        const Group &g = *gp;
+        const int n = g.n;
+        std::vector<std::vector<TermDev>> per_row(g.rows.size());
+        std::vector<uint64_t> xs;
+        for (size_t r = 0; r < g.rows.size(); r++) {
+            int b = g.rows[r];
+            for (int k = 0; k < od.K; k++)
+                for (const HTerm &t : od.sums[(size_t)b * od.K + k]) {
+                    TermDev td{};
+                    for (auto &f : t.factors) {
+                        uint64_t bit = 1ull << (n - 1 - (int)f.first);
+                        if (f.second == 1 || f.second == 2) td.x |= bit;
+                        if (f.second == 2 || f.second == 3) td.z |= bit;
+                        if (f.second == 2) td.ny++;
+                    }
+                    td.k = k;
+                    td.coeff = t.coeff;
+                    per_row[r].push_back(td);
+                    xs.push_back(td.x);
+                }
+        }
+        auto og = std::make_unique<ObsGroupDev>();
+        og->geom = expectation_geometry(n, std::min(p->pd->opt.tile, 12), std::min(p->pd->opt.low, 10), xs);
+        const TileGeom &gm = og->geom;
+        auto local_mask = [&](uint64_t m) {
+            uint32_t r = 0;
+            for (int k = 0; k < gm.c; k++)
+                if ((m >> k) & 1) r |= 1u << k;
+            for (int k = 0; k < gm.h; k++)
+                if ((m >> gm.hb[k]) & 1) r |= 1u << (gm.c + k);
+            return r;
+        };
+        bool uniform = true;
+        for (auto &row : per_row) {
+            for (auto &td : row) {
+                td.xout = td.x & gm.fixed_mask;
+                td.xl = local_mask(td.x);
+                td.zl = local_mask(td.z);
+            }
+        }
+        for (size_t r = 1; r < per_row.size() && uniform; r++)
+            uniform = per_row[r].size() == per_row[0].size() &&
+                      std::memcmp(per_row[r].data(), per_row[0].data(), per_row[0].size() * sizeof(TermDev)) == 0;
+        std::vector<TermDev> flat;
+        std::vector<int32_t> begin(g.rows.size()), count(g.rows.size());
+        for (size_t r = 0; r < per_row.size(); r++) {
+            if (uniform && r > 0) {
+                begin[r] = 0;
+                count[r] = (int32_t)per_row[0].size();
+                continue;
+            }
+            begin[r] = (int32_t)flat.size();
+            count[r] = (int32_t)per_row[r].size();
+            flat.insert(flat.end(), per_row[r].begin(), per_row[r].end());
+            og->tmax = std::max(og->tmax, count[r]);
+        }
+        upload(og->terms, flat);
+        upload(og->begin, begin);
+        upload(og->count, count);
+        out.push_back(std::move(og));
+    }
+    for (auto &old : p->obs_dev) {
+        old->terms.release();
+        old->begin.release();
+        old->count.release();
+    }
+    p->obs_dev = std::move(out);
+    p->obs_id = o->od->id;
+}
+
+// expectations of group gi's rows from the state workspace into out[b, k]
+void expect_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    ObsGroupDev &og = *p->obs_dev[gi];
+    const int nrows = (int)g.rows.size();
+    if (K == 0 || nrows == 0) return;
+    ExpArgs a{};
+    a.state = psi;
+    a.row_stride = (int64_t)1 << g.n;
+    a.rows = (const int32_t *)gd.ident.p;
+    a.terms = (const TermDev *)og.terms.p;
+    a.row_term_begin = (const int32_t *)og.begin.p;
+    a.row_term_count = (const int32_t *)og.count.p;
+    a.g = og.geom;
+    a.tiles_log2 = g.n - og.geom.t;
+    a.wg_per_row = wg_for(nrows, a.tiles_log2);
+    a.tmax = std::max(og.tmax, 1);
+    a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)nrows * a.wg_per_row * a.tmax);
+    hip_check(launch_expect(a, nrows, s), "expectation launch");
+    ExpReduceArgs r{};
+    r.rows = (const int32_t *)gd.rows.p;
+    r.terms = a.terms;
+    r.row_term_begin = a.row_term_begin;
+    r.row_term_count = a.row_term_count;
+    r.partial = a.partial;
+    r.wg_per_row = a.wg_per_row;
+    r.tmax = a.tmax;
+    r.K = K;
+    r.out = out;
+    hip_check(launch_expect_reduce(r, nrows, s), "expectation reduce launch");
+}
+
+hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+void check_align(const void *p, size_t a, const char *name)
+{
+    if (reinterpret_cast<uintptr_t>(p) % a != 0)
+        fail(TQ_E_INVALID, std::string(name) + " must be " + std::to_string(a) + "-byte aligned");
+}
+
+void fill_levels(SampArgs &a, int n)
+{
+    a.count[0] = (int64_t)1 << n;
+    a.off[0] = 0;
+    int k = 0;
+    int64_t total = 0;
+    while (a.count[k] > 64) {
+        a.count[k + 1] = (a.count[k] + 63) / 64;
+        a.off[k + 1] = total;
+        total += a.count[k + 1];
+        k++;
+    }
+    a.nlev = k;
+    a.row_level = std::max<int64_t>(total, 1);
+}
+
+} // namespace
+
+// ------------------------------------------------------------------- ABI
+extern "C" {
+
+const char *tq_last_error(void) { return g_err.c_str(); }
+const char *tq_version(void) { return "tq 0.1 (gfx950)"; }
+
+tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *opt, tq_program *out)
+{
+    return guarded([&] {
+        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        *out = nullptr;
+        Options o;
+        if (opt) {
+            if (opt->max_tile_qubits) {
+                if (opt->max_tile_qubits < 8 || opt->max_tile_qubits > 13)
+                    fail(TQ_E_INVALID, "max_tile_qubits must be in 8..13");
+                o.tile = opt->max_tile_qubits;
+            }
+            if (opt->low_qubits) {
+                if (opt->low_qubits < 3 || opt->low_qubits > 8) fail(TQ_E_INVALID, "low_qubits must be in 3..8");
+                o.low = opt->low_qubits;
+            }
+            if (opt->fuse < 0) o.fuse = false;
+        }
+        if (o.low > o.tile - 2) o.low = o.tile - 2;
+        auto p = std::make_unique<tq_program_s>();
+        p->pd = parse_program(blob, nbytes, o);
+        *out = p.release();
+    });
+}
+
+void tq_program_destroy(tq_program prog) { delete prog; }
+
+tq_status tq_program_info(tq_program prog, int32_t *B, int32_t *S, int32_t *max_qubits, int32_t *qpc)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        if (B) *B = prog->pd->B;
+        if (S) *S = prog->pd->S;
+        if (max_qubits) *max_qubits = prog->pd->nmax;
+        if (qpc)
+            for (int b = 0; b < prog->pd->B; b++) qpc[b] = prog->pd->circuits[b].n;
+    });
+}
+
+tq_status tq_observables_create(const void *blob, size_t nbytes, tq_observables *out)
+{
+    return guarded([&] {
+        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        *out = nullptr;
+        auto o = std::make_unique<tq_observables_s>();
+        o->od = parse_observables(blob, nbytes);
+        o->od->id = g_obs_counter.fetch_add(1);
+        *out = o.release();
+    });
+}
+
+void tq_observables_destroy(tq_observables obs) { delete obs; }
+
+tq_status tq_observables_info(tq_observables obs, int32_t *B, int32_t *K)
+{
+    return guarded([&] {
+        if (!obs) fail(TQ_E_INVALID, "observables handle is NULL");
+        if (B) *B = obs->od->B;
+        if (K) *K = obs->od->K;
+    });
+}
+
+tq_status tq_simulate_state(tq_program prog, const float *theta, void *states, void *stream)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        const ProgramData &pd = *prog->pd;
+        if (pd.B == 0) return;
+        if (!states) fail(TQ_E_INVALID, "states is NULL");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(states, 16, "states");
+        check_align(theta, 4, "symbol_values");
+        ensure_device(prog);
+        hipStream_t s = as_stream(stream);
+        const int64_t stride = (int64_t)1 << pd.nmax;
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+            forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s);
+            if (g.n < pd.nmax)
+                hip_check(launch_zero_tail((float2 *)states, stride, (const int32_t *)gd.rows.p, (int)g.rows.size(),
+                                           (int64_t)1 << g.n, stride, s),
+                          "zero tail launch");
+        }
+    });
+}
+
+tq_status tq_expectation(tq_program prog, const float *theta, tq_observables obs, float *out, void *stream)
+{
+    return guarded([&] {
+        if (!prog || !obs) fail(TQ_E_INVALID, "program or observables is NULL");
+        const ProgramData &pd = *prog->pd;
+        check_obs_fit(prog, obs);
+        if (pd.B == 0 || obs->od->K == 0) return;
+        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(out, 4, "out");
+        check_align(theta, 4, "symbol_values");
+        ensure_device(prog);
+        ensure_obs(prog, obs);
+        hipStream_t s = as_stream(stream);
+        float2 *psi = psi_ws(prog);
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+            expect_group(prog, gi, psi + gd.psi_off, obs->od->K, out, s);
+        }
+    });
+}
+
+tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables obs, const float *upstream, float *grad,
+                          float *expectations, void *stream)
+{
+    return guarded([&] {
+        if (!prog || !obs) fail(TQ_E_INVALID, "program or observables is NULL");
+        const ProgramData &pd = *prog->pd;
+        check_obs_fit(prog, obs);
+        if (pd.B == 0) return;
+        if (pd.S > 0 && (!theta || !grad)) fail(TQ_E_INVALID, "symbol_values or grad is NULL");
+        if (obs->od->K > 0 && !upstream) fail(TQ_E_INVALID, "upstream is NULL");
+        check_align(theta, 4, "symbol_values");
+        check_align(grad, 4, "grad");
+        check_align(upstream, 4, "upstream");
+        check_align(expectations, 4, "expectations");
+        ensure_device(prog);
+        ensure_obs(prog, obs);
+        hipStream_t s = as_stream(stream);
+        float2 *psi = psi_ws(prog), *phi = phi_ws(prog);
+        const int K = obs->od->K;
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            ObsGroupDev &og = *prog->obs_dev[gi];
+            const int nrows = (int)g.rows.size();
+            const int64_t stride = (int64_t)1 << g.n;
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
+            forward(prog, gi, psi + gd.psi_off, stride, (const int32_t *)gd.ident.p, s);
+            if (expectations && K > 0) expect_group(prog, gi, psi + gd.psi_off, K, expectations, s);
+            if (pd.S == 0) continue;
+            // phi = H_g psi
+            HArgs h{};
+            h.psi = psi + gd.psi_off;
+            h.phi = phi + gd.psi_off;
+            h.row_stride = stride;
+            h.rows = (const int32_t *)gd.ident.p;
+            h.brows = (const int32_t *)gd.rows.p;
+            h.terms = (const TermDev *)og.terms.p;
+            h.row_term_begin = (const int32_t *)og.begin.p;
+            h.row_term_count = (const int32_t *)og.count.p;
+            h.upstream = upstream;
+            h.K = K;
+            h.g = og.geom;
+            h.tiles_log2 = g.n - og.geom.t;
+            h.wg_per_row = wg_for(nrows, h.tiles_log2);
+            hip_check(launch_apply_h(h, nrows, s), "H_g launch");
+            // reverse sweep
+            const int trl = g.rev.empty() ? 0 : g.n - g.rev[0].geom.t;
+            const int wg = wg_for(nrows, trl);
+            double *gpart =
+                (double *)prog->gpart.ensure(sizeof(double) * (size_t)nrows * wg * std::max(g.n_gslots, 1));
+            int gbase = 0;
+            for (size_t pi = 0; pi < g.rev.size(); pi++) {
+                const Pass &ps = g.rev[pi];
+                RevArgs r{};
+                r.psi = psi + gd.psi_off;
+                r.phi = phi + gd.psi_off;
+                r.row_stride = stride;
+                r.rows = (const int32_t *)gd.ident.p;
+                r.mats = mat_ws(prog) + gd.mat_off;
+                r.mat_stride = std::max(g.mat_block, 1);
+                r.ops = (const PassOp *)gd.rev_ops.p + gd.rev_op_off[pi];
+                r.nops = (int)ps.ops.size();
+                r.g = ps.geom;
+                r.tiles_log2 = g.n - ps.geom.t;
+                r.wg_per_row = wg;
+                r.store = pi + 1 < g.rev.size();
+                r.gpart = gpart;
+                r.n_gslots = g.n_gslots;
+                int gc = 0;
+                for (const PassOp &op : ps.ops) gc += op.ngrad;
+                r.gbase = gbase;
+                r.gcount = gc;
+                gbase += gc;
+                hip_check(launch_rev_pass(r, nrows, s), "reverse pass launch");
+            }
+            GradReduceArgs gr{};
+            gr.rows = (const int32_t *)gd.rows.p;
+            gr.gpart = gpart;
+            gr.wg_per_row = wg;
+            gr.n_gslots = g.n_gslots;
+            gr.sym_begin = (const int32_t *)gd.sym_begin.p;
+            gr.sym_gslots = (const int32_t *)gd.sym_gslots.p;
+            gr.gslot_slot = (const int32_t *)gd.gslot_slot.p;
+            gr.slot_scale = (const double *)gd.scale.p;
+            gr.uniform = g.uniform_slots;
+            gr.n_slots = g.n_slots;
+            gr.S = pd.S;
+            gr.grad = grad;
+            hip_check(launch_grad_reduce(gr, nrows, s), "gradient reduce launch");
+        }
+    });
+}
+
+tq_status tq_sample(tq_program prog, const float *theta, int64_t n_shots, uint64_t seed, uint64_t *out, void *stream)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        if (n_shots < 0) fail(TQ_E_INVALID, "n_shots is negative");
+        const ProgramData &pd = *prog->pd;
+        if (pd.B == 0 || n_shots == 0) return;
+        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(out, 8, "out");
+        check_align(theta, 4, "symbol_values");
+        ensure_device(prog);
+        hipStream_t s = as_stream(stream);
+        float2 *psi = psi_ws(prog);
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+            SampArgs a{};
+            a.state = psi + gd.psi_off;
+            a.row_stride = (int64_t)1 << g.n;
+            a.rows = (const int32_t *)gd.ident.p;
+            a.brows = (const int32_t *)gd.rows.p;
+            fill_levels(a, g.n);
+            a.levels = (uint64_t *)prog->levels.ensure(sizeof(uint64_t) * a.row_level * g.rows.size());
+            a.n_shots = n_shots;
+            a.seed = seed;
+            a.out = out;
+            hip_check(launch_sample(a, (int)g.rows.size(), s), "sampler launch");
+        }
+    });
+}
+
+tq_status tq_amplitudes(tq_program prog, const float *theta, const uint64_t *bitstrings, int64_t M, void *amps,
+                        void *stream)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        if (M < 0) fail(TQ_E_INVALID, "M is negative");
+        const ProgramData &pd = *prog->pd;
+        if (pd.B == 0 || M == 0) return;
+        if (!bitstrings || !amps) fail(TQ_E_INVALID, "bitstrings or amps is NULL");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(bitstrings, 8, "bitstrings");
+        check_align(amps, 8, "amps");
+        check_align(theta, 4, "symbol_values");
+        ensure_device(prog);
+        hipStream_t s = as_stream(stream);
+        float2 *psi = psi_ws(prog);
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+            GatherArgs a{};
+            a.state = psi + gd.psi_off;
+            a.row_stride = (int64_t)1 << g.n;
+            a.rows = (const int32_t *)gd.ident.p;
+            a.brows = (const int32_t *)gd.rows.p;
+            a.n = g.n;
+            a.bits = bitstrings;
+            a.M = M;
+            a.out = (float2 *)amps;
+            hip_check(launch_gather(a, (int)g.rows.size(), s), "gather launch");
+        }
+    });
+}
+
+tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
+                               uint64_t *out, void *stream)
+{
+    return guarded([&] {
+        if (B < 0 || n < 0 || n > kMaxQubits || n_shots < 0) fail(TQ_E_INVALID, "bad B, n or n_shots");
+        if (B == 0 || n_shots == 0) return;
+        if (!states || !out) fail(TQ_E_INVALID, "states or out is NULL");
+        check_align(states, 8, "states");
+        check_align(out, 8, "out");
+        hipStream_t s = as_stream(stream);
+        SampArgs a{};
+        a.state = (const float2 *)states;
+        a.row_stride = (int64_t)1 << n;
+        fill_levels(a, n);
+        // stream-ordered workspace: allocated and released in the stream's order
+        void *lv = nullptr;
+        if (hipMallocAsync(&lv, sizeof(uint64_t) * a.row_level * (size_t)B, s) != hipSuccess) {
+            (void)hipGetLastError();
+            fail(TQ_E_NOMEM, "sampler workspace allocation failed");
+        }
+        a.levels = (uint64_t *)lv;
+        a.n_shots = n_shots;
+        a.seed = seed;
+        a.out = out;
+        hipError_t e = launch_sample(a, B, s);
+        hipError_t f = hipFreeAsync(lv, s);
+        hip_check(e, "sampler launch");
+        hip_check(f, "hipFreeAsync");
+    });
+}
+
+} // extern "C"

@@ -1,0 +1,97 @@
+// tq_internal.h -- data structures shared by the host planner and the HIP
+// kernels of libtq.  Nothing here is part of the public ABI.
+#pragma once
+#include <cstdint>
+
+namespace tq {
+
+// Opcodes of the program blob (the public list is in include/tq.h).
+enum Opcode : uint16_t {
+    OP_H = 1, OP_X, OP_Y, OP_Z, OP_RX, OP_RY, OP_RZ, OP_XPOW, OP_YPOW, OP_ZPOW,
+    OP_CZ, OP_CNOT, OP_CZPOW, OP_CNOTPOW, OP_XXPOW, OP_YYPOW, OP_ZZPOW, OP_RZZ,
+    OP_SQRTX, OP_SQRTY, OP_SQRTW, OP_FSIM, OP_MATRIX1, OP_MATRIX2, OP_SWAP,
+    OP_COUNT
+};
+
+constexpr int kMaxQubits = 32;
+constexpr int kThreads = 256;  // threads per workgroup of every tile kernel
+constexpr uint8_t kFixed = 0xFF;  // "bit not in the tile" marker
+constexpr int kMaxGradPerPass = 1024;  // gradient slots one reverse pass accumulates
+
+// One gate of a structure, as the device matrix builder reads it.
+struct GateDev {
+    uint16_t op;
+    uint8_t nq, np;
+    int32_t slot0;     // first of its np parameter slots
+    int32_t explicit_; // index of its explicit matrix (MATRIX1/2) or -1
+};
+
+// How a matrix is rendered by the builder.
+enum Form : uint8_t {
+    FORM_FULL = 0,   // 2x2 for 1q gates, 4x4 for 2q gates
+    FORM_CBLOCK = 1, // 2x2 target block of a controlled gate (CNOT, CNOTPOW)
+};
+
+// A member of a fused product: gate index, and for a 2q gate inside a 2q
+// product whether its qubit order is reversed relative to the product's.
+struct Member {
+    int32_t gate;
+    uint8_t swapped;
+    uint8_t form;
+    uint8_t pad[2];
+};
+
+// Build tasks of the matrix builder; each writes one matrix per batch row.
+enum TaskKind : uint8_t {
+    BT_PRODUCT = 0, // product of members (last member applied last)
+    BT_DAGGER = 1,  // conjugate transpose of a single member
+    BT_DERIV = 2,   // derivative of a single member w.r.t. parameter `which`
+};
+
+struct BuildTask {
+    uint8_t kind;
+    uint8_t dim;    // 2 or 4
+    uint8_t diag;   // store only the diagonal (dim entries)
+    uint8_t which;  // BT_DERIV parameter index
+    int32_t out;    // offset (complex entries) in the row's matrix block
+    int32_t mem_begin, mem_count;
+};
+
+// Kinds of ops a tile pass applies.
+enum OpKind : uint8_t {
+    K_M1 = 1, // dense 2x2 on local bit q0; optional control qubit q1
+    K_M2 = 2, // dense 4x4 on local bits (q0 = first qubit, q1 = second)
+    K_D1 = 3, // diagonal on q0 (local or fixed)
+    K_D2 = 4, // diagonal on (q0, q1), entry index 2*bit(q0) + bit(q1)
+};
+
+struct PassOp {
+    uint8_t kind;
+    uint8_t l0, l1;   // local bit of q0 / q1 in the tile, kFixed if outside
+    uint8_t p0, p1;   // global bit position of q0 / q1
+    uint8_t ctrl;     // K_M1: 1 if q1 is a control qubit
+    uint8_t cval;     // K_M1: the control value that enables the op
+    uint8_t ngrad;    // reverse ops: symbolic parameters (0..2)
+    int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
+    int32_t dmat[2];  // reverse: offsets of dW/deta_j
+    int32_t gslot[2]; // reverse: gradient slot ids
+};
+
+// Tile geometry of a pass: t local bits = `c` low bits + high bits hb[].
+struct TileGeom {
+    int32_t n, t, c, h;
+    uint64_t fixed_mask; // global bits (< n) outside the tile
+    uint8_t hb[kMaxQubits];
+};
+
+// A Pauli term with masks in global index bits and in tile-local bits.
+struct TermDev {
+    uint64_t x, z;      // global masks
+    uint64_t xout;      // bits of x outside the tile
+    uint32_t xl, zl;    // local masks
+    int32_t k;          // observable index
+    int32_t ny;         // number of Y factors (mod 4 used)
+    double coeff;
+};
+
+} // namespace tq

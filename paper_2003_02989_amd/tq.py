@@ -1,0 +1,197 @@
+"""Python binding of libtq: argument marshalling only.
+
+Every function takes torch tensors that live on the current HIP device,
+checks their dtype, shape and contiguity, and passes raw device pointers and
+the current stream to the C ABI declared in include/tq.h.  All arithmetic
+happens in the library's HIP kernels; there is no fallback: if libtq.so
+cannot be loaded every call raises.
+"""
+import ctypes
+import os
+import struct
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtq.so")
+
+TQ_OK, TQ_E_INVALID, TQ_E_UNSUPPORTED, TQ_E_NOMEM, TQ_E_DEVICE = range(5)
+_STATUS = {1: "TQ_E_INVALID", 2: "TQ_E_UNSUPPORTED", 3: "TQ_E_NOMEM", 4: "TQ_E_DEVICE"}
+
+
+class TQError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class _Options(ctypes.Structure):
+    _fields_ = [("max_tile_qubits", ctypes.c_int32), ("low_qubits", ctypes.c_int32),
+                ("fuse", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libtq.so (raises OSError when it is missing: there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise OSError(f"{LIB_PATH} is missing: build it with `python -m paper_2003_02989_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, u64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
+        p32 = ctypes.POINTER(ctypes.c_int32)
+        L.tq_last_error.restype = ctypes.c_char_p
+        L.tq_version.restype = ctypes.c_char_p
+        L.tq_program_create.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(_Options), ctypes.POINTER(vp)]
+        L.tq_program_destroy.argtypes = [vp]
+        L.tq_program_destroy.restype = None
+        L.tq_program_info.argtypes = [vp, p32, p32, p32, p32]
+        L.tq_observables_create.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(vp)]
+        L.tq_observables_destroy.argtypes = [vp]
+        L.tq_observables_destroy.restype = None
+        L.tq_observables_info.argtypes = [vp, p32, p32]
+        L.tq_simulate_state.argtypes = [vp, vp, vp, vp]
+        L.tq_expectation.argtypes = [vp, vp, vp, vp, vp]
+        L.tq_sample.argtypes = [vp, vp, i64, u64, vp, vp]
+        L.tq_adjoint_grad.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.tq_amplitudes.argtypes = [vp, vp, vp, i64, vp, vp]
+        L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
+        for f in ("tq_program_create", "tq_program_info", "tq_observables_create", "tq_observables_info",
+                  "tq_simulate_state", "tq_expectation", "tq_sample", "tq_adjoint_grad", "tq_amplitudes",
+                  "tq_sample_from_state"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != TQ_OK:
+        raise TQError(rc, lib().tq_last_error().decode())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, dtype, shape, name):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Program:
+    """A parsed and planned batch of circuits (``tq_program``)."""
+
+    def __init__(self, blob: bytes, max_tile_qubits=0, low_qubits=0, fuse=True):
+        opt = _Options(max_tile_qubits, low_qubits, 1 if fuse else -1, 0)
+        h = ctypes.c_void_p()
+        _check(lib().tq_program_create(blob, len(blob), ctypes.byref(opt), ctypes.byref(h)))
+        self._h = h
+        B, S, n = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().tq_program_info(h, ctypes.byref(B), ctypes.byref(S), ctypes.byref(n), None))
+        self.B, self.S, self.max_qubits = B.value, S.value, n.value
+        q = (ctypes.c_int32 * max(self.B, 1))()
+        _check(lib().tq_program_info(h, None, None, None, q))
+        self.qubits = list(q)[: self.B]
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().tq_program_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+
+class Observables:
+    """B x K Pauli sums (``tq_observables``)."""
+
+    def __init__(self, blob: bytes):
+        h = ctypes.c_void_p()
+        _check(lib().tq_observables_create(blob, len(blob), ctypes.byref(h)))
+        self._h = h
+        self.B, self.K = struct.unpack_from("<II", blob, 8)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().tq_observables_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+
+def _theta(prog, symbol_values):
+    if prog.S == 0:
+        return None
+    return _dev(symbol_values, torch.float32, (prog.B, prog.S), "symbol_values")
+
+
+def simulate_state(prog, symbol_values, out=None, stream=None):
+    if out is None:
+        out = torch.empty((prog.B, 1 << prog.max_qubits), dtype=torch.complex64, device="cuda")
+    p = _dev(out, torch.complex64, (prog.B, 1 << prog.max_qubits), "states")
+    _check(lib().tq_simulate_state(prog._h, _theta(prog, symbol_values), p, _stream(stream)))
+    return out
+
+
+def expectation(prog, symbol_values, obs, out=None, stream=None):
+    if out is None:
+        out = torch.empty((prog.B, obs.K), dtype=torch.float32, device="cuda")
+    p = _dev(out, torch.float32, (prog.B, obs.K), "out")
+    _check(lib().tq_expectation(prog._h, _theta(prog, symbol_values), obs._h, p, _stream(stream)))
+    return out
+
+
+def adjoint_grad(prog, symbol_values, obs, upstream, grad=None, expectations=None, stream=None):
+    """Returns grad [B, S]; fills `expectations` [B, K] too when given."""
+    if grad is None:
+        grad = torch.empty((prog.B, prog.S), dtype=torch.float32, device="cuda")
+    g = _dev(grad, torch.float32, (prog.B, prog.S), "grad") if prog.S else None
+    u = _dev(upstream, torch.float32, (prog.B, obs.K), "upstream")
+    e = _dev(expectations, torch.float32, (prog.B, obs.K), "expectations")
+    _check(lib().tq_adjoint_grad(prog._h, _theta(prog, symbol_values), obs._h, u, g, e, _stream(stream)))
+    return grad
+
+
+def sample(prog, symbol_values, n_shots, seed, out=None, stream=None):
+    """Bitstrings as int64 [B, n_shots] (the bit patterns of the uint64 output)."""
+    if out is None:
+        out = torch.empty((prog.B, n_shots), dtype=torch.int64, device="cuda")
+    p = _dev(out, torch.int64, (prog.B, n_shots), "out")
+    _check(lib().tq_sample(prog._h, _theta(prog, symbol_values), int(n_shots), ctypes.c_uint64(seed), p,
+                           _stream(stream)))
+    return out
+
+
+def amplitudes(prog, symbol_values, bitstrings, out=None, stream=None):
+    M = bitstrings.shape[1]
+    b = _dev(bitstrings, torch.int64, (prog.B, M), "bitstrings")
+    if out is None:
+        out = torch.empty((prog.B, M), dtype=torch.complex64, device="cuda")
+    p = _dev(out, torch.complex64, (prog.B, M), "amps")
+    _check(lib().tq_amplitudes(prog._h, _theta(prog, symbol_values), b, M, p, _stream(stream)))
+    return out
+
+
+def sample_from_state(states, n_shots, seed, out=None, stream=None):
+    B, N = states.shape
+    n = N.bit_length() - 1
+    if (1 << n) != N:
+        raise ValueError("state length must be a power of two")
+    s = _dev(states, torch.complex64, (B, N), "states")
+    if out is None:
+        out = torch.empty((B, n_shots), dtype=torch.int64, device="cuda")
+    p = _dev(out, torch.int64, (B, n_shots), "out")
+    _check(lib().tq_sample_from_state(s, B, n, int(n_shots), ctypes.c_uint64(seed), p, _stream(stream)))
+    return out

@@ -1,0 +1,106 @@
+"""Host-side checks of the C ABI, no GPU needed: libtq.so loads, exports
+every function include/tq.h declares, and rejects malformed input on the
+host before any device call."""
+import ctypes
+import os
+import re
+import struct
+
+import pytest
+
+from paper_2003_02989_amd import tq
+from paper_2003_02989_amd import workloads as wl
+from paper_2003_02989_amd.circuits import Circuit, observable_blob, program_blob, sym
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "tq.h")).read()
+    return sorted(set(re.findall(r"\b(tq_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 14
+    L = tq.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def create(blob, **kw):
+    return tq.Program(blob, **kw)
+
+
+def status_of(fn):
+    with pytest.raises(tq.TQError) as e:
+        fn()
+    return e.value.status
+
+
+def test_program_info_roundtrip():
+    w = wl.random_batch(3, B=5, n=6, n_gates=12, n_symbols=3, hetero=True)
+    p = create(w.program_blob())
+    assert (p.B, p.S, p.max_qubits) == (5, 3, max(c.n for c in w.circuits))
+    assert p.qubits == [c.n for c in w.circuits]
+
+
+def gate_blob(op, nq, npar, qubits, params=(), n=3, S=1):
+    body = struct.pack("<HBB", op, nq, npar) + struct.pack(f"<{len(qubits)}I", *qubits)
+    for s, scale, off in params:
+        body += struct.pack("<idd", s, scale, off)
+    return b"TQP1" + struct.pack("<III", 1, 1, S) + struct.pack("<II", n, 1) + body
+
+
+def test_bad_programs_are_rejected_on_the_host():
+    good = gate_blob(5, 1, 1, [0], [(0, 1.0, 0.0)])
+    create(good)
+    assert status_of(lambda: create(b"XXXX" + good[4:])) == tq.TQ_E_INVALID
+    assert status_of(lambda: create(good[:-3])) == tq.TQ_E_INVALID
+    assert status_of(lambda: create(good + b"\0")) == tq.TQ_E_INVALID
+    assert status_of(lambda: create(gate_blob(5, 1, 1, [3], [(0, 1.0, 0.0)]))) == tq.TQ_E_INVALID  # qubit >= n
+    assert status_of(lambda: create(gate_blob(11, 2, 0, [1, 1]))) == tq.TQ_E_INVALID  # repeated qubit
+    assert status_of(lambda: create(gate_blob(5, 1, 1, [0], [(1, 1.0, 0.0)]))) == tq.TQ_E_INVALID  # symbol >= S
+    assert status_of(lambda: create(gate_blob(5, 2, 1, [0, 1], [(0, 1.0, 0.0)]))) == tq.TQ_E_INVALID  # arity
+    assert status_of(lambda: create(gate_blob(99, 1, 0, [0]))) == tq.TQ_E_UNSUPPORTED  # opcode
+    big = b"TQP1" + struct.pack("<III", 1, 1, 0) + struct.pack("<II", 33, 0)
+    assert status_of(lambda: create(big)) == tq.TQ_E_UNSUPPORTED
+    assert status_of(lambda: create(good, max_tile_qubits=20)) == tq.TQ_E_INVALID
+
+
+def test_bad_observables_are_rejected():
+    ok = observable_blob([[[(1.0, [(0, "Z")])]]])
+    tq.Observables(ok)
+    bad_code = ok[:-1] + b"\x07"
+    assert status_of(lambda: tq.Observables(bad_code)) == tq.TQ_E_INVALID
+    dup = observable_blob([[[(1.0, [(0, "Z"), (0, "X")])]]])
+    assert status_of(lambda: tq.Observables(dup)) == tq.TQ_E_INVALID
+    assert status_of(lambda: tq.Observables(ok[:-2])) == tq.TQ_E_INVALID
+
+
+def test_compute_calls_validate_before_touching_the_device():
+    L = tq.lib()
+    c = Circuit(2).add("RX", 0, [sym(0)]).add("CNOT", (0, 1))
+    p = create(program_blob([c, c], 1))
+    o = tq.Observables(observable_blob([[[(1.0, [(1, "Z")])]]] * 2))
+    o1 = tq.Observables(observable_blob([[[(1.0, [(1, "Z")])]]]))
+    o3 = tq.Observables(observable_blob([[[(1.0, [(2, "Z")])]]] * 2))
+    fake = ctypes.c_void_p(16)
+    assert L.tq_expectation(p._h, fake, o._h, None, None) == tq.TQ_E_INVALID  # out NULL
+    assert L.tq_expectation(p._h, None, o._h, fake, None) == tq.TQ_E_INVALID  # theta NULL with S > 0
+    assert L.tq_expectation(p._h, fake, o1._h, fake, None) == tq.TQ_E_INVALID  # batch mismatch
+    assert L.tq_expectation(p._h, fake, o3._h, fake, None) == tq.TQ_E_INVALID  # qubit >= n_b
+    assert b"qubit" in L.tq_last_error()
+    assert L.tq_sample(p._h, fake, -1, 0, fake, None) == tq.TQ_E_INVALID
+    assert L.tq_amplitudes(p._h, fake, None, 3, fake, None) == tq.TQ_E_INVALID
+    assert L.tq_adjoint_grad(p._h, fake, o._h, None, fake, None, None) == tq.TQ_E_INVALID
+    assert L.tq_simulate_state(p._h, fake, None, None) == tq.TQ_E_INVALID
+    assert L.tq_sample_from_state(fake, 1, 40, 1, 0, fake, None) == tq.TQ_E_INVALID
+    assert L.tq_program_create(b"", 0, None, None) == tq.TQ_E_INVALID
+    # empty work is a no-op that needs no device
+    assert L.tq_sample(p._h, fake, 0, 0, None, None) == tq.TQ_OK
+    assert L.tq_sample_from_state(None, 0, 3, 5, 0, None, None) == tq.TQ_OK
+
+
+def test_version():
+    assert tq.lib().tq_version().startswith(b"tq ")

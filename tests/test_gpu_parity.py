@@ -1,0 +1,109 @@
+"""GPU parity: the HIP library against the complex128 oracle on the same
+seeded inputs, at sizes the oracle finishes in seconds: random circuits over
+the whole opcode set (heterogeneous batches, several tile passes, fixed bits,
+partner tiles in HBM), planner options, determinism."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL_AMP, TOL_EXP, compare, dev, gpu_outputs, oracle_outputs, say
+from oracle import oracle as orc
+from paper_2003_02989_amd import tq
+from paper_2003_02989_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_small_heterogeneous(seed):
+    w = wl.random_batch(9000 + seed, B=6, n=7, n_gates=40, n_symbols=4, K=3, hetero=True)
+    say("random small", seed)
+    compare(gpu_outputs(w), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("n,tile,low", [(10, 8, 3), (12, 8, 6), (13, 9, 4), (14, 12, 6), (11, 8, 5)])
+def test_random_tiled(n, tile, low):
+    # n > tile: several passes, diagonal and control bits outside the tile,
+    # expectation partners in other tiles
+    w = wl.random_batch(100 * n + tile, B=3, n=n, n_gates=60, n_symbols=5, K=2)
+    say("random tiled", n, tile, low)
+    compare(gpu_outputs(w, max_tile_qubits=tile, low_qubits=low), oracle_outputs(w))
+
+
+def test_unfused_matches():
+    w = wl.random_batch(4242, B=4, n=9, n_gates=50, n_symbols=3, K=2)
+    compare(gpu_outputs(w, fuse=False), oracle_outputs(w))
+    compare(gpu_outputs(w, max_tile_qubits=8, fuse=False), oracle_outputs(w))
+
+
+def test_amplitudes_and_padding():
+    w = wl.random_batch(77, B=5, n=8, n_gates=30, n_symbols=2, K=1, hetero=True)
+    p = tq.Program(w.program_blob())
+    th = dev(w.theta)
+    st = tq.simulate_state(p, th).cpu().numpy()
+    ref = oracle_outputs(w, want=("state",))["state"]
+    for b, c in enumerate(w.circuits):
+        assert not np.any(st[b, 1 << c.n:]), "zero padding"
+    rng = np.random.default_rng(5)
+    bits = np.stack([rng.integers(0, 1 << c.n, size=33) for c in w.circuits]).astype(np.int64)
+    bits[0, 0] = 1 << 40  # out of range -> zero amplitude
+    a = tq.amplitudes(p, th, dev(bits, torch.int64)).cpu().numpy()
+    for b in range(w.B):
+        for m in range(33):
+            x = int(bits[b, m])
+            want = ref[b, x] if x < ref.shape[1] and (x >> w.circuits[b].n) == 0 else 0
+            assert abs(a[b, m] - want) < TOL_AMP
+
+
+def test_bitwise_deterministic():
+    w = wl.random_batch(31337, B=4, n=13, n_gates=60, n_symbols=6, K=3)
+    a = gpu_outputs(w, max_tile_qubits=9)
+    b = gpu_outputs(w, max_tile_qubits=9)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_no_symbols_and_empty_circuits():
+    from paper_2003_02989_amd.circuits import Circuit
+    c0 = Circuit(3)
+    c1 = Circuit(2).add("H", 0).add("CNOT", (0, 1))
+    w = wl.Workload("mixed", [c0, c1], 0, np.zeros((2, 0), np.float32),
+                    [[[(1.0, [(0, "Z")]), (0.5, [])]], [[(1.0, [(0, "Z"), (1, "Z")])]]], np.ones((2, 1), np.float32))
+    g = gpu_outputs(w, want=("state", "exp"))
+    compare(g, oracle_outputs(w, want=("state", "exp")))
+    assert abs(g["exp"][0, 0] - 1.5) < TOL_EXP and abs(g["exp"][1, 0] - 1.0) < TOL_EXP
+
+
+@pytest.mark.parametrize("n", [3, 6, 12, 17])
+def test_sampler_bit_exact_on_shared_state(n):
+    rng = np.random.default_rng(n)
+    B = 3
+    z = (rng.standard_normal((B, 1 << n)) + 1j * rng.standard_normal((B, 1 << n))).astype(np.complex64)
+    z /= np.linalg.norm(z, axis=1, keepdims=True)
+    z = z.astype(np.complex64)
+    z[1, ::3] = 0  # zero-probability outcomes are never drawn
+    shots = 20000
+    g = tq.sample_from_state(dev(z, torch.complex64), shots, seed=1234 + n).cpu().numpy().astype(np.uint64)
+    r = orc.sample_from_state(z, shots, seed=1234 + n)
+    say("sampler", n, "mismatches", int((g != r).sum()))
+    assert np.array_equal(g, r)
+    assert not np.any((g[1] % 3) == 0)
+
+
+def test_full_pipeline_samples_fall_in_oracle_intervals():
+    # samples of the complex64 pipeline must fall in the oracle's CDF interval
+    # widened by the state difference (the two states differ by rounding)
+    w = wl.random_batch(555, B=2, n=8, n_gates=40, n_symbols=3, K=1)
+    p = tq.Program(w.program_blob())
+    shots, seed = 4000, 99
+    g = tq.sample(p, dev(w.theta), shots, seed).cpu().numpy().astype(np.uint64)
+    ref_state = oracle_outputs(w, want=("state",))["state"]
+    gst = tq.simulate_state(p, dev(w.theta)).cpu().numpy()
+    for b in range(w.B):
+        pr = np.abs(ref_state[b]) ** 2
+        C = np.concatenate([[0.0], np.cumsum(pr)])
+        delta = 2 * np.linalg.norm(gst[b] - ref_state[b]) + 1e-9
+        for k in range(shots):
+            u = orc.splitmix64(seed, b * shots + k) / 2.0 ** 64
+            i = int(g[b, k])
+            assert C[i] - delta <= u * C[-1] <= C[i + 1] + delta
