@@ -1,0 +1,271 @@
+"""Benchmark of the batched state-vector hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config c2|c1|c3|c4|c5] [--no-cpu-baseline]
+
+One step is one call of the configuration's hot path on its full batch with
+inputs resident in HBM:
+  c1, c2, c5  tq_adjoint_grad with expectation output (forward passes, Pauli-sum
+              expectations, H_g, reverse adjoint passes, gradient reduction)
+  c3          tq_expectation
+  c4          tq_amplitudes (4096 bitstrings) + tq_sample (10^6 shots)
+The default workload is c2, the 10-qubit QNN classifier with batch 1024.
+Rank 0 prints one JSON line.  The dominant kernel (largest device time per
+step, measured with HIP events) gets a roofline entry; the oracle, timed on
+the host's cores on a bounded sample, gives the cpu_baseline entry.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "effective HBM GB/s per fused-gate pass; circuit-expectations/sec at batch"
+KERNELS = ("build", "pass", "expect", "expect_reduce", "apply_h", "rev_pass", "grad_reduce", "samp_l1",
+           "samp_shots", "gather")
+PEAK_HBM_GBS = 8000.0
+PEAK_FP32_TFLOPS = 157.3
+
+
+def workload(name):
+    from paper_2003_02989_amd import workloads as wl
+    return wl.CONFIGS[name]()
+
+
+def describe_workload(name, w):
+    n = w.n_max
+    if name == "c1":
+        return f"c1 hardware-efficient ansatz n={n} B={w.B} 2 layers RX,RY,RZ + CZ ladder, sum Z, expectations+adjoint grads"
+    if name == "c2":
+        return f"c2 QNN classifier n={n} B={w.B} RX(pi x) encoding + 4 layers ZZ^t, XX^t to readout, Z_9, expectations+adjoint grads"
+    if name == "c3":
+        return f"c3 QAOA MaxCut n={n} B={w.B} p=4 random 3-regular graph, cut observable, expectations"
+    if name == "c4":
+        return f"c4 random circuit n={n} B=1 depth 20 sqrtX/Y/W + fSim 5x6 grid, 4096 amplitudes + 10^6 samples"
+    return f"c5 VQE ansatz n={n} B={w.B} 10 layers RY,RZ + CNOT ring, 200 Pauli strings, expectations+adjoint grads"
+
+
+# algorithmic work of one op applied to one amplitude (complex mul = 6 flops,
+# complex add = 2): dense 2x2 matvec 14, dense 4x4 30, diagonal 6; a
+# controlled 2x2 touches half the amplitudes
+def op_flops(op, n_local_ctrl):
+    k = op["kind"]
+    if k == "M1":
+        return 7.0 if (op["ctrl"] and n_local_ctrl) else 14.0
+    if k == "M2":
+        return 30.0
+    return 6.0
+
+
+def kernel_work(plan, kernel, n_obs_terms, n_rows_total):
+    """Algorithmic (flops, HBM bytes) of all launches of `kernel` in one step,
+    and the number of those launches, from the program's plan."""
+    flops = bytes_ = 0.0
+    launches = 0
+    for g in plan["groups"]:
+        amps = float(g["rows"]) * (1 << g["n"])
+        if kernel == "pass":
+            for ps in g["fwd"]:
+                launches += 1
+                f = 12.0 if ps["product_init"] else 0.0
+                for op in ps["ops"]:
+                    f += op_flops(op, op["ctrl"] and op["l"][1] != 255)
+                flops += f * amps
+                bytes_ += (8.0 if ps["product_init"] else 16.0) * amps
+        elif kernel == "rev_pass":
+            for i, ps in enumerate(g["rev"]):
+                launches += 1
+                f = 0.0
+                for op in ps["ops"]:
+                    base = op_flops(op, op["ctrl"] and op["l"][1] != 255)
+                    f += 2 * base + op["ngrad"] * (base + 4.0)
+                flops += f * amps
+                bytes_ += (32.0 if i + 1 < len(g["rev"]) else 16.0) * amps
+        elif kernel == "expect":
+            launches += 1
+            flops += 4.0 * n_obs_terms * amps
+            bytes_ += 8.0 * amps
+        elif kernel == "apply_h":
+            launches += 1
+            flops += 8.0 * n_obs_terms * amps
+            bytes_ += 16.0 * amps
+    return flops, bytes_, launches
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the batched path has no "
+              "multi-GPU mode in this build", file=sys.stderr)
+        sys.exit(1)
+
+    import numpy as np
+    import torch
+
+    from paper_2003_02989_amd import tq
+
+    local_rank = int(os.environ.get("LOCAL_RANK", "0"))
+    torch.cuda.set_device(local_rank)
+    w = workload(args.config)
+    B, K = w.B, w.K
+    t_cold0 = time.perf_counter()
+    prog = tq.Program(w.program_blob())
+    obs = tq.Observables(w.observable_blob())
+    t_create = time.perf_counter() - t_cold0
+    theta = torch.as_tensor(w.theta, device="cuda") if w.n_symbols else None
+    up = torch.as_tensor(w.upstream, device="cuda")
+    exp = torch.empty((B, K), dtype=torch.float32, device="cuda")
+    grad = torch.empty((B, w.n_symbols), dtype=torch.float32, device="cuda")
+    if args.config == "c4":
+        bits = torch.as_tensor(w.extras["bitstrings"].astype(np.int64), device="cuda")
+        amps = torch.empty((1, bits.shape[1]), dtype=torch.complex64, device="cuda")
+        n_shots = w.extras["n_shots"]
+        shots = torch.empty((1, n_shots), dtype=torch.int64, device="cuda")
+
+    def step():
+        if args.config in ("c1", "c2", "c5"):
+            tq.adjoint_grad(prog, theta, obs, up, grad=grad, expectations=exp)
+        elif args.config == "c3":
+            tq.expectation(prog, theta, obs, out=exp)
+        else:
+            tq.amplitudes(prog, None, bits, out=amps)
+            tq.sample(prog, None, n_shots, w.extras["seed"], out=shots)
+
+    t0 = time.perf_counter()
+    step()
+    torch.cuda.synchronize()
+    t_first = time.perf_counter() - t0
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # dominant kernel: device time per step of every kernel, from HIP events
+    per_kernel = {}
+    for kname in KERNELS:
+        tq.profile_start(kname)
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        n_l, ms = tq.profile_read()
+        tq.profile_start(None)
+        if n_l:
+            per_kernel[kname] = ms / 2
+    dominant = max(per_kernel, key=per_kernel.get)
+
+    # timed region; the dominant kernel's launches are bracketed by events
+    tq.profile_start(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    n_launch, dom_ms = tq.profile_read()
+    tq.profile_start(None)
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    plan = tq.describe(prog)
+    n_terms = sum(len(t) for t in w.observables[0])
+    flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, B)
+    avg_ms = dom_ms / max(n_launch, 1)
+    if args.config in ("c1", "c2"):
+        bound, unit, peak = "alu", "TFLOP/s", PEAK_FP32_TFLOPS
+        achieved = (flops / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e12
+        traffic = None
+    else:
+        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+        achieved = (bytes_ / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e9
+        traffic = None
+
+    if args.config == "c4":
+        value = B * amps.shape[1] / (ms_per_step * 1e-3)
+        unit_v = "amplitudes/s (with 10^6 samples per step)"
+    else:
+        value = B * K / (ms_per_step * 1e-3)
+        unit_v = "circuit-expectations/s" + (" (with adjoint gradients)" if args.config in ("c1", "c2", "c5") else "")
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": unit_v,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "c64",
+        "data": "synthetic (seeded generators, no datasets)",
+        "config": {"workload": describe_workload(args.config, w), "batch": B, "qubits": w.n_max,
+                   "symbols": w.n_symbols, "observables": K, "pauli_terms": n_terms,
+                   "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3},
+        "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": traffic, "launches_per_step": launches_per_step,
+                     "avg_launch_ms": avg_ms,
+                     "algorithmic_per_launch": (flops if bound == "alu" else bytes_) / max(launches_per_step, 1)},
+        "kernel_ms_per_step": per_kernel,
+    }
+
+    if not args.no_cpu_baseline and local_rank == 0:
+        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(name, w, budget_s):
+    """The oracle on the host cores, on a bounded sample of the same workload."""
+    import numpy as np
+
+    from oracle import oracle as orc
+    orc.build()
+    threads = orc.num_threads()
+    if name == "c4":
+        from paper_2003_02989_amd import workloads as wl
+        ws = wl.c4_random(rows=4, cols=6, n_shots=10_000)
+        p = orc.Program(ws.program_blob())
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            orc.amplitudes(p, np.zeros((1, 0)), ws.extras["bitstrings"])
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+        dt = (time.perf_counter() - t0) / reps
+        return {"value": 4096 / dt, "unit": "amplitudes/s", "cores": threads, "kind": "oracle",
+                "sample": f"24-qubit (4x6 grid) version of the depth-20 circuit, full simulation per call, {reps} calls"}
+    rows = 1
+    done_rows = 0
+    t0 = time.perf_counter()
+    while True:
+        r = list(range(min(rows, w.B)))
+        from paper_2003_02989_amd.workloads import Workload
+        sub = Workload(w.name, [w.circuits[i] for i in r], w.n_symbols, w.theta[r], [w.observables[i] for i in r],
+                       w.upstream[r])
+        p = orc.Program(sub.program_blob())
+        o = orc.Observables(sub.observable_blob())
+        th = sub.theta.astype(np.float64)
+        orc.expectation(p, th, o)
+        if name != "c3":
+            orc.adjoint_grad(p, th, o, sub.upstream.astype(np.float64))
+        done_rows += len(r)
+        el = time.perf_counter() - t0
+        if el > budget_s:
+            break
+        rows = min(max(rows * 2, 1), w.B)
+    what = "expectations" + (" + adjoint gradients" if name != "c3" else "")
+    return {"value": done_rows * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "
+                      f"the full batch) in {el:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -158,6 +158,22 @@ tq_status tq_amplitudes(tq_program prog, const float *symbol_values, const uint6
 tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
                                uint64_t *out, void *stream);
 
+/* Plan introspection: a JSON description of the program's structure groups
+ * and of the tile passes planned for each (tile bits, ops, fused members,
+ * gradient slots).  Writes at most cap bytes (NUL terminated) into buf and
+ * the full size including the NUL into *needed (either may be NULL). */
+tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *needed);
+
+/* Kernel timing for benchmarks.  After tq_profile_start(name) every launch of
+ * the named kernel ("build", "pass", "expect", "expect_reduce", "apply_h",
+ * "rev_pass", "grad_reduce", "samp_l1", "samp_shots", "gather") is bracketed
+ * by a pair of HIP events recorded on its launch stream; NULL or "" stops
+ * recording.  tq_profile_read waits for the recorded events, returns the
+ * number of bracketed launches and their total duration in milliseconds, and
+ * clears the record.  Process-wide; not meant for concurrent use. */
+tq_status tq_profile_start(const char *kernel);
+tq_status tq_profile_read(int64_t *launches, double *total_ms);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *tq_last_error(void);
 const char *tq_version(void);

@@ -21,7 +21,7 @@ struct BuildArgs {
     const float *theta;
     int S;
     const int32_t *rows;
-    float2 *mats;
+    double2 *mats;
     int64_t mat_stride;
 };
 
@@ -29,7 +29,7 @@ struct PassArgs {
     float2 *state;
     int64_t row_stride;
     const int32_t *rows;
-    const float2 *mats;
+    const double2 *mats;
     int64_t mat_stride;
     const PassOp *ops;
     int nops;
@@ -79,7 +79,7 @@ struct RevArgs {
     float2 *psi, *phi;
     int64_t row_stride;
     const int32_t *rows;
-    const float2 *mats;
+    const double2 *mats;
     int64_t mat_stride;
     const PassOp *ops;
     int nops;
@@ -127,6 +127,8 @@ struct GatherArgs {
     float2 *out;
 };
 
+void profile_start(const char *kernel);
+hipError_t profile_read(int64_t *launches, double *total_ms);
 size_t pass_lds_bytes(const TileGeom &g, bool product_init);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);

@@ -10,21 +10,32 @@
 // floating-point atomics), so every output is bitwise reproducible.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <string>
+#include <vector>
+
 #include "kernels.h"
 
 namespace tq {
 
 // ------------------------------------------------------------ small helpers
-__device__ __forceinline__ float2 cmul(float2 a, float2 b)
+// fp64 arithmetic on complex64 amplitudes: gate matrices stay in float64 and
+// every product is formed in float64; only the stored amplitude is rounded
+__device__ __forceinline__ double2 up2(float2 a) { return make_double2((double)a.x, (double)a.y); }
+__device__ __forceinline__ float2 down2(double2 a) { return make_float2((float)a.x, (float)a.y); }
+__device__ __forceinline__ double2 zmul(double2 a, double2 b)
 {
-    return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+    return make_double2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
 }
-__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
-__device__ __forceinline__ float2 cmul2(float2 m0, float2 a0, float2 m1, float2 a1)
+__device__ __forceinline__ double2 zmul2(double2 m0, double2 a0, double2 m1, double2 a1)
 {
-    return make_float2(m0.x * a0.x - m0.y * a0.y + m1.x * a1.x - m1.y * a1.y,
-                       m0.x * a0.y + m0.y * a0.x + m1.x * a1.y + m1.y * a1.x);
+    return make_double2(m0.x * a0.x - m0.y * a0.y + m1.x * a1.x - m1.y * a1.y,
+                        m0.x * a0.y + m0.y * a0.x + m1.x * a1.y + m1.y * a1.x);
 }
+__device__ __forceinline__ double2 zadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
+// Re(conj(a) b)
+__device__ __forceinline__ double zdotr(double2 a, double2 b) { return a.x * b.x + a.y * b.y; }
+
 // insert a zero bit at position k of p
 __device__ __forceinline__ uint32_t ins0(uint32_t p, int k) { return ((p >> k) << (k + 1)) | (p & ((1u << k) - 1)); }
 
@@ -249,11 +260,11 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
             for (int i = 0; i < d * d; i++) acc[i] = t[i];
         }
     }
-    float2 *out = a.mats + (int64_t)row * a.mat_stride + bt.out;
+    double2 *out = a.mats + (int64_t)row * a.mat_stride + bt.out;
     if (bt.diag) {
-        for (int i = 0; i < d; i++) out[i] = make_float2((float)acc[i * d + i].x, (float)acc[i * d + i].y);
+        for (int i = 0; i < d; i++) out[i] = make_double2(acc[i * d + i].x, acc[i * d + i].y);
     } else {
-        for (int i = 0; i < d * d; i++) out[i] = make_float2((float)acc[i].x, (float)acc[i].y);
+        for (int i = 0; i < d * d; i++) out[i] = make_double2(acc[i].x, acc[i].y);
     }
 }
 
@@ -308,12 +319,12 @@ __device__ __forceinline__ int bit_of(uint8_t loc, uint8_t pos, uint32_t l, uint
 }
 
 // ------------------------------------------------------ forward tile ops
-__device__ void apply_op(const PassOp &op, const float2 *__restrict__ m, float2 *lds, int t, uint64_t fb)
+__device__ void apply_op(const PassOp &op, const double2 *__restrict__ m, float2 *lds, int t, uint64_t fb)
 {
     const uint32_t T = 1u << t;
     const int tid = threadIdx.x, nt = blockDim.x;
     if (op.kind == K_M1) {
-        const float2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+        const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
         const int tb = op.l0;
         if (op.ctrl && op.l1 != kFixed) {
             const int cb = op.l1;
@@ -321,41 +332,41 @@ __device__ void apply_op(const PassOp &op, const float2 *__restrict__ m, float2 
             const uint32_t cv = (uint32_t)op.cval << cb;
             for (uint32_t p = tid; p < T / 4; p += nt) {
                 uint32_t i = ins0(ins0(p, lo), hi) | cv, j = i | (1u << tb);
-                float2 a0 = lds[i], a1 = lds[j];
-                lds[i] = cmul2(m00, a0, m01, a1);
-                lds[j] = cmul2(m10, a0, m11, a1);
+                double2 a0 = up2(lds[i]), a1 = up2(lds[j]);
+                lds[i] = down2(zmul2(m00, a0, m01, a1));
+                lds[j] = down2(zmul2(m10, a0, m11, a1));
             }
             return;
         }
         if (op.ctrl && (int)((fb >> op.p1) & 1) != op.cval) return;
         for (uint32_t p = tid; p < T / 2; p += nt) {
             uint32_t i = ins0(p, tb), j = i | (1u << tb);
-            float2 a0 = lds[i], a1 = lds[j];
-            lds[i] = cmul2(m00, a0, m01, a1);
-            lds[j] = cmul2(m10, a0, m11, a1);
+            double2 a0 = up2(lds[i]), a1 = up2(lds[j]);
+            lds[i] = down2(zmul2(m00, a0, m01, a1));
+            lds[j] = down2(zmul2(m10, a0, m11, a1));
         }
     } else if (op.kind == K_M2) {
-        float2 mm[16];
+        double2 mm[16];
         for (int i = 0; i < 16; i++) mm[i] = m[i];
         const int b0 = op.l0, b1 = op.l1;
         const int lo = min(b0, b1), hi = max(b0, b1);
         for (uint32_t p = tid; p < T / 4; p += nt) {
             uint32_t i00 = ins0(ins0(p, lo), hi);
             uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
-            float2 v0 = lds[i00], v1 = lds[i01], v2 = lds[i10], v3 = lds[i11];
-            lds[i00] = cadd(cmul2(mm[0], v0, mm[1], v1), cmul2(mm[2], v2, mm[3], v3));
-            lds[i01] = cadd(cmul2(mm[4], v0, mm[5], v1), cmul2(mm[6], v2, mm[7], v3));
-            lds[i10] = cadd(cmul2(mm[8], v0, mm[9], v1), cmul2(mm[10], v2, mm[11], v3));
-            lds[i11] = cadd(cmul2(mm[12], v0, mm[13], v1), cmul2(mm[14], v2, mm[15], v3));
+            double2 v0 = up2(lds[i00]), v1 = up2(lds[i01]), v2 = up2(lds[i10]), v3 = up2(lds[i11]);
+            lds[i00] = down2(zadd(zmul2(mm[0], v0, mm[1], v1), zmul2(mm[2], v2, mm[3], v3)));
+            lds[i01] = down2(zadd(zmul2(mm[4], v0, mm[5], v1), zmul2(mm[6], v2, mm[7], v3)));
+            lds[i10] = down2(zadd(zmul2(mm[8], v0, mm[9], v1), zmul2(mm[10], v2, mm[11], v3)));
+            lds[i11] = down2(zadd(zmul2(mm[12], v0, mm[13], v1), zmul2(mm[14], v2, mm[15], v3)));
         }
     } else {  // diagonal K_D1 / K_D2
         const bool two = op.kind == K_D2;
-        float2 d[4];
+        double2 d[4];
         for (int i = 0; i < (two ? 4 : 2); i++) d[i] = m[i];
         for (uint32_t l = tid; l < T; l += nt) {
             int idx = bit_of(op.l0, op.p0, l, fb);
             if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
-            lds[l] = cmul(d[idx], lds[l]);
+            lds[l] = down2(zmul(d[idx], up2(lds[l])));
         }
     }
 }
@@ -369,14 +380,14 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
     const int T = 1 << t;
     float2 *lds = reinterpret_cast<float2 *>(smem);
     uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
-    float2 *p1 = reinterpret_cast<float2 *>(hi_off + (1 << g.h));
+    double2 *p1 = reinterpret_cast<double2 *>(hi_off + (1 << g.h));
     const int a1 = t / 2;
-    float2 *p2 = p1 + (1 << a1);
+    double2 *p2 = p1 + (1 << a1);
 
     const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
     const int b = a.rows[row];
     float2 *st = a.state + (int64_t)b * a.row_stride;
-    const float2 *M = a.mats + (int64_t)row * a.mat_stride;
+    const double2 *M = a.mats + (int64_t)row * a.mat_stride;
     build_hi_off(g, hi_off);
     TileCtx tc{&g, hi_off, (1u << g.c) - 1};
 
@@ -386,12 +397,12 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
             const bool first = j < (1 << a1);
             const int k0 = first ? 0 : a1, k1 = first ? a1 : t;
             const int v = first ? j : j - (1 << a1);
-            float2 acc = make_float2(1.f, 0.f);
+            double2 acc = make_double2(1.0, 0.0);
             for (int k = k0; k < k1; k++) {
                 int pos = k < g.c ? k : g.hb[k - g.c];
                 int q = g.n - 1 - pos;
-                const float2 *im = M + a.init_mat[q];
-                acc = cmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
+                const double2 *im = M + a.init_mat[q];
+                acc = zmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
             }
             if (first) p1[v] = acc;
             else p2[v] = acc;
@@ -403,14 +414,14 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
     for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
         const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
         if (a.product_init) {
-            float2 f = make_float2(1.f, 0.f);
+            double2 f = make_double2(1.0, 0.0);
             for (uint64_t fm = g.fixed_mask; fm; fm &= fm - 1) {
                 int pos = __ffsll((unsigned long long)fm) - 1;
-                const float2 *im = M + a.init_mat[g.n - 1 - pos];
-                f = cmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
+                const double2 *im = M + a.init_mat[g.n - 1 - pos];
+                f = zmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
             }
             for (int l = threadIdx.x; l < T; l += blockDim.x)
-                lds[l] = cmul(f, cmul(p1[l & ((1 << a1) - 1)], p2[l >> a1]));
+                lds[l] = down2(zmul(f, zmul(p1[l & ((1 << a1) - 1)], p2[l >> a1])));
         } else {
             tile_copy<true>(tc, lds, st, fb, T);
         }
@@ -433,7 +444,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
 // where m is the lowest set bit of x's in-tile part (partner in LDS) or, when
 // x flips fixed bits, of its out-of-tile part (partner tile in HBM, and only
 // tiles with that bit clear count the pair).
-__device__ __forceinline__ double re_iny(int ny, double s, float2 A)
+__device__ __forceinline__ double re_iny(int ny, double s, double2 A)
 {
     switch (ny & 3) {
     case 0: return s * A.x;
@@ -452,8 +463,8 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
     if (tm.x == 0) {
         const int zf = par64(fb & tm.z);
         for (uint32_t l = tid; l < T; l += nt) {
-            float2 v = lds[l];
-            double pr = (double)v.x * v.x + (double)v.y * v.y;
+            double2 v = up2(lds[l]);
+            double pr = v.x * v.x + v.y * v.y;
             acc += ((zf ^ par32(l & tm.zl)) ? -pr : pr);
         }
     } else if (tm.xout == 0) {
@@ -461,8 +472,8 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
         const int mb = __ffs(tm.xl) - 1;
         for (uint32_t p = tid; p < T / 2; p += nt) {
             uint32_t i = ins0(p, mb), j = i ^ tm.xl;
-            float2 a = lds[i], c = lds[j];
-            float2 A = make_float2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);  // conj(a) c
+            double2 a = up2(lds[i]), c = up2(lds[j]);
+            double2 A = make_double2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);  // conj(a) c
             double s = (zf ^ par32(j & tm.zl)) ? -2.0 : 2.0;
             acc += re_iny(tm.ny, s, A);
         }
@@ -473,8 +484,8 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
         const int zf = par64(fj & tm.z);
         for (uint32_t l = tid; l < T; l += nt) {
             uint32_t lj = l ^ tm.xl;
-            float2 a = lds[l], c = row[tile_index(tc, fj, lj)];
-            float2 A = make_float2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);
+            double2 a = up2(lds[l]), c = up2(row[tile_index(tc, fj, lj)]);
+            double2 A = make_double2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);
             double s = (zf ^ par32(lj & tm.zl)) ? -2.0 : 2.0;
             acc += re_iny(tm.ny, s, A);
         }
@@ -611,7 +622,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
     const int b = a.rows[row];
     float2 *sp = a.psi + (int64_t)b * a.row_stride;
     float2 *sf = a.phi + (int64_t)b * a.row_stride;
-    const float2 *M = a.mats + (int64_t)row * a.mat_stride;
+    const double2 *M = a.mats + (int64_t)row * a.mat_stride;
     build_hi_off(g, hi_off);
     for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) acc[j] = 0;
     TileCtx tc{&g, hi_off, (1u << g.c) - 1};
@@ -627,13 +638,15 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         __syncthreads();
         for (int oi = 0; oi < a.nops; oi++) {
             const PassOp op = a.ops[oi];
-            const float2 *m = M + op.mat;
+            const double2 *m = M + op.mat;
             double g0 = 0, g1 = 0;
             if (op.kind == K_M1) {
-                const float2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
-                float2 d0[4] = {}, d1[4] = {};
-                for (int i = 0; i < 4 && op.ngrad > 0; i++) d0[i] = M[op.dmat[0] + i];
-                for (int i = 0; i < 4 && op.ngrad > 1; i++) d1[i] = M[op.dmat[1] + i];
+                const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+                double2 d0[4], d1[4];
+                for (int i = 0; i < 4; i++) {
+                    d0[i] = op.ngrad > 0 ? M[op.dmat[0] + i] : make_double2(0, 0);
+                    d1[i] = op.ngrad > 1 ? M[op.dmat[1] + i] : make_double2(0, 0);
+                }
                 const int tb = op.l0;
                 bool active = true;
                 uint32_t count = T / 2;
@@ -654,25 +667,21 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
                     for (uint32_t p = tid; p < count; p += nt) {
                         uint32_t i = cb >= 0 ? (ins0(ins0(p, lo), hi) | cv) : ins0(p, tb);
                         uint32_t j = i | (1u << tb);
-                        float2 a0 = lp[i], a1 = lp[j];
-                        float2 b0 = cmul2(m00, a0, m01, a1), b1 = cmul2(m10, a0, m11, a1);
-                        lp[i] = b0;
-                        lp[j] = b1;
-                        float2 f0 = lf[i], f1 = lf[j];
-                        if (op.ngrad > 0) {
-                            float2 e0 = cmul2(d0[0], b0, d0[1], b1), e1 = cmul2(d0[2], b0, d0[3], b1);
-                            g0 += (double)(f0.x * e0.x + f0.y * e0.y) + (double)(f1.x * e1.x + f1.y * e1.y);
-                        }
-                        if (op.ngrad > 1) {
-                            float2 e0 = cmul2(d1[0], b0, d1[1], b1), e1 = cmul2(d1[2], b0, d1[3], b1);
-                            g1 += (double)(f0.x * e0.x + f0.y * e0.y) + (double)(f1.x * e1.x + f1.y * e1.y);
-                        }
-                        lf[i] = cmul2(m00, f0, m01, f1);
-                        lf[j] = cmul2(m10, f0, m11, f1);
+                        double2 a0 = up2(lp[i]), a1 = up2(lp[j]);
+                        double2 b0 = zmul2(m00, a0, m01, a1), b1 = zmul2(m10, a0, m11, a1);
+                        lp[i] = down2(b0);
+                        lp[j] = down2(b1);
+                        double2 f0 = up2(lf[i]), f1 = up2(lf[j]);
+                        if (op.ngrad > 0)
+                            g0 += zdotr(f0, zmul2(d0[0], b0, d0[1], b1)) + zdotr(f1, zmul2(d0[2], b0, d0[3], b1));
+                        if (op.ngrad > 1)
+                            g1 += zdotr(f0, zmul2(d1[0], b0, d1[1], b1)) + zdotr(f1, zmul2(d1[2], b0, d1[3], b1));
+                        lf[i] = down2(zmul2(m00, f0, m01, f1));
+                        lf[j] = down2(zmul2(m10, f0, m11, f1));
                     }
                 }
             } else if (op.kind == K_M2) {
-                float2 mm[16];
+                double2 mm[16];
                 for (int i = 0; i < 16; i++) mm[i] = m[i];
                 const int b0 = op.l0, b1 = op.l1;
                 const int lo = min(b0, b1), hi = max(b0, b1);
@@ -682,51 +691,43 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
                     ix[1] = ix[0] | (1u << b1);
                     ix[2] = ix[0] | (1u << b0);
                     ix[3] = ix[1] | (1u << b0);
-                    float2 v[4], u[4], f[4];
-                    for (int r = 0; r < 4; r++) v[r] = lp[ix[r]];
+                    double2 v[4], u[4], f[4];
+                    for (int r = 0; r < 4; r++) v[r] = up2(lp[ix[r]]);
                     for (int r = 0; r < 4; r++)
-                        u[r] = cadd(cmul2(mm[4 * r], v[0], mm[4 * r + 1], v[1]),
-                                    cmul2(mm[4 * r + 2], v[2], mm[4 * r + 3], v[3]));
-                    for (int r = 0; r < 4; r++) lp[ix[r]] = u[r];
-                    for (int r = 0; r < 4; r++) f[r] = lf[ix[r]];
+                        u[r] = zadd(zmul2(mm[4 * r], v[0], mm[4 * r + 1], v[1]), zmul2(mm[4 * r + 2], v[2], mm[4 * r + 3], v[3]));
+                    for (int r = 0; r < 4; r++) lp[ix[r]] = down2(u[r]);
+                    for (int r = 0; r < 4; r++) f[r] = up2(lf[ix[r]]);
                     for (int gq = 0; gq < op.ngrad; gq++) {
-                        const float2 *dm = M + op.dmat[gq];
-                        double s = 0;
-                        for (int r = 0; r < 4; r++) {
-                            float2 e = cadd(cmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
-                                            cmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3]));
-                            s += (double)(f[r].x * e.x + f[r].y * e.y);
-                        }
-                        if (gq == 0) g0 += s;
-                        else g1 += s;
+                        const double2 *dm = M + op.dmat[gq];
+                        double sacc = 0;
+                        for (int r = 0; r < 4; r++)
+                            sacc += zdotr(f[r], zadd(zmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
+                                                     zmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3])));
+                        if (gq == 0) g0 += sacc;
+                        else g1 += sacc;
                     }
                     for (int r = 0; r < 4; r++)
-                        lf[ix[r]] = cadd(cmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]),
-                                         cmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3]));
+                        lf[ix[r]] = down2(zadd(zmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]),
+                                               zmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3])));
                 }
             } else {
                 const bool two = op.kind == K_D2;
-                float2 d[4], dd0[4] = {}, dd1[4] = {};
-                for (int i = 0; i < (two ? 4 : 2); i++) {
-                    d[i] = m[i];
-                    if (op.ngrad > 0) dd0[i] = M[op.dmat[0] + i];
-                    if (op.ngrad > 1) dd1[i] = M[op.dmat[1] + i];
+                double2 d[4], dd0[4], dd1[4];
+                for (int i = 0; i < 4; i++) {
+                    const bool in = i < (two ? 4 : 2);
+                    d[i] = in ? m[i] : make_double2(0, 0);
+                    dd0[i] = in && op.ngrad > 0 ? M[op.dmat[0] + i] : make_double2(0, 0);
+                    dd1[i] = in && op.ngrad > 1 ? M[op.dmat[1] + i] : make_double2(0, 0);
                 }
                 for (uint32_t l = tid; l < T; l += nt) {
                     int idx = bit_of(op.l0, op.p0, l, fb);
                     if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
-                    float2 u = cmul(d[idx], lp[l]);
-                    lp[l] = u;
-                    float2 f = lf[l];
-                    if (op.ngrad > 0) {
-                        float2 e = cmul(dd0[idx], u);
-                        g0 += (double)(f.x * e.x + f.y * e.y);
-                    }
-                    if (op.ngrad > 1) {
-                        float2 e = cmul(dd1[idx], u);
-                        g1 += (double)(f.x * e.x + f.y * e.y);
-                    }
-                    lf[l] = cmul(d[idx], f);
+                    double2 u = zmul(d[idx], up2(lp[l]));
+                    lp[l] = down2(u);
+                    double2 f = up2(lf[l]);
+                    if (op.ngrad > 0) g0 += zdotr(f, zmul(dd0[idx], u));
+                    if (op.ngrad > 1) g1 += zdotr(f, zmul(dd1[idx], u));
+                    lf[l] = down2(zmul(d[idx], f));
                 }
             }
             if (op.ngrad > 0) {
@@ -889,6 +890,64 @@ __global__ void k_zero_tail(float2 *state, int64_t row_stride, const int32_t *ro
 }
 
 // ------------------------------------------------------- launch wrappers
+// Opt-in profiler: launches of the selected kernel are bracketed by a pair
+// of HIP events recorded on the launch stream.
+namespace prof {
+std::mutex mu;
+std::string target;
+std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+
+struct Scope {
+    hipEvent_t b = nullptr, e = nullptr;
+    hipStream_t s;
+    Scope(const char *name, hipStream_t st) : s(st)
+    {
+        std::lock_guard<std::mutex> l(mu);
+        if (target.empty() || target != name) return;
+        if (hipEventCreate(&b) != hipSuccess || hipEventCreate(&e) != hipSuccess) {
+            b = e = nullptr;
+            return;
+        }
+        (void)hipEventRecord(b, s);
+    }
+    ~Scope()
+    {
+        if (!b) return;
+        (void)hipEventRecord(e, s);
+        std::lock_guard<std::mutex> l(mu);
+        events.emplace_back(b, e);
+    }
+};
+} // namespace prof
+
+void profile_start(const char *kernel)
+{
+    std::lock_guard<std::mutex> l(prof::mu);
+    prof::target = kernel ? kernel : "";
+}
+
+hipError_t profile_read(int64_t *launches, double *total_ms)
+{
+    std::lock_guard<std::mutex> l(prof::mu);
+    double tot = 0;
+    hipError_t err = hipSuccess;
+    for (auto &pe : prof::events) {
+        float ms = 0;
+        hipError_t e = hipEventSynchronize(pe.second);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, pe.first, pe.second);
+        if (e != hipSuccess) err = e;
+        tot += ms;
+    }
+    *launches = (int64_t)prof::events.size();
+    *total_ms = tot;
+    for (auto &pe : prof::events) {
+        (void)hipEventDestroy(pe.first);
+        (void)hipEventDestroy(pe.second);
+    }
+    prof::events.clear();
+    return err;
+}
+
 namespace {
 template <class K> hipError_t set_lds(K kernel, size_t bytes)
 {
@@ -903,6 +962,7 @@ hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s)
     int n = a.task_end - a.task_begin;
     if (n <= 0 || nrows <= 0) return hipSuccess;
     dim3 grid((n + 255) / 256, nrows);
+    prof::Scope ps("build", s);
     hipLaunchKernelGGL(k_build_mats, grid, dim3(256), 0, s, a);
     return hipGetLastError();
 }
@@ -910,7 +970,7 @@ hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s)
 size_t pass_lds_bytes(const TileGeom &g, bool product_init)
 {
     size_t b = sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h);
-    if (product_init) b += sizeof(float2) * (((size_t)1 << (g.t / 2)) + ((size_t)1 << (g.t - g.t / 2)));
+    if (product_init) b += sizeof(double2) * (((size_t)1 << (g.t / 2)) + ((size_t)1 << (g.t - g.t / 2)));
     return b;
 }
 
@@ -919,6 +979,7 @@ hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s)
     size_t lds = pass_lds_bytes(a.g, a.product_init != 0);
     hipError_t e = set_lds(k_pass, lds);
     if (e != hipSuccess) return e;
+    prof::Scope ps("pass", s);
     hipLaunchKernelGGL(k_pass, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
@@ -929,12 +990,14 @@ hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s)
                  sizeof(double) * 4 * kTermChunk;
     hipError_t e = set_lds(k_expect, lds);
     if (e != hipSuccess) return e;
+    prof::Scope ps("expect", s);
     hipLaunchKernelGGL(k_expect, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_expect_reduce(const ExpReduceArgs &a, int nrows, hipStream_t s)
 {
+    prof::Scope ps("expect_reduce", s);
     hipLaunchKernelGGL(k_expect_reduce, dim3(nrows), dim3(64), 0, s, a);
     return hipGetLastError();
 }
@@ -944,6 +1007,7 @@ hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s)
     size_t lds = sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h);
     hipError_t e = set_lds(k_apply_h, lds);
     if (e != hipSuccess) return e;
+    prof::Scope ps("apply_h", s);
     hipLaunchKernelGGL(k_apply_h, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
@@ -954,12 +1018,14 @@ hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s)
                  sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
     hipError_t e = set_lds(k_rev_pass, lds);
     if (e != hipSuccess) return e;
+    prof::Scope ps("rev_pass", s);
     hipLaunchKernelGGL(k_rev_pass, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s)
 {
+    prof::Scope ps("grad_reduce", s);
     hipLaunchKernelGGL(k_grad_reduce, dim3(nrows), dim3(256), 0, s, a);
     return hipGetLastError();
 }
@@ -968,18 +1034,24 @@ hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s)
 {
     if (nrows <= 0) return hipSuccess;
     if (a.nlev >= 1) {
-        hipLaunchKernelGGL(k_samp_l1, dim3((unsigned)((a.count[1] + 3) / 4), nrows), dim3(256), 0, s, a);
+        {
+            prof::Scope ps("samp_l1", s);
+            hipLaunchKernelGGL(k_samp_l1, dim3((unsigned)((a.count[1] + 3) / 4), nrows), dim3(256), 0, s, a);
+        }
         for (int k = 1; k < a.nlev; k++)
             hipLaunchKernelGGL(k_samp_up, dim3((unsigned)((a.count[k + 1] + 3) / 4), nrows), dim3(256), 0, s, a, k);
     }
-    if (a.n_shots > 0)
+    if (a.n_shots > 0) {
+        prof::Scope ps("samp_shots", s);
         hipLaunchKernelGGL(k_samp_shots, dim3((unsigned)((a.n_shots + 3) / 4), nrows), dim3(256), 0, s, a);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s)
 {
     if (a.M <= 0 || nrows <= 0) return hipSuccess;
+    prof::Scope ps("gather", s);
     hipLaunchKernelGGL(k_gather, dim3((unsigned)((a.M + 255) / 256), nrows), dim3(256), 0, s, a);
     return hipGetLastError();
 }

@@ -6,6 +6,8 @@
 
 #include <algorithm>
 #include <atomic>
+#include <map>
+#include <sstream>
 #include <cstring>
 #include <memory>
 #include <string>
@@ -191,7 +193,7 @@ void ensure_device(tq_program p)
 
 float2 *psi_ws(tq_program p) { return (float2 *)p->psi.ensure(p->psi_total * sizeof(float2)); }
 float2 *phi_ws(tq_program p) { return (float2 *)p->phi.ensure(p->psi_total * sizeof(float2)); }
-float2 *mat_ws(tq_program p) { return (float2 *)p->mats.ensure(p->mat_total * sizeof(float2)); }
+double2 *mat_ws(tq_program p) { return (double2 *)p->mats.ensure(p->mat_total * sizeof(double2)); }
 
 // Symbol resolution + fused matrices for the task range [begin, end).
 void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end, hipStream_t s)
@@ -706,6 +708,73 @@ tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t
         hipError_t f = hipFreeAsync(lv, s);
         hip_check(e, "sampler launch");
         hip_check(f, "hipFreeAsync");
+    });
+}
+
+tq_status tq_profile_start(const char *kernel)
+{
+    return guarded([&] { profile_start(kernel); });
+}
+
+tq_status tq_profile_read(int64_t *launches, double *total_ms)
+{
+    return guarded([&] {
+        if (!launches || !total_ms) fail(TQ_E_INVALID, "launches or total_ms is NULL");
+        hip_check(profile_read(launches, total_ms), "profile read");
+    });
+}
+
+tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *needed)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        const ProgramData &pd = *prog->pd;
+        std::ostringstream o;
+        static const char *kinds[] = {"?", "M1", "M2", "D1", "D2"};
+        o << "{\"B\":" << pd.B << ",\"S\":" << pd.S << ",\"nmax\":" << pd.nmax << ",\"tile\":" << pd.opt.tile
+          << ",\"low\":" << pd.opt.low << ",\"groups\":[";
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            std::map<int32_t, int> members_at;  // matrix offset -> member count
+            for (const BuildTask &bt : g.tasks)
+                if (bt.kind != BT_DERIV) members_at[bt.out] = bt.mem_count;
+            int absorbed = 0;
+            for (int q = 0; q < g.n; q++)
+                for (const BuildTask &bt : g.tasks)
+                    if (bt.out == g.init_mat[q]) absorbed += bt.mem_count;
+            o << (gi ? "," : "") << "{\"n\":" << g.n << ",\"rows\":" << g.rows.size() << ",\"gates\":" << g.gates.size()
+              << ",\"slots\":" << g.n_slots << ",\"mat_block\":" << g.mat_block << ",\"n_gslots\":" << g.n_gslots
+              << ",\"absorbed\":" << absorbed << ",\"uniform_slots\":" << (g.uniform_slots ? 1 : 0);
+            for (int dir = 0; dir < 2; dir++) {
+                const std::vector<Pass> &pv = dir == 0 ? g.fwd : g.rev;
+                o << (dir == 0 ? ",\"fwd\":[" : ",\"rev\":[");
+                for (size_t pi = 0; pi < pv.size(); pi++) {
+                    const Pass &ps = pv[pi];
+                    o << (pi ? "," : "") << "{\"t\":" << ps.geom.t << ",\"c\":" << ps.geom.c << ",\"h\":" << ps.geom.h
+                      << ",\"hb\":[";
+                    for (int k = 0; k < ps.geom.h; k++) o << (k ? "," : "") << (int)ps.geom.hb[k];
+                    o << "],\"product_init\":" << (ps.product_init ? 1 : 0) << ",\"ops\":[";
+                    for (size_t k = 0; k < ps.ops.size(); k++) {
+                        const PassOp &op = ps.ops[k];
+                        o << (k ? "," : "") << "{\"kind\":\"" << kinds[op.kind] << "\",\"p\":[" << (int)op.p0 << ","
+                          << (int)op.p1 << "],\"l\":[" << (int)op.l0 << "," << (int)op.l1 << "],\"ctrl\":" << (int)op.ctrl
+                          << ",\"ngrad\":" << (int)op.ngrad << ",\"members\":"
+                          << (members_at.count(op.mat) ? members_at[op.mat] : 0) << "}";
+                    }
+                    o << "]}";
+                }
+                o << "]";
+            }
+            o << "}";
+        }
+        o << "]}";
+        const std::string js = o.str();
+        if (needed) *needed = js.size() + 1;
+        if (buf && cap > 0) {
+            size_t n = std::min(cap - 1, js.size());
+            std::memcpy(buf, js.data(), n);
+            buf[n] = 0;
+        }
     });
 }
 

@@ -58,9 +58,12 @@ def lib():
         L.tq_adjoint_grad.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.tq_amplitudes.argtypes = [vp, vp, vp, i64, vp, vp]
         L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
+        L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
+        L.tq_profile_start.argtypes = [ctypes.c_char_p]
+        L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
         for f in ("tq_program_create", "tq_program_info", "tq_observables_create", "tq_observables_info",
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_adjoint_grad", "tq_amplitudes",
-                  "tq_sample_from_state"):
+                  "tq_sample_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -107,9 +110,9 @@ class Program:
         self.qubits = list(q)[: self.B]
 
     def close(self):
-        if getattr(self, "_h", None):
-            lib().tq_program_destroy(self._h)
-            self._h = None
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.tq_program_destroy(h)
 
     __del__ = close
 
@@ -124,11 +127,32 @@ class Observables:
         self.B, self.K = struct.unpack_from("<II", blob, 8)
 
     def close(self):
-        if getattr(self, "_h", None):
-            lib().tq_observables_destroy(self._h)
-            self._h = None
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.tq_observables_destroy(h)
 
     __del__ = close
+
+
+def describe(prog):
+    """The plan of a program as a dict (tq_program_describe)."""
+    import json
+    need = ctypes.c_size_t()
+    _check(lib().tq_program_describe(prog._h, None, 0, ctypes.byref(need)))
+    buf = ctypes.create_string_buffer(need.value)
+    _check(lib().tq_program_describe(prog._h, buf, need.value, None))
+    return json.loads(buf.value.decode())
+
+
+def profile_start(kernel):
+    _check(lib().tq_profile_start(kernel.encode() if kernel else None))
+
+
+def profile_read():
+    """(launches, total_ms) of the bracketed launches since profile_start."""
+    n, ms = ctypes.c_int64(), ctypes.c_double()
+    _check(lib().tq_profile_read(ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
 
 
 def _theta(prog, symbol_values):

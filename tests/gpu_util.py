@@ -67,3 +67,12 @@ def compare(gpu, ref, tol_exp=TOL_EXP, tol_grad=TOL_GRAD, tol_amp=TOL_AMP):
         if "exp" in ref:
             err = np.abs(gpu["grad_exp"] - ref["exp"]).max()
             assert err <= tol_exp, f"expectation (adjoint call) error {err:.3e}"
+
+
+def sub_workload(w, rows):
+    """The rows `rows` of workload w as a workload of their own (the oracle
+    computes sampled rows of a full-size batch one by one)."""
+    from paper_2003_02989_amd.workloads import Workload
+    rows = list(rows)
+    return Workload(w.name + "_rows", [w.circuits[r] for r in rows], w.n_symbols, w.theta[rows],
+                    [w.observables[r] for r in rows], w.upstream[rows], dict(w.extras))

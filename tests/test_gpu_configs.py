@@ -1,0 +1,111 @@
+"""GPU parity on the five workload configurations: at full size where the
+oracle finishes in seconds (c1, c2), on reduced sizes that still span several
+tiles, and at full size on sampled rows the oracle computes one by one (c3,
+c5) or against stored oracle values (c4, tests/golden/c4_n30.npz written by
+tests/golden/make_c4_golden.py)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import TOL_AMP, TOL_EXP, TOL_GRAD, compare, dev, gpu_outputs, oracle_outputs, say, sub_workload
+from oracle import oracle as orc
+from paper_2003_02989_amd import tq
+from paper_2003_02989_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def test_c1_full():
+    w = wl.c1_hea()
+    say("c1 full")
+    compare(gpu_outputs(w), oracle_outputs(w))
+    w.upstream = np.random.default_rng(1).standard_normal(w.upstream.shape).astype(np.float32)
+    compare(gpu_outputs(w, want=("exp", "grad")), oracle_outputs(w, want=("exp", "grad")))
+
+
+def test_c2_full():
+    w = wl.c2_qnn()
+    say("c2 full")
+    compare(gpu_outputs(w, want=("exp", "grad")), oracle_outputs(w, want=("exp", "grad")))
+
+
+def test_c3_reduced():
+    w = wl.c3_qaoa(B=16, n=14)
+    say("c3 reduced n=14 B=16")
+    compare(gpu_outputs(w), oracle_outputs(w))
+
+
+def test_c3_full_sampled_rows():
+    w = wl.c3_qaoa()
+    say("c3 full n=20 B=256")
+    g = gpu_outputs(w, want=("exp", "grad"))
+    rows = [0, 97, 255]
+    ref = oracle_outputs(sub_workload(w, rows), want=("exp", "grad"))
+    gs = {"exp": g["exp"][rows], "grad": g["grad"][rows], "grad_exp": g["grad_exp"][rows]}
+    compare(gs, ref)
+    # invariants over every row: 0 <= <C> <= |E|
+    assert np.all(g["exp"] >= -TOL_EXP) and np.all(g["exp"] <= 30 + TOL_EXP)
+
+
+def test_c5_reduced():
+    w = wl.c5_vqe(B=24, n=12, layers=10, n_terms=200)
+    say("c5 reduced n=12 B=24")
+    compare(gpu_outputs(w), oracle_outputs(w))
+
+
+def test_c5_full_sampled_rows():
+    w = wl.c5_vqe()
+    say("c5 full n=16 B=4096")
+    g = gpu_outputs(w, want=("exp", "grad"))
+    rows = [0, 1234, 4095]
+    ref = oracle_outputs(sub_workload(w, rows), want=("exp", "grad"))
+    compare({"exp": g["exp"][rows], "grad": g["grad"][rows], "grad_exp": g["grad_exp"][rows]}, ref)
+
+
+def _c4_check(w, amps_ref, sum_p2, norm2_ref, n):
+    p = tq.Program(w.program_blob())
+    bits = dev(w.extras["bitstrings"].astype(np.int64), torch.int64)
+    a = tq.amplitudes(p, None, bits).cpu().numpy()[0]
+    err = np.linalg.norm(a.astype(np.complex128) - amps_ref)
+    say("c4 n", n, "amplitude L2 error", err)
+    assert err <= TOL_AMP
+    st = tq.simulate_state(p, None)
+    norm2 = float(torch.sum(torch.abs(st.view(torch.float32)) ** 2).double().item())
+    assert abs(norm2 - norm2_ref) < 1e-4
+    shots = w.extras["n_shots"]
+    smp = tq.sample(p, None, shots, w.extras["seed"])
+    # cross-entropy identity: mean over exact samples of 2^n p(x) is 2^n sum p^2
+    pr = (torch.abs(st[0]) ** 2).double()
+    xeb = float((pr[smp[0]] * 2.0 ** n).mean().item())
+    var = float(((pr[smp[0]] * 2.0 ** n) ** 2).mean().item()) - xeb ** 2
+    sigma = (var / shots) ** 0.5
+    say("c4 xeb", xeb, "expected", sum_p2 * 2.0 ** n, "sigma", sigma)
+    assert abs(xeb - sum_p2 * 2.0 ** n) < 4 * sigma
+    # the sampler is bit-exact on the device's own complex64 state
+    host_state = st.cpu().numpy()
+    ref = orc.sample_from_state(host_state, shots, w.extras["seed"])
+    assert np.array_equal(smp.cpu().numpy().astype(np.uint64), ref)
+    return st
+
+
+def test_c4_reduced():
+    w = wl.c4_random(rows=4, cols=5, n_shots=200_000)
+    say("c4 reduced n=20")
+    ref = orc.simulate_state(orc.Program(w.program_blob()), np.zeros((1, 0)))[0]
+    bits = w.extras["bitstrings"][0].astype(np.int64)
+    p2 = np.abs(ref) ** 2
+    st = _c4_check(w, ref[bits], float((p2 * p2).sum()), float(p2.sum()), 20)
+    err = np.linalg.norm(st.cpu().numpy()[0].astype(np.complex128) - ref)
+    assert err <= TOL_AMP
+
+
+def test_c4_full_against_golden():
+    path = os.path.join(GOLDEN, "c4_n30.npz")
+    g = np.load(path)
+    w = wl.c4_random()
+    assert np.array_equal(g["bitstrings"], w.extras["bitstrings"][0])
+    say("c4 full n=30")
+    _c4_check(w, g["amplitudes"], float(g["sum_p2"]), float(g["norm2"]), 30)
