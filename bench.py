@@ -23,8 +23,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "effective HBM GB/s per fused-gate pass; circuit-expectations/sec at batch"
-KERNELS = ("build", "pass", "expect", "expect_reduce", "apply_h", "rev_pass", "grad_reduce", "samp_l1",
-           "samp_shots", "gather")
+KERNELS = ("build", "resident", "pass", "expect", "expect_reduce", "apply_h", "rev_pass", "grad_reduce",
+           "samp_l1", "samp_shots", "gather")
 PEAK_HBM_GBS = 8000.0
 PEAK_FP32_TFLOPS = 157.3
 
@@ -56,17 +56,47 @@ def op_flops(op, n_local_ctrl):
         return 7.0 if (op["ctrl"] and n_local_ctrl) else 14.0
     if k == "M2":
         return 30.0
+    if k == "P2":
+        return 14.0
     return 6.0
 
 
-def kernel_work(plan, kernel, n_obs_terms, n_rows_total):
+def fwd_flops(g):
+    f = 0.0
+    for i, ps in enumerate(g["fwd"]):
+        f += 12.0 if ps["product_init"] else 0.0
+        for op in ps["ops"]:
+            f += op_flops(op, op["ctrl"] and op["l"][1] != 255)
+    return f
+
+
+def rev_flops(g):
+    f = 0.0
+    for ps in g["rev"]:
+        for op in ps["ops"]:
+            base = op_flops(op, op["ctrl"] and op["l"][1] != 255)
+            f += 2 * base + op["ngrad"] * (base + 4.0)
+    return f
+
+
+def kernel_work(plan, kernel, n_obs_terms, adjoint):
     """Algorithmic (flops, HBM bytes) of all launches of `kernel` in one step,
-    and the number of those launches, from the program's plan."""
+    and the number of those launches, from the program's plan.  Per amplitude:
+    a forward op costs its matvec (op_flops), a reverse op two matvecs (psi
+    and phi) plus one matvec and a 4-flop dot product per symbolic parameter,
+    an expectation term 4 flops, an H_g term 8 flops."""
     flops = bytes_ = 0.0
     launches = 0
     for g in plan["groups"]:
         amps = float(g["rows"]) * (1 << g["n"])
-        if kernel == "pass":
+        if kernel == "resident":
+            launches += 1
+            f = fwd_flops(g) + 4.0 * n_obs_terms
+            if adjoint:
+                f += 8.0 * n_obs_terms + rev_flops(g)
+            flops += f * amps
+            bytes_ += 0.0
+        elif kernel == "pass":
             for ps in g["fwd"]:
                 launches += 1
                 f = 12.0 if ps["product_init"] else 0.0
@@ -175,7 +205,7 @@ def main():
 
     plan = tq.describe(prog)
     n_terms = sum(len(t) for t in w.observables[0])
-    flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, B)
+    flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, args.config in ("c1", "c2", "c5"))
     avg_ms = dom_ms / max(n_launch, 1)
     if args.config in ("c1", "c2"):
         bound, unit, peak = "alu", "TFLOP/s", PEAK_FP32_TFLOPS

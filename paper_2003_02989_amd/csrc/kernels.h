@@ -38,6 +38,7 @@ struct PassArgs {
     int wg_per_row;
     int product_init;
     int32_t init_mat[kMaxQubits];
+    int mat_begin, mat_end;  // the pass's matrices, staged in LDS
 };
 
 struct ExpArgs {
@@ -88,6 +89,37 @@ struct RevArgs {
     int store;
     double *gpart;  // [nrows][wg_per_row][n_gslots]
     int n_gslots, gbase, gcount;
+    int mat_begin, mat_end;
+};
+
+struct ResArgs {
+    const double2 *mats;  // row blocks built by k_build_mats
+    int64_t mat_stride;
+    const double *slot_scale;
+    int uniform, n_slots;
+    int S;
+    const int32_t *rows;  // batch index of each row
+    int mat_block;        // LDS matrix entries
+    int n;
+    const PassOp *fops;
+    int nfops;
+    int32_t init_mat[kMaxQubits];
+    // optional state output
+    float2 *state_out;
+    int64_t out_stride;
+    const int32_t *out_rows;
+    // optional expectations
+    const TermDev *terms;
+    const int32_t *row_term_begin, *row_term_count;
+    int K;
+    float *exp_out;
+    int nacc, gacc;  // accumulators: [0, gacc) terms, [gacc, gacc + n_gslots) gradients
+    // optional adjoint
+    const PassOp *rops;
+    int nrops;
+    const float *upstream;
+    const int32_t *sym_begin, *sym_gslots, *gslot_slot;
+    float *grad;
 };
 
 struct GradReduceArgs {
@@ -129,7 +161,9 @@ struct GatherArgs {
 
 void profile_start(const char *kernel);
 hipError_t profile_read(int64_t *launches, double *total_ms);
-size_t pass_lds_bytes(const TileGeom &g, bool product_init);
+size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat);
+size_t resident_lds_bytes(int n, int nmat, int nacc, bool adjoint);
+hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
 hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s);

@@ -75,7 +75,7 @@ __device__ __forceinline__ cd cdadd(cd a, cd b) { return cd{a.x + b.x, a.y + b.y
 __device__ __forceinline__ cd cdscale(cd a, double s) { return cd{a.x * s, a.y * s}; }
 
 // m: row-major d x d, zero-initialised by the caller
-__device__ int gate_matrix_dev(int op, const double *eta, const double *ex, int form, cd *m)
+__device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const double *ex, int form, cd *m)
 {
     const double r = 0.70710678118654752440;
     double c, s;
@@ -151,7 +151,7 @@ __device__ int gate_matrix_dev(int op, const double *eta, const double *ex, int 
 }
 
 // derivative with respect to parameter `which` (m zero-initialised)
-__device__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd *m)
+__device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd *m)
 {
     double c, s;
     const double pi = 3.14159265358979323846;
@@ -202,18 +202,101 @@ __device__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd
 }
 
 // permutation of a 4x4 two-qubit matrix for reversed qubit order (|ab> -> |ba>)
-__device__ void swap_qubits4(cd *m)
+__device__ __forceinline__ void swap_qubits4(cd *m)
 {
-    const int pm[4] = {0, 2, 1, 3};
     cd t[16];
+#pragma unroll
     for (int i = 0; i < 4; i++)
-        for (int j = 0; j < 4; j++) t[pm[i] * 4 + pm[j]] = m[i * 4 + j];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int pi = (i == 1) ? 2 : (i == 2) ? 1 : i, pj = (j == 1) ? 2 : (j == 2) ? 1 : j;
+            t[pi * 4 + pj] = m[i * 4 + j];
+        }
+#pragma unroll
     for (int i = 0; i < 16; i++) m[i] = t[i];
 }
 
+// Where the builder finds one batch row's parameters.
+struct BuildCtx {
+    const Member *members;
+    const GateDev *gates;
+    const int32_t *slot_sym;
+    const double *scale, *off;  // this row's scale and offset per slot
+    const double *explicit_mats;
+    const float *theta;         // this row's symbol values
+};
+
+// One build task for one row: symbol resolution eta = scale*theta + offset
+// and the fused product / dagger / derivative, all in float64.  D is the
+// matrix dimension; fixed at compile time so every array stays in registers.
+template <int D> __device__ __forceinline__ void build_task_d(const BuildTask &bt, const BuildCtx &c, double2 *out)
+{
+    cd acc[16], g[16];
+#pragma unroll
+    for (int i = 0; i < 16; i++) acc[i] = C(0, 0);
+#pragma unroll
+    for (int i = 0; i < D; i++) acc[i * D + i] = C(1, 0);
+    for (int mi = 0; mi < bt.mem_count; mi++) {
+        const Member mem = c.members[bt.mem_begin + mi];
+        const GateDev gd = c.gates[mem.gate];
+        double eta[2] = {0, 0};
+        for (int j = 0; j < gd.np; j++) {
+            const int slot = gd.slot0 + j;
+            const int sy = c.slot_sym[slot];
+            eta[j] = sy >= 0 ? c.scale[slot] * (double)c.theta[sy] + c.off[slot] : c.off[slot];
+        }
+        const double *ex = gd.explicit_ >= 0 ? c.explicit_mats + 32 * gd.explicit_ : nullptr;
+#pragma unroll
+        for (int i = 0; i < 16; i++) g[i] = C(0, 0);
+        const int gdim = bt.kind == BT_DERIV ? gate_deriv_dev(gd.op, eta, bt.which, mem.form, g)
+                                             : gate_matrix_dev(gd.op, eta, ex, mem.form, g);
+        if (gdim != D) continue;  // the planner never mixes dimensions
+        if (D == 4 && mem.swapped) swap_qubits4(g);
+        if (bt.kind == BT_DAGGER) {
+#pragma unroll
+            for (int i = 0; i < D; i++)
+#pragma unroll
+                for (int j = 0; j < D; j++) acc[i * D + j] = C(g[j * D + i].x, -g[j * D + i].y);
+        } else if (bt.kind == BT_DERIV) {
+#pragma unroll
+            for (int i = 0; i < D * D; i++) acc[i] = g[i];
+        } else {
+            cd t[16];
+#pragma unroll
+            for (int i = 0; i < D; i++)
+#pragma unroll
+                for (int j = 0; j < D; j++) {
+                    cd sacc = C(0, 0);
+#pragma unroll
+                    for (int k = 0; k < D; k++) sacc = cdadd(sacc, cdmul(g[i * D + k], acc[k * D + j]));
+                    t[i * D + j] = sacc;
+                }
+#pragma unroll
+            for (int i = 0; i < D * D; i++) acc[i] = t[i];
+        }
+    }
+    if (bt.diag >= 2) {
+        // a I + b P: a from entry (0,0), b from entry (0,3) (P_03 = 1 for XX, -1 for YY)
+        const double sg = bt.diag == 3 ? -1.0 : 1.0;
+        out[0] = make_double2(acc[0].x, acc[0].y);
+        out[1] = make_double2(sg * acc[D - 1].x, sg * acc[D - 1].y);
+    } else if (bt.diag) {
+#pragma unroll
+        for (int i = 0; i < D; i++) out[i] = make_double2(acc[i * D + i].x, acc[i * D + i].y);
+    } else {
+#pragma unroll
+        for (int i = 0; i < D * D; i++) out[i] = make_double2(acc[i].x, acc[i].y);
+    }
+}
+
+__device__ __forceinline__ void build_task(const BuildTask &bt, const BuildCtx &c, double2 *out)
+{
+    if (bt.dim == 2) build_task_d<2>(bt, c, out);
+    else build_task_d<4>(bt, c, out);
+}
+
 // --------------------------------------------------- matrix build kernel
-// One thread per (row, task): symbol resolution eta = scale*theta + offset
-// and the fused product / dagger / derivative in float64, stored complex64.
+// One thread per (row, task); the result goes to the row's matrix block.
 __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
 {
     const int row = blockIdx.y;
@@ -221,70 +304,30 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     if (ti >= a.task_end) return;
     const BuildTask bt = a.tasks[ti];
     const int b = a.rows[row];
-    const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots);
-    const double *off = a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots);
-    const float *theta = a.theta + (int64_t)b * a.S;
-    const int d = bt.dim;
-    cd acc[16], g[16];
-    for (int i = 0; i < 16; i++) acc[i] = C(0, 0);
-    for (int i = 0; i < d; i++) acc[i * d + i] = C(1, 0);
-    for (int mi = 0; mi < bt.mem_count; mi++) {
-        const Member mem = a.members[bt.mem_begin + mi];
-        const GateDev gd = a.gates[mem.gate];
-        double eta[2] = {0, 0};
-        for (int j = 0; j < gd.np; j++) {
-            int slot = gd.slot0 + j;
-            int sy = a.slot_sym[slot];
-            eta[j] = sy >= 0 ? scale[slot] * (double)theta[sy] + off[slot] : off[slot];
-        }
-        const double *ex = gd.explicit_ >= 0 ? a.explicit_mats + 32 * gd.explicit_ : nullptr;
-        for (int i = 0; i < 16; i++) g[i] = C(0, 0);
-        int gdim;
-        if (bt.kind == BT_DERIV) gdim = gate_deriv_dev(gd.op, eta, bt.which, mem.form, g);
-        else gdim = gate_matrix_dev(gd.op, eta, ex, mem.form, g);
-        if (gdim != d) continue;  // the planner never mixes dimensions
-        if (mem.swapped) swap_qubits4(g);
-        if (bt.kind == BT_DAGGER) {
-            for (int i = 0; i < d; i++)
-                for (int j = 0; j < d; j++) acc[i * d + j] = C(g[j * d + i].x, -g[j * d + i].y);
-        } else if (bt.kind == BT_DERIV) {
-            for (int i = 0; i < d * d; i++) acc[i] = g[i];
-        } else {
-            cd t[16];
-            for (int i = 0; i < d; i++)
-                for (int j = 0; j < d; j++) {
-                    cd sacc = C(0, 0);
-                    for (int k = 0; k < d; k++) sacc = cdadd(sacc, cdmul(g[i * d + k], acc[k * d + j]));
-                    t[i * d + j] = sacc;
-                }
-            for (int i = 0; i < d * d; i++) acc[i] = t[i];
-        }
-    }
-    double2 *out = a.mats + (int64_t)row * a.mat_stride + bt.out;
-    if (bt.diag) {
-        for (int i = 0; i < d; i++) out[i] = make_double2(acc[i * d + i].x, acc[i * d + i].y);
-    } else {
-        for (int i = 0; i < d * d; i++) out[i] = make_double2(acc[i].x, acc[i].y);
-    }
+    BuildCtx c{a.members, a.gates, a.slot_sym,
+               a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots),
+               a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots), a.explicit_mats,
+               a.theta + (int64_t)b * a.S};
+    build_task(bt, c, a.mats + (int64_t)row * a.mat_stride + bt.out);
 }
 
 // ------------------------------------------------------------ tile access
 struct TileCtx {
-    const TileGeom *g;
     const uint64_t *hi_off;  // LDS table: global offset of each high-bit combination
     uint32_t lowmask;
+    int c;                   // contiguous low bits
 };
 
 __device__ __forceinline__ uint64_t tile_index(const TileCtx &tc, uint64_t fb, uint32_t l)
 {
-    return fb | (l & tc.lowmask) | tc.hi_off[l >> tc.g->c];
+    return fb | (l & tc.lowmask) | tc.hi_off[l >> tc.c];
 }
 
 // copy a tile between HBM and LDS; two amplitudes per float4 when c >= 1
 template <bool kLoad>
 __device__ __forceinline__ void tile_copy(const TileCtx &tc, float2 *lds, float2 *row, uint64_t fb, int T)
 {
-    if (tc.g->c >= 1) {
+    if (tc.c >= 1) {
         for (int l = 2 * threadIdx.x; l < T; l += 2 * blockDim.x) {
             float4 *p = reinterpret_cast<float4 *>(row + tile_index(tc, fb, l));
             if (kLoad) {
@@ -319,7 +362,34 @@ __device__ __forceinline__ int bit_of(uint8_t loc, uint8_t pos, uint32_t l, uint
 }
 
 // ------------------------------------------------------ forward tile ops
-__device__ void apply_op(const PassOp &op, const double2 *__restrict__ m, float2 *lds, int t, uint64_t fb)
+// Diagonal entry index of local element l: 2*bit(q0) + bit(q1) for K_D2,
+// bit(q0) for K_D1, each bit taken from the tile index or the fixed bits.
+__device__ __forceinline__ int diag_index(const PassOp &op, uint32_t l, uint64_t fb)
+{
+    int idx = bit_of(op.l0, op.p0, l, fb);
+    if (op.kind == K_D2) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
+    return idx;
+}
+
+// (a I + b P) on the quad (v00, v01, v10, v11); P = XX (sg = 1) or YY
+// (sg = -1): P couples 00 with 11 (sign sg) and 01 with 10 (sign +1)
+struct Quad {
+    double2 v00, v01, v10, v11;
+};
+__device__ __forceinline__ Quad p2_apply(double2 a, double2 b, double sg, const Quad &v)
+{
+    const double2 bs = make_double2(sg * b.x, sg * b.y);
+    Quad o;
+    o.v00 = zadd(zmul(a, v.v00), zmul(bs, v.v11));
+    o.v11 = zadd(zmul(a, v.v11), zmul(bs, v.v00));
+    o.v01 = zadd(zmul(a, v.v01), zmul(b, v.v10));
+    o.v10 = zadd(zmul(a, v.v10), zmul(b, v.v01));
+    return o;
+}
+
+// Apply one op to a tile of 2^t amplitudes in LDS.  `m` is the op's matrix
+// (row major; diagonal ops keep their diagonal only), in LDS or global memory.
+__device__ void apply_op(const PassOp &op, const double2 *m, float2 *lds, int t, uint64_t fb)
 {
     const uint32_t T = 1u << t;
     const int tid = threadIdx.x, nt = blockDim.x;
@@ -346,8 +416,7 @@ __device__ void apply_op(const PassOp &op, const double2 *__restrict__ m, float2
             lds[j] = down2(zmul2(m10, a0, m11, a1));
         }
     } else if (op.kind == K_M2) {
-        double2 mm[16];
-        for (int i = 0; i < 16; i++) mm[i] = m[i];
+        const double2 *mm = m;
         const int b0 = op.l0, b1 = op.l1;
         const int lo = min(b0, b1), hi = max(b0, b1);
         for (uint32_t p = tid; p < T / 4; p += nt) {
@@ -359,16 +428,145 @@ __device__ void apply_op(const PassOp &op, const double2 *__restrict__ m, float2
             lds[i10] = down2(zadd(zmul2(mm[8], v0, mm[9], v1), zmul2(mm[10], v2, mm[11], v3)));
             lds[i11] = down2(zadd(zmul2(mm[12], v0, mm[13], v1), zmul2(mm[14], v2, mm[15], v3)));
         }
-    } else {  // diagonal K_D1 / K_D2
-        const bool two = op.kind == K_D2;
-        double2 d[4];
-        for (int i = 0; i < (two ? 4 : 2); i++) d[i] = m[i];
+    } else if (op.kind == K_P2) {
+        const double2 ca = m[0], cb = m[1];
+        const double sg = op.ptype == 2 ? -1.0 : 1.0;
+        const int b0 = op.l0, b1 = op.l1;
+        const int lo = min(b0, b1), hi = max(b0, b1);
+        for (uint32_t p = tid; p < T / 4; p += nt) {
+            uint32_t i00 = ins0(ins0(p, lo), hi);
+            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
+            Quad v{up2(lds[i00]), up2(lds[i01]), up2(lds[i10]), up2(lds[i11])};
+            Quad o = p2_apply(ca, cb, sg, v);
+            lds[i00] = down2(o.v00);
+            lds[i01] = down2(o.v01);
+            lds[i10] = down2(o.v10);
+            lds[i11] = down2(o.v11);
+        }
+    } else {  // diagonal
+        for (uint32_t l = tid; l < T; l += nt) lds[l] = down2(zmul(m[diag_index(op, l, fb)], up2(lds[l])));
+    }
+}
+
+// One reversed gate W on the psi and phi tiles: psi <- W^dagger psi, then
+// g_j += Re <phi| dW/deta_j |psi> over this thread's elements, then
+// phi <- W^dagger phi.  M is the row's matrix block (op offsets index it).
+__device__ void rev_op(const PassOp &op, const double2 *M, int base, float2 *lp, float2 *lf, int t,
+                       uint64_t fb, double &g0, double &g1)
+{
+    const uint32_t T = 1u << t;
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const double2 *m = M + (op.mat - base);
+    const double2 *d0 = M + (op.ngrad > 0 ? op.dmat[0] - base : 0);
+    const double2 *d1 = M + (op.ngrad > 1 ? op.dmat[1] - base : 0);
+    if (op.kind == K_M1) {
+        const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+        const int tb = op.l0;
+        uint32_t count = T / 2;
+        int lo = tb, hi = tb, cb = -1;
+        uint32_t cv = 0;
+        if (op.ctrl) {
+            if (op.l1 == kFixed) {
+                if ((int)((fb >> op.p1) & 1) != op.cval) return;
+            } else {
+                cb = op.l1;
+                lo = min(tb, cb);
+                hi = max(tb, cb);
+                cv = (uint32_t)op.cval << cb;
+                count = T / 4;
+            }
+        }
+        for (uint32_t p = tid; p < count; p += nt) {
+            uint32_t i = cb >= 0 ? (ins0(ins0(p, lo), hi) | cv) : ins0(p, tb);
+            uint32_t j = i | (1u << tb);
+            double2 a0 = up2(lp[i]), a1 = up2(lp[j]);
+            double2 b0 = zmul2(m00, a0, m01, a1), b1 = zmul2(m10, a0, m11, a1);
+            lp[i] = down2(b0);
+            lp[j] = down2(b1);
+            double2 f0 = up2(lf[i]), f1 = up2(lf[j]);
+            if (op.ngrad > 0) g0 += zdotr(f0, zmul2(d0[0], b0, d0[1], b1)) + zdotr(f1, zmul2(d0[2], b0, d0[3], b1));
+            if (op.ngrad > 1) g1 += zdotr(f0, zmul2(d1[0], b0, d1[1], b1)) + zdotr(f1, zmul2(d1[2], b0, d1[3], b1));
+            lf[i] = down2(zmul2(m00, f0, m01, f1));
+            lf[j] = down2(zmul2(m10, f0, m11, f1));
+        }
+    } else if (op.kind == K_M2) {
+        const double2 *mm = m;
+        const int b0 = op.l0, b1 = op.l1;
+        const int lo = min(b0, b1), hi = max(b0, b1);
+        for (uint32_t p = tid; p < T / 4; p += nt) {
+            uint32_t ix[4];
+            ix[0] = ins0(ins0(p, lo), hi);
+            ix[1] = ix[0] | (1u << b1);
+            ix[2] = ix[0] | (1u << b0);
+            ix[3] = ix[1] | (1u << b0);
+            double2 u[4], f[4];
+            {
+                const double2 v0 = up2(lp[ix[0]]), v1 = up2(lp[ix[1]]), v2 = up2(lp[ix[2]]), v3 = up2(lp[ix[3]]);
+#pragma unroll
+                for (int r = 0; r < 4; r++)
+                    u[r] = zadd(zmul2(mm[4 * r], v0, mm[4 * r + 1], v1), zmul2(mm[4 * r + 2], v2, mm[4 * r + 3], v3));
+            }
+#pragma unroll
+            for (int r = 0; r < 4; r++) lp[ix[r]] = down2(u[r]);
+#pragma unroll
+            for (int r = 0; r < 4; r++) f[r] = up2(lf[ix[r]]);
+            for (int gq = 0; gq < op.ngrad; gq++) {
+                const double2 *dm = gq == 0 ? d0 : d1;
+                double sacc = 0;
+#pragma unroll
+                for (int r = 0; r < 4; r++)
+                    sacc += zdotr(f[r], zadd(zmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
+                                             zmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3])));
+                if (gq == 0) g0 += sacc;
+                else g1 += sacc;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; r++)
+                lf[ix[r]] = down2(zadd(zmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]), zmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3])));
+        }
+    } else if (op.kind == K_P2) {
+        const double2 ca = m[0], cb = m[1];
+        const double sg = op.ptype == 2 ? -1.0 : 1.0;
+        const int b0 = op.l0, b1 = op.l1;
+        const int lo = min(b0, b1), hi = max(b0, b1);
+        for (uint32_t p = tid; p < T / 4; p += nt) {
+            uint32_t i00 = ins0(ins0(p, lo), hi);
+            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
+            Quad v{up2(lp[i00]), up2(lp[i01]), up2(lp[i10]), up2(lp[i11])};
+            Quad u = p2_apply(ca, cb, sg, v);
+            lp[i00] = down2(u.v00);
+            lp[i01] = down2(u.v01);
+            lp[i10] = down2(u.v10);
+            lp[i11] = down2(u.v11);
+            Quad f{up2(lf[i00]), up2(lf[i01]), up2(lf[i10]), up2(lf[i11])};
+            if (op.ngrad > 0) {
+                Quad e = p2_apply(d0[0], d0[1], sg, u);
+                g0 += zdotr(f.v00, e.v00) + zdotr(f.v01, e.v01) + zdotr(f.v10, e.v10) + zdotr(f.v11, e.v11);
+            }
+            Quad o = p2_apply(ca, cb, sg, f);
+            lf[i00] = down2(o.v00);
+            lf[i01] = down2(o.v01);
+            lf[i10] = down2(o.v10);
+            lf[i11] = down2(o.v11);
+        }
+    } else {
         for (uint32_t l = tid; l < T; l += nt) {
-            int idx = bit_of(op.l0, op.p0, l, fb);
-            if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
-            lds[l] = down2(zmul(d[idx], up2(lds[l])));
+            const int idx = diag_index(op, l, fb);
+            const double2 dg = m[idx];
+            double2 u = zmul(dg, up2(lp[l]));
+            lp[l] = down2(u);
+            double2 f = up2(lf[l]);
+            if (op.ngrad > 0) g0 += zdotr(f, zmul(d0[idx], u));
+            if (op.ngrad > 1) g1 += zdotr(f, zmul(d1[idx], u));
+            lf[l] = down2(zmul(dg, f));
         }
     }
+}
+
+// Stage the matrices [begin, end) of a row block into LDS.
+__device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_block, int begin, int end)
+{
+    for (int i = begin + (int)threadIdx.x; i < end; i += blockDim.x) dst[i - begin] = row_block[i];
 }
 
 // ------------------------------------------------------- forward pass
@@ -380,16 +578,19 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
     const int T = 1 << t;
     float2 *lds = reinterpret_cast<float2 *>(smem);
     uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
-    double2 *p1 = reinterpret_cast<double2 *>(hi_off + (1 << g.h));
+    double2 *lm = reinterpret_cast<double2 *>(hi_off + (1 << g.h));  // the pass's matrices
+    double2 *p1 = lm + (a.mat_end - a.mat_begin);
     const int a1 = t / 2;
     double2 *p2 = p1 + (1 << a1);
 
     const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
     const int b = a.rows[row];
     float2 *st = a.state + (int64_t)b * a.row_stride;
-    const double2 *M = a.mats + (int64_t)row * a.mat_stride;
     build_hi_off(g, hi_off);
-    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, a.mat_begin, a.mat_end);
+    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
+    __syncthreads();
+    const double2 *M = lm;  // offsets below are taken relative to mat_begin
 
     if (a.product_init) {
         // per-qubit product-state vectors: column 0 of each init matrix
@@ -401,7 +602,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
             for (int k = k0; k < k1; k++) {
                 int pos = k < g.c ? k : g.hb[k - g.c];
                 int q = g.n - 1 - pos;
-                const double2 *im = M + a.init_mat[q];
+                const double2 *im = M + (a.init_mat[q] - a.mat_begin);
                 acc = zmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
             }
             if (first) p1[v] = acc;
@@ -417,7 +618,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
             double2 f = make_double2(1.0, 0.0);
             for (uint64_t fm = g.fixed_mask; fm; fm &= fm - 1) {
                 int pos = __ffsll((unsigned long long)fm) - 1;
-                const double2 *im = M + a.init_mat[g.n - 1 - pos];
+                const double2 *im = M + (a.init_mat[g.n - 1 - pos] - a.mat_begin);
                 f = zmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
             }
             for (int l = threadIdx.x; l < T; l += blockDim.x)
@@ -428,7 +629,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
         __syncthreads();
         for (int oi = 0; oi < a.nops; oi++) {
             const PassOp op = a.ops[oi];
-            apply_op(op, M + op.mat, lds, t, fb);
+            apply_op(op, M + (op.mat - a.mat_begin), lds, t, fb);
             __syncthreads();
         }
         tile_copy<false>(tc, lds, st, fb, T);
@@ -509,7 +710,7 @@ __global__ __launch_bounds__(256) void k_expect(ExpArgs a)
     const TermDev *terms = a.terms + a.row_term_begin[row];
     const int nterm = a.row_term_count[row];
     build_hi_off(g, hi_off);
-    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
     const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
 
     for (int c0 = 0; c0 < nterm; c0 += kTermChunk) {
@@ -556,7 +757,29 @@ __global__ void k_expect_reduce(ExpReduceArgs a)
 
 // --------------------------------------------------- phi = H_g psi
 // (P psi)[i] = i^{ny} (-1)^{|(i ^ x) & z|} psi[i ^ x]; the coefficient of term
-// t of observable k is upstream[b, k] * coeff_t.
+// t of observable k is upstream[b, k] * coeff_t.  One output element.
+__device__ __forceinline__ float2 h_elem(uint32_t l, uint64_t fb, const TermDev *terms, int nterm, const float *up,
+                                         const float2 *lds, const TileCtx &tc, const float2 *ps)
+{
+    double ax = 0, ay = 0;
+    for (int k = 0; k < nterm; k++) {
+        const TermDev tm = terms[k];
+        const uint32_t lj = l ^ tm.xl;
+        const uint64_t fj = fb ^ tm.xout;
+        float2 v = tm.xout == 0 ? lds[lj] : ps[tile_index(tc, fj, lj)];
+        double cf = tm.coeff * (double)up[tm.k];
+        if (par64(fj & tm.z) ^ par32(lj & tm.zl)) cf = -cf;
+        double vx = v.x, vy = v.y;
+        switch (tm.ny & 3) {
+        case 0: ax += cf * vx; ay += cf * vy; break;
+        case 1: ax -= cf * vy; ay += cf * vx; break;
+        case 2: ax -= cf * vx; ay -= cf * vy; break;
+        default: ax += cf * vy; ay -= cf * vx; break;
+        }
+    }
+    return make_float2((float)ax, (float)ay);
+}
+
 __global__ __launch_bounds__(256) void k_apply_h(HArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -573,40 +796,21 @@ __global__ __launch_bounds__(256) void k_apply_h(HArgs a)
     const int nterm = a.row_term_count[row];
     const float *up = a.upstream + (int64_t)a.brows[row] * a.K;
     build_hi_off(g, hi_off);
-    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
     __syncthreads();  // hi_off is read by every thread below
     const int64_t ntiles = (int64_t)1 << a.tiles_log2;
     for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
         const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
         tile_copy<true>(tc, lds, const_cast<float2 *>(ps), fb, T);
         __syncthreads();
-        for (int l = threadIdx.x; l < T; l += blockDim.x) {
-            double ax = 0, ay = 0;
-            for (int k = 0; k < nterm; k++) {
-                const TermDev tm = terms[k];
-                const uint32_t lj = l ^ tm.xl;
-                const uint64_t fj = fb ^ tm.xout;
-                float2 v = tm.xout == 0 ? lds[lj] : ps[tile_index(tc, fj, lj)];
-                double cf = tm.coeff * (double)up[tm.k];
-                if (par64(fj & tm.z) ^ par32(lj & tm.zl)) cf = -cf;
-                double vx = v.x, vy = v.y;
-                switch (tm.ny & 3) {
-                case 0: ax += cf * vx; ay += cf * vy; break;
-                case 1: ax -= cf * vy; ay += cf * vx; break;
-                case 2: ax -= cf * vx; ay -= cf * vy; break;
-                default: ax += cf * vy; ay -= cf * vx; break;
-                }
-            }
-            ph[tile_index(tc, fb, l)] = make_float2((float)ax, (float)ay);
-        }
+        for (int l = threadIdx.x; l < T; l += blockDim.x)
+            ph[tile_index(tc, fb, l)] = h_elem(l, fb, terms, nterm, up, lds, tc, ps);
         __syncthreads();
     }
 }
 
 // ------------------------------------------------------ reverse pass
-// psi and phi tiles side by side in LDS.  For each op (a reversed gate W):
-// psi <- W^dagger psi; for every symbolic parameter accumulate
-// Re <phi| dW/deta |psi>; phi <- W^dagger phi.
+// psi and phi tiles side by side in LDS; the pass's matrices too.
 __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -616,16 +820,17 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
     float2 *lp = reinterpret_cast<float2 *>(smem);
     float2 *lf = lp + T;
     uint64_t *hi_off = reinterpret_cast<uint64_t *>(lf + T);
-    double *acc = reinterpret_cast<double *>(hi_off + (1 << g.h));  // [4][gcount]
+    double2 *lm = reinterpret_cast<double2 *>(hi_off + (1 << g.h));
+    double *acc = reinterpret_cast<double *>(lm + (a.mat_end - a.mat_begin));  // [4][gcount]
 
     const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
     const int b = a.rows[row];
     float2 *sp = a.psi + (int64_t)b * a.row_stride;
     float2 *sf = a.phi + (int64_t)b * a.row_stride;
-    const double2 *M = a.mats + (int64_t)row * a.mat_stride;
     build_hi_off(g, hi_off);
+    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, a.mat_begin, a.mat_end);
     for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) acc[j] = 0;
-    TileCtx tc{&g, hi_off, (1u << g.c) - 1};
+    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
     const int tid = threadIdx.x, nt = blockDim.x;
     const int wave = tid / 64, lane = tid % 64;
     __syncthreads();
@@ -638,98 +843,8 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         __syncthreads();
         for (int oi = 0; oi < a.nops; oi++) {
             const PassOp op = a.ops[oi];
-            const double2 *m = M + op.mat;
             double g0 = 0, g1 = 0;
-            if (op.kind == K_M1) {
-                const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
-                double2 d0[4], d1[4];
-                for (int i = 0; i < 4; i++) {
-                    d0[i] = op.ngrad > 0 ? M[op.dmat[0] + i] : make_double2(0, 0);
-                    d1[i] = op.ngrad > 1 ? M[op.dmat[1] + i] : make_double2(0, 0);
-                }
-                const int tb = op.l0;
-                bool active = true;
-                uint32_t count = T / 2;
-                int lo = tb, hi = tb, cb = -1;
-                uint32_t cv = 0;
-                if (op.ctrl) {
-                    if (op.l1 == kFixed) {
-                        active = (int)((fb >> op.p1) & 1) == op.cval;
-                    } else {
-                        cb = op.l1;
-                        lo = min(tb, cb);
-                        hi = max(tb, cb);
-                        cv = (uint32_t)op.cval << cb;
-                        count = T / 4;
-                    }
-                }
-                if (active) {
-                    for (uint32_t p = tid; p < count; p += nt) {
-                        uint32_t i = cb >= 0 ? (ins0(ins0(p, lo), hi) | cv) : ins0(p, tb);
-                        uint32_t j = i | (1u << tb);
-                        double2 a0 = up2(lp[i]), a1 = up2(lp[j]);
-                        double2 b0 = zmul2(m00, a0, m01, a1), b1 = zmul2(m10, a0, m11, a1);
-                        lp[i] = down2(b0);
-                        lp[j] = down2(b1);
-                        double2 f0 = up2(lf[i]), f1 = up2(lf[j]);
-                        if (op.ngrad > 0)
-                            g0 += zdotr(f0, zmul2(d0[0], b0, d0[1], b1)) + zdotr(f1, zmul2(d0[2], b0, d0[3], b1));
-                        if (op.ngrad > 1)
-                            g1 += zdotr(f0, zmul2(d1[0], b0, d1[1], b1)) + zdotr(f1, zmul2(d1[2], b0, d1[3], b1));
-                        lf[i] = down2(zmul2(m00, f0, m01, f1));
-                        lf[j] = down2(zmul2(m10, f0, m11, f1));
-                    }
-                }
-            } else if (op.kind == K_M2) {
-                double2 mm[16];
-                for (int i = 0; i < 16; i++) mm[i] = m[i];
-                const int b0 = op.l0, b1 = op.l1;
-                const int lo = min(b0, b1), hi = max(b0, b1);
-                for (uint32_t p = tid; p < T / 4; p += nt) {
-                    uint32_t ix[4];
-                    ix[0] = ins0(ins0(p, lo), hi);
-                    ix[1] = ix[0] | (1u << b1);
-                    ix[2] = ix[0] | (1u << b0);
-                    ix[3] = ix[1] | (1u << b0);
-                    double2 v[4], u[4], f[4];
-                    for (int r = 0; r < 4; r++) v[r] = up2(lp[ix[r]]);
-                    for (int r = 0; r < 4; r++)
-                        u[r] = zadd(zmul2(mm[4 * r], v[0], mm[4 * r + 1], v[1]), zmul2(mm[4 * r + 2], v[2], mm[4 * r + 3], v[3]));
-                    for (int r = 0; r < 4; r++) lp[ix[r]] = down2(u[r]);
-                    for (int r = 0; r < 4; r++) f[r] = up2(lf[ix[r]]);
-                    for (int gq = 0; gq < op.ngrad; gq++) {
-                        const double2 *dm = M + op.dmat[gq];
-                        double sacc = 0;
-                        for (int r = 0; r < 4; r++)
-                            sacc += zdotr(f[r], zadd(zmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
-                                                     zmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3])));
-                        if (gq == 0) g0 += sacc;
-                        else g1 += sacc;
-                    }
-                    for (int r = 0; r < 4; r++)
-                        lf[ix[r]] = down2(zadd(zmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]),
-                                               zmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3])));
-                }
-            } else {
-                const bool two = op.kind == K_D2;
-                double2 d[4], dd0[4], dd1[4];
-                for (int i = 0; i < 4; i++) {
-                    const bool in = i < (two ? 4 : 2);
-                    d[i] = in ? m[i] : make_double2(0, 0);
-                    dd0[i] = in && op.ngrad > 0 ? M[op.dmat[0] + i] : make_double2(0, 0);
-                    dd1[i] = in && op.ngrad > 1 ? M[op.dmat[1] + i] : make_double2(0, 0);
-                }
-                for (uint32_t l = tid; l < T; l += nt) {
-                    int idx = bit_of(op.l0, op.p0, l, fb);
-                    if (two) idx = 2 * idx + bit_of(op.l1, op.p1, l, fb);
-                    double2 u = zmul(d[idx], up2(lp[l]));
-                    lp[l] = down2(u);
-                    double2 f = up2(lf[l]);
-                    if (op.ngrad > 0) g0 += zdotr(f, zmul(dd0[idx], u));
-                    if (op.ngrad > 1) g1 += zdotr(f, zmul(dd1[idx], u));
-                    lf[l] = down2(zmul(d[idx], f));
-                }
-            }
+            rev_op(op, lm, a.mat_begin, lp, lf, t, fb, g0, g1);
             if (op.ngrad > 0) {
                 double v = wave_sum(g0);
                 if (lane == 0) acc[wave * a.gcount + (op.gslot[0] - a.gbase)] += v;
@@ -767,6 +882,100 @@ __global__ void k_grad_reduce(GradReduceArgs a)
             sum += 2.0 * scale[a.gslot_slot[gs]] * v;
         }
         a.grad[(int64_t)b * a.S + s] = (float)sum;
+    }
+}
+
+// ---------------------------------------------------- resident circuits
+// Small circuits (psi, phi and every matrix of the row fit in LDS): one
+// workgroup per batch row does the whole call -- matrix build, product-state
+// init, forward gates, expectations, H_g, reverse sweep, gradient reduction --
+// in one launch.  Outputs are reduced in a fixed order inside the workgroup.
+__global__ __launch_bounds__(256) void k_resident(ResArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int n = a.n;
+    const uint32_t T = 1u << n;
+    const int row = blockIdx.x;
+    const int b = a.rows[row];
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int wave = tid / 64, lane = tid % 64;
+    double2 *lm = reinterpret_cast<double2 *>(smem);                      // [mat_block]
+    double *acc = reinterpret_cast<double *>(lm + a.mat_block);           // [4][nacc]
+    float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);            // [T]
+    float2 *lf = lp + T;                                                  // [T] (adjoint)
+    // whole-state tile: every term's partner is local, so the tile index
+    // table and the HBM partner pointer are never used (valid LDS addresses
+    // are passed instead of null pointers)
+    TileCtx tc{reinterpret_cast<const uint64_t *>(acc), T - 1, n};
+
+    // 1. the row's fused matrices (built by k_build_mats) into LDS
+    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, 0, a.mat_block);
+    for (int j = tid; j < 4 * a.nacc; j += nt) acc[j] = 0;
+    __syncthreads();
+    // 2. product-state initialisation
+    for (uint32_t l = tid; l < T; l += nt) {
+        double2 v = make_double2(1.0, 0.0);
+        for (int q = 0; q < n; q++) v = zmul(v, lm[a.init_mat[q] + (((l >> (n - 1 - q)) & 1) ? 2 : 0)]);
+        lp[l] = down2(v);
+    }
+    __syncthreads();
+    // 3. forward gates
+    for (int oi = 0; oi < a.nfops; oi++) {
+        const PassOp op = a.fops[oi];
+        apply_op(op, lm + op.mat, lp, n, 0);
+        __syncthreads();
+    }
+    // 4. state output and expectation terms
+    if (a.state_out) {
+        float2 *out = a.state_out + (int64_t)a.out_rows[row] * a.out_stride;
+        for (uint32_t l = tid; l < T; l += nt) out[l] = lp[l];
+    }
+    const TermDev *terms = a.terms ? a.terms + a.row_term_begin[row] : nullptr;
+    const int nterm = a.terms ? a.row_term_count[row] : 0;
+    for (int k = 0; k < nterm; k++) {
+        double v = wave_sum(term_tile_sum(terms[k], tc, lp, lp, 0, n));
+        if (lane == 0) acc[wave * a.nacc + k] += v;
+    }
+    // 5. adjoint sweep
+    if (a.grad) {
+        const float *up = a.upstream + (int64_t)b * a.K;
+        for (uint32_t l = tid; l < T; l += nt) lf[l] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
+        __syncthreads();
+        for (int oi = 0; oi < a.nrops; oi++) {
+            const PassOp op = a.rops[oi];
+            double g0 = 0, g1 = 0;
+            rev_op(op, lm, 0, lp, lf, n, 0, g0, g1);
+            if (op.ngrad > 0) {
+                double v = wave_sum(g0);
+                if (lane == 0) acc[wave * a.nacc + a.gacc + op.gslot[0]] += v;
+            }
+            if (op.ngrad > 1) {
+                double v = wave_sum(g1);
+                if (lane == 0) acc[wave * a.nacc + a.gacc + op.gslot[1]] += v;
+            }
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+    // 6. outputs
+    auto total = [&](int j) { return ((acc[j] + acc[a.nacc + j]) + acc[2 * a.nacc + j]) + acc[3 * a.nacc + j]; };
+    if (a.exp_out)
+        for (int k = tid; k < a.K; k += nt) {
+            double sum = 0;
+            for (int ti = 0; ti < nterm; ti++)
+                if (terms[ti].k == k) sum += terms[ti].coeff * total(ti);
+            a.exp_out[(int64_t)b * a.K + k] = (float)sum;
+        }
+    if (a.grad) {
+        const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots);
+        for (int s = tid; s < a.S; s += nt) {
+            double sum = 0;
+            for (int k = a.sym_begin[s]; k < a.sym_begin[s + 1]; k++) {
+                const int gs = a.sym_gslots[k];
+                sum += 2.0 * scale[a.gslot_slot[gs]] * total(a.gacc + gs);
+            }
+            a.grad[(int64_t)b * a.S + s] = (float)sum;
+        }
     }
 }
 
@@ -967,16 +1176,16 @@ hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s)
     return hipGetLastError();
 }
 
-size_t pass_lds_bytes(const TileGeom &g, bool product_init)
+size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat)
 {
-    size_t b = sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h);
+    size_t b = sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) + sizeof(double2) * nmat;
     if (product_init) b += sizeof(double2) * (((size_t)1 << (g.t / 2)) + ((size_t)1 << (g.t - g.t / 2)));
     return b;
 }
 
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s)
 {
-    size_t lds = pass_lds_bytes(a.g, a.product_init != 0);
+    size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     hipError_t e = set_lds(k_pass, lds);
     if (e != hipSuccess) return e;
     prof::Scope ps("pass", s);
@@ -1015,11 +1224,28 @@ hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s)
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s)
 {
     size_t lds = 2 * sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
-                 sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
+                 sizeof(double2) * (size_t)(a.mat_end - a.mat_begin) + sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
     hipError_t e = set_lds(k_rev_pass, lds);
     if (e != hipSuccess) return e;
     prof::Scope ps("rev_pass", s);
     hipLaunchKernelGGL(k_rev_pass, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+size_t resident_lds_bytes(int n, int nmat, int nacc, bool adjoint)
+{
+    return sizeof(double2) * (size_t)nmat + sizeof(double) * 4 * (size_t)nacc +
+           sizeof(float2) * ((size_t)1 << n) * (adjoint ? 2 : 1);
+}
+
+hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s)
+{
+    if (nrows <= 0) return hipSuccess;
+    size_t lds = resident_lds_bytes(a.n, a.mat_block, a.nacc, a.grad != nullptr);
+    hipError_t e = set_lds(k_resident, lds);
+    if (e != hipSuccess) return e;
+    prof::Scope ps("resident", s);
+    hipLaunchKernelGGL(k_resident, dim3(nrows), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
 

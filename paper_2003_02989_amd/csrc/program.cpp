@@ -59,7 +59,7 @@ bool op_shape(int op, int &nq, int &np)
 }
 
 // Gate classes as the tile passes see them.
-enum Cls { C_1D, C_1M, C_CTRL, C_2D, C_2M };
+enum Cls { C_1D, C_1M, C_CTRL, C_2D, C_2M, C_2P };
 
 int classify(int op)
 {
@@ -70,7 +70,9 @@ int classify(int op)
         return C_CTRL;
     case OP_CZ: case OP_CZPOW: case OP_ZZPOW: case OP_RZZ:
         return C_2D;
-    case OP_XXPOW: case OP_YYPOW: case OP_FSIM: case OP_MATRIX2: case OP_SWAP:
+    case OP_XXPOW: case OP_YYPOW:
+        return C_2P;
+    case OP_FSIM: case OP_MATRIX2: case OP_SWAP:
         return C_2M;
     default:
         return C_1M;
@@ -218,14 +220,14 @@ struct Planner {
         g.mat_block += entries;
         return o;
     }
-    int add_task(uint8_t kind, int dim, bool diag, int which, const std::vector<Member> &mem)
+    int add_task(uint8_t kind, int dim, int storage, int which, const std::vector<Member> &mem)
     {
         BuildTask bt{};
         bt.kind = kind;
         bt.dim = (uint8_t)dim;
-        bt.diag = diag;
+        bt.diag = (uint8_t)storage;
         bt.which = (uint8_t)which;
-        bt.out = alloc(diag ? dim : dim * dim);
+        bt.out = alloc(storage == 1 ? dim : storage >= 2 ? 2 : dim * dim);
         bt.mem_begin = (int32_t)g.members.size();
         bt.mem_count = (int32_t)mem.size();
         for (const auto &m : mem) g.members.push_back(m);
@@ -233,6 +235,46 @@ struct Planner {
         return (int)g.tasks.size() - 1;
     }
 };
+
+// Append a pass, split into consecutive passes over the same tile when its
+// matrices would not fit the LDS staging area (op k owns the matrix entries
+// from its offset up to the next op's).
+void push_split(std::vector<Pass> &out, Pass ps)
+{
+    if (ps.mat_end - ps.mat_begin <= kMaxPassMat) {
+        out.push_back(std::move(ps));
+        return;
+    }
+    Pass cur;
+    cur.geom = ps.geom;
+    cur.product_init = ps.product_init;
+    cur.mat_begin = ps.mat_begin;
+    for (size_t k = 0; k < ps.ops.size(); k++) {
+        const int32_t op_begin = ps.ops[k].mat;
+        const int32_t op_end = k + 1 < ps.ops.size() ? ps.ops[k + 1].mat : ps.mat_end;
+        if (op_end - cur.mat_begin > kMaxPassMat && !cur.ops.empty()) {
+            cur.mat_end = op_begin;
+            out.push_back(cur);
+            cur.ops.clear();
+            cur.mat_begin = op_begin;
+            cur.product_init = false;
+        }
+        cur.ops.push_back(ps.ops[k]);
+    }
+    cur.mat_end = ps.mat_end;
+    out.push_back(std::move(cur));
+}
+
+int op_dim(const PassOp &op) { return (op.kind == K_M2 || op.kind == K_D2 || op.kind == K_P2) ? 4 : 2; }
+
+// how the builder stores an op's matrix: 0 dense, 1 diagonal, 2 / 3 the
+// pair (a, b) of a I + b XX / a I + b YY
+int storage_of(const PassOp &op)
+{
+    if (op.kind == K_D1 || op.kind == K_D2) return 1;
+    if (op.kind == K_P2) return op.ptype == 1 ? 2 : 3;
+    return 0;
+}
 
 PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
 {
@@ -245,6 +287,10 @@ PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
     case C_1M: op.kind = K_M1; break;
     case C_CTRL: op.kind = K_M1; break;
     case C_2D: op.kind = K_D2; break;
+    case C_2P:
+        op.kind = K_P2;
+        op.ptype = g.gates[gi].op == OP_XXPOW ? 1 : 2;
+        break;
     default: op.kind = K_M2; break;
     }
     if (cls == C_CTRL) {  // q0 field = target, q1 field = control
@@ -293,7 +339,7 @@ void plan_group(Group &g, const Options &opt, int S)
     for (int q = 0; q < n; q++) {
         std::vector<Member> mem;
         for (int gi : absorbed[q]) mem.push_back(Member{gi, 0, FORM_FULL, {0, 0}});
-        int ti = P.add_task(BT_PRODUCT, 2, false, 0, mem);
+        int ti = P.add_task(BT_PRODUCT, 2, 0, 0, mem);
         g.init_mat[q] = g.tasks[ti].out;
     }
 
@@ -333,12 +379,16 @@ void plan_group(Group &g, const Options &opt, int S)
                     continue;
                 }
             }
-            if (opt.fuse && (cls == C_2D || cls == C_2M)) {
+            if (opt.fuse && (cls == C_2D || cls == C_2M || cls == C_2P)) {
                 int o = last[q0];
                 if (o >= 0 && last[q1] == o && ops[o].qb >= 0 &&
                     ((ops[o].qa == q0 && ops[o].qb == q1) || (ops[o].qa == q1 && ops[o].qb == q0))) {
                     ops[o].mem.push_back(Member{gi, (uint8_t)(ops[o].qa != q0), FORM_FULL, {0, 0}});
-                    if (cls == C_2M) ops[o].op.kind = K_M2;
+                    // products of a I + b P with one P keep that form (P^2 = I,
+                    // and P is symmetric in its two qubits); anything else is dense
+                    const uint8_t pt = g.gates[gi].op == OP_XXPOW ? 1 : 2;
+                    if (cls == C_2P && ops[o].op.kind == K_P2 && ops[o].op.ptype == pt) continue;
+                    ops[o].op.kind = (cls == C_2D && ops[o].op.kind == K_D2) ? K_D2 : K_M2;
                     continue;
                 }
             }
@@ -352,16 +402,17 @@ void plan_group(Group &g, const Options &opt, int S)
             last[q0] = oi;
             if (g.gates[gi].nq == 2) last[q1] = oi;
         }
+        ps.mat_begin = pi == 0 ? 0 : g.mat_block;
         for (auto &ob : ops) {
-            bool diag = ob.op.kind == K_D1 || ob.op.kind == K_D2;
-            int dim = (ob.op.kind == K_M2 || ob.op.kind == K_D2) ? 4 : 2;
-            int ti = P.add_task(BT_PRODUCT, dim, diag, 0, ob.mem);
+            int ti = P.add_task(BT_PRODUCT, op_dim(ob.op), storage_of(ob.op), 0, ob.mem);
             ob.op.mat = g.tasks[ti].out;
             ps.ops.push_back(ob.op);
         }
-        g.fwd.push_back(std::move(ps));
+        ps.mat_end = g.mat_block;
+        push_split(g.fwd, std::move(ps));
     }
     g.fwd_tasks.end = (int)g.tasks.size();
+    g.fwd_mat_end = g.mat_block;
 
     // reverse passes: every gate, last first, W^dagger and dW/deta per op;
     // two states share the LDS, so the tile is one bit smaller at most 12
@@ -393,11 +444,11 @@ void plan_group(Group &g, const Options &opt, int S)
     for (auto &s : rs) {
         Pass ps;
         ps.geom = geom_from_bits(n, std::min(opt.low, trev - 2), s.bits);
+        ps.mat_begin = g.mat_block;
         for (int gi : s.items) {
             int cls = classify(g.gates[gi].op);
             PassOp op = base_op(g, ps.geom, gi, n);
-            bool diag = op.kind == K_D1 || op.kind == K_D2;
-            int dim = (op.kind == K_M2 || op.kind == K_D2) ? 4 : 2;
+            const int dim = op_dim(op), diag = storage_of(op);
             Member m{gi, 0, (uint8_t)(cls == C_CTRL ? FORM_CBLOCK : FORM_FULL), {0, 0}};
             int ti = P.add_task(BT_DAGGER, dim, diag, 0, {m});
             op.mat = g.tasks[ti].out;
@@ -413,7 +464,8 @@ void plan_group(Group &g, const Options &opt, int S)
             }
             ps.ops.push_back(op);
         }
-        g.rev.push_back(std::move(ps));
+        ps.mat_end = g.mat_block;
+        push_split(g.rev, std::move(ps));
     }
     g.rev_tasks.end = (int)g.tasks.size();
 
@@ -423,7 +475,7 @@ void plan_group(Group &g, const Options &opt, int S)
             for (const PassOp &op : ps.ops) {
                 bool ok = true;
                 if (op.kind == K_M1) ok = op.l0 < ps.geom.t && (!op.ctrl || op.l1 == kFixed || op.l1 < ps.geom.t);
-                if (op.kind == K_M2) ok = op.l0 < ps.geom.t && op.l1 < ps.geom.t && op.l0 != op.l1;
+                if (op.kind == K_M2 || op.kind == K_P2) ok = op.l0 < ps.geom.t && op.l1 < ps.geom.t && op.l0 != op.l1;
                 if (op.kind == K_D1 || op.kind == K_D2) ok = op.p0 < n && (op.kind == K_D1 || op.p1 < n);
                 if (!ok) fail(TQ_E_UNSUPPORTED, "internal planner error: op outside its tile");
             }

@@ -39,6 +39,7 @@ struct Pass {
     TileGeom geom;
     std::vector<PassOp> ops;
     bool product_init = false;
+    int32_t mat_begin = 0, mat_end = 0;  // the pass's matrices in the row block
 };
 
 // Build-task ranges of a group: [begin, end) into Group::tasks.
@@ -69,7 +70,7 @@ struct Group {
     std::vector<int32_t> gslot_slot;            // gradient slot -> parameter slot
     std::vector<int32_t> sym_gslot_begin;       // [S+1] CSR symbol -> gradient slots
     std::vector<int32_t> sym_gslots;
-    TileGeom egeom;                             // tile geometry of expectation / H_g kernels
+    int32_t fwd_mat_end = 0;                    // forward matrices (with the product init) end here
 };
 
 struct ProgramData {

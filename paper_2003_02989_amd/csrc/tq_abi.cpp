@@ -242,6 +242,8 @@ void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const i
         a.wg_per_row = wg_for(nrows, a.tiles_log2);
         a.product_init = ps.product_init;
         for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
+        a.mat_begin = ps.mat_begin;
+        a.mat_end = ps.mat_end;
         hip_check(launch_pass(a, nrows, s), "pass launch");
     }
 }
@@ -375,6 +377,77 @@ void expect_group(tq_program p, size_t gi, const float2 *psi, int K, float *out,
 
 hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Small circuits run as one resident kernel per call when psi (and phi), the
+// row's matrices and the accumulators fit in LDS.
+constexpr size_t kResidentLds = 150 * 1024;
+
+bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
+{
+    const Group &g = *p->pd->groups[gi];
+    if (g.n > std::min(p->pd->opt.tile, 12)) return false;
+    const int nmat = std::max(adjoint ? g.mat_block : g.fwd_mat_end, 1);
+    const int nacc = std::max(tmax + (adjoint ? g.n_gslots : 0), 1);
+    return resident_lds_bytes(g.n, nmat, nacc, adjoint) <= kResidentLds;
+}
+
+ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    build_mats(p, gi, theta, g.fwd_tasks.begin, adjoint ? g.rev_tasks.end : g.fwd_tasks.end, s);
+    ResArgs a{};
+    a.mats = mat_ws(p) + gd.mat_off;
+    a.mat_stride = std::max(g.mat_block, 1);
+    a.slot_scale = (const double *)gd.scale.p;
+    a.uniform = g.uniform_slots;
+    a.n_slots = g.n_slots;
+    a.S = p->pd->S;
+    a.rows = (const int32_t *)gd.rows.p;
+    a.mat_block = std::max(adjoint ? g.mat_block : g.fwd_mat_end, 1);
+    a.n = g.n;
+    a.fops = (const PassOp *)gd.fwd_ops.p;
+    a.nfops = 0;
+    for (const Pass &ps : g.fwd) a.nfops += (int)ps.ops.size();
+    for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
+    a.rops = (const PassOp *)gd.rev_ops.p;
+    for (const Pass &ps : g.rev) a.nrops += (int)ps.ops.size();
+    a.sym_begin = (const int32_t *)gd.sym_begin.p;
+    a.sym_gslots = (const int32_t *)gd.sym_gslots.p;
+    a.gslot_slot = (const int32_t *)gd.gslot_slot.p;
+    a.nacc = 1;
+    return a;
+}
+
+void resident_terms(tq_program p, size_t gi, ResArgs &a, int K, float *exp_out)
+{
+    ObsGroupDev &og = *p->obs_dev[gi];
+    a.terms = (const TermDev *)og.terms.p;
+    a.row_term_begin = (const int32_t *)og.begin.p;
+    a.row_term_count = (const int32_t *)og.count.p;
+    a.K = K;
+    a.exp_out = exp_out;
+    a.gacc = og.tmax;
+    a.nacc = std::max(og.tmax, 1);
+}
+
+// the final states of group gi into its rows of the state workspace
+void forward_to_ws(tq_program p, size_t gi, const float *theta, float2 *psi, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    if (resident(p, gi, false, 0)) {
+        ResArgs a = resident_args(p, gi, theta, false, s);
+        a.state_out = psi;
+        a.out_stride = (int64_t)1 << g.n;
+        a.out_rows = (const int32_t *)gd.ident.p;
+        hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+        return;
+    }
+    build_mats(p, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+    forward(p, gi, psi, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+}
+
+
 void check_align(const void *p, size_t a, const char *name)
 {
     if (reinterpret_cast<uintptr_t>(p) % a != 0)
@@ -483,8 +556,16 @@ tq_status tq_simulate_state(tq_program prog, const float *theta, void *states, v
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-            forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s);
+            if (resident(prog, gi, false, 0)) {
+                ResArgs a = resident_args(prog, gi, theta, false, s);
+                a.state_out = (float2 *)states;
+                a.out_stride = stride;
+                a.out_rows = (const int32_t *)gd.rows.p;
+                hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+            } else {
+                build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
+                forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s);
+            }
             if (g.n < pd.nmax)
                 hip_check(launch_zero_tail((float2 *)states, stride, (const int32_t *)gd.rows.p, (int)g.rows.size(),
                                            (int64_t)1 << g.n, stride, s),
@@ -511,6 +592,12 @@ tq_status tq_expectation(tq_program prog, const float *theta, tq_observables obs
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
+            if (resident(prog, gi, false, prog->obs_dev[gi]->tmax)) {
+                ResArgs a = resident_args(prog, gi, theta, false, s);
+                resident_terms(prog, gi, a, obs->od->K, out);
+                hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+                continue;
+            }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
             forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
             expect_group(prog, gi, psi + gd.psi_off, obs->od->K, out, s);
@@ -543,6 +630,18 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
             ObsGroupDev &og = *prog->obs_dev[gi];
             const int nrows = (int)g.rows.size();
             const int64_t stride = (int64_t)1 << g.n;
+            if (resident(prog, gi, true, og.tmax)) {
+                ResArgs a = resident_args(prog, gi, theta, pd.S > 0, s);
+                resident_terms(prog, gi, a, K, expectations);
+                if (pd.S > 0) {
+                    a.upstream = upstream;
+                    a.grad = grad;
+                    a.nacc = og.tmax + g.n_gslots;
+                }
+                a.nacc = std::max(a.nacc, 1);
+                hip_check(launch_resident(a, nrows, s), "resident launch");
+                continue;
+            }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
             forward(prog, gi, psi + gd.psi_off, stride, (const int32_t *)gd.ident.p, s);
             if (expectations && K > 0) expect_group(prog, gi, psi + gd.psi_off, K, expectations, s);
@@ -590,6 +689,8 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                 for (const PassOp &op : ps.ops) gc += op.ngrad;
                 r.gbase = gbase;
                 r.gcount = gc;
+                r.mat_begin = ps.mat_begin;
+                r.mat_end = ps.mat_end;
                 gbase += gc;
                 hip_check(launch_rev_pass(r, nrows, s), "reverse pass launch");
             }
@@ -628,8 +729,7 @@ tq_status tq_sample(tq_program prog, const float *theta, int64_t n_shots, uint64
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s);
             SampArgs a{};
             a.state = psi + gd.psi_off;
             a.row_stride = (int64_t)1 << g.n;
@@ -664,8 +764,7 @@ tq_status tq_amplitudes(tq_program prog, const float *theta, const uint64_t *bit
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s);
             GatherArgs a{};
             a.state = psi + gd.psi_off;
             a.row_stride = (int64_t)1 << g.n;
@@ -730,7 +829,7 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
         if (!prog) fail(TQ_E_INVALID, "program is NULL");
         const ProgramData &pd = *prog->pd;
         std::ostringstream o;
-        static const char *kinds[] = {"?", "M1", "M2", "D1", "D2"};
+        static const char *kinds[] = {"?", "M1", "M2", "D1", "D2", "P2"};
         o << "{\"B\":" << pd.B << ",\"S\":" << pd.S << ",\"nmax\":" << pd.nmax << ",\"tile\":" << pd.opt.tile
           << ",\"low\":" << pd.opt.low << ",\"groups\":[";
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {

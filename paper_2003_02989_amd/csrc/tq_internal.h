@@ -16,7 +16,8 @@ enum Opcode : uint16_t {
 constexpr int kMaxQubits = 32;
 constexpr int kThreads = 256;  // threads per workgroup of every tile kernel
 constexpr uint8_t kFixed = 0xFF;  // "bit not in the tile" marker
-constexpr int kMaxGradPerPass = 1024;  // gradient slots one reverse pass accumulates
+constexpr int kMaxGradPerPass = 512;  // gradient slots one reverse pass accumulates
+constexpr int kMaxPassMat = 2048;     // matrix entries (complex128) one pass stages in LDS
 
 // One gate of a structure, as the device matrix builder reads it.
 struct GateDev {
@@ -51,7 +52,7 @@ enum TaskKind : uint8_t {
 struct BuildTask {
     uint8_t kind;
     uint8_t dim;    // 2 or 4
-    uint8_t diag;   // store only the diagonal (dim entries)
+    uint8_t diag;   // store only the diagonal (dim entries); 2 = store (a, b) of a I + b XX, 3 = of a I + b YY
     uint8_t which;  // BT_DERIV parameter index
     int32_t out;    // offset (complex entries) in the row's matrix block
     int32_t mem_begin, mem_count;
@@ -63,6 +64,7 @@ enum OpKind : uint8_t {
     K_M2 = 2, // dense 4x4 on local bits (q0 = first qubit, q1 = second)
     K_D1 = 3, // diagonal on q0 (local or fixed)
     K_D2 = 4, // diagonal on (q0, q1), entry index 2*bit(q0) + bit(q1)
+    K_P2 = 5, // a I + b P on local bits (q0, q1) with P = XX (ptype 1) or YY (ptype 2)
 };
 
 struct PassOp {
@@ -72,6 +74,8 @@ struct PassOp {
     uint8_t ctrl;     // K_M1: 1 if q1 is a control qubit
     uint8_t cval;     // K_M1: the control value that enables the op
     uint8_t ngrad;    // reverse ops: symbolic parameters (0..2)
+    uint8_t ptype;    // K_P2: 1 = XX, 2 = YY
+    uint8_t pad[3];
     int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
     int32_t dmat[2];  // reverse: offsets of dW/deta_j
     int32_t gslot[2]; // reverse: gradient slot ids

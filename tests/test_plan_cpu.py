@@ -26,7 +26,7 @@ def check_plan(w, **kw):
             for op in ps["ops"]:
                 if op["kind"] in ("M1", "M2"):
                     assert op["l"][0] < t
-                if op["kind"] == "M2":
+                if op["kind"] in ("M2", "P2"):
                     assert op["l"][1] < t and op["l"][0] != op["l"][1]
         assert g["fwd"][0]["product_init"] == 1
     return d
