@@ -132,6 +132,8 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the batched path has no "
@@ -145,6 +147,9 @@ def main():
 
     local_rank = int(os.environ.get("LOCAL_RANK", "0"))
     torch.cuda.set_device(local_rank)
+    if args.sweep:
+        sweep(args.steps)
+        return
     w = workload(args.config)
     B, K = w.B, w.K
     t_cold0 = time.perf_counter()
@@ -249,6 +254,93 @@ def main():
     if not args.no_cpu_baseline and local_rank == 0:
         line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def sweep(steps):
+    """Effective HBM bandwidth of single-gate passes and of the expectation
+    kernel for n = 24..30 with batches sized so the states span >= 1 GiB (the
+    256 MB last-level cache cannot hold them).  A pass time is the difference
+    of two programs with max_pass_gates = 1 (every gate its own pass) that
+    differ by G test gates, divided by G.  One JSON line per case."""
+    import numpy as np
+    import torch
+
+    from paper_2003_02989_amd import tq
+    from paper_2003_02989_amd.circuits import Circuit, const, observable_blob, program_blob
+
+    G = 8
+
+    def pass_ms(n, B, prefix, gate):
+        times = []
+        for with_test in (True, False):
+            circuits = []
+            for _ in range(B):
+                c = Circuit(n)
+                for g in prefix:
+                    c.add(*g)
+                if with_test:
+                    for _ in range(G):
+                        c.add(*gate)
+                circuits.append(c)
+            prog = tq.Program(program_blob(circuits, 0), max_pass_gates=1)
+            st = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
+            tq.simulate_state(prog, None, out=st)
+            torch.cuda.synchronize()
+            tq.profile_start("pass")
+            for _ in range(steps):
+                tq.simulate_state(prog, None, out=st)
+            torch.cuda.synchronize()
+            nl, ms = tq.profile_read()
+            tq.profile_start(None)
+            times.append(ms / steps)
+            del st, prog
+        return (times[0] - times[1]) / G
+
+    for n in (24, 26, 28, 30):
+        B = max(1, (1 << 27) >> n)
+        q = lambda bit: n - 1 - bit  # qubit on index bit `bit`
+        cases = []
+        for bit in sorted({0, 3, 6, 10, n - 1}):
+            cases.append((f"1q RX on bit {bit}", [("CZ", (q(bit), q((bit + 1) % n)))], ("RX", q(bit), [const(0.3)])))
+        cases.append((f"fSim on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
+                      ("FSIM", (q(n - 1), q(n - 2)), [const(0.7), const(0.4)])))
+        cases.append(("fSim on bits 0,1", [("CZ", (q(0), q(1)))], ("FSIM", (q(0), q(1)), [const(0.7), const(0.4)])))
+        cases.append((f"XX^t on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
+                      ("XXPOW", (q(n - 1), q(n - 2)), [const(0.3)])))
+        cases.append((f"CNOT control bit {n-1}, target bit 0", [("CZ", (q(n - 1), q(0)))], ("CNOT", (q(n - 1), q(0)))))
+        cases.append((f"RZZ on bits {n-1},0 (diagonal)", [("CZ", (q(n - 1), q(0)))], ("RZZ", (q(n - 1), q(0)), [const(0.3)])))
+        for name, prefix, gate in cases:
+            ms = pass_ms(n, B, prefix, gate)
+            gbs = 16.0 * (1 << n) * B / (ms * 1e-3) / 1e9
+            print(json.dumps({"sweep": "gate_pass", "n": n, "batch": B, "case": name, "ms_per_pass": ms,
+                              "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
+        # expectation kernel: sum_i Z_i, and 16 random X/Y/Z strings
+        rng = np.random.default_rng(n)
+        obs_sets = {"sum Z_i": [(1.0, [(i, "Z")]) for i in range(n)],
+                    "16 XYZ strings": [(float(rng.standard_normal()),
+                                        [(int(x), "XYZ"[int(rng.integers(0, 3))])
+                                         for x in rng.choice(n, size=int(rng.integers(1, 5)), replace=False)])
+                                       for _ in range(16)]}
+        c = Circuit(n)
+        for i in range(n - 1):
+            c.add("CZ", (i, i + 1))
+        prog = tq.Program(program_blob([c] * B, 0))
+        for oname, terms in obs_sets.items():
+            obs = tq.Observables(observable_blob([[terms]] * B))
+            out = torch.empty((B, 1), dtype=torch.float32, device="cuda")
+            tq.expectation(prog, None, obs, out=out)
+            torch.cuda.synchronize()
+            tq.profile_start("expect")
+            for _ in range(steps):
+                tq.expectation(prog, None, obs, out=out)
+            torch.cuda.synchronize()
+            nl, ms = tq.profile_read()
+            tq.profile_start(None)
+            ms /= max(nl, 1)
+            gbs = 8.0 * (1 << n) * B / (ms * 1e-3) / 1e9
+            print(json.dumps({"sweep": "expectation", "n": n, "batch": B, "case": oname, "ms": ms,
+                              "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
+        del prog
 
 
 def cpu_baseline(name, w, budget_s):

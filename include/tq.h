@@ -62,12 +62,15 @@ typedef enum {
  *                    wavefront reads runs of 2^low_qubits amplitudes
  *                    (default 6, allowed 3..8);
  *   fuse:            1 = fuse neighbouring gates into one matrix (default),
- *                    -1 = apply every gate on its own. */
+ *                    -1 = apply every gate on its own;
+ *   max_pass_gates:  at most this many gates per sweep over the state
+ *                    (default 0 = no limit; 1 makes every gate its own pass,
+ *                    which measures the bandwidth of single-gate passes). */
 typedef struct {
     int32_t max_tile_qubits;
     int32_t low_qubits;
     int32_t fuse;
-    int32_t reserved;
+    int32_t max_pass_gates;
 } tq_options;
 
 /* Parse, validate and plan a batch of B parameterized circuits over S symbols

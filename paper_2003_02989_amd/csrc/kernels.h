@@ -31,8 +31,9 @@ struct PassArgs {
     const int32_t *rows;
     const double2 *mats;
     int64_t mat_stride;
-    const PassOp *ops;
-    int nops;
+    const PassOp *ops;     // the group's forward ops (stages index them)
+    const Stage *stages;   // this pass's stages
+    int nstages;
     TileGeom g;
     int tiles_log2;
     int wg_per_row;
@@ -82,8 +83,9 @@ struct RevArgs {
     const int32_t *rows;
     const double2 *mats;
     int64_t mat_stride;
-    const PassOp *ops;
-    int nops;
+    const PassOp *ops;     // the group's reverse ops
+    const Stage *stages;   // this pass's stages
+    int nstages;
     TileGeom g;
     int tiles_log2, wg_per_row;
     int store;
@@ -102,7 +104,8 @@ struct ResArgs {
     int mat_block;        // LDS matrix entries
     int n;
     const PassOp *fops;
-    int nfops;
+    const Stage *fstages;
+    int nfstages;
     int32_t init_mat[kMaxQubits];
     // optional state output
     float2 *state_out;
@@ -116,7 +119,8 @@ struct ResArgs {
     int nacc, gacc;  // accumulators: [0, gacc) terms, [gacc, gacc + n_gslots) gradients
     // optional adjoint
     const PassOp *rops;
-    int nrops;
+    const Stage *rstages;
+    int nrstages;
     const float *upstream;
     const int32_t *sym_begin, *sym_gslots, *gslot_slot;
     float *grad;

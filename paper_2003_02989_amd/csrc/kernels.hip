@@ -36,6 +36,11 @@ __device__ __forceinline__ double2 zadd(double2 a, double2 b) { return make_doub
 // Re(conj(a) b)
 __device__ __forceinline__ double zdotr(double2 a, double2 b) { return a.x * b.x + a.y * b.y; }
 
+// LDS position of tile element i: an XOR swizzle that keeps runs of 32
+// consecutive elements on distinct bank pairs and spreads strided stage
+// gathers (lanes 2^r elements apart) over the banks as well
+__device__ __forceinline__ uint32_t sw(uint32_t i) { return i ^ ((i >> 5) & 31u); }
+
 // insert a zero bit at position k of p
 __device__ __forceinline__ uint32_t ins0(uint32_t p, int k) { return ((p >> k) << (k + 1)) | (p & ((1u << k) - 1)); }
 
@@ -275,7 +280,12 @@ template <int D> __device__ __forceinline__ void build_task_d(const BuildTask &b
             for (int i = 0; i < D * D; i++) acc[i] = t[i];
         }
     }
-    if (bt.diag >= 2) {
+    if (bt.diag == 4) {
+        // excitation preserving: |00> phase, the (|01>, |10>) block, |11> phase
+        const int ix[6] = {0, 5, 6, 9, 10, 15};
+#pragma unroll
+        for (int i = 0; i < 6; i++) out[i] = make_double2(acc[ix[i]].x, acc[ix[i]].y);
+    } else if (bt.diag >= 2) {
         // a I + b P: a from entry (0,0), b from entry (0,3) (P_03 = 1 for XX, -1 for YY)
         const double sg = bt.diag == 3 ? -1.0 : 1.0;
         out[0] = make_double2(acc[0].x, acc[0].y);
@@ -332,16 +342,17 @@ __device__ __forceinline__ void tile_copy(const TileCtx &tc, float2 *lds, float2
             float4 *p = reinterpret_cast<float4 *>(row + tile_index(tc, fb, l));
             if (kLoad) {
                 float4 v = *p;
-                lds[l] = make_float2(v.x, v.y);
-                lds[l + 1] = make_float2(v.z, v.w);
+                lds[sw(l)] = make_float2(v.x, v.y);
+                lds[sw(l + 1)] = make_float2(v.z, v.w);
             } else {
-                *p = make_float4(lds[l].x, lds[l].y, lds[l + 1].x, lds[l + 1].y);
+                const float2 u0 = lds[sw(l)], u1 = lds[sw(l + 1)];
+                *p = make_float4(u0.x, u0.y, u1.x, u1.y);
             }
         }
     } else {
         for (int l = threadIdx.x; l < T; l += blockDim.x) {
-            if (kLoad) lds[l] = row[tile_index(tc, fb, l)];
-            else row[tile_index(tc, fb, l)] = lds[l];
+            if (kLoad) lds[sw(l)] = row[tile_index(tc, fb, l)];
+            else row[tile_index(tc, fb, l)] = lds[sw(l)];
         }
     }
 }
@@ -387,179 +398,533 @@ __device__ __forceinline__ Quad p2_apply(double2 a, double2 b, double sg, const 
     return o;
 }
 
-// Apply one op to a tile of 2^t amplitudes in LDS.  `m` is the op's matrix
-// (row major; diagonal ops keep their diagonal only), in LDS or global memory.
-__device__ void apply_op(const PassOp &op, const double2 *m, float2 *lds, int t, uint64_t fb)
+// ------------------------------------------------------- register stages
+// A stage's ops run on the 2^R amplitudes one thread holds in registers (in
+// fp64); register index k has bit j set when tile bit stage.bits[j] is set.
+// An op bit outside the stage comes from the item's base index or the fixed
+// bits of the tile.
+
+// Register-level ops.  Every variant is a template on the register bits it
+// touches, so the element pattern is fixed at compile time (no selects).
+
+// dense 2x2 on register bit J
+template <int R, int J> __device__ __forceinline__ void rm1(double2 *a, const double2 *m)
 {
-    const uint32_t T = 1u << t;
-    const int tid = threadIdx.x, nt = blockDim.x;
-    if (op.kind == K_M1) {
-        const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
-        const int tb = op.l0;
-        if (op.ctrl && op.l1 != kFixed) {
-            const int cb = op.l1;
-            const int lo = min(tb, cb), hi = max(tb, cb);
-            const uint32_t cv = (uint32_t)op.cval << cb;
-            for (uint32_t p = tid; p < T / 4; p += nt) {
-                uint32_t i = ins0(ins0(p, lo), hi) | cv, j = i | (1u << tb);
-                double2 a0 = up2(lds[i]), a1 = up2(lds[j]);
-                lds[i] = down2(zmul2(m00, a0, m01, a1));
-                lds[j] = down2(zmul2(m10, a0, m11, a1));
-            }
-            return;
+    const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        a[k] = zmul2(m00, x, m01, y);
+        a[kk] = zmul2(m10, x, m11, y);
+    }
+}
+// sum of Re(conj(f) (dm a)) over the pairs of rm1
+template <int R, int J> __device__ __forceinline__ double rm1_dot(const double2 *a, const double2 *f, const double2 *dm)
+{
+    const double2 m00 = dm[0], m01 = dm[1], m10 = dm[2], m11 = dm[3];
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        s += zdotr(f[k], zmul2(m00, a[k], m01, a[kk])) + zdotr(f[kk], zmul2(m10, a[k], m11, a[kk]));
+    }
+    return s;
+}
+// dense 2x2 on register bit J where register bit C is 1 (controlled gates)
+template <int R, int J, int C> __device__ __forceinline__ void rm1c(double2 *a, const double2 *m)
+{
+    const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> J) & 1) || !((k >> C) & 1)) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        a[k] = zmul2(m00, x, m01, y);
+        a[kk] = zmul2(m10, x, m11, y);
+    }
+}
+template <int R, int J, int C>
+__device__ __forceinline__ double rm1c_dot(const double2 *a, const double2 *f, const double2 *dm)
+{
+    const double2 m00 = dm[0], m01 = dm[1], m10 = dm[2], m11 = dm[3];
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> J) & 1) || !((k >> C) & 1)) continue;
+        const int kk = k | (1 << J);
+        s += zdotr(f[k], zmul2(m00, a[k], m01, a[kk])) + zdotr(f[kk], zmul2(m10, a[k], m11, a[kk]));
+    }
+    return s;
+}
+// diagonal (e0, e1) on register bit J
+template <int R, int J> __device__ __forceinline__ void rd1(double2 *a, double2 e0, double2 e1)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) a[k] = zmul(((k >> J) & 1) ? e1 : e0, a[k]);
+}
+template <int R, int J> __device__ __forceinline__ double rd1_dot(const double2 *a, const double2 *f, double2 e0, double2 e1)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) s += zdotr(f[k], zmul(((k >> J) & 1) ? e1 : e0, a[k]));
+    return s;
+}
+// diagonal on register bits (LO, HI), entry index 2*bit(LO) + bit(HI)
+template <int R, int LO, int HI>
+__device__ __forceinline__ void rd2(double2 *a, double2 e0, double2 e1, double2 e2, double2 e3)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = 2 * ((k >> LO) & 1) + ((k >> HI) & 1);
+        a[k] = zmul(idx == 0 ? e0 : idx == 1 ? e1 : idx == 2 ? e2 : e3, a[k]);
+    }
+}
+template <int R, int LO, int HI>
+__device__ __forceinline__ double rd2_dot(const double2 *a, const double2 *f, double2 e0, double2 e1, double2 e2, double2 e3)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = 2 * ((k >> LO) & 1) + ((k >> HI) & 1);
+        s += zdotr(f[k], zmul(idx == 0 ? e0 : idx == 1 ? e1 : idx == 2 ? e2 : e3, a[k]));
+    }
+    return s;
+}
+template <int R> __device__ __forceinline__ void rscale(double2 *a, double2 e)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) a[k] = zmul(e, a[k]);
+}
+template <int R> __device__ __forceinline__ double rscale_dot(const double2 *a, const double2 *f, double2 e)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) s += zdotr(f[k], zmul(e, a[k]));
+    return s;
+}
+
+// dense 4x4 on register bits (LO = the op's first qubit, HI = its second):
+// local index 2*bit(q0) + bit(q1) = 2*bit(LO) + bit(HI)
+template <int R, int LO, int HI> __device__ __forceinline__ void rm2(double2 *a, const double2 *m)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        const double2 v00 = a[k], v01 = a[k01], v10 = a[k10], v11 = a[k11];
+        a[k] = zadd(zmul2(m[0], v00, m[1], v01), zmul2(m[2], v10, m[3], v11));
+        a[k01] = zadd(zmul2(m[4], v00, m[5], v01), zmul2(m[6], v10, m[7], v11));
+        a[k10] = zadd(zmul2(m[8], v00, m[9], v01), zmul2(m[10], v10, m[11], v11));
+        a[k11] = zadd(zmul2(m[12], v00, m[13], v01), zmul2(m[14], v10, m[15], v11));
+    }
+}
+template <int R, int LO, int HI> __device__ __forceinline__ double rm2_dot(const double2 *a, const double2 *f, const double2 *m)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        const double2 v00 = a[k], v01 = a[k01], v10 = a[k10], v11 = a[k11];
+        s += zdotr(f[k], zadd(zmul2(m[0], v00, m[1], v01), zmul2(m[2], v10, m[3], v11)));
+        s += zdotr(f[k01], zadd(zmul2(m[4], v00, m[5], v01), zmul2(m[6], v10, m[7], v11)));
+        s += zdotr(f[k10], zadd(zmul2(m[8], v00, m[9], v01), zmul2(m[10], v10, m[11], v11)));
+        s += zdotr(f[k11], zadd(zmul2(m[12], v00, m[13], v01), zmul2(m[14], v10, m[15], v11)));
+    }
+    return s;
+}
+// excitation preserving on (LO = q0, HI = q1): m = {p00, b00, b01, b10, b11, p11};
+// out01 = b00 v01 + b01 v10, out10 = b10 v01 + b11 v10
+template <int R, int LO, int HI> __device__ __forceinline__ void rf2(double2 *a, const double2 *m)
+{
+    const double2 p00 = m[0], b00 = m[1], b01 = m[2], b10 = m[3], b11 = m[4], p11 = m[5];
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        const double2 v01 = a[k01], v10 = a[k10];
+        a[k] = zmul(p00, a[k]);
+        a[k01] = zmul2(b00, v01, b01, v10);
+        a[k10] = zmul2(b10, v01, b11, v10);
+        a[k11] = zmul(p11, a[k11]);
+    }
+}
+template <int R, int LO, int HI> __device__ __forceinline__ double rf2_dot(const double2 *a, const double2 *f, const double2 *m)
+{
+    const double2 p00 = m[0], b00 = m[1], b01 = m[2], b10 = m[3], b11 = m[4], p11 = m[5];
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        s += zdotr(f[k], zmul(p00, a[k])) + zdotr(f[k11], zmul(p11, a[k11]));
+        s += zdotr(f[k01], zmul2(b00, a[k01], b01, a[k10])) + zdotr(f[k10], zmul2(b10, a[k01], b11, a[k10]));
+    }
+    return s;
+}
+
+// a I + b P on register bits (LO, HI); P = XX (sg = 1) or YY (sg = -1), symmetric in the two qubits
+template <int R, int LO, int HI> __device__ __forceinline__ void rp2(double2 *a, double2 ca, double2 cb, double sg)
+{
+    const double2 bs = make_double2(sg * cb.x, sg * cb.y);
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int kL = k | (1 << LO), kH = k | (1 << HI), k11 = kL | kH;
+        const double2 v00 = a[k], vL = a[kL], vH = a[kH], v11 = a[k11];
+        a[k] = zadd(zmul(ca, v00), zmul(bs, v11));
+        a[k11] = zadd(zmul(ca, v11), zmul(bs, v00));
+        a[kL] = zadd(zmul(ca, vL), zmul(cb, vH));
+        a[kH] = zadd(zmul(ca, vH), zmul(cb, vL));
+    }
+}
+template <int R, int LO, int HI> __device__ __forceinline__ double rp2_dot(const double2 *a, const double2 *f, double2 ca, double2 cb, double sg)
+{
+    const double2 bs = make_double2(sg * cb.x, sg * cb.y);
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int kL = k | (1 << LO), kH = k | (1 << HI), k11 = kL | kH;
+        s += zdotr(f[k], zadd(zmul(ca, a[k]), zmul(bs, a[k11])));
+        s += zdotr(f[k11], zadd(zmul(ca, a[k11]), zmul(bs, a[k])));
+        s += zdotr(f[kL], zadd(zmul(ca, a[kL]), zmul(cb, a[kH])));
+        s += zdotr(f[kH], zadd(zmul(ca, a[kH]), zmul(cb, a[kL])));
+    }
+    return s;
+}
+
+// Runtime register bit(s) -> template instantiation, written out as switches
+// (no lambdas: the register arrays must stay in registers).
+#define TQ_PAIR_SWITCH(R, LO, HI, CALL)                                                                             \
+    switch ((LO) * 4 + (HI)) {                                                                                      \
+    case 1: if constexpr (R > 1) { constexpr int lo_ = 0, hi_ = 1; CALL; } break;                                   \
+    case 2: if constexpr (R > 2) { constexpr int lo_ = 0, hi_ = 2; CALL; } break;                                   \
+    case 3: if constexpr (R > 3) { constexpr int lo_ = 0, hi_ = 3; CALL; } break;                                   \
+    case 6: if constexpr (R > 2) { constexpr int lo_ = 1, hi_ = 2; CALL; } break;                                   \
+    case 7: if constexpr (R > 3) { constexpr int lo_ = 1, hi_ = 3; CALL; } break;                                   \
+    case 11: if constexpr (R > 3) { constexpr int lo_ = 2, hi_ = 3; CALL; } break;                                  \
+    default: break;                                                                                                 \
+    }
+#define TQ_ORDERED_SWITCH(R, J, C, CALL)                                                                            \
+    switch ((J) * 4 + (C)) {                                                                                        \
+    case 1: if constexpr (R > 1) { constexpr int j_ = 0, c_ = 1; CALL; } break;                                     \
+    case 2: if constexpr (R > 2) { constexpr int j_ = 0, c_ = 2; CALL; } break;                                     \
+    case 3: if constexpr (R > 3) { constexpr int j_ = 0, c_ = 3; CALL; } break;                                     \
+    case 4: if constexpr (R > 1) { constexpr int j_ = 1, c_ = 0; CALL; } break;                                     \
+    case 6: if constexpr (R > 2) { constexpr int j_ = 1, c_ = 2; CALL; } break;                                     \
+    case 7: if constexpr (R > 3) { constexpr int j_ = 1, c_ = 3; CALL; } break;                                     \
+    case 8: if constexpr (R > 2) { constexpr int j_ = 2, c_ = 0; CALL; } break;                                     \
+    case 9: if constexpr (R > 2) { constexpr int j_ = 2, c_ = 1; CALL; } break;                                     \
+    case 11: if constexpr (R > 3) { constexpr int j_ = 2, c_ = 3; CALL; } break;                                    \
+    case 12: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 0; CALL; } break;                                    \
+    case 13: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 1; CALL; } break;                                    \
+    case 14: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 2; CALL; } break;                                    \
+    default: break;                                                                                                 \
+    }
+#define TQ_BIT_SWITCH(R, J, CALL)                                                                                   \
+    switch (J) {                                                                                                    \
+    case 0: if constexpr (R > 0) { constexpr int j_ = 0; CALL; } break;                                             \
+    case 1: if constexpr (R > 1) { constexpr int j_ = 1; CALL; } break;                                             \
+    case 2: if constexpr (R > 2) { constexpr int j_ = 2; CALL; } break;                                             \
+    case 3: if constexpr (R > 3) { constexpr int j_ = 3; CALL; } break;                                             \
+    default: break;                                                                                                 \
+    }
+
+// How a diagonal op acts on a stage item: both bits in registers, one bit
+// (the other one's value fixed for the item), or none (one scalar).
+struct DiagPlan {
+    int mode;     // 0: scalar, 1: one register bit, 2: two register bits
+    int j0, j1;   // register bits (mode 1: j0; mode 2: j0 < j1)
+    int e[4];     // entry indices, ordered by the register bits' pattern
+};
+__device__ __forceinline__ DiagPlan diag_plan(const PassOp &op, uint32_t base, uint64_t fb)
+{
+    DiagPlan d{};
+    if (op.kind == K_D1) {
+        if (op.s0 != kFixed) {
+            d.mode = 1;
+            d.j0 = op.s0;
+            d.e[0] = 0;
+            d.e[1] = 1;
+        } else {
+            d.mode = 0;
+            d.e[0] = bit_of(op.l0, op.p0, base, fb);
         }
-        if (op.ctrl && (int)((fb >> op.p1) & 1) != op.cval) return;
-        for (uint32_t p = tid; p < T / 2; p += nt) {
-            uint32_t i = ins0(p, tb), j = i | (1u << tb);
-            double2 a0 = up2(lds[i]), a1 = up2(lds[j]);
-            lds[i] = down2(zmul2(m00, a0, m01, a1));
-            lds[j] = down2(zmul2(m10, a0, m11, a1));
+        return d;
+    }
+    const bool r0 = op.s0 != kFixed, r1 = op.s1 != kFixed;
+    if (r0 && r1) {
+        d.mode = 2;
+        d.j0 = min(op.s0, op.s1);
+        d.j1 = max(op.s0, op.s1);
+        // idx = 2*bit(q0) + bit(q1); pattern index = 2*bit(j0) + bit(j1)
+        const bool q0lo = op.s0 < op.s1;
+        d.e[0] = 0;
+        d.e[1] = q0lo ? 1 : 2;
+        d.e[2] = q0lo ? 2 : 1;
+        d.e[3] = 3;
+    } else if (r0) {
+        d.mode = 1;
+        d.j0 = op.s0;
+        const int v = bit_of(op.l1, op.p1, base, fb);
+        d.e[0] = v;
+        d.e[1] = 2 + v;
+    } else if (r1) {
+        d.mode = 1;
+        d.j0 = op.s1;
+        const int v = bit_of(op.l0, op.p0, base, fb);
+        d.e[0] = 2 * v;
+        d.e[1] = 2 * v + 1;
+    } else {
+        d.mode = 0;
+        d.e[0] = 2 * bit_of(op.l0, op.p0, base, fb) + bit_of(op.l1, op.p1, base, fb);
+    }
+    return d;
+}
+
+template <int R> __device__ __forceinline__ void reg_diag(const DiagPlan &d, const double2 *m, double2 *a)
+{
+    if (d.mode == 0) {
+        rscale<R>(a, m[d.e[0]]);
+    } else if (d.mode == 1) {
+        const double2 e0 = m[d.e[0]], e1 = m[d.e[1]];
+        TQ_BIT_SWITCH(R, d.j0, (rd1<R, j_>(a, e0, e1)))
+    } else {
+        const double2 e0 = m[d.e[0]], e1 = m[d.e[1]], e2 = m[d.e[2]], e3 = m[d.e[3]];
+        TQ_PAIR_SWITCH(R, d.j0, d.j1, (rd2<R, lo_, hi_>(a, e0, e1, e2, e3)))
+    }
+}
+template <int R> __device__ __forceinline__ double reg_diag_dot(const DiagPlan &d, const double2 *m, const double2 *a, const double2 *f)
+{
+    double s = 0;
+    if (d.mode == 0) {
+        s = rscale_dot<R>(a, f, m[d.e[0]]);
+    } else if (d.mode == 1) {
+        const double2 e0 = m[d.e[0]], e1 = m[d.e[1]];
+        TQ_BIT_SWITCH(R, d.j0, (s = rd1_dot<R, j_>(a, f, e0, e1)))
+    } else {
+        const double2 e0 = m[d.e[0]], e1 = m[d.e[1]], e2 = m[d.e[2]], e3 = m[d.e[3]];
+        TQ_PAIR_SWITCH(R, d.j0, d.j1, (s = rd2_dot<R, lo_, hi_>(a, f, e0, e1, e2, e3)))
+    }
+    return s;
+}
+
+// the control of a K_M1 op: -2 = off for this item, -1 = none (or on), else its register bit
+__device__ __forceinline__ int reg_ctrl(const PassOp &op, uint32_t base, uint64_t fb)
+{
+    if (!op.ctrl) return -1;
+    if (op.s1 != kFixed) return op.s1;
+    return bit_of(op.l1, op.p1, base, fb) == op.cval ? -1 : -2;
+}
+
+// forward op on registers
+template <int R> __device__ __forceinline__ void reg_op(const PassOp &op, const double2 *m, double2 *a, uint32_t base, uint64_t fb)
+{
+    switch (op.kind) {
+    case K_M1: {
+        const int c = reg_ctrl(op, base, fb);
+        if (c == -2) return;
+        if (c == -1) {
+            TQ_BIT_SWITCH(R, op.s0, (rm1<R, j_>(a, m)))
+        } else {
+            TQ_ORDERED_SWITCH(R, op.s0, c, (rm1c<R, j_, c_>(a, m)))
         }
-    } else if (op.kind == K_M2) {
-        const double2 *mm = m;
-        const int b0 = op.l0, b1 = op.l1;
-        const int lo = min(b0, b1), hi = max(b0, b1);
-        for (uint32_t p = tid; p < T / 4; p += nt) {
-            uint32_t i00 = ins0(ins0(p, lo), hi);
-            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
-            double2 v0 = up2(lds[i00]), v1 = up2(lds[i01]), v2 = up2(lds[i10]), v3 = up2(lds[i11]);
-            lds[i00] = down2(zadd(zmul2(mm[0], v0, mm[1], v1), zmul2(mm[2], v2, mm[3], v3)));
-            lds[i01] = down2(zadd(zmul2(mm[4], v0, mm[5], v1), zmul2(mm[6], v2, mm[7], v3)));
-            lds[i10] = down2(zadd(zmul2(mm[8], v0, mm[9], v1), zmul2(mm[10], v2, mm[11], v3)));
-            lds[i11] = down2(zadd(zmul2(mm[12], v0, mm[13], v1), zmul2(mm[14], v2, mm[15], v3)));
-        }
-    } else if (op.kind == K_P2) {
-        const double2 ca = m[0], cb = m[1];
+        return;
+    }
+    case K_M2: TQ_PAIR_SWITCH(R, op.s0, op.s1, (rm2<R, lo_, hi_>(a, m))) return;
+    case K_F2: TQ_PAIR_SWITCH(R, op.s0, op.s1, (rf2<R, lo_, hi_>(a, m))) return;
+    case K_P2: {
         const double sg = op.ptype == 2 ? -1.0 : 1.0;
-        const int b0 = op.l0, b1 = op.l1;
-        const int lo = min(b0, b1), hi = max(b0, b1);
-        for (uint32_t p = tid; p < T / 4; p += nt) {
-            uint32_t i00 = ins0(ins0(p, lo), hi);
-            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
-            Quad v{up2(lds[i00]), up2(lds[i01]), up2(lds[i10]), up2(lds[i11])};
-            Quad o = p2_apply(ca, cb, sg, v);
-            lds[i00] = down2(o.v00);
-            lds[i01] = down2(o.v01);
-            lds[i10] = down2(o.v10);
-            lds[i11] = down2(o.v11);
-        }
-    } else {  // diagonal
-        for (uint32_t l = tid; l < T; l += nt) lds[l] = down2(zmul(m[diag_index(op, l, fb)], up2(lds[l])));
+        const double2 ca = m[0], cb = m[1];
+        TQ_PAIR_SWITCH(R, min(op.s0, op.s1), max(op.s0, op.s1), (rp2<R, lo_, hi_>(a, ca, cb, sg)))
+        return;
+    }
+    default: reg_diag<R>(diag_plan(op, base, fb), m, a); return;
     }
 }
 
-// One reversed gate W on the psi and phi tiles: psi <- W^dagger psi, then
-// g_j += Re <phi| dW/deta_j |psi> over this thread's elements, then
-// phi <- W^dagger phi.  M is the row's matrix block (op offsets index it).
-__device__ void rev_op(const PassOp &op, const double2 *M, int base, float2 *lp, float2 *lf, int t,
-                       uint64_t fb, double &g0, double &g1)
+// reverse op on registers: a <- W^dagger a (m = W^dagger); g_j += sum Re(conj(f) dW_j a);
+// f <- W^dagger f
+template <int R>
+__device__ __forceinline__ void reg_rev_op(const PassOp &op, const double2 *m, const double2 *d0, const double2 *d1,
+                                           double2 *a, double2 *f, uint32_t base, uint64_t fb, double &g0, double &g1)
 {
-    const uint32_t T = 1u << t;
-    const int tid = threadIdx.x, nt = blockDim.x;
-    const double2 *m = M + (op.mat - base);
-    const double2 *d0 = M + (op.ngrad > 0 ? op.dmat[0] - base : 0);
-    const double2 *d1 = M + (op.ngrad > 1 ? op.dmat[1] - base : 0);
-    if (op.kind == K_M1) {
-        const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
-        const int tb = op.l0;
-        uint32_t count = T / 2;
-        int lo = tb, hi = tb, cb = -1;
-        uint32_t cv = 0;
-        if (op.ctrl) {
-            if (op.l1 == kFixed) {
-                if ((int)((fb >> op.p1) & 1) != op.cval) return;
-            } else {
-                cb = op.l1;
-                lo = min(tb, cb);
-                hi = max(tb, cb);
-                cv = (uint32_t)op.cval << cb;
-                count = T / 4;
-            }
+    switch (op.kind) {
+    case K_M1: {
+        const int c = reg_ctrl(op, base, fb);
+        if (c == -2) return;
+        if (c == -1) {
+            TQ_BIT_SWITCH(R, op.s0, ({
+                rm1<R, j_>(a, m);
+                if (op.ngrad > 0) g0 += rm1_dot<R, j_>(a, f, d0);
+                if (op.ngrad > 1) g1 += rm1_dot<R, j_>(a, f, d1);
+                rm1<R, j_>(f, m);
+            }))
+        } else {
+            TQ_ORDERED_SWITCH(R, op.s0, c, ({
+                rm1c<R, j_, c_>(a, m);
+                if (op.ngrad > 0) g0 += rm1c_dot<R, j_, c_>(a, f, d0);
+                if (op.ngrad > 1) g1 += rm1c_dot<R, j_, c_>(a, f, d1);
+                rm1c<R, j_, c_>(f, m);
+            }))
         }
-        for (uint32_t p = tid; p < count; p += nt) {
-            uint32_t i = cb >= 0 ? (ins0(ins0(p, lo), hi) | cv) : ins0(p, tb);
-            uint32_t j = i | (1u << tb);
-            double2 a0 = up2(lp[i]), a1 = up2(lp[j]);
-            double2 b0 = zmul2(m00, a0, m01, a1), b1 = zmul2(m10, a0, m11, a1);
-            lp[i] = down2(b0);
-            lp[j] = down2(b1);
-            double2 f0 = up2(lf[i]), f1 = up2(lf[j]);
-            if (op.ngrad > 0) g0 += zdotr(f0, zmul2(d0[0], b0, d0[1], b1)) + zdotr(f1, zmul2(d0[2], b0, d0[3], b1));
-            if (op.ngrad > 1) g1 += zdotr(f0, zmul2(d1[0], b0, d1[1], b1)) + zdotr(f1, zmul2(d1[2], b0, d1[3], b1));
-            lf[i] = down2(zmul2(m00, f0, m01, f1));
-            lf[j] = down2(zmul2(m10, f0, m11, f1));
-        }
-    } else if (op.kind == K_M2) {
-        const double2 *mm = m;
-        const int b0 = op.l0, b1 = op.l1;
-        const int lo = min(b0, b1), hi = max(b0, b1);
-        for (uint32_t p = tid; p < T / 4; p += nt) {
-            uint32_t ix[4];
-            ix[0] = ins0(ins0(p, lo), hi);
-            ix[1] = ix[0] | (1u << b1);
-            ix[2] = ix[0] | (1u << b0);
-            ix[3] = ix[1] | (1u << b0);
-            double2 u[4], f[4];
-            {
-                const double2 v0 = up2(lp[ix[0]]), v1 = up2(lp[ix[1]]), v2 = up2(lp[ix[2]]), v3 = up2(lp[ix[3]]);
-#pragma unroll
-                for (int r = 0; r < 4; r++)
-                    u[r] = zadd(zmul2(mm[4 * r], v0, mm[4 * r + 1], v1), zmul2(mm[4 * r + 2], v2, mm[4 * r + 3], v3));
-            }
-#pragma unroll
-            for (int r = 0; r < 4; r++) lp[ix[r]] = down2(u[r]);
-#pragma unroll
-            for (int r = 0; r < 4; r++) f[r] = up2(lf[ix[r]]);
-            for (int gq = 0; gq < op.ngrad; gq++) {
-                const double2 *dm = gq == 0 ? d0 : d1;
-                double sacc = 0;
-#pragma unroll
-                for (int r = 0; r < 4; r++)
-                    sacc += zdotr(f[r], zadd(zmul2(dm[4 * r], u[0], dm[4 * r + 1], u[1]),
-                                             zmul2(dm[4 * r + 2], u[2], dm[4 * r + 3], u[3])));
-                if (gq == 0) g0 += sacc;
-                else g1 += sacc;
-            }
-#pragma unroll
-            for (int r = 0; r < 4; r++)
-                lf[ix[r]] = down2(zadd(zmul2(mm[4 * r], f[0], mm[4 * r + 1], f[1]), zmul2(mm[4 * r + 2], f[2], mm[4 * r + 3], f[3])));
-        }
-    } else if (op.kind == K_P2) {
-        const double2 ca = m[0], cb = m[1];
+        return;
+    }
+    case K_M2:
+        TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
+            rm2<R, lo_, hi_>(a, m);
+            if (op.ngrad > 0) g0 += rm2_dot<R, lo_, hi_>(a, f, d0);
+            if (op.ngrad > 1) g1 += rm2_dot<R, lo_, hi_>(a, f, d1);
+            rm2<R, lo_, hi_>(f, m);
+        }))
+        return;
+    case K_F2:
+        TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
+            rf2<R, lo_, hi_>(a, m);
+            if (op.ngrad > 0) g0 += rf2_dot<R, lo_, hi_>(a, f, d0);
+            if (op.ngrad > 1) g1 += rf2_dot<R, lo_, hi_>(a, f, d1);
+            rf2<R, lo_, hi_>(f, m);
+        }))
+        return;
+    case K_P2: {
         const double sg = op.ptype == 2 ? -1.0 : 1.0;
-        const int b0 = op.l0, b1 = op.l1;
-        const int lo = min(b0, b1), hi = max(b0, b1);
-        for (uint32_t p = tid; p < T / 4; p += nt) {
-            uint32_t i00 = ins0(ins0(p, lo), hi);
-            uint32_t i01 = i00 | (1u << b1), i10 = i00 | (1u << b0), i11 = i01 | (1u << b0);
-            Quad v{up2(lp[i00]), up2(lp[i01]), up2(lp[i10]), up2(lp[i11])};
-            Quad u = p2_apply(ca, cb, sg, v);
-            lp[i00] = down2(u.v00);
-            lp[i01] = down2(u.v01);
-            lp[i10] = down2(u.v10);
-            lp[i11] = down2(u.v11);
-            Quad f{up2(lf[i00]), up2(lf[i01]), up2(lf[i10]), up2(lf[i11])};
+        const double2 ca = m[0], cb = m[1];
+        TQ_PAIR_SWITCH(R, min(op.s0, op.s1), max(op.s0, op.s1), ({
+            rp2<R, lo_, hi_>(a, ca, cb, sg);
+            if (op.ngrad > 0) g0 += rp2_dot<R, lo_, hi_>(a, f, d0[0], d0[1], sg);
+            rp2<R, lo_, hi_>(f, ca, cb, sg);
+        }))
+        return;
+    }
+    default: {
+        const DiagPlan d = diag_plan(op, base, fb);
+        reg_diag<R>(d, m, a);
+        if (op.ngrad > 0) g0 += reg_diag_dot<R>(d, d0, a, f);
+        if (op.ngrad > 1) g1 += reg_diag_dot<R>(d, d1, a, f);
+        reg_diag<R>(d, m, f);
+        return;
+    }
+    }
+}
+
+// LDS offsets of a stage's register elements
+template <int R> __device__ __forceinline__ void stage_offsets(const Stage &st, uint32_t *off)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        uint32_t o = 0;
+#pragma unroll
+        for (int j = 0; j < R; j++)
+            if ((k >> j) & 1) o |= 1u << st.bits[j];
+        off[k] = o;
+    }
+}
+
+template <int R> __device__ __forceinline__ uint32_t stage_base(const Stage &st, uint32_t item)
+{
+    uint32_t base = item;
+#pragma unroll
+    for (int j = 0; j < R; j++) base = ins0(base, st.bits[j]);
+    return base;
+}
+
+// One forward stage over a tile of 2^t amplitudes in LDS.  M holds the
+// matrices from row-block offset mbase on.
+template <int R>
+__device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lds, int t, uint64_t fb)
+{
+    uint32_t off[1 << R];
+    stage_offsets<R>(st, off);
+    const uint32_t nitems = 1u << (t - R);
+    for (uint32_t item = threadIdx.x; item < nitems; item += blockDim.x) {
+        const uint32_t base = stage_base<R>(st, item);
+        double2 a[1 << R];
+#pragma unroll
+        for (int k = 0; k < (1 << R); k++) a[k] = up2(lds[sw(base | off[k])]);
+        for (int oi = st.op_begin; oi < st.op_end; oi++) {
+            const PassOp op = ops[oi];
+            reg_op<R>(op, M + (op.mat - mbase), a, base, fb);
+        }
+#pragma unroll
+        for (int k = 0; k < (1 << R); k++) lds[sw(base | off[k])] = down2(a[k]);
+    }
+}
+
+__device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lds, int t, uint64_t fb)
+{
+    switch (st.r) {
+    case 4:
+        if constexpr (kStageBitsFwd >= 4) run_stage<4>(st, ops, M, mbase, lds, t, fb);
+        break;
+    case 3: run_stage<3>(st, ops, M, mbase, lds, t, fb); break;
+    case 2: run_stage<2>(st, ops, M, mbase, lds, t, fb); break;
+    case 1: run_stage<1>(st, ops, M, mbase, lds, t, fb); break;
+    default: run_stage<0>(st, ops, M, mbase, lds, t, fb); break;
+    }
+}
+
+// One reverse stage on the psi and phi tiles.  Every thread runs the same
+// number of item iterations so that the wavefront reductions of the gradient
+// contributions see whole waves; acc[wave * astride + slot - abase].
+template <int R>
+__device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lp, float2 *lf,
+                              int t, uint64_t fb, double *acc, int astride, int abase)
+{
+    uint32_t off[1 << R];
+    stage_offsets<R>(st, off);
+    const uint32_t nitems = 1u << (t - R);
+    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+    const uint32_t iters = (nitems + blockDim.x - 1) / blockDim.x;
+    for (uint32_t it = 0; it < iters; it++) {
+        const uint32_t item = it * blockDim.x + threadIdx.x;
+        const bool active = item < nitems;
+        const uint32_t base = stage_base<R>(st, active ? item : 0);
+        double2 a[1 << R], f[1 << R];
+#pragma unroll
+        for (int k = 0; k < (1 << R); k++) {
+            a[k] = active ? up2(lp[sw(base | off[k])]) : make_double2(0, 0);
+            f[k] = active ? up2(lf[sw(base | off[k])]) : make_double2(0, 0);
+        }
+        for (int oi = st.op_begin; oi < st.op_end; oi++) {
+            const PassOp op = ops[oi];
+            const double2 *m = M + (op.mat - mbase);
+            const double2 *d0 = M + (op.ngrad > 0 ? op.dmat[0] - mbase : 0);
+            const double2 *d1 = M + (op.ngrad > 1 ? op.dmat[1] - mbase : 0);
+            double g0 = 0, g1 = 0;
+            reg_rev_op<R>(op, m, d0, d1, a, f, base, fb, g0, g1);
             if (op.ngrad > 0) {
-                Quad e = p2_apply(d0[0], d0[1], sg, u);
-                g0 += zdotr(f.v00, e.v00) + zdotr(f.v01, e.v01) + zdotr(f.v10, e.v10) + zdotr(f.v11, e.v11);
+                const double v = wave_sum(active ? g0 : 0.0);
+                if (lane == 0) acc[wave * astride + op.gslot[0] - abase] += v;
             }
-            Quad o = p2_apply(ca, cb, sg, f);
-            lf[i00] = down2(o.v00);
-            lf[i01] = down2(o.v01);
-            lf[i10] = down2(o.v10);
-            lf[i11] = down2(o.v11);
+            if (op.ngrad > 1) {
+                const double v = wave_sum(active ? g1 : 0.0);
+                if (lane == 0) acc[wave * astride + op.gslot[1] - abase] += v;
+            }
         }
-    } else {
-        for (uint32_t l = tid; l < T; l += nt) {
-            const int idx = diag_index(op, l, fb);
-            const double2 dg = m[idx];
-            double2 u = zmul(dg, up2(lp[l]));
-            lp[l] = down2(u);
-            double2 f = up2(lf[l]);
-            if (op.ngrad > 0) g0 += zdotr(f, zmul(d0[idx], u));
-            if (op.ngrad > 1) g1 += zdotr(f, zmul(d1[idx], u));
-            lf[l] = down2(zmul(dg, f));
+        if (active) {
+#pragma unroll
+            for (int k = 0; k < (1 << R); k++) {
+                lp[sw(base | off[k])] = down2(a[k]);
+                lf[sw(base | off[k])] = down2(f[k]);
+            }
         }
+    }
+}
+
+__device__ __forceinline__ void run_rev_stage_any(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lp, float2 *lf,
+                                  int t, uint64_t fb, double *acc, int astride, int abase)
+{
+    switch (st.r) {
+    case 3:
+        if constexpr (kStageBitsRev >= 3) run_rev_stage<3>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase);
+        break;
+    case 2: run_rev_stage<2>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
+    case 1: run_rev_stage<1>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
+    default: run_rev_stage<0>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
     }
 }
 
@@ -622,14 +987,14 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
                 f = zmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
             }
             for (int l = threadIdx.x; l < T; l += blockDim.x)
-                lds[l] = down2(zmul(f, zmul(p1[l & ((1 << a1) - 1)], p2[l >> a1])));
+                lds[sw(l)] = down2(zmul(f, zmul(p1[l & ((1 << a1) - 1)], p2[l >> a1])));
         } else {
             tile_copy<true>(tc, lds, st, fb, T);
         }
         __syncthreads();
-        for (int oi = 0; oi < a.nops; oi++) {
-            const PassOp op = a.ops[oi];
-            apply_op(op, M + (op.mat - a.mat_begin), lds, t, fb);
+        for (int si = 0; si < a.nstages; si++) {
+            const Stage st = a.stages[si];
+            run_stage_any(st, a.ops, M, a.mat_begin, lds, t, fb);
             __syncthreads();
         }
         tile_copy<false>(tc, lds, st, fb, T);
@@ -664,7 +1029,7 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
     if (tm.x == 0) {
         const int zf = par64(fb & tm.z);
         for (uint32_t l = tid; l < T; l += nt) {
-            double2 v = up2(lds[l]);
+            double2 v = up2(lds[sw(l)]);
             double pr = v.x * v.x + v.y * v.y;
             acc += ((zf ^ par32(l & tm.zl)) ? -pr : pr);
         }
@@ -673,7 +1038,7 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
         const int mb = __ffs(tm.xl) - 1;
         for (uint32_t p = tid; p < T / 2; p += nt) {
             uint32_t i = ins0(p, mb), j = i ^ tm.xl;
-            double2 a = up2(lds[i]), c = up2(lds[j]);
+            double2 a = up2(lds[sw(i)]), c = up2(lds[sw(j)]);
             double2 A = make_double2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);  // conj(a) c
             double s = (zf ^ par32(j & tm.zl)) ? -2.0 : 2.0;
             acc += re_iny(tm.ny, s, A);
@@ -685,7 +1050,7 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
         const int zf = par64(fj & tm.z);
         for (uint32_t l = tid; l < T; l += nt) {
             uint32_t lj = l ^ tm.xl;
-            double2 a = up2(lds[l]), c = up2(row[tile_index(tc, fj, lj)]);
+            double2 a = up2(lds[sw(l)]), c = up2(row[tile_index(tc, fj, lj)]);
             double2 A = make_double2(a.x * c.x + a.y * c.y, a.x * c.y - a.y * c.x);
             double s = (zf ^ par32(lj & tm.zl)) ? -2.0 : 2.0;
             acc += re_iny(tm.ny, s, A);
@@ -766,7 +1131,7 @@ __device__ __forceinline__ float2 h_elem(uint32_t l, uint64_t fb, const TermDev 
         const TermDev tm = terms[k];
         const uint32_t lj = l ^ tm.xl;
         const uint64_t fj = fb ^ tm.xout;
-        float2 v = tm.xout == 0 ? lds[lj] : ps[tile_index(tc, fj, lj)];
+        float2 v = tm.xout == 0 ? lds[sw(lj)] : ps[tile_index(tc, fj, lj)];
         double cf = tm.coeff * (double)up[tm.k];
         if (par64(fj & tm.z) ^ par32(lj & tm.zl)) cf = -cf;
         double vx = v.x, vy = v.y;
@@ -841,18 +1206,9 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         tile_copy<true>(tc, lp, sp, fb, T);
         tile_copy<true>(tc, lf, sf, fb, T);
         __syncthreads();
-        for (int oi = 0; oi < a.nops; oi++) {
-            const PassOp op = a.ops[oi];
-            double g0 = 0, g1 = 0;
-            rev_op(op, lm, a.mat_begin, lp, lf, t, fb, g0, g1);
-            if (op.ngrad > 0) {
-                double v = wave_sum(g0);
-                if (lane == 0) acc[wave * a.gcount + (op.gslot[0] - a.gbase)] += v;
-            }
-            if (op.ngrad > 1) {
-                double v = wave_sum(g1);
-                if (lane == 0) acc[wave * a.gcount + (op.gslot[1] - a.gbase)] += v;
-            }
+        for (int si = 0; si < a.nstages; si++) {
+            const Stage st = a.stages[si];
+            run_rev_stage_any(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase);
             __syncthreads();
         }
         if (a.store) {
@@ -916,19 +1272,19 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
     for (uint32_t l = tid; l < T; l += nt) {
         double2 v = make_double2(1.0, 0.0);
         for (int q = 0; q < n; q++) v = zmul(v, lm[a.init_mat[q] + (((l >> (n - 1 - q)) & 1) ? 2 : 0)]);
-        lp[l] = down2(v);
+        lp[sw(l)] = down2(v);
     }
     __syncthreads();
     // 3. forward gates
-    for (int oi = 0; oi < a.nfops; oi++) {
-        const PassOp op = a.fops[oi];
-        apply_op(op, lm + op.mat, lp, n, 0);
+    for (int si = 0; si < a.nfstages; si++) {
+        const Stage st = a.fstages[si];
+        run_stage_any(st, a.fops, lm, 0, lp, n, 0);
         __syncthreads();
     }
     // 4. state output and expectation terms
     if (a.state_out) {
         float2 *out = a.state_out + (int64_t)a.out_rows[row] * a.out_stride;
-        for (uint32_t l = tid; l < T; l += nt) out[l] = lp[l];
+        for (uint32_t l = tid; l < T; l += nt) out[l] = lp[sw(l)];
     }
     const TermDev *terms = a.terms ? a.terms + a.row_term_begin[row] : nullptr;
     const int nterm = a.terms ? a.row_term_count[row] : 0;
@@ -939,20 +1295,11 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
     // 5. adjoint sweep
     if (a.grad) {
         const float *up = a.upstream + (int64_t)b * a.K;
-        for (uint32_t l = tid; l < T; l += nt) lf[l] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
+        for (uint32_t l = tid; l < T; l += nt) lf[sw(l)] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
         __syncthreads();
-        for (int oi = 0; oi < a.nrops; oi++) {
-            const PassOp op = a.rops[oi];
-            double g0 = 0, g1 = 0;
-            rev_op(op, lm, 0, lp, lf, n, 0, g0, g1);
-            if (op.ngrad > 0) {
-                double v = wave_sum(g0);
-                if (lane == 0) acc[wave * a.nacc + a.gacc + op.gslot[0]] += v;
-            }
-            if (op.ngrad > 1) {
-                double v = wave_sum(g1);
-                if (lane == 0) acc[wave * a.nacc + a.gacc + op.gslot[1]] += v;
-            }
+        for (int si = 0; si < a.nrstages; si++) {
+            const Stage st = a.rstages[si];
+            run_rev_stage_any(st, a.rops, lm, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc);
             __syncthreads();
         }
     }

@@ -59,7 +59,7 @@ bool op_shape(int op, int &nq, int &np)
 }
 
 // Gate classes as the tile passes see them.
-enum Cls { C_1D, C_1M, C_CTRL, C_2D, C_2M, C_2P };
+enum Cls { C_1D, C_1M, C_CTRL, C_2D, C_2M, C_2P, C_2F };
 
 int classify(int op)
 {
@@ -72,7 +72,9 @@ int classify(int op)
         return C_2D;
     case OP_XXPOW: case OP_YYPOW:
         return C_2P;
-    case OP_FSIM: case OP_MATRIX2: case OP_SWAP:
+    case OP_FSIM: case OP_SWAP:
+        return C_2F;
+    case OP_MATRIX2:
         return C_2M;
     default:
         return C_1M;
@@ -112,14 +114,21 @@ struct Sched {
 // deferred and blocks its qubits.  The free tile bits are then filled with
 // the targets of the earliest deferred gates and the scan is repeated with
 // the tile fixed, so that the pass takes every gate that became possible.
-std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n, int t, int c)
+std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n, int t, int c, int cap)
 {
     std::vector<Sched> out;
     if (n <= t) {
         Sched s;
         for (int b = 0; b < n; b++) s.bits.push_back(b);
-        s.items = items;
-        out.push_back(s);
+        if (cap <= 0) {
+            s.items = items;
+            out.push_back(s);
+        } else {
+            for (size_t i = 0; i < items.size(); i += cap) {
+                s.items.assign(items.begin() + i, items.begin() + std::min(items.size(), i + cap));
+                out.push_back(s);
+            }
+        }
         return out;
     }
     auto pos = [n](int q) { return n - 1 - q; };
@@ -178,6 +187,15 @@ std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n
             }
         }
         if (s.items.empty()) fail(TQ_E_UNSUPPORTED, "planner made no progress");
+        if (cap > 0 && (int)s.items.size() > cap) {
+            // keep the first `cap` gates; everything else stays in order
+            std::vector<char> kept(g.gates.size(), 0);
+            s.items.resize(cap);
+            for (int gi : s.items) kept[gi] = 1;
+            deferred.clear();
+            for (int gi : remaining)
+                if (!kept[gi]) deferred.push_back(gi);
+        }
         out.push_back(std::move(s));
         remaining.swap(deferred);
     }
@@ -227,7 +245,7 @@ struct Planner {
         bt.dim = (uint8_t)dim;
         bt.diag = (uint8_t)storage;
         bt.which = (uint8_t)which;
-        bt.out = alloc(storage == 1 ? dim : storage >= 2 ? 2 : dim * dim);
+        bt.out = alloc(storage == 1 ? dim : storage == 4 ? 6 : storage >= 2 ? 2 : dim * dim);
         bt.mem_begin = (int32_t)g.members.size();
         bt.mem_count = (int32_t)mem.size();
         for (const auto &m : mem) g.members.push_back(m);
@@ -235,6 +253,76 @@ struct Planner {
         return (int)g.tasks.size() - 1;
     }
 };
+
+// Group a pass's ops into register stages: consecutive ops whose dense
+// (non-diagonal) tile bits fit a set R of at most rmax bits.  Diagonal ops and
+// control bits outside R read their bit from the item's base index.  R is
+// padded with the highest free tile bits, so that the items of neighbouring
+// lanes sit at neighbouring LDS addresses.
+void make_stages(Pass &ps, int rmax, Group &g, const std::map<int32_t, int> &task_at)
+{
+    const int t = ps.geom.t;
+    const int r = std::min(rmax, t);
+    ps.stages.clear();
+    std::vector<int> R;
+    int begin = 0;
+    auto close = [&](int end) {
+        if (end <= begin) return;
+        Stage st{};
+        std::vector<int> bits = R;
+        for (int b = t - 1; b >= 0 && (int)bits.size() < r; b--)
+            if (std::find(bits.begin(), bits.end(), b) == bits.end()) bits.push_back(b);
+        std::sort(bits.begin(), bits.end());
+        st.r = (uint8_t)r;
+        for (int j = 0; j < r; j++) st.bits[j] = (uint8_t)bits[j];
+        st.op_begin = ps.op_offset + begin;
+        st.op_end = ps.op_offset + end;
+        for (int k = begin; k < end; k++) {
+            PassOp &op = ps.ops[k];
+            auto idx = [&](uint8_t l) -> uint8_t {
+                for (int j = 0; j < r; j++)
+                    if (l != kFixed && bits[j] == l) return (uint8_t)j;
+                return kFixed;
+            };
+            op.s0 = idx(op.l0);
+            op.s1 = idx(op.l1);
+            // dense 4x4 ops are stored with their first qubit on the lower
+            // register bit: swap the op's qubits and its matrices' qubit order
+            if ((op.kind == K_M2 || op.kind == K_F2) && op.s0 > op.s1) {
+                std::swap(op.l0, op.l1);
+                std::swap(op.p0, op.p1);
+                std::swap(op.s0, op.s1);
+                std::vector<int32_t> outs{op.mat};
+                for (int j = 0; j < op.ngrad; j++) outs.push_back(op.dmat[j]);
+                for (int32_t o : outs) {
+                    const BuildTask &bt = g.tasks[task_at.at(o)];
+                    for (int mi = 0; mi < bt.mem_count; mi++) g.members[bt.mem_begin + mi].swapped ^= 1;
+                }
+            }
+        }
+        ps.stages.push_back(st);
+        R.clear();
+        begin = end;
+    };
+    for (int k = 0; k < (int)ps.ops.size(); k++) {
+        const PassOp &op = ps.ops[k];
+        std::vector<int> need;
+        if (op.kind == K_M1) need.push_back(op.l0);
+        if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2) {
+            need.push_back(op.l0);
+            need.push_back(op.l1);
+        }
+        std::vector<int> u = R;
+        for (int b : need)
+            if (std::find(u.begin(), u.end(), b) == u.end()) u.push_back(b);
+        if ((int)u.size() > r) {
+            close(k);
+            u = need;
+        }
+        R = u;
+    }
+    close((int)ps.ops.size());
+}
 
 // Append a pass, split into consecutive passes over the same tile when its
 // matrices would not fit the LDS staging area (op k owns the matrix entries
@@ -265,7 +353,10 @@ void push_split(std::vector<Pass> &out, Pass ps)
     out.push_back(std::move(cur));
 }
 
-int op_dim(const PassOp &op) { return (op.kind == K_M2 || op.kind == K_D2 || op.kind == K_P2) ? 4 : 2; }
+int op_dim(const PassOp &op)
+{
+    return (op.kind == K_M2 || op.kind == K_D2 || op.kind == K_P2 || op.kind == K_F2) ? 4 : 2;
+}
 
 // how the builder stores an op's matrix: 0 dense, 1 diagonal, 2 / 3 the
 // pair (a, b) of a I + b XX / a I + b YY
@@ -273,6 +364,7 @@ int storage_of(const PassOp &op)
 {
     if (op.kind == K_D1 || op.kind == K_D2) return 1;
     if (op.kind == K_P2) return op.ptype == 1 ? 2 : 3;
+    if (op.kind == K_F2) return 4;
     return 0;
 }
 
@@ -291,6 +383,7 @@ PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
         op.kind = K_P2;
         op.ptype = g.gates[gi].op == OP_XXPOW ? 1 : 2;
         break;
+    case C_2F: op.kind = K_F2; break;
     default: op.kind = K_M2; break;
     }
     if (cls == C_CTRL) {  // q0 field = target, q1 field = control
@@ -347,7 +440,7 @@ void plan_group(Group &g, const Options &opt, int S)
     std::vector<int> fitems;
     for (int gi = 0; gi < G; gi++)
         if (!is_absorbed[gi]) fitems.push_back(gi);
-    auto fs = schedule(g, fitems, n, opt.tile, opt.low);
+    auto fs = schedule(g, fitems, n, opt.tile, opt.low, opt.max_pass_gates);
     if (fs.empty()) {  // nothing beyond the product state: one generating pass
         Sched s;
         for (int b = 0; b < std::min(n, opt.tile); b++) s.bits.push_back(b);
@@ -379,7 +472,7 @@ void plan_group(Group &g, const Options &opt, int S)
                     continue;
                 }
             }
-            if (opt.fuse && (cls == C_2D || cls == C_2M || cls == C_2P)) {
+            if (opt.fuse && (cls == C_2D || cls == C_2M || cls == C_2P || cls == C_2F)) {
                 int o = last[q0];
                 if (o >= 0 && last[q1] == o && ops[o].qb >= 0 &&
                     ((ops[o].qa == q0 && ops[o].qb == q1) || (ops[o].qa == q1 && ops[o].qb == q0))) {
@@ -387,8 +480,15 @@ void plan_group(Group &g, const Options &opt, int S)
                     // products of a I + b P with one P keep that form (P^2 = I,
                     // and P is symmetric in its two qubits); anything else is dense
                     const uint8_t pt = g.gates[gi].op == OP_XXPOW ? 1 : 2;
-                    if (cls == C_2P && ops[o].op.kind == K_P2 && ops[o].op.ptype == pt) continue;
-                    ops[o].op.kind = (cls == C_2D && ops[o].op.kind == K_D2) ? K_D2 : K_M2;
+                    const uint8_t k = ops[o].op.kind;
+                    if (cls == C_2P && k == K_P2 && ops[o].op.ptype == pt) continue;
+                    // diagonal and excitation-preserving gates stay in their classes
+                    if (cls == C_2D && k == K_D2) continue;
+                    if ((cls == C_2D || cls == C_2F) && (k == K_D2 || k == K_F2)) {
+                        ops[o].op.kind = K_F2;
+                        continue;
+                    }
+                    ops[o].op.kind = K_M2;
                     continue;
                 }
             }
@@ -420,7 +520,7 @@ void plan_group(Group &g, const Options &opt, int S)
     std::vector<int> ritems;
     for (int gi = G - 1; gi >= 0; gi--) ritems.push_back(gi);
     int trev = std::min(opt.tile, 12);
-    auto rs0 = schedule(g, ritems, n, trev, std::min(opt.low, trev - 2));
+    auto rs0 = schedule(g, ritems, n, trev, std::min(opt.low, trev - 2), opt.max_pass_gates);
     // the reverse kernel keeps per-wave accumulators of every gradient slot of
     // a pass in LDS: split passes that would hold too many
     std::vector<Sched> rs;
@@ -469,13 +569,30 @@ void plan_group(Group &g, const Options &opt, int S)
     }
     g.rev_tasks.end = (int)g.tasks.size();
 
+    // register stages of every pass
+    std::map<int32_t, int> task_at;
+    for (int i = 0; i < (int)g.tasks.size(); i++) task_at[g.tasks[i].out] = i;
+    int off = 0;
+    for (Pass &ps : g.fwd) {
+        ps.op_offset = off;
+        make_stages(ps, kStageBitsFwd, g, task_at);
+        off += (int)ps.ops.size();
+    }
+    off = 0;
+    for (Pass &ps : g.rev) {
+        ps.op_offset = off;
+        make_stages(ps, kStageBitsRev, g, task_at);
+        off += (int)ps.ops.size();
+    }
+
     // every dense op must find its target bits in the tile
     for (const std::vector<Pass> *pv : {&g.fwd, &g.rev})
         for (const Pass &ps : *pv)
             for (const PassOp &op : ps.ops) {
                 bool ok = true;
                 if (op.kind == K_M1) ok = op.l0 < ps.geom.t && (!op.ctrl || op.l1 == kFixed || op.l1 < ps.geom.t);
-                if (op.kind == K_M2 || op.kind == K_P2) ok = op.l0 < ps.geom.t && op.l1 < ps.geom.t && op.l0 != op.l1;
+                if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2)
+                    ok = op.l0 < ps.geom.t && op.l1 < ps.geom.t && op.l0 != op.l1;
                 if (op.kind == K_D1 || op.kind == K_D2) ok = op.p0 < n && (op.kind == K_D1 || op.p1 < n);
                 if (!ok) fail(TQ_E_UNSUPPORTED, "internal planner error: op outside its tile");
             }

@@ -19,6 +19,7 @@ struct Options {
     int tile = 12;    // forward tile bits
     int low = 6;      // contiguous low bits per tile
     bool fuse = true;
+    int max_pass_gates = 0;  // 0: no limit
 };
 
 struct HGate {
@@ -40,6 +41,8 @@ struct Pass {
     std::vector<PassOp> ops;
     bool product_init = false;
     int32_t mat_begin = 0, mat_end = 0;  // the pass's matrices in the row block
+    int32_t op_offset = 0;               // index of the pass's first op in the group's op array
+    std::vector<Stage> stages;           // op indices relative to the group's op array
 };
 
 // Build-task ranges of a group: [begin, end) into Group::tasks.

@@ -82,8 +82,9 @@ struct ObsGroupDev {
 
 struct GroupDev {
     DevBuf rows, ident, gates, slot_sym, scale, off, explicit_, tasks, members, fwd_ops, rev_ops, sym_begin,
-        sym_gslots, gslot_slot;
-    std::vector<int> fwd_op_off, rev_op_off;
+        sym_gslots, gslot_slot, fwd_stages, rev_stages;
+    std::vector<int> fwd_op_off, rev_op_off, fwd_stage_off, rev_stage_off;
+    int n_fwd_stages = 0, n_rev_stages = 0;
     size_t psi_off = 0;  // amplitude offset of this group's rows in the state workspaces
     size_t mat_off = 0;  // offset in the matrix workspace
 };
@@ -108,7 +109,7 @@ struct tq_program_s {
         for (auto &g : gdev) {
             for (DevBuf *b : {&g->rows, &g->ident, &g->gates, &g->slot_sym, &g->scale, &g->off, &g->explicit_,
                               &g->tasks, &g->members, &g->fwd_ops, &g->rev_ops, &g->sym_begin, &g->sym_gslots,
-                              &g->gslot_slot})
+                              &g->gslot_slot, &g->fwd_stages, &g->rev_stages})
                 b->release();
         }
         for (auto &o : obs_dev) {
@@ -176,6 +177,19 @@ void ensure_device(tq_program p)
         }
         upload(gd->fwd_ops, fo);
         upload(gd->rev_ops, ro);
+        std::vector<Stage> fs, rs;
+        for (const Pass &ps : g.fwd) {
+            gd->fwd_stage_off.push_back((int)fs.size());
+            fs.insert(fs.end(), ps.stages.begin(), ps.stages.end());
+        }
+        for (const Pass &ps : g.rev) {
+            gd->rev_stage_off.push_back((int)rs.size());
+            rs.insert(rs.end(), ps.stages.begin(), ps.stages.end());
+        }
+        gd->n_fwd_stages = (int)fs.size();
+        gd->n_rev_stages = (int)rs.size();
+        upload(gd->fwd_stages, fs);
+        upload(gd->rev_stages, rs);
         upload(gd->sym_begin, g.sym_gslot_begin);
         upload(gd->sym_gslots, g.sym_gslots);
         upload(gd->gslot_slot, g.gslot_slot);
@@ -235,8 +249,9 @@ void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const i
         a.rows = srows;
         a.mats = mat_ws(p) + gd.mat_off;
         a.mat_stride = std::max(g.mat_block, 1);
-        a.ops = (const PassOp *)gd.fwd_ops.p + gd.fwd_op_off[pi];
-        a.nops = (int)ps.ops.size();
+        a.ops = (const PassOp *)gd.fwd_ops.p;
+        a.stages = (const Stage *)gd.fwd_stages.p + gd.fwd_stage_off[pi];
+        a.nstages = (int)ps.stages.size();
         a.g = ps.geom;
         a.tiles_log2 = g.n - ps.geom.t;
         a.wg_per_row = wg_for(nrows, a.tiles_log2);
@@ -406,11 +421,12 @@ ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint,
     a.mat_block = std::max(adjoint ? g.mat_block : g.fwd_mat_end, 1);
     a.n = g.n;
     a.fops = (const PassOp *)gd.fwd_ops.p;
-    a.nfops = 0;
-    for (const Pass &ps : g.fwd) a.nfops += (int)ps.ops.size();
+    a.fstages = (const Stage *)gd.fwd_stages.p;
+    a.nfstages = gd.n_fwd_stages;
     for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
     a.rops = (const PassOp *)gd.rev_ops.p;
-    for (const Pass &ps : g.rev) a.nrops += (int)ps.ops.size();
+    a.rstages = (const Stage *)gd.rev_stages.p;
+    a.nrstages = gd.n_rev_stages;
     a.sym_begin = (const int32_t *)gd.sym_begin.p;
     a.sym_gslots = (const int32_t *)gd.sym_gslots.p;
     a.gslot_slot = (const int32_t *)gd.gslot_slot.p;
@@ -495,6 +511,8 @@ tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *o
                 o.low = opt->low_qubits;
             }
             if (opt->fuse < 0) o.fuse = false;
+            if (opt->max_pass_gates < 0) fail(TQ_E_INVALID, "max_pass_gates must be >= 0");
+            o.max_pass_gates = opt->max_pass_gates;
         }
         if (o.low > o.tile - 2) o.low = o.tile - 2;
         auto p = std::make_unique<tq_program_s>();
@@ -677,8 +695,9 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                 r.rows = (const int32_t *)gd.ident.p;
                 r.mats = mat_ws(prog) + gd.mat_off;
                 r.mat_stride = std::max(g.mat_block, 1);
-                r.ops = (const PassOp *)gd.rev_ops.p + gd.rev_op_off[pi];
-                r.nops = (int)ps.ops.size();
+                r.ops = (const PassOp *)gd.rev_ops.p;
+                r.stages = (const Stage *)gd.rev_stages.p + gd.rev_stage_off[pi];
+                r.nstages = (int)ps.stages.size();
                 r.g = ps.geom;
                 r.tiles_log2 = g.n - ps.geom.t;
                 r.wg_per_row = wg;
@@ -829,7 +848,7 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
         if (!prog) fail(TQ_E_INVALID, "program is NULL");
         const ProgramData &pd = *prog->pd;
         std::ostringstream o;
-        static const char *kinds[] = {"?", "M1", "M2", "D1", "D2", "P2"};
+        static const char *kinds[] = {"?", "M1", "M2", "D1", "D2", "P2", "F2"};
         o << "{\"B\":" << pd.B << ",\"S\":" << pd.S << ",\"nmax\":" << pd.nmax << ",\"tile\":" << pd.opt.tile
           << ",\"low\":" << pd.opt.low << ",\"groups\":[";
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {

@@ -52,7 +52,8 @@ enum TaskKind : uint8_t {
 struct BuildTask {
     uint8_t kind;
     uint8_t dim;    // 2 or 4
-    uint8_t diag;   // store only the diagonal (dim entries); 2 = store (a, b) of a I + b XX, 3 = of a I + b YY
+    uint8_t diag;   // storage: 0 dense, 1 diagonal (dim entries), 2 / 3 the pair (a, b) of
+                    // a I + b XX / a I + b YY, 4 the six entries of an excitation-preserving 4x4
     uint8_t which;  // BT_DERIV parameter index
     int32_t out;    // offset (complex entries) in the row's matrix block
     int32_t mem_begin, mem_count;
@@ -65,6 +66,8 @@ enum OpKind : uint8_t {
     K_D1 = 3, // diagonal on q0 (local or fixed)
     K_D2 = 4, // diagonal on (q0, q1), entry index 2*bit(q0) + bit(q1)
     K_P2 = 5, // a I + b P on local bits (q0, q1) with P = XX (ptype 1) or YY (ptype 2)
+    K_F2 = 6, // excitation preserving on local bits (q0, q1): phase on |00>, 2x2 block on
+              // (|01>, |10>), phase on |11> (fSim, SWAP and their products with diagonals)
 };
 
 struct PassOp {
@@ -75,10 +78,24 @@ struct PassOp {
     uint8_t cval;     // K_M1: the control value that enables the op
     uint8_t ngrad;    // reverse ops: symbolic parameters (0..2)
     uint8_t ptype;    // K_P2: 1 = XX, 2 = YY
-    uint8_t pad[3];
+    uint8_t s0, s1;   // register index of q0 / q1 within the op's stage, kFixed if not in it
+    uint8_t pad;
     int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
     int32_t dmat[2];  // reverse: offsets of dW/deta_j
     int32_t gslot[2]; // reverse: gradient slot ids
+};
+
+// A stage: consecutive ops of a pass whose dense qubits lie in a set R of at
+// most kStageBits tile bits.  Each thread holds the 2^r amplitudes of one
+// "item" (a fixed assignment of the tile bits outside R) in registers while
+// the stage's ops run, so the stage costs one LDS round trip.
+constexpr int kStageBitsFwd = 4;
+constexpr int kStageBitsRev = 2;
+struct Stage {
+    uint8_t r;        // register bits
+    uint8_t bits[4];  // their tile-local positions, ascending
+    uint8_t pad[3];
+    int32_t op_begin, op_end;  // ops, as indices into the group's op array
 };
 
 // Tile geometry of a pass: t local bits = `c` low bits + high bits hb[].

@@ -27,7 +27,7 @@ class TQError(RuntimeError):
 
 class _Options(ctypes.Structure):
     _fields_ = [("max_tile_qubits", ctypes.c_int32), ("low_qubits", ctypes.c_int32),
-                ("fuse", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("fuse", ctypes.c_int32), ("max_pass_gates", ctypes.c_int32)]
 
 
 _lib = None
@@ -97,8 +97,8 @@ def _dev(t, dtype, shape, name):
 class Program:
     """A parsed and planned batch of circuits (``tq_program``)."""
 
-    def __init__(self, blob: bytes, max_tile_qubits=0, low_qubits=0, fuse=True):
-        opt = _Options(max_tile_qubits, low_qubits, 1 if fuse else -1, 0)
+    def __init__(self, blob: bytes, max_tile_qubits=0, low_qubits=0, fuse=True, max_pass_gates=0):
+        opt = _Options(max_tile_qubits, low_qubits, 1 if fuse else -1, max_pass_gates)
         h = ctypes.c_void_p()
         _check(lib().tq_program_create(blob, len(blob), ctypes.byref(opt), ctypes.byref(h)))
         self._h = h
