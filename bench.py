@@ -23,7 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "effective HBM GB/s per fused-gate pass; circuit-expectations/sec at batch"
-KERNELS = ("build", "resident", "pass", "expect", "expect_reduce", "apply_h", "rev_pass", "grad_reduce",
+KERNELS = ("build", "resident", "pass", "pauli", "pauli_reduce", "rev_pass", "grad_reduce",
            "samp_l1", "samp_shots", "gather")
 PEAK_HBM_GBS = 8000.0
 PEAK_FP32_TFLOPS = 157.3
@@ -84,7 +84,7 @@ def kernel_work(plan, kernel, n_obs_terms, adjoint):
     and the number of those launches, from the program's plan.  Per amplitude:
     a forward op costs its matvec (op_flops), a reverse op two matvecs (psi
     and phi) plus one matvec and a 4-flop dot product per symbolic parameter,
-    an expectation term 4 flops, an H_g term 8 flops."""
+    an expectation term 4 flops, an H_g term 4 more."""
     flops = bytes_ = 0.0
     launches = 0
     for g in plan["groups"]:
@@ -113,14 +113,12 @@ def kernel_work(plan, kernel, n_obs_terms, adjoint):
                     f += 2 * base + op["ngrad"] * (base + 4.0)
                 flops += f * amps
                 bytes_ += (32.0 if i + 1 < len(g["rev"]) else 16.0) * amps
-        elif kernel == "expect":
+        elif kernel == "pauli":
+            # one sweep: expectations (4 flops per term and amplitude), and
+            # with the adjoint also phi = H_g psi (4 more, and phi written)
             launches += 1
-            flops += 4.0 * n_obs_terms * amps
-            bytes_ += 8.0 * amps
-        elif kernel == "apply_h":
-            launches += 1
-            flops += 8.0 * n_obs_terms * amps
-            bytes_ += 16.0 * amps
+            flops += (8.0 if adjoint else 4.0) * n_obs_terms * amps
+            bytes_ += (16.0 if adjoint else 8.0) * amps
     return flops, bytes_, launches
 
 
@@ -269,6 +267,24 @@ def sweep(steps):
     from paper_2003_02989_amd.circuits import Circuit, const, observable_blob, program_blob
 
     G = 8
+    tile = int(os.environ.get("TQ_SWEEP_TILE", "0"))
+
+    # plain device copy of the same footprint: the practical HBM ceiling
+    for n in (26, 30):
+        B = max(1, (1 << 27) >> n)
+        src = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        gbs = 16.0 * (1 << n) * B / (ms * 1e-3) / 1e9
+        print(json.dumps({"sweep": "device_copy", "n": n, "batch": B, "case": "torch copy_", "ms": ms,
+                          "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
+        del src, dst
 
     def pass_ms(n, B, prefix, gate):
         times = []
@@ -282,7 +298,7 @@ def sweep(steps):
                     for _ in range(G):
                         c.add(*gate)
                 circuits.append(c)
-            prog = tq.Program(program_blob(circuits, 0), max_pass_gates=1)
+            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=1)
             st = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
             tq.simulate_state(prog, None, out=st)
             torch.cuda.synchronize()
@@ -330,7 +346,7 @@ def sweep(steps):
             out = torch.empty((B, 1), dtype=torch.float32, device="cuda")
             tq.expectation(prog, None, obs, out=out)
             torch.cuda.synchronize()
-            tq.profile_start("expect")
+            tq.profile_start("pauli")
             for _ in range(steps):
                 tq.expectation(prog, None, obs, out=out)
             torch.cuda.synchronize()

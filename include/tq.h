@@ -168,7 +168,7 @@ tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t
 tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *needed);
 
 /* Kernel timing for benchmarks.  After tq_profile_start(name) every launch of
- * the named kernel ("build", "pass", "expect", "expect_reduce", "apply_h",
+ * the named kernel ("build", "resident", "pass", "pauli", "pauli_reduce",
  * "rev_pass", "grad_reduce", "samp_l1", "samp_shots", "gather") is bracketed
  * by a pair of HIP events recorded on its launch stream; NULL or "" stops
  * recording.  tq_profile_read waits for the recorded events, returns the

@@ -6,7 +6,6 @@
 
 namespace tq {
 
-constexpr int kTermChunk = 256;  // terms whose partial sums one expectation sweep accumulates
 constexpr int kMaxLevels = 8;    // sampler levels (64-ary), enough for 2^48 amplitudes
 
 struct BuildArgs {
@@ -42,39 +41,32 @@ struct PassArgs {
     int mat_begin, mat_end;  // the pass's matrices, staged in LDS
 };
 
-struct ExpArgs {
-    const float2 *state;
-    int64_t row_stride;
-    const int32_t *rows;
-    const TermDev *terms;
-    const int32_t *row_term_begin, *row_term_count;
-    TileGeom g;
-    int tiles_log2, wg_per_row;
-    double *partial;  // [nrows][wg_per_row][tmax]
-    int tmax;
-};
-
-struct ExpReduceArgs {
-    const int32_t *rows;
-    const TermDev *terms;
-    const int32_t *row_term_begin, *row_term_count;
-    const double *partial;
-    int wg_per_row, tmax, K;
-    float *out;
-};
-
-struct HArgs {
+struct PauliArgs {
     const float2 *psi;
-    float2 *phi;
+    float2 *phi;             // NULL: expectations only
+    int phi_accumulate;      // add into phi instead of overwriting it
     int64_t row_stride;
-    const int32_t *rows;   // state rows
-    const int32_t *brows;  // batch index of each row (upstream)
-    const TermDev *terms;
-    const int32_t *row_term_begin, *row_term_count;
-    const float *upstream;
-    int K;
+    const int32_t *rows;     // state rows
+    const int32_t *brows;    // batch index of each row (upstream)
+    const PChunk *chunks;
+    const int32_t *row_chunk_begin, *row_chunk_count;
+    const PXfGroup *xfg;
+    const PXGroup *xg;
+    const PUSub *us;
+    const PTerm *terms;
+    const float *upstream;   // [B, K] (phi only)
+    int K;                   // observables per row (upstream stride)
+    int k_begin, k_count;    // observables of this launch
     TileGeom g;
     int tiles_log2, wg_per_row;
+    double *partial;         // [nrows][wg_per_row][k_count]
+};
+
+struct PauliReduceArgs {
+    const int32_t *rows;     // batch index of each row
+    const double *partial;
+    int wg_per_row, K, k_begin, k_count;
+    float *out;
 };
 
 struct RevArgs {
@@ -170,9 +162,11 @@ size_t resident_lds_bytes(int n, int nmat, int nacc, bool adjoint);
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
-hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s);
-hipError_t launch_expect_reduce(const ExpReduceArgs &a, int nrows, hipStream_t s);
-hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s);
+// Tiles of the Pauli kernel: 2^t amplitudes with t <= kPauliTileMax.
+constexpr int kPauliTileMax = 12;
+size_t pauli_lds_bytes(const TileGeom &g, int k_count, bool partner);
+hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t s);
+hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s);
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s);
 hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s);
 hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s);

@@ -21,6 +21,21 @@ namespace tq {
 // ------------------------------------------------------------ small helpers
 // fp64 arithmetic on complex64 amplitudes: gate matrices stay in float64 and
 // every product is formed in float64; only the stored amplitude is rounded
+// Read-only tables (ops, stages, term lists) are read through the constant
+// address space: with a uniform index the load becomes a scalar-cache load
+// instead of a vector memory load that the wave has to wait for.
+template <class T> __device__ __forceinline__ T cget(const T *p, int64_t i)
+{
+    static_assert(sizeof(T) % 4 == 0, "tables are read in 32-bit words");
+    typedef const __attribute__((address_space(4))) uint32_t cword;
+    cword *q = (cword *)(p + i);
+    T v;
+    uint32_t *d = reinterpret_cast<uint32_t *>(&v);
+#pragma unroll
+    for (int k = 0; k < (int)(sizeof(T) / 4); k++) d[k] = q[k];
+    return v;
+}
+
 __device__ __forceinline__ double2 up2(float2 a) { return make_double2((double)a.x, (double)a.y); }
 __device__ __forceinline__ float2 down2(double2 a) { return make_float2((float)a.x, (float)a.y); }
 __device__ __forceinline__ double2 zmul(double2 a, double2 b)
@@ -313,7 +328,7 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     const int ti = blockIdx.x * blockDim.x + threadIdx.x + a.task_begin;
     if (ti >= a.task_end) return;
     const BuildTask bt = a.tasks[ti];
-    const int b = a.rows[row];
+    const int b = cget(a.rows, row);
     BuildCtx c{a.members, a.gates, a.slot_sym,
                a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots),
                a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots), a.explicit_mats,
@@ -333,20 +348,56 @@ __device__ __forceinline__ uint64_t tile_index(const TileCtx &tc, uint64_t fb, u
     return fb | (l & tc.lowmask) | tc.hi_off[l >> tc.c];
 }
 
-// copy a tile between HBM and LDS; two amplitudes per float4 when c >= 1
-template <bool kLoad>
+// Copy a tile between HBM and LDS, two amplitudes per 16-byte access when
+// c >= 1.  Each thread issues a batch of kCopyBatch global accesses before it
+// touches LDS, so that a wavefront keeps that many requests in flight instead
+// of waiting for every load before the next one is issued.
+constexpr int kCopyBatch = 16;
+// The per-thread index of a copy is recomputed at every call: the empty asm
+// keeps the compiler from hoisting the copies' address arithmetic out of the
+// tile loop, where it would stay live across the register-heavy stages.
+__device__ __forceinline__ int copy_lane0()
+{
+    int l = 2 * (int)threadIdx.x;
+    asm volatile("" : "+v"(l));
+    return l;
+}
+
+template <bool kLoad, int kBatch = kCopyBatch>
 __device__ __forceinline__ void tile_copy(const TileCtx &tc, float2 *lds, float2 *row, uint64_t fb, int T)
 {
     if (tc.c >= 1) {
-        for (int l = 2 * threadIdx.x; l < T; l += 2 * blockDim.x) {
-            float4 *p = reinterpret_cast<float4 *>(row + tile_index(tc, fb, l));
+        const int step = 2 * blockDim.x;
+        for (int l0 = copy_lane0(); l0 < T; l0 += kBatch * step) {
+            float4 v[kBatch];
             if (kLoad) {
-                float4 v = *p;
-                lds[sw(l)] = make_float2(v.x, v.y);
-                lds[sw(l + 1)] = make_float2(v.z, v.w);
+#pragma unroll
+                for (int k = 0; k < kBatch; k++) {
+                    const int l = l0 + k * step;
+                    if (l < T) v[k] = *reinterpret_cast<const float4 *>(row + tile_index(tc, fb, l));
+                }
+#pragma unroll
+                for (int k = 0; k < kBatch; k++) {
+                    const int l = l0 + k * step;
+                    if (l < T) {
+                        lds[sw(l)] = make_float2(v[k].x, v[k].y);
+                        lds[sw(l + 1)] = make_float2(v[k].z, v[k].w);
+                    }
+                }
             } else {
-                const float2 u0 = lds[sw(l)], u1 = lds[sw(l + 1)];
-                *p = make_float4(u0.x, u0.y, u1.x, u1.y);
+#pragma unroll
+                for (int k = 0; k < kBatch; k++) {
+                    const int l = l0 + k * step;
+                    if (l < T) {
+                        const float2 u0 = lds[sw(l)], u1 = lds[sw(l + 1)];
+                        v[k] = make_float4(u0.x, u0.y, u1.x, u1.y);
+                    }
+                }
+#pragma unroll
+                for (int k = 0; k < kBatch; k++) {
+                    const int l = l0 + k * step;
+                    if (l < T) *reinterpret_cast<float4 *>(row + tile_index(tc, fb, l)) = v[k];
+                }
             }
         }
     } else {
@@ -846,7 +897,7 @@ __device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, co
 #pragma unroll
         for (int k = 0; k < (1 << R); k++) a[k] = up2(lds[sw(base | off[k])]);
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
-            const PassOp op = ops[oi];
+            const PassOp op = cget(ops, oi);
             reg_op<R>(op, M + (op.mat - mbase), a, base, fb);
         }
 #pragma unroll
@@ -890,7 +941,7 @@ __device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops
             f[k] = active ? up2(lf[sw(base | off[k])]) : make_double2(0, 0);
         }
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
-            const PassOp op = ops[oi];
+            const PassOp op = cget(ops, oi);
             const double2 *m = M + (op.mat - mbase);
             const double2 *d0 = M + (op.ngrad > 0 ? op.dmat[0] - mbase : 0);
             const double2 *d1 = M + (op.ngrad > 1 ? op.dmat[1] - mbase : 0);
@@ -949,7 +1000,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
     double2 *p2 = p1 + (1 << a1);
 
     const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = a.rows[row];
+    const int b = cget(a.rows, row);
     float2 *st = a.state + (int64_t)b * a.row_stride;
     build_hi_off(g, hi_off);
     stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, a.mat_begin, a.mat_end);
@@ -993,7 +1044,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
         }
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
-            const Stage st = a.stages[si];
+            const Stage st = cget(a.stages, si);
             run_stage_any(st, a.ops, M, a.mat_begin, lds, t, fb);
             __syncthreads();
         }
@@ -1059,67 +1110,6 @@ __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const floa
     return acc;
 }
 
-__global__ __launch_bounds__(256) void k_expect(ExpArgs a)
-{
-    extern __shared__ __align__(16) unsigned char smem[];
-    const TileGeom &g = a.g;
-    const int t = g.t;
-    const int T = 1 << t;
-    float2 *lds = reinterpret_cast<float2 *>(smem);
-    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
-    double *acc = reinterpret_cast<double *>(hi_off + (1 << g.h));  // [4][kTermChunk]
-
-    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = a.rows[row];
-    const float2 *st = a.state + (int64_t)b * a.row_stride;
-    const TermDev *terms = a.terms + a.row_term_begin[row];
-    const int nterm = a.row_term_count[row];
-    build_hi_off(g, hi_off);
-    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
-    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-
-    for (int c0 = 0; c0 < nterm; c0 += kTermChunk) {
-        const int cn = min(kTermChunk, nterm - c0);
-        for (int j = threadIdx.x; j < 4 * kTermChunk; j += blockDim.x) acc[j] = 0;
-        __syncthreads();
-        const int64_t ntiles = (int64_t)1 << a.tiles_log2;
-        for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
-            const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
-            tile_copy<true>(tc, lds, const_cast<float2 *>(st), fb, T);
-            __syncthreads();
-            for (int k = 0; k < cn; k++) {
-                double v = wave_sum(term_tile_sum(terms[c0 + k], tc, lds, st, fb, t));
-                if (lane == 0) acc[wave * kTermChunk + k] += v;
-            }
-            __syncthreads();
-        }
-        double *out = a.partial + ((int64_t)row * a.wg_per_row + w) * a.tmax + c0;
-        for (int k = threadIdx.x; k < cn; k += blockDim.x)
-            out[k] = ((acc[k] + acc[kTermChunk + k]) + acc[2 * kTermChunk + k]) + acc[3 * kTermChunk + k];
-        __syncthreads();
-    }
-}
-
-// out[b, k] = sum over the row's terms of observable k: coeff * sum_w partial
-__global__ void k_expect_reduce(ExpReduceArgs a)
-{
-    const int row = blockIdx.x;
-    const int b = a.rows[row];
-    const TermDev *terms = a.terms + a.row_term_begin[row];
-    const int nterm = a.row_term_count[row];
-    const double *p = a.partial + (int64_t)row * a.wg_per_row * a.tmax;
-    for (int k = threadIdx.x; k < a.K; k += blockDim.x) {
-        double sum = 0;
-        for (int ti = 0; ti < nterm; ti++) {
-            if (terms[ti].k != k) continue;
-            double s = 0;
-            for (int w = 0; w < a.wg_per_row; w++) s += p[(int64_t)w * a.tmax + ti];
-            sum += terms[ti].coeff * s;
-        }
-        a.out[(int64_t)b * a.K + k] = (float)sum;
-    }
-}
-
 // --------------------------------------------------- phi = H_g psi
 // (P psi)[i] = i^{ny} (-1)^{|(i ^ x) & z|} psi[i ^ x]; the coefficient of term
 // t of observable k is upstream[b, k] * coeff_t.  One output element.
@@ -1128,7 +1118,7 @@ __device__ __forceinline__ float2 h_elem(uint32_t l, uint64_t fb, const TermDev 
 {
     double ax = 0, ay = 0;
     for (int k = 0; k < nterm; k++) {
-        const TermDev tm = terms[k];
+        const TermDev tm = cget(terms, k);
         const uint32_t lj = l ^ tm.xl;
         const uint64_t fj = fb ^ tm.xout;
         float2 v = tm.xout == 0 ? lds[sw(lj)] : ps[tile_index(tc, fj, lj)];
@@ -1145,33 +1135,178 @@ __device__ __forceinline__ float2 h_elem(uint32_t l, uint64_t fb, const TermDev 
     return make_float2((float)ax, (float)ay);
 }
 
-__global__ __launch_bounds__(256) void k_apply_h(HArgs a)
+// ------------------------------------------------ Pauli sums on tiles
+// The hardware hands consecutive workgroup ids to the 8 XCDs in turn; this
+// renumbering gives each XCD a contiguous range of (row, tile) work so that
+// the tiles of one row, which read each other as partner tiles, share that
+// XCD's L2.
+__device__ __forceinline__ int xcd_block(int bid, int nb)
+{
+    if (nb % 8) return bid;
+    return (bid % 8) * (nb / 8) + bid / 8;
+}
+
+// Expectations of Pauli sums, and optionally phi = sum_k g_k h_k psi, over
+// tiles of T = 256 P amplitudes (T < 256 when P == 1: the state is smaller).
+// Thread tid owns the amplitudes l = tid + 256 r of the tile.  For each x
+// group the thread forms d(l) = sum_t c'_t chi_{z_t}(l) from the group's
+// terms (one sign per term and thread, one per u sub-group and register),
+// reads the partner amplitudes psi_{l ^ x} once, and adds
+// Re(conj(psi_l) d(l) psi_{l ^ x}) to the group's observable and
+// g_k d(l) psi_{l ^ x} to phi_l.  Accumulation is in fp64; each workgroup
+// reduces its expectation partials in a fixed order.
+template <int P, bool kPhi>
+__global__ __launch_bounds__(256) void k_pauli(PauliArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const TileGeom &g = a.g;
-    const int t = g.t;
-    const int T = 1 << t;
-    float2 *lds = reinterpret_cast<float2 *>(smem);
-    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
-    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = a.rows[row];
+    const int T = 1 << g.t;
+    float2 *la = reinterpret_cast<float2 *>(smem);
+    uint64_t *hi_off = reinterpret_cast<uint64_t *>(la + T);
+    double *red = reinterpret_cast<double *>(hi_off + (1 << g.h));  // [kPauliChunk][4 waves]
+    double *esum = red + 4 * kPauliChunk;                           // [k_count]
+    float2 *lb = reinterpret_cast<float2 *>(esum + a.k_count);      // partner tile (when any xF != 0)
+
+    const int bid = xcd_block(blockIdx.x, gridDim.x);
+    const int row = bid / a.wg_per_row, w = bid % a.wg_per_row;
+    const int b = cget(a.rows, row);
     const float2 *ps = a.psi + (int64_t)b * a.row_stride;
-    float2 *ph = a.phi + (int64_t)b * a.row_stride;
-    const TermDev *terms = a.terms + a.row_term_begin[row];
-    const int nterm = a.row_term_count[row];
-    const float *up = a.upstream + (int64_t)a.brows[row] * a.K;
+    const PChunk *chunks = a.chunks + cget(a.row_chunk_begin, row);
+    const int nchunks = cget(a.row_chunk_count, row);
+    const float *up = kPhi ? a.upstream + (int64_t)a.brows[row] * a.K : nullptr;
+    const int tid = threadIdx.x, wave = tid / 64, lane = tid % 64;
+    const bool active = tid < T;
+    const int kend = a.k_begin + a.k_count;
     build_hi_off(g, hi_off);
+    for (int j = tid; j < a.k_count; j += blockDim.x) esum[j] = 0;
     TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
-    __syncthreads();  // hi_off is read by every thread below
+    __syncthreads();
+
     const int64_t ntiles = (int64_t)1 << a.tiles_log2;
     for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
         const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
-        tile_copy<true>(tc, lds, const_cast<float2 *>(ps), fb, T);
+        tile_copy<true, (P > 1 ? P / 2 : 1)>(tc, la, const_cast<float2 *>(ps), fb, T);
         __syncthreads();
-        for (int l = threadIdx.x; l < T; l += blockDim.x)
-            ph[tile_index(tc, fb, l)] = h_elem(l, fb, terms, nterm, up, lds, tc, ps);
+        float2 own[P];
+#pragma unroll
+        for (int r = 0; r < P; r++) own[r] = active ? la[sw(tid + 256 * r)] : make_float2(0.f, 0.f);
+        double2 acc[kPhi ? P : 1];
+#pragma unroll
+        for (int r = 0; r < (kPhi ? P : 1); r++) acc[r] = make_double2(0.0, 0.0);
+
+        for (int ci = 0; ci < nchunks; ci++) {
+            const PChunk ch = cget(chunks, ci);
+            if (ch.k0 < a.k_begin || ch.k0 >= kend) continue;
+            double ek[kPauliChunk];
+#pragma unroll
+            for (int j = 0; j < kPauliChunk; j++) ek[j] = 0.0;
+            for (int xi = ch.xf_begin; xi < ch.xf_end; xi++) {
+                const PXfGroup xf = cget(a.xfg, xi);
+                const float2 *src = la;
+                if (xf.xF) {
+                    __syncthreads();  // the previous partner tile is consumed
+                    tile_copy<true, (P > 1 ? P / 2 : 1)>(tc, lb, const_cast<float2 *>(ps), fb ^ xf.xF, T);
+                    __syncthreads();
+                    src = lb;
+                }
+                for (int gi = xf.x_begin; gi < xf.x_end; gi++) {
+                    const PXGroup xg = cget(a.xg, gi);
+                    double dr[P], di[P];
+#pragma unroll
+                    for (int r = 0; r < P; r++) dr[r] = di[r] = 0.0;
+                    for (int ui = xg.u_begin; ui < xg.u_end; ui++) {
+                        const PUSub us = cget(a.us, ui);
+                        double er = 0.0, ei = 0.0;
+                        for (int ti = us.t_begin; ti < us.t_end; ti++) {
+                            const PTerm tm = cget(a.terms, ti);
+                            const double c = (par64(fb & tm.zF) ^ par32((uint32_t)tid & tm.zlo)) ? -tm.c : tm.c;
+                            if (tm.im) ei += c;
+                            else er += c;
+                        }
+#pragma unroll
+                        for (int r = 0; r < P; r++) {
+                            const double sg = (__popc(us.u & (uint32_t)r) & 1) ? -1.0 : 1.0;
+                            dr[r] = fma(sg, er, dr[r]);
+                            di[r] = fma(sg, ei, di[r]);
+                        }
+                    }
+                    const bool self = xf.xF == 0 && xg.xT == 0;
+                    const double gk = kPhi ? (double)up[ch.k0 + xg.kk] : 0.0;
+                    double ex = 0.0;
+                    if (!(xg.flags & 2)) {
+#pragma unroll
+                        for (int r = 0; r < P; r++) {
+                            float2 pv = own[r];
+                            if (!self && active) pv = src[sw((tid + 256 * r) ^ xg.xT)];
+                            const double tr = dr[r] * (double)pv.x, ti = dr[r] * (double)pv.y;
+                            ex = fma((double)own[r].x, tr, fma((double)own[r].y, ti, ex));
+                            if (kPhi) {
+                                acc[r].x = fma(gk, tr, acc[r].x);
+                                acc[r].y = fma(gk, ti, acc[r].y);
+                            }
+                        }
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < P; r++) {
+                            float2 pv = own[r];
+                            if (!self && active) pv = src[sw((tid + 256 * r) ^ xg.xT)];
+                            const double px = pv.x, py = pv.y;
+                            const double tr = fma(dr[r], px, -di[r] * py), ti = fma(dr[r], py, di[r] * px);
+                            ex = fma((double)own[r].x, tr, fma((double)own[r].y, ti, ex));
+                            if (kPhi) {
+                                acc[r].x = fma(gk, tr, acc[r].x);
+                                acc[r].y = fma(gk, ti, acc[r].y);
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < kPauliChunk; j++) ek[j] += (j == xg.kk) ? ex : 0.0;
+                }
+            }
+            // this tile's share of the chunk's expectations, in a fixed order
+#pragma unroll
+            for (int j = 0; j < kPauliChunk; j++)
+                if (j < ch.nk) {
+                    const double v = wave_sum(ek[j]);
+                    if (lane == 0) red[j * 4 + wave] = v;
+                }
+            __syncthreads();
+            if (tid < ch.nk)
+                esum[ch.k0 - a.k_begin + tid] += ((red[tid * 4] + red[tid * 4 + 1]) + red[tid * 4 + 2]) + red[tid * 4 + 3];
+            __syncthreads();
+        }
+        if (kPhi && active) {
+            float2 *ph = a.phi + (int64_t)b * a.row_stride;
+#pragma unroll
+            for (int r = 0; r < P; r++) {
+                const uint64_t i = tile_index(tc, fb, tid + 256 * r);
+                double2 v = acc[r];
+                if (a.phi_accumulate) v = zadd(v, up2(ph[i]));
+                ph[i] = down2(v);
+            }
+        }
         __syncthreads();
     }
+    double *out = a.partial + ((int64_t)row * a.wg_per_row + w) * a.k_count;
+    for (int j = tid; j < a.k_count; j += blockDim.x) out[j] = esum[j];
+}
+
+// out[b, k] = sum over the row's workgroups of their partials: one block per
+// (row, observable), strided sums then a tree, all in a fixed order.
+__global__ __launch_bounds__(256) void k_pauli_reduce(PauliReduceArgs a)
+{
+    __shared__ double red[256];
+    const int row = blockIdx.x, j = blockIdx.y;
+    const double *p = a.partial + (int64_t)row * a.wg_per_row * a.k_count + j;
+    double s = 0;
+    for (int w = threadIdx.x; w < a.wg_per_row; w += blockDim.x) s += p[(int64_t)w * a.k_count];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) a.out[(int64_t)a.rows[row] * a.K + a.k_begin + j] = (float)red[0];
 }
 
 // ------------------------------------------------------ reverse pass
@@ -1189,7 +1324,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
     double *acc = reinterpret_cast<double *>(lm + (a.mat_end - a.mat_begin));  // [4][gcount]
 
     const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = a.rows[row];
+    const int b = cget(a.rows, row);
     float2 *sp = a.psi + (int64_t)b * a.row_stride;
     float2 *sf = a.phi + (int64_t)b * a.row_stride;
     build_hi_off(g, hi_off);
@@ -1197,7 +1332,6 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
     for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) acc[j] = 0;
     TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
     const int tid = threadIdx.x, nt = blockDim.x;
-    const int wave = tid / 64, lane = tid % 64;
     __syncthreads();
 
     const int64_t ntiles = (int64_t)1 << a.tiles_log2;
@@ -1207,7 +1341,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         tile_copy<true>(tc, lf, sf, fb, T);
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
-            const Stage st = a.stages[si];
+            const Stage st = cget(a.stages, si);
             run_rev_stage_any(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase);
             __syncthreads();
         }
@@ -1226,7 +1360,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
 __global__ void k_grad_reduce(GradReduceArgs a)
 {
     const int row = blockIdx.x;
-    const int b = a.rows[row];
+    const int b = cget(a.rows, row);
     const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots);
     const double *p = a.gpart + (int64_t)row * a.wg_per_row * a.n_gslots;
     for (int s = threadIdx.x; s < a.S; s += blockDim.x) {
@@ -1252,7 +1386,7 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
     const int n = a.n;
     const uint32_t T = 1u << n;
     const int row = blockIdx.x;
-    const int b = a.rows[row];
+    const int b = cget(a.rows, row);
     const int tid = threadIdx.x, nt = blockDim.x;
     const int wave = tid / 64, lane = tid % 64;
     double2 *lm = reinterpret_cast<double2 *>(smem);                      // [mat_block]
@@ -1277,7 +1411,7 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
     __syncthreads();
     // 3. forward gates
     for (int si = 0; si < a.nfstages; si++) {
-        const Stage st = a.fstages[si];
+        const Stage st = cget(a.fstages, si);
         run_stage_any(st, a.fops, lm, 0, lp, n, 0);
         __syncthreads();
     }
@@ -1289,7 +1423,7 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
     const TermDev *terms = a.terms ? a.terms + a.row_term_begin[row] : nullptr;
     const int nterm = a.terms ? a.row_term_count[row] : 0;
     for (int k = 0; k < nterm; k++) {
-        double v = wave_sum(term_tile_sum(terms[k], tc, lp, lp, 0, n));
+        double v = wave_sum(term_tile_sum(cget(terms, k), tc, lp, lp, 0, n));
         if (lane == 0) acc[wave * a.nacc + k] += v;
     }
     // 5. adjoint sweep
@@ -1298,7 +1432,7 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
         for (uint32_t l = tid; l < T; l += nt) lf[sw(l)] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
         __syncthreads();
         for (int si = 0; si < a.nrstages; si++) {
-            const Stage st = a.rstages[si];
+            const Stage st = cget(a.rstages, si);
             run_rev_stage_any(st, a.rops, lm, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc);
             __syncthreads();
         }
@@ -1540,31 +1674,49 @@ hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_expect(const ExpArgs &a, int nrows, hipStream_t s)
+size_t pauli_lds_bytes(const TileGeom &g, int k_count, bool partner)
 {
-    size_t lds = sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
-                 sizeof(double) * 4 * kTermChunk;
-    hipError_t e = set_lds(k_expect, lds);
-    if (e != hipSuccess) return e;
-    prof::Scope ps("expect", s);
-    hipLaunchKernelGGL(k_expect, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return sizeof(float2) * ((size_t)1 << g.t) * (partner ? 2 : 1) + sizeof(uint64_t) * ((size_t)1 << g.h) +
+           sizeof(double) * (4 * kPauliChunk + (size_t)k_count);
+}
+
+template <int P>
+hipError_t launch_pauli_p(const PauliArgs &a, int nrows, size_t lds, hipStream_t s)
+{
+    const dim3 grid(nrows * a.wg_per_row);
+    if (a.phi) {
+        hipError_t e = set_lds(k_pauli<P, true>, lds);
+        if (e != hipSuccess) return e;
+        prof::Scope ps("pauli", s);
+        hipLaunchKernelGGL((k_pauli<P, true>), grid, dim3(kThreads), lds, s, a);
+    } else {
+        hipError_t e = set_lds(k_pauli<P, false>, lds);
+        if (e != hipSuccess) return e;
+        prof::Scope ps("pauli", s);
+        hipLaunchKernelGGL((k_pauli<P, false>), grid, dim3(kThreads), lds, s, a);
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_expect_reduce(const ExpReduceArgs &a, int nrows, hipStream_t s)
+hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t s)
 {
-    prof::Scope ps("expect_reduce", s);
-    hipLaunchKernelGGL(k_expect_reduce, dim3(nrows), dim3(64), 0, s, a);
-    return hipGetLastError();
+    if (nrows <= 0) return hipSuccess;
+    const size_t lds = pauli_lds_bytes(a.g, a.k_count, partner);
+    switch (a.g.t <= 8 ? 1 : 1 << (a.g.t - 8)) {
+    case 1: return launch_pauli_p<1>(a, nrows, lds, s);
+    case 2: return launch_pauli_p<2>(a, nrows, lds, s);
+    case 4: return launch_pauli_p<4>(a, nrows, lds, s);
+    case 8: return launch_pauli_p<8>(a, nrows, lds, s);
+    case 16: return launch_pauli_p<16>(a, nrows, lds, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
-hipError_t launch_apply_h(const HArgs &a, int nrows, hipStream_t s)
+hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s)
 {
-    size_t lds = sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h);
-    hipError_t e = set_lds(k_apply_h, lds);
-    if (e != hipSuccess) return e;
-    prof::Scope ps("apply_h", s);
-    hipLaunchKernelGGL(k_apply_h, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    if (nrows <= 0 || a.k_count <= 0) return hipSuccess;
+    prof::Scope ps("pauli_reduce", s);
+    hipLaunchKernelGGL(k_pauli_reduce, dim3(nrows, a.k_count), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

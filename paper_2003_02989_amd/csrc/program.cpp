@@ -628,6 +628,108 @@ TileGeom expectation_geometry(int n, int t, int c, const std::vector<uint64_t> &
     return geom_from_bits(n, c, bits);
 }
 
+PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vector<TermDev>> &per_row, bool uniform)
+{
+    PauliTables pt;
+    std::vector<uint64_t> xs;
+    for (size_t r = 0; r < per_row.size() && (r == 0 || !uniform); r++)
+        for (const TermDev &td : per_row[r]) xs.push_back(td.x);
+    pt.geom = expectation_geometry(n, std::min(n, t), std::min(c, std::min(n, t)), xs);
+    const TileGeom &gm = pt.geom;
+    auto local = [&](uint64_t m) {
+        uint32_t v = 0;
+        for (int k = 0; k < gm.c; k++)
+            if ((m >> k) & 1) v |= 1u << k;
+        for (int k = 0; k < gm.h; k++)
+            if ((m >> gm.hb[k]) & 1) v |= 1u << (gm.c + k);
+        return v;
+    };
+    struct Item {
+        int chunk;
+        uint64_t xF;
+        uint32_t xT;
+        int k;
+        uint32_t u;
+        PTerm term;
+    };
+    const int nchunk = (K + kPauliChunk - 1) / kPauliChunk;
+    pt.row_begin.assign(per_row.size(), 0);
+    pt.row_count.assign(per_row.size(), nchunk);
+    for (size_t r = 0; r < per_row.size(); r++) {
+        if (uniform && r > 0) {
+            pt.row_begin[r] = pt.row_begin[0];
+            continue;
+        }
+        std::vector<Item> items;
+        items.reserve(per_row[r].size());
+        for (const TermDev &td : per_row[r]) {
+            Item it{};
+            it.chunk = td.k / kPauliChunk;
+            it.k = td.k;
+            it.xF = td.x & gm.fixed_mask;
+            it.xT = local(td.x);
+            const uint32_t zT = local(td.z);
+            it.u = zT >> 8;
+            // c' = c i^{ny} chi_z(x): real for even ny, imaginary for odd ny
+            const int ny = td.ny & 3;
+            double v = td.coeff;
+            if (__builtin_popcountll(td.z & td.x) & 1) v = -v;
+            if (ny >= 2) v = -v;
+            it.term = PTerm{td.z & gm.fixed_mask, zT & 0xffu, (uint32_t)(ny & 1), v};
+            if (it.xF) pt.partner = true;
+            items.push_back(it);
+        }
+        std::stable_sort(items.begin(), items.end(), [](const Item &a, const Item &b) {
+            if (a.chunk != b.chunk) return a.chunk < b.chunk;
+            if (a.xF != b.xF) return a.xF < b.xF;
+            if (a.xT != b.xT) return a.xT < b.xT;
+            if (a.k != b.k) return a.k < b.k;
+            return a.u < b.u;
+        });
+        pt.row_begin[r] = (int32_t)pt.chunks.size();
+        size_t i = 0;
+        for (int ci = 0; ci < nchunk; ci++) {
+            PChunk ch{};
+            ch.k0 = ci * kPauliChunk;
+            ch.nk = std::min(kPauliChunk, K - ch.k0);
+            ch.xf_begin = (int32_t)pt.xfg.size();
+            while (i < items.size() && items[i].chunk == ci) {
+                PXfGroup xf{};
+                xf.xF = items[i].xF;
+                xf.x_begin = (int32_t)pt.xg.size();
+                while (i < items.size() && items[i].chunk == ci && items[i].xF == xf.xF) {
+                    PXGroup xg{};
+                    xg.xT = items[i].xT;
+                    xg.kk = items[i].k - ch.k0;
+                    xg.u_begin = (int32_t)pt.us.size();
+                    const int k = items[i].k;
+                    while (i < items.size() && items[i].chunk == ci && items[i].xF == xf.xF && items[i].xT == xg.xT &&
+                           items[i].k == k) {
+                        PUSub us{};
+                        us.u = items[i].u;
+                        us.t_begin = (int32_t)pt.terms.size();
+                        while (i < items.size() && items[i].chunk == ci && items[i].xF == xf.xF &&
+                               items[i].xT == xg.xT && items[i].k == k && items[i].u == us.u) {
+                            xg.flags |= items[i].term.im ? 2u : 1u;
+                            pt.terms.push_back(items[i].term);
+                            i++;
+                        }
+                        us.t_end = (int32_t)pt.terms.size();
+                        pt.us.push_back(us);
+                    }
+                    xg.u_end = (int32_t)pt.us.size();
+                    pt.xg.push_back(xg);
+                }
+                xf.x_end = (int32_t)pt.xg.size();
+                pt.xfg.push_back(xf);
+            }
+            ch.xf_end = (int32_t)pt.xfg.size();
+            pt.chunks.push_back(ch);
+        }
+    }
+    return pt;
+}
+
 std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt)
 {
     if (!blob) fail(TQ_E_INVALID, "program blob is NULL");

@@ -101,4 +101,20 @@ std::unique_ptr<ObsData> parse_observables(const void *blob, size_t nbytes);
 // often flipped by the terms' X/Y factors.
 TileGeom expectation_geometry(int n, int t, int c, const std::vector<uint64_t> &xmasks);
 
+// Term tables of the tile Pauli kernel for the rows of one structure group
+// (terms given with global masks x, z, their Y count, observable and
+// coefficient).  Rows with identical term lists may share one table
+// (`uniform`).  Every row gets ceil(K / kPauliChunk) chunks.
+struct PauliTables {
+    TileGeom geom;
+    bool partner = false;  // some term flips a bit outside the tile
+    std::vector<PChunk> chunks;
+    std::vector<int32_t> row_begin, row_count;
+    std::vector<PXfGroup> xfg;
+    std::vector<PXGroup> xg;
+    std::vector<PUSub> us;
+    std::vector<PTerm> terms;
+};
+PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vector<TermDev>> &per_row, bool uniform);
+
 } // namespace tq

@@ -77,8 +77,20 @@ int wg_for(int nrows, int tiles_log2)
 struct ObsGroupDev {
     TileGeom geom;
     int tmax = 0;
-    DevBuf terms, begin, count;
+    DevBuf terms, begin, count;  // TermDev tables (resident kernel)
+    // tables of the tile Pauli kernel
+    TileGeom pgeom;
+    bool partner = false;
+    DevBuf chunks, cbegin, ccount, xfg, xg, us, pterms;
+    void release()
+    {
+        for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms}) b->release();
+    }
 };
+
+// Tile size of the Pauli kernel (log2 amplitudes): 2048 amplitudes, eight
+// per thread.
+constexpr int kPauliTile = 11;
 
 struct GroupDev {
     DevBuf rows, ident, gates, slot_sym, scale, off, explicit_, tasks, members, fwd_ops, rev_ops, sym_begin,
@@ -112,11 +124,7 @@ struct tq_program_s {
                               &g->gslot_slot, &g->fwd_stages, &g->rev_stages})
                 b->release();
         }
-        for (auto &o : obs_dev) {
-            o->terms.release();
-            o->begin.release();
-            o->count.release();
-        }
+        for (auto &o : obs_dev) o->release();
         for (DevBuf *b : {&psi, &phi, &mats, &partial, &gpart, &levels}) b->release();
     }
 };
@@ -345,49 +353,77 @@ void ensure_obs(tq_program p, tq_observables o)
         upload(og->terms, flat);
         upload(og->begin, begin);
         upload(og->count, count);
+        PauliTables pt = pauli_tables(n, std::min(p->pd->opt.tile, kPauliTile), p->pd->opt.low, od.K, per_row, uniform);
+        og->pgeom = pt.geom;
+        og->partner = pt.partner;
+        upload(og->chunks, pt.chunks);
+        upload(og->cbegin, pt.row_begin);
+        upload(og->ccount, pt.row_count);
+        upload(og->xfg, pt.xfg);
+        upload(og->xg, pt.xg);
+        upload(og->us, pt.us);
+        upload(og->pterms, pt.terms);
         out.push_back(std::move(og));
     }
-    for (auto &old : p->obs_dev) {
-        old->terms.release();
-        old->begin.release();
-        old->count.release();
-    }
+    for (auto &old : p->obs_dev) old->release();
     p->obs_dev = std::move(out);
     p->obs_id = o->od->id;
 }
 
-// expectations of group gi's rows from the state workspace into out[b, k]
-void expect_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+// Run the Pauli kernel over group gi's rows: expectations into out[b, k]
+// (when out is not NULL) and, when phi is not NULL, phi = sum_k g_k h_k psi
+// with g = upstream.  Observables are split over launches so that the
+// per-workgroup partials stay within a bounded workspace.
+void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, int K, float *out,
+                 hipStream_t s)
 {
     const Group &g = *p->pd->groups[gi];
     GroupDev &gd = *p->gdev[gi];
     ObsGroupDev &og = *p->obs_dev[gi];
     const int nrows = (int)g.rows.size();
     if (K == 0 || nrows == 0) return;
-    ExpArgs a{};
-    a.state = psi;
+    PauliArgs a{};
+    a.psi = psi;
+    a.phi = phi;
     a.row_stride = (int64_t)1 << g.n;
     a.rows = (const int32_t *)gd.ident.p;
-    a.terms = (const TermDev *)og.terms.p;
-    a.row_term_begin = (const int32_t *)og.begin.p;
-    a.row_term_count = (const int32_t *)og.count.p;
-    a.g = og.geom;
-    a.tiles_log2 = g.n - og.geom.t;
-    a.wg_per_row = wg_for(nrows, a.tiles_log2);
-    a.tmax = std::max(og.tmax, 1);
-    a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)nrows * a.wg_per_row * a.tmax);
-    hip_check(launch_expect(a, nrows, s), "expectation launch");
-    ExpReduceArgs r{};
-    r.rows = (const int32_t *)gd.rows.p;
-    r.terms = a.terms;
-    r.row_term_begin = a.row_term_begin;
-    r.row_term_count = a.row_term_count;
-    r.partial = a.partial;
-    r.wg_per_row = a.wg_per_row;
-    r.tmax = a.tmax;
-    r.K = K;
-    r.out = out;
-    hip_check(launch_expect_reduce(r, nrows, s), "expectation reduce launch");
+    a.brows = (const int32_t *)gd.rows.p;
+    a.chunks = (const PChunk *)og.chunks.p;
+    a.row_chunk_begin = (const int32_t *)og.cbegin.p;
+    a.row_chunk_count = (const int32_t *)og.ccount.p;
+    a.xfg = (const PXfGroup *)og.xfg.p;
+    a.xg = (const PXGroup *)og.xg.p;
+    a.us = (const PUSub *)og.us.p;
+    a.terms = (const PTerm *)og.pterms.p;
+    a.upstream = upstream;
+    a.K = K;
+    a.g = og.pgeom;
+    a.tiles_log2 = g.n - og.pgeom.t;
+    // every tile of a row in flight at once (partner tiles then come from L2),
+    // up to 2^18 workgroups per launch
+    const int64_t ntiles = (int64_t)1 << a.tiles_log2;
+    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, ((int64_t)1 << 18) / nrows));
+    const int64_t slots = (int64_t)nrows * a.wg_per_row;
+    const int kmax = (int)std::max<int64_t>(
+        kPauliChunk, std::min<int64_t>(1024, ((int64_t)32 << 20) / slots) / kPauliChunk * kPauliChunk);
+    for (int k0 = 0; k0 < K; k0 += kmax) {
+        a.k_begin = k0;
+        a.k_count = std::min(kmax, K - k0);
+        a.phi_accumulate = k0 > 0;
+        a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)slots * a.k_count);
+        hip_check(launch_pauli(a, nrows, og.partner, s), "Pauli kernel launch");
+        if (out) {
+            PauliReduceArgs r{};
+            r.rows = a.brows;
+            r.partial = a.partial;
+            r.wg_per_row = a.wg_per_row;
+            r.K = K;
+            r.k_begin = k0;
+            r.k_count = a.k_count;
+            r.out = out;
+            hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
+        }
+    }
 }
 
 hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
@@ -618,7 +654,7 @@ tq_status tq_expectation(tq_program prog, const float *theta, tq_observables obs
             }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
             forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
-            expect_group(prog, gi, psi + gd.psi_off, obs->od->K, out, s);
+            pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, obs->od->K, out, s);
         }
     });
 }
@@ -662,24 +698,16 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
             }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
             forward(prog, gi, psi + gd.psi_off, stride, (const int32_t *)gd.ident.p, s);
-            if (expectations && K > 0) expect_group(prog, gi, psi + gd.psi_off, K, expectations, s);
-            if (pd.S == 0) continue;
-            // phi = H_g psi
-            HArgs h{};
-            h.psi = psi + gd.psi_off;
-            h.phi = phi + gd.psi_off;
-            h.row_stride = stride;
-            h.rows = (const int32_t *)gd.ident.p;
-            h.brows = (const int32_t *)gd.rows.p;
-            h.terms = (const TermDev *)og.terms.p;
-            h.row_term_begin = (const int32_t *)og.begin.p;
-            h.row_term_count = (const int32_t *)og.count.p;
-            h.upstream = upstream;
-            h.K = K;
-            h.g = og.geom;
-            h.tiles_log2 = g.n - og.geom.t;
-            h.wg_per_row = wg_for(nrows, h.tiles_log2);
-            hip_check(launch_apply_h(h, nrows, s), "H_g launch");
+            if (pd.S == 0) {
+                if (expectations && K > 0) pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, K, expectations, s);
+                continue;
+            }
+            // phi = H_g psi, with the expectations from the same sweep
+            if (K > 0)
+                pauli_group(prog, gi, psi + gd.psi_off, phi + gd.psi_off, upstream, K, expectations, s);
+            else
+                hip_check(launch_zero_tail(phi + gd.psi_off, stride, (const int32_t *)gd.ident.p, nrows, 0, stride, s),
+                          "phi clear");
             // reverse sweep
             const int trl = g.rev.empty() ? 0 : g.n - g.rev[0].geom.t;
             const int wg = wg_for(nrows, trl);

@@ -115,4 +115,41 @@ struct TermDev {
     double coeff;
 };
 
+// Pauli sums in the form the tile kernel evaluates them.  With l a tile-local
+// index, the thread layout l = tid + 256 r splits l into its low 8 bits (the
+// thread) and the bits above (the thread's register r).  A term
+// c i^{ny} X^x Z^z acts on a tile with fixed bits fb as
+//     (P psi)_l = c' chi_zF(fb) chi_zlo(tid) chi_u(r) psi_{l ^ xT} (tile fb ^ xF),
+// chi_m(v) = (-1)^{|m & v|}, where c' = c i^{ny} chi_z(x) is real or purely
+// imaginary.  Terms are grouped by observable chunk, then by the out-of-tile
+// part xF of x (one partner tile per group), then by (xT, observable), then
+// by u, so that the per-amplitude work is one partner read per x group.
+constexpr int kPauliChunk = 4;  // observables accumulated together
+struct PTerm {
+    uint64_t zF;     // z outside the tile (global bits)
+    uint32_t zlo;    // z on tile bits 0..7
+    uint32_t im;     // 1: c' is imaginary (value in c)
+    double c;        // real or imaginary part of c'
+};
+struct PUSub {       // terms sharing u = z on tile bits 8..t-1
+    uint32_t u;
+    int32_t t_begin, t_end;
+    int32_t pad;
+};
+struct PXGroup {     // terms of one observable sharing x
+    uint32_t xT;     // x on the tile bits
+    int32_t kk;      // observable within the chunk
+    int32_t u_begin, u_end;
+    uint32_t flags;  // 1: some c' real, 2: some c' imaginary
+    int32_t pad;
+};
+struct PXfGroup {    // x groups sharing the partner tile fb ^ xF
+    uint64_t xF;
+    int32_t x_begin, x_end;
+};
+struct PChunk {      // observables [k0, k0 + nk), nk <= kPauliChunk
+    int32_t k0, nk;
+    int32_t xf_begin, xf_end;
+};
+
 } // namespace tq

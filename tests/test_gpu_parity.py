@@ -107,3 +107,17 @@ def test_full_pipeline_samples_fall_in_oracle_intervals():
             u = orc.splitmix64(seed, b * shots + k) / 2.0 ** 64
             i = int(g[b, k])
             assert C[i] - delta <= u * C[-1] <= C[i + 1] + delta
+
+
+@pytest.mark.parametrize("n,tile", [(14, 12), (9, 8), (6, 12)])
+def test_many_observables_and_terms(n, tile):
+    # K = 9 observables (three accumulation chunks), one of them an empty sum,
+    # dense terms whose Z factors spread over the thread and register bits of
+    # the Pauli tiles, X/Y factors outside the tile (partner tiles)
+    rng = wl.rng_for(7000 + n)
+    w = wl.random_batch(7100 + n, B=3, n=n, n_gates=50, n_symbols=4, K=9)
+    for b in range(w.B):
+        w.observables[b] = wl.random_observables(rng, n, 9, max_terms=14)
+        w.observables[b][4] = []
+    say("many observables", n, tile)
+    compare(gpu_outputs(w, max_tile_qubits=tile), oracle_outputs(w))
