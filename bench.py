@@ -26,7 +26,7 @@ METRIC = "effective HBM GB/s per fused-gate pass; circuit-expectations/sec at ba
 KERNELS = ("build", "resident", "pass", "pauli", "pauli_reduce", "rev_pass", "grad_reduce",
            "samp_l1", "samp_shots", "gather")
 PEAK_HBM_GBS = 8000.0
-PEAK_FP32_TFLOPS = 157.3
+PEAK_FP64_TFLOPS = 78.6  # fp64 vector: 256 CUs x 2.4 GHz x 128 flop/clk
 
 
 def workload(name):
@@ -163,6 +163,7 @@ def main():
         amps = torch.empty((1, bits.shape[1]), dtype=torch.complex64, device="cuda")
         n_shots = w.extras["n_shots"]
         shots = torch.empty((1, n_shots), dtype=torch.int64, device="cuda")
+        state = torch.empty((1, 1 << w.circuits[0].n), dtype=torch.complex64, device="cuda")
 
     def step():
         if args.config in ("c1", "c2", "c5"):
@@ -170,8 +171,10 @@ def main():
         elif args.config == "c3":
             tq.expectation(prog, theta, obs, out=exp)
         else:
-            tq.amplitudes(prog, None, bits, out=amps)
-            tq.sample(prog, None, n_shots, w.extras["seed"], out=shots)
+            # one simulation serves both outputs
+            tq.simulate_state(prog, None, out=state)
+            tq.amplitudes_from_state(state, bits, out=amps)
+            tq.sample_from_state(state, n_shots, w.extras["seed"], out=shots)
 
     t0 = time.perf_counter()
     step()
@@ -211,7 +214,7 @@ def main():
     flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, args.config in ("c1", "c2", "c5"))
     avg_ms = dom_ms / max(n_launch, 1)
     if args.config in ("c1", "c2"):
-        bound, unit, peak = "alu", "TFLOP/s", PEAK_FP32_TFLOPS
+        bound, unit, peak = "alu", "TFLOP/s", PEAK_FP64_TFLOPS
         achieved = (flops / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e12
         traffic = None
     else:
@@ -237,9 +240,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "c64",
+        "dtype": "f64",
         "data": "synthetic (seeded generators, no datasets)",
-        "config": {"workload": describe_workload(args.config, w), "batch": B, "qubits": w.n_max,
+        "config": {"workload": describe_workload(args.config, w), "storage": "complex64", "batch": B, "qubits": w.n_max,
                    "symbols": w.n_symbols, "observables": K, "pauli_terms": n_terms,
                    "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3},
         "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,

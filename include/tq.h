@@ -161,6 +161,14 @@ tq_status tq_amplitudes(tq_program prog, const float *symbol_values, const uint6
 tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
                                uint64_t *out, void *stream);
 
+/* The amplitude lookup of tq_amplitudes applied to given states: states
+ * complex64 [B, 2^n] device array, bitstrings uint64 [B, M] (an entry >= 2^n
+ * yields a zero amplitude), amps complex64 [B, M].  With tq_simulate_state
+ * and tq_sample_from_state it serves a state that is both sampled and
+ * queried for amplitudes with one simulation. */
+tq_status tq_amplitudes_from_state(const void *states, int32_t B, int32_t n, const uint64_t *bitstrings, int64_t M,
+                                   void *amps, void *stream);
+
 /* Plan introspection: a JSON description of the program's structure groups
  * and of the tile passes planned for each (tile bits, ops, fused members,
  * gradient slots).  Writes at most cap bytes (NUL terminated) into buf and

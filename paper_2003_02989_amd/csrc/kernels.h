@@ -93,7 +93,6 @@ struct ResArgs {
     int uniform, n_slots;
     int S;
     const int32_t *rows;  // batch index of each row
-    int mat_block;        // LDS matrix entries
     int n;
     const PassOp *fops;
     const Stage *fstages;
@@ -147,8 +146,8 @@ struct SampArgs {
 struct GatherArgs {
     const float2 *state;
     int64_t row_stride;
-    const int32_t *rows;   // state rows
-    const int32_t *brows;  // batch index of each row
+    const int32_t *rows;   // state rows (NULL: row r is state row r)
+    const int32_t *brows;  // batch index of each row (NULL: row r is batch row r)
     int n;
     const uint64_t *bits;
     int64_t M;
@@ -158,7 +157,7 @@ struct GatherArgs {
 void profile_start(const char *kernel);
 hipError_t profile_read(int64_t *launches, double *total_ms);
 size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat);
-size_t resident_lds_bytes(int n, int nmat, int nacc, bool adjoint);
+size_t resident_lds_bytes(int n, int nacc, bool adjoint);
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);

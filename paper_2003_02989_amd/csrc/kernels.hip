@@ -449,6 +449,19 @@ __device__ __forceinline__ Quad p2_apply(double2 a, double2 b, double sg, const 
     return o;
 }
 
+// Matrix entries seen by the register ops: a pointer into LDS, or an SMat,
+// which reads a row's matrix block in HBM through the scalar cache (uniform
+// indices land in scalar registers and feed the FMAs directly).
+struct SMat {
+    const __attribute__((address_space(4))) double *p;
+    __device__ __forceinline__ double2 operator[](int i) const { return make_double2(p[2 * i], p[2 * i + 1]); }
+    __device__ __forceinline__ SMat operator+(int i) const { return SMat{p + 2 * i}; }
+};
+__device__ __forceinline__ SMat smat(const double2 *block)
+{
+    return SMat{(const __attribute__((address_space(4))) double *)block};
+}
+
 // ------------------------------------------------------- register stages
 // A stage's ops run on the 2^R amplitudes one thread holds in registers (in
 // fp64); register index k has bit j set when tile bit stage.bits[j] is set.
@@ -459,7 +472,7 @@ __device__ __forceinline__ Quad p2_apply(double2 a, double2 b, double sg, const 
 // touches, so the element pattern is fixed at compile time (no selects).
 
 // dense 2x2 on register bit J
-template <int R, int J> __device__ __forceinline__ void rm1(double2 *a, const double2 *m)
+template <int R, int J, class MT> __device__ __forceinline__ void rm1(double2 *a, MT m)
 {
     const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
 #pragma unroll
@@ -472,7 +485,7 @@ template <int R, int J> __device__ __forceinline__ void rm1(double2 *a, const do
     }
 }
 // sum of Re(conj(f) (dm a)) over the pairs of rm1
-template <int R, int J> __device__ __forceinline__ double rm1_dot(const double2 *a, const double2 *f, const double2 *dm)
+template <int R, int J, class MT> __device__ __forceinline__ double rm1_dot(const double2 *a, const double2 *f, MT dm)
 {
     const double2 m00 = dm[0], m01 = dm[1], m10 = dm[2], m11 = dm[3];
     double s = 0;
@@ -485,7 +498,7 @@ template <int R, int J> __device__ __forceinline__ double rm1_dot(const double2 
     return s;
 }
 // dense 2x2 on register bit J where register bit C is 1 (controlled gates)
-template <int R, int J, int C> __device__ __forceinline__ void rm1c(double2 *a, const double2 *m)
+template <int R, int J, int C, class MT> __device__ __forceinline__ void rm1c(double2 *a, MT m)
 {
     const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
 #pragma unroll
@@ -497,8 +510,8 @@ template <int R, int J, int C> __device__ __forceinline__ void rm1c(double2 *a, 
         a[kk] = zmul2(m10, x, m11, y);
     }
 }
-template <int R, int J, int C>
-__device__ __forceinline__ double rm1c_dot(const double2 *a, const double2 *f, const double2 *dm)
+template <int R, int J, int C, class MT>
+__device__ __forceinline__ double rm1c_dot(const double2 *a, const double2 *f, MT dm)
 {
     const double2 m00 = dm[0], m01 = dm[1], m10 = dm[2], m11 = dm[3];
     double s = 0;
@@ -559,7 +572,7 @@ template <int R> __device__ __forceinline__ double rscale_dot(const double2 *a, 
 
 // dense 4x4 on register bits (LO = the op's first qubit, HI = its second):
 // local index 2*bit(q0) + bit(q1) = 2*bit(LO) + bit(HI)
-template <int R, int LO, int HI> __device__ __forceinline__ void rm2(double2 *a, const double2 *m)
+template <int R, int LO, int HI, class MT> __device__ __forceinline__ void rm2(double2 *a, MT m)
 {
 #pragma unroll
     for (int k = 0; k < (1 << R); k++) {
@@ -572,7 +585,7 @@ template <int R, int LO, int HI> __device__ __forceinline__ void rm2(double2 *a,
         a[k11] = zadd(zmul2(m[12], v00, m[13], v01), zmul2(m[14], v10, m[15], v11));
     }
 }
-template <int R, int LO, int HI> __device__ __forceinline__ double rm2_dot(const double2 *a, const double2 *f, const double2 *m)
+template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rm2_dot(const double2 *a, const double2 *f, MT m)
 {
     double s = 0;
 #pragma unroll
@@ -589,7 +602,7 @@ template <int R, int LO, int HI> __device__ __forceinline__ double rm2_dot(const
 }
 // excitation preserving on (LO = q0, HI = q1): m = {p00, b00, b01, b10, b11, p11};
 // out01 = b00 v01 + b01 v10, out10 = b10 v01 + b11 v10
-template <int R, int LO, int HI> __device__ __forceinline__ void rf2(double2 *a, const double2 *m)
+template <int R, int LO, int HI, class MT> __device__ __forceinline__ void rf2(double2 *a, MT m)
 {
     const double2 p00 = m[0], b00 = m[1], b01 = m[2], b10 = m[3], b11 = m[4], p11 = m[5];
 #pragma unroll
@@ -603,7 +616,7 @@ template <int R, int LO, int HI> __device__ __forceinline__ void rf2(double2 *a,
         a[k11] = zmul(p11, a[k11]);
     }
 }
-template <int R, int LO, int HI> __device__ __forceinline__ double rf2_dot(const double2 *a, const double2 *f, const double2 *m)
+template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rf2_dot(const double2 *a, const double2 *f, MT m)
 {
     const double2 p00 = m[0], b00 = m[1], b01 = m[2], b10 = m[3], b11 = m[4], p11 = m[5];
     double s = 0;
@@ -737,7 +750,7 @@ __device__ __forceinline__ DiagPlan diag_plan(const PassOp &op, uint32_t base, u
     return d;
 }
 
-template <int R> __device__ __forceinline__ void reg_diag(const DiagPlan &d, const double2 *m, double2 *a)
+template <int R, class MT> __device__ __forceinline__ void reg_diag(const DiagPlan &d, MT m, double2 *a)
 {
     if (d.mode == 0) {
         rscale<R>(a, m[d.e[0]]);
@@ -749,7 +762,7 @@ template <int R> __device__ __forceinline__ void reg_diag(const DiagPlan &d, con
         TQ_PAIR_SWITCH(R, d.j0, d.j1, (rd2<R, lo_, hi_>(a, e0, e1, e2, e3)))
     }
 }
-template <int R> __device__ __forceinline__ double reg_diag_dot(const DiagPlan &d, const double2 *m, const double2 *a, const double2 *f)
+template <int R, class MT> __device__ __forceinline__ double reg_diag_dot(const DiagPlan &d, MT m, const double2 *a, const double2 *f)
 {
     double s = 0;
     if (d.mode == 0) {
@@ -773,7 +786,7 @@ __device__ __forceinline__ int reg_ctrl(const PassOp &op, uint32_t base, uint64_
 }
 
 // forward op on registers
-template <int R> __device__ __forceinline__ void reg_op(const PassOp &op, const double2 *m, double2 *a, uint32_t base, uint64_t fb)
+template <int R, class MT> __device__ __forceinline__ void reg_op(const PassOp &op, MT m, double2 *a, uint32_t base, uint64_t fb)
 {
     switch (op.kind) {
     case K_M1: {
@@ -800,8 +813,8 @@ template <int R> __device__ __forceinline__ void reg_op(const PassOp &op, const 
 
 // reverse op on registers: a <- W^dagger a (m = W^dagger); g_j += sum Re(conj(f) dW_j a);
 // f <- W^dagger f
-template <int R>
-__device__ __forceinline__ void reg_rev_op(const PassOp &op, const double2 *m, const double2 *d0, const double2 *d1,
+template <int R, class MT>
+__device__ __forceinline__ void reg_rev_op(const PassOp &op, MT m, MT d0, MT d1,
                                            double2 *a, double2 *f, uint32_t base, uint64_t fb, double &g0, double &g1)
 {
     switch (op.kind) {
@@ -885,66 +898,76 @@ template <int R> __device__ __forceinline__ uint32_t stage_base(const Stage &st,
 
 // One forward stage over a tile of 2^t amplitudes in LDS.  M holds the
 // matrices from row-block offset mbase on.
-template <int R>
-__device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lds, int t, uint64_t fb)
+template <int R, class MT>
+__device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lds, int t, uint64_t fb,
+                                          int tid, int nt)
 {
+    // sw() is linear over xor and base, off[k] have disjoint bits, so the
+    // swizzled address of base | off[k] is sw(base) ^ sw(off[k])
     uint32_t off[1 << R];
     stage_offsets<R>(st, off);
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) off[k] = sw(off[k]);
     const uint32_t nitems = 1u << (t - R);
-    for (uint32_t item = threadIdx.x; item < nitems; item += blockDim.x) {
-        const uint32_t base = stage_base<R>(st, item);
+    for (uint32_t item = tid; item < nitems; item += nt) {
+        const uint32_t base = stage_base<R>(st, item), sb = sw(base);
         double2 a[1 << R];
 #pragma unroll
-        for (int k = 0; k < (1 << R); k++) a[k] = up2(lds[sw(base | off[k])]);
+        for (int k = 0; k < (1 << R); k++) a[k] = up2(lds[sb ^ off[k]]);
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
             const PassOp op = cget(ops, oi);
             reg_op<R>(op, M + (op.mat - mbase), a, base, fb);
         }
 #pragma unroll
-        for (int k = 0; k < (1 << R); k++) lds[sw(base | off[k])] = down2(a[k]);
+        for (int k = 0; k < (1 << R); k++) lds[sb ^ off[k]] = down2(a[k]);
     }
 }
 
-__device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lds, int t, uint64_t fb)
+// tid / nt: this thread's index among the nt threads that share the tile
+template <class MT>
+__device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lds, int t,
+                                              uint64_t fb, int tid, int nt)
 {
     switch (st.r) {
     case 4:
-        if constexpr (kStageBitsFwd >= 4) run_stage<4>(st, ops, M, mbase, lds, t, fb);
+        if constexpr (kStageBitsFwd >= 4) run_stage<4>(st, ops, M, mbase, lds, t, fb, tid, nt);
         break;
-    case 3: run_stage<3>(st, ops, M, mbase, lds, t, fb); break;
-    case 2: run_stage<2>(st, ops, M, mbase, lds, t, fb); break;
-    case 1: run_stage<1>(st, ops, M, mbase, lds, t, fb); break;
-    default: run_stage<0>(st, ops, M, mbase, lds, t, fb); break;
+    case 3: run_stage<3>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
+    case 2: run_stage<2>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
+    case 1: run_stage<1>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
+    default: run_stage<0>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
     }
 }
 
 // One reverse stage on the psi and phi tiles.  Every thread runs the same
 // number of item iterations so that the wavefront reductions of the gradient
 // contributions see whole waves; acc[wave * astride + slot - abase].
-template <int R>
-__device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lp, float2 *lf,
-                              int t, uint64_t fb, double *acc, int astride, int abase)
+template <int R, class MT>
+__device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lp, float2 *lf,
+                              int t, uint64_t fb, double *acc, int astride, int abase, int tid, int nt)
 {
     uint32_t off[1 << R];
     stage_offsets<R>(st, off);
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) off[k] = sw(off[k]);  // see run_stage
     const uint32_t nitems = 1u << (t - R);
-    const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
-    const uint32_t iters = (nitems + blockDim.x - 1) / blockDim.x;
+    const int wave = tid / 64, lane = tid % 64;
+    const uint32_t iters = (nitems + nt - 1) / nt;
     for (uint32_t it = 0; it < iters; it++) {
-        const uint32_t item = it * blockDim.x + threadIdx.x;
+        const uint32_t item = it * nt + tid;
         const bool active = item < nitems;
-        const uint32_t base = stage_base<R>(st, active ? item : 0);
+        const uint32_t base = stage_base<R>(st, active ? item : 0), sb = sw(base);
         double2 a[1 << R], f[1 << R];
 #pragma unroll
         for (int k = 0; k < (1 << R); k++) {
-            a[k] = active ? up2(lp[sw(base | off[k])]) : make_double2(0, 0);
-            f[k] = active ? up2(lf[sw(base | off[k])]) : make_double2(0, 0);
+            a[k] = active ? up2(lp[sb ^ off[k]]) : make_double2(0, 0);
+            f[k] = active ? up2(lf[sb ^ off[k]]) : make_double2(0, 0);
         }
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
             const PassOp op = cget(ops, oi);
-            const double2 *m = M + (op.mat - mbase);
-            const double2 *d0 = M + (op.ngrad > 0 ? op.dmat[0] - mbase : 0);
-            const double2 *d1 = M + (op.ngrad > 1 ? op.dmat[1] - mbase : 0);
+            const MT m = M + (op.mat - mbase);
+            const MT d0 = M + (op.ngrad > 0 ? op.dmat[0] - mbase : 0);
+            const MT d1 = M + (op.ngrad > 1 ? op.dmat[1] - mbase : 0);
             double g0 = 0, g1 = 0;
             reg_rev_op<R>(op, m, d0, d1, a, f, base, fb, g0, g1);
             if (op.ngrad > 0) {
@@ -959,23 +982,24 @@ __device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops
         if (active) {
 #pragma unroll
             for (int k = 0; k < (1 << R); k++) {
-                lp[sw(base | off[k])] = down2(a[k]);
-                lf[sw(base | off[k])] = down2(f[k]);
+                lp[sb ^ off[k]] = down2(a[k]);
+                lf[sb ^ off[k]] = down2(f[k]);
             }
         }
     }
 }
 
-__device__ __forceinline__ void run_rev_stage_any(const Stage &st, const PassOp *ops, const double2 *M, int mbase, float2 *lp, float2 *lf,
-                                  int t, uint64_t fb, double *acc, int astride, int abase)
+template <class MT>
+__device__ __forceinline__ void run_rev_stage_any(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lp, float2 *lf,
+                                  int t, uint64_t fb, double *acc, int astride, int abase, int tid, int nt)
 {
     switch (st.r) {
     case 3:
-        if constexpr (kStageBitsRev >= 3) run_rev_stage<3>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase);
+        if constexpr (kStageBitsRev >= 3) run_rev_stage<3>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt);
         break;
-    case 2: run_rev_stage<2>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
-    case 1: run_rev_stage<1>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
-    default: run_rev_stage<0>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase); break;
+    case 2: run_rev_stage<2>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt); break;
+    case 1: run_rev_stage<1>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt); break;
+    default: run_rev_stage<0>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt); break;
     }
 }
 
@@ -986,7 +1010,7 @@ __device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_bloc
 }
 
 // ------------------------------------------------------- forward pass
-__global__ __launch_bounds__(256) void k_pass(PassArgs a)
+__global__ __launch_bounds__(256, 4) void k_pass(PassArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const TileGeom &g = a.g;
@@ -1045,7 +1069,7 @@ __global__ __launch_bounds__(256) void k_pass(PassArgs a)
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_stage_any(st, a.ops, M, a.mat_begin, lds, t, fb);
+            run_stage_any(st, a.ops, M, a.mat_begin, lds, t, fb, threadIdx.x, blockDim.x);
             __syncthreads();
         }
         tile_copy<false>(tc, lds, st, fb, T);
@@ -1072,10 +1096,9 @@ __device__ __forceinline__ double re_iny(int ny, double s, double2 A)
 }
 
 __device__ double term_tile_sum(const TermDev &tm, const TileCtx &tc, const float2 *lds, const float2 *row, uint64_t fb,
-                                int t)
+                                int t, int tid, int nt)
 {
     const uint32_t T = 1u << t;
-    const int tid = threadIdx.x, nt = blockDim.x;
     double acc = 0;
     if (tm.x == 0) {
         const int zf = par64(fb & tm.z);
@@ -1342,7 +1365,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_rev_stage_any(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase);
+            run_rev_stage_any(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase, threadIdx.x, blockDim.x);
             __syncthreads();
         }
         if (a.store) {
@@ -1377,74 +1400,75 @@ __global__ void k_grad_reduce(GradReduceArgs a)
 
 // ---------------------------------------------------- resident circuits
 // Small circuits (psi, phi and every matrix of the row fit in LDS): one
-// workgroup per batch row does the whole call -- matrix build, product-state
-// init, forward gates, expectations, H_g, reverse sweep, gradient reduction --
-// in one launch.  Outputs are reduced in a fixed order inside the workgroup.
-__global__ __launch_bounds__(256) void k_resident(ResArgs a)
+// workgroup per batch row does the whole call -- product-state init, forward
+// gates, expectations, H_g, reverse sweep, gradient reduction -- in one
+// launch, on the matrices k_build_mats wrote.  At most 128 registers per
+// thread, so that four rows share a CU.  Outputs are reduced in a fixed order.
+template <class MT>
+__device__ __forceinline__ void resident_row(const ResArgs &a, MT M, double *acc, float2 *lp, float2 *lf, int row, int tid,
+                                             int nt)
 {
-    extern __shared__ __align__(16) unsigned char smem[];
     const int n = a.n;
     const uint32_t T = 1u << n;
-    const int row = blockIdx.x;
     const int b = cget(a.rows, row);
-    const int tid = threadIdx.x, nt = blockDim.x;
     const int wave = tid / 64, lane = tid % 64;
-    double2 *lm = reinterpret_cast<double2 *>(smem);                      // [mat_block]
-    double *acc = reinterpret_cast<double *>(lm + a.mat_block);           // [4][nacc]
-    float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);            // [T]
-    float2 *lf = lp + T;                                                  // [T] (adjoint)
+    const int nw = nt / 64;  // accumulator copies, one per wave
+    auto sync = [] { __syncthreads(); };
     // whole-state tile: every term's partner is local, so the tile index
     // table and the HBM partner pointer are never used (valid LDS addresses
     // are passed instead of null pointers)
     TileCtx tc{reinterpret_cast<const uint64_t *>(acc), T - 1, n};
 
-    // 1. the row's fused matrices (built by k_build_mats) into LDS
-    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, 0, a.mat_block);
-    for (int j = tid; j < 4 * a.nacc; j += nt) acc[j] = 0;
-    __syncthreads();
-    // 2. product-state initialisation
+    for (int j = tid; j < nw * a.nacc; j += nt) acc[j] = 0;
+    // product-state initialisation
     for (uint32_t l = tid; l < T; l += nt) {
         double2 v = make_double2(1.0, 0.0);
-        for (int q = 0; q < n; q++) v = zmul(v, lm[a.init_mat[q] + (((l >> (n - 1 - q)) & 1) ? 2 : 0)]);
+        for (int q = 0; q < n; q++) v = zmul(v, M[a.init_mat[q] + (((l >> (n - 1 - q)) & 1) ? 2 : 0)]);
         lp[sw(l)] = down2(v);
     }
-    __syncthreads();
-    // 3. forward gates
+    sync();
+    // forward gates
     for (int si = 0; si < a.nfstages; si++) {
         const Stage st = cget(a.fstages, si);
-        run_stage_any(st, a.fops, lm, 0, lp, n, 0);
-        __syncthreads();
+        run_stage_any(st, a.fops, M, 0, lp, n, 0, tid, nt);
+        sync();
     }
-    // 4. state output and expectation terms
+    // state output and expectation terms
     if (a.state_out) {
         float2 *out = a.state_out + (int64_t)a.out_rows[row] * a.out_stride;
         for (uint32_t l = tid; l < T; l += nt) out[l] = lp[sw(l)];
     }
-    const TermDev *terms = a.terms ? a.terms + a.row_term_begin[row] : nullptr;
-    const int nterm = a.terms ? a.row_term_count[row] : 0;
+    const TermDev *terms = a.terms ? a.terms + cget(a.row_term_begin, row) : nullptr;
+    const int nterm = a.terms ? cget(a.row_term_count, row) : 0;
     for (int k = 0; k < nterm; k++) {
-        double v = wave_sum(term_tile_sum(cget(terms, k), tc, lp, lp, 0, n));
+        double v = wave_sum(term_tile_sum(cget(terms, k), tc, lp, lp, 0, n, tid, nt));
         if (lane == 0) acc[wave * a.nacc + k] += v;
     }
-    // 5. adjoint sweep
+    // adjoint sweep
     if (a.grad) {
         const float *up = a.upstream + (int64_t)b * a.K;
         for (uint32_t l = tid; l < T; l += nt) lf[sw(l)] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
-        __syncthreads();
+        sync();
         for (int si = 0; si < a.nrstages; si++) {
             const Stage st = cget(a.rstages, si);
-            run_rev_stage_any(st, a.rops, lm, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc);
-            __syncthreads();
+            run_rev_stage_any(st, a.rops, M, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc, tid, nt);
+            sync();
         }
     }
-    __syncthreads();
-    // 6. outputs
-    auto total = [&](int j) { return ((acc[j] + acc[a.nacc + j]) + acc[2 * a.nacc + j]) + acc[3 * a.nacc + j]; };
+    sync();
+    // outputs
+    auto total = [&](int j) {
+        double s = 0;
+        for (int w = 0; w < nw; w++) s += acc[w * a.nacc + j];
+        return s;
+    };
     if (a.exp_out)
         for (int k = tid; k < a.K; k += nt) {
             double sum = 0;
-            for (int ti = 0; ti < nterm; ti++)
-                if (terms[ti].k == k) sum += terms[ti].coeff * total(ti);
+            for (int ti = 0; ti < nterm; ti++) {
+                const TermDev tm = cget(terms, ti);
+                if (tm.k == k) sum += tm.coeff * total(ti);
+            }
             a.exp_out[(int64_t)b * a.K + k] = (float)sum;
         }
     if (a.grad) {
@@ -1458,6 +1482,16 @@ __global__ __launch_bounds__(256) void k_resident(ResArgs a)
             a.grad[(int64_t)b * a.S + s] = (float)sum;
         }
     }
+}
+
+__global__ __launch_bounds__(256, 4) void k_resident(ResArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const uint32_t T = 1u << a.n;
+    double *acc = reinterpret_cast<double *>(smem);              // [4][nacc]
+    float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);   // [T]
+    float2 *lf = lp + T;                                         // [T] (adjoint)
+    resident_row(a, smat(a.mats + (int64_t)blockIdx.x * a.mat_stride), acc, lp, lf, blockIdx.x, threadIdx.x, blockDim.x);
 }
 
 // ------------------------------------------------------------- sampling
@@ -1563,12 +1597,12 @@ __global__ __launch_bounds__(256) void k_samp_shots(SampArgs a)
 __global__ void k_gather(GatherArgs a)
 {
     const int row = blockIdx.y;
-    const int b = a.brows[row];
+    const int b = a.brows ? a.brows[row] : row;
     const int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (m >= a.M) return;
     const uint64_t x = a.bits[(int64_t)b * a.M + m];
     float2 v = make_float2(0.f, 0.f);
-    if ((x >> a.n) == 0) v = a.state[(int64_t)a.rows[row] * a.row_stride + (int64_t)x];
+    if ((x >> a.n) == 0) v = a.state[(int64_t)(a.rows ? a.rows[row] : row) * a.row_stride + (int64_t)x];
     a.out[(int64_t)b * a.M + m] = v;
 }
 
@@ -1731,16 +1765,15 @@ hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s)
     return hipGetLastError();
 }
 
-size_t resident_lds_bytes(int n, int nmat, int nacc, bool adjoint)
+size_t resident_lds_bytes(int n, int nacc, bool adjoint)
 {
-    return sizeof(double2) * (size_t)nmat + sizeof(double) * 4 * (size_t)nacc +
-           sizeof(float2) * ((size_t)1 << n) * (adjoint ? 2 : 1);
+    return sizeof(double) * 4 * (size_t)nacc + sizeof(float2) * ((size_t)1 << n) * (adjoint ? 2 : 1);
 }
 
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s)
 {
     if (nrows <= 0) return hipSuccess;
-    size_t lds = resident_lds_bytes(a.n, a.mat_block, a.nacc, a.grad != nullptr);
+    size_t lds = resident_lds_bytes(a.n, a.nacc, a.grad != nullptr);
     hipError_t e = set_lds(k_resident, lds);
     if (e != hipSuccess) return e;
     prof::Scope ps("resident", s);

@@ -436,9 +436,8 @@ bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
 {
     const Group &g = *p->pd->groups[gi];
     if (g.n > std::min(p->pd->opt.tile, 12)) return false;
-    const int nmat = std::max(adjoint ? g.mat_block : g.fwd_mat_end, 1);
     const int nacc = std::max(tmax + (adjoint ? g.n_gslots : 0), 1);
-    return resident_lds_bytes(g.n, nmat, nacc, adjoint) <= kResidentLds;
+    return resident_lds_bytes(g.n, nacc, adjoint) <= kResidentLds;
 }
 
 ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint, hipStream_t s)
@@ -454,7 +453,6 @@ ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint,
     a.n_slots = g.n_slots;
     a.S = p->pd->S;
     a.rows = (const int32_t *)gd.rows.p;
-    a.mat_block = std::max(adjoint ? g.mat_block : g.fwd_mat_end, 1);
     a.n = g.n;
     a.fops = (const PassOp *)gd.fwd_ops.p;
     a.fstages = (const Stage *)gd.fwd_stages.p;
@@ -857,6 +855,27 @@ tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t
     });
 }
 
+tq_status tq_amplitudes_from_state(const void *states, int32_t B, int32_t n, const uint64_t *bitstrings, int64_t M,
+                                   void *amps, void *stream)
+{
+    return guarded([&] {
+        if (B < 0 || n < 0 || n > kMaxQubits || M < 0) fail(TQ_E_INVALID, "bad B, n or M");
+        if (B == 0 || M == 0) return;
+        if (!states || !bitstrings || !amps) fail(TQ_E_INVALID, "states, bitstrings or amps is NULL");
+        check_align(states, 8, "states");
+        check_align(bitstrings, 8, "bitstrings");
+        check_align(amps, 8, "amps");
+        GatherArgs a{};
+        a.state = (const float2 *)states;
+        a.row_stride = (int64_t)1 << n;
+        a.n = n;
+        a.bits = bitstrings;
+        a.M = M;
+        a.out = (float2 *)amps;
+        hip_check(launch_gather(a, B, as_stream(stream)), "gather launch");
+    });
+}
+
 tq_status tq_profile_start(const char *kernel)
 {
     return guarded([&] { profile_start(kernel); });
@@ -906,6 +925,13 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
                           << (int)op.p1 << "],\"l\":[" << (int)op.l0 << "," << (int)op.l1 << "],\"ctrl\":" << (int)op.ctrl
                           << ",\"ngrad\":" << (int)op.ngrad << ",\"members\":"
                           << (members_at.count(op.mat) ? members_at[op.mat] : 0) << "}";
+                    }
+                    o << "],\"stages\":[";
+                    for (size_t k = 0; k < ps.stages.size(); k++) {
+                        const Stage &sg = ps.stages[k];
+                        o << (k ? "," : "") << "{\"r\":" << (int)sg.r << ",\"bits\":[";
+                        for (int j = 0; j < sg.r; j++) o << (j ? "," : "") << (int)sg.bits[j];
+                        o << "],\"ops\":" << (sg.op_end - sg.op_begin) << "}";
                     }
                     o << "]}";
                 }

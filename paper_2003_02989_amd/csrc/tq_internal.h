@@ -89,7 +89,7 @@ struct PassOp {
 // most kStageBits tile bits.  Each thread holds the 2^r amplitudes of one
 // "item" (a fixed assignment of the tile bits outside R) in registers while
 // the stage's ops run, so the stage costs one LDS round trip.
-constexpr int kStageBitsFwd = 4;
+constexpr int kStageBitsFwd = 3;
 constexpr int kStageBitsRev = 2;
 struct Stage {
     uint8_t r;        // register bits

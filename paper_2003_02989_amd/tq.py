@@ -58,12 +58,13 @@ def lib():
         L.tq_adjoint_grad.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.tq_amplitudes.argtypes = [vp, vp, vp, i64, vp, vp]
         L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
+        L.tq_amplitudes_from_state.argtypes = [vp, i32, i32, vp, i64, vp, vp]
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
         L.tq_profile_start.argtypes = [ctypes.c_char_p]
         L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
         for f in ("tq_program_create", "tq_program_info", "tq_observables_create", "tq_observables_info",
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_adjoint_grad", "tq_amplitudes",
-                  "tq_sample_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read"):
+                  "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -218,4 +219,20 @@ def sample_from_state(states, n_shots, seed, out=None, stream=None):
         out = torch.empty((B, n_shots), dtype=torch.int64, device="cuda")
     p = _dev(out, torch.int64, (B, n_shots), "out")
     _check(lib().tq_sample_from_state(s, B, n, int(n_shots), ctypes.c_uint64(seed), p, _stream(stream)))
+    return out
+
+
+def amplitudes_from_state(states, bitstrings, out=None, stream=None):
+    """Amplitudes [B, M] of given states [B, 2^n] at bitstrings int64 [B, M]."""
+    B, N = states.shape
+    n = N.bit_length() - 1
+    if (1 << n) != N:
+        raise ValueError("state length must be a power of two")
+    M = bitstrings.shape[1]
+    s = _dev(states, torch.complex64, (B, N), "states")
+    b = _dev(bitstrings, torch.int64, (B, M), "bitstrings")
+    if out is None:
+        out = torch.empty((B, M), dtype=torch.complex64, device="cuda")
+    p = _dev(out, torch.complex64, (B, M), "amps")
+    _check(lib().tq_amplitudes_from_state(s, B, n, b, M, p, _stream(stream)))
     return out

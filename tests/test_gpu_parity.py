@@ -121,3 +121,29 @@ def test_many_observables_and_terms(n, tile):
         w.observables[b][4] = []
     say("many observables", n, tile)
     compare(gpu_outputs(w, max_tile_qubits=tile), oracle_outputs(w))
+
+
+@pytest.mark.gpu
+def test_amplitudes_from_state_matches_amplitudes():
+    # the state-based lookup returns what tq_amplitudes returns, bit for bit,
+    # including out-of-range bitstrings (zero amplitude)
+    w = wl.random_batch(4711, B=3, n=11, n_gates=40, n_symbols=3, K=1)
+    p = tq.Program(w.program_blob())
+    th = dev(w.theta)
+    rng = np.random.default_rng(5)
+    bits = rng.integers(0, 1 << 12, size=(3, 300)).astype(np.int64)
+    b = torch.as_tensor(bits, device="cuda")
+    st = tq.simulate_state(p, th)
+    a1 = tq.amplitudes(p, th, b).cpu().numpy()
+    a2 = tq.amplitudes_from_state(st, b).cpu().numpy()
+    assert np.array_equal(a1, a2)
+    assert np.all(a2[bits >= (1 << 11)] == 0)
+
+
+@pytest.mark.parametrize("n,B", [(3, 5), (6, 9), (10, 7), (11, 3), (12, 2)])
+def test_resident_layouts(n, B):
+    # one wavefront per row (n <= 10; B not a multiple of the four rows of a
+    # workgroup) and one workgroup per row (n = 11, 12)
+    w = wl.random_batch(8800 + n, B=B, n=n, n_gates=70, n_symbols=6, K=2)
+    say("resident", n, B)
+    compare(gpu_outputs(w), oracle_outputs(w))
