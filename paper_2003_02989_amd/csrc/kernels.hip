@@ -839,20 +839,26 @@ __device__ __forceinline__ void reg_rev_op(const PassOp &op, MT m, MT d0, MT d1,
         return;
     }
     case K_M2:
-        TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
-            rm2<R, lo_, hi_>(a, m);
-            if (op.ngrad > 0) g0 += rm2_dot<R, lo_, hi_>(a, f, d0);
-            if (op.ngrad > 1) g1 += rm2_dot<R, lo_, hi_>(a, f, d1);
-            rm2<R, lo_, hi_>(f, m);
-        }))
+        // dense two-qubit ops only occur in stages of at most kRevDense2Bits
+        // register bits (planner): wider instances are not compiled
+        if constexpr (R <= kRevDense2Bits) {
+            TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
+                rm2<R, lo_, hi_>(a, m);
+                if (op.ngrad > 0) g0 += rm2_dot<R, lo_, hi_>(a, f, d0);
+                if (op.ngrad > 1) g1 += rm2_dot<R, lo_, hi_>(a, f, d1);
+                rm2<R, lo_, hi_>(f, m);
+            }))
+        }
         return;
     case K_F2:
-        TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
-            rf2<R, lo_, hi_>(a, m);
-            if (op.ngrad > 0) g0 += rf2_dot<R, lo_, hi_>(a, f, d0);
-            if (op.ngrad > 1) g1 += rf2_dot<R, lo_, hi_>(a, f, d1);
-            rf2<R, lo_, hi_>(f, m);
-        }))
+        if constexpr (R <= kRevDense2Bits) {
+            TQ_PAIR_SWITCH(R, op.s0, op.s1, ({
+                rf2<R, lo_, hi_>(a, m);
+                if (op.ngrad > 0) g0 += rf2_dot<R, lo_, hi_>(a, f, d0);
+                if (op.ngrad > 1) g1 += rf2_dot<R, lo_, hi_>(a, f, d1);
+                rf2<R, lo_, hi_>(f, m);
+            }))
+        }
         return;
     case K_P2: {
         const double sg = op.ptype == 2 ? -1.0 : 1.0;
@@ -939,9 +945,40 @@ __device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops
     }
 }
 
-// One reverse stage on the psi and phi tiles.  Every thread runs the same
-// number of item iterations so that the wavefront reductions of the gradient
-// contributions see whole waves; acc[wave * astride + slot - abase].
+// Register accumulators of a stage's gradient parameters, indexed by a
+// uniform k < kMaxStageGrads (a branch, so that the array stays in registers).
+__device__ __forceinline__ void gadd(double *g, int k, double v)
+{
+    switch (k) {
+    case 0: g[0] += v; break;
+    case 1: g[1] += v; break;
+    case 2: g[2] += v; break;
+    case 3: g[3] += v; break;
+    case 4: g[4] += v; break;
+    case 5: g[5] += v; break;
+    case 6: g[6] += v; break;
+    default: g[7] += v; break;
+    }
+}
+__device__ __forceinline__ double gget(const double *g, int k)
+{
+    switch (k) {
+    case 0: return g[0];
+    case 1: return g[1];
+    case 2: return g[2];
+    case 3: return g[3];
+    case 4: return g[4];
+    case 5: return g[5];
+    case 6: return g[6];
+    default: return g[7];
+    }
+}
+static_assert(kMaxStageGrads == 8, "gadd/gget cover eight accumulators");
+
+// One reverse stage on the psi and phi tiles.  Each thread sums the
+// gradient contributions of its items in registers; after the items, one
+// wavefront reduction per gradient parameter adds into
+// acc[wave * astride + slot - abase].
 template <int R, class MT>
 __device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lp, float2 *lf,
                               int t, uint64_t fb, double *acc, int astride, int abase, int tid, int nt)
@@ -952,17 +989,18 @@ __device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops
     for (int k = 0; k < (1 << R); k++) off[k] = sw(off[k]);  // see run_stage
     const uint32_t nitems = 1u << (t - R);
     const int wave = tid / 64, lane = tid % 64;
-    const uint32_t iters = (nitems + nt - 1) / nt;
-    for (uint32_t it = 0; it < iters; it++) {
-        const uint32_t item = it * nt + tid;
-        const bool active = item < nitems;
-        const uint32_t base = stage_base<R>(st, active ? item : 0), sb = sw(base);
+    double gacc[kMaxStageGrads];
+#pragma unroll
+    for (int j = 0; j < kMaxStageGrads; j++) gacc[j] = 0.0;
+    for (uint32_t item = tid; item < nitems; item += nt) {
+        const uint32_t base = stage_base<R>(st, item), sb = sw(base);
         double2 a[1 << R], f[1 << R];
 #pragma unroll
         for (int k = 0; k < (1 << R); k++) {
-            a[k] = active ? up2(lp[sb ^ off[k]]) : make_double2(0, 0);
-            f[k] = active ? up2(lf[sb ^ off[k]]) : make_double2(0, 0);
+            a[k] = up2(lp[sb ^ off[k]]);
+            f[k] = up2(lf[sb ^ off[k]]);
         }
+        int gk = 0;
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
             const PassOp op = cget(ops, oi);
             const MT m = M + (op.mat - mbase);
@@ -970,32 +1008,35 @@ __device__ __forceinline__ void run_rev_stage(const Stage &st, const PassOp *ops
             const MT d1 = M + (op.ngrad > 1 ? op.dmat[1] - mbase : 0);
             double g0 = 0, g1 = 0;
             reg_rev_op<R>(op, m, d0, d1, a, f, base, fb, g0, g1);
-            if (op.ngrad > 0) {
-                const double v = wave_sum(active ? g0 : 0.0);
-                if (lane == 0) acc[wave * astride + op.gslot[0] - abase] += v;
-            }
-            if (op.ngrad > 1) {
-                const double v = wave_sum(active ? g1 : 0.0);
-                if (lane == 0) acc[wave * astride + op.gslot[1] - abase] += v;
-            }
+            if (op.ngrad > 0) gadd(gacc, gk++, g0);
+            if (op.ngrad > 1) gadd(gacc, gk++, g1);
         }
-        if (active) {
 #pragma unroll
-            for (int k = 0; k < (1 << R); k++) {
-                lp[sb ^ off[k]] = down2(a[k]);
-                lf[sb ^ off[k]] = down2(f[k]);
-            }
+        for (int k = 0; k < (1 << R); k++) {
+            lp[sb ^ off[k]] = down2(a[k]);
+            lf[sb ^ off[k]] = down2(f[k]);
+        }
+    }
+    int gk = 0;
+    for (int oi = st.op_begin; oi < st.op_end; oi++) {
+        const PassOp op = cget(ops, oi);
+        for (int j = 0; j < op.ngrad; j++) {
+            const double v = wave_sum(gget(gacc, gk++));
+            const int slot = j == 0 ? op.gslot[0] : op.gslot[1];
+            if (lane == 0) acc[wave * astride + slot - abase] += v;
         }
     }
 }
 
-template <class MT>
+// kRMax: the widest stage the caller's plans contain (narrower kernels
+// compile fewer register variants)
+template <int kRMax, class MT>
 __device__ __forceinline__ void run_rev_stage_any(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lp, float2 *lf,
                                   int t, uint64_t fb, double *acc, int astride, int abase, int tid, int nt)
 {
     switch (st.r) {
     case 3:
-        if constexpr (kStageBitsRev >= 3) run_rev_stage<3>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt);
+        if constexpr (kRMax >= 3) run_rev_stage<3>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt);
         break;
     case 2: run_rev_stage<2>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt); break;
     case 1: run_rev_stage<1>(st, ops, M, mbase, lp, lf, t, fb, acc, astride, abase, tid, nt); break;
@@ -1365,7 +1406,7 @@ __global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_rev_stage_any(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase, threadIdx.x, blockDim.x);
+            run_rev_stage_any<kStageBitsRev>(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase, threadIdx.x, blockDim.x);
             __syncthreads();
         }
         if (a.store) {
@@ -1451,7 +1492,7 @@ __device__ __forceinline__ void resident_row(const ResArgs &a, MT M, double *acc
         sync();
         for (int si = 0; si < a.nrstages; si++) {
             const Stage st = cget(a.rstages, si);
-            run_rev_stage_any(st, a.rops, M, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc, tid, nt);
+            run_rev_stage_any<kStageBitsRevResident>(st, a.rops, M, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc, tid, nt);
             sync();
         }
     }

@@ -259,15 +259,20 @@ struct Planner {
 // control bits outside R read their bit from the item's base index.  R is
 // padded with the highest free tile bits, so that the items of neighbouring
 // lanes sit at neighbouring LDS addresses.
-void make_stages(Pass &ps, int rmax, Group &g, const std::map<int32_t, int> &task_at)
+// Split a pass's ops into register stages of at most rmax bits; a stage that
+// holds a dense 4x4 or fSim-type op has at most rdense bits.
+void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at)
 {
     const int t = ps.geom.t;
-    const int r = std::min(rmax, t);
+    int r = std::min(rmax, t);
+    const int rd = std::min(rdense, r);
+    bool dense = false;  // the open stage holds a dense two-qubit op
     ps.stages.clear();
     std::vector<int> R;
     int begin = 0;
     auto close = [&](int end) {
         if (end <= begin) return;
+        const int r = dense ? rd : std::min(rmax, t);
         Stage st{};
         std::vector<int> bits = R;
         for (int b = t - 1; b >= 0 && (int)bits.size() < r; b--)
@@ -304,6 +309,7 @@ void make_stages(Pass &ps, int rmax, Group &g, const std::map<int32_t, int> &tas
         R.clear();
         begin = end;
     };
+    int ngrad = 0;  // gradient parameters of the open stage
     for (int k = 0; k < (int)ps.ops.size(); k++) {
         const PassOp &op = ps.ops[k];
         std::vector<int> need;
@@ -312,14 +318,19 @@ void make_stages(Pass &ps, int rmax, Group &g, const std::map<int32_t, int> &tas
             need.push_back(op.l0);
             need.push_back(op.l1);
         }
+        const bool d = op.kind == K_M2 || op.kind == K_F2;
         std::vector<int> u = R;
         for (int b : need)
             if (std::find(u.begin(), u.end(), b) == u.end()) u.push_back(b);
-        if ((int)u.size() > r) {
+        if ((int)u.size() > ((dense || d) ? rd : r) || ngrad + op.ngrad > kMaxStageGrads) {
             close(k);
             u = need;
+            ngrad = 0;
+            dense = false;
         }
         R = u;
+        ngrad += op.ngrad;
+        dense = dense || d;
     }
     close((int)ps.ops.size());
 }
@@ -575,13 +586,13 @@ void plan_group(Group &g, const Options &opt, int S)
     int off = 0;
     for (Pass &ps : g.fwd) {
         ps.op_offset = off;
-        make_stages(ps, kStageBitsFwd, g, task_at);
+        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at);
         off += (int)ps.ops.size();
     }
     off = 0;
     for (Pass &ps : g.rev) {
         ps.op_offset = off;
-        make_stages(ps, kStageBitsRev, g, task_at);
+        make_stages(ps, n <= std::min(opt.tile, 12) ? kStageBitsRevResident : kStageBitsRev, kRevDense2Bits, g, task_at);
         off += (int)ps.ops.size();
     }
 

@@ -436,6 +436,11 @@ bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
 {
     const Group &g = *p->pd->groups[gi];
     if (g.n > std::min(p->pd->opt.tile, 12)) return false;
+    // the resident kernel is compiled for reverse stages of at most
+    // kStageBitsRevResident bits (the planner's choice for such circuits)
+    for (const Pass &ps : g.rev)
+        for (const Stage &st : ps.stages)
+            if (st.r > kStageBitsRevResident) return false;
     const int nacc = std::max(tmax + (adjoint ? g.n_gslots : 0), 1);
     return resident_lds_bytes(g.n, nacc, adjoint) <= kResidentLds;
 }

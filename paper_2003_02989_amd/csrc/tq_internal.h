@@ -90,7 +90,12 @@ struct PassOp {
 // "item" (a fixed assignment of the tile bits outside R) in registers while
 // the stage's ops run, so the stage costs one LDS round trip.
 constexpr int kStageBitsFwd = 3;
-constexpr int kStageBitsRev = 2;
+constexpr int kStageBitsRev = 3;
+constexpr int kRevDense2Bits = 2;  // reverse stages holding a dense 4x4 or fSim-type op
+constexpr int kStageBitsRevResident = 2;  // circuits small enough for the resident kernel
+// Gradient parameters of one reverse stage: each thread keeps their partial
+// sums in registers over the stage's items.
+constexpr int kMaxStageGrads = 8;
 struct Stage {
     uint8_t r;        // register bits
     uint8_t bits[4];  // their tile-local positions, ascending
