@@ -15,6 +15,7 @@
 #include <algorithm>
 #include <cstring>
 #include <map>
+#include <set>
 
 #include "../../include/tq.h"
 
@@ -254,38 +255,144 @@ struct Planner {
     }
 };
 
-// Group a pass's ops into register stages: consecutive ops whose dense
-// (non-diagonal) tile bits fit a set R of at most rmax bits.  Diagonal ops and
-// control bits outside R read their bit from the item's base index.  R is
-// padded with the highest free tile bits, so that the items of neighbouring
-// lanes sit at neighbouring LDS addresses.
-// Split a pass's ops into register stages of at most rmax bits; a stage that
-// holds a dense 4x4 or fSim-type op has at most rdense bits.
+// Group a pass's ops into register stages: sets of ops whose dense
+// (non-diagonal) tile bits fit a set R of at most rmax bits (rdense when the
+// stage holds a dense 4x4 or fSim-type op) and that hold at most
+// kMaxStageGrads gradient parameters.  Diagonal ops and control bits outside
+// R read their bit from the item's base index.  Ops that share no qubit
+// commute, so the ops are reordered within their dependency order (ops on a
+// common qubit keep their order): each stage starts from the earliest ready
+// op and grows R by the bits that make the most ready ops fit, taking every
+// op that fits.  R is padded with the highest free tile bits, so that the
+// items of neighbouring lanes sit at neighbouring LDS addresses.
 void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at)
 {
     const int t = ps.geom.t;
-    int r = std::min(rmax, t);
+    const int r = std::min(rmax, t);
     const int rd = std::min(rdense, r);
-    bool dense = false;  // the open stage holds a dense two-qubit op
+    const int nops = (int)ps.ops.size();
     ps.stages.clear();
-    std::vector<int> R;
-    int begin = 0;
-    auto close = [&](int end) {
-        if (end <= begin) return;
-        const int r = dense ? rd : std::min(rmax, t);
-        Stage st{};
-        std::vector<int> bits = R;
-        for (int b = t - 1; b >= 0 && (int)bits.size() < r; b--)
+
+    // register bits an op needs, the qubits (global bits) it acts on
+    auto need = [](const PassOp &op) {
+        std::vector<int> v;
+        if (op.kind == K_M1) v.push_back(op.l0);
+        if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2) {
+            v.push_back(op.l0);
+            v.push_back(op.l1);
+        }
+        return v;
+    };
+    auto is_dense = [](const PassOp &op) { return op.kind == K_M2 || op.kind == K_F2; };
+    std::vector<std::vector<int>> succ(nops);
+    std::vector<int> indeg(nops, 0);
+    {
+        std::map<int, int> last;  // qubit -> latest op on it
+        for (int k = 0; k < nops; k++) {
+            const PassOp &op = ps.ops[k];
+            std::vector<int> qs{op.p0};
+            if (op.kind != K_D1 && (op.kind != K_M1 || op.ctrl)) qs.push_back(op.p1);
+            std::vector<int> preds;
+            for (int q : qs) {
+                auto it = last.find(q);
+                if (it != last.end() && std::find(preds.begin(), preds.end(), it->second) == preds.end())
+                    preds.push_back(it->second);
+                last[q] = k;
+            }
+            for (int pr : preds) succ[pr].push_back(k);
+            indeg[k] = (int)preds.size();
+        }
+    }
+    std::set<int> ready;
+    for (int k = 0; k < nops; k++)
+        if (indeg[k] == 0) ready.insert(k);
+    std::vector<int> order;
+    std::vector<std::pair<std::vector<int>, std::pair<int, int>>> stage_list;  // (R, [begin, end) in order)
+    while (!ready.empty()) {
+        std::vector<int> R;
+        bool dense = false;
+        int ngrad = 0;
+        const int begin = (int)order.size();
+        auto union_with = [&](const std::vector<int> &bits) {
+            std::vector<int> u = R;
+            for (int b : bits)
+                if (std::find(u.begin(), u.end(), b) == u.end()) u.push_back(b);
+            return u;
+        };
+        auto fits = [&](int k, const std::vector<int> &bits, bool dense_now) {
+            const PassOp &op = ps.ops[k];
+            if (ngrad + op.ngrad > kMaxStageGrads) return false;
+            for (int b : need(op))
+                if (std::find(bits.begin(), bits.end(), b) == bits.end()) return false;
+            return !((dense_now || is_dense(op)) && (int)bits.size() > rd);
+        };
+        for (;;) {
+            // take every ready op that fits R, until none does
+            bool took = true;
+            while (took) {
+                took = false;
+                for (auto it = ready.begin(); it != ready.end(); ++it) {
+                    const int k = *it;
+                    if (!fits(k, R, dense)) continue;
+                    order.push_back(k);
+                    ngrad += ps.ops[k].ngrad;
+                    dense = dense || is_dense(ps.ops[k]);
+                    ready.erase(it);
+                    for (int sk : succ[k])
+                        if (--indeg[sk] == 0) ready.insert(sk);
+                    took = true;
+                    break;
+                }
+            }
+            // grow R by the bits of the ready op that lets the most ready ops fit
+            int best = -1, best_score = -1;
+            std::vector<int> best_u;
+            int considered = 0;
+            for (int k : ready) {
+                if (++considered > 64) break;
+                const PassOp &op = ps.ops[k];
+                if (ngrad + op.ngrad > kMaxStageGrads) continue;
+                std::vector<int> u = union_with(need(op));
+                const bool dn = dense || is_dense(op);
+                if ((int)u.size() > (dn ? rd : r)) continue;
+                int score = 0;
+                for (int j : ready)
+                    if (fits(j, u, dn)) score++;
+                if (score > best_score) {
+                    best = k;
+                    best_score = score;
+                    best_u = u;
+                }
+            }
+            if (best < 0) break;
+            R = best_u;
+        }
+        stage_list.push_back({R, {begin, (int)order.size()}});
+        if ((int)order.size() == begin) fail(TQ_E_UNSUPPORTED, "internal planner error: empty stage");
+    }
+    if ((int)order.size() != nops) fail(TQ_E_UNSUPPORTED, "internal planner error: op dependency cycle");
+    std::vector<PassOp> ops(nops);
+    for (int k = 0; k < nops; k++) ops[k] = ps.ops[order[k]];
+    ps.ops = std::move(ops);
+
+    for (auto &sl : stage_list) {
+        const int begin = sl.second.first, end = sl.second.second;
+        bool dense = false;
+        for (int k = begin; k < end; k++) dense = dense || is_dense(ps.ops[k]);
+        const int rs = dense ? rd : r;
+        std::vector<int> bits = sl.first;
+        for (int b = t - 1; b >= 0 && (int)bits.size() < rs; b--)
             if (std::find(bits.begin(), bits.end(), b) == bits.end()) bits.push_back(b);
         std::sort(bits.begin(), bits.end());
-        st.r = (uint8_t)r;
-        for (int j = 0; j < r; j++) st.bits[j] = (uint8_t)bits[j];
+        Stage st{};
+        st.r = (uint8_t)rs;
+        for (int j = 0; j < rs; j++) st.bits[j] = (uint8_t)bits[j];
         st.op_begin = ps.op_offset + begin;
         st.op_end = ps.op_offset + end;
         for (int k = begin; k < end; k++) {
             PassOp &op = ps.ops[k];
             auto idx = [&](uint8_t l) -> uint8_t {
-                for (int j = 0; j < r; j++)
+                for (int j = 0; j < rs; j++)
                     if (l != kFixed && bits[j] == l) return (uint8_t)j;
                 return kFixed;
             };
@@ -306,33 +413,7 @@ void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_
             }
         }
         ps.stages.push_back(st);
-        R.clear();
-        begin = end;
-    };
-    int ngrad = 0;  // gradient parameters of the open stage
-    for (int k = 0; k < (int)ps.ops.size(); k++) {
-        const PassOp &op = ps.ops[k];
-        std::vector<int> need;
-        if (op.kind == K_M1) need.push_back(op.l0);
-        if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2) {
-            need.push_back(op.l0);
-            need.push_back(op.l1);
-        }
-        const bool d = op.kind == K_M2 || op.kind == K_F2;
-        std::vector<int> u = R;
-        for (int b : need)
-            if (std::find(u.begin(), u.end(), b) == u.end()) u.push_back(b);
-        if ((int)u.size() > ((dense || d) ? rd : r) || ngrad + op.ngrad > kMaxStageGrads) {
-            close(k);
-            u = need;
-            ngrad = 0;
-            dense = false;
-        }
-        R = u;
-        ngrad += op.ngrad;
-        dense = dense || d;
     }
-    close((int)ps.ops.size());
 }
 
 // Append a pass, split into consecutive passes over the same tile when its
