@@ -662,40 +662,49 @@ template <int R, int LO, int HI> __device__ __forceinline__ double rp2_dot(const
 }
 
 // Runtime register bit(s) -> template instantiation, written out as switches
-// (no lambdas: the register arrays must stay in registers).
-#define TQ_PAIR_SWITCH(R, LO, HI, CALL)                                                                             \
-    switch ((LO) * 4 + (HI)) {                                                                                      \
-    case 1: if constexpr (R > 1) { constexpr int lo_ = 0, hi_ = 1; CALL; } break;                                   \
-    case 2: if constexpr (R > 2) { constexpr int lo_ = 0, hi_ = 2; CALL; } break;                                   \
-    case 3: if constexpr (R > 3) { constexpr int lo_ = 0, hi_ = 3; CALL; } break;                                   \
-    case 6: if constexpr (R > 2) { constexpr int lo_ = 1, hi_ = 2; CALL; } break;                                   \
-    case 7: if constexpr (R > 3) { constexpr int lo_ = 1, hi_ = 3; CALL; } break;                                   \
-    case 11: if constexpr (R > 3) { constexpr int lo_ = 2, hi_ = 3; CALL; } break;                                  \
-    default: break;                                                                                                 \
-    }
-#define TQ_ORDERED_SWITCH(R, J, C, CALL)                                                                            \
-    switch ((J) * 4 + (C)) {                                                                                        \
-    case 1: if constexpr (R > 1) { constexpr int j_ = 0, c_ = 1; CALL; } break;                                     \
-    case 2: if constexpr (R > 2) { constexpr int j_ = 0, c_ = 2; CALL; } break;                                     \
-    case 3: if constexpr (R > 3) { constexpr int j_ = 0, c_ = 3; CALL; } break;                                     \
-    case 4: if constexpr (R > 1) { constexpr int j_ = 1, c_ = 0; CALL; } break;                                     \
-    case 6: if constexpr (R > 2) { constexpr int j_ = 1, c_ = 2; CALL; } break;                                     \
-    case 7: if constexpr (R > 3) { constexpr int j_ = 1, c_ = 3; CALL; } break;                                     \
-    case 8: if constexpr (R > 2) { constexpr int j_ = 2, c_ = 0; CALL; } break;                                     \
-    case 9: if constexpr (R > 2) { constexpr int j_ = 2, c_ = 1; CALL; } break;                                     \
-    case 11: if constexpr (R > 3) { constexpr int j_ = 2, c_ = 3; CALL; } break;                                    \
-    case 12: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 0; CALL; } break;                                    \
-    case 13: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 1; CALL; } break;                                    \
-    case 14: if constexpr (R > 3) { constexpr int j_ = 3, c_ = 2; CALL; } break;                                    \
-    default: break;                                                                                                 \
-    }
+// (no lambdas: the register arrays must stay in registers).  Each switch
+// covers exactly the valid cases of its R, the last one as `default`: a
+// switch with a path that leaves the registers untouched makes the compiler
+// copy the whole register array on every op.
+#define TQ_C1(J_, CALL) { constexpr int j_ = J_; CALL; } break;
 #define TQ_BIT_SWITCH(R, J, CALL)                                                                                   \
-    switch (J) {                                                                                                    \
-    case 0: if constexpr (R > 0) { constexpr int j_ = 0; CALL; } break;                                             \
-    case 1: if constexpr (R > 1) { constexpr int j_ = 1; CALL; } break;                                             \
-    case 2: if constexpr (R > 2) { constexpr int j_ = 2; CALL; } break;                                             \
-    case 3: if constexpr (R > 3) { constexpr int j_ = 3; CALL; } break;                                             \
-    default: break;                                                                                                 \
+    if constexpr (R == 1) {                                                                                         \
+        constexpr int j_ = 0; CALL;                                                                                 \
+    } else if constexpr (R == 2) {                                                                                  \
+        switch (J) { case 0: TQ_C1(0, CALL) default: TQ_C1(1, CALL) }                                              \
+    } else if constexpr (R == 3) {                                                                                  \
+        switch (J) { case 0: TQ_C1(0, CALL) case 1: TQ_C1(1, CALL) default: TQ_C1(2, CALL) }                       \
+    } else if constexpr (R == 4) {                                                                                  \
+        switch (J) { case 0: TQ_C1(0, CALL) case 1: TQ_C1(1, CALL) case 2: TQ_C1(2, CALL) default: TQ_C1(3, CALL) } \
+    }
+#define TQ_C2(L_, H_, CALL) { constexpr int lo_ = L_, hi_ = H_; CALL; } break;
+#define TQ_PAIR_SWITCH(R, LO, HI, CALL)                                                                             \
+    if constexpr (R == 2) {                                                                                         \
+        constexpr int lo_ = 0, hi_ = 1; CALL;                                                                       \
+    } else if constexpr (R == 3) {                                                                                  \
+        switch ((LO) * 4 + (HI)) { case 1: TQ_C2(0, 1, CALL) case 2: TQ_C2(0, 2, CALL) default: TQ_C2(1, 2, CALL) } \
+    } else if constexpr (R == 4) {                                                                                  \
+        switch ((LO) * 4 + (HI)) {                                                                                  \
+        case 1: TQ_C2(0, 1, CALL) case 2: TQ_C2(0, 2, CALL) case 3: TQ_C2(0, 3, CALL)                               \
+        case 6: TQ_C2(1, 2, CALL) case 7: TQ_C2(1, 3, CALL) default: TQ_C2(2, 3, CALL)                              \
+        }                                                                                                           \
+    }
+#define TQ_CO(J_, C_, CALL) { constexpr int j_ = J_, c_ = C_; CALL; } break;
+#define TQ_ORDERED_SWITCH(R, J, C, CALL)                                                                            \
+    if constexpr (R == 2) {                                                                                         \
+        switch ((J) * 4 + (C)) { case 1: TQ_CO(0, 1, CALL) default: TQ_CO(1, 0, CALL) }                            \
+    } else if constexpr (R == 3) {                                                                                  \
+        switch ((J) * 4 + (C)) {                                                                                    \
+        case 1: TQ_CO(0, 1, CALL) case 2: TQ_CO(0, 2, CALL) case 4: TQ_CO(1, 0, CALL)                               \
+        case 6: TQ_CO(1, 2, CALL) case 8: TQ_CO(2, 0, CALL) default: TQ_CO(2, 1, CALL)                              \
+        }                                                                                                           \
+    } else if constexpr (R == 4) {                                                                                  \
+        switch ((J) * 4 + (C)) {                                                                                    \
+        case 1: TQ_CO(0, 1, CALL) case 2: TQ_CO(0, 2, CALL) case 3: TQ_CO(0, 3, CALL)                               \
+        case 4: TQ_CO(1, 0, CALL) case 6: TQ_CO(1, 2, CALL) case 7: TQ_CO(1, 3, CALL)                               \
+        case 8: TQ_CO(2, 0, CALL) case 9: TQ_CO(2, 1, CALL) case 11: TQ_CO(2, 3, CALL)                              \
+        case 12: TQ_CO(3, 0, CALL) case 13: TQ_CO(3, 1, CALL) default: TQ_CO(3, 2, CALL)                            \
+        }                                                                                                           \
     }
 
 // How a diagonal op acts on a stage item: both bits in registers, one bit
@@ -777,12 +786,27 @@ template <int R, class MT> __device__ __forceinline__ double reg_diag_dot(const 
     return s;
 }
 
-// the control of a K_M1 op: -2 = off for this item, -1 = none (or on), else its register bit
-__device__ __forceinline__ int reg_ctrl(const PassOp &op, uint32_t base, uint64_t fb)
+// A K_M1 op whose control bit lies outside the stage acts on an item only
+// when that bit (from the item's base index or the tile's fixed bits) is 1.
+// The matrix is selected per lane -- the op's or the identity -- so that
+// every path writes the registers.
+struct Mat2 {
+    double2 e[4];
+    __device__ __forceinline__ double2 operator[](int i) const { return e[i]; }
+};
+template <class MT> __device__ __forceinline__ Mat2 ctrl_sel(MT m, bool on)
 {
-    if (!op.ctrl) return -1;
-    if (op.s1 != kFixed) return op.s1;
-    return bit_of(op.l1, op.p1, base, fb) == op.cval ? -1 : -2;
+    const double2 one = make_double2(1.0, 0.0), zero = make_double2(0.0, 0.0);
+    Mat2 r;
+    r.e[0] = on ? m[0] : one;
+    r.e[1] = on ? m[1] : zero;
+    r.e[2] = on ? m[2] : zero;
+    r.e[3] = on ? m[3] : one;
+    return r;
+}
+__device__ __forceinline__ bool ctrl_on(const PassOp &op, uint32_t base, uint64_t fb)
+{
+    return bit_of(op.l1, op.p1, base, fb) == op.cval;
 }
 
 // forward op on registers
@@ -790,12 +814,13 @@ template <int R, class MT> __device__ __forceinline__ void reg_op(const PassOp &
 {
     switch (op.kind) {
     case K_M1: {
-        const int c = reg_ctrl(op, base, fb);
-        if (c == -2) return;
-        if (c == -1) {
+        if (!op.ctrl) {
             TQ_BIT_SWITCH(R, op.s0, (rm1<R, j_>(a, m)))
+        } else if (op.s1 != kFixed) {
+            TQ_ORDERED_SWITCH(R, op.s0, op.s1, (rm1c<R, j_, c_>(a, m)))
         } else {
-            TQ_ORDERED_SWITCH(R, op.s0, c, (rm1c<R, j_, c_>(a, m)))
+            const Mat2 ms = ctrl_sel(m, ctrl_on(op, base, fb));
+            TQ_BIT_SWITCH(R, op.s0, (rm1<R, j_>(a, ms)))
         }
         return;
     }
@@ -819,21 +844,29 @@ __device__ __forceinline__ void reg_rev_op(const PassOp &op, MT m, MT d0, MT d1,
 {
     switch (op.kind) {
     case K_M1: {
-        const int c = reg_ctrl(op, base, fb);
-        if (c == -2) return;
-        if (c == -1) {
+        if (!op.ctrl) {
             TQ_BIT_SWITCH(R, op.s0, ({
                 rm1<R, j_>(a, m);
                 if (op.ngrad > 0) g0 += rm1_dot<R, j_>(a, f, d0);
                 if (op.ngrad > 1) g1 += rm1_dot<R, j_>(a, f, d1);
                 rm1<R, j_>(f, m);
             }))
-        } else {
-            TQ_ORDERED_SWITCH(R, op.s0, c, ({
+        } else if (op.s1 != kFixed) {
+            TQ_ORDERED_SWITCH(R, op.s0, op.s1, ({
                 rm1c<R, j_, c_>(a, m);
                 if (op.ngrad > 0) g0 += rm1c_dot<R, j_, c_>(a, f, d0);
                 if (op.ngrad > 1) g1 += rm1c_dot<R, j_, c_>(a, f, d1);
                 rm1c<R, j_, c_>(f, m);
+            }))
+        } else {
+            // an item whose control is off sees the identity and a zero derivative
+            const bool on = ctrl_on(op, base, fb);
+            const Mat2 ms = ctrl_sel(m, on);
+            TQ_BIT_SWITCH(R, op.s0, ({
+                rm1<R, j_>(a, ms);
+                if (op.ngrad > 0) g0 += on ? rm1_dot<R, j_>(a, f, d0) : 0.0;
+                if (op.ngrad > 1) g1 += on ? rm1_dot<R, j_>(a, f, d1) : 0.0;
+                rm1<R, j_>(f, ms);
             }))
         }
         return;
@@ -1375,7 +1408,7 @@ __global__ __launch_bounds__(256) void k_pauli_reduce(PauliReduceArgs a)
 
 // ------------------------------------------------------ reverse pass
 // psi and phi tiles side by side in LDS; the pass's matrices too.
-__global__ __launch_bounds__(256) void k_rev_pass(RevArgs a)
+__global__ __launch_bounds__(256, 2) void k_rev_pass(RevArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const TileGeom &g = a.g;
