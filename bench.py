@@ -29,6 +29,40 @@ PEAK_HBM_GBS = 8000.0
 PEAK_FP64_TFLOPS = 78.6  # fp64 vector: 256 CUs x 2.4 GHz x 128 flop/clk
 
 
+# HBM traffic per launch of a dominant kernel, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE runs (profiles/traffic.json, scaled by the counters' reading for
+# a plain device copy of known size).  Valid only for the sources it was
+# measured with: the hash below must match.
+TRAFFIC_SOURCES = ("paper_2003_02989_amd/csrc/kernels.hip", "paper_2003_02989_amd/csrc/kernels.h",
+                   "paper_2003_02989_amd/csrc/tq_internal.h", "paper_2003_02989_amd/csrc/program.cpp",
+                   "paper_2003_02989_amd/csrc/tq_abi.cpp")
+
+
+def sources_hash():
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(root, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config, kernel):
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha256") != sources_hash():
+        return None
+    e = t.get("configs", {}).get(config)
+    if not e or e.get("kernel") != kernel:
+        return None
+    return e.get("bytes_per_launch")
+
+
 def workload(name):
     from paper_2003_02989_amd import workloads as wl
     return wl.CONFIGS[name]()
@@ -132,6 +166,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy a 1 GiB device buffer three times (reference for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the batched path has no "
@@ -147,6 +183,14 @@ def main():
     torch.cuda.set_device(local_rank)
     if args.sweep:
         sweep(args.steps)
+        return
+    if args.copy_calibration:
+        src = torch.ones(1 << 27, dtype=torch.complex64, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": 8 << 27, "bytes_written": 8 << 27, "copies": 3}))
         return
     w = workload(args.config)
     B, K = w.B, w.K
@@ -213,14 +257,13 @@ def main():
     n_terms = sum(len(t) for t in w.observables[0])
     flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, args.config in ("c1", "c2", "c5"))
     avg_ms = dom_ms / max(n_launch, 1)
+    traffic = measured_traffic(args.config, dominant)
     if args.config in ("c1", "c2"):
         bound, unit, peak = "alu", "TFLOP/s", PEAK_FP64_TFLOPS
         achieved = (flops / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e12
-        traffic = None
     else:
         bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
         achieved = (bytes_ / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e9
-        traffic = None
 
     if args.config == "c4":
         value = B * amps.shape[1] / (ms_per_step * 1e-3)

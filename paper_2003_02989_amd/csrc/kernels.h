@@ -24,6 +24,15 @@ struct BuildArgs {
     int64_t mat_stride;
 };
 
+struct StageBuildArgs {
+    const Stage *stages;   // the group's forward stages
+    const int32_t *list;   // indices of the dense ones
+    int nlist;
+    const PassOp *ops;     // the group's forward ops
+    double2 *mats;
+    int64_t mat_stride;
+};
+
 struct PassArgs {
     float2 *state;
     int64_t row_stride;
@@ -160,6 +169,7 @@ size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat);
 size_t resident_lds_bytes(int n, int nacc, bool adjoint);
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
+hipError_t launch_build_stage(const StageBuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
 // Tiles of the Pauli kernel: 2^t amplitudes with t <= kPauliTileMax.
 constexpr int kPauliTileMax = 12;

@@ -937,9 +937,30 @@ template <int R> __device__ __forceinline__ uint32_t stage_base(const Stage &st,
 
 // One forward stage over a tile of 2^t amplitudes in LDS.  M holds the
 // matrices from row-block offset mbase on.
+// Dense stage: a <- S a with the 2^R x 2^R stage matrix S (row major),
+// read through the scalar cache.
+template <int R> __device__ __forceinline__ void rdense(double2 *a, SMat S)
+{
+    constexpr int N = 1 << R;
+    double2 b[N];
+#pragma unroll
+    for (int k = 0; k < N; k++) {
+        double re = 0.0, im = 0.0;
+#pragma unroll
+        for (int j = 0; j < N; j++) {
+            const double2 m = S[k * N + j];
+            re = fma(m.x, a[j].x, fma(-m.y, a[j].y, re));
+            im = fma(m.x, a[j].y, fma(m.y, a[j].x, im));
+        }
+        b[k] = make_double2(re, im);
+    }
+#pragma unroll
+    for (int k = 0; k < N; k++) a[k] = b[k];
+}
+
 template <int R, class MT>
-__device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lds, int t, uint64_t fb,
-                                          int tid, int nt)
+__device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, MT M, int mbase, SMat G, float2 *lds, int t,
+                                          uint64_t fb, int tid, int nt)
 {
     // sw() is linear over xor and base, off[k] have disjoint bits, so the
     // swizzled address of base | off[k] is sw(base) ^ sw(off[k])
@@ -953,28 +974,33 @@ __device__ __forceinline__ void run_stage(const Stage &st, const PassOp *ops, MT
         double2 a[1 << R];
 #pragma unroll
         for (int k = 0; k < (1 << R); k++) a[k] = up2(lds[sb ^ off[k]]);
-        for (int oi = st.op_begin; oi < st.op_end; oi++) {
-            const PassOp op = cget(ops, oi);
-            reg_op<R>(op, M + (op.mat - mbase), a, base, fb);
+        if (st.dense) {
+            rdense<R>(a, G + st.mat);
+        } else {
+            for (int oi = st.op_begin; oi < st.op_end; oi++) {
+                const PassOp op = cget(ops, oi);
+                reg_op<R>(op, M + (op.mat - mbase), a, base, fb);
+            }
         }
 #pragma unroll
         for (int k = 0; k < (1 << R); k++) lds[sb ^ off[k]] = down2(a[k]);
     }
 }
 
-// tid / nt: this thread's index among the nt threads that share the tile
+// tid / nt: this thread's index among the nt threads that share the tile;
+// G: the row's matrix block in HBM (dense stage matrices)
 template <class MT>
-__device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops, MT M, int mbase, float2 *lds, int t,
+__device__ __forceinline__ void run_stage_any(const Stage &st, const PassOp *ops, MT M, int mbase, SMat G, float2 *lds, int t,
                                               uint64_t fb, int tid, int nt)
 {
     switch (st.r) {
     case 4:
-        if constexpr (kStageBitsFwd >= 4) run_stage<4>(st, ops, M, mbase, lds, t, fb, tid, nt);
+        if constexpr (kStageBitsFwd >= 4) run_stage<4>(st, ops, M, mbase, G, lds, t, fb, tid, nt);
         break;
-    case 3: run_stage<3>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
-    case 2: run_stage<2>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
-    case 1: run_stage<1>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
-    default: run_stage<0>(st, ops, M, mbase, lds, t, fb, tid, nt); break;
+    case 3: run_stage<3>(st, ops, M, mbase, G, lds, t, fb, tid, nt); break;
+    case 2: run_stage<2>(st, ops, M, mbase, G, lds, t, fb, tid, nt); break;
+    case 1: run_stage<1>(st, ops, M, mbase, G, lds, t, fb, tid, nt); break;
+    default: run_stage<0>(st, ops, M, mbase, G, lds, t, fb, tid, nt); break;
     }
 }
 
@@ -1077,6 +1103,41 @@ __device__ __forceinline__ void run_rev_stage_any(const Stage &st, const PassOp 
     }
 }
 
+// Dense stage matrices: column j of a stage's matrix is the stage's ops
+// applied to the basis vector e_j (the same register ops the op-by-op path
+// runs), one thread per column, in fp64.
+template <int R> __device__ __forceinline__ void build_stage_r(const Stage &st, const PassOp *ops, const double2 *block,
+                                                              double2 *out, int j)
+{
+    constexpr int N = 1 << R;
+    double2 a[N];
+#pragma unroll
+    for (int k = 0; k < N; k++) a[k] = make_double2(k == j ? 1.0 : 0.0, 0.0);
+    for (int oi = st.op_begin; oi < st.op_end; oi++) {
+        const PassOp op = cget(ops, oi);
+        reg_op<R>(op, block + op.mat, a, 0u, 0ull);
+    }
+#pragma unroll
+    for (int k = 0; k < N; k++) out[k * N + j] = a[k];
+}
+
+__global__ __launch_bounds__(64) void k_build_stage(StageBuildArgs a)
+{
+    const int si = blockIdx.x, row = blockIdx.y, j = threadIdx.x;
+    const Stage st = cget(a.stages, cget(a.list, si));
+    if (j >= (1 << st.r)) return;
+    double2 *block = a.mats + (int64_t)row * a.mat_stride;
+    double2 *out = block + st.mat;
+    switch (st.r) {
+    case 4:
+        if constexpr (kStageBitsFwd >= 4) build_stage_r<4>(st, a.ops, block, out, j);
+        break;
+    case 3: build_stage_r<3>(st, a.ops, block, out, j); break;
+    case 2: build_stage_r<2>(st, a.ops, block, out, j); break;
+    default: build_stage_r<1>(st, a.ops, block, out, j); break;
+    }
+}
+
 // Stage the matrices [begin, end) of a row block into LDS.
 __device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_block, int begin, int end)
 {
@@ -1084,7 +1145,7 @@ __device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_bloc
 }
 
 // ------------------------------------------------------- forward pass
-__global__ __launch_bounds__(256, 4) void k_pass(PassArgs a)
+__global__ __launch_bounds__(256) void k_pass(PassArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
     const TileGeom &g = a.g;
@@ -1143,7 +1204,7 @@ __global__ __launch_bounds__(256, 4) void k_pass(PassArgs a)
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_stage_any(st, a.ops, M, a.mat_begin, lds, t, fb, threadIdx.x, blockDim.x);
+            run_stage_any(st, a.ops, M, a.mat_begin, smat(a.mats + (int64_t)row * a.mat_stride), lds, t, fb, threadIdx.x, blockDim.x);
             __syncthreads();
         }
         tile_copy<false>(tc, lds, st, fb, T);
@@ -1479,8 +1540,8 @@ __global__ void k_grad_reduce(GradReduceArgs a)
 // launch, on the matrices k_build_mats wrote.  At most 128 registers per
 // thread, so that four rows share a CU.  Outputs are reduced in a fixed order.
 template <class MT>
-__device__ __forceinline__ void resident_row(const ResArgs &a, MT M, double *acc, float2 *lp, float2 *lf, int row, int tid,
-                                             int nt)
+__device__ __forceinline__ void resident_row(const ResArgs &a, MT M, SMat G, double *acc, float2 *lp, float2 *lf, int row,
+                                             int tid, int nt)
 {
     const int n = a.n;
     const uint32_t T = 1u << n;
@@ -1504,7 +1565,7 @@ __device__ __forceinline__ void resident_row(const ResArgs &a, MT M, double *acc
     // forward gates
     for (int si = 0; si < a.nfstages; si++) {
         const Stage st = cget(a.fstages, si);
-        run_stage_any(st, a.fops, M, 0, lp, n, 0, tid, nt);
+        run_stage_any(st, a.fops, M, 0, G, lp, n, 0, tid, nt);
         sync();
     }
     // state output and expectation terms
@@ -1565,7 +1626,8 @@ __global__ __launch_bounds__(256, 4) void k_resident(ResArgs a)
     double *acc = reinterpret_cast<double *>(smem);              // [4][nacc]
     float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);   // [T]
     float2 *lf = lp + T;                                         // [T] (adjoint)
-    resident_row(a, smat(a.mats + (int64_t)blockIdx.x * a.mat_stride), acc, lp, lf, blockIdx.x, threadIdx.x, blockDim.x);
+    const SMat M = smat(a.mats + (int64_t)blockIdx.x * a.mat_stride);
+    resident_row(a, M, M, acc, lp, lf, blockIdx.x, threadIdx.x, blockDim.x);
 }
 
 // ------------------------------------------------------------- sampling
@@ -1754,6 +1816,14 @@ template <class K> hipError_t set_lds(K kernel, size_t bytes)
                                (int)bytes);
 }
 } // namespace
+
+hipError_t launch_build_stage(const StageBuildArgs &a, int nrows, hipStream_t s)
+{
+    if (a.nlist <= 0 || nrows <= 0) return hipSuccess;
+    prof::Scope ps("build", s);
+    hipLaunchKernelGGL(k_build_stage, dim3(a.nlist, nrows), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s)
 {

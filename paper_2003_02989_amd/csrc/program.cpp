@@ -416,6 +416,47 @@ void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_
     }
 }
 
+// A stage is fusable when every op acts alike on all items: its register
+// bits, and for controls and diagonals every bit, lie in the stage.
+bool stage_fusable(const Pass &ps, const Stage &st)
+{
+    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++) {
+        const PassOp &op = ps.ops[k];
+        switch (op.kind) {
+        case K_M1:
+            if (op.ctrl && op.s1 == kFixed) return false;
+            break;
+        case K_D1:
+            if (op.s0 == kFixed) return false;
+            break;
+        case K_D2:
+            if (op.s0 == kFixed || op.s1 == kFixed) return false;
+            break;
+        default: break;
+        }
+    }
+    return true;
+}
+
+// Dense stage cost (fp64 instructions per amplitude: a 2^r x 2^r complex
+// matvec, 4 per entry of a row) against the ops' own costs plus their
+// dispatch overhead.
+bool dense_pays(const Pass &ps, const Stage &st)
+{
+    const int dense = 4 << st.r;
+    int ops = 0;
+    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++) {
+        const PassOp &op = ps.ops[k];
+        int c = 4;
+        if (op.kind == K_M1) c = op.ctrl ? 4 : 8;
+        if (op.kind == K_M2) c = 16;
+        if (op.kind == K_F2) c = 6;
+        if (op.kind == K_P2) c = 8;
+        ops += c + kOpDispatchCost;
+    }
+    return dense < ops;
+}
+
 // Append a pass, split into consecutive passes over the same tile when its
 // matrices would not fit the LDS staging area (op k owns the matrix entries
 // from its offset up to the next op's).
@@ -669,6 +710,16 @@ void plan_group(Group &g, const Options &opt, int S)
         ps.op_offset = off;
         make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at);
         off += (int)ps.ops.size();
+        // forward stages whose ops act alike on every item become one dense
+        // matrix when that is cheaper than the ops one by one (matrix
+        // entries appended to the row block, built after the op matrices)
+        for (Stage &st : ps.stages) {
+            if (!stage_fusable(ps, st) || !dense_pays(ps, st)) continue;
+            st.dense = 1;
+            st.mat = g.mat_block;
+            g.mat_block += 1 << (2 * st.r);
+            g.dense_stages.push_back({(int)(&ps - g.fwd.data()), (int)(&st - ps.stages.data())});
+        }
     }
     off = 0;
     for (Pass &ps : g.rev) {

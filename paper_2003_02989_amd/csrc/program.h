@@ -74,7 +74,12 @@ struct Group {
     std::vector<int32_t> sym_gslot_begin;       // [S+1] CSR symbol -> gradient slots
     std::vector<int32_t> sym_gslots;
     int32_t fwd_mat_end = 0;                    // forward matrices (with the product init) end here
+    std::vector<std::pair<int, int>> dense_stages;  // (forward pass, stage) with a stage matrix
 };
+
+// Per-op dispatch overhead of the register ops, in fp64-instruction
+// equivalents per amplitude (measured: ~6 for 2x2 ops at three register bits).
+constexpr int kOpDispatchCost = 6;
 
 struct ProgramData {
     int B = 0, S = 0, nmax = 0;

@@ -94,9 +94,9 @@ constexpr int kPauliTile = 11;
 
 struct GroupDev {
     DevBuf rows, ident, gates, slot_sym, scale, off, explicit_, tasks, members, fwd_ops, rev_ops, sym_begin,
-        sym_gslots, gslot_slot, fwd_stages, rev_stages;
+        sym_gslots, gslot_slot, fwd_stages, rev_stages, dense_list;
     std::vector<int> fwd_op_off, rev_op_off, fwd_stage_off, rev_stage_off;
-    int n_fwd_stages = 0, n_rev_stages = 0;
+    int n_fwd_stages = 0, n_rev_stages = 0, n_dense = 0;
     size_t psi_off = 0;  // amplitude offset of this group's rows in the state workspaces
     size_t mat_off = 0;  // offset in the matrix workspace
 };
@@ -121,7 +121,7 @@ struct tq_program_s {
         for (auto &g : gdev) {
             for (DevBuf *b : {&g->rows, &g->ident, &g->gates, &g->slot_sym, &g->scale, &g->off, &g->explicit_,
                               &g->tasks, &g->members, &g->fwd_ops, &g->rev_ops, &g->sym_begin, &g->sym_gslots,
-                              &g->gslot_slot, &g->fwd_stages, &g->rev_stages})
+                              &g->gslot_slot, &g->fwd_stages, &g->rev_stages, &g->dense_list})
                 b->release();
         }
         for (auto &o : obs_dev) o->release();
@@ -198,6 +198,10 @@ void ensure_device(tq_program p)
         gd->n_rev_stages = (int)rs.size();
         upload(gd->fwd_stages, fs);
         upload(gd->rev_stages, rs);
+        std::vector<int32_t> dl;
+        for (auto &d : g.dense_stages) dl.push_back(gd->fwd_stage_off[d.first] + d.second);
+        gd->n_dense = (int)dl.size();
+        upload(gd->dense_list, dl);
         upload(gd->sym_begin, g.sym_gslot_begin);
         upload(gd->sym_gslots, g.sym_gslots);
         upload(gd->gslot_slot, g.gslot_slot);
@@ -240,6 +244,17 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.mats = mat_ws(p) + gd.mat_off;
     a.mat_stride = std::max(g.mat_block, 1);
     hip_check(launch_build(a, (int)g.rows.size(), s), "matrix build launch");
+    if (begin <= g.fwd_tasks.begin && end >= g.fwd_tasks.end && gd.n_dense > 0) {
+        // dense forward stages, from the op matrices just built
+        StageBuildArgs sb{};
+        sb.stages = (const Stage *)gd.fwd_stages.p;
+        sb.list = (const int32_t *)gd.dense_list.p;
+        sb.nlist = gd.n_dense;
+        sb.ops = (const PassOp *)gd.fwd_ops.p;
+        sb.mats = a.mats;
+        sb.mat_stride = a.mat_stride;
+        hip_check(launch_build_stage(sb, (int)g.rows.size(), s), "stage matrix build launch");
+    }
 }
 
 // Forward passes of group gi into `state` (row r of the group at
@@ -936,7 +951,7 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
                         const Stage &sg = ps.stages[k];
                         o << (k ? "," : "") << "{\"r\":" << (int)sg.r << ",\"bits\":[";
                         for (int j = 0; j < sg.r; j++) o << (j ? "," : "") << (int)sg.bits[j];
-                        o << "],\"ops\":" << (sg.op_end - sg.op_begin) << "}";
+                        o << "],\"ops\":" << (sg.op_end - sg.op_begin) << ",\"dense\":" << (int)sg.dense << "}";
                     }
                     o << "]}";
                 }

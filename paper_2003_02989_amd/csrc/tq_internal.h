@@ -99,8 +99,10 @@ constexpr int kMaxStageGrads = 8;
 struct Stage {
     uint8_t r;        // register bits
     uint8_t bits[4];  // their tile-local positions, ascending
-    uint8_t pad[3];
+    uint8_t dense;    // 1: the stage's ops are applied as one 2^r x 2^r matrix
+    uint8_t pad[2];
     int32_t op_begin, op_end;  // ops, as indices into the group's op array
+    int32_t mat;      // dense: offset of the stage matrix (row major) in the row block
 };
 
 // Tile geometry of a pass: t local bits = `c` low bits + high bits hb[].
