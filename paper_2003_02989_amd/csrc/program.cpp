@@ -255,49 +255,127 @@ struct Planner {
     }
 };
 
-// Group a pass's ops into register stages: sets of ops whose dense
-// (non-diagonal) tile bits fit a set R of at most rmax bits (rdense when the
-// stage holds a dense 4x4 or fSim-type op) and that hold at most
-// kMaxStageGrads gradient parameters.  Diagonal ops and control bits outside
-// R read their bit from the item's base index.  Ops that share no qubit
-// commute, so the ops are reordered within their dependency order (ops on a
-// common qubit keep their order): each stage starts from the earliest ready
-// op and grows R by the bits that make the most ready ops fit, taking every
-// op that fits.  R is padded with the highest free tile bits, so that the
-// items of neighbouring lanes sit at neighbouring LDS addresses.
-void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at)
+// Register stages.  A stage is a set of ops of a pass whose dense
+// (non-diagonal) tile bits fit a set R of at most rmax bits (rdense when it
+// holds a dense 4x4 or fSim-type op) and that hold at most kMaxStageGrads
+// gradient parameters; each thread keeps the 2^|R| amplitudes of one item in
+// registers while the stage's ops run.  Diagonal ops and control bits
+// outside R read their bit from the item's base index.  Ops commute when
+// they act diagonally on every qubit they share, so the ops of a pass are
+// reordered within that dependency order to pack them into few stages.
+// R is padded with the highest free tile bits, so that the items of
+// neighbouring lanes sit at neighbouring LDS addresses.
+namespace stages {
+
+std::vector<int> need(const PassOp &op)
+{
+    std::vector<int> v;
+    if (op.kind == K_M1) v.push_back(op.l0);
+    if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2) {
+        v.push_back(op.l0);
+        v.push_back(op.l1);
+    }
+    return v;
+}
+
+bool is_dense(const PassOp &op) { return op.kind == K_M2 || op.kind == K_F2; }
+
+// bits that make an op act alike on all items of a stage when they are
+// register bits: also a control bit, and the in-tile bits of a diagonal
+std::vector<int> soft(const PassOp &op)
+{
+    std::vector<int> v = need(op);
+    auto add = [&](uint8_t l) {
+        if (l != kFixed && std::find(v.begin(), v.end(), (int)l) == v.end()) v.push_back(l);
+    };
+    if (op.kind == K_M1 && op.ctrl) add(op.l1);
+    if (op.kind == K_D1) add(op.l0);
+    if (op.kind == K_D2) {
+        add(op.l0);
+        add(op.l1);
+    }
+    return v;
+}
+
+bool has(const std::vector<int> &bits, int b) { return std::find(bits.begin(), bits.end(), b) != bits.end(); }
+
+// R padded to rs bits with the highest free tile bits, ascending
+std::vector<int> padded(std::vector<int> bits, int rs, int t)
+{
+    for (int b = t - 1; b >= 0 && (int)bits.size() < rs; b--)
+        if (!has(bits, b)) bits.push_back(b);
+    std::sort(bits.begin(), bits.end());
+    return bits;
+}
+
+// an op acts alike on all items of a stage with these register bits
+bool uniform(const PassOp &op, const std::vector<int> &bits)
+{
+    for (int b : soft(op))
+        if (!has(bits, b)) return false;
+    if ((op.kind == K_D1 || op.kind == K_D2) && op.l0 == kFixed) return false;
+    if (op.kind == K_D2 && op.l1 == kFixed) return false;
+    if (op.kind == K_M1 && op.ctrl && op.l1 == kFixed) return false;
+    return true;
+}
+
+// fp64-instruction equivalents per amplitude of one op in a register stage
+int op_cost(const PassOp &op)
+{
+    int c = 4;
+    if (op.kind == K_M1) c = op.ctrl ? 4 : 8;
+    if (op.kind == K_M2) c = 16;
+    if (op.kind == K_F2) c = 6;
+    if (op.kind == K_P2) c = 8;
+    return c + kOpDispatchCost;
+}
+
+struct Packing {
+    std::vector<int> order;  // ops in stage order
+    struct St {
+        std::vector<int> bits;  // padded register bits
+        int begin, end;         // range in `order`
+        bool dense2;            // holds a dense two-qubit op
+    };
+    std::vector<St> st;
+    int cost = 0;
+};
+
+// Greedy packing.  commute: use the commutation of diagonal ops (else ops
+// sharing any qubit keep their order); soft_first: grow R with the bits that
+// make an op uniform, and take uniform ops before per-item ones.
+Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first, bool forward)
 {
     const int t = ps.geom.t;
     const int r = std::min(rmax, t);
     const int rd = std::min(rdense, r);
     const int nops = (int)ps.ops.size();
-    ps.stages.clear();
-
-    // register bits an op needs, the qubits (global bits) it acts on
-    auto need = [](const PassOp &op) {
-        std::vector<int> v;
-        if (op.kind == K_M1) v.push_back(op.l0);
-        if (op.kind == K_M2 || op.kind == K_P2 || op.kind == K_F2) {
-            v.push_back(op.l0);
-            v.push_back(op.l1);
-        }
-        return v;
-    };
-    auto is_dense = [](const PassOp &op) { return op.kind == K_M2 || op.kind == K_F2; };
     std::vector<std::vector<int>> succ(nops);
     std::vector<int> indeg(nops, 0);
     {
-        std::map<int, int> last;  // qubit -> latest op on it
+        std::map<int, int> last_nd;                  // qubit -> latest op not diagonal on it
+        std::map<int, std::vector<int>> diag_since;  // qubit -> ops diagonal on it since then
         for (int k = 0; k < nops; k++) {
             const PassOp &op = ps.ops[k];
-            std::vector<int> qs{op.p0};
-            if (op.kind != K_D1 && (op.kind != K_M1 || op.ctrl)) qs.push_back(op.p1);
+            std::vector<std::pair<int, bool>> qs;  // (qubit, op diagonal on it)
+            const bool diag = commute && (op.kind == K_D1 || op.kind == K_D2);
+            qs.push_back({op.p0, diag});
+            if (op.kind == K_M1 && op.ctrl) qs.push_back({op.p1, commute});
+            else if (op.kind != K_D1 && op.kind != K_M1) qs.push_back({op.p1, diag});
             std::vector<int> preds;
-            for (int q : qs) {
-                auto it = last.find(q);
-                if (it != last.end() && std::find(preds.begin(), preds.end(), it->second) == preds.end())
-                    preds.push_back(it->second);
-                last[q] = k;
+            auto dep = [&](int pr) {
+                if (std::find(preds.begin(), preds.end(), pr) == preds.end()) preds.push_back(pr);
+            };
+            for (auto &qd : qs) {
+                auto it = last_nd.find(qd.first);
+                if (it != last_nd.end()) dep(it->second);
+                if (qd.second) {
+                    diag_since[qd.first].push_back(k);
+                } else {
+                    for (int pr : diag_since[qd.first]) dep(pr);
+                    diag_since[qd.first].clear();
+                    last_nd[qd.first] = k;
+                }
             }
             for (int pr : preds) succ[pr].push_back(k);
             indeg[k] = (int)preds.size();
@@ -306,45 +384,46 @@ void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_
     std::set<int> ready;
     for (int k = 0; k < nops; k++)
         if (indeg[k] == 0) ready.insert(k);
-    std::vector<int> order;
-    std::vector<std::pair<std::vector<int>, std::pair<int, int>>> stage_list;  // (R, [begin, end) in order)
+    Packing P;
     while (!ready.empty()) {
         std::vector<int> R;
         bool dense = false;
         int ngrad = 0;
-        const int begin = (int)order.size();
+        const int begin = (int)P.order.size();
         auto union_with = [&](const std::vector<int> &bits) {
             std::vector<int> u = R;
             for (int b : bits)
-                if (std::find(u.begin(), u.end(), b) == u.end()) u.push_back(b);
+                if (!has(u, b)) u.push_back(b);
             return u;
         };
-        auto fits = [&](int k, const std::vector<int> &bits, bool dense_now) {
+        auto fits = [&](int k, const std::vector<int> &bits, bool dense_now, bool soft_bits) {
             const PassOp &op = ps.ops[k];
             if (ngrad + op.ngrad > kMaxStageGrads) return false;
-            for (int b : need(op))
-                if (std::find(bits.begin(), bits.end(), b) == bits.end()) return false;
+            for (int b : soft_bits ? soft(op) : need(op))
+                if (!has(bits, b)) return false;
             return !((dense_now || is_dense(op)) && (int)bits.size() > rd);
         };
-        for (;;) {
-            // take every ready op that fits R, until none does
-            bool took = true;
+        auto take = [&](bool soft_bits) {
+            bool any = false, took = true;
             while (took) {
                 took = false;
                 for (auto it = ready.begin(); it != ready.end(); ++it) {
                     const int k = *it;
-                    if (!fits(k, R, dense)) continue;
-                    order.push_back(k);
+                    if (!fits(k, R, dense, soft_bits)) continue;
+                    P.order.push_back(k);
                     ngrad += ps.ops[k].ngrad;
                     dense = dense || is_dense(ps.ops[k]);
                     ready.erase(it);
                     for (int sk : succ[k])
                         if (--indeg[sk] == 0) ready.insert(sk);
-                    took = true;
+                    took = any = true;
                     break;
                 }
             }
-            // grow R by the bits of the ready op that lets the most ready ops fit
+            return any;
+        };
+        // grow R by the bits of the ready op that lets the most ready ops fit
+        auto grow = [&]() {
             int best = -1, best_score = -1;
             std::vector<int> best_u;
             int considered = 0;
@@ -352,44 +431,73 @@ void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_
                 if (++considered > 64) break;
                 const PassOp &op = ps.ops[k];
                 if (ngrad + op.ngrad > kMaxStageGrads) continue;
-                std::vector<int> u = union_with(need(op));
                 const bool dn = dense || is_dense(op);
-                if ((int)u.size() > (dn ? rd : r)) continue;
+                std::vector<int> u = union_with(soft_first ? soft(op) : need(op));
+                if ((int)u.size() > (dn ? rd : r)) u = union_with(need(op));
+                if ((int)u.size() > (dn ? rd : r) || u.size() == R.size()) continue;
                 int score = 0;
                 for (int j : ready)
-                    if (fits(j, u, dn)) score++;
+                    if (fits(j, u, dn, soft_first)) score++;
                 if (score > best_score) {
                     best = k;
                     best_score = score;
                     best_u = u;
                 }
             }
-            if (best < 0) break;
+            if (best < 0) return false;
             R = best_u;
+            return true;
+        };
+        for (;;) {
+            if (soft_first && take(true)) continue;
+            if (!soft_first && take(false)) continue;
+            if (grow()) continue;
+            if (soft_first && take(false)) continue;
+            break;
         }
-        stage_list.push_back({R, {begin, (int)order.size()}});
-        if ((int)order.size() == begin) fail(TQ_E_UNSUPPORTED, "internal planner error: empty stage");
+        if ((int)P.order.size() == begin) fail(TQ_E_UNSUPPORTED, "internal planner error: empty stage");
+        Packing::St st{padded(R, dense ? rd : r, t), begin, (int)P.order.size(), dense};
+        // modelled cost: one LDS round trip plus the ops, or the dense
+        // matrix where the stage can use one
+        int ops = 0;
+        bool uni = forward;
+        for (int i = begin; i < st.end; i++) {
+            ops += op_cost(ps.ops[P.order[i]]);
+            uni = uni && uniform(ps.ops[P.order[i]], st.bits);
+        }
+        P.cost += kStageCost + (uni ? std::min(ops, 4 << (int)st.bits.size()) : ops);
+        P.st.push_back(st);
     }
-    if ((int)order.size() != nops) fail(TQ_E_UNSUPPORTED, "internal planner error: op dependency cycle");
+    if ((int)P.order.size() != nops) fail(TQ_E_UNSUPPORTED, "internal planner error: op dependency cycle");
+    return P;
+}
+
+} // namespace stages
+
+void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at, bool forward)
+{
+    const int nops = (int)ps.ops.size();
+    ps.stages.clear();
+    stages::Packing best;
+    bool first = true;
+    for (int v = 0; v < 4; v++) {
+        stages::Packing P = stages::pack(ps, rmax, rdense, v & 1, v & 2, forward);
+        if (first || P.cost < best.cost) best = std::move(P);
+        first = false;
+    }
     std::vector<PassOp> ops(nops);
-    for (int k = 0; k < nops; k++) ops[k] = ps.ops[order[k]];
+    for (int k = 0; k < nops; k++) ops[k] = ps.ops[best.order[k]];
     ps.ops = std::move(ops);
 
-    for (auto &sl : stage_list) {
-        const int begin = sl.second.first, end = sl.second.second;
-        bool dense = false;
-        for (int k = begin; k < end; k++) dense = dense || is_dense(ps.ops[k]);
-        const int rs = dense ? rd : r;
-        std::vector<int> bits = sl.first;
-        for (int b = t - 1; b >= 0 && (int)bits.size() < rs; b--)
-            if (std::find(bits.begin(), bits.end(), b) == bits.end()) bits.push_back(b);
-        std::sort(bits.begin(), bits.end());
+    for (auto &sl : best.st) {
+        const std::vector<int> &bits = sl.bits;
+        const int rs = (int)bits.size();
         Stage st{};
         st.r = (uint8_t)rs;
         for (int j = 0; j < rs; j++) st.bits[j] = (uint8_t)bits[j];
-        st.op_begin = ps.op_offset + begin;
-        st.op_end = ps.op_offset + end;
-        for (int k = begin; k < end; k++) {
+        st.op_begin = ps.op_offset + sl.begin;
+        st.op_end = ps.op_offset + sl.end;
+        for (int k = sl.begin; k < sl.end; k++) {
             PassOp &op = ps.ops[k];
             auto idx = [&](uint8_t l) -> uint8_t {
                 for (int j = 0; j < rs; j++)
@@ -443,18 +551,9 @@ bool stage_fusable(const Pass &ps, const Stage &st)
 // dispatch overhead.
 bool dense_pays(const Pass &ps, const Stage &st)
 {
-    const int dense = 4 << st.r;
     int ops = 0;
-    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++) {
-        const PassOp &op = ps.ops[k];
-        int c = 4;
-        if (op.kind == K_M1) c = op.ctrl ? 4 : 8;
-        if (op.kind == K_M2) c = 16;
-        if (op.kind == K_F2) c = 6;
-        if (op.kind == K_P2) c = 8;
-        ops += c + kOpDispatchCost;
-    }
-    return dense < ops;
+    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++) ops += stages::op_cost(ps.ops[k]);
+    return (4 << st.r) < ops;
 }
 
 // Append a pass, split into consecutive passes over the same tile when its
@@ -708,7 +807,7 @@ void plan_group(Group &g, const Options &opt, int S)
     int off = 0;
     for (Pass &ps : g.fwd) {
         ps.op_offset = off;
-        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at);
+        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at, true);
         off += (int)ps.ops.size();
         // forward stages whose ops act alike on every item become one dense
         // matrix when that is cheaper than the ops one by one (matrix
@@ -724,7 +823,8 @@ void plan_group(Group &g, const Options &opt, int S)
     off = 0;
     for (Pass &ps : g.rev) {
         ps.op_offset = off;
-        make_stages(ps, n <= std::min(opt.tile, 12) ? kStageBitsRevResident : kStageBitsRev, kRevDense2Bits, g, task_at);
+        make_stages(ps, n <= std::min(opt.tile, 12) ? kStageBitsRevResident : kStageBitsRev, kRevDense2Bits, g, task_at,
+                    false);
         off += (int)ps.ops.size();
     }
 
