@@ -71,10 +71,29 @@ __device__ uint64_t pdep64(uint64_t v, uint64_t mask)
     return r;
 }
 
+// Wavefront sum of a double, in the VALU: DPP quad swaps and row mirrors
+// sum each row of 16 lanes, then the four row sums are read out and added
+// (in the same order in every lane, so every lane returns the same value).
+template <int kCtrl> __device__ __forceinline__ double dpp_mov(double v)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_mov_dpp((int)b, kCtrl, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), kCtrl, 0xf, 0xf, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+__device__ __forceinline__ double read_lane(double v, int lane)
+{
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)b, lane), hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
 __device__ __forceinline__ double wave_sum(double v)
 {
-    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
-    return v;
+    v += dpp_mov<0xb1>(v);   // quad_perm [1,0,3,2]: lane ^ 1
+    v += dpp_mov<0x4e>(v);   // quad_perm [2,3,0,1]: lane ^ 2
+    v += dpp_mov<0x141>(v);  // row_half_mirror: the other quad of the half row
+    v += dpp_mov<0x140>(v);  // row_mirror: the other half of the row
+    return (read_lane(v, 0) + read_lane(v, 16)) + (read_lane(v, 32) + read_lane(v, 48));
 }
 
 // parity of popcount
