@@ -71,6 +71,19 @@ struct PauliArgs {
     double *partial;         // [nrows][wg_per_row][k_count]
 };
 
+struct DiagArgs {
+    const float2 *psi;
+    int64_t row_stride;
+    const int32_t *rows;     // state rows
+    const DChunk *chunks;
+    const int32_t *row_chunk_begin, *row_chunk_count;
+    const DClass *classes;
+    const DTerm *terms;
+    int k_begin, k_count;    // observables of this launch
+    int blocks_log2, wg_per_row;
+    double *partial;         // [nrows][wg_per_row][k_count]
+};
+
 struct PauliReduceArgs {
     const int32_t *rows;     // batch index of each row
     const double *partial;
@@ -175,6 +188,8 @@ hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
 constexpr int kPauliTileMax = 12;
 size_t pauli_lds_bytes(const TileGeom &g, int k_count, bool partner);
 hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t s);
+// amax: the largest class count of a chunk (<= kDiagClassMax)
+hipError_t launch_pauli_diag(const DiagArgs &a, int nrows, int amax, hipStream_t s);
 hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s);
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s);
 hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s);

@@ -1486,6 +1486,121 @@ __global__ __launch_bounds__(256) void k_pauli_reduce(PauliReduceArgs a)
     if (threadIdx.x == 0) a.out[(int64_t)a.rows[row] * a.K + a.k_begin + j] = (float)red[0];
 }
 
+// ------------------------------------------ diagonal Pauli sums in HBM
+// Expectations of Z-only Pauli sums, streamed from HBM without LDS staging:
+// workgroup w of a row sweeps the blocks w, w + wg_per_row, ... of the row,
+// loading each thread's 16 amplitudes of the next block while it transforms
+// the current one.  The class weights D(blk) are staged in LDS for
+// kDiagRefill blocks at a time (a wave per class, a lane per block; classes
+// past the chunk's get weight zero, so every block runs the same straight-line
+// code).  Class c
+// accumulates D(blk) W_v in its own register; the thread's sign chi_zT(tid)
+// is applied once at the end, before the fixed-order reduction of each
+// observable.
+template <int A>
+__global__ __launch_bounds__(256) void k_pauli_diag(DiagArgs a)
+{
+    __shared__ double dw[A * kDiagRefill];
+    __shared__ double red[4];
+    extern __shared__ __align__(16) unsigned char smem[];
+    double *esum = reinterpret_cast<double *>(smem);  // [k_count]
+
+    const int bid = xcd_block(blockIdx.x, gridDim.x);
+    const int row = bid / a.wg_per_row, w = bid % a.wg_per_row;
+    const int b = cget(a.rows, row);
+    const float4 *ps = reinterpret_cast<const float4 *>(a.psi + (int64_t)b * a.row_stride);
+    const int tid = threadIdx.x, lane = tid % 64;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+    // blocks of this workgroup: w + i wg_per_row for i < mine (w < wg_per_row <= blocks)
+    const int64_t mine = (((int64_t)1 << a.blocks_log2) - w + a.wg_per_row - 1) / a.wg_per_row;
+    const int kend = a.k_begin + a.k_count;
+    const DChunk *chunks = a.chunks + cget(a.row_chunk_begin, row);
+    const int nchunks = cget(a.row_chunk_count, row);
+    for (int j = tid; j < a.k_count; j += blockDim.x) esum[j] = 0;
+
+    for (int ci = 0; ci < nchunks; ci++) {
+        const DChunk ch = cget(chunks, ci);
+        if (ch.k_hi < a.k_begin || ch.k_lo >= kend) continue;
+        const DClass *cls = a.classes + ch.c_begin;
+        const int ncls = ch.c_end - ch.c_begin;
+        double G[A];
+        uint32_t vv[A];
+#pragma unroll
+        for (int c = 0; c < A; c++) {
+            G[c] = 0.0;
+            vv[c] = c < ncls ? cget(cls, c).v : 0u;
+        }
+        float4 nx[8];
+        auto load = [&](int64_t i) {
+            const float4 *src = ps + ((w + i * a.wg_per_row) << (kDiagBlockBits - 1)) + tid;
+#pragma unroll
+            for (int j = 0; j < 8; j++) nx[j] = src[256 * j];
+        };
+        load(0);
+        for (int64_t i = 0; i < mine; i++) {
+            const int slot = (int)(i % kDiagRefill);
+            if (slot == 0) {
+                __syncthreads();  // the previous weights are consumed
+                const uint64_t blk = (uint64_t)(w + (i + lane) * a.wg_per_row);
+                for (int c = wave; c < A; c += 4) {
+                    double d = 0.0;  // classes past the chunk's weigh nothing
+                    if (c < ncls) {
+                        const DClass cc = cget(cls, c);
+                        for (int t = cc.t_begin; t < cc.t_end; t++) {
+                            const DTerm tm = cget(a.terms, t);
+                            d += par64(blk & tm.zB) ? -tm.c : tm.c;
+                        }
+                    }
+                    dw[lane * A + c] = d;
+                }
+                __syncthreads();
+            }
+            double p[16];
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                p[2 * j] = fma((double)nx[j].x, (double)nx[j].x, (double)nx[j].y * (double)nx[j].y);
+                p[2 * j + 1] = fma((double)nx[j].z, (double)nx[j].z, (double)nx[j].w * (double)nx[j].w);
+            }
+            if (i + 1 < mine) load(i + 1);
+            // Walsh transform over the four register bits: p[v] = W_v
+#pragma unroll
+            for (int sb = 1; sb < 16; sb <<= 1)
+#pragma unroll
+                for (int r = 0; r < 16; r++)
+                    if (!(r & sb)) {
+                        const double x = p[r], y = p[r | sb];
+                        p[r] = x + y;
+                        p[r | sb] = x - y;
+                    }
+            double dv[A];
+#pragma unroll
+            for (int c = 0; c < A; c++) dv[c] = dw[slot * A + c];
+#pragma unroll
+            for (int c = 0; c < A; c++) G[c] = fma(dv[c], p[vv[c]], G[c]);
+        }
+        // thread signs, then one fixed-order reduction per observable
+        const int k_first = ch.k_lo > a.k_begin ? ch.k_lo : a.k_begin;
+        const int k_last = ch.k_hi < kend - 1 ? ch.k_hi : kend - 1;
+        for (int k = k_first; k <= k_last; k++) {
+            double e = 0.0;
+#pragma unroll
+            for (int c = 0; c < A; c++)
+                if (c < ncls) {
+                    const DClass cc = cget(cls, c);
+                    if (cc.k == k) e += par32((uint32_t)tid & cc.zT) ? -G[c] : G[c];
+                }
+            const double v = wave_sum(e);
+            if (lane == 0) red[wave] = v;
+            __syncthreads();
+            if (tid == 0) esum[k - a.k_begin] += ((red[0] + red[1]) + red[2]) + red[3];
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+    double *out = a.partial + ((int64_t)row * a.wg_per_row + w) * a.k_count;
+    for (int j = tid; j < a.k_count; j += blockDim.x) out[j] = esum[j];
+}
+
 // ------------------------------------------------------ reverse pass
 // psi and phi tiles side by side in LDS; the pass's matrices too.
 __global__ __launch_bounds__(256, 2) void k_rev_pass(RevArgs a)
@@ -1558,36 +1673,36 @@ __global__ void k_grad_reduce(GradReduceArgs a)
 // gates, expectations, H_g, reverse sweep, gradient reduction -- in one
 // launch, on the matrices k_build_mats wrote.  At most 128 registers per
 // thread, so that four rows share a CU.  Outputs are reduced in a fixed order.
+// The resident computation in three parts around the forward and reverse
+// register stages (which the generic kernel loops over and a specialised
+// kernel spells out).  acc: one accumulator row per wave (terms, then
+// gradient slots); lp/lf: psi/phi of the row in LDS.
 template <class MT>
-__device__ __forceinline__ void resident_row(const ResArgs &a, MT M, SMat G, double *acc, float2 *lp, float2 *lf, int row,
-                                             int tid, int nt)
+__device__ __forceinline__ void resident_begin(const ResArgs &a, MT M, double *acc, float2 *lp, int tid, int nt)
 {
     const int n = a.n;
     const uint32_t T = 1u << n;
-    const int b = cget(a.rows, row);
-    const int wave = tid / 64, lane = tid % 64;
-    const int nw = nt / 64;  // accumulator copies, one per wave
-    auto sync = [] { __syncthreads(); };
-    // whole-state tile: every term's partner is local, so the tile index
-    // table and the HBM partner pointer are never used (valid LDS addresses
-    // are passed instead of null pointers)
-    TileCtx tc{reinterpret_cast<const uint64_t *>(acc), T - 1, n};
-
-    for (int j = tid; j < nw * a.nacc; j += nt) acc[j] = 0;
+    for (int j = tid; j < (nt / 64) * a.nacc; j += nt) acc[j] = 0;
     // product-state initialisation
     for (uint32_t l = tid; l < T; l += nt) {
         double2 v = make_double2(1.0, 0.0);
         for (int q = 0; q < n; q++) v = zmul(v, M[a.init_mat[q] + (((l >> (n - 1 - q)) & 1) ? 2 : 0)]);
         lp[sw(l)] = down2(v);
     }
-    sync();
-    // forward gates
-    for (int si = 0; si < a.nfstages; si++) {
-        const Stage st = cget(a.fstages, si);
-        run_stage_any(st, a.fops, M, 0, G, lp, n, 0, tid, nt);
-        sync();
-    }
-    // state output and expectation terms
+    __syncthreads();
+}
+
+// state output, expectation terms, and (adjoint) phi = H_g psi
+__device__ __forceinline__ void resident_middle(const ResArgs &a, double *acc, float2 *lp, float2 *lf, int row, int tid, int nt)
+{
+    const int n = a.n;
+    const uint32_t T = 1u << n;
+    const int b = cget(a.rows, row);
+    const int wave = tid / 64, lane = tid % 64;
+    // whole-state tile: every term's partner is local, so the tile index
+    // table and the HBM partner pointer are never used (valid LDS addresses
+    // are passed instead of null pointers)
+    TileCtx tc{reinterpret_cast<const uint64_t *>(acc), T - 1, n};
     if (a.state_out) {
         float2 *out = a.state_out + (int64_t)a.out_rows[row] * a.out_stride;
         for (uint32_t l = tid; l < T; l += nt) out[l] = lp[sw(l)];
@@ -1598,19 +1713,21 @@ __device__ __forceinline__ void resident_row(const ResArgs &a, MT M, SMat G, dou
         double v = wave_sum(term_tile_sum(cget(terms, k), tc, lp, lp, 0, n, tid, nt));
         if (lane == 0) acc[wave * a.nacc + k] += v;
     }
-    // adjoint sweep
     if (a.grad) {
         const float *up = a.upstream + (int64_t)b * a.K;
         for (uint32_t l = tid; l < T; l += nt) lf[sw(l)] = h_elem(l, 0, terms, nterm, up, lp, tc, lp);
-        sync();
-        for (int si = 0; si < a.nrstages; si++) {
-            const Stage st = cget(a.rstages, si);
-            run_rev_stage_any<kStageBitsRevResident>(st, a.rops, M, 0, lp, lf, n, 0, acc, a.nacc, -a.gacc, tid, nt);
-            sync();
-        }
+        __syncthreads();
     }
-    sync();
-    // outputs
+}
+
+// outputs: expectations and gradients, reduced over the waves in a fixed order
+__device__ __forceinline__ void resident_end(const ResArgs &a, double *acc, int row, int tid, int nt)
+{
+    __syncthreads();
+    const int b = cget(a.rows, row);
+    const int nw = nt / 64;
+    const TermDev *terms = a.terms ? a.terms + cget(a.row_term_begin, row) : nullptr;
+    const int nterm = a.terms ? cget(a.row_term_count, row) : 0;
     auto total = [&](int j) {
         double s = 0;
         for (int w = 0; w < nw; w++) s += acc[w * a.nacc + j];
@@ -1646,7 +1763,21 @@ __global__ __launch_bounds__(256, 4) void k_resident(ResArgs a)
     float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);   // [T]
     float2 *lf = lp + T;                                         // [T] (adjoint)
     const SMat M = smat(a.mats + (int64_t)blockIdx.x * a.mat_stride);
-    resident_row(a, M, M, acc, lp, lf, blockIdx.x, threadIdx.x, blockDim.x);
+    const int tid = threadIdx.x, nt = blockDim.x;
+    resident_begin(a, M, acc, lp, tid, nt);
+    for (int si = 0; si < a.nfstages; si++) {
+        const Stage st = cget(a.fstages, si);
+        run_stage_any(st, a.fops, M, 0, M, lp, a.n, 0, tid, nt);
+        __syncthreads();
+    }
+    resident_middle(a, acc, lp, lf, blockIdx.x, tid, nt);
+    if (a.grad)
+        for (int si = 0; si < a.nrstages; si++) {
+            const Stage st = cget(a.rstages, si);
+            run_rev_stage_any<kStageBitsRevResident>(st, a.rops, M, 0, lp, lf, a.n, 0, acc, a.nacc, -a.gacc, tid, nt);
+            __syncthreads();
+        }
+    resident_end(a, acc, blockIdx.x, tid, nt);
 }
 
 // ------------------------------------------------------------- sampling
@@ -1907,6 +2038,24 @@ hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t
     case 16: return launch_pauli_p<16>(a, nrows, lds, s);
     default: return hipErrorInvalidValue;
     }
+}
+
+template <int A> hipError_t launch_pauli_diag_a(const DiagArgs &a, int nrows, hipStream_t s)
+{
+    const size_t lds = sizeof(double) * (size_t)a.k_count;
+    hipError_t e = set_lds(k_pauli_diag<A>, lds);
+    if (e != hipSuccess) return e;
+    prof::Scope ps("pauli", s);
+    hipLaunchKernelGGL(k_pauli_diag<A>, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pauli_diag(const DiagArgs &a, int nrows, int amax, hipStream_t s)
+{
+    if (nrows <= 0) return hipSuccess;
+    if (amax <= 8) return launch_pauli_diag_a<8>(a, nrows, s);
+    if (amax <= 16) return launch_pauli_diag_a<16>(a, nrows, s);
+    return launch_pauli_diag_a<kDiagClassMax>(a, nrows, s);
 }
 
 hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s)

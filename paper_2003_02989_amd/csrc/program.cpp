@@ -973,6 +973,72 @@ PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vect
     return pt;
 }
 
+DiagTables diag_tables(const std::vector<std::vector<TermDev>> &per_row, bool uniform)
+{
+    DiagTables dt;
+    struct Item {
+        int k;
+        uint32_t v, zT;
+        uint64_t zB;
+        double c;
+    };
+    dt.row_begin.assign(per_row.size(), 0);
+    dt.row_count.assign(per_row.size(), 0);
+    for (size_t r = 0; r < per_row.size(); r++) {
+        if (uniform && r > 0) {
+            dt.row_begin[r] = dt.row_begin[0];
+            dt.row_count[r] = dt.row_count[0];
+            continue;
+        }
+        std::vector<Item> items;
+        for (const TermDev &td : per_row[r]) {
+            if (td.x) fail(TQ_E_INVALID, "internal error: diagonal tables for a term with X or Y factors");
+            const uint64_t z = td.z;
+            items.push_back(Item{td.k, (uint32_t)((z & 1) | (((z >> 9) & 7) << 1)), (uint32_t)((z >> 1) & 0xff),
+                                 z >> kDiagBlockBits, td.coeff});
+        }
+        std::stable_sort(items.begin(), items.end(), [](const Item &a, const Item &b) {
+            if (a.k != b.k) return a.k < b.k;
+            if (a.v != b.v) return a.v < b.v;
+            if (a.zT != b.zT) return a.zT < b.zT;
+            return a.zB < b.zB;
+        });
+        dt.row_begin[r] = (int32_t)dt.chunks.size();
+        DChunk ch{};
+        ch.c_begin = (int32_t)dt.classes.size();
+        auto close_chunk = [&]() {
+            ch.c_end = (int32_t)dt.classes.size();
+            if (ch.c_end > ch.c_begin) {
+                ch.k_lo = dt.classes[ch.c_begin].k;
+                ch.k_hi = dt.classes[ch.c_end - 1].k;
+                dt.amax = std::max(dt.amax, ch.c_end - ch.c_begin);
+                dt.chunks.push_back(ch);
+            }
+            ch.c_begin = ch.c_end;
+        };
+        for (size_t i = 0; i < items.size();) {
+            if ((int)dt.classes.size() - ch.c_begin == kDiagClassMax) close_chunk();
+            DClass cl{};
+            cl.k = items[i].k;
+            cl.v = items[i].v;
+            cl.zT = items[i].zT;
+            cl.t_begin = (int32_t)dt.terms.size();
+            for (; i < items.size() && items[i].k == cl.k && items[i].v == cl.v && items[i].zT == cl.zT; i++) {
+                // equal block masks share one weight term
+                if (dt.terms.size() > (size_t)cl.t_begin && dt.terms.back().zB == items[i].zB)
+                    dt.terms.back().c += items[i].c;
+                else
+                    dt.terms.push_back(DTerm{items[i].zB, items[i].c});
+            }
+            cl.t_end = (int32_t)dt.terms.size();
+            dt.classes.push_back(cl);
+        }
+        close_chunk();
+        dt.row_count[r] = (int32_t)dt.chunks.size() - dt.row_begin[r];
+    }
+    return dt;
+}
+
 std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt)
 {
     if (!blob) fail(TQ_E_INVALID, "program blob is NULL");

@@ -125,4 +125,15 @@ struct PauliTables {
 };
 PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vector<TermDev>> &per_row, bool uniform);
 
+// Tables of the diagonal (Z-only) Pauli kernel: every term of every row must
+// have x = 0 and the states at least kDiagBlockBits qubits.
+struct DiagTables {
+    std::vector<DChunk> chunks;
+    std::vector<int32_t> row_begin, row_count;
+    std::vector<DClass> classes;
+    std::vector<DTerm> terms;
+    int amax = 0;  // largest class count of a chunk
+};
+DiagTables diag_tables(const std::vector<std::vector<TermDev>> &per_row, bool uniform);
+
 } // namespace tq

@@ -82,9 +82,15 @@ struct ObsGroupDev {
     TileGeom pgeom;
     bool partner = false;
     DevBuf chunks, cbegin, ccount, xfg, xg, us, pterms;
+    // tables of the diagonal Pauli kernel (all terms Z-only, n >= kDiagBlockBits)
+    bool diag = false;
+    int damax = 0;
+    DevBuf dchunks, dcbegin, dccount, dclasses, dterms;
     void release()
     {
-        for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms}) b->release();
+        for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
+                          &dcbegin, &dccount, &dclasses, &dterms})
+            b->release();
     }
 };
 
@@ -378,11 +384,64 @@ void ensure_obs(tq_program p, tq_observables o)
         upload(og->xg, pt.xg);
         upload(og->us, pt.us);
         upload(og->pterms, pt.terms);
+        bool diag = n >= kDiagBlockBits;
+        for (auto &row : per_row)
+            for (auto &td : row) diag = diag && td.x == 0;
+        if (diag) {
+            DiagTables dt = diag_tables(per_row, uniform);
+            og->diag = true;
+            og->damax = dt.amax;
+            upload(og->dchunks, dt.chunks);
+            upload(og->dcbegin, dt.row_begin);
+            upload(og->dccount, dt.row_count);
+            upload(og->dclasses, dt.classes);
+            upload(og->dterms, dt.terms);
+        }
         out.push_back(std::move(og));
     }
     for (auto &old : p->obs_dev) old->release();
     p->obs_dev = std::move(out);
     p->obs_id = o->od->id;
+}
+
+// Expectations of Z-only Pauli sums over group gi's rows (n >= 12), streamed
+// from HBM by the diagonal kernel.
+void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    ObsGroupDev &og = *p->obs_dev[gi];
+    const int nrows = (int)g.rows.size();
+    DiagArgs a{};
+    a.psi = psi;
+    a.row_stride = (int64_t)1 << g.n;
+    a.rows = (const int32_t *)gd.ident.p;
+    a.chunks = (const DChunk *)og.dchunks.p;
+    a.row_chunk_begin = (const int32_t *)og.dcbegin.p;
+    a.row_chunk_count = (const int32_t *)og.dccount.p;
+    a.classes = (const DClass *)og.dclasses.p;
+    a.terms = (const DTerm *)og.dterms.p;
+    a.blocks_log2 = g.n - kDiagBlockBits;
+    // about eight workgroups per compute unit, each sweeping many blocks
+    const int64_t nblk = (int64_t)1 << a.blocks_log2;
+    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(nblk, 2048 / nrows));
+    const int64_t slots = (int64_t)nrows * a.wg_per_row;
+    const int kmax = (int)std::max<int64_t>(1, std::min<int64_t>(1024, ((int64_t)32 << 20) / slots));
+    for (int k0 = 0; k0 < K; k0 += kmax) {
+        a.k_begin = k0;
+        a.k_count = std::min(kmax, K - k0);
+        a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)slots * a.k_count);
+        hip_check(launch_pauli_diag(a, nrows, og.damax, s), "diagonal Pauli kernel launch");
+        PauliReduceArgs r{};
+        r.rows = (const int32_t *)gd.rows.p;
+        r.partial = a.partial;
+        r.wg_per_row = a.wg_per_row;
+        r.K = K;
+        r.k_begin = k0;
+        r.k_count = a.k_count;
+        r.out = out;
+        hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
+    }
 }
 
 // Run the Pauli kernel over group gi's rows: expectations into out[b, k]
@@ -397,6 +456,10 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     ObsGroupDev &og = *p->obs_dev[gi];
     const int nrows = (int)g.rows.size();
     if (K == 0 || nrows == 0) return;
+    if (!phi && og.diag) {
+        diag_group(p, gi, psi, K, out, s);
+        return;
+    }
     PauliArgs a{};
     a.psi = psi;
     a.phi = phi;

@@ -159,4 +159,34 @@ struct PChunk {      // observables [k0, k0 + nk), nk <= kPauliChunk
     int32_t xf_begin, xf_end;
 };
 
+// Diagonal (Z-only) Pauli sums over whole states, read straight from HBM.
+// A state is cut into blocks of 2^12 amplitudes; thread tid of a block holds
+// the 16 amplitudes 512 j + 2 tid + e (j < 8, e < 2).  With r = e + 2 j the
+// register index, a term c Z^z splits z into zB (block bits 12..n-1), zT
+// (bits 1..8, the thread) and v (bit 0 and bits 9..11, the register):
+//     <Z^z> = sum_blk chi_zB(blk) sum_tid chi_zT(tid) W_v(blk, tid),
+//     W_v = sum_r chi_v(r) |psi|^2,
+// so each thread needs the Walsh transform W of its 16 probabilities and one
+// accumulator per class of terms sharing (observable, v, zT); the sign of
+// the block is folded into a per-block class weight
+// D(blk) = sum_{t in class} c_t chi_zB_t(blk).
+constexpr int kDiagBlockBits = 12;
+constexpr int kDiagClassMax = 32;   // classes accumulated in one sweep
+constexpr int kDiagRefill = 64;     // blocks whose class weights are staged at once
+struct DTerm {
+    uint64_t zB;     // z on the block bits, shifted down by kDiagBlockBits
+    double c;
+};
+struct DClass {
+    int32_t k;       // observable
+    uint32_t v;      // register mask (bit 0: index bit 0; bits 1..3: index bits 9..11)
+    uint32_t zT;     // thread mask (index bits 1..8)
+    int32_t t_begin, t_end;
+    int32_t pad;
+};
+struct DChunk {      // classes swept together, observables k_lo..k_hi
+    int32_t c_begin, c_end;
+    int32_t k_lo, k_hi;
+};
+
 } // namespace tq

@@ -123,6 +123,43 @@ def test_many_observables_and_terms(n, tile):
     compare(gpu_outputs(w, max_tile_qubits=tile), oracle_outputs(w))
 
 
+def _z_observables(rng, n, K, many):
+    # Z-only sums: one with `many` terms (more classes than one sweep of the
+    # diagonal kernel holds), an empty one, identity terms, a repeated
+    # string, and sum_i Z_i
+    row = []
+    for k in range(K):
+        if k == 1:
+            row.append([])
+            continue
+        if k == K - 1:
+            row.append([(0.3, [(q, "Z")]) for q in range(n)])
+            continue
+        T = many if k == 0 else int(rng.integers(1, 6))
+        terms = []
+        for _ in range(T):
+            w = int(rng.integers(0, 6))
+            support = sorted(int(q) for q in rng.choice(n, size=w, replace=False)) if w else []
+            terms.append((0.25 * float(rng.standard_normal()), [(q, "Z") for q in support]))
+        if k == 2:
+            terms += [terms[-1], (0.5, [])]
+        row.append(terms)
+    return row
+
+
+@pytest.mark.parametrize("n,B,uniform", [(12, 3, False), (13, 2, False), (17, 2, False), (14, 4, True)])
+def test_diagonal_observables(n, B, uniform):
+    # Z-only observables on states of >= 12 qubits take the streaming
+    # diagonal kernel (expectations) and the tile kernel (adjoint)
+    rng = wl.rng_for(5100 + n)
+    w = wl.random_batch(5200 + n, B=B, n=n, n_gates=50, n_symbols=4, K=5)
+    shared = _z_observables(rng, n, 5, many=45)
+    for b in range(B):
+        w.observables[b] = shared if uniform else _z_observables(rng, n, 5, many=45)
+    say("diagonal observables", n, B, uniform)
+    compare(gpu_outputs(w), oracle_outputs(w))
+
+
 @pytest.mark.gpu
 def test_amplitudes_from_state_matches_amplitudes():
     # the state-based lookup returns what tq_amplitudes returns, bit for bit,
