@@ -163,6 +163,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-specialize", action="store_true",
+                    help="run resident circuits (c1, c2) with the precompiled table-driven kernel instead of the "
+                         "one compiled for their structure")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
@@ -195,7 +198,8 @@ def main():
     w = workload(args.config)
     B, K = w.B, w.K
     t_cold0 = time.perf_counter()
-    prog = tq.Program(w.program_blob())
+    specialize = args.config in ("c1", "c2") and not args.no_specialize
+    prog = tq.Program(w.program_blob(), specialize=specialize)
     obs = tq.Observables(w.observable_blob())
     t_create = time.perf_counter() - t_cold0
     theta = torch.as_tensor(w.theta, device="cuda") if w.n_symbols else None
@@ -287,7 +291,8 @@ def main():
         "data": "synthetic (seeded generators, no datasets)",
         "config": {"workload": describe_workload(args.config, w), "storage": "complex64", "batch": B, "qubits": w.n_max,
                    "symbols": w.n_symbols, "observables": K, "pauli_terms": n_terms,
-                   "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3},
+                   "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3,
+                   "specialized_kernel": specialize},
         "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": traffic, "launches_per_step": launches_per_step,
                      "avg_launch_ms": avg_ms,

@@ -65,12 +65,19 @@ typedef enum {
  *                    -1 = apply every gate on its own;
  *   max_pass_gates:  at most this many gates per sweep over the state
  *                    (default 0 = no limit; 1 makes every gate its own pass,
- *                    which measures the bandwidth of single-gate passes). */
+ *                    which measures the bandwidth of single-gate passes);
+ *   specialize:      1 = circuits small enough to run resident (one
+ *                    workgroup per batch row, state in LDS) use a kernel
+ *                    generated for their structure and compiled with hipRTC
+ *                    on first use (or by tq_program_specialize), with every
+ *                    stage and op written in as constants; 0 = the
+ *                    precompiled kernel that reads the plan from tables. */
 typedef struct {
     int32_t max_tile_qubits;
     int32_t low_qubits;
     int32_t fuse;
     int32_t max_pass_gates;
+    int32_t specialize;
 } tq_options;
 
 /* Parse, validate and plan a batch of B parameterized circuits over S symbols
@@ -96,6 +103,15 @@ typedef struct {
  * tq_program_destroy. */
 tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *opt, tq_program *out);
 void tq_program_destroy(tq_program prog);
+
+/* Compile the kernels a program created with specialize = 1 generates for
+ * its circuit structures, ahead of their first launch.  target NULL: for the
+ * current device (the kernels are cached until the process ends); otherwise
+ * an offload target such as "gfx950", for which the code is only compiled and
+ * checked (no device is needed).  A compiler failure returns TQ_E_DEVICE with
+ * the compiler's log in tq_last_error(); programs without specialize = 1 or
+ * without resident structures return TQ_OK at once. */
+tq_status tq_program_specialize(tq_program prog, const char *target);
 
 /* Batch size, symbol count, largest qubit count, and (when not NULL) the
  * qubit count of every circuit into qubits_per_circuit[B] (host memory). */

@@ -1,0 +1,182 @@
+// kernel_args.h -- argument blocks of the libtq kernels (plain structs that
+// the host fills and the kernels take by value).
+#pragma once
+#ifndef __HIPCC_RTC__
+#include <hip/hip_runtime.h>
+#endif
+
+#include "tq_internal.h"
+
+namespace tq {
+
+constexpr int kMaxLevels = 8;    // sampler levels (64-ary), enough for 2^48 amplitudes
+
+struct BuildArgs {
+    const BuildTask *tasks;
+    int task_begin, task_end;
+    const Member *members;
+    const GateDev *gates;
+    const int32_t *slot_sym;
+    const double *slot_scale, *slot_off;
+    int uniform, n_slots;
+    const double *explicit_mats;
+    const float *theta;
+    int S;
+    const int32_t *rows;
+    double2 *mats;
+    int64_t mat_stride;
+};
+
+struct StageBuildArgs {
+    const Stage *stages;   // the group's forward stages
+    const int32_t *list;   // indices of the dense ones
+    int nlist;
+    const PassOp *ops;     // the group's forward ops
+    double2 *mats;
+    int64_t mat_stride;
+};
+
+struct PassArgs {
+    float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;
+    const double2 *mats;
+    int64_t mat_stride;
+    const PassOp *ops;     // the group's forward ops (stages index them)
+    const Stage *stages;   // this pass's stages
+    int nstages;
+    TileGeom g;
+    int tiles_log2;
+    int wg_per_row;
+    int product_init;
+    int32_t init_mat[kMaxQubits];
+    int mat_begin, mat_end;  // the pass's matrices, staged in LDS
+};
+
+struct PauliArgs {
+    const float2 *psi;
+    float2 *phi;             // NULL: expectations only
+    int phi_accumulate;      // add into phi instead of overwriting it
+    int64_t row_stride;
+    const int32_t *rows;     // state rows
+    const int32_t *brows;    // batch index of each row (upstream)
+    const PChunk *chunks;
+    const int32_t *row_chunk_begin, *row_chunk_count;
+    const PXfGroup *xfg;
+    const PXGroup *xg;
+    const PUSub *us;
+    const PTerm *terms;
+    const float *upstream;   // [B, K] (phi only)
+    int K;                   // observables per row (upstream stride)
+    int k_begin, k_count;    // observables of this launch
+    TileGeom g;
+    int tiles_log2, wg_per_row;
+    double *partial;         // [nrows][wg_per_row][k_count]
+};
+
+struct DiagArgs {
+    const float2 *psi;
+    int64_t row_stride;
+    const int32_t *rows;     // state rows
+    const DChunk *chunks;
+    const int32_t *row_chunk_begin, *row_chunk_count;
+    const DClass *classes;
+    const DTerm *terms;
+    int k_begin, k_count;    // observables of this launch
+    int blocks_log2, wg_per_row;
+    double *partial;         // [nrows][wg_per_row][k_count]
+};
+
+struct PauliReduceArgs {
+    const int32_t *rows;     // batch index of each row
+    const double *partial;
+    int wg_per_row, K, k_begin, k_count;
+    float *out;
+};
+
+struct RevArgs {
+    float2 *psi, *phi;
+    int64_t row_stride;
+    const int32_t *rows;
+    const double2 *mats;
+    int64_t mat_stride;
+    const PassOp *ops;     // the group's reverse ops
+    const Stage *stages;   // this pass's stages
+    int nstages;
+    TileGeom g;
+    int tiles_log2, wg_per_row;
+    int store;
+    double *gpart;  // [nrows][wg_per_row][n_gslots]
+    int n_gslots, gbase, gcount;
+    int mat_begin, mat_end;
+};
+
+struct ResArgs {
+    const double2 *mats;  // row blocks built by k_build_mats
+    int64_t mat_stride;
+    const double *slot_scale;
+    int uniform, n_slots;
+    int S;
+    const int32_t *rows;  // batch index of each row
+    int n;
+    const PassOp *fops;
+    const Stage *fstages;
+    int nfstages;
+    int32_t init_mat[kMaxQubits];
+    // optional state output
+    float2 *state_out;
+    int64_t out_stride;
+    const int32_t *out_rows;
+    // optional expectations
+    const TermDev *terms;
+    const int32_t *row_term_begin, *row_term_count;
+    int K;
+    float *exp_out;
+    int nacc, gacc;  // accumulators: [0, gacc) terms, [gacc, gacc + n_gslots) gradients
+    // optional adjoint
+    const PassOp *rops;
+    const Stage *rstages;
+    int nrstages;
+    const float *upstream;
+    const int32_t *sym_begin, *sym_gslots, *gslot_slot;
+    float *grad;
+};
+
+struct GradReduceArgs {
+    const int32_t *rows;
+    const double *gpart;
+    int wg_per_row, n_gslots;
+    const int32_t *sym_begin, *sym_gslots, *gslot_slot;
+    const double *slot_scale;
+    int uniform, n_slots;
+    int S;
+    float *grad;
+};
+
+struct SampArgs {
+    const float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;   // state rows (NULL: the row index)
+    const int32_t *brows;  // batch index of each row (NULL: the row index)
+    uint64_t *levels;
+    int64_t row_level;  // entries per row
+    int nlev;           // stored levels 1..nlev; level nlev has at most 64 entries
+    int64_t count[kMaxLevels + 1];
+    int64_t off[kMaxLevels + 1];
+    int64_t n_shots;
+    uint64_t seed;
+    uint64_t *out;
+};
+
+struct GatherArgs {
+    const float2 *state;
+    int64_t row_stride;
+    const int32_t *rows;   // state rows (NULL: row r is state row r)
+    const int32_t *brows;  // batch index of each row (NULL: row r is batch row r)
+    int n;
+    const uint64_t *bits;
+    int64_t M;
+    float2 *out;
+};
+
+} // namespace tq

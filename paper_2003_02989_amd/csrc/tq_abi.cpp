@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "../../include/tq.h"
+#include "jit.h"
 #include "kernels.h"
 #include "program.h"
 
@@ -523,6 +524,24 @@ bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
     return resident_lds_bytes(g.n, nacc, adjoint) <= kResidentLds;
 }
 
+// Launch the resident kernel of group gi: the one specialised for the
+// group's structure when the program asks for it and its LDS fits the
+// default window, else the precompiled one.
+void run_resident(tq_program p, size_t gi, const ResArgs &a, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    const int nrows = (int)g.rows.size();
+    const size_t lds = resident_lds_bytes(a.n, a.nacc, a.grad != nullptr);
+    if (p->pd->opt.specialize && lds <= 65536) {
+        std::string log;
+        const hipError_t e = launch_resident_spec(g, a, nrows, lds, s, &log);
+        if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+        hip_check(e, "specialised resident launch");
+        return;
+    }
+    hip_check(launch_resident(a, nrows, s), "resident launch");
+}
+
 ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint, hipStream_t s)
 {
     const Group &g = *p->pd->groups[gi];
@@ -573,7 +592,7 @@ void forward_to_ws(tq_program p, size_t gi, const float *theta, float2 *psi, hip
         a.state_out = psi;
         a.out_stride = (int64_t)1 << g.n;
         a.out_rows = (const int32_t *)gd.ident.p;
-        hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+        run_resident(p, gi, a, s);
         return;
     }
     build_mats(p, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
@@ -630,6 +649,8 @@ tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *o
             if (opt->fuse < 0) o.fuse = false;
             if (opt->max_pass_gates < 0) fail(TQ_E_INVALID, "max_pass_gates must be >= 0");
             o.max_pass_gates = opt->max_pass_gates;
+            if (opt->specialize < 0 || opt->specialize > 1) fail(TQ_E_INVALID, "specialize must be 0 or 1");
+            o.specialize = opt->specialize == 1;
         }
         if (o.low > o.tile - 2) o.low = o.tile - 2;
         auto p = std::make_unique<tq_program_s>();
@@ -649,6 +670,21 @@ tq_status tq_program_info(tq_program prog, int32_t *B, int32_t *S, int32_t *max_
         if (max_qubits) *max_qubits = prog->pd->nmax;
         if (qpc)
             for (int b = 0; b < prog->pd->B; b++) qpc[b] = prog->pd->circuits[b].n;
+    });
+}
+
+tq_status tq_program_specialize(tq_program prog, const char *target)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        if (!prog->pd->opt.specialize) return;
+        for (size_t gi = 0; gi < prog->pd->groups.size(); gi++) {
+            if (!resident(prog, gi, false, 0)) continue;
+            std::string log;
+            const hipError_t e = prepare_resident_spec(*prog->pd->groups[gi], target, &log);
+            if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+            hip_check(e, "specialised kernel compilation");
+        }
     });
 }
 
@@ -696,7 +732,7 @@ tq_status tq_simulate_state(tq_program prog, const float *theta, void *states, v
                 a.state_out = (float2 *)states;
                 a.out_stride = stride;
                 a.out_rows = (const int32_t *)gd.rows.p;
-                hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+                run_resident(prog, gi, a, s);
             } else {
                 build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
                 forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s);
@@ -730,7 +766,7 @@ tq_status tq_expectation(tq_program prog, const float *theta, tq_observables obs
             if (resident(prog, gi, false, prog->obs_dev[gi]->tmax)) {
                 ResArgs a = resident_args(prog, gi, theta, false, s);
                 resident_terms(prog, gi, a, obs->od->K, out);
-                hip_check(launch_resident(a, (int)g.rows.size(), s), "resident launch");
+                run_resident(prog, gi, a, s);
                 continue;
             }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
@@ -774,7 +810,7 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                     a.nacc = og.tmax + g.n_gslots;
                 }
                 a.nacc = std::max(a.nacc, 1);
-                hip_check(launch_resident(a, nrows, s), "resident launch");
+                run_resident(prog, gi, a, s);
                 continue;
             }
             build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);

@@ -1,7 +1,17 @@
 // tq_internal.h -- data structures shared by the host planner and the HIP
 // kernels of libtq.  Nothing here is part of the public ABI.
 #pragma once
+#ifdef __HIPCC_RTC__
+// the run-time compiler brings its own fixed-width integer types
+using __hip_internal::int32_t;
+using __hip_internal::int64_t;
+using __hip_internal::uint16_t;
+using __hip_internal::uint32_t;
+using __hip_internal::uint64_t;
+using __hip_internal::uint8_t;
+#else
 #include <cstdint>
+#endif
 
 namespace tq {
 

@@ -27,7 +27,7 @@ class TQError(RuntimeError):
 
 class _Options(ctypes.Structure):
     _fields_ = [("max_tile_qubits", ctypes.c_int32), ("low_qubits", ctypes.c_int32),
-                ("fuse", ctypes.c_int32), ("max_pass_gates", ctypes.c_int32)]
+                ("fuse", ctypes.c_int32), ("max_pass_gates", ctypes.c_int32), ("specialize", ctypes.c_int32)]
 
 
 _lib = None
@@ -48,6 +48,7 @@ def lib():
         L.tq_program_destroy.argtypes = [vp]
         L.tq_program_destroy.restype = None
         L.tq_program_info.argtypes = [vp, p32, p32, p32, p32]
+        L.tq_program_specialize.argtypes = [vp, ctypes.c_char_p]
         L.tq_observables_create.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(vp)]
         L.tq_observables_destroy.argtypes = [vp]
         L.tq_observables_destroy.restype = None
@@ -62,7 +63,7 @@ def lib():
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
         L.tq_profile_start.argtypes = [ctypes.c_char_p]
         L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
-        for f in ("tq_program_create", "tq_program_info", "tq_observables_create", "tq_observables_info",
+        for f in ("tq_program_create", "tq_program_info", "tq_program_specialize", "tq_observables_create", "tq_observables_info",
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_adjoint_grad", "tq_amplitudes",
                   "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read"):
             getattr(L, f).restype = ctypes.c_int
@@ -98,8 +99,8 @@ def _dev(t, dtype, shape, name):
 class Program:
     """A parsed and planned batch of circuits (``tq_program``)."""
 
-    def __init__(self, blob: bytes, max_tile_qubits=0, low_qubits=0, fuse=True, max_pass_gates=0):
-        opt = _Options(max_tile_qubits, low_qubits, 1 if fuse else -1, max_pass_gates)
+    def __init__(self, blob: bytes, max_tile_qubits=0, low_qubits=0, fuse=True, max_pass_gates=0, specialize=False):
+        opt = _Options(max_tile_qubits, low_qubits, 1 if fuse else -1, max_pass_gates, 1 if specialize else 0)
         h = ctypes.c_void_p()
         _check(lib().tq_program_create(blob, len(blob), ctypes.byref(opt), ctypes.byref(h)))
         self._h = h
@@ -133,6 +134,13 @@ class Observables:
             _lib.tq_observables_destroy(h)
 
     __del__ = close
+
+
+def specialize(prog, target=None):
+    """Compile the program's structure-specialised kernels now (for the
+    current device, or only check them for an offload target such as
+    "gfx950" when `target` is given)."""
+    _check(lib().tq_program_specialize(prog._h, target.encode() if target else None))
 
 
 def describe(prog):

@@ -104,3 +104,22 @@ def test_compute_calls_validate_before_touching_the_device():
 
 def test_version():
     assert tq.lib().tq_version().startswith(b"tq ")
+
+
+def test_specialized_kernels_compile_for_gfx950():
+    # the kernels generated per circuit structure compile with hipRTC for
+    # gfx950 (no device needed): the two resident configurations and random
+    # structures over the whole opcode set
+    for w in (wl.c1_hea(), wl.c2_qnn(B=4),
+              wl.random_batch(6601, B=3, n=10, n_gates=60, n_symbols=5, K=3, hetero=True)):
+        p = create(w.program_blob(), specialize=True)
+        tq.specialize(p, "gfx950")
+    # a program without the option has nothing to compile
+    tq.specialize(create(wl.c2_qnn(B=2).program_blob()), "gfx950")
+
+
+def test_specialize_option_is_validated():
+    blob = wl.c1_hea().program_blob()
+    opt = tq._Options(0, 0, 1, 0, 2)
+    h = ctypes.c_void_p()
+    assert tq.lib().tq_program_create(blob, len(blob), ctypes.byref(opt), ctypes.byref(h)) == tq.TQ_E_INVALID

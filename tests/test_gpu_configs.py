@@ -32,6 +32,19 @@ def test_c2_full():
     compare(gpu_outputs(w, want=("exp", "grad")), oracle_outputs(w, want=("exp", "grad")))
 
 
+@pytest.mark.parametrize("name", ["c1", "c2"])
+def test_specialized_resident_configs(name):
+    # the structure-specialised resident kernel against the oracle, and
+    # against the precompiled kernel it stands in for
+    w = wl.CONFIGS[name]()
+    say(name, "specialised")
+    g = gpu_outputs(w, want=("exp", "grad"), specialize=True)
+    compare(g, oracle_outputs(w, want=("exp", "grad")))
+    base = gpu_outputs(w, want=("exp", "grad"))
+    assert np.abs(g["grad"] - base["grad"]).max() <= 1e-6
+    assert np.abs(g["exp"] - base["exp"]).max() <= 1e-6
+
+
 def test_c3_reduced():
     w = wl.c3_qaoa(B=16, n=14)
     say("c3 reduced n=14 B=16")

@@ -184,3 +184,13 @@ def test_resident_layouts(n, B):
     w = wl.random_batch(8800 + n, B=B, n=n, n_gates=70, n_symbols=6, K=2)
     say("resident", n, B)
     compare(gpu_outputs(w), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_specialized_resident_random(seed):
+    # structure-specialised resident kernels on heterogeneous batches of
+    # random circuits over the whole opcode set (one kernel per structure),
+    # states included (forward-only launches)
+    w = wl.random_batch(6600 + seed, B=4, n=9 + seed, n_gates=60, n_symbols=5, K=3, hetero=True)
+    say("specialised resident", seed)
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
