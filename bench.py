@@ -33,9 +33,9 @@ PEAK_FP64_TFLOPS = 78.6  # fp64 vector: 256 CUs x 2.4 GHz x 128 flop/clk
 # WRITE_SIZE runs (profiles/traffic.json, scaled by the counters' reading for
 # a plain device copy of known size).  Valid only for the sources it was
 # measured with: the hash below must match.
-TRAFFIC_SOURCES = ("paper_2003_02989_amd/csrc/kernels.hip", "paper_2003_02989_amd/csrc/kernels.h",
-                   "paper_2003_02989_amd/csrc/tq_internal.h", "paper_2003_02989_amd/csrc/program.cpp",
-                   "paper_2003_02989_amd/csrc/tq_abi.cpp")
+TRAFFIC_SOURCES = tuple("paper_2003_02989_amd/csrc/" + f for f in (
+    "kernels.hip", "kernels.h", "kernel_args.h", "device_ops.h", "tq_internal.h", "program.cpp", "program.h",
+    "tq_abi.cpp", "jit.cpp", "jit.h"))
 
 
 def sources_hash():
@@ -169,6 +169,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
+    ap.add_argument("--sweep-cases", default="all", choices=["all", "gates", "expectation"],
+                    help="with --sweep: which kernels to sweep")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB device buffer three times (reference for the HBM byte counters)")
     args = ap.parse_args()
@@ -185,7 +187,7 @@ def main():
     local_rank = int(os.environ.get("LOCAL_RANK", "0"))
     torch.cuda.set_device(local_rank)
     if args.sweep:
-        sweep(args.steps)
+        sweep(args.steps, args.sweep_cases)
         return
     if args.copy_calibration:
         src = torch.ones(1 << 27, dtype=torch.complex64, device="cuda")
@@ -305,7 +307,7 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def sweep(steps):
+def sweep(steps, cases="all"):
     """Effective HBM bandwidth of single-gate passes and of the expectation
     kernel for n = 24..30 with batches sized so the states span >= 1 GiB (the
     256 MB last-level cache cannot hold them).  A pass time is the difference
@@ -321,7 +323,7 @@ def sweep(steps):
     tile = int(os.environ.get("TQ_SWEEP_TILE", "0"))
 
     # plain device copy of the same footprint: the practical HBM ceiling
-    for n in (26, 30):
+    for n in ((26, 30) if cases in ("all", "gates") else ()):
         B = max(1, (1 << 27) >> n)
         src = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
         dst = torch.empty_like(src)
@@ -366,28 +368,34 @@ def sweep(steps):
     for n in (24, 26, 28, 30):
         B = max(1, (1 << 27) >> n)
         q = lambda bit: n - 1 - bit  # qubit on index bit `bit`
-        cases = []
+        gate_cases = []
         for bit in sorted({0, 3, 6, 10, n - 1}):
-            cases.append((f"1q RX on bit {bit}", [("CZ", (q(bit), q((bit + 1) % n)))], ("RX", q(bit), [const(0.3)])))
-        cases.append((f"fSim on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
+            gate_cases.append((f"1q RX on bit {bit}", [("CZ", (q(bit), q((bit + 1) % n)))], ("RX", q(bit), [const(0.3)])))
+        gate_cases.append((f"fSim on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
                       ("FSIM", (q(n - 1), q(n - 2)), [const(0.7), const(0.4)])))
-        cases.append(("fSim on bits 0,1", [("CZ", (q(0), q(1)))], ("FSIM", (q(0), q(1)), [const(0.7), const(0.4)])))
-        cases.append((f"XX^t on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
+        gate_cases.append(("fSim on bits 0,1", [("CZ", (q(0), q(1)))], ("FSIM", (q(0), q(1)), [const(0.7), const(0.4)])))
+        gate_cases.append((f"XX^t on bits {n-1},{n-2}", [("CZ", (q(n - 1), q(n - 2)))],
                       ("XXPOW", (q(n - 1), q(n - 2)), [const(0.3)])))
-        cases.append((f"CNOT control bit {n-1}, target bit 0", [("CZ", (q(n - 1), q(0)))], ("CNOT", (q(n - 1), q(0)))))
-        cases.append((f"RZZ on bits {n-1},0 (diagonal)", [("CZ", (q(n - 1), q(0)))], ("RZZ", (q(n - 1), q(0)), [const(0.3)])))
-        for name, prefix, gate in cases:
+        gate_cases.append((f"CNOT control bit {n-1}, target bit 0", [("CZ", (q(n - 1), q(0)))], ("CNOT", (q(n - 1), q(0)))))
+        gate_cases.append((f"RZZ on bits {n-1},0 (diagonal)", [("CZ", (q(n - 1), q(0)))], ("RZZ", (q(n - 1), q(0)), [const(0.3)])))
+        for name, prefix, gate in (gate_cases if cases in ("all", "gates") else []):
             ms = pass_ms(n, B, prefix, gate)
             gbs = 16.0 * (1 << n) * B / (ms * 1e-3) / 1e9
             print(json.dumps({"sweep": "gate_pass", "n": n, "batch": B, "case": name, "ms_per_pass": ms,
                               "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
-        # expectation kernel: sum_i Z_i, and 16 random X/Y/Z strings
+        if cases not in ("all", "expectation"):
+            continue
+        # expectation kernels: sum_i Z_i, 30 random Z_i Z_j plus a constant
+        # (the QAOA cost's shape), and 16 random X/Y/Z strings
         rng = np.random.default_rng(n)
         obs_sets = {"sum Z_i": [(1.0, [(i, "Z")]) for i in range(n)],
                     "16 XYZ strings": [(float(rng.standard_normal()),
                                         [(int(x), "XYZ"[int(rng.integers(0, 3))])
                                          for x in rng.choice(n, size=int(rng.integers(1, 5)), replace=False)])
-                                       for _ in range(16)]}
+                                       for _ in range(16)],
+                    "30 ZZ + constant": [(-0.5, [(int(a), "Z"), (int(b), "Z")])
+                                         for a, b in (rng.choice(n, size=2, replace=False) for _ in range(30))]
+                                        + [(15.0, [])]}
         c = Circuit(n)
         for i in range(n - 1):
             c.add("CZ", (i, i + 1))
