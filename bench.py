@@ -164,8 +164,8 @@ def main():
     ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-specialize", action="store_true",
-                    help="run resident circuits (c1, c2) with the precompiled table-driven kernel instead of the "
-                         "one compiled for their structure")
+                    help="run with the precompiled table-driven kernels instead of the ones compiled for the "
+                         "circuit structure on the first call")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
@@ -200,7 +200,7 @@ def main():
     w = workload(args.config)
     B, K = w.B, w.K
     t_cold0 = time.perf_counter()
-    specialize = args.config in ("c1", "c2") and not args.no_specialize
+    specialize = not args.no_specialize
     prog = tq.Program(w.program_blob(), specialize=specialize)
     obs = tq.Observables(w.observable_blob())
     t_create = time.perf_counter() - t_cold0

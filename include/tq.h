@@ -66,12 +66,13 @@ typedef enum {
  *   max_pass_gates:  at most this many gates per sweep over the state
  *                    (default 0 = no limit; 1 makes every gate its own pass,
  *                    which measures the bandwidth of single-gate passes);
- *   specialize:      1 = circuits small enough to run resident (one
- *                    workgroup per batch row, state in LDS) use a kernel
- *                    generated for their structure and compiled with hipRTC
- *                    on first use (or by tq_program_specialize), with every
- *                    stage and op written in as constants; 0 = the
- *                    precompiled kernel that reads the plan from tables. */
+ *   specialize:      1 = every circuit structure runs kernels generated
+ *                    for it (the resident kernel, or its forward tile passes)
+ *                    and compiled with hipRTC on first use (or by
+ *                    tq_program_specialize), with every stage and op written
+ *                    in as constants; 0 = the precompiled kernels that read
+ *                    the plan from tables.  Reverse tile passes always use
+ *                    the precompiled kernel. */
 typedef struct {
     int32_t max_tile_qubits;
     int32_t low_qubits;
@@ -105,12 +106,14 @@ tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *o
 void tq_program_destroy(tq_program prog);
 
 /* Compile the kernels a program created with specialize = 1 generates for
- * its circuit structures, ahead of their first launch.  target NULL: for the
- * current device (the kernels are cached until the process ends); otherwise
- * an offload target such as "gfx950", for which the code is only compiled and
- * checked (no device is needed).  A compiler failure returns TQ_E_DEVICE with
- * the compiler's log in tq_last_error(); programs without specialize = 1 or
- * without resident structures return TQ_OK at once. */
+ * its circuit structures (per structure: the resident kernel when its
+ * circuits run resident, else its forward tile passes), ahead of their first
+ * launch.
+ * target NULL: for the current device (the kernels are cached until the
+ * process ends); otherwise an offload target such as "gfx950", for which the
+ * code is only compiled and checked (no device is needed).  A compiler
+ * failure returns TQ_E_DEVICE with the compiler's log in tq_last_error(); a
+ * program without specialize = 1 returns TQ_OK at once. */
 tq_status tq_program_specialize(tq_program prog, const char *target);
 
 /* Batch size, symbol count, largest qubit count, and (when not NULL) the

@@ -27,7 +27,8 @@ def write_prelude(path):
     text = []
     for h in JIT_HEADERS:
         with open(os.path.join(CSRC, h)) as f:
-            text += [line for line in f.read().split("\n") if not line.startswith('#include "')]
+            text += [line for line in f.read().split("\n")
+                     if not line.startswith('#include "') and line.strip() != "#pragma once"]
     body = "\n".join(text)
     delim = "TQJIT"
     assert ")" + delim + '"' not in body
@@ -54,7 +55,7 @@ def build(verbose=True):
         subprocess.check_call(cmd)
         objs.append(obj)
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs + ["-lhiprtc"]
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs + ["-lhiprtc", "-pthread"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

@@ -693,7 +693,7 @@ template <int R> __device__ __forceinline__ uint32_t stage_base(const Stage &st,
 // matrices from row-block offset mbase on.
 // Dense stage: a <- S a with the 2^R x 2^R stage matrix S (row major),
 // read through the scalar cache.
-template <int R> __device__ __forceinline__ void rdense(double2 *a, SMat S)
+template <int R, class MT> __device__ __forceinline__ void rdense(double2 *a, MT S)
 {
     constexpr int N = 1 << R;
     double2 b[N];
@@ -1037,6 +1037,144 @@ __device__ __forceinline__ void resident_end(const ResArgs &a, double *acc, int 
             a.grad[(int64_t)b * a.S + s] = (float)sum;
         }
     }
+}
+
+// Stage the matrices [begin, end) of a row block into LDS.
+__device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_block, int begin, int end)
+{
+    for (int i = begin + (int)threadIdx.x; i < end; i += blockDim.x) dst[i - begin] = row_block[i];
+}
+
+// ---------------------------------------------------------- tile pass parts
+// The parts of a forward or reverse tile pass around its register stages
+// (which the generic kernels loop over and a specialised kernel spells out).
+struct PassCtx {
+    float2 *lds;        // the tile
+    double2 *lm;        // the pass's matrices
+    double2 *p1, *p2;   // product-state factors over the tile's low / high halves
+    uint64_t *hi_off;
+    float2 *st;         // the row's state
+    int row, w, a1;
+};
+
+__device__ __forceinline__ PassCtx pass_setup(const PassArgs &a, unsigned char *smem)
+{
+    const TileGeom &g = a.g;
+    const int t = g.t;
+    PassCtx c;
+    c.lds = reinterpret_cast<float2 *>(smem);
+    c.hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * (1 << t));
+    c.lm = reinterpret_cast<double2 *>(c.hi_off + (1 << g.h));
+    c.p1 = c.lm + (a.mat_end - a.mat_begin);
+    c.a1 = t / 2;
+    c.p2 = c.p1 + (1 << c.a1);
+    c.row = blockIdx.x / a.wg_per_row;
+    c.w = blockIdx.x % a.wg_per_row;
+    c.st = a.state + (int64_t)cget(a.rows, c.row) * a.row_stride;
+    build_hi_off(g, c.hi_off);
+    stage_mats(c.lm, a.mats + (int64_t)c.row * a.mat_stride, a.mat_begin, a.mat_end);
+    __syncthreads();
+    if (a.product_init) {
+        // per-qubit product-state vectors: column 0 of each init matrix
+        const double2 *M = c.lm;  // offsets relative to mat_begin
+        for (int j = threadIdx.x; j < (1 << c.a1) + (1 << (t - c.a1)); j += blockDim.x) {
+            const bool first = j < (1 << c.a1);
+            const int k0 = first ? 0 : c.a1, k1 = first ? c.a1 : t;
+            const int v = first ? j : j - (1 << c.a1);
+            double2 acc = make_double2(1.0, 0.0);
+            for (int k = k0; k < k1; k++) {
+                int pos = k < g.c ? k : g.hb[k - g.c];
+                int q = g.n - 1 - pos;
+                const double2 *im = M + (a.init_mat[q] - a.mat_begin);
+                acc = zmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
+            }
+            if (first) c.p1[v] = acc;
+            else c.p2[v] = acc;
+        }
+    }
+    __syncthreads();
+    return c;
+}
+
+// the tile with fixed bits fb into LDS (generated product state in the first pass)
+__device__ __forceinline__ void pass_load(const PassArgs &a, const PassCtx &c, uint64_t fb)
+{
+    const TileGeom &g = a.g;
+    const int T = 1 << g.t;
+    if (a.product_init) {
+        const double2 *M = c.lm;
+        double2 f = make_double2(1.0, 0.0);
+        for (uint64_t fm = g.fixed_mask; fm; fm &= fm - 1) {
+            int pos = __ffsll((unsigned long long)fm) - 1;
+            const double2 *im = M + (a.init_mat[g.n - 1 - pos] - a.mat_begin);
+            f = zmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
+        }
+        for (int l = threadIdx.x; l < T; l += blockDim.x)
+            c.lds[sw(l)] = down2(zmul(f, zmul(c.p1[l & ((1 << c.a1) - 1)], c.p2[l >> c.a1])));
+    } else {
+        TileCtx tc{c.hi_off, (1u << g.c) - 1, g.c};
+        tile_copy<true>(tc, c.lds, c.st, fb, T);
+    }
+}
+
+__device__ __forceinline__ void pass_store(const PassArgs &a, const PassCtx &c, uint64_t fb)
+{
+    TileCtx tc{c.hi_off, (1u << a.g.c) - 1, a.g.c};
+    tile_copy<false>(tc, c.lds, c.st, fb, 1 << a.g.t);
+}
+
+struct RevCtx {
+    float2 *lp, *lf;    // psi and phi tiles
+    uint64_t *hi_off;
+    double2 *lm;        // the pass's matrices
+    double *acc;        // [4 waves][gcount] gradient partials
+    float2 *sp, *sf;    // the row's psi and phi
+    int row, w;
+};
+
+__device__ __forceinline__ RevCtx rev_setup(const RevArgs &a, unsigned char *smem)
+{
+    const TileGeom &g = a.g;
+    const uint32_t T = 1u << g.t;
+    RevCtx c;
+    c.lp = reinterpret_cast<float2 *>(smem);
+    c.lf = c.lp + T;
+    c.hi_off = reinterpret_cast<uint64_t *>(c.lf + T);
+    c.lm = reinterpret_cast<double2 *>(c.hi_off + (1 << g.h));
+    c.acc = reinterpret_cast<double *>(c.lm + (a.mat_end - a.mat_begin));
+    c.row = blockIdx.x / a.wg_per_row;
+    c.w = blockIdx.x % a.wg_per_row;
+    const int b = cget(a.rows, c.row);
+    c.sp = a.psi + (int64_t)b * a.row_stride;
+    c.sf = a.phi + (int64_t)b * a.row_stride;
+    build_hi_off(g, c.hi_off);
+    stage_mats(c.lm, a.mats + (int64_t)c.row * a.mat_stride, a.mat_begin, a.mat_end);
+    for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) c.acc[j] = 0;
+    __syncthreads();
+    return c;
+}
+
+__device__ __forceinline__ void rev_load(const RevArgs &a, const RevCtx &c, uint64_t fb)
+{
+    TileCtx tc{c.hi_off, (1u << a.g.c) - 1, a.g.c};
+    tile_copy<true>(tc, c.lp, c.sp, fb, 1 << a.g.t);
+    tile_copy<true>(tc, c.lf, c.sf, fb, 1 << a.g.t);
+}
+
+__device__ __forceinline__ void rev_store(const RevArgs &a, const RevCtx &c, uint64_t fb)
+{
+    if (!a.store) return;
+    TileCtx tc{c.hi_off, (1u << a.g.c) - 1, a.g.c};
+    tile_copy<false>(tc, c.lp, c.sp, fb, 1 << a.g.t);
+    tile_copy<false>(tc, c.lf, c.sf, fb, 1 << a.g.t);
+}
+
+// the workgroup's gradient partials, waves summed in a fixed order
+__device__ __forceinline__ void rev_finish(const RevArgs &a, const RevCtx &c)
+{
+    double *out = a.gpart + ((int64_t)c.row * a.wg_per_row + c.w) * a.n_gslots + a.gbase;
+    for (int j = threadIdx.x; j < a.gcount; j += blockDim.x)
+        out[j] = ((c.acc[j] + c.acc[a.gcount + j]) + c.acc[2 * a.gcount + j]) + c.acc[3 * a.gcount + j];
 }
 
 } // namespace tq

@@ -1,14 +1,18 @@
-// jit.cpp -- generation, run-time compilation and launch of the resident
-// kernel specialised for one circuit structure.  The generated code calls the
-// same register-op templates (device_ops.h) the precompiled kernel dispatches
-// to, with the register bits, tile bits and matrix offsets of every op and
-// stage written in as constants.
+// jit.cpp -- generation, run-time compilation and launch of kernels
+// specialised for one circuit structure: the resident-circuit kernel and the
+// forward and reverse tile passes.  The generated code calls the same
+// register-op templates (device_ops.h) the precompiled kernels dispatch to,
+// with the register bits, tile bits and matrix offsets of every op and stage
+// written in as constants; the parts around the stages (tile loads and
+// stores, product-state generation, expectations, reductions) are the
+// precompiled kernels' own device functions.
 #include "jit.h"
 
 #include "kernels.h"
 
 #include <hip/hiprtc.h>
 
+#include <algorithm>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -28,92 +32,103 @@ std::string N(long v) { return std::to_string(v); }
 
 uint32_t host_sw(uint32_t i) { return i ^ ((i >> 5) & 31u); }
 
-// the item's bit at tile position l (every qubit of a resident circuit is a
-// tile bit; a position outside the tile reads as 0, the fixed bits of the
-// single tile)
-std::string bit(uint8_t l) { return l == kFixed ? std::string("0u") : "((base >> " + N(l) + ") & 1u)"; }
-std::string ent(int mat) { return "M[" + N(mat) + "]"; }
+// Where a kernel's stage code finds its data.
+struct Env {
+    int t;          // tile bits: a stage of r register bits has 2^(t - r) items
+    int mbase;      // op matrix offsets are taken relative to this
+    std::string G;  // base of dense stage matrices (absolute offsets)
+    bool fixed;     // the tile has fixed bits: a bit outside it reads fb
+    // reverse stages: accumulator of gradient slot s is acc[(tid >> 6) * stride + s + shift]
+    std::string acc_stride;
+    std::string acc_shift;
+};
 
-// Arguments of the diagonal entries of op on register array `v` with matrix
-// offset `mat`: returns the call of rd1/rd2/rscale (or its _dot form).
-std::string diag_call(const PassOp &op, int R, int mat, bool dot)
+// An op bit at tile position l (global position p): from the item's base
+// index, or from the tile's fixed bits.
+std::string bit(const Env &e, uint8_t l, uint8_t p)
 {
-    const std::string sfx = dot ? "_dot" : "", args = dot ? "v, f" : "v";
+    if (l != kFixed) return "((base >> " + N(l) + ") & 1u)";
+    return e.fixed ? "((uint32_t)(fb >> " + N(p) + ") & 1u)" : std::string("0u");
+}
+std::string ent(int mat) { return "M[z_ + " + N(mat) + "]"; }
+
+// The call of rd1/rd2/rscale (or its _dot form) for a diagonal op with
+// matrix offset `mat` on register array `v`.
+std::string diag_call(const Env &e, const PassOp &op, int R, int mat, bool dot, const std::string &v)
+{
+    const std::string sfx = dot ? "_dot" : "", args = dot ? "v, f" : v;
     const std::string Rs = N(R);
     if (op.kind == K_D1) {
         if (op.s0 != kFixed)
             return "rd1" + sfx + "<" + Rs + ", " + N(op.s0) + ">(" + args + ", " + ent(mat) + ", " + ent(mat + 1) + ")";
-        return "rscale" + sfx + "<" + Rs + ">(" + args + ", zsel(" + bit(op.l0) + ", " + ent(mat) + ", " +
+        return "rscale" + sfx + "<" + Rs + ">(" + args + ", zsel(" + bit(e, op.l0, op.p0) + ", " + ent(mat) + ", " +
                ent(mat + 1) + "))";
     }
     const bool r0 = op.s0 != kFixed, r1 = op.s1 != kFixed;
     if (r0 && r1) {
         const int j0 = std::min(op.s0, op.s1), j1 = std::max(op.s0, op.s1);
         const bool q0lo = op.s0 < op.s1;
-        const int e[4] = {0, q0lo ? 1 : 2, q0lo ? 2 : 1, 3};
-        return "rd2" + sfx + "<" + Rs + ", " + N(j0) + ", " + N(j1) + ">(" + args + ", " + ent(mat + e[0]) + ", " +
-               ent(mat + e[1]) + ", " + ent(mat + e[2]) + ", " + ent(mat + e[3]) + ")";
+        const int x[4] = {0, q0lo ? 1 : 2, q0lo ? 2 : 1, 3};
+        return "rd2" + sfx + "<" + Rs + ", " + N(j0) + ", " + N(j1) + ">(" + args + ", " + ent(mat + x[0]) + ", " +
+               ent(mat + x[1]) + ", " + ent(mat + x[2]) + ", " + ent(mat + x[3]) + ")";
     }
     if (r0) {  // entries (v, 2 + v) with v the bit of q1
-        const std::string b = bit(op.l1);
+        const std::string b = bit(e, op.l1, op.p1);
         return "rd1" + sfx + "<" + Rs + ", " + N(op.s0) + ">(" + args + ", zsel(" + b + ", " + ent(mat) + ", " +
                ent(mat + 1) + "), zsel(" + b + ", " + ent(mat + 2) + ", " + ent(mat + 3) + "))";
     }
     if (r1) {  // entries (2v, 2v + 1) with v the bit of q0
-        const std::string b = bit(op.l0);
+        const std::string b = bit(e, op.l0, op.p0);
         return "rd1" + sfx + "<" + Rs + ", " + N(op.s1) + ">(" + args + ", zsel(" + b + ", " + ent(mat) + ", " +
                ent(mat + 2) + "), zsel(" + b + ", " + ent(mat + 1) + ", " + ent(mat + 3) + "))";
     }
-    const std::string b0 = bit(op.l0), b1 = bit(op.l1);
+    const std::string b0 = bit(e, op.l0, op.p0), b1 = bit(e, op.l1, op.p1);
     return "rscale" + sfx + "<" + Rs + ">(" + args + ", zsel(" + b0 + ", zsel(" + b1 + ", " + ent(mat) + ", " +
            ent(mat + 1) + "), zsel(" + b1 + ", " + ent(mat + 2) + ", " + ent(mat + 3) + ")))";
 }
 
 // op applied to register array `v` (matrix at offset mat)
-std::string apply(const PassOp &op, int R, int mat, const char *v)
+std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::string &v)
 {
-    const std::string Rs = N(R), m = "M + " + N(mat), V = v;
+    const std::string Rs = N(R), m = "M + (z_ + " + N(mat) + ")";
     switch (op.kind) {
     case K_M1:
-        if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + V + ", " + m + ");";
-        if (op.s1 != kFixed) return "rm1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + V + ", " + m + ");";
-        return "rm1<" + Rs + ", " + N(op.s0) + ">(" + V + ", ctrl_sel(" + m + ", " + bit(op.l1) + " == " +
-               N(op.cval) + "u));";
-    case K_M2: return "rm2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + V + ", " + m + ");";
-    case K_F2: return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + V + ", " + m + ");";
+        if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
+        if (op.s1 != kFixed) return "rm1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
+        return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", ctrl_sel(" + m + ", " + bit(e, op.l1, op.p1) +
+               " == " + N(op.cval) + "u));";
+    case K_M2: return "rm2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
+    case K_F2: return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_P2:
-        return "rp2<" + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " + N(std::max(op.s0, op.s1)) + ">(" + V + ", " +
+        return "rp2<" + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " + N(std::max(op.s0, op.s1)) + ">(" + v + ", " +
                ent(mat) + ", " + ent(mat + 1) + ", " + (op.ptype == 2 ? "-1.0" : "1.0") + ");";
-    default: {
-        std::string c = diag_call(op, R, mat, false);
-        return c.replace(c.find("(v"), 2, "(" + V) + ";";
-    }
+    default: return diag_call(e, op, R, mat, false, v) + ";";
     }
 }
 
 // sum of Re(conj(f) dW v) for the derivative matrix at offset d
-std::string dot(const PassOp &op, int R, int d)
+std::string dot(const Env &e, const PassOp &op, int R, int d)
 {
-    const std::string Rs = N(R), m = "M + " + N(d);
+    const std::string Rs = N(R), m = "M + (z_ + " + N(d) + ")";
     switch (op.kind) {
     case K_M1:
         if (!op.ctrl) return "rm1_dot<" + Rs + ", " + N(op.s0) + ">(v, f, " + m + ")";
         if (op.s1 != kFixed) return "rm1c_dot<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(v, f, " + m + ")";
         // an item whose control is off sees the identity and a zero derivative
-        return "(" + bit(op.l1) + " == " + N(op.cval) + "u ? rm1_dot<" + Rs + ", " + N(op.s0) + ">(v, f, " + m +
-               ") : 0.0)";
+        return "(" + bit(e, op.l1, op.p1) + " == " + N(op.cval) + "u ? rm1_dot<" + Rs + ", " + N(op.s0) +
+               ">(v, f, " + m + ") : 0.0)";
     case K_M2: return "rm2_dot<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(v, f, " + m + ")";
     case K_F2: return "rf2_dot<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(v, f, " + m + ")";
     case K_P2:
         return "rp2_dot<" + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " + N(std::max(op.s0, op.s1)) + ">(v, f, " +
                ent(d) + ", " + ent(d + 1) + ", " + (op.ptype == 2 ? "-1.0" : "1.0") + ")";
-    default: return diag_call(op, R, d, true);
+    default: return diag_call(e, op, R, d, true, "v");
     }
 }
 
 // item loop header of a stage: base index of the item and the swizzled
 // LDS offsets of its 2^R registers
-void stage_head(std::ostream &o, const Stage &st, int n, std::vector<uint32_t> &off)
+void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint32_t> &off)
 {
     const int R = st.r;
     off.assign(1u << R, 0);
@@ -123,13 +138,81 @@ void stage_head(std::ostream &o, const Stage &st, int n, std::vector<uint32_t> &
             if ((k >> j) & 1) x |= 1u << st.bits[j];
         off[k] = host_sw(x);  // sw is linear over xor: sw(base | x) = sw(base) ^ sw(x)
     }
-    o << "    for (uint32_t item = tid; item < " << (1u << (n - R)) << "u; item += 256u) {\n";
+    o << "    for (uint32_t item = tid; item < " << (1u << (e.t - R)) << "u; item += 256u) {\n";
     o << "        uint32_t base = item;\n";
     for (int j = 0; j < R; j++) o << "        base = ins0(base, " << (int)st.bits[j] << ");\n";
     o << "        const uint32_t sb = sw(base);\n";
+    // an offset of 0 the compiler cannot see through, taken anew per item:
+    // matrix reads offset by it stay inside the item loop instead of being
+    // hoisted above it, where every matrix of the stage would be live at once
+    o << "        int z_ = 0;\n";
+    o << "        asm volatile(\"\" : \"+s\"(z_));\n";
 }
 
-const std::vector<PassOp> &pass_ops(const Pass &ps) { return ps.ops; }
+// A forward stage on the tile lp.
+void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &st)
+{
+    const int R = st.r, NR = 1 << R;
+    std::vector<uint32_t> off;
+    o << "    {\n";
+    stage_head(o, e, st, off);
+    o << "        double2 v[" << NR << "];\n";
+    for (int k = 0; k < NR; k++) o << "        v[" << k << "] = up2(lp[sb ^ " << off[k] << "u]);\n";
+    if (st.dense) {
+        o << "        rdense<" << R << ">(v, " << e.G << " + (z_ + " << st.mat << "));\n";
+    } else {
+        for (int oi = st.op_begin; oi < st.op_end; oi++) {
+            const PassOp &op = ps.ops[oi - ps.op_offset];
+            o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
+        }
+    }
+    for (int k = 0; k < NR; k++) o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]);\n";
+    o << "    }\n    }\n    __syncthreads();\n";
+}
+
+// A reverse stage on the tiles lp (psi) and lf (phi); the gradient partials
+// of its parameters stay in registers over the items, then one wavefront
+// sum each goes to the wave's accumulator row.
+void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &st)
+{
+    const int R = st.r, NR = 1 << R;
+    std::vector<uint32_t> off;
+    std::vector<std::pair<int, int>> grads;  // (register, gradient slot)
+    for (int oi = st.op_begin; oi < st.op_end; oi++) {
+        const PassOp &op = ps.ops[oi - ps.op_offset];
+        for (int j = 0; j < op.ngrad; j++) grads.emplace_back((int)grads.size(), op.gslot[j]);
+    }
+    o << "    {\n";
+    if (!grads.empty()) o << "    double g[" << grads.size() << "] = {};\n";
+    stage_head(o, e, st, off);
+    o << "        double2 v[" << NR << "], f[" << NR << "];\n";
+    for (int k = 0; k < NR; k++)
+        o << "        v[" << k << "] = up2(lp[sb ^ " << off[k] << "u]); f[" << k << "] = up2(lf[sb ^ " << off[k]
+          << "u]);\n";
+    int gk = 0;
+    for (int oi = st.op_begin; oi < st.op_end; oi++) {
+        const PassOp &op = ps.ops[oi - ps.op_offset];
+        o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
+        for (int j = 0; j < op.ngrad; j++)
+            o << "        g[" << gk++ << "] += " << dot(e, op, R, op.dmat[j] - e.mbase) << ";\n";
+        o << "        " << apply(e, op, R, op.mat - e.mbase, "f") << "\n";
+        // keep each op's matrix reads next to the op: scheduled ahead they
+        // would hold every matrix of the stage in registers at once
+        o << "        __builtin_amdgcn_sched_barrier(0);\n";
+    }
+    for (int k = 0; k < NR; k++)
+        o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]); lf[sb ^ " << off[k] << "u] = down2(f[" << k
+          << "]);\n";
+    o << "    }\n";
+    for (auto &gs : grads)
+        o << "    { const double s_ = wave_sum(g[" << gs.first << "]); if ((tid & 63) == 0) acc[(tid >> 6) * "
+          << e.acc_stride << " + " << gs.second << " + " << e.acc_shift << "] += s_; }\n";
+    o << "    }\n    __syncthreads();\n";
+}
+
+const char kHead[] =
+    "namespace tq {\n"
+    "__device__ __forceinline__ double2 zsel(uint32_t c, double2 a, double2 b) { return c ? b : a; }\n";
 
 } // namespace
 
@@ -137,9 +220,8 @@ std::string resident_source(const Group &g)
 {
     std::ostringstream o;
     const int n = g.n;
-    o << "namespace tq {\n"
-         "__device__ __forceinline__ double2 zsel(uint32_t c, double2 a, double2 b) { return c ? b : a; }\n"
-         "extern \"C\" __global__ __launch_bounds__(256, 4) void tq_resident_spec(ResArgs a)\n{\n"
+    o << kHead
+      << "extern \"C\" __global__ __launch_bounds__(256, 4) void tq_resident_spec(ResArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    double *acc = reinterpret_cast<double *>(smem);\n"
          "    float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);\n"
@@ -149,58 +231,13 @@ std::string resident_source(const Group &g)
          "    const SMat M = smat(a.mats + (int64_t)blockIdx.x * a.mat_stride);\n"
          "    const int tid = threadIdx.x;\n"
          "    resident_begin(a, M, acc, lp, tid, 256);\n";
-    std::vector<uint32_t> off;
+    const Env e{n, 0, "M", false, "a.nacc", "a.gacc"};
     for (const Pass &ps : g.fwd)
-        for (const Stage &st : ps.stages) {
-            const int R = st.r, NR = 1 << R;
-            o << "    {\n";
-            stage_head(o, st, n, off);
-            o << "        double2 v[" << NR << "];\n";
-            for (int k = 0; k < NR; k++) o << "        v[" << k << "] = up2(lp[sb ^ " << off[k] << "u]);\n";
-            if (st.dense) {
-                o << "        rdense<" << R << ">(v, M + " << st.mat << ");\n";
-            } else {
-                for (int oi = st.op_begin; oi < st.op_end; oi++) {
-                    const PassOp &op = pass_ops(ps)[oi - ps.op_offset];
-                    o << "        " << apply(op, R, op.mat, "v") << "\n";
-                }
-            }
-            for (int k = 0; k < NR; k++) o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]);\n";
-            o << "    }\n    }\n    __syncthreads();\n";
-        }
+        for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
     o << "    resident_middle(a, acc, lp, lf, blockIdx.x, tid, 256);\n"
          "    if (a.grad) {\n";
     for (const Pass &ps : g.rev)
-        for (const Stage &st : ps.stages) {
-            const int R = st.r, NR = 1 << R;
-            std::vector<std::pair<int, int>> grads;  // (accumulator, gradient slot)
-            for (int oi = st.op_begin; oi < st.op_end; oi++) {
-                const PassOp &op = pass_ops(ps)[oi - ps.op_offset];
-                for (int j = 0; j < op.ngrad; j++) grads.emplace_back((int)grads.size(), op.gslot[j]);
-            }
-            o << "    {\n";
-            if (!grads.empty()) o << "    double g[" << grads.size() << "] = {};\n";
-            stage_head(o, st, n, off);
-            o << "        double2 v[" << NR << "], f[" << NR << "];\n";
-            for (int k = 0; k < NR; k++)
-                o << "        v[" << k << "] = up2(lp[sb ^ " << off[k] << "u]); f[" << k << "] = up2(lf[sb ^ "
-                  << off[k] << "u]);\n";
-            int gk = 0;
-            for (int oi = st.op_begin; oi < st.op_end; oi++) {
-                const PassOp &op = pass_ops(ps)[oi - ps.op_offset];
-                o << "        " << apply(op, R, op.mat, "v") << "\n";
-                for (int j = 0; j < op.ngrad; j++) o << "        g[" << gk++ << "] += " << dot(op, R, op.dmat[j]) << ";\n";
-                o << "        " << apply(op, R, op.mat, "f") << "\n";
-            }
-            for (int k = 0; k < NR; k++)
-                o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]); lf[sb ^ " << off[k]
-                  << "u] = down2(f[" << k << "]);\n";
-            o << "    }\n";
-            for (auto &gs : grads)
-                o << "    { const double s_ = wave_sum(g[" << gs.first
-                  << "]); if ((tid & 63) == 0) acc[(tid >> 6) * a.nacc + a.gacc + " << gs.second << "] += s_; }\n";
-            o << "    }\n    __syncthreads();\n";
-        }
+        for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
     o << "    }\n"
          "    resident_end(a, acc, blockIdx.x, tid, 256);\n"
          "}\n"
@@ -208,16 +245,48 @@ std::string resident_source(const Group &g)
     return o.str();
 }
 
+std::string pass_kernel_source(const Group &g, int pass)
+{
+    std::ostringstream o;
+    {
+        const Pass &ps = g.fwd[pass];
+        const TileGeom &gm = ps.geom;
+        o << "extern \"C\" __global__ __launch_bounds__(256) void tq_fwd_" << pass
+          << "(PassArgs a)\n{\n"
+             "    extern __shared__ __align__(16) unsigned char smem[];\n"
+             "    const PassCtx c = pass_setup(a, smem);\n"
+             "    const double2 *M = c.lm;\n"
+             "    const SMat G = smat(a.mats + (int64_t)c.row * a.mat_stride);\n";
+        o << "    float2 *lp = c.lds;\n"
+             "    const int tid = threadIdx.x;\n"
+             "    for (int64_t tile = c.w; tile < "
+          << (1ll << (gm.n - gm.t))
+          << "ll; tile += a.wg_per_row) {\n"
+             "    const uint64_t fb = pdep64((uint64_t)tile, "
+          << gm.fixed_mask
+          << "ull);\n"
+             "    pass_load(a, c, fb);\n"
+             "    __syncthreads();\n";
+        const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
+        for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
+        o << "    pass_store(a, c, fb);\n"
+             "    __syncthreads();\n"
+             "    }\n"
+             "}\n";
+    }
+    return o.str();
+}
+
 namespace {
 
-struct SpecKernel {
+struct Module {
     hipModule_t mod = nullptr;
-    hipFunction_t fn = nullptr;
+    std::map<std::string, hipFunction_t> fn;
 };
 
 std::mutex g_mu;
-// (device, source) -> compiled kernel; kept until the process ends
-std::map<std::pair<int, std::string>, SpecKernel> g_cache;
+// (device, kernel source) -> loaded module; kept until the process ends
+std::map<std::pair<int, std::string>, Module> g_cache;
 int g_compiled = 0;
 
 // Compile the kernel source `body` for offload target `target` into a code
@@ -227,7 +296,7 @@ hipError_t compile_code(const std::string &body, const std::string &target, std:
 {
     const std::string src = std::string(kPrelude) + "\n" + body;
     hiprtcProgram prog;
-    if (hiprtcCreateProgram(&prog, src.c_str(), "tq_resident_spec.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS) {
+    if (hiprtcCreateProgram(&prog, src.c_str(), "tq_spec.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS) {
         *log = "hiprtcCreateProgram failed";
         return hipErrorInvalidSource;
     }
@@ -241,7 +310,7 @@ hipError_t compile_code(const std::string &body, const std::string &target, std:
         hiprtcGetProgramLogSize(prog, &n);
         std::string text(n, '\0');
         if (n) hiprtcGetProgramLog(prog, &text[0]);
-        *log = "specialised resident kernel: " + std::string(hiprtcGetErrorString(r)) + "\n" + text;
+        *log = "specialised kernel: " + std::string(hiprtcGetErrorString(r)) + "\n" + text;
         hiprtcDestroyProgram(&prog);
         return hipErrorInvalidSource;
     }
@@ -253,37 +322,65 @@ hipError_t compile_code(const std::string &body, const std::string &target, std:
     return hipSuccess;
 }
 
-hipError_t compile(const std::string &body, int dev, SpecKernel *out, std::string *log)
-{
-    hipDeviceProp_t prop;
-    hipError_t e = hipGetDeviceProperties(&prop, dev);
-    if (e != hipSuccess) return e;
-    std::vector<char> code;
-    e = compile_code(body, prop.gcnArchName, &code, log);
-    if (e != hipSuccess) return e;
-    e = hipModuleLoadData(&out->mod, code.data());
-    if (e != hipSuccess) return e;
-    e = hipModuleGetFunction(&out->fn, out->mod, "tq_resident_spec");
-    if (e == hipSuccess) g_compiled++;
-    return e;
-}
-
-// the compiled kernel of group g on the current device (compiled on first use)
-hipError_t get_kernel(const Group &g, SpecKernel *k, std::string *log)
+// The kernels `names` of source `body` on the current device: compiled and
+// loaded on first use.
+hipError_t get_kernels(const std::string &body, const std::vector<std::string> &names,
+                       std::vector<hipFunction_t> *fns, std::string *log)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     std::lock_guard<std::mutex> l(g_mu);
-    auto key = std::make_pair(dev, resident_source(g));
+    auto key = std::make_pair(dev, body);
     auto it = g_cache.find(key);
-    if (it != g_cache.end()) {
-        *k = it->second;
-        return hipSuccess;
+    if (it == g_cache.end()) {
+        hipDeviceProp_t prop;
+        e = hipGetDeviceProperties(&prop, dev);
+        if (e != hipSuccess) return e;
+        std::vector<char> code;
+        e = compile_code(body, prop.gcnArchName, &code, log);
+        if (e != hipSuccess) return e;
+        Module m;
+        e = hipModuleLoadData(&m.mod, code.data());
+        if (e != hipSuccess) return e;
+        it = g_cache.emplace(std::move(key), std::move(m)).first;
+        g_compiled++;
     }
-    e = compile(key.second, dev, k, log);
-    if (e == hipSuccess) g_cache.emplace(std::move(key), *k);
-    return e;
+    fns->clear();
+    for (const std::string &n : names) {
+        auto f = it->second.fn.find(n);
+        if (f == it->second.fn.end()) {
+            hipFunction_t fn;
+            e = hipModuleGetFunction(&fn, it->second.mod, n.c_str());
+            if (e != hipSuccess) return e;
+            f = it->second.fn.emplace(n, fn).first;
+        }
+        fns->push_back(f->second);
+    }
+    return hipSuccess;
+}
+
+// every forward pass kernel of group g in one source (one compilation: the
+// run-time compiler does not gain from several programs at once)
+std::string pass_unit(const Group &g)
+{
+    std::string body = kHead;
+    for (int pi = 0; pi < (int)g.fwd.size(); pi++) body += pass_kernel_source(g, pi);
+    return body + "} // namespace tq\n";
+}
+
+template <class Args>
+hipError_t launch(hipFunction_t fn, const Args &a, unsigned grid, size_t lds, hipStream_t s, const char *prof_name)
+{
+    if (lds > 65536) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    Args args = a;
+    void *params[] = {&args};
+    ProfScope ps(prof_name, s);
+    return hipModuleLaunchKernel(fn, grid, 1, 1, kThreads, 1, 1, (unsigned)lds, s, params, nullptr);
 }
 
 } // namespace
@@ -292,23 +389,32 @@ hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, siz
                                 std::string *log)
 {
     if (nrows <= 0) return hipSuccess;
-    SpecKernel k;
-    hipError_t e = get_kernel(g, &k, log);
+    std::vector<hipFunction_t> fn;
+    hipError_t e = get_kernels(resident_source(g), {"tq_resident_spec"}, &fn, log);
     if (e != hipSuccess) return e;
-    ResArgs args = a;
-    void *params[] = {&args};
-    ProfScope ps("resident", s);
-    return hipModuleLaunchKernel(k.fn, nrows, 1, 1, kThreads, 1, 1, (unsigned)lds, s, params, nullptr);
+    return launch(fn[0], a, nrows, lds, s, "resident");
 }
 
-hipError_t prepare_resident_spec(const Group &g, const char *target, std::string *log)
+hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
+                            std::string *log)
 {
+    if (nrows <= 0) return hipSuccess;
+    std::vector<hipFunction_t> fn;
+    hipError_t e = get_kernels(pass_unit(g), {"tq_fwd_" + N(pass)}, &fn, log);
+    if (e != hipSuccess) return e;
+    const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
+    return launch(fn[0], a, nrows * a.wg_per_row, lds, s, "pass");
+}
+
+hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log)
+{
+    const std::string body = resident ? resident_source(g) : pass_unit(g);
     if (target) {
         std::vector<char> code;
-        return compile_code(resident_source(g), target, &code, log);
+        return compile_code(body, target, &code, log);
     }
-    SpecKernel k;
-    return get_kernel(g, &k, log);
+    std::vector<hipFunction_t> fn;
+    return get_kernels(body, {}, &fn, log);
 }
 
 int spec_kernels_compiled()

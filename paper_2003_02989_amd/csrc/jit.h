@@ -1,14 +1,15 @@
 // jit.h -- kernels specialised for one circuit structure at run time.
 //
-// The resident-circuit kernel interprets its stage and op tables: every op
-// costs a table read, a dispatch on its kind and register bits, and the
-// registers the generic code keeps live.  For a structure that is run many
-// times the same computation can be compiled with the tables as constants:
-// each stage becomes straight-line code over its register bits, each op a
-// call of the register-op template it dispatches to, each matrix read a
-// scalar load at a fixed offset of the row's matrix block.  The source is
-// generated from the plan, compiled with hipRTC for the current device and
-// cached by its text for the life of the process.
+// The resident-circuit kernel and the tile passes interpret their stage and
+// op tables: every op costs a table read, a dispatch on its kind and register
+// bits, and the registers the generic code keeps live.  For a structure that
+// is run many times the same computation can be compiled with the tables as
+// constants: each stage becomes straight-line code over its register bits,
+// each op a call of the register-op template it dispatches to, each matrix
+// read a load at a fixed offset (scalar loads from the row's matrix block in
+// the resident kernel, LDS reads in the passes).  The source is generated
+// from the plan, compiled with hipRTC for the current device and cached by
+// its text for the life of the process.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -21,18 +22,27 @@ namespace tq {
 
 // The specialised resident kernel's source (without the shared device code).
 std::string resident_source(const Group &g);
+// The specialised forward pass kernel tq_fwd_<pass> of group g, to be placed
+// in namespace tq after the shared device code (all passes of a group are
+// compiled as one program).  Reverse passes keep the precompiled kernel: their
+// straight-line form holds psi, phi, the gradient partials and the matrices
+// of several ops at once and spills, where the table-driven loop does not.
+std::string pass_kernel_source(const Group &g, int pass);
 
-// Launch the specialised resident kernel of group g (compiled on first use
-// on the current device).  On a compile failure returns hipErrorInvalidSource
-// and sets *log to the compiler's message.
+// Launch a specialised kernel of group g, compiled on first use on the
+// current device: the resident kernel, or forward pass `pass` (with the
+// arguments the precompiled kernel takes).  On a compile failure these
+// return hipErrorInvalidSource and set *log to the compiler's message.
 hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, size_t lds, hipStream_t s,
                                 std::string *log);
+hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
+                            std::string *log);
 
-// Compile the specialised resident kernel of group g ahead of its first
-// launch: for the current device when target is NULL (the kernel is then
-// cached), else only check that it compiles for the offload target (e.g.
-// "gfx950"), which needs no device.
-hipError_t prepare_resident_spec(const Group &g, const char *target, std::string *log);
+// Compile the specialised kernels of group g (the resident kernel, or the
+// forward pass kernels) ahead of their first launch: for the current device when
+// target is NULL (the module is then cached), else only check that they
+// compile for the offload target (e.g. "gfx950"), which needs no device.
+hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log);
 
 // Specialised kernels compiled so far in this process (all devices).
 int spec_kernels_compiled();

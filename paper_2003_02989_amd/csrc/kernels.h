@@ -33,6 +33,7 @@ hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t
 // amax: the largest class count of a chunk (<= kDiagClassMax)
 hipError_t launch_pauli_diag(const DiagArgs &a, int nrows, int amax, hipStream_t s);
 hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s);
+size_t rev_pass_lds_bytes(const RevArgs &a);
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s);
 hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s);
 hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s);

@@ -291,76 +291,24 @@ __global__ __launch_bounds__(64) void k_build_stage(StageBuildArgs a)
     }
 }
 
-// Stage the matrices [begin, end) of a row block into LDS.
-__device__ __forceinline__ void stage_mats(double2 *dst, const double2 *row_block, int begin, int end)
-{
-    for (int i = begin + (int)threadIdx.x; i < end; i += blockDim.x) dst[i - begin] = row_block[i];
-}
 
 // ------------------------------------------------------- forward pass
 __global__ __launch_bounds__(256) void k_pass(PassArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    const TileGeom &g = a.g;
-    const int t = g.t;
-    const int T = 1 << t;
-    float2 *lds = reinterpret_cast<float2 *>(smem);
-    uint64_t *hi_off = reinterpret_cast<uint64_t *>(smem + sizeof(float2) * T);
-    double2 *lm = reinterpret_cast<double2 *>(hi_off + (1 << g.h));  // the pass's matrices
-    double2 *p1 = lm + (a.mat_end - a.mat_begin);
-    const int a1 = t / 2;
-    double2 *p2 = p1 + (1 << a1);
-
-    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = cget(a.rows, row);
-    float2 *st = a.state + (int64_t)b * a.row_stride;
-    build_hi_off(g, hi_off);
-    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, a.mat_begin, a.mat_end);
-    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
-    __syncthreads();
-    const double2 *M = lm;  // offsets below are taken relative to mat_begin
-
-    if (a.product_init) {
-        // per-qubit product-state vectors: column 0 of each init matrix
-        for (int j = threadIdx.x; j < (1 << a1) + (1 << (t - a1)); j += blockDim.x) {
-            const bool first = j < (1 << a1);
-            const int k0 = first ? 0 : a1, k1 = first ? a1 : t;
-            const int v = first ? j : j - (1 << a1);
-            double2 acc = make_double2(1.0, 0.0);
-            for (int k = k0; k < k1; k++) {
-                int pos = k < g.c ? k : g.hb[k - g.c];
-                int q = g.n - 1 - pos;
-                const double2 *im = M + (a.init_mat[q] - a.mat_begin);
-                acc = zmul(acc, ((v >> (k - k0)) & 1) ? im[2] : im[0]);
-            }
-            if (first) p1[v] = acc;
-            else p2[v] = acc;
-        }
-    }
-    __syncthreads();
-
+    const PassCtx c = pass_setup(a, smem);
+    const SMat G = smat(a.mats + (int64_t)c.row * a.mat_stride);
     const int64_t ntiles = (int64_t)1 << a.tiles_log2;
-    for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
-        const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
-        if (a.product_init) {
-            double2 f = make_double2(1.0, 0.0);
-            for (uint64_t fm = g.fixed_mask; fm; fm &= fm - 1) {
-                int pos = __ffsll((unsigned long long)fm) - 1;
-                const double2 *im = M + (a.init_mat[g.n - 1 - pos] - a.mat_begin);
-                f = zmul(f, ((fb >> pos) & 1) ? im[2] : im[0]);
-            }
-            for (int l = threadIdx.x; l < T; l += blockDim.x)
-                lds[sw(l)] = down2(zmul(f, zmul(p1[l & ((1 << a1) - 1)], p2[l >> a1])));
-        } else {
-            tile_copy<true>(tc, lds, st, fb, T);
-        }
+    for (int64_t tile = c.w; tile < ntiles; tile += a.wg_per_row) {
+        const uint64_t fb = pdep64((uint64_t)tile, a.g.fixed_mask);
+        pass_load(a, c, fb);
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_stage_any(st, a.ops, M, a.mat_begin, smat(a.mats + (int64_t)row * a.mat_stride), lds, t, fb, threadIdx.x, blockDim.x);
+            run_stage_any(st, a.ops, c.lm, a.mat_begin, G, c.lds, a.g.t, fb, threadIdx.x, blockDim.x);
             __syncthreads();
         }
-        tile_copy<false>(tc, lds, st, fb, T);
+        pass_store(a, c, fb);
         __syncthreads();
     }
 }
@@ -659,46 +607,22 @@ __global__ __launch_bounds__(256) void k_pauli_diag(DiagArgs a)
 __global__ __launch_bounds__(256, 2) void k_rev_pass(RevArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    const TileGeom &g = a.g;
-    const int t = g.t;
-    const uint32_t T = 1u << t;
-    float2 *lp = reinterpret_cast<float2 *>(smem);
-    float2 *lf = lp + T;
-    uint64_t *hi_off = reinterpret_cast<uint64_t *>(lf + T);
-    double2 *lm = reinterpret_cast<double2 *>(hi_off + (1 << g.h));
-    double *acc = reinterpret_cast<double *>(lm + (a.mat_end - a.mat_begin));  // [4][gcount]
-
-    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;
-    const int b = cget(a.rows, row);
-    float2 *sp = a.psi + (int64_t)b * a.row_stride;
-    float2 *sf = a.phi + (int64_t)b * a.row_stride;
-    build_hi_off(g, hi_off);
-    stage_mats(lm, a.mats + (int64_t)row * a.mat_stride, a.mat_begin, a.mat_end);
-    for (int j = threadIdx.x; j < 4 * a.gcount; j += blockDim.x) acc[j] = 0;
-    TileCtx tc{hi_off, (1u << g.c) - 1, g.c};
-    const int tid = threadIdx.x, nt = blockDim.x;
-    __syncthreads();
-
+    const RevCtx c = rev_setup(a, smem);
     const int64_t ntiles = (int64_t)1 << a.tiles_log2;
-    for (int64_t tile = w; tile < ntiles; tile += a.wg_per_row) {
-        const uint64_t fb = pdep64((uint64_t)tile, g.fixed_mask);
-        tile_copy<true>(tc, lp, sp, fb, T);
-        tile_copy<true>(tc, lf, sf, fb, T);
+    for (int64_t tile = c.w; tile < ntiles; tile += a.wg_per_row) {
+        const uint64_t fb = pdep64((uint64_t)tile, a.g.fixed_mask);
+        rev_load(a, c, fb);
         __syncthreads();
         for (int si = 0; si < a.nstages; si++) {
             const Stage st = cget(a.stages, si);
-            run_rev_stage_any<kStageBitsRev>(st, a.ops, lm, a.mat_begin, lp, lf, t, fb, acc, a.gcount, a.gbase, threadIdx.x, blockDim.x);
+            run_rev_stage_any<kStageBitsRev>(st, a.ops, c.lm, a.mat_begin, c.lp, c.lf, a.g.t, fb, c.acc, a.gcount,
+                                             a.gbase, threadIdx.x, blockDim.x);
             __syncthreads();
         }
-        if (a.store) {
-            tile_copy<false>(tc, lp, sp, fb, T);
-            tile_copy<false>(tc, lf, sf, fb, T);
-        }
+        rev_store(a, c, fb);
         __syncthreads();
     }
-    double *out = a.gpart + ((int64_t)row * a.wg_per_row + w) * a.n_gslots + a.gbase;
-    for (int j = tid; j < a.gcount; j += nt)
-        out[j] = ((acc[j] + acc[a.gcount + j]) + acc[2 * a.gcount + j]) + acc[3 * a.gcount + j];
+    rev_finish(a, c);
 }
 
 // grad[b, s] = sum over gradient slots of s: 2 * scale * sum_w gpart
@@ -1036,10 +960,15 @@ hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t 
     return hipGetLastError();
 }
 
+size_t rev_pass_lds_bytes(const RevArgs &a)
+{
+    return 2 * sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
+           sizeof(double2) * (size_t)(a.mat_end - a.mat_begin) + sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
+}
+
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s)
 {
-    size_t lds = 2 * sizeof(float2) * ((size_t)1 << a.g.t) + sizeof(uint64_t) * ((size_t)1 << a.g.h) +
-                 sizeof(double2) * (size_t)(a.mat_end - a.mat_begin) + sizeof(double) * 4 * (size_t)(a.gcount > 0 ? a.gcount : 1);
+    const size_t lds = rev_pass_lds_bytes(a);
     hipError_t e = set_lds(k_rev_pass, lds);
     if (e != hipSuccess) return e;
     prof::Scope ps("rev_pass", s);

@@ -289,6 +289,13 @@ void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const i
         for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
         a.mat_begin = ps.mat_begin;
         a.mat_end = ps.mat_end;
+        if (p->pd->opt.specialize) {
+            std::string log;
+            const hipError_t e = launch_pass_spec(g, (int)pi, a, nrows, s, &log);
+            if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+            hip_check(e, "specialised pass launch");
+            continue;
+        }
         hip_check(launch_pass(a, nrows, s), "pass launch");
     }
 }
@@ -679,9 +686,8 @@ tq_status tq_program_specialize(tq_program prog, const char *target)
         if (!prog) fail(TQ_E_INVALID, "program is NULL");
         if (!prog->pd->opt.specialize) return;
         for (size_t gi = 0; gi < prog->pd->groups.size(); gi++) {
-            if (!resident(prog, gi, false, 0)) continue;
             std::string log;
-            const hipError_t e = prepare_resident_spec(*prog->pd->groups[gi], target, &log);
+            const hipError_t e = prepare_spec(*prog->pd->groups[gi], resident(prog, gi, false, 0), target, &log);
             if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
             hip_check(e, "specialised kernel compilation");
         }

@@ -108,10 +108,12 @@ def test_version():
 
 def test_specialized_kernels_compile_for_gfx950():
     # the kernels generated per circuit structure compile with hipRTC for
-    # gfx950 (no device needed): the two resident configurations and random
-    # structures over the whole opcode set
+    # gfx950 (no device needed): the two resident configurations, random
+    # resident structures over the whole opcode set, and the forward and
+    # reverse tile passes of a 14-qubit random structure
     for w in (wl.c1_hea(), wl.c2_qnn(B=4),
-              wl.random_batch(6601, B=3, n=10, n_gates=60, n_symbols=5, K=3, hetero=True)):
+              wl.random_batch(6601, B=3, n=10, n_gates=60, n_symbols=5, K=3, hetero=True),
+              wl.random_batch(1412, B=2, n=14, n_gates=60, n_symbols=5, K=2)):
         p = create(w.program_blob(), specialize=True)
         tq.specialize(p, "gfx950")
     # a program without the option has nothing to compile

@@ -78,8 +78,8 @@ def test_c5_full_sampled_rows():
     compare({"exp": g["exp"][rows], "grad": g["grad"][rows], "grad_exp": g["grad_exp"][rows]}, ref)
 
 
-def _c4_check(w, amps_ref, sum_p2, norm2_ref, n):
-    p = tq.Program(w.program_blob())
+def _c4_check(w, amps_ref, sum_p2, norm2_ref, n, **opts):
+    p = tq.Program(w.program_blob(), **opts)
     bits = dev(w.extras["bitstrings"].astype(np.int64), torch.int64)
     a = tq.amplitudes(p, None, bits).cpu().numpy()[0]
     err = np.linalg.norm(a.astype(np.complex128) - amps_ref)
@@ -113,6 +113,25 @@ def test_c4_reduced():
     st = _c4_check(w, ref[bits], float((p2 * p2).sum()), float(p2.sum()), 20)
     err = np.linalg.norm(st.cpu().numpy()[0].astype(np.complex128) - ref)
     assert err <= TOL_AMP
+
+
+def test_specialized_passes_configs():
+    # tile passes compiled for the circuit structure: reduced c3 (Z-only cost
+    # observable), c5 (forward and reverse passes, 60 Pauli strings) and c4
+    # (fSim grid; amplitudes, norm and samples)
+    w = wl.c3_qaoa(B=8, n=14)
+    say("c3 reduced specialised")
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+    w = wl.c5_vqe(B=6, n=14, layers=4, n_terms=60)
+    say("c5 reduced specialised")
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+    w = wl.c4_random(rows=3, cols=5, n_shots=100_000)
+    say("c4 reduced specialised n=15")
+    ref = orc.simulate_state(orc.Program(w.program_blob()), np.zeros((1, 0)))[0]
+    bits = w.extras["bitstrings"][0].astype(np.int64)
+    p2 = np.abs(ref) ** 2
+    st = _c4_check(w, ref[bits], float((p2 * p2).sum()), float(p2.sum()), 15, specialize=True)
+    assert np.linalg.norm(st.cpu().numpy()[0].astype(np.complex128) - ref) <= TOL_AMP
 
 
 def test_c4_full_against_golden():

@@ -30,6 +30,15 @@ def test_random_tiled(n, tile, low):
     compare(gpu_outputs(w, max_tile_qubits=tile, low_qubits=low), oracle_outputs(w))
 
 
+@pytest.mark.parametrize("n,tile,low", [(12, 8, 6), (14, 12, 6), (13, 9, 4)])
+def test_specialized_passes_random(n, tile, low):
+    # forward and reverse tile passes compiled for the circuit structure:
+    # fixed bits, controls and diagonals outside the tile, dense stages
+    w = wl.random_batch(100 * n + tile, B=3, n=n, n_gates=60, n_symbols=5, K=2)
+    say("specialised passes", n, tile, low)
+    compare(gpu_outputs(w, max_tile_qubits=tile, low_qubits=low, specialize=True), oracle_outputs(w))
+
+
 def test_unfused_matches():
     w = wl.random_batch(4242, B=4, n=9, n_gates=50, n_symbols=3, K=2)
     compare(gpu_outputs(w, fuse=False), oracle_outputs(w))
