@@ -187,7 +187,7 @@ def main():
     local_rank = int(os.environ.get("LOCAL_RANK", "0"))
     torch.cuda.set_device(local_rank)
     if args.sweep:
-        sweep(args.steps, args.sweep_cases)
+        sweep(args.steps, args.sweep_cases, not args.no_specialize)
         return
     if args.copy_calibration:
         src = torch.ones(1 << 27, dtype=torch.complex64, device="cuda")
@@ -307,7 +307,7 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def sweep(steps, cases="all"):
+def sweep(steps, cases="all", specialize=True):
     """Effective HBM bandwidth of single-gate passes and of the expectation
     kernel for n = 24..30 with batches sized so the states span >= 1 GiB (the
     256 MB last-level cache cannot hold them).  A pass time is the difference
@@ -351,7 +351,8 @@ def sweep(steps, cases="all"):
                     for _ in range(G):
                         c.add(*gate)
                 circuits.append(c)
-            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=1)
+            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=1,
+                              specialize=specialize)
             st = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
             tq.simulate_state(prog, None, out=st)
             torch.cuda.synchronize()
@@ -399,7 +400,7 @@ def sweep(steps, cases="all"):
         c = Circuit(n)
         for i in range(n - 1):
             c.add("CZ", (i, i + 1))
-        prog = tq.Program(program_blob([c] * B, 0))
+        prog = tq.Program(program_blob([c] * B, 0), specialize=specialize)
         for oname, terms in obs_sets.items():
             obs = tq.Observables(observable_blob([[terms]] * B))
             out = torch.empty((B, 1), dtype=torch.float32, device="cuda")

@@ -30,6 +30,8 @@ hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
 constexpr int kPauliTileMax = 12;
 size_t pauli_lds_bytes(const TileGeom &g, int k_count, bool partner);
 hipError_t launch_pauli(const PauliArgs &a, int nrows, bool partner, hipStream_t s);
+// Workgroups of the diagonal kernel that fit on the device at once (0 if unknown).
+int pauli_diag_slots(int amax, int k_count);
 // amax: the largest class count of a chunk (<= kDiagClassMax)
 hipError_t launch_pauli_diag(const DiagArgs &a, int nrows, int amax, hipStream_t s);
 hipError_t launch_pauli_reduce(const PauliReduceArgs &a, int nrows, hipStream_t s);

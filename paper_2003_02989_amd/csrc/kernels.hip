@@ -10,6 +10,7 @@
 // floating-point atomics), so every output is bitwise reproducible.
 #include <hip/hip_runtime.h>
 
+#include <map>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -942,6 +943,30 @@ template <int A> hipError_t launch_pauli_diag_a(const DiagArgs &a, int nrows, hi
     prof::Scope ps("pauli", s);
     hipLaunchKernelGGL(k_pauli_diag<A>, dim3(nrows * a.wg_per_row), dim3(kThreads), lds, s, a);
     return hipGetLastError();
+}
+
+template <int A> int pauli_diag_slots_a(size_t lds)
+{
+    // per (device, dynamic LDS size): the query is not free and the answer fixed
+    static std::mutex mu;
+    static std::map<std::pair<int, size_t>, int> known;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    std::lock_guard<std::mutex> l(mu);
+    auto it = known.find({dev, lds});
+    if (it != known.end()) return it->second;
+    int per_cu = 0, cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_pauli_diag<A>, kThreads, lds) != hipSuccess) return 0;
+    return known[{dev, lds}] = per_cu * cus;
+}
+
+int pauli_diag_slots(int amax, int k_count)
+{
+    const size_t lds = sizeof(double) * (size_t)k_count;
+    if (amax <= 8) return pauli_diag_slots_a<8>(lds);
+    if (amax <= 16) return pauli_diag_slots_a<16>(lds);
+    return pauli_diag_slots_a<kDiagClassMax>(lds);
 }
 
 hipError_t launch_pauli_diag(const DiagArgs &a, int nrows, int amax, hipStream_t s)

@@ -430,9 +430,12 @@ void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, h
     a.classes = (const DClass *)og.dclasses.p;
     a.terms = (const DTerm *)og.dterms.p;
     a.blocks_log2 = g.n - kDiagBlockBits;
-    // about eight workgroups per compute unit, each sweeping many blocks
+    // one round of workgroups over the device (as many as fit at once), each
+    // sweeping many blocks: no partial last round
     const int64_t nblk = (int64_t)1 << a.blocks_log2;
-    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(nblk, 2048 / nrows));
+    int fit = pauli_diag_slots(og.damax, std::min(K, 1024));
+    if (fit <= 0) fit = 2048;
+    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(nblk, fit / nrows));
     const int64_t slots = (int64_t)nrows * a.wg_per_row;
     const int kmax = (int)std::max<int64_t>(1, std::min<int64_t>(1024, ((int64_t)32 << 20) / slots));
     for (int k0 = 0; k0 < K; k0 += kmax) {
