@@ -412,9 +412,10 @@ def sweep(steps, cases="all", specialize=True):
             torch.cuda.synchronize()
             nl, ms = tq.profile_read()
             tq.profile_start(None)
-            ms /= max(nl, 1)
+            ms /= steps  # every launch of the call (one per pass of the plan)
             gbs = 8.0 * (1 << n) * B / (ms * 1e-3) / 1e9
             print(json.dumps({"sweep": "expectation", "n": n, "batch": B, "case": oname, "ms": ms,
+                              "launches_per_call": nl // steps,
                               "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
         del prog
 

@@ -13,6 +13,7 @@
 #include <hip/hiprtc.h>
 
 #include <algorithm>
+#include <cstdio>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -29,6 +30,13 @@ const char kPrelude[] =
     ;
 
 std::string N(long v) { return std::to_string(v); }
+
+// LDS of a specialised Pauli pass: the tile, its high-bit offsets and the
+// per-wave sums of at most `nk` observables (every pass has at most 16)
+size_t pauli_spec_lds_bytes(const TileGeom &g, int)
+{
+    return sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) + sizeof(double) * 4 * 16;
+}
 
 uint32_t host_sw(uint32_t i) { return i ^ ((i >> 5) & 31u); }
 
@@ -279,6 +287,153 @@ std::string pass_kernel_source(const Group &g, int pass)
 
 namespace {
 
+// A mask in global index bits as tile-local bits of geometry gm.
+uint32_t local_mask(const TileGeom &gm, uint64_t m)
+{
+    uint32_t v = 0;
+    for (int k = 0; k < gm.c; k++)
+        if ((m >> k) & 1) v |= 1u << k;
+    for (int k = 0; k < gm.h; k++)
+        if ((m >> gm.hb[k]) & 1) v |= 1u << (gm.c + k);
+    return v;
+}
+
+std::string dbl(double v)
+{
+    char b[40];
+    snprintf(b, sizeof b, "%.17g", v);
+    return b;
+}
+
+} // namespace
+
+std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
+{
+    std::ostringstream o;
+    o << kHead;
+    for (size_t pi = 0; pi < passes.size(); pi++) {
+        const PauliPass &pp = passes[pi];
+        const TileGeom &gm = pp.geom;
+        const int t = gm.t, P = 1 << (t - 8);
+        // observables of the pass, and the register accumulator of each
+        std::vector<int> ks;
+        for (const SpecTerm &tm : pp.terms)
+            if (std::find(ks.begin(), ks.end(), tm.k) == ks.end()) ks.push_back(tm.k);
+        std::sort(ks.begin(), ks.end());
+        auto slot = [&](int k) { return (int)(std::find(ks.begin(), ks.end(), k) - ks.begin()); };
+        const int NK = (int)ks.size();
+        o << "extern \"C\" __global__ __launch_bounds__(256) void tq_pauli_" << pi
+          << "(PauliSpecArgs a)\n{\n"
+             "    extern __shared__ __align__(16) unsigned char smem[];\n"
+             "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
+             "    uint64_t *hi_off = reinterpret_cast<uint64_t *>(la + "
+          << (1 << t)
+          << ");\n"
+             "    double *red = reinterpret_cast<double *>(hi_off + "
+          << (1 << gm.h)
+          << ");\n"
+             "    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;\n"
+             "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
+             "    float2 *ps = const_cast<float2 *>(a.psi) + (int64_t)cget(a.rows, row) * a.row_stride;\n"
+             "    build_hi_off(a.g, hi_off);\n"
+             "    __syncthreads();  // hi_off complete before the first tile load\n"
+             "    const TileCtx tc{hi_off, "
+          << ((1u << gm.c) - 1) << "u, " << gm.c
+          << "};\n"
+             "    const uint32_t st = sw((uint32_t)tid);\n";
+        // group terms by their tile X mask; per term its real coefficient,
+        // its real/imaginary part and its sign pattern
+        struct TT {
+            uint32_t zlo, zhi;
+            uint64_t zF;
+            double C;
+            bool im;
+            int kk;
+        };
+        std::map<uint32_t, std::vector<TT>> groups;
+        for (const SpecTerm &tm : pp.terms) {
+            const uint32_t xT = local_mask(gm, tm.x), zT = local_mask(gm, tm.z);
+            const int ny = tm.ny & 3;
+            const double chi = (__builtin_popcountll(tm.x & tm.z) & 1) ? -1.0 : 1.0;
+            // <P> = Re(c' sum_l chi_z(l) conj(psi_l) psi_{l^x}), c' = coeff i^ny chi_z(x):
+            // ny even: c' real, Re part; ny odd: c' = i b, -b times the Im part
+            double C = (ny & 1) ? -(tm.coeff * (ny == 1 ? 1.0 : -1.0) * chi) : tm.coeff * (ny == 2 ? -1.0 : 1.0) * chi;
+            // pairs {l, l^x} summed once when x has a register bit: twice the half
+            if (xT >> 8) C *= 2.0;
+            groups[xT].push_back(TT{zT & 0xffu, zT >> 8, tm.z & gm.fixed_mask, C, (ny & 1) != 0, slot(tm.k)});
+        }
+        int ti = 0;
+        for (auto &g : groups)
+            for (const TT &tt : g.second)
+                o << "    const double L" << ti++ << " = par32((uint32_t)tid & " << tt.zlo << "u) ? " << dbl(-tt.C) << " : "
+                  << dbl(tt.C) << ";\n";
+        for (int j = 0; j < NK; j++) o << "    double e" << j << " = 0.0;\n";
+        o << "    for (int64_t tile = w; tile < " << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
+          << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
+          << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
+          << "    __syncthreads();\n"
+          << "    double2 o[" << P << "];\n";
+        for (int r = 0; r < P; r++) o << "    o[" << r << "] = up2(la[st ^ " << host_sw(256u * r) << "u]);\n";
+        ti = 0;
+        for (auto &g : groups) {
+            const uint32_t xT = g.first, xlo = xT & 0xffu, xhi = xT >> 8;
+            const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
+            const std::vector<TT> &tts = g.second;
+            bool any_re = false, any_im = false;
+            for (const TT &tt : tts) (tt.im ? any_im : any_re) = true;
+            o << "    {\n";
+            for (size_t j = 0; j < tts.size(); j++) o << "        double s" << j << " = 0.0;\n";
+            if (xT) o << "        const uint32_t pt = sw((uint32_t)tid ^ " << xlo << "u);\n";
+            for (int r = 0; r < P; r++) {
+                if (pivot >= 0 && ((r >> pivot) & 1)) continue;
+                if (xT) {
+                    o << "        { const double2 p = up2(la[pt ^ " << host_sw(256u * (r ^ xhi)) << "u]);\n";
+                    if (any_re) o << "          const double re = fma(o[" << r << "].x, p.x, o[" << r << "].y * p.y);\n";
+                    if (any_im) o << "          const double im = fma(o[" << r << "].x, p.y, -o[" << r << "].y * p.x);\n";
+                } else {
+                    o << "        { const double re = fma(o[" << r << "].x, o[" << r << "].x, o[" << r << "].y * o[" << r
+                      << "].y);\n";
+                }
+                for (size_t j = 0; j < tts.size(); j++) {
+                    const bool neg = __builtin_popcount(tts[j].zhi & (uint32_t)r) & 1;
+                    o << "          s" << j << (neg ? " -= " : " += ") << (tts[j].im ? "im" : "re") << ";\n";
+                }
+                o << "        }\n";
+            }
+            for (size_t j = 0; j < tts.size(); j++, ti++)
+                o << "        e" << tts[j].kk << " = fma(par64(fb & " << tts[j].zF << "ull) ? -L" << ti << " : L" << ti
+                  << ", s" << j << ", e" << tts[j].kk << ");\n";
+            o << "    }\n";
+        }
+        o << "    __syncthreads();\n"
+             "    }\n";
+        // fixed-order reduction: waves, then the four wave sums
+        for (int j = 0; j < NK; j++)
+            o << "    { const double v = wave_sum(e" << j << "); if (lane == 0) red[wave * " << NK << " + " << j
+              << "] = v; }\n";
+        o << "    __syncthreads();\n"
+             "    double *out = a.partial + ((int64_t)(row * a.npass + "
+          << pi
+          << ") * a.wg_per_row + w) * a.k_count;\n"
+             "    for (int k = tid; k < a.k_count; k += 256) {\n"
+             "        double v = 0.0;\n"
+             "        switch (k) {\n";
+        for (int j = 0; j < NK; j++)
+            o << "        case " << ks[j] << ": v = ((red[" << j << "] + red[" << NK + j << "]) + red[" << 2 * NK + j
+              << "]) + red[" << 3 * NK + j << "]; break;\n";
+        o << "        default: break;\n"
+             "        }\n"
+             "        out[k] = v;\n"
+             "    }\n"
+             "}\n";
+        (void)K;
+    }
+    o << "} // namespace tq\n";
+    return o.str();
+}
+
+namespace {
+
 struct Module {
     hipModule_t mod = nullptr;
     std::map<std::string, hipFunction_t> fn;
@@ -404,6 +559,30 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     return launch(fn[0], a, nrows * a.wg_per_row, lds, s, "pass");
+}
+
+hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
+                             std::string *log)
+{
+    if (nrows <= 0) return hipSuccess;
+    std::vector<hipFunction_t> fn;
+    hipError_t e = get_kernels(src, {"tq_pauli_" + N(pass)}, &fn, log);
+    if (e != hipSuccess) return e;
+    const size_t lds = pauli_spec_lds_bytes(a.g, 4);
+    return launch(fn[0], a, nrows * a.wg_per_row, lds, s, "pauli");
+}
+
+int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log)
+{
+    std::vector<hipFunction_t> fn;
+    if (get_kernels(src, {"tq_pauli_0"}, &fn, log) != hipSuccess) return 0;
+    int dev = 0, per_cu = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn[0], kThreads, pauli_spec_lds_bytes(g, 4)) !=
+        hipSuccess)
+        return 0;
+    return per_cu * cus;
 }
 
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log)

@@ -38,6 +38,16 @@ hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, siz
 hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
                             std::string *log);
 
+// Kernels tq_pauli_<pass> computing the expectations of one observable set
+// (the same on every row, at most 16 observables) pass by pass: each pass's
+// tile holds the X bits of its terms; partials go to
+// partial[row][npass][wg_per_row][k_count].
+std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K);
+hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
+                             std::string *log);
+// Workgroups of a specialised Pauli pass that fit on the device at once (0 if unknown).
+int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log);
+
 // Compile the specialised kernels of group g (the resident kernel, or the
 // forward pass kernels) ahead of their first launch: for the current device when
 // target is NULL (the module is then cached), else only check that they

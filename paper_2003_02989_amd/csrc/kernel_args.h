@@ -87,6 +87,18 @@ struct DiagArgs {
     double *partial;         // [nrows][wg_per_row][k_count]
 };
 
+// A pass of the Pauli kernel specialised for one observable set.
+struct PauliSpecArgs {
+    const float2 *psi;
+    int64_t row_stride;
+    const int32_t *rows;     // state rows
+    TileGeom g;              // the pass's tile
+    int wg_per_row;
+    int npass, pass;         // partial slots: [nrows][npass][wg_per_row][k_count]
+    int k_count;
+    double *partial;
+};
+
 struct PauliReduceArgs {
     const int32_t *rows;     // batch index of each row
     const double *partial;

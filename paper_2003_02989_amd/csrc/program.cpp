@@ -973,6 +973,61 @@ PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vect
     return pt;
 }
 
+bool pauli_spec_plan(int n, int t, int c, const std::vector<TermDev> &terms, std::vector<PauliPass> *passes)
+{
+    passes->clear();
+    const int h = t - c;
+    const uint64_t low = (1ull << c) - 1;
+    std::vector<const TermDev *> left;
+    for (const TermDev &td : terms) {
+        if (__builtin_popcountll(td.x & ~low) > h) return false;
+        left.push_back(&td);
+    }
+    while (!left.empty()) {
+        // grow the set S of high tile bits greedily: each step adds the X
+        // mask that keeps S within h bits and covers the most terms
+        uint64_t S = 0;
+        for (;;) {
+            uint64_t best = 0;
+            size_t best_cov = 0;
+            int best_size = 0;
+            for (const TermDev *td : left) {
+                const uint64_t U = S | (td->x & ~low);
+                if (U == S || __builtin_popcountll(U) > h) continue;
+                size_t cov = 0;
+                for (const TermDev *o : left) cov += ((o->x & ~low) & ~U) == 0;
+                const int size = __builtin_popcountll(U);
+                if (cov > best_cov || (cov == best_cov && size < best_size)) {
+                    best = U;
+                    best_cov = cov;
+                    best_size = size;
+                }
+            }
+            if (!best) break;
+            S = best;
+        }
+        std::vector<int> bits;
+        for (int b = 0; b < c; b++) bits.push_back(b);
+        for (int b = c; b < n; b++)
+            if ((S >> b) & 1) bits.push_back(b);
+        for (int b = c; b < n && (int)bits.size() < t; b++)
+            if (!((S >> b) & 1)) bits.push_back(b);
+        std::sort(bits.begin(), bits.end());
+        PauliPass ps;
+        ps.geom = geom_from_bits(n, c, bits);
+        std::vector<const TermDev *> rest;
+        for (const TermDev *td : left) {
+            if (((td->x & ~low) & ~S) == 0)
+                ps.terms.push_back(SpecTerm{td->k, td->x, td->z, td->ny, td->coeff});
+            else
+                rest.push_back(td);
+        }
+        passes->push_back(std::move(ps));
+        left.swap(rest);
+    }
+    return true;
+}
+
 DiagTables diag_tables(const std::vector<std::vector<TermDev>> &per_row, bool uniform)
 {
     DiagTables dt;

@@ -126,6 +126,24 @@ struct PauliTables {
 };
 PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vector<TermDev>> &per_row, bool uniform);
 
+// Passes of the Pauli kernel specialised for one observable set (the same
+// terms on every row): each pass's tile holds the X bits of all its terms, so
+// that every partner amplitude is in the tile and the state is read once per
+// pass.  Terms are given with global masks.
+struct SpecTerm {
+    int k;            // observable
+    uint64_t x, z;
+    int ny;           // Y factors
+    double coeff;
+};
+struct PauliPass {
+    TileGeom geom;
+    std::vector<SpecTerm> terms;
+};
+// Plans passes over tiles of t bits (c low bits); false when some term flips
+// more bits above the low ones than a tile holds.
+bool pauli_spec_plan(int n, int t, int c, const std::vector<TermDev> &terms, std::vector<PauliPass> *passes);
+
 // Tables of the diagonal (Z-only) Pauli kernel: every term of every row must
 // have x = 0 and the states at least kDiagBlockBits qubits.
 struct DiagTables {

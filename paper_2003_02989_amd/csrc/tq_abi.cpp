@@ -87,6 +87,10 @@ struct ObsGroupDev {
     bool diag = false;
     int damax = 0;
     DevBuf dchunks, dcbegin, dccount, dclasses, dterms;
+    // passes and source of the kernels specialised for the observable set
+    // (specialize = 1, every row the same terms, tiles that hold every X mask)
+    std::vector<PauliPass> spec_passes;
+    std::string spec_src;
     void release()
     {
         for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
@@ -395,6 +399,12 @@ void ensure_obs(tq_program p, tq_observables o)
         bool diag = n >= kDiagBlockBits;
         for (auto &row : per_row)
             for (auto &td : row) diag = diag && td.x == 0;
+        const int spec_t = std::min(p->pd->opt.tile, 12);
+        size_t nterms = 0;
+        for (auto &row : per_row) nterms = std::max(nterms, row.size());
+        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= 64 && n > spec_t &&
+            pauli_spec_plan(n, spec_t, std::min(p->pd->opt.low, spec_t - 2), per_row[0], &og->spec_passes))
+            og->spec_src = pauli_spec_source(og->spec_passes, od.K);
         if (diag) {
             DiagTables dt = diag_tables(per_row, uniform);
             og->diag = true;
@@ -455,6 +465,48 @@ void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, h
     }
 }
 
+// Expectations of an observable set the same on every row of group gi, by
+// the kernels specialised for it: one state read per pass of the plan.
+void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    ObsGroupDev &og = *p->obs_dev[gi];
+    const int nrows = (int)g.rows.size();
+    const int npass = (int)og.spec_passes.size();
+    std::string log;
+    int fit = pauli_spec_slots(og.spec_src, og.spec_passes[0].geom, &log);
+    if (fit <= 0) {
+        if (!log.empty()) fail(TQ_E_DEVICE, log);
+        fit = 2048;
+    }
+    const int64_t ntiles = (int64_t)1 << (g.n - og.spec_passes[0].geom.t);
+    PauliSpecArgs a{};
+    a.psi = psi;
+    a.row_stride = (int64_t)1 << g.n;
+    a.rows = (const int32_t *)gd.ident.p;
+    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
+    a.npass = npass;
+    a.k_count = K;
+    a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)nrows * npass * a.wg_per_row * K);
+    for (int pi = 0; pi < npass; pi++) {
+        a.g = og.spec_passes[pi].geom;
+        a.pass = pi;
+        const hipError_t e = launch_pauli_spec(og.spec_src, pi, a, nrows, s, &log);
+        if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+        hip_check(e, "specialised Pauli launch");
+    }
+    PauliReduceArgs r{};
+    r.rows = (const int32_t *)gd.rows.p;
+    r.partial = a.partial;
+    r.wg_per_row = npass * a.wg_per_row;  // the passes' workgroups side by side
+    r.K = K;
+    r.k_begin = 0;
+    r.k_count = K;
+    r.out = out;
+    hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
+}
+
 // Run the Pauli kernel over group gi's rows: expectations into out[b, k]
 // (when out is not NULL) and, when phi is not NULL, phi = sum_k g_k h_k psi
 // with g = upstream.  Observables are split over launches so that the
@@ -469,6 +521,10 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     if (K == 0 || nrows == 0) return;
     if (!phi && og.diag) {
         diag_group(p, gi, psi, K, out, s);
+        return;
+    }
+    if (!phi && !og.spec_passes.empty()) {
+        spec_pauli_group(p, gi, psi, K, out, s);
         return;
     }
     PauliArgs a{};

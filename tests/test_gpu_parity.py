@@ -169,6 +169,22 @@ def test_diagonal_observables(n, B, uniform):
     compare(gpu_outputs(w), oracle_outputs(w))
 
 
+@pytest.mark.parametrize("n,B", [(13, 3), (16, 2), (20, 1)])
+def test_specialized_pauli_passes(n, B):
+    # an observable set the same on every row (X/Y/Z strings of weight <= 4,
+    # identity and Z-only terms, three observables) on states larger than a
+    # tile: expectations by the passes compiled for it, each tile holding the
+    # X bits of its terms
+    rng = wl.rng_for(5300 + n)
+    w = wl.random_batch(5400 + n, B=B, n=n, n_gates=60, n_symbols=4, K=3)
+    shared = wl.random_observables(rng, n, 3, max_terms=12, max_weight=4)
+    shared[1] = shared[1] + [(0.7, []), (-0.4, [(0, "Z"), (n - 1, "Z")])]
+    for b in range(B):
+        w.observables[b] = shared
+    say("specialised Pauli passes", n, B)
+    compare(gpu_outputs(w, want=("exp",), specialize=True), oracle_outputs(w, want=("exp",)))
+
+
 @pytest.mark.gpu
 def test_amplitudes_from_state_matches_amplitudes():
     # the state-based lookup returns what tq_amplitudes returns, bit for bit,
