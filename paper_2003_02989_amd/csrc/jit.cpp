@@ -33,10 +33,13 @@ std::string N(long v) { return std::to_string(v); }
 
 // LDS of a specialised Pauli pass: the tile, its high-bit offsets and the
 // per-wave sums of at most `nk` observables (every pass has at most 16)
-size_t pauli_spec_lds_bytes(const TileGeom &g, int)
+size_t pauli_spec_lds_bytes(const TileGeom &g)
 {
-    return sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) + sizeof(double) * 4 * 16;
+    // the tile, its high-bit offsets, and per-wave sums of at most 16
+    // observables for at most 16 waves
+    return sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) + sizeof(double) * 16 * 16;
 }
+int pauli_spec_threads(const TileGeom &g) { return 1 << (g.t - 4); }
 
 uint32_t host_sw(uint32_t i) { return i ^ ((i >> 5) & 31u); }
 
@@ -314,7 +317,9 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
     for (size_t pi = 0; pi < passes.size(); pi++) {
         const PauliPass &pp = passes[pi];
         const TileGeom &gm = pp.geom;
-        const int t = gm.t, P = 1 << (t - 8);
+        // 16 amplitudes per thread: a tile of 2^t amplitudes takes 2^(t-4)
+        // threads (tb bits of the tile index select the thread)
+        const int t = gm.t, P = 16, tb = t - 4, NT = 1 << tb, NW = NT / 64;
         // observables of the pass, and the register accumulator of each
         std::vector<int> ks;
         for (const SpecTerm &tm : pp.terms)
@@ -322,7 +327,7 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
         std::sort(ks.begin(), ks.end());
         auto slot = [&](int k) { return (int)(std::find(ks.begin(), ks.end(), k) - ks.begin()); };
         const int NK = (int)ks.size();
-        o << "extern \"C\" __global__ __launch_bounds__(256) void tq_pauli_" << pi
+        o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void tq_pauli_" << pi
           << "(PauliSpecArgs a)\n{\n"
              "    extern __shared__ __align__(16) unsigned char smem[];\n"
              "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
@@ -359,8 +364,8 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
             // ny even: c' real, Re part; ny odd: c' = i b, -b times the Im part
             double C = (ny & 1) ? -(tm.coeff * (ny == 1 ? 1.0 : -1.0) * chi) : tm.coeff * (ny == 2 ? -1.0 : 1.0) * chi;
             // pairs {l, l^x} summed once when x has a register bit: twice the half
-            if (xT >> 8) C *= 2.0;
-            groups[xT].push_back(TT{zT & 0xffu, zT >> 8, tm.z & gm.fixed_mask, C, (ny & 1) != 0, slot(tm.k)});
+            if (xT >> tb) C *= 2.0;
+            groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, tm.z & gm.fixed_mask, C, (ny & 1) != 0, slot(tm.k)});
         }
         int ti = 0;
         for (auto &g : groups)
@@ -371,40 +376,55 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
         o << "    for (int64_t tile = w; tile < " << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
           << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
           << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
-          << "    __syncthreads();\n"
-          << "    double2 o[" << P << "];\n";
-        for (int r = 0; r < P; r++) o << "    o[" << r << "] = up2(la[st ^ " << host_sw(256u * r) << "u]);\n";
+          << "    __syncthreads();\n";
+        // register by register: the own amplitude, then every term group's
+        // partner; one running sum per term
+        std::vector<std::pair<uint32_t, const std::vector<TT> *>> gl;
+        for (auto &g : groups) gl.emplace_back(g.first, &g.second);
+        for (size_t gi = 0; gi < gl.size(); gi++) {
+            const uint32_t xT = gl[gi].first;
+            if (xT) o << "    const uint32_t pt" << gi << " = sw((uint32_t)tid ^ " << (xT & (uint32_t)(NT - 1)) << "u);\n";
+        }
         ti = 0;
-        for (auto &g : groups) {
-            const uint32_t xT = g.first, xlo = xT & 0xffu, xhi = xT >> 8;
-            const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
-            const std::vector<TT> &tts = g.second;
-            bool any_re = false, any_im = false;
-            for (const TT &tt : tts) (tt.im ? any_im : any_re) = true;
-            o << "    {\n";
-            for (size_t j = 0; j < tts.size(); j++) o << "        double s" << j << " = 0.0;\n";
-            if (xT) o << "        const uint32_t pt = sw((uint32_t)tid ^ " << xlo << "u);\n";
-            for (int r = 0; r < P; r++) {
-                if (pivot >= 0 && ((r >> pivot) & 1)) continue;
-                if (xT) {
-                    o << "        { const double2 p = up2(la[pt ^ " << host_sw(256u * (r ^ xhi)) << "u]);\n";
-                    if (any_re) o << "          const double re = fma(o[" << r << "].x, p.x, o[" << r << "].y * p.y);\n";
-                    if (any_im) o << "          const double im = fma(o[" << r << "].x, p.y, -o[" << r << "].y * p.x);\n";
-                } else {
-                    o << "        { const double re = fma(o[" << r << "].x, o[" << r << "].x, o[" << r << "].y * o[" << r
-                      << "].y);\n";
+        for (size_t gi = 0; gi < gl.size(); gi++)
+            for (size_t j = 0; j < gl[gi].second->size(); j++) o << "    double s" << ti++ << " = 0.0;\n";
+        for (int r = 0; r < P; r++) {
+            o << "    {\n        const double2 o = up2(la[st ^ " << host_sw((uint32_t)NT * r) << "u]);\n";
+            int tj = 0;
+            for (size_t gi = 0; gi < gl.size(); gi++) {
+                const uint32_t xT = gl[gi].first, xhi = xT >> tb;
+                const std::vector<TT> &tts = *gl[gi].second;
+                const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
+                if (pivot >= 0 && ((r >> pivot) & 1)) {  // the other half of the pairs
+                    tj += (int)tts.size();
+                    continue;
                 }
-                for (size_t j = 0; j < tts.size(); j++) {
-                    const bool neg = __builtin_popcount(tts[j].zhi & (uint32_t)r) & 1;
-                    o << "          s" << j << (neg ? " -= " : " += ") << (tts[j].im ? "im" : "re") << ";\n";
+                bool any_re = false, any_im = false;
+                for (const TT &tt : tts) (tt.im ? any_im : any_re) = true;
+                o << "        {\n";
+                if (xT) {
+                    o << "        const double2 p = up2(la[pt" << gi << " ^ " << host_sw((uint32_t)NT * (r ^ xhi))
+                      << "u]);\n";
+                    if (any_re) o << "        const double re = fma(o.x, p.x, o.y * p.y);\n";
+                    if (any_im) o << "        const double im = fma(o.x, p.y, -o.y * p.x);\n";
+                } else {
+                    o << "        const double re = fma(o.x, o.x, o.y * o.y);\n";
+                }
+                for (const TT &tt : tts) {
+                    const bool neg = __builtin_popcount(tt.zhi & (uint32_t)r) & 1;
+                    o << "        s" << tj++ << (neg ? " -= " : " += ") << (tt.im ? "im" : "re") << ";\n";
                 }
                 o << "        }\n";
             }
-            for (size_t j = 0; j < tts.size(); j++, ti++)
-                o << "        e" << tts[j].kk << " = fma(par64(fb & " << tts[j].zF << "ull) ? -L" << ti << " : L" << ti
-                  << ", s" << j << ", e" << tts[j].kk << ");\n";
             o << "    }\n";
         }
+        ti = 0;
+        for (size_t gi = 0; gi < gl.size(); gi++)
+            for (const TT &tt : *gl[gi].second) {
+                o << "    e" << tt.kk << " = fma(par64(fb & " << tt.zF << "ull) ? -L" << ti << " : L" << ti << ", s" << ti
+                  << ", e" << tt.kk << ");\n";
+                ti++;
+            }
         o << "    __syncthreads();\n"
              "    }\n";
         // fixed-order reduction: waves, then the four wave sums
@@ -415,12 +435,16 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
              "    double *out = a.partial + ((int64_t)(row * a.npass + "
           << pi
           << ") * a.wg_per_row + w) * a.k_count;\n"
-             "    for (int k = tid; k < a.k_count; k += 256) {\n"
+             "    for (int k = tid; k < a.k_count; k += "
+          << NT
+          << ") {\n"
              "        double v = 0.0;\n"
              "        switch (k) {\n";
-        for (int j = 0; j < NK; j++)
-            o << "        case " << ks[j] << ": v = ((red[" << j << "] + red[" << NK + j << "]) + red[" << 2 * NK + j
-              << "]) + red[" << 3 * NK + j << "]; break;\n";
+        for (int j = 0; j < NK; j++) {
+            o << "        case " << ks[j] << ": v = red[" << j << "]";
+            for (int wv = 1; wv < NW; wv++) o << "; v += red[" << wv * NK + j << "]";
+            o << "; break;\n";
+        }
         o << "        default: break;\n"
              "        }\n"
              "        out[k] = v;\n"
@@ -525,7 +549,8 @@ std::string pass_unit(const Group &g)
 }
 
 template <class Args>
-hipError_t launch(hipFunction_t fn, const Args &a, unsigned grid, size_t lds, hipStream_t s, const char *prof_name)
+hipError_t launch(hipFunction_t fn, const Args &a, unsigned grid, size_t lds, hipStream_t s, const char *prof_name,
+                  unsigned threads = kThreads)
 {
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
@@ -535,7 +560,7 @@ hipError_t launch(hipFunction_t fn, const Args &a, unsigned grid, size_t lds, hi
     Args args = a;
     void *params[] = {&args};
     ProfScope ps(prof_name, s);
-    return hipModuleLaunchKernel(fn, grid, 1, 1, kThreads, 1, 1, (unsigned)lds, s, params, nullptr);
+    return hipModuleLaunchKernel(fn, grid, 1, 1, threads, 1, 1, (unsigned)lds, s, params, nullptr);
 }
 
 } // namespace
@@ -568,8 +593,7 @@ hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecAr
     std::vector<hipFunction_t> fn;
     hipError_t e = get_kernels(src, {"tq_pauli_" + N(pass)}, &fn, log);
     if (e != hipSuccess) return e;
-    const size_t lds = pauli_spec_lds_bytes(a.g, 4);
-    return launch(fn[0], a, nrows * a.wg_per_row, lds, s, "pauli");
+    return launch(fn[0], a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
 }
 
 int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log)
@@ -579,8 +603,12 @@ int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log
     int dev = 0, per_cu = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn[0], kThreads, pauli_spec_lds_bytes(g, 4)) !=
-        hipSuccess)
+    if (pauli_spec_lds_bytes(g) > 65536 &&
+        hipFuncSetAttribute(reinterpret_cast<const void *>(fn[0]), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)pauli_spec_lds_bytes(g)) != hipSuccess)
+        return 0;
+    if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn[0], pauli_spec_threads(g),
+                                                           pauli_spec_lds_bytes(g)) != hipSuccess)
         return 0;
     return per_cu * cus;
 }

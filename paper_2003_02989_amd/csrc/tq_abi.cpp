@@ -399,12 +399,19 @@ void ensure_obs(tq_program p, tq_observables o)
         bool diag = n >= kDiagBlockBits;
         for (auto &row : per_row)
             for (auto &td : row) diag = diag && td.x == 0;
-        const int spec_t = std::min(p->pd->opt.tile, 12);
         size_t nterms = 0;
         for (auto &row : per_row) nterms = std::max(nterms, row.size());
-        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= 64 && n > spec_t &&
-            pauli_spec_plan(n, spec_t, std::min(p->pd->opt.low, spec_t - 2), per_row[0], &og->spec_passes))
-            og->spec_src = pauli_spec_source(og->spec_passes, od.K);
+        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= 64) {
+            // tiles of 2^12..2^14 amplitudes (16 per thread): the fewest
+            // passes, then the smallest tile
+            for (int t = 12; t <= 14 && t < n; t++) {
+                std::vector<PauliPass> pp;
+                if (pauli_spec_plan(n, t, std::min(p->pd->opt.low, t - 2), per_row[0], &pp) &&
+                    (og->spec_passes.empty() || pp.size() < og->spec_passes.size()))
+                    og->spec_passes = std::move(pp);
+            }
+            if (!og->spec_passes.empty()) og->spec_src = pauli_spec_source(og->spec_passes, od.K);
+        }
         if (diag) {
             DiagTables dt = diag_tables(per_row, uniform);
             og->diag = true;

@@ -169,7 +169,7 @@ def test_diagonal_observables(n, B, uniform):
     compare(gpu_outputs(w), oracle_outputs(w))
 
 
-@pytest.mark.parametrize("n,B", [(13, 3), (16, 2), (20, 1)])
+@pytest.mark.parametrize("n,B", [(13, 3), (16, 2), (18, 2), (20, 1)])
 def test_specialized_pauli_passes(n, B):
     # an observable set the same on every row (X/Y/Z strings of weight <= 4,
     # identity and Z-only terms, three observables) on states larger than a
