@@ -324,6 +324,85 @@ template <int R> __device__ __forceinline__ double rscale_dot(const double2 *a, 
     return s;
 }
 
+// The same diagonal ops when some entries are known to be exactly 1 (bit k
+// of U: entry k; its amplitudes are left as they are) or, for derivatives,
+// exactly 0 (bit k of Z: entry k contributes nothing).
+template <int R, int J, int U> __device__ __forceinline__ void rd1u(double2 *a, double2 e0, double2 e1)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = (k >> J) & 1;
+        if ((U >> idx) & 1) continue;
+        a[k] = zmul(idx ? e1 : e0, a[k]);
+    }
+}
+template <int R, int J, int Z> __device__ __forceinline__ double rd1_dotz(const double2 *a, const double2 *f, double2 e0, double2 e1)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = (k >> J) & 1;
+        if ((Z >> idx) & 1) continue;
+        s += zdotr(f[k], zmul(idx ? e1 : e0, a[k]));
+    }
+    return s;
+}
+template <int R, int LO, int HI, int U>
+__device__ __forceinline__ void rd2u(double2 *a, double2 e0, double2 e1, double2 e2, double2 e3)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = 2 * ((k >> LO) & 1) + ((k >> HI) & 1);
+        if ((U >> idx) & 1) continue;
+        a[k] = zmul(idx == 0 ? e0 : idx == 1 ? e1 : idx == 2 ? e2 : e3, a[k]);
+    }
+}
+template <int R, int LO, int HI, int Z>
+__device__ __forceinline__ double rd2_dotz(const double2 *a, const double2 *f, double2 e0, double2 e1, double2 e2, double2 e3)
+{
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        const int idx = 2 * ((k >> LO) & 1) + ((k >> HI) & 1);
+        if ((Z >> idx) & 1) continue;
+        s += zdotr(f[k], zmul(idx == 0 ? e0 : idx == 1 ? e1 : idx == 2 ? e2 : e3, a[k]));
+    }
+    return s;
+}
+
+// X on register bit J: the pairs swap (no arithmetic); controlled by
+// register bit C, or per lane by `on` (a control outside the stage)
+template <int R, int J> __device__ __forceinline__ void rx1(double2 *a)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const double2 x = a[k];
+        a[k] = a[k | (1 << J)];
+        a[k | (1 << J)] = x;
+    }
+}
+template <int R, int J, int C> __device__ __forceinline__ void rx1c(double2 *a)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> J) & 1) || !((k >> C) & 1)) continue;
+        const double2 x = a[k];
+        a[k] = a[k | (1 << J)];
+        a[k | (1 << J)] = x;
+    }
+}
+template <int R, int J> __device__ __forceinline__ void rx1_if(double2 *a, bool on)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const double2 x = a[k], y = a[k | (1 << J)];
+        a[k] = on ? y : x;
+        a[k | (1 << J)] = on ? x : y;
+    }
+}
+
 // dense 4x4 on register bits (LO = the op's first qubit, HI = its second):
 // local index 2*bit(q0) + bit(q1) = 2*bit(LO) + bit(HI)
 template <int R, int LO, int HI, class MT> __device__ __forceinline__ void rm2(double2 *a, MT m)
@@ -598,7 +677,17 @@ __device__ __forceinline__ void reg_rev_op(const PassOp &op, MT m, MT d0, MT d1,
 {
     switch (op.kind) {
     case K_M1: {
-        if (!op.ctrl) {
+        if (op.hint & kHintX) {
+            // a constant X (CNOT's target block): the pairs swap, no gradient
+            if (!op.ctrl) {
+                TQ_BIT_SWITCH(R, op.s0, ({ rx1<R, j_>(a); rx1<R, j_>(f); }))
+            } else if (op.s1 != kFixed) {
+                TQ_ORDERED_SWITCH(R, op.s0, op.s1, ({ rx1c<R, j_, c_>(a); rx1c<R, j_, c_>(f); }))
+            } else {
+                const bool on = ctrl_on(op, base, fb);
+                TQ_BIT_SWITCH(R, op.s0, ({ rx1_if<R, j_>(a, on); rx1_if<R, j_>(f, on); }))
+            }
+        } else if (!op.ctrl) {
             TQ_BIT_SWITCH(R, op.s0, ({
                 rm1<R, j_>(a, m);
                 if (op.ngrad > 0) g0 += rm1_dot<R, j_>(a, f, d0);

@@ -69,9 +69,13 @@ std::string diag_call(const Env &e, const PassOp &op, int R, int mat, bool dot, 
 {
     const std::string sfx = dot ? "_dot" : "", args = dot ? "v, f" : v;
     const std::string Rs = N(R);
+    // entries exactly 1 in W (skipped) are exactly 0 in dW (skipped in dots)
+    const int um = op.hint & 0xf;
+    const std::string ux = um ? (dot ? "_dotz" : "u") : sfx;
+    const std::string ut = um ? ", " + N(um) : "";
     if (op.kind == K_D1) {
         if (op.s0 != kFixed)
-            return "rd1" + sfx + "<" + Rs + ", " + N(op.s0) + ">(" + args + ", " + ent(mat) + ", " + ent(mat + 1) + ")";
+            return "rd1" + ux + "<" + Rs + ", " + N(op.s0) + ut + ">(" + args + ", " + ent(mat) + ", " + ent(mat + 1) + ")";
         return "rscale" + sfx + "<" + Rs + ">(" + args + ", zsel(" + bit(e, op.l0, op.p0) + ", " + ent(mat) + ", " +
                ent(mat + 1) + "))";
     }
@@ -80,7 +84,12 @@ std::string diag_call(const Env &e, const PassOp &op, int R, int mat, bool dot, 
         const int j0 = std::min(op.s0, op.s1), j1 = std::max(op.s0, op.s1);
         const bool q0lo = op.s0 < op.s1;
         const int x[4] = {0, q0lo ? 1 : 2, q0lo ? 2 : 1, 3};
-        return "rd2" + sfx + "<" + Rs + ", " + N(j0) + ", " + N(j1) + ">(" + args + ", " + ent(mat + x[0]) + ", " +
+        // the unit mask in the register-bit order of the arguments
+        int um2 = 0;
+        for (int k = 0; k < 4; k++)
+            if ((um >> x[k]) & 1) um2 |= 1 << k;
+        const std::string ut2 = um ? ", " + N(um2) : "";
+        return "rd2" + ux + "<" + Rs + ", " + N(j0) + ", " + N(j1) + ut2 + ">(" + args + ", " + ent(mat + x[0]) + ", " +
                ent(mat + x[1]) + ", " + ent(mat + x[2]) + ", " + ent(mat + x[3]) + ")";
     }
     if (r0) {  // entries (v, 2 + v) with v the bit of q1
@@ -102,6 +111,11 @@ std::string diag_call(const Env &e, const PassOp &op, int R, int mat, bool dot, 
 std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::string &v)
 {
     const std::string Rs = N(R), m = "M + (z_ + " + N(mat) + ")";
+    if (op.kind == K_M1 && (op.hint & kHintX)) {  // a swap: no matrix read, no arithmetic
+        if (!op.ctrl) return "rx1<" + Rs + ", " + N(op.s0) + ">(" + v + ");";
+        if (op.s1 != kFixed) return "rx1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ");";
+        return "rx1_if<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + bit(e, op.l1, op.p1) + " == " + N(op.cval) + "u);";
+    }
     switch (op.kind) {
     case K_M1:
         if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";

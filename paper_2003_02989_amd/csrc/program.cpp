@@ -600,6 +600,34 @@ int storage_of(const PassOp &op)
     return 0;
 }
 
+// Structure a gate's matrix has for every parameter value (PassOp::hint):
+// the diagonal entries that are exactly 1 (entry index 2 bit(q0) + bit(q1);
+// the gates listed are symmetric in their qubits), or exactly X.
+uint8_t gate_hint(int op, bool cblock)
+{
+    switch (op) {
+    case OP_Z: case OP_ZPOW: return 1;           // diag(1, .)
+    case OP_CZ: case OP_CZPOW: return 1 | 2 | 4;  // diag(1, 1, 1, .)
+    case OP_ZZPOW: return 1 | 8;                 // diag(1, ., ., 1)
+    case OP_X: return kHintX;
+    case OP_CNOT: return cblock ? kHintX : 0;
+    default: return 0;
+    }
+}
+
+// The hint of an op fusing `mem`: entries that are 1 in every member stay 1;
+// an X stays X only alone.
+uint8_t op_hint(const Group &g, const PassOp &op, const std::vector<Member> &mem)
+{
+    if (op.kind == K_D1 || op.kind == K_D2) {
+        uint8_t h = 0xf;
+        for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, false) & 0xf;
+        return h;
+    }
+    if (op.kind == K_M1 && mem.size() == 1) return gate_hint(g.gates[mem[0].gate].op, mem[0].form == FORM_CBLOCK) & kHintX;
+    return 0;
+}
+
 PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
 {
     PassOp op{};
@@ -738,6 +766,7 @@ void plan_group(Group &g, const Options &opt, int S)
         for (auto &ob : ops) {
             int ti = P.add_task(BT_PRODUCT, op_dim(ob.op), storage_of(ob.op), 0, ob.mem);
             ob.op.mat = g.tasks[ti].out;
+            ob.op.hint = op_hint(g, ob.op, ob.mem);
             ps.ops.push_back(ob.op);
         }
         ps.mat_end = g.mat_block;
@@ -784,6 +813,7 @@ void plan_group(Group &g, const Options &opt, int S)
             Member m{gi, 0, (uint8_t)(cls == C_CTRL ? FORM_CBLOCK : FORM_FULL), {0, 0}};
             int ti = P.add_task(BT_DAGGER, dim, diag, 0, {m});
             op.mat = g.tasks[ti].out;
+            op.hint = op_hint(g, op, {m});  // W^dagger keeps the structure of W
             op.ngrad = 0;
             for (int j = 0; j < g.gates[gi].np; j++) {
                 int slot = g.gates[gi].slot0 + j;
