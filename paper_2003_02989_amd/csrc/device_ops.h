@@ -370,6 +370,35 @@ __device__ __forceinline__ double rd2_dotz(const double2 *a, const double2 *f, d
     return s;
 }
 
+// dense 2x2 with a real matrix (imaginary parts exactly 0: RY, H and their
+// products) on register bit J: half the arithmetic of rm1
+template <int R, int J, class MT> __device__ __forceinline__ void rm1r(double2 *a, MT m)
+{
+    const double m00 = m[0].x, m01 = m[1].x, m10 = m[2].x, m11 = m[3].x;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        a[k] = make_double2(fma(m00, x.x, m01 * y.x), fma(m00, x.y, m01 * y.y));
+        a[kk] = make_double2(fma(m10, x.x, m11 * y.x), fma(m10, x.y, m11 * y.y));
+    }
+}
+template <int R, int J, class MT> __device__ __forceinline__ double rm1r_dot(const double2 *a, const double2 *f, MT dm)
+{
+    const double m00 = dm[0].x, m01 = dm[1].x, m10 = dm[2].x, m11 = dm[3].x;
+    double s = 0;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        // Re(conj(f_k) (m00 x + m01 y)) + Re(conj(f_kk) (m10 x + m11 y))
+        s += m00 * zdotr(f[k], x) + m01 * zdotr(f[k], y) + m10 * zdotr(f[kk], x) + m11 * zdotr(f[kk], y);
+    }
+    return s;
+}
+
 // X on register bit J: the pairs swap (no arithmetic); controlled by
 // register bit C, or per lane by `on` (a control outside the stage)
 template <int R, int J> __device__ __forceinline__ void rx1(double2 *a)
@@ -687,6 +716,13 @@ __device__ __forceinline__ void reg_rev_op(const PassOp &op, MT m, MT d0, MT d1,
                 const bool on = ctrl_on(op, base, fb);
                 TQ_BIT_SWITCH(R, op.s0, ({ rx1_if<R, j_>(a, on); rx1_if<R, j_>(f, on); }))
             }
+        } else if (!op.ctrl && (op.hint & kHintReal)) {
+            TQ_BIT_SWITCH(R, op.s0, ({
+                rm1r<R, j_>(a, m);
+                if (op.ngrad > 0) g0 += rm1r_dot<R, j_>(a, f, d0);
+                if (op.ngrad > 1) g1 += rm1r_dot<R, j_>(a, f, d1);
+                rm1r<R, j_>(f, m);
+            }))
         } else if (!op.ctrl) {
             TQ_BIT_SWITCH(R, op.s0, ({
                 rm1<R, j_>(a, m);

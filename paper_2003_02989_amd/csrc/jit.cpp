@@ -118,6 +118,7 @@ std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::str
     }
     switch (op.kind) {
     case K_M1:
+        if (!op.ctrl && (op.hint & kHintReal)) return "rm1r<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (op.s1 != kFixed) return "rm1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
         return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", ctrl_sel(" + m + ", " + bit(e, op.l1, op.p1) +
@@ -137,6 +138,7 @@ std::string dot(const Env &e, const PassOp &op, int R, int d)
     const std::string Rs = N(R), m = "M + (z_ + " + N(d) + ")";
     switch (op.kind) {
     case K_M1:
+        if (!op.ctrl && (op.hint & kHintReal)) return "rm1r_dot<" + Rs + ", " + N(op.s0) + ">(v, f, " + m + ")";
         if (!op.ctrl) return "rm1_dot<" + Rs + ", " + N(op.s0) + ">(v, f, " + m + ")";
         if (op.s1 != kFixed) return "rm1c_dot<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(v, f, " + m + ")";
         // an item whose control is off sees the identity and a zero derivative

@@ -609,8 +609,9 @@ uint8_t gate_hint(int op, bool cblock)
     case OP_Z: case OP_ZPOW: return 1;           // diag(1, .)
     case OP_CZ: case OP_CZPOW: return 1 | 2 | 4;  // diag(1, 1, 1, .)
     case OP_ZZPOW: return 1 | 8;                 // diag(1, ., ., 1)
-    case OP_X: return kHintX;
-    case OP_CNOT: return cblock ? kHintX : 0;
+    case OP_X: return kHintX | kHintReal;
+    case OP_CNOT: return cblock ? kHintX | kHintReal : 0;
+    case OP_RY: case OP_H: return kHintReal;  // real for every angle, and so is dRY/dtheta
     default: return 0;
     }
 }
@@ -624,7 +625,13 @@ uint8_t op_hint(const Group &g, const PassOp &op, const std::vector<Member> &mem
         for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, false) & 0xf;
         return h;
     }
-    if (op.kind == K_M1 && mem.size() == 1) return gate_hint(g.gates[mem[0].gate].op, mem[0].form == FORM_CBLOCK) & kHintX;
+    if (op.kind == K_M1) {
+        // a product of real matrices is real; an X stays X only alone
+        uint8_t h = kHintReal;
+        for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, m.form == FORM_CBLOCK);
+        if (mem.size() == 1) h |= gate_hint(g.gates[mem[0].gate].op, mem[0].form == FORM_CBLOCK) & kHintX;
+        return h;
+    }
     return 0;
 }
 

@@ -81,6 +81,7 @@ enum OpKind : uint8_t {
 };
 
 constexpr uint8_t kHintX = 16;
+constexpr uint8_t kHintReal = 32;  // K_M1: the matrix and its derivatives are real
 struct PassOp {
     uint8_t kind;
     uint8_t l0, l1;   // local bit of q0 / q1 in the tile, kFixed if outside
@@ -92,7 +93,7 @@ struct PassOp {
     uint8_t s0, s1;   // register index of q0 / q1 within the op's stage, kFixed if not in it
     uint8_t hint;     // structure every parameter value keeps: K_D1 / K_D2 bit k (k < 4): diagonal
                       // entry k of the matrix is exactly 1 (and of dW/deta exactly 0); K_M1
-                      // kHintX: the matrix is exactly X (a swap)
+                      // kHintX: the matrix is exactly X (a swap); kHintReal: it is real
     int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
     int32_t dmat[2];  // reverse: offsets of dW/deta_j
     int32_t gslot[2]; // reverse: gradient slot ids
