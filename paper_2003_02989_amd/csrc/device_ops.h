@@ -399,6 +399,23 @@ template <int R, int J, class MT> __device__ __forceinline__ double rm1r_dot(con
     return s;
 }
 
+// dense 2x2 on register bit J applied where `on` (a control outside the
+// stage, per lane): the product is formed on every lane and kept or dropped,
+// the matrix entries themselves stay uniform
+template <int R, int J, class MT> __device__ __forceinline__ void rm1_on(double2 *a, MT m, bool on)
+{
+    const double2 m00 = m[0], m01 = m[1], m10 = m[2], m11 = m[3];
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        const double2 nx = zmul2(m00, x, m01, y), ny = zmul2(m10, x, m11, y);
+        a[k] = on ? nx : x;
+        a[kk] = on ? ny : y;
+    }
+}
+
 // X on register bit J: the pairs swap (no arithmetic); controlled by
 // register bit C, or per lane by `on` (a control outside the stage)
 template <int R, int J> __device__ __forceinline__ void rx1(double2 *a)

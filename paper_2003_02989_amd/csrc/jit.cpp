@@ -121,8 +121,8 @@ std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::str
         if (!op.ctrl && (op.hint & kHintReal)) return "rm1r<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (op.s1 != kFixed) return "rm1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
-        return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", ctrl_sel(" + m + ", " + bit(e, op.l1, op.p1) +
-               " == " + N(op.cval) + "u));";
+        return "rm1_on<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ", " + bit(e, op.l1, op.p1) + " == " +
+               N(op.cval) + "u);";
     case K_M2: return "rm2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_F2: return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_P2:
@@ -301,6 +301,43 @@ std::string pass_kernel_source(const Group &g, int pass)
              "    }\n"
              "}\n";
     }
+    return o.str();
+}
+
+std::string rev_pass_kernel_source(const Group &g, int pass)
+{
+    std::ostringstream o;
+    int gbase = 0;
+    for (int pi = 0; pi < pass; pi++)
+        for (const PassOp &op : g.rev[pi].ops) gbase += op.ngrad;
+    const Pass &ps = g.rev[pass];
+    const TileGeom &gm = ps.geom;
+    int gcount = 0;
+    for (const PassOp &op : ps.ops) gcount += op.ngrad;
+    o << "extern \"C\" __global__ __launch_bounds__(256, 2) void tq_rev_" << pass
+      << "(RevArgs a)\n{\n"
+         "    extern __shared__ __align__(16) unsigned char smem[];\n"
+         "    const RevCtx c = rev_setup(a, smem);\n"
+         "    const double2 *M = c.lm;\n"
+         "    float2 *lp = c.lp, *lf = c.lf;\n"
+         "    double *acc = c.acc;\n"
+         "    const int tid = threadIdx.x;\n"
+         "    for (int64_t tile = c.w; tile < "
+      << (1ll << (gm.n - gm.t))
+      << "ll; tile += a.wg_per_row) {\n"
+         "    const uint64_t fb = pdep64((uint64_t)tile, "
+      << gm.fixed_mask
+      << "ull);\n"
+         "    rev_load(a, c, fb);\n"
+         "    __syncthreads();\n";
+    // accumulator rows of gcount slots, the pass's first slot at column 0
+    const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
+    for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
+    o << "    rev_store(a, c, fb);\n"
+         "    __syncthreads();\n"
+         "    }\n"
+         "    rev_finish(a, c);\n"
+         "}\n";
     return o.str();
 }
 
@@ -555,12 +592,13 @@ hipError_t get_kernels(const std::string &body, const std::vector<std::string> &
     return hipSuccess;
 }
 
-// every forward pass kernel of group g in one source (one compilation: the
-// run-time compiler does not gain from several programs at once)
+// every pass kernel of group g in one source (one compilation: the run-time
+// compiler does not gain from several programs at once)
 std::string pass_unit(const Group &g)
 {
     std::string body = kHead;
     for (int pi = 0; pi < (int)g.fwd.size(); pi++) body += pass_kernel_source(g, pi);
+    for (int pi = 0; pi < (int)g.rev.size(); pi++) body += rev_pass_kernel_source(g, pi);
     return body + "} // namespace tq\n";
 }
 
@@ -627,6 +665,16 @@ int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log
                                                            pauli_spec_lds_bytes(g)) != hipSuccess)
         return 0;
     return per_cu * cus;
+}
+
+hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int nrows, hipStream_t s,
+                                std::string *log)
+{
+    if (nrows <= 0) return hipSuccess;
+    std::vector<hipFunction_t> fn;
+    hipError_t e = get_kernels(pass_unit(g), {"tq_rev_" + N(pass)}, &fn, log);
+    if (e != hipSuccess) return e;
+    return launch(fn[0], a, nrows * a.wg_per_row, rev_pass_lds_bytes(a), s, "rev_pass");
 }
 
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log)

@@ -22,21 +22,22 @@ namespace tq {
 
 // The specialised resident kernel's source (without the shared device code).
 std::string resident_source(const Group &g);
-// The specialised forward pass kernel tq_fwd_<pass> of group g, to be placed
-// in namespace tq after the shared device code (all passes of a group are
-// compiled as one program).  Reverse passes keep the precompiled kernel: their
-// straight-line form holds psi, phi, the gradient partials and the matrices
-// of several ops at once and spills, where the table-driven loop does not.
+// The specialised forward (tq_fwd_<pass>) and reverse (tq_rev_<pass>) tile
+// pass kernels of group g, to be placed in namespace tq after the shared
+// device code (all passes of a group are compiled as one program).
 std::string pass_kernel_source(const Group &g, int pass);
+std::string rev_pass_kernel_source(const Group &g, int pass);
 
 // Launch a specialised kernel of group g, compiled on first use on the
-// current device: the resident kernel, or forward pass `pass` (with the
-// arguments the precompiled kernel takes).  On a compile failure these
+// current device: the resident kernel, or forward / reverse pass `pass` (with
+// the arguments the precompiled kernel takes).  On a compile failure these
 // return hipErrorInvalidSource and set *log to the compiler's message.
 hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, size_t lds, hipStream_t s,
                                 std::string *log);
 hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
                             std::string *log);
+hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int nrows, hipStream_t s,
+                                std::string *log);
 
 // Kernels tq_pauli_<pass> computing the expectations of one observable set
 // (the same on every row, at most 16 observables) pass by pass: each pass's

@@ -936,6 +936,13 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                 r.mat_begin = ps.mat_begin;
                 r.mat_end = ps.mat_end;
                 gbase += gc;
+                if (pd.opt.specialize) {
+                    std::string log;
+                    const hipError_t e = launch_rev_pass_spec(g, (int)pi, r, nrows, s, &log);
+                    if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+                    hip_check(e, "specialised reverse pass launch");
+                    continue;
+                }
                 hip_check(launch_rev_pass(r, nrows, s), "reverse pass launch");
             }
             GradReduceArgs gr{};
