@@ -52,6 +52,7 @@ struct Env {
     // reverse stages: accumulator of gradient slot s is acc[(tid >> 6) * stride + s + shift]
     std::string acc_stride;
     std::string acc_shift;
+    int nt = kThreads;  // threads of the workgroup
 };
 
 // An op bit at tile position l (global position p): from the item's base
@@ -165,7 +166,7 @@ void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint
             if ((k >> j) & 1) x |= 1u << st.bits[j];
         off[k] = host_sw(x);  // sw is linear over xor: sw(base | x) = sw(base) ^ sw(x)
     }
-    o << "    for (uint32_t item = tid; item < " << (1u << (e.t - R)) << "u; item += 256u) {\n";
+    o << "    for (uint32_t item = tid; item < " << (1u << (e.t - R)) << "u; item += " << e.nt << "u) {\n";
     o << "        uint32_t base = item;\n";
     for (int j = 0; j < R; j++) o << "        base = ins0(base, " << (int)st.bits[j] << ");\n";
     o << "        const uint32_t sb = sw(base);\n";
@@ -243,12 +244,19 @@ const char kHead[] =
 
 } // namespace
 
+int resident_threads(const Group &)
+{
+    // four wavefronts: fewer (one thread per item of a three-bit stage) leave
+    // the SIMDs less to interleave and measured slower on the 10-qubit circuits
+    return kThreads;
+}
+
 std::string resident_source(const Group &g)
 {
     std::ostringstream o;
-    const int n = g.n;
+    const int n = g.n, nt = resident_threads(g);
     o << kHead
-      << "extern \"C\" __global__ __launch_bounds__(256, 4) void tq_resident_spec(ResArgs a)\n{\n"
+      << "extern \"C\" __global__ __launch_bounds__(" << nt << ") void tq_resident_spec(ResArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    double *acc = reinterpret_cast<double *>(smem);\n"
          "    float2 *lp = reinterpret_cast<float2 *>(acc + 4 * a.nacc);\n"
@@ -257,16 +265,17 @@ std::string resident_source(const Group &g)
       << "u;\n"
          "    const SMat M = smat(a.mats + (int64_t)blockIdx.x * a.mat_stride);\n"
          "    const int tid = threadIdx.x;\n"
-         "    resident_begin(a, M, acc, lp, tid, 256);\n";
-    const Env e{n, 0, "M", false, "a.nacc", "a.gacc"};
+         "    resident_begin(a, M, acc, lp, tid, " << nt << ");\n";
+    Env e{n, 0, "M", false, "a.nacc", "a.gacc"};
+    e.nt = nt;
     for (const Pass &ps : g.fwd)
         for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
-    o << "    resident_middle(a, acc, lp, lf, blockIdx.x, tid, 256);\n"
+    o << "    resident_middle(a, acc, lp, lf, blockIdx.x, tid, " << nt << ");\n"
          "    if (a.grad) {\n";
     for (const Pass &ps : g.rev)
         for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
     o << "    }\n"
-         "    resident_end(a, acc, blockIdx.x, tid, 256);\n"
+         "    resident_end(a, acc, blockIdx.x, tid, " << nt << ");\n"
          "}\n"
          "} // namespace tq\n";
     return o.str();
@@ -626,7 +635,7 @@ hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, siz
     std::vector<hipFunction_t> fn;
     hipError_t e = get_kernels(resident_source(g), {"tq_resident_spec"}, &fn, log);
     if (e != hipSuccess) return e;
-    return launch(fn[0], a, nrows, lds, s, "resident");
+    return launch(fn[0], a, nrows, lds, s, "resident", resident_threads(g));
 }
 
 hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
