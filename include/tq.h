@@ -67,12 +67,14 @@ typedef enum {
  *                    (default 0 = no limit; 1 makes every gate its own pass,
  *                    which measures the bandwidth of single-gate passes);
  *   specialize:      1 = every circuit structure runs kernels generated
- *                    for it (the resident kernel, or its forward tile passes)
- *                    and compiled with hipRTC on first use (or by
- *                    tq_program_specialize), with every stage and op written
- *                    in as constants; 0 = the precompiled kernels that read
- *                    the plan from tables.  Reverse tile passes always use
- *                    the precompiled kernel. */
+ *                    for it (the resident kernel, or its forward and reverse
+ *                    tile passes) and compiled with hipRTC on first use (or
+ *                    by tq_program_specialize), with every stage and op
+ *                    written in as constants; likewise an observable set that
+ *                    is the same on every row (at most 16 observables and 64
+ *                    terms, some with X or Y factors) gets expectation passes
+ *                    generated for its terms.  0 = the precompiled kernels
+ *                    that read the plan from tables (default). */
 typedef struct {
     int32_t max_tile_qubits;
     int32_t low_qubits;
@@ -107,8 +109,8 @@ void tq_program_destroy(tq_program prog);
 
 /* Compile the kernels a program created with specialize = 1 generates for
  * its circuit structures (per structure: the resident kernel when its
- * circuits run resident, else its forward tile passes), ahead of their first
- * launch.
+ * circuits run resident, else its forward and reverse tile passes), ahead of
+ * their first launch.
  * target NULL: for the current device (the kernels are cached until the
  * process ends); otherwise an offload target such as "gfx950", for which the
  * code is only compiled and checked (no device is needed).  A compiler

@@ -50,7 +50,7 @@ hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecAr
 int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log);
 
 // Compile the specialised kernels of group g (the resident kernel, or the
-// forward pass kernels) ahead of their first launch: for the current device when
+// forward and reverse pass kernels) ahead of their first launch: for the current device when
 // target is NULL (the module is then cached), else only check that they
 // compile for the offload target (e.g. "gfx950"), which needs no device.
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log);

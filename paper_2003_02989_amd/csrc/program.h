@@ -20,7 +20,7 @@ struct Options {
     int low = 6;      // contiguous low bits per tile
     bool fuse = true;
     int max_pass_gates = 0;  // 0: no limit
-    bool specialize = false; // resident kernels compiled per circuit structure at run time
+    bool specialize = false; // kernels compiled per circuit structure at run time
 };
 
 struct HGate {
