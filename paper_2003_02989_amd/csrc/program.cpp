@@ -860,8 +860,7 @@ void plan_group(Group &g, const Options &opt, int S)
     off = 0;
     for (Pass &ps : g.rev) {
         ps.op_offset = off;
-        make_stages(ps, n <= std::min(opt.tile, 12) ? kStageBitsRevResident : kStageBitsRev, kRevDense2Bits, g, task_at,
-                    false);
+        make_stages(ps, rev_stage_bits(n, opt), kRevDense2Bits, g, task_at, false);
         off += (int)ps.ops.size();
     }
 

@@ -2,6 +2,7 @@
 // groups (circuits of the batch that share gates and symbol wiring) and the
 // pass plans the kernels execute.
 #pragma once
+#include <algorithm>
 #include <memory>
 #include <string>
 #include <vector>
@@ -84,6 +85,18 @@ constexpr int kOpDispatchCost = 6;
 // One register stage's LDS round trip in the same units (measured: ~0.29 ms
 // per stage of a 2^30-amplitude pass).
 constexpr int kStageCost = 11;
+
+// Register bits of reverse stages.  Circuits small enough for the resident
+// kernel keep kStageBitsRevResident (the width the precompiled resident kernel
+// is compiled for), except states of at most kWideRevQubits qubits whose
+// kernel is generated per structure: there a workgroup of one thread per
+// three-bit item runs kStageBitsRev-bit stages (half the LDS round trips).
+constexpr int kWideRevQubits = 10;
+inline int rev_stage_bits(int n, const Options &opt)
+{
+    if (n > std::min(opt.tile, 12)) return kStageBitsRev;
+    return opt.specialize && n <= kWideRevQubits ? kStageBitsRev : kStageBitsRevResident;
+}
 
 struct ProgramData {
     int B = 0, S = 0, nmax = 0;

@@ -591,18 +591,22 @@ hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 // Small circuits run as one resident kernel per call when psi (and phi), the
 // row's matrices and the accumulators fit in LDS.
 constexpr size_t kResidentLds = 150 * 1024;
+// the specialised resident kernel is launched with at most the default
+// dynamic LDS window
+constexpr size_t kResidentSpecLds = 64 * 1024;
 
 bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
 {
     const Group &g = *p->pd->groups[gi];
     if (g.n > std::min(p->pd->opt.tile, 12)) return false;
-    // the resident kernel is compiled for reverse stages of at most
-    // kStageBitsRevResident bits (the planner's choice for such circuits)
+    const int nacc = std::max(tmax + (adjoint ? g.n_gslots : 0), 1);
+    const size_t lds = resident_lds_bytes(g.n, nacc, adjoint);
+    // the precompiled resident kernel runs reverse stages of at most
+    // kStageBitsRevResident bits; wider ones need the specialised kernel
     for (const Pass &ps : g.rev)
         for (const Stage &st : ps.stages)
-            if (st.r > kStageBitsRevResident) return false;
-    const int nacc = std::max(tmax + (adjoint ? g.n_gslots : 0), 1);
-    return resident_lds_bytes(g.n, nacc, adjoint) <= kResidentLds;
+            if (st.r > kStageBitsRevResident && !(p->pd->opt.specialize && lds <= kResidentSpecLds)) return false;
+    return lds <= kResidentLds;
 }
 
 // Launch the resident kernel of group gi: the one specialised for the
@@ -613,7 +617,7 @@ void run_resident(tq_program p, size_t gi, const ResArgs &a, hipStream_t s)
     const Group &g = *p->pd->groups[gi];
     const int nrows = (int)g.rows.size();
     const size_t lds = resident_lds_bytes(a.n, a.nacc, a.grad != nullptr);
-    if (p->pd->opt.specialize && lds <= 65536) {
+    if (p->pd->opt.specialize && lds <= kResidentSpecLds) {
         std::string log;
         const hipError_t e = launch_resident_spec(g, a, nrows, lds, s, &log);
         if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
