@@ -13,6 +13,9 @@
 #include <hip/hiprtc.h>
 
 #include <algorithm>
+#include <tuple>
+#include <cmath>
+#include <array>
 #include <cstdio>
 #include <map>
 #include <memory>
@@ -30,6 +33,13 @@ const char kPrelude[] =
     ;
 
 std::string N(long v) { return std::to_string(v); }
+// a double literal that reads back exactly
+std::string dbl(double v)
+{
+    char b[40];
+    snprintf(b, sizeof b, "%.17g", v);
+    return std::string(b).find_first_of(".en") == std::string::npos ? std::string(b) + ".0" : std::string(b);
+}
 
 // LDS of a specialised Pauli pass: the tile, its high-bit offsets and the
 // per-wave sums of at most `nk` observables (every pass has at most 16)
@@ -53,6 +63,7 @@ struct Env {
     std::string acc_stride;
     std::string acc_shift;
     int nt = kThreads;  // threads of the workgroup
+    const Group *grp = nullptr;  // reverse stages: gradients from gate generators where known
 };
 
 // An op bit at tile position l (global position p): from the item's base
@@ -154,6 +165,103 @@ std::string dot(const Env &e, const PassOp &op, int R, int d)
     }
 }
 
+// Im<f| G |v> for the generator terms of one parameter, on the registers
+// before the op is applied, as a block that adds it to `acc`; "" when a term
+// flips a bit outside the stage.  Term c i^ny X^x Z^z pairs register k with
+// k' = k ^ x and contributes c (-1)^|z & bits(k')| Im(i^ny conj(f_k) v_k'),
+// i.e. +-c times Im or Re of conj(f_k) v_k'.  Signs of z bits outside the
+// stage are per item: the coefficients of a (k, k', part) entry are kept
+// for the four values of the op's two bits, entries with proportional
+// coefficient vectors share an accumulator (two FMAs per entry), and each
+// accumulator is weighted once per item.
+std::string gen_dot(const Env &e, const PassOp &op, int R, const std::vector<GenTerm> &terms, const std::string &acc)
+{
+    const int NR = 1 << R;
+    const bool r0 = op.s0 != kFixed, r1 = op.s1 != kFixed;
+    std::map<std::tuple<int, int, int>, std::array<double, 4>> ent;  // (k, k', re) -> coefficient per (b0, b1)
+    for (const GenTerm &tm : terms) {
+        int xr = 0;
+        if (tm.x & 1) {
+            if (!r0) return "";
+            xr |= 1 << op.s0;
+        }
+        if (tm.x & 2) {
+            if (!r1) return "";
+            xr |= 1 << op.s1;
+        }
+        const int rt = ((tm.z & 1) && !r0 ? 1 : 0) | ((tm.z & 2) && !r1 ? 2 : 0);  // z bits read per item
+        const double sny = (tm.ny & 2) ? -1.0 : 1.0;                              // i^2 = -1
+        for (int k = 0; k < NR; k++) {
+            const int kp = k ^ xr;
+            int par = 0;
+            if ((tm.z & 1) && r0) par ^= (kp >> op.s0) & 1;
+            if ((tm.z & 2) && r1) par ^= (kp >> op.s1) & 1;
+            auto it = ent.find({k, kp, tm.ny & 1});
+            if (it == ent.end()) it = ent.emplace(std::make_tuple(k, kp, tm.ny & 1), std::array<double, 4>{}).first;
+            for (int rho = 0; rho < 4; rho++)
+                it->second[rho] += tm.c * sny * (((par ^ __builtin_popcount(rt & rho)) & 1) ? -1.0 : 1.0);
+        }
+    }
+    // accumulator classes: coefficient vectors up to sign
+    std::vector<std::array<double, 4>> cls;
+    std::vector<std::vector<std::pair<std::tuple<int, int, int>, double>>> mem;
+    for (auto &en : ent) {
+        const std::array<double, 4> &a = en.second;
+        int first = -1;
+        for (int r = 0; r < 4 && first < 0; r++)
+            if (std::fabs(a[r]) > 1e-15) first = r;
+        if (first < 0) continue;
+        const double sg = a[first] < 0 ? -1.0 : 1.0;
+        std::array<double, 4> key;
+        for (int r = 0; r < 4; r++) key[r] = sg * a[r];
+        size_t ci = 0;
+        for (; ci < cls.size(); ci++) {
+            bool same = true;
+            for (int r = 0; r < 4; r++) same &= std::fabs(cls[ci][r] - key[r]) <= 1e-12 * std::fabs(key[first]);
+            if (same) break;
+        }
+        if (ci == cls.size()) {
+            cls.push_back(key);
+            mem.emplace_back();
+        }
+        mem[ci].emplace_back(en.first, sg);
+    }
+    // two chains per accumulator (the two FMAs of an entry), summed at the end
+    std::ostringstream o;
+    o << "{ ";
+    for (size_t ci = 0; ci < cls.size(); ci++) o << "double t" << ci << "a = 0.0, t" << ci << "b = 0.0; ";
+    for (size_t ci = 0; ci < cls.size(); ci++)
+        for (auto &m : mem[ci]) {
+            const int k = std::get<0>(m.first), kp = std::get<1>(m.first);
+            const bool re = std::get<2>(m.first);
+            const std::string p = m.second < 0 ? "-" : "", q = m.second < 0 ? "" : "-";
+            const std::string A = "t" + N((long)ci) + "a", B = "t" + N((long)ci) + "b";
+            const std::string F = "f[" + N(k) + "]", V = "v[" + N(kp) + "]";
+            if (re)  // Re(conj(f) v) = f.x v.x + f.y v.y
+                o << A << " = fma(" << p << F << ".x, " << V << ".x, " << A << "); " << B << " = fma(" << p << F
+                  << ".y, " << V << ".y, " << B << "); ";
+            else     // Im(conj(f) v) = f.x v.y - f.y v.x
+                o << A << " = fma(" << p << F << ".x, " << V << ".y, " << A << "); " << B << " = fma(" << q << F
+                  << ".y, " << V << ".x, " << B << "); ";
+        }
+    const std::string b0 = r0 ? "" : bit(e, op.l0, op.p0), b1 = r1 ? "" : bit(e, op.l1, op.p1);
+    o << acc << " += 0.0";
+    for (size_t ci = 0; ci < cls.size(); ci++) {
+        const std::array<double, 4> &a = cls[ci];
+        const bool v0 = a[0] != a[1] || a[2] != a[3], v1 = a[0] != a[2] || a[1] != a[3];
+        std::string w;
+        if (!v0 && !v1) w = dbl(a[0]);
+        else if (!v1) w = "(" + b0 + " ? " + dbl(a[1]) + " : " + dbl(a[0]) + ")";
+        else if (!v0) w = "(" + b1 + " ? " + dbl(a[2]) + " : " + dbl(a[0]) + ")";
+        else
+            w = "(" + b1 + " ? (" + b0 + " ? " + dbl(a[3]) + " : " + dbl(a[2]) + ") : (" + b0 + " ? " + dbl(a[1]) +
+                " : " + dbl(a[0]) + "))";
+        o << " + " << w << " * (t" << ci << "a + t" << ci << "b)";
+    }
+    o << "; }";
+    return o.str();
+}
+
 // item loop header of a stage: base index of the item and the swizzled
 // LDS offsets of its 2^R registers
 void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint32_t> &off)
@@ -220,9 +328,24 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
     int gk = 0;
     for (int oi = st.op_begin; oi < st.op_end; oi++) {
         const PassOp &op = ps.ops[oi - ps.op_offset];
-        o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
-        for (int j = 0; j < op.ngrad; j++)
-            o << "        g[" << gk++ << "] += " << dot(e, op, R, op.dmat[j] - e.mbase) << ";\n";
+        // gradients from the gate's generator on the registers before the op
+        // (no derivative matrix read), else Re(conj(f) dW v) after W^dagger v
+        std::vector<std::string> gd;
+        for (int j = 0; j < op.ngrad && e.grp; j++) {
+            std::vector<GenTerm> gt;
+            const std::string c = op_generator(*e.grp, op, j, &gt) ? gen_dot(e, op, R, gt, "g[" + N(gk + j) + "]") : "";
+            if (c.empty()) break;
+            gd.push_back(c);
+        }
+        if ((int)gd.size() == op.ngrad) {
+            for (const std::string &c : gd) o << "        " << c << "\n";
+            gk += op.ngrad;
+            o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
+        } else {
+            o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
+            for (int j = 0; j < op.ngrad; j++)
+                o << "        g[" << gk++ << "] += " << dot(e, op, R, op.dmat[j] - e.mbase) << ";\n";
+        }
         o << "        " << apply(e, op, R, op.mat - e.mbase, "f") << "\n";
         // keep each op's matrix reads next to the op: scheduled ahead they
         // would hold every matrix of the stage in registers at once
@@ -274,6 +397,7 @@ std::string resident_source(const Group &g)
          "    resident_begin(a, M, acc, lp, tid, " << nt << ");\n";
     Env e{n, 0, "M", false, "a.nacc", "a.gacc"};
     e.nt = nt;
+    e.grp = &g;
     for (const Pass &ps : g.fwd)
         for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
     o << "    resident_middle(a, acc, lp, lf, blockIdx.x, tid, " << nt << ");\n"
@@ -346,7 +470,8 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
          "    rev_load(a, c, fb);\n"
          "    __syncthreads();\n";
     // accumulator rows of gcount slots, the pass's first slot at column 0
-    const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
+    Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
+    e.grp = &g;
     for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
     o << "    rev_store(a, c, fb);\n"
          "    __syncthreads();\n"
@@ -367,13 +492,6 @@ uint32_t local_mask(const TileGeom &gm, uint64_t m)
     for (int k = 0; k < gm.h; k++)
         if ((m >> gm.hb[k]) & 1) v |= 1u << (gm.c + k);
     return v;
-}
-
-std::string dbl(double v)
-{
-    char b[40];
-    snprintf(b, sizeof b, "%.17g", v);
-    return b;
 }
 
 } // namespace

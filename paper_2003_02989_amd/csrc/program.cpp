@@ -13,6 +13,7 @@
 #include "program.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <map>
 #include <set>
@@ -635,6 +636,45 @@ uint8_t op_hint(const Group &g, const PassOp &op, const std::vector<Member> &mem
     return 0;
 }
 
+// Generator terms of gate `opcode` w.r.t. its parameter `which`, in the op
+// frame: a controlled gate's op has its target as q0 and its control as q1,
+// every other two-qubit op keeps the gate's qubit order (q0 the first).
+// Rotations are exp(-i eta P / 2); power gates P^t = exp(-i pi t (P - I) / 2)
+// (the phase convention of the program format); fSim(theta, phi) =
+// exp(-i theta (XX + YY) / 2) exp(-i phi |11><11|), two commuting factors.
+bool gate_generator(int opcode, int which, std::vector<GenTerm> *t)
+{
+    constexpr double h = 0.5, q = 0.25, hp = M_PI / 2, qp = M_PI / 4;
+    t->clear();
+    auto add = [&](int x, int z, int ny, double c) { t->push_back(GenTerm{(uint8_t)x, (uint8_t)z, (uint8_t)ny, c}); };
+    switch (opcode) {
+    case OP_RX: add(1, 0, 0, h); return true;
+    case OP_RY: add(1, 1, 1, h); return true;  // Y = i X Z
+    case OP_RZ: add(0, 1, 0, h); return true;
+    case OP_XPOW: add(1, 0, 0, hp); add(0, 0, 0, -hp); return true;
+    case OP_YPOW: add(1, 1, 1, hp); add(0, 0, 0, -hp); return true;
+    case OP_ZPOW: add(0, 1, 0, hp); add(0, 0, 0, -hp); return true;
+    case OP_XXPOW: add(3, 0, 0, hp); add(0, 0, 0, -hp); return true;
+    case OP_YYPOW: add(3, 3, 2, hp); add(0, 0, 0, -hp); return true;  // YY = -XX ZZ
+    case OP_ZZPOW: add(0, 3, 0, hp); add(0, 0, 0, -hp); return true;
+    case OP_RZZ: add(0, 3, 0, h); return true;
+    case OP_CZPOW:  // (pi/2)(CZ - I) = -pi |11><11| = -(pi/4)(I - Z0 - Z1 + Z0 Z1)
+        add(0, 0, 0, -qp); add(0, 1, 0, qp); add(0, 2, 0, qp); add(0, 3, 0, -qp);
+        return true;
+    case OP_CNOTPOW:  // (pi/2)|1><1|_c (X_t - I) = (pi/4)(X_t - I - Z_c X_t + Z_c); t = q0, c = q1
+        add(1, 0, 0, qp); add(0, 0, 0, -qp); add(1, 2, 0, -qp); add(0, 2, 0, qp);
+        return true;
+    case OP_FSIM:
+        if (which == 0) {  // (XX + YY) / 2
+            add(3, 0, 0, h); add(3, 3, 2, h);
+        } else {           // |11><11| = (I - Z0 - Z1 + Z0 Z1) / 4
+            add(0, 0, 0, q); add(0, 1, 0, -q); add(0, 2, 0, -q); add(0, 3, 0, q);
+        }
+        return true;
+    default: return false;
+    }
+}
+
 PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
 {
     PassOp op{};
@@ -886,6 +926,17 @@ void plan_group(Group &g, const Options &opt, int S)
 }
 
 } // namespace
+
+bool op_generator(const Group &g, const PassOp &op, int j, std::vector<GenTerm> *terms)
+{
+    if (j >= op.ngrad) return false;
+    for (int k = g.rev_tasks.begin; k < g.rev_tasks.end; k++) {
+        const BuildTask &bt = g.tasks[k];
+        if (bt.kind != BT_DERIV || bt.out != op.dmat[j] || bt.mem_count != 1) continue;
+        return gate_generator(g.gates[g.members[bt.mem_begin].gate].op, bt.which, terms);
+    }
+    return false;
+}
 
 TileGeom expectation_geometry(int n, int t, int c, const std::vector<uint64_t> &xmasks)
 {

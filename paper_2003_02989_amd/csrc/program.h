@@ -86,6 +86,21 @@ constexpr int kOpDispatchCost = 6;
 // per stage of a 2^30-amplitude pass).
 constexpr int kStageCost = 11;
 
+// Generators of the parameterised gates.  Every such gate is, as a function
+// of one of its parameters eta, W(eta) = exp(-i eta G) times factors that
+// commute with G and do not depend on eta, so dW/deta = -i G W and the
+// adjoint term Re<phi| dW |psi_before> equals Im<phi| G |psi_after>
+// (Sec. "Adjoint Gradient Backpropagation in Simulations").  G is given as
+// real-weighted Pauli strings c i^ny X^x Z^z on the op's qubits (bit 0 of x
+// and z: the op's q0, bit 1: its q1).
+struct GenTerm {
+    uint8_t x, z, ny;
+    double c;
+};
+// The generator of parameter j of reverse op `op` (a single gate); false when
+// the gate has none of the listed forms.
+bool op_generator(const Group &g, const PassOp &op, int j, std::vector<GenTerm> *terms);
+
 // Register bits of reverse stages.  Circuits small enough for the resident
 // kernel keep kStageBitsRevResident (the width the precompiled resident kernel
 // is compiled for), except states of at most kWideRevQubits qubits whose

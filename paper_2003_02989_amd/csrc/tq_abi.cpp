@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <iomanip>
 #include <map>
 #include <sstream>
 #include <cstring>
@@ -1134,7 +1135,21 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
                         o << (k ? "," : "") << "{\"kind\":\"" << kinds[op.kind] << "\",\"p\":[" << (int)op.p0 << ","
                           << (int)op.p1 << "],\"l\":[" << (int)op.l0 << "," << (int)op.l1 << "],\"ctrl\":" << (int)op.ctrl
                           << ",\"ngrad\":" << (int)op.ngrad << ",\"members\":"
-                          << (members_at.count(op.mat) ? members_at[op.mat] : 0) << "}";
+                          << (members_at.count(op.mat) ? members_at[op.mat] : 0);
+                        if (dir == 1) {  // generator terms [x, z, ny, c] of each gradient parameter
+                            o << ",\"gen\":[";
+                            for (int j = 0; j < op.ngrad; j++) {
+                                std::vector<GenTerm> gt;
+                                o << (j ? "," : "") << "[";
+                                if (op_generator(g, op, j, &gt))
+                                    for (size_t m = 0; m < gt.size(); m++)
+                                        o << (m ? "," : "") << "[" << (int)gt[m].x << "," << (int)gt[m].z << ","
+                                          << (int)gt[m].ny << "," << std::setprecision(17) << gt[m].c << "]";
+                                o << "]";
+                            }
+                            o << "]";
+                        }
+                        o << "}";
                     }
                     o << "],\"stages\":[";
                     for (size_t k = 0; k < ps.stages.size(); k++) {
