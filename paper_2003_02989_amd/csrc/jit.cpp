@@ -750,45 +750,78 @@ hipError_t launch(hipFunction_t fn, const Args &a, unsigned grid, size_t lds, hi
     return hipModuleLaunchKernel(fn, grid, 1, 1, threads, 1, 1, (unsigned)lds, s, params, nullptr);
 }
 
+// Kernel `name` of the program whose source `src()` generates, through the
+// caller's memo (slot `slot` of `nslots`) when it has one: the source is
+// generated and looked up only the first time on a device.
+template <class Src>
+hipError_t memo_kernel(SpecMemo *memo, size_t slot, size_t nslots, Src &&src, const std::string &name,
+                       hipFunction_t *fn, std::string *log)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot]) {
+        *fn = memo->fn[slot];
+        return hipSuccess;
+    }
+    std::vector<hipFunction_t> fns;
+    e = get_kernels(src(), {name}, &fns, log);
+    if (e != hipSuccess) return e;
+    *fn = fns[0];
+    if (memo) {
+        if (memo->dev != dev || memo->fn.size() != nslots) {
+            memo->dev = dev;
+            memo->fn.assign(nslots, nullptr);
+            memo->slots = -1;
+        }
+        if (slot < nslots) memo->fn[slot] = fns[0];
+    }
+    return hipSuccess;
+}
+
 } // namespace
 
 hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, size_t lds, hipStream_t s,
-                                std::string *log)
+                                std::string *log, SpecMemo *memo)
 {
     if (nrows <= 0) return hipSuccess;
-    std::vector<hipFunction_t> fn;
-    hipError_t e = get_kernels(resident_source(g), {"tq_resident_spec"}, &fn, log);
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, 0, 1, [&] { return resident_source(g); }, "tq_resident_spec", &fn, log);
     if (e != hipSuccess) return e;
-    return launch(fn[0], a, nrows, lds, s, "resident", resident_threads(g));
+    return launch(fn, a, nrows, lds, s, "resident", resident_threads(g));
 }
 
 hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
-                            std::string *log)
+                            std::string *log, SpecMemo *memo)
 {
     if (nrows <= 0) return hipSuccess;
-    std::vector<hipFunction_t> fn;
-    hipError_t e = get_kernels(pass_unit(g), {"tq_fwd_" + N(pass)}, &fn, log);
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, (size_t)pass, g.fwd.size() + g.rev.size(), [&] { return pass_unit(g); },
+                               "tq_fwd_" + N(pass), &fn, log);
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
-    return launch(fn[0], a, nrows * a.wg_per_row, lds, s, "pass");
+    return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
 }
 
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
-                             std::string *log)
+                             std::string *log, SpecMemo *memo)
 {
     if (nrows <= 0) return hipSuccess;
-    std::vector<hipFunction_t> fn;
-    hipError_t e = get_kernels(src, {"tq_pauli_" + N(pass)}, &fn, log);
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_pauli_" + N(pass), &fn,
+                               log);
     if (e != hipSuccess) return e;
-    return launch(fn[0], a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
+    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
 }
 
-int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log)
+int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo)
 {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (memo && memo->dev == dev && memo->slots >= 0) return memo->slots;
     std::vector<hipFunction_t> fn;
     if (get_kernels(src, {"tq_pauli_0"}, &fn, log) != hipSuccess) return 0;
-    int dev = 0, per_cu = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    int per_cu = 0, cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
     if (pauli_spec_lds_bytes(g) > 65536 &&
         hipFuncSetAttribute(reinterpret_cast<const void *>(fn[0]), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -797,17 +830,19 @@ int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log
     if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn[0], pauli_spec_threads(g),
                                                            pauli_spec_lds_bytes(g)) != hipSuccess)
         return 0;
+    if (memo && memo->dev == dev) memo->slots = per_cu * cus;
     return per_cu * cus;
 }
 
 hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int nrows, hipStream_t s,
-                                std::string *log)
+                                std::string *log, SpecMemo *memo)
 {
     if (nrows <= 0) return hipSuccess;
-    std::vector<hipFunction_t> fn;
-    hipError_t e = get_kernels(pass_unit(g), {"tq_rev_" + N(pass)}, &fn, log);
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, g.fwd.size() + (size_t)pass, g.fwd.size() + g.rev.size(),
+                               [&] { return pass_unit(g); }, "tq_rev_" + N(pass), &fn, log);
     if (e != hipSuccess) return e;
-    return launch(fn[0], a, nrows * a.wg_per_row, rev_pass_lds_bytes(a), s, "rev_pass");
+    return launch(fn, a, nrows * a.wg_per_row, rev_pass_lds_bytes(a), s, "rev_pass");
 }
 
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log)

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <string>
+#include <vector>
 
 #include "kernel_args.h"
 #include "program.h"
@@ -28,16 +29,28 @@ std::string resident_source(const Group &g);
 std::string pass_kernel_source(const Group &g, int pass);
 std::string rev_pass_kernel_source(const Group &g, int pass);
 
+// Handles of one structure's specialised kernels on one device.  The caller
+// keeps one per structure (and per kind of kernel) so that repeated launches
+// neither regenerate the source nor look it up in the process-wide cache;
+// it is reset when the current device changes.
+struct SpecMemo {
+    int dev = -1;
+    std::vector<hipFunction_t> fn;  // by kernel slot, null until looked up
+    int slots = -1;                 // pauli_spec_slots' answer, -1 until asked
+};
+
 // Launch a specialised kernel of group g, compiled on first use on the
 // current device: the resident kernel, or forward / reverse pass `pass` (with
 // the arguments the precompiled kernel takes).  On a compile failure these
 // return hipErrorInvalidSource and set *log to the compiler's message.
+// `memo` (one per group and kind: resident, or the group's passes) may be
+// NULL.
 hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, size_t lds, hipStream_t s,
-                                std::string *log);
+                                std::string *log, SpecMemo *memo);
 hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nrows, hipStream_t s,
-                            std::string *log);
+                            std::string *log, SpecMemo *memo);
 hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int nrows, hipStream_t s,
-                                std::string *log);
+                                std::string *log, SpecMemo *memo);
 
 // Kernels tq_pauli_<pass> computing the expectations of one observable set
 // (the same on every row, at most 16 observables) pass by pass: each pass's
@@ -45,9 +58,9 @@ hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int 
 // partial[row][npass][wg_per_row][k_count].
 std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K);
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
-                             std::string *log);
+                             std::string *log, SpecMemo *memo);
 // Workgroups of a specialised Pauli pass that fit on the device at once (0 if unknown).
-int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log);
+int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo);
 
 // Compile the specialised kernels of group g (the resident kernel, or the
 // forward and reverse pass kernels) ahead of their first launch: for the current device when

@@ -92,6 +92,7 @@ struct ObsGroupDev {
     // (specialize = 1, every row the same terms, tiles that hold every X mask)
     std::vector<PauliPass> spec_passes;
     std::string spec_src;
+    SpecMemo spec_memo;
     void release()
     {
         for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
@@ -111,6 +112,8 @@ struct GroupDev {
     int n_fwd_stages = 0, n_rev_stages = 0, n_dense = 0;
     size_t psi_off = 0;  // amplitude offset of this group's rows in the state workspaces
     size_t mat_off = 0;  // offset in the matrix workspace
+    // specialised kernels of the group: the resident kernel, the tile passes
+    SpecMemo res_memo, pass_memo;
 };
 
 } // namespace
@@ -296,7 +299,7 @@ void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const i
         a.mat_end = ps.mat_end;
         if (p->pd->opt.specialize) {
             std::string log;
-            const hipError_t e = launch_pass_spec(g, (int)pi, a, nrows, s, &log);
+            const hipError_t e = launch_pass_spec(g, (int)pi, a, nrows, s, &log, &gd.pass_memo);
             if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
             hip_check(e, "specialised pass launch");
             continue;
@@ -491,7 +494,7 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
     const int nrows = (int)g.rows.size();
     const int npass = (int)og.spec_passes.size();
     std::string log;
-    int fit = pauli_spec_slots(og.spec_src, og.spec_passes[0].geom, &log);
+    int fit = pauli_spec_slots(og.spec_src, og.spec_passes[0].geom, &log, &og.spec_memo);
     if (fit <= 0) {
         if (!log.empty()) fail(TQ_E_DEVICE, log);
         fit = 2048;
@@ -508,7 +511,7 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
     for (int pi = 0; pi < npass; pi++) {
         a.g = og.spec_passes[pi].geom;
         a.pass = pi;
-        const hipError_t e = launch_pauli_spec(og.spec_src, pi, a, nrows, s, &log);
+        const hipError_t e = launch_pauli_spec(og.spec_src, pi, a, nrows, s, &log, &og.spec_memo);
         if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
         hip_check(e, "specialised Pauli launch");
     }
@@ -620,7 +623,7 @@ void run_resident(tq_program p, size_t gi, const ResArgs &a, hipStream_t s)
     const size_t lds = resident_lds_bytes(a.n, a.nacc, a.grad != nullptr);
     if (p->pd->opt.specialize && lds <= kResidentSpecLds) {
         std::string log;
-        const hipError_t e = launch_resident_spec(g, a, nrows, lds, s, &log);
+        const hipError_t e = launch_resident_spec(g, a, nrows, lds, s, &log, &p->gdev[gi]->res_memo);
         if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
         hip_check(e, "specialised resident launch");
         return;
@@ -943,7 +946,7 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                 gbase += gc;
                 if (pd.opt.specialize) {
                     std::string log;
-                    const hipError_t e = launch_rev_pass_spec(g, (int)pi, r, nrows, s, &log);
+                    const hipError_t e = launch_rev_pass_spec(g, (int)pi, r, nrows, s, &log, &gd.pass_memo);
                     if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
                     hip_check(e, "specialised reverse pass launch");
                     continue;
