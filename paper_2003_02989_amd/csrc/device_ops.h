@@ -37,6 +37,15 @@ __device__ __forceinline__ double2 zmul2(double2 m0, double2 a0, double2 m1, dou
     return make_double2(m0.x * a0.x - m0.y * a0.y + m1.x * a1.x - m1.y * a1.y,
                         m0.x * a0.y + m0.y * a0.x + m1.x * a1.y + m1.y * a1.x);
 }
+// m0 a0 + m1 a1 + m2 a2 + m3 a3: one multiply and seven FMAs per component
+__device__ __forceinline__ double2 zmul4(double2 m0, double2 a0, double2 m1, double2 a1, double2 m2, double2 a2,
+                                         double2 m3, double2 a3)
+{
+    return make_double2(m0.x * a0.x - m0.y * a0.y + m1.x * a1.x - m1.y * a1.y + m2.x * a2.x - m2.y * a2.y +
+                            m3.x * a3.x - m3.y * a3.y,
+                        m0.x * a0.y + m0.y * a0.x + m1.x * a1.y + m1.y * a1.x + m2.x * a2.y + m2.y * a2.x +
+                            m3.x * a3.y + m3.y * a3.x);
+}
 __device__ __forceinline__ double2 zadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
 // Re(conj(a) b)
 __device__ __forceinline__ double zdotr(double2 a, double2 b) { return a.x * b.x + a.y * b.y; }
@@ -196,10 +205,10 @@ __device__ __forceinline__ Quad p2_apply(double2 a, double2 b, double sg, const 
 {
     const double2 bs = make_double2(sg * b.x, sg * b.y);
     Quad o;
-    o.v00 = zadd(zmul(a, v.v00), zmul(bs, v.v11));
-    o.v11 = zadd(zmul(a, v.v11), zmul(bs, v.v00));
-    o.v01 = zadd(zmul(a, v.v01), zmul(b, v.v10));
-    o.v10 = zadd(zmul(a, v.v10), zmul(b, v.v01));
+    o.v00 = zmul2(a, v.v00, bs, v.v11);
+    o.v11 = zmul2(a, v.v11, bs, v.v00);
+    o.v01 = zmul2(a, v.v01, b, v.v10);
+    o.v10 = zmul2(a, v.v10, b, v.v01);
     return o;
 }
 
@@ -458,10 +467,10 @@ template <int R, int LO, int HI, class MT> __device__ __forceinline__ void rm2(d
         if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
         const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
         const double2 v00 = a[k], v01 = a[k01], v10 = a[k10], v11 = a[k11];
-        a[k] = zadd(zmul2(m[0], v00, m[1], v01), zmul2(m[2], v10, m[3], v11));
-        a[k01] = zadd(zmul2(m[4], v00, m[5], v01), zmul2(m[6], v10, m[7], v11));
-        a[k10] = zadd(zmul2(m[8], v00, m[9], v01), zmul2(m[10], v10, m[11], v11));
-        a[k11] = zadd(zmul2(m[12], v00, m[13], v01), zmul2(m[14], v10, m[15], v11));
+        a[k] = zmul4(m[0], v00, m[1], v01, m[2], v10, m[3], v11);
+        a[k01] = zmul4(m[4], v00, m[5], v01, m[6], v10, m[7], v11);
+        a[k10] = zmul4(m[8], v00, m[9], v01, m[10], v10, m[11], v11);
+        a[k11] = zmul4(m[12], v00, m[13], v01, m[14], v10, m[15], v11);
     }
 }
 template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rm2_dot(const double2 *a, const double2 *f, MT m)
@@ -472,10 +481,10 @@ template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rm2
         if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
         const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
         const double2 v00 = a[k], v01 = a[k01], v10 = a[k10], v11 = a[k11];
-        s += zdotr(f[k], zadd(zmul2(m[0], v00, m[1], v01), zmul2(m[2], v10, m[3], v11)));
-        s += zdotr(f[k01], zadd(zmul2(m[4], v00, m[5], v01), zmul2(m[6], v10, m[7], v11)));
-        s += zdotr(f[k10], zadd(zmul2(m[8], v00, m[9], v01), zmul2(m[10], v10, m[11], v11)));
-        s += zdotr(f[k11], zadd(zmul2(m[12], v00, m[13], v01), zmul2(m[14], v10, m[15], v11)));
+        s += zdotr(f[k], zmul4(m[0], v00, m[1], v01, m[2], v10, m[3], v11));
+        s += zdotr(f[k01], zmul4(m[4], v00, m[5], v01, m[6], v10, m[7], v11));
+        s += zdotr(f[k10], zmul4(m[8], v00, m[9], v01, m[10], v10, m[11], v11));
+        s += zdotr(f[k11], zmul4(m[12], v00, m[13], v01, m[14], v10, m[15], v11));
     }
     return s;
 }
@@ -518,10 +527,10 @@ template <int R, int LO, int HI> __device__ __forceinline__ void rp2(double2 *a,
         if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
         const int kL = k | (1 << LO), kH = k | (1 << HI), k11 = kL | kH;
         const double2 v00 = a[k], vL = a[kL], vH = a[kH], v11 = a[k11];
-        a[k] = zadd(zmul(ca, v00), zmul(bs, v11));
-        a[k11] = zadd(zmul(ca, v11), zmul(bs, v00));
-        a[kL] = zadd(zmul(ca, vL), zmul(cb, vH));
-        a[kH] = zadd(zmul(ca, vH), zmul(cb, vL));
+        a[k] = zmul2(ca, v00, bs, v11);
+        a[k11] = zmul2(ca, v11, bs, v00);
+        a[kL] = zmul2(ca, vL, cb, vH);
+        a[kH] = zmul2(ca, vH, cb, vL);
     }
 }
 template <int R, int LO, int HI> __device__ __forceinline__ double rp2_dot(const double2 *a, const double2 *f, double2 ca, double2 cb, double sg)
@@ -532,10 +541,10 @@ template <int R, int LO, int HI> __device__ __forceinline__ double rp2_dot(const
     for (int k = 0; k < (1 << R); k++) {
         if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
         const int kL = k | (1 << LO), kH = k | (1 << HI), k11 = kL | kH;
-        s += zdotr(f[k], zadd(zmul(ca, a[k]), zmul(bs, a[k11])));
-        s += zdotr(f[k11], zadd(zmul(ca, a[k11]), zmul(bs, a[k])));
-        s += zdotr(f[kL], zadd(zmul(ca, a[kL]), zmul(cb, a[kH])));
-        s += zdotr(f[kH], zadd(zmul(ca, a[kH]), zmul(cb, a[kL])));
+        s += zdotr(f[k], zmul2(ca, a[k], bs, a[k11]));
+        s += zdotr(f[k11], zmul2(ca, a[k11], bs, a[k]));
+        s += zdotr(f[kL], zmul2(ca, a[kL], cb, a[kH]));
+        s += zdotr(f[kH], zmul2(ca, a[kH], cb, a[kL]));
     }
     return s;
 }

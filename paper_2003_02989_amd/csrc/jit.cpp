@@ -262,6 +262,106 @@ std::string gen_dot(const Env &e, const PassOp &op, int R, const std::vector<Gen
     return o.str();
 }
 
+bool is_diag(const PassOp &op) { return op.kind == K_D1 || op.kind == K_D2; }
+
+// The entry of diagonal op `op` (matrix at offset mat) that multiplies
+// register k of a stage, as an expression; "" when it is exactly 1.  Bits of
+// the op outside the stage select per item.
+std::string diag_entry(const Env &e, const PassOp &op, int mat, int k)
+{
+    const int um = op.hint & 0xf;
+    auto en = [&](int idx) { return ((um >> idx) & 1) ? std::string("make_double2(1.0, 0.0)") : ent(mat + idx); };
+    auto unit = [&](int idx) { return ((um >> idx) & 1) != 0; };
+    if (op.kind == K_D1) {
+        if (op.s0 != kFixed) {
+            const int idx = (k >> op.s0) & 1;
+            return unit(idx) ? "" : ent(mat + idx);
+        }
+        if (unit(0) && unit(1)) return "";
+        return "zsel(" + bit(e, op.l0, op.p0) + ", " + en(0) + ", " + en(1) + ")";
+    }
+    const bool r0 = op.s0 != kFixed, r1 = op.s1 != kFixed;
+    const int c0 = r0 ? (k >> op.s0) & 1 : 0, c1 = r1 ? (k >> op.s1) & 1 : 0;
+    if (r0 && r1) return unit(2 * c0 + c1) ? "" : ent(mat + 2 * c0 + c1);
+    if (r0) {
+        if (unit(2 * c0) && unit(2 * c0 + 1)) return "";
+        return "zsel(" + bit(e, op.l1, op.p1) + ", " + en(2 * c0) + ", " + en(2 * c0 + 1) + ")";
+    }
+    if (r1) {
+        if (unit(c1) && unit(2 + c1)) return "";
+        return "zsel(" + bit(e, op.l0, op.p0) + ", " + en(c1) + ", " + en(2 + c1) + ")";
+    }
+    if (unit(0) && unit(1) && unit(2) && unit(3)) return "";
+    const std::string b0 = bit(e, op.l0, op.p0), b1 = bit(e, op.l1, op.p1);
+    return "zsel(" + b0 + ", zsel(" + b1 + ", " + en(0) + ", " + en(1) + "), zsel(" + b1 + ", " + en(2) + ", " + en(3) +
+           "))";
+}
+
+// A run of consecutive diagonal ops of a stage as one diagonal: its entries
+// are multiplied together over the register bits the run touches (per item,
+// with the out-of-stage bits), then each register of the arrays `arrs` is
+// multiplied once.  Returns "" when op by op is no more expensive (complex
+// multiplies counted).
+std::string diag_run(const Env &e, const std::vector<const PassOp *> &run, int R, const std::vector<std::string> &arrs)
+{
+    int jm = 0;  // register bits the run touches
+    for (const PassOp *op : run) {
+        if (op->s0 != kFixed) jm |= 1 << op->s0;
+        if (op->kind == K_D2 && op->s1 != kFixed) jm |= 1 << op->s1;
+    }
+    std::vector<int> jb;
+    for (int j = 0; j < R; j++)
+        if ((jm >> j) & 1) jb.push_back(j);
+    const int NJ = 1 << jb.size(), NR = 1 << R;
+    auto rep = [&](int j) {  // a register index with the run's bits set as j says
+        int k = 0;
+        for (size_t i = 0; i < jb.size(); i++)
+            if ((j >> i) & 1) k |= 1 << jb[i];
+        return k;
+    };
+    auto proj = [&](int k) {
+        int j = 0;
+        for (size_t i = 0; i < jb.size(); i++)
+            if ((k >> jb[i]) & 1) j |= 1 << i;
+        return j;
+    };
+    std::vector<bool> one(NJ, true);
+    std::ostringstream b;
+    int fused = 0, direct = 0;
+    for (const PassOp *op : run) {
+        const int mat = op->mat - e.mbase;
+        for (int k = 0; k < NR; k++) direct += !diag_entry(e, *op, mat, k).empty();
+        for (int j = 0; j < NJ; j++) {
+            const std::string x = diag_entry(e, *op, mat, rep(j));
+            if (x.empty()) continue;
+            if (one[j]) {
+                b << "d" << j << "_ = " << x << "; ";
+                one[j] = false;
+            } else {
+                b << "d" << j << "_ = zmul(d" << j << "_, " << x << "); ";
+                fused++;
+            }
+        }
+    }
+    std::ostringstream a;
+    for (const std::string &v : arrs)
+        for (int k = 0; k < NR; k++)
+            if (!one[proj(k)]) {
+                a << v << "[" << k << "] = zmul(d" << proj(k) << "_, " << v << "[" << k << "]); ";
+                fused++;
+            }
+    if (fused >= direct * (int)arrs.size()) return "";
+    std::ostringstream o;
+    o << "{ double2";
+    for (int j = 0, first = 1; j < NJ; j++)
+        if (!one[j]) {
+            o << (first ? " " : ", ") << "d" << j << "_";
+            first = 0;
+        }
+    o << "; " << b.str() << a.str() << "}";
+    return o.str();
+}
+
 // item loop header of a stage: base index of the item and the swizzled
 // LDS offsets of its 2^R registers
 void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint32_t> &off)
@@ -299,6 +399,18 @@ void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
     } else {
         for (int oi = st.op_begin; oi < st.op_end; oi++) {
             const PassOp &op = ps.ops[oi - ps.op_offset];
+            if (is_diag(op)) {
+                std::vector<const PassOp *> run;
+                int oe = oi;
+                for (; oe < st.op_end && is_diag(ps.ops[oe - ps.op_offset]); oe++)
+                    run.push_back(&ps.ops[oe - ps.op_offset]);
+                const std::string c = run.size() > 1 ? diag_run(e, run, R, {"v"}) : "";
+                if (!c.empty()) {
+                    o << "        " << c << "\n";
+                    oi = oe - 1;
+                    continue;
+                }
+            }
             o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
         }
     }
@@ -328,6 +440,42 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
     int gk = 0;
     for (int oi = st.op_begin; oi < st.op_end; oi++) {
         const PassOp &op = ps.ops[oi - ps.op_offset];
+        // A run of diagonal ops whose gradients all come from diagonal
+        // generators: the ops commute with each other and with the
+        // generators, so Im<f|G|v> is the same before every op of the run;
+        // all its gradients are taken first, then the run is applied to v
+        // and f as one diagonal.
+        if (is_diag(op) && e.grp) {
+            std::vector<const PassOp *> run;
+            std::vector<std::string> dots;
+            int gkr = gk;
+            for (int oe = oi; oe < st.op_end && is_diag(ps.ops[oe - ps.op_offset]); oe++) {
+                const PassOp &ro = ps.ops[oe - ps.op_offset];
+                std::vector<std::string> od;
+                bool ok = true;
+                for (int j = 0; j < ro.ngrad && ok; j++) {
+                    std::vector<GenTerm> gt;
+                    ok = op_generator(*e.grp, ro, j, &gt);
+                    for (const GenTerm &tm : gt) ok = ok && tm.x == 0;
+                    const std::string c = ok ? gen_dot(e, ro, R, gt, "g[" + N(gkr + j) + "]") : "";
+                    ok = ok && !c.empty();
+                    od.push_back(c);
+                }
+                if (!ok) break;
+                run.push_back(&ro);
+                dots.insert(dots.end(), od.begin(), od.end());
+                gkr += ro.ngrad;
+            }
+            const std::string c = run.size() > 1 ? diag_run(e, run, R, {"v", "f"}) : "";
+            if (!c.empty()) {
+                for (const std::string &d : dots) o << "        " << d << "\n";
+                o << "        " << c << "\n";
+                o << "        __builtin_amdgcn_sched_barrier(0);\n";
+                gk = gkr;
+                oi = oi + (int)run.size() - 1;
+                continue;
+            }
+        }
         // gradients from the gate's generator on the registers before the op
         // (no derivative matrix read), else Re(conj(f) dW v) after W^dagger v
         std::vector<std::string> gd;
