@@ -393,6 +393,21 @@ template <int R, int J, class MT> __device__ __forceinline__ void rm1r(double2 *
         a[kk] = make_double2(fma(m10, x.x, m11 * y.x), fma(m10, x.y, m11 * y.y));
     }
 }
+// dense 2x2 with real diagonal and imaginary off-diagonal entries (RX and its
+// products; their real parts, resp. imaginary parts, are exactly 0) on
+// register bit J: half the arithmetic of rm1
+template <int R, int J, class MT> __device__ __forceinline__ void rm1x(double2 *a, MT m)
+{
+    const double d0 = m[0].x, o01 = m[1].y, o10 = m[2].y, d1 = m[3].x;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        const double2 x = a[k], y = a[kk];
+        a[k] = make_double2(fma(d0, x.x, -o01 * y.y), fma(d0, x.y, o01 * y.x));
+        a[kk] = make_double2(fma(d1, y.x, -o10 * x.y), fma(d1, y.y, o10 * x.x));
+    }
+}
 template <int R, int J, class MT> __device__ __forceinline__ double rm1r_dot(const double2 *a, const double2 *f, MT dm)
 {
     const double m00 = dm[0].x, m01 = dm[1].x, m10 = dm[2].x, m11 = dm[3].x;
@@ -502,6 +517,28 @@ template <int R, int LO, int HI, class MT> __device__ __forceinline__ void rf2(d
         a[k01] = zmul2(b00, v01, b01, v10);
         a[k10] = zmul2(b10, v01, b11, v10);
         a[k11] = zmul(p11, a[k11]);
+    }
+}
+// rf2 for an op whose structure holds for every parameter value: bit 0 / bit
+// 3 of U: the |00> / |11> phase is exactly 1 (left out); RX: the block has
+// real diagonal and imaginary off-diagonal entries (fSim)
+template <int R, int LO, int HI, int U, bool RX, class MT> __device__ __forceinline__ void rf2x(double2 *a, MT m)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        const double2 x = a[k01], y = a[k10];
+        if (!(U & 1)) a[k] = zmul(m[0], a[k]);
+        if (RX) {
+            const double b00 = m[1].x, b01 = m[2].y, b10 = m[3].y, b11 = m[4].x;
+            a[k01] = make_double2(fma(b00, x.x, -b01 * y.y), fma(b00, x.y, b01 * y.x));
+            a[k10] = make_double2(fma(b11, y.x, -b10 * x.y), fma(b11, y.y, b10 * x.x));
+        } else {
+            a[k01] = zmul2(m[1], x, m[2], y);
+            a[k10] = zmul2(m[3], x, m[4], y);
+        }
+        if (!(U & 8)) a[k11] = zmul(m[5], a[k11]);
     }
 }
 template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rf2_dot(const double2 *a, const double2 *f, MT m)

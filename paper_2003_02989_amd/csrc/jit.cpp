@@ -131,12 +131,17 @@ std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::str
     switch (op.kind) {
     case K_M1:
         if (!op.ctrl && (op.hint & kHintReal)) return "rm1r<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
+        if (!op.ctrl && (op.hint & kHintRX)) return "rm1x<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (!op.ctrl) return "rm1<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ");";
         if (op.s1 != kFixed) return "rm1c<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
         return "rm1_on<" + Rs + ", " + N(op.s0) + ">(" + v + ", " + m + ", " + bit(e, op.l1, op.p1) + " == " +
                N(op.cval) + "u);";
     case K_M2: return "rm2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
-    case K_F2: return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
+    case K_F2:
+        if (op.hint & (9 | kHintRX))
+            return "rf2x<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ", " + N(op.hint & 9) + ", " +
+                   ((op.hint & kHintRX) ? "true" : "false") + ">(" + v + ", " + m + ");";
+        return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_P2:
         return "rp2<" + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " + N(std::max(op.s0, op.s1)) + ">(" + v + ", " +
                ent(mat) + ", " + ent(mat + 1) + ", " + (op.ptype == 2 ? "-1.0" : "1.0") + ");";
@@ -565,7 +570,8 @@ std::string pass_kernel_source(const Group &g, int pass)
     {
         const Pass &ps = g.fwd[pass];
         const TileGeom &gm = ps.geom;
-        o << "extern \"C\" __global__ __launch_bounds__(256) void tq_fwd_" << pass
+        // at most 128 registers: four workgroups of the tile's LDS share a CU
+        o << "extern \"C\" __global__ __launch_bounds__(256, 4) void tq_fwd_" << pass
           << "(PassArgs a)\n{\n"
              "    extern __shared__ __align__(16) unsigned char smem[];\n"
              "    const PassCtx c = pass_setup(a, smem);\n"

@@ -321,14 +321,14 @@ bool uniform(const PassOp &op, const std::vector<int> &bits)
 }
 
 // fp64-instruction equivalents per amplitude of one op in a register stage
-int op_cost(const PassOp &op)
+int op_cost(const PassOp &op, int dispatch)
 {
     int c = 4;
-    if (op.kind == K_M1) c = op.ctrl ? 4 : 8;
+    if (op.kind == K_M1) c = op.ctrl || (op.hint & (kHintReal | kHintRX)) ? 4 : 8;
     if (op.kind == K_M2) c = 16;
-    if (op.kind == K_F2) c = 6;
+    if (op.kind == K_F2) c = (op.hint & kHintRX) ? 4 : 6;
     if (op.kind == K_P2) c = 8;
-    return c + kOpDispatchCost;
+    return c + dispatch;
 }
 
 struct Packing {
@@ -345,7 +345,7 @@ struct Packing {
 // Greedy packing.  commute: use the commutation of diagonal ops (else ops
 // sharing any qubit keep their order); soft_first: grow R with the bits that
 // make an op uniform, and take uniform ops before per-item ones.
-Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first, bool forward)
+Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first, bool forward, int dispatch)
 {
     const int t = ps.geom.t;
     const int r = std::min(rmax, t);
@@ -463,7 +463,7 @@ Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first
         int ops = 0;
         bool uni = forward;
         for (int i = begin; i < st.end; i++) {
-            ops += op_cost(ps.ops[P.order[i]]);
+            ops += op_cost(ps.ops[P.order[i]], dispatch);
             uni = uni && uniform(ps.ops[P.order[i]], st.bits);
         }
         P.cost += kStageCost + (uni ? std::min(ops, 4 << (int)st.bits.size()) : ops);
@@ -475,14 +475,15 @@ Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first
 
 } // namespace stages
 
-void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at, bool forward)
+void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_t, int> &task_at, bool forward,
+                 int dispatch)
 {
     const int nops = (int)ps.ops.size();
     ps.stages.clear();
     stages::Packing best;
     bool first = true;
     for (int v = 0; v < 4; v++) {
-        stages::Packing P = stages::pack(ps, rmax, rdense, v & 1, v & 2, forward);
+        stages::Packing P = stages::pack(ps, rmax, rdense, v & 1, v & 2, forward, dispatch);
         if (first || P.cost < best.cost) best = std::move(P);
         first = false;
     }
@@ -550,10 +551,11 @@ bool stage_fusable(const Pass &ps, const Stage &st)
 // Dense stage cost (fp64 instructions per amplitude: a 2^r x 2^r complex
 // matvec, 4 per entry of a row) against the ops' own costs plus their
 // dispatch overhead.
-bool dense_pays(const Pass &ps, const Stage &st)
+bool dense_pays(const Pass &ps, const Stage &st, int dispatch)
 {
     int ops = 0;
-    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++) ops += stages::op_cost(ps.ops[k]);
+    for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++)
+        ops += stages::op_cost(ps.ops[k], dispatch);
     return (4 << st.r) < ops;
 }
 
@@ -613,8 +615,21 @@ uint8_t gate_hint(int op, bool cblock)
     case OP_X: return kHintX | kHintReal;
     case OP_CNOT: return cblock ? kHintX | kHintReal : 0;
     case OP_RY: case OP_H: return kHintReal;  // real for every angle, and so is dRY/dtheta
+    case OP_RX: return kHintRX;               // cos on the diagonal, -i sin off it
     default: return 0;
     }
+}
+
+// The K_F2 hint of one member gate: fSim keeps 1 on |00> and an RX-form
+// block; SWAP keeps 1 on |00> and |11>; a diagonal gate keeps its unit
+// entries on |00> and |11>, and the block's form when its |01> and |10>
+// entries are exactly 1.
+uint8_t f2_member_hint(int op)
+{
+    if (op == OP_FSIM) return 1 | kHintRX;
+    if (op == OP_SWAP) return 1 | 8;
+    const uint8_t u = gate_hint(op, false) & 0xf;
+    return (u & 9) | ((u & 6) == 6 ? kHintRX : 0);
 }
 
 // The hint of an op fusing `mem`: entries that are 1 in every member stay 1;
@@ -626,9 +641,15 @@ uint8_t op_hint(const Group &g, const PassOp &op, const std::vector<Member> &mem
         for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, false) & 0xf;
         return h;
     }
+    if (op.kind == K_F2) {
+        uint8_t h = 1 | 8 | kHintRX;
+        for (const Member &m : mem) h &= f2_member_hint(g.gates[m.gate].op);
+        return h;
+    }
     if (op.kind == K_M1) {
-        // a product of real matrices is real; an X stays X only alone
-        uint8_t h = kHintReal;
+        // a product of real matrices is real, of RX-form matrices RX-form; an
+        // X stays X only alone
+        uint8_t h = kHintReal | kHintRX;
         for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, m.form == FORM_CBLOCK);
         if (mem.size() == 1) h |= gate_hint(g.gates[mem[0].gate].op, mem[0].form == FORM_CBLOCK) & kHintX;
         return h;
@@ -882,15 +903,16 @@ void plan_group(Group &g, const Options &opt, int S)
     std::map<int32_t, int> task_at;
     for (int i = 0; i < (int)g.tasks.size(); i++) task_at[g.tasks[i].out] = i;
     int off = 0;
+    const int dispatch = opt.specialize ? kOpDispatchCostSpec : kOpDispatchCost;
     for (Pass &ps : g.fwd) {
         ps.op_offset = off;
-        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at, true);
+        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at, true, dispatch);
         off += (int)ps.ops.size();
         // forward stages whose ops act alike on every item become one dense
         // matrix when that is cheaper than the ops one by one (matrix
         // entries appended to the row block, built after the op matrices)
         for (Stage &st : ps.stages) {
-            if (!stage_fusable(ps, st) || !dense_pays(ps, st)) continue;
+            if (!stage_fusable(ps, st) || !dense_pays(ps, st, dispatch)) continue;
             st.dense = 1;
             st.mat = g.mat_block;
             g.mat_block += 1 << (2 * st.r);
@@ -900,7 +922,7 @@ void plan_group(Group &g, const Options &opt, int S)
     off = 0;
     for (Pass &ps : g.rev) {
         ps.op_offset = off;
-        make_stages(ps, rev_stage_bits(n, opt), kRevDense2Bits, g, task_at, false);
+        make_stages(ps, rev_stage_bits(n, opt), kRevDense2Bits, g, task_at, false, dispatch);
         off += (int)ps.ops.size();
     }
 

@@ -82,6 +82,9 @@ struct Group {
 // Per-op dispatch overhead of the register ops, in fp64-instruction
 // equivalents per amplitude (measured: ~6 for 2x2 ops at three register bits).
 constexpr int kOpDispatchCost = 6;
+// The same for kernels generated for the circuit structure, whose ops are
+// straight-line code (no table reads or dispatch; a register move or two).
+constexpr int kOpDispatchCostSpec = 1;
 // One register stage's LDS round trip in the same units (measured: ~0.29 ms
 // per stage of a 2^30-amplitude pass).
 constexpr int kStageCost = 11;

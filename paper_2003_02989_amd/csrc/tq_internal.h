@@ -82,6 +82,9 @@ enum OpKind : uint8_t {
 
 constexpr uint8_t kHintX = 16;
 constexpr uint8_t kHintReal = 32;  // K_M1: the matrix and its derivatives are real
+// K_M1: real diagonal and imaginary off-diagonal entries (RX and its products;
+// so are the derivatives); K_F2: the (|01>, |10>) block has that form (fSim)
+constexpr uint8_t kHintRX = 64;
 struct PassOp {
     uint8_t kind;
     uint8_t l0, l1;   // local bit of q0 / q1 in the tile, kFixed if outside
@@ -93,7 +96,9 @@ struct PassOp {
     uint8_t s0, s1;   // register index of q0 / q1 within the op's stage, kFixed if not in it
     uint8_t hint;     // structure every parameter value keeps: K_D1 / K_D2 bit k (k < 4): diagonal
                       // entry k of the matrix is exactly 1 (and of dW/deta exactly 0); K_M1
-                      // kHintX: the matrix is exactly X (a swap); kHintReal: it is real
+                      // kHintX: the matrix is exactly X (a swap); kHintReal: it is real;
+                      // kHintRX (K_M1, K_F2) as above; K_F2 bit 0 / bit 3: the phase on
+                      // |00> / |11> is exactly 1
     int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
     int32_t dmat[2];  // reverse: offsets of dW/deta_j
     int32_t gslot[2]; // reverse: gradient slot ids
