@@ -570,6 +570,22 @@ template <int R, int LO, int HI> __device__ __forceinline__ void rp2(double2 *a,
         a[kH] = zmul2(ca, vH, cb, vL);
     }
 }
+// rp2 with a real and b imaginary (XX^t without its global phase, and its
+// products): half the arithmetic
+template <int R, int LO, int HI> __device__ __forceinline__ void rp2x(double2 *a, double2 ca, double2 cb, double sg)
+{
+    const double p = ca.x, q = cb.y, qs = sg * cb.y;
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int kL = k | (1 << LO), kH = k | (1 << HI), k11 = kL | kH;
+        const double2 v00 = a[k], vL = a[kL], vH = a[kH], v11 = a[k11];
+        a[k] = make_double2(fma(p, v00.x, -qs * v11.y), fma(p, v00.y, qs * v11.x));
+        a[k11] = make_double2(fma(p, v11.x, -qs * v00.y), fma(p, v11.y, qs * v00.x));
+        a[kL] = make_double2(fma(p, vL.x, -q * vH.y), fma(p, vL.y, q * vH.x));
+        a[kH] = make_double2(fma(p, vH.x, -q * vL.y), fma(p, vH.y, q * vL.x));
+    }
+}
 template <int R, int LO, int HI> __device__ __forceinline__ double rp2_dot(const double2 *a, const double2 *f, double2 ca, double2 cb, double sg)
 {
     const double2 bs = make_double2(sg * cb.x, sg * cb.y);

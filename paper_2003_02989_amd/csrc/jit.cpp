@@ -143,8 +143,9 @@ std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::str
                    ((op.hint & kHintRX) ? "true" : "false") + ">(" + v + ", " + m + ");";
         return "rf2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_P2:
-        return "rp2<" + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " + N(std::max(op.s0, op.s1)) + ">(" + v + ", " +
-               ent(mat) + ", " + ent(mat + 1) + ", " + (op.ptype == 2 ? "-1.0" : "1.0") + ");";
+        return std::string((op.hint & kHintRX) ? "rp2x<" : "rp2<") + Rs + ", " + N(std::min(op.s0, op.s1)) + ", " +
+               N(std::max(op.s0, op.s1)) + ">(" + v + ", " + ent(mat) + ", " + ent(mat + 1) + ", " +
+               (op.ptype == 2 ? "-1.0" : "1.0") + ");";
     default: return diag_call(e, op, R, mat, false, v) + ";";
     }
 }
@@ -185,6 +186,10 @@ std::string gen_dot(const Env &e, const PassOp &op, int R, const std::vector<Gen
     const bool r0 = op.s0 != kFixed, r1 = op.s1 != kFixed;
     std::map<std::tuple<int, int, int>, std::array<double, 4>> ent;  // (k, k', re) -> coefficient per (b0, b1)
     for (const GenTerm &tm : terms) {
+        // an identity term adds c Im<f|v>, which vanishes: f and v have been
+        // transformed by the same unitaries since f = H_g v (H_g Hermitian),
+        // so <f|v> = <psi|H_g|psi> is real
+        if (tm.x == 0 && tm.z == 0) continue;
         int xr = 0;
         if (tm.x & 1) {
             if (!r0) return "";

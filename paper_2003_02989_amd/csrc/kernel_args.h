@@ -25,6 +25,12 @@ struct BuildArgs {
     const int32_t *rows;
     double2 *mats;
     int64_t mat_stride;
+    // the task writing this matrix offset (the first qubit's product-init
+    // matrix; the first task of the range) also multiplies it by the row's
+    // global phase, the sum of the phases the gate matrices leave out; -1: none
+    int32_t phase_out;
+    int32_t n_phase;
+    const PhaseTerm *phase_terms;
 };
 
 struct StageBuildArgs {

@@ -25,6 +25,19 @@ namespace tq {
 // involutory generator G, G^t = (1+w)/2 I + (1-w)/2 G with w = e^{i pi t}
 // (the phase convention e^{i pi t/2}(cos(pi t/2) I - i sin(pi t/2) G)), and a
 // rotation exp(-i theta G / 2) = cos(theta/2) I - i sin(theta/2) G.
+//
+// Gates whose matrix is a global phase times a matrix of simpler form are
+// built without that phase: RZ(theta) = e^{-i theta/2} diag(1, e^{i theta}),
+// RZZ(gamma) = e^{-i gamma/2} diag(1, e^{i gamma}, e^{i gamma}, 1) (entries
+// exactly 1), X^t, sqrt X, XX^t = e^{i pi t/2}(cos I - i sin G) (real
+// diagonal, imaginary off-diagonal), Y^t, sqrt Y = e^{i pi t/2}(cos I - i sin
+// Y) (real); YY^t keeps its phase.  The phases of a row sum to one global
+// phase, a linear form in the parameters that the planner lists per group
+// (PhaseTerm), which the builder multiplies into the first qubit's
+// product-init matrix:
+// states and amplitudes come out with the gates' own phases, while every
+// intermediate state differs from its phased counterpart by a global phase
+// alone, which no expectation, gradient or probability sees.
 struct cd {
     double x, y;
 };
@@ -50,18 +63,23 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
         sincos(eta[0] * 0.5, &s, &c);
         m[0] = C(c, 0); m[1] = C(-s, 0); m[2] = C(s, 0); m[3] = C(c, 0); return 2;
     case OP_RZ:
-        sincos(eta[0] * 0.5, &s, &c);
-        m[0] = C(c, -s); m[3] = C(c, s); return 2;
-    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_SQRTX: case OP_SQRTY: case OP_SQRTW: {
-        double t = (op == OP_SQRTX || op == OP_SQRTY || op == OP_SQRTW) ? 0.5 : eta[0];
+        sincos(eta[0], &s, &c);
+        m[0] = C(1, 0); m[3] = C(c, s); return 2;
+    case OP_XPOW: case OP_SQRTX: case OP_YPOW: case OP_SQRTY: {
+        sincospi(0.5 * (op == OP_XPOW || op == OP_YPOW ? eta[0] : 0.5), &s, &c);
+        m[0] = m[3] = C(c, 0);
+        if (op == OP_XPOW || op == OP_SQRTX) { m[1] = m[2] = C(0, -s); }
+        else { m[1] = C(-s, 0); m[2] = C(s, 0); }
+        return 2;
+    }
+    case OP_ZPOW: case OP_SQRTW: {
+        double t = op == OP_SQRTW ? 0.5 : eta[0];
         sincospi(t, &s, &c);
         cd a = C(0.5 * (1 + c), 0.5 * s);   // (1 + w) / 2
         cd bq = C(0.5 * (1 - c), -0.5 * s); // (1 - w) / 2
         if (op == OP_ZPOW) { m[0] = C(1, 0); m[3] = C(c, s); return 2; }
         m[0] = a; m[3] = a;
-        if (op == OP_XPOW || op == OP_SQRTX) { m[1] = bq; m[2] = bq; }
-        else if (op == OP_YPOW || op == OP_SQRTY) { m[1] = cdmul(bq, C(0, -1)); m[2] = cdmul(bq, C(0, 1)); }
-        else { m[1] = cdmul(bq, C(r, -r)); m[2] = cdmul(bq, C(r, r)); } // W = [[0, e^{-i pi/4}], [e^{i pi/4}, 0]]
+        m[1] = cdmul(bq, C(r, -r)); m[2] = cdmul(bq, C(r, r)); // W = [[0, e^{-i pi/4}], [e^{i pi/4}, 0]]
         return 2;
     }
     case OP_CZ:
@@ -78,20 +96,25 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
         if (form == FORM_CBLOCK) { m[0] = m[3] = a; m[1] = m[2] = bq; return 2; }
         m[0] = m[5] = C(1, 0); m[10] = m[15] = a; m[11] = m[14] = bq; return 4;
     }
-    case OP_XXPOW: case OP_YYPOW: {
+    case OP_XXPOW: {
+        sincospi(0.5 * eta[0], &s, &c);
+        m[0] = m[5] = m[10] = m[15] = C(c, 0);
+        m[3] = m[6] = m[9] = m[12] = C(0, -s);
+        return 4;
+    }
+    case OP_YYPOW: {  // with its phase: (1+w)/2 I + (1-w)/2 YY
         sincospi(eta[0], &s, &c);
-        cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
+        const cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
         m[0] = m[5] = m[10] = m[15] = a;
-        if (op == OP_XXPOW) { m[3] = m[6] = m[9] = m[12] = bq; }
-        else { m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq; } // YY: -|11><00| - |00><11| + |10><01| + |01><10|
+        m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq;  // YY: -|11><00| - |00><11| + |10><01| + |01><10|
         return 4;
     }
     case OP_ZZPOW:
         sincospi(eta[0], &s, &c);
         m[0] = m[15] = C(1, 0); m[5] = m[10] = C(c, s); return 4;
     case OP_RZZ:
-        sincos(eta[0] * 0.5, &s, &c);
-        m[0] = m[15] = C(c, -s); m[5] = m[10] = C(c, s); return 4;
+        sincos(eta[0], &s, &c);
+        m[0] = m[15] = C(1, 0); m[5] = m[10] = C(c, s); return 4;
     case OP_FSIM:
         sincos(eta[0], &s, &c);
         m[0] = C(1, 0); m[5] = m[10] = C(c, 0); m[6] = m[9] = C(0, -s);
@@ -121,29 +144,35 @@ __device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int whi
     case OP_RY:
         sincos(eta[0] * 0.5, &s, &c);
         m[0] = C(-0.5 * s, 0); m[1] = C(-0.5 * c, 0); m[2] = C(0.5 * c, 0); m[3] = C(-0.5 * s, 0); return 2;
-    case OP_RZ:
-        sincos(eta[0] * 0.5, &s, &c);
-        m[0] = C(-0.5 * s, -0.5 * c); m[3] = C(-0.5 * s, 0.5 * c); return 2;
+    case OP_RZ:  // d/dtheta diag(1, e^{i theta})
+        sincos(eta[0], &s, &c);
+        m[3] = C(-s, c); return 2;
     case OP_RZZ:
-        sincos(eta[0] * 0.5, &s, &c);
-        m[0] = m[15] = C(-0.5 * s, -0.5 * c); m[5] = m[10] = C(-0.5 * s, 0.5 * c); return 4;
-    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW:
-    case OP_XXPOW: case OP_YYPOW: case OP_ZZPOW: {
+        sincos(eta[0], &s, &c);
+        m[5] = m[10] = C(-s, c); return 4;
+    case OP_XPOW: case OP_YPOW: case OP_XXPOW: {
+        // d/dt (cos(pi t/2) I - i sin(pi t/2) G) = (pi/2)(-sin I - i cos G)
+        sincospi(0.5 * eta[0], &s, &c);
+        const cd a = C(-0.5 * pi * s, 0), bq = C(0, -0.5 * pi * c);
+        switch (op) {
+        case OP_XPOW: m[0] = m[3] = a; m[1] = m[2] = bq; return 2;
+        case OP_YPOW: m[0] = m[3] = a; m[1] = C(-0.5 * pi * c, 0); m[2] = C(0.5 * pi * c, 0); return 2;
+        default: m[0] = m[5] = m[10] = m[15] = a; m[3] = m[6] = m[9] = m[12] = bq; return 4;
+        }
+    }
+    case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW: case OP_ZZPOW: case OP_YYPOW: {
         // d/dt G^t = (i pi w / 2)(I - G), w = e^{i pi t}
         sincospi(eta[0], &s, &c);
         cd k = C(-0.5 * pi * s, 0.5 * pi * c);  // i pi w / 2
         cd mk = cdscale(k, -1);
         switch (op) {
-        case OP_XPOW: m[0] = m[3] = k; m[1] = m[2] = mk; return 2;
-        case OP_YPOW: m[0] = m[3] = k; m[1] = cdmul(mk, C(0, -1)); m[2] = cdmul(mk, C(0, 1)); return 2;
         case OP_ZPOW: m[3] = cdscale(k, 2); return 2;
         case OP_CZPOW: m[15] = cdscale(k, 2); return 4;
         case OP_CNOTPOW:
             if (form == FORM_CBLOCK) { m[0] = m[3] = k; m[1] = m[2] = mk; return 2; }
             m[10] = m[15] = k; m[11] = m[14] = mk; return 4;
-        case OP_XXPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[6] = m[9] = m[12] = mk; return 4;
-        case OP_YYPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[12] = k; m[6] = m[9] = mk; return 4;
         case OP_ZZPOW: m[5] = m[10] = cdscale(k, 2); return 4;
+        case OP_YYPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[12] = k; m[6] = m[9] = mk; return 4;
         }
         return 0;
     }
@@ -185,6 +214,17 @@ struct BuildCtx {
     const float *theta;         // this row's symbol values
 };
 
+// symbol resolution eta = scale*theta + offset (or the constant) of a parameter slot
+__device__ __forceinline__ double slot_value(const BuildCtx &c, int slot)
+{
+    const int sy = c.slot_sym[slot];
+    return sy >= 0 ? c.scale[slot] * (double)c.theta[sy] + c.off[slot] : c.off[slot];
+}
+__device__ __forceinline__ void resolve(const BuildCtx &c, const GateDev &gd, double *eta)
+{
+    for (int j = 0; j < gd.np; j++) eta[j] = slot_value(c, gd.slot0 + j);
+}
+
 // One build task for one row: symbol resolution eta = scale*theta + offset
 // and the fused product / dagger / derivative, all in float64.  D is the
 // matrix dimension; fixed at compile time so every array stays in registers.
@@ -199,11 +239,7 @@ template <int D> __device__ __forceinline__ void build_task_d(const BuildTask &b
         const Member mem = c.members[bt.mem_begin + mi];
         const GateDev gd = c.gates[mem.gate];
         double eta[2] = {0, 0};
-        for (int j = 0; j < gd.np; j++) {
-            const int slot = gd.slot0 + j;
-            const int sy = c.slot_sym[slot];
-            eta[j] = sy >= 0 ? c.scale[slot] * (double)c.theta[sy] + c.off[slot] : c.off[slot];
-        }
+        resolve(c, gd, eta);
         const double *ex = gd.explicit_ >= 0 ? c.explicit_mats + 32 * gd.explicit_ : nullptr;
 #pragma unroll
         for (int i = 0; i < 16; i++) g[i] = C(0, 0);
@@ -265,14 +301,39 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
 {
     const int row = blockIdx.y;
     const int ti = blockIdx.x * blockDim.x + threadIdx.x + a.task_begin;
-    if (ti >= a.task_end) return;
-    const BuildTask bt = a.tasks[ti];
     const int b = cget(a.rows, row);
     BuildCtx c{a.members, a.gates, a.slot_sym,
                a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots),
                a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots), a.explicit_mats,
                a.theta + (int64_t)b * a.S};
-    build_task(bt, c, a.mats + (int64_t)row * a.mat_stride + bt.out);
+    if (ti < a.task_end) {
+        const BuildTask bt = a.tasks[ti];
+        build_task(bt, c, a.mats + (int64_t)row * a.mat_stride + bt.out);
+    }
+    if (a.phase_out < 0 || blockIdx.x != 0) return;
+    // the row's global phase (block 0 of the row; its thread 0 built the
+    // product-init matrix at phase_out), reduced in a fixed order
+    __shared__ double part[256];
+    double ph = 0.0;
+    for (int j = threadIdx.x; j < a.n_phase; j += blockDim.x) {
+        const PhaseTerm pt = a.phase_terms[j];
+        ph += pt.slot >= 0 ? pt.c * slot_value(c, pt.slot) : pt.c;
+    }
+    part[threadIdx.x] = ph;
+    __syncthreads();
+    for (int h = blockDim.x / 2; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        double s, co;
+        sincos(part[0], &s, &co);
+        double2 *out = a.mats + (int64_t)row * a.mat_stride + a.phase_out;
+        for (int i = 0; i < 4; i++) {
+            const double2 v = out[i];
+            out[i] = make_double2(co * v.x - s * v.y, co * v.y + s * v.x);
+        }
+    }
 }
 
 __global__ __launch_bounds__(64) void k_build_stage(StageBuildArgs a)

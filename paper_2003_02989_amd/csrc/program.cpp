@@ -609,13 +609,16 @@ int storage_of(const PassOp &op)
 uint8_t gate_hint(int op, bool cblock)
 {
     switch (op) {
-    case OP_Z: case OP_ZPOW: return 1;           // diag(1, .)
-    case OP_CZ: case OP_CZPOW: return 1 | 2 | 4;  // diag(1, 1, 1, .)
-    case OP_ZZPOW: return 1 | 8;                 // diag(1, ., ., 1)
+    case OP_Z: case OP_ZPOW: case OP_RZ: return 1;  // diag(1, .) (RZ without its global phase)
+    case OP_CZ: case OP_CZPOW: return 1 | 2 | 4;     // diag(1, 1, 1, .)
+    case OP_ZZPOW: case OP_RZZ: return 1 | 8;        // diag(1, ., ., 1)
     case OP_X: return kHintX | kHintReal;
     case OP_CNOT: return cblock ? kHintX | kHintReal : 0;
     case OP_RY: case OP_H: return kHintReal;  // real for every angle, and so is dRY/dtheta
     case OP_RX: return kHintRX;               // cos on the diagonal, -i sin off it
+    // power gates without their global phase e^{i pi t/2}: cos I - i sin G
+    case OP_XPOW: case OP_SQRTX: case OP_XXPOW: return kHintRX;
+    case OP_YPOW: case OP_SQRTY: return kHintReal;
     default: return 0;
     }
 }
@@ -639,6 +642,11 @@ uint8_t op_hint(const Group &g, const PassOp &op, const std::vector<Member> &mem
     if (op.kind == K_D1 || op.kind == K_D2) {
         uint8_t h = 0xf;
         for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, false) & 0xf;
+        return h;
+    }
+    if (op.kind == K_P2) {  // a I + b P with a real, b imaginary stays so under products
+        uint8_t h = kHintRX;
+        for (const Member &m : mem) h &= gate_hint(g.gates[m.gate].op, false);
         return h;
     }
     if (op.kind == K_F2) {
@@ -735,11 +743,37 @@ PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
     return op;
 }
 
+// The global phase the builder leaves out of a gate's matrix (the matrix is
+// e^{i phase} times the one built), linear in its parameter: phase = c eta,
+// or the constant c.  Rotations about Z and ZZ: e^{-i eta/2}; power gates of
+// X, Y and XX: e^{i pi t/2}; sqrt X and sqrt Y: e^{i pi/4}.
+bool gate_phase(int op, double *c, bool *constant)
+{
+    *constant = false;
+    switch (op) {
+    case OP_RZ: case OP_RZZ: *c = -0.5; return true;
+    case OP_XPOW: case OP_YPOW: case OP_XXPOW: *c = 0.5 * M_PI; return true;
+    case OP_SQRTX: case OP_SQRTY: *c = 0.25 * M_PI; *constant = true; return true;
+    default: return false;
+    }
+}
+
 void plan_group(Group &g, const Options &opt, int S)
 {
     const int n = g.n;
     Planner P{g};
     const int G = (int)g.gates.size();
+
+    // terms of the row's global phase; the constant ones summed into one
+    double phase_const = 0.0;
+    for (int gi = 0; gi < G; gi++) {
+        double c;
+        bool constant;
+        if (!gate_phase(g.gates[gi].op, &c, &constant)) continue;
+        if (constant) phase_const += c;
+        else g.phase_terms.push_back(PhaseTerm{g.gates[gi].slot0, 0, c});
+    }
+    if (phase_const != 0.0) g.phase_terms.push_back(PhaseTerm{-1, 0, phase_const});
 
     // Product-state initialisation: the single-qubit gates a qubit sees
     // before its first two-qubit gate act on |0> alone, so the first pass

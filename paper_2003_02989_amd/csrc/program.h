@@ -77,6 +77,7 @@ struct Group {
     std::vector<int32_t> sym_gslots;
     int32_t fwd_mat_end = 0;                    // forward matrices (with the product init) end here
     std::vector<std::pair<int, int>> dense_stages;  // (forward pass, stage) with a stage matrix
+    std::vector<PhaseTerm> phase_terms;         // the row's global phase, linear in the parameters
 };
 
 // Per-op dispatch overhead of the register ops, in fp64-instruction

@@ -107,7 +107,7 @@ constexpr int kPauliTile = 11;
 
 struct GroupDev {
     DevBuf rows, ident, gates, slot_sym, scale, off, explicit_, tasks, members, fwd_ops, rev_ops, sym_begin,
-        sym_gslots, gslot_slot, fwd_stages, rev_stages, dense_list;
+        sym_gslots, gslot_slot, fwd_stages, rev_stages, dense_list, phase_terms;
     std::vector<int> fwd_op_off, rev_op_off, fwd_stage_off, rev_stage_off;
     int n_fwd_stages = 0, n_rev_stages = 0, n_dense = 0;
     size_t psi_off = 0;  // amplitude offset of this group's rows in the state workspaces
@@ -136,7 +136,7 @@ struct tq_program_s {
         for (auto &g : gdev) {
             for (DevBuf *b : {&g->rows, &g->ident, &g->gates, &g->slot_sym, &g->scale, &g->off, &g->explicit_,
                               &g->tasks, &g->members, &g->fwd_ops, &g->rev_ops, &g->sym_begin, &g->sym_gslots,
-                              &g->gslot_slot, &g->fwd_stages, &g->rev_stages, &g->dense_list})
+                              &g->gslot_slot, &g->fwd_stages, &g->rev_stages, &g->dense_list, &g->phase_terms})
                 b->release();
         }
         for (auto &o : obs_dev) o->release();
@@ -189,6 +189,7 @@ void ensure_device(tq_program p)
         upload(gd->explicit_, g.explicit_mats);
         upload(gd->tasks, g.tasks);
         upload(gd->members, g.members);
+        upload(gd->phase_terms, g.phase_terms);
         std::vector<PassOp> fo, ro;
         for (const Pass &ps : g.fwd) {
             gd->fwd_op_off.push_back((int)fo.size());
@@ -258,6 +259,12 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.rows = (const int32_t *)gd.rows.p;
     a.mats = mat_ws(p) + gd.mat_off;
     a.mat_stride = std::max(g.mat_block, 1);
+    // the first qubit's product-init matrix (built by the range's first
+    // task) carries the row's global phase
+    const bool init = g.n > 0 && begin == g.fwd_tasks.begin && end > begin && !g.phase_terms.empty();
+    a.phase_out = init ? g.init_mat[0] : -1;
+    a.n_phase = (int32_t)g.phase_terms.size();
+    a.phase_terms = (const PhaseTerm *)gd.phase_terms.p;
     hip_check(launch_build(a, (int)g.rows.size(), s), "matrix build launch");
     if (begin <= g.fwd_tasks.begin && end >= g.fwd_tasks.end && gd.n_dense > 0) {
         // dense forward stages, from the op matrices just built

@@ -52,6 +52,14 @@ struct Member {
     uint8_t pad[2];
 };
 
+// One term of a row's global phase (the phases the gate matrices leave out):
+// c * eta(slot), or the constant c when slot < 0.
+struct PhaseTerm {
+    int32_t slot;
+    int32_t pad;
+    double c;
+};
+
 // Build tasks of the matrix builder; each writes one matrix per batch row.
 enum TaskKind : uint8_t {
     BT_PRODUCT = 0, // product of members (last member applied last)
@@ -83,7 +91,8 @@ enum OpKind : uint8_t {
 constexpr uint8_t kHintX = 16;
 constexpr uint8_t kHintReal = 32;  // K_M1: the matrix and its derivatives are real
 // K_M1: real diagonal and imaginary off-diagonal entries (RX and its products;
-// so are the derivatives); K_F2: the (|01>, |10>) block has that form (fSim)
+// so are the derivatives); K_F2: the (|01>, |10>) block has that form (fSim);
+// K_P2: a real and b imaginary
 constexpr uint8_t kHintRX = 64;
 struct PassOp {
     uint8_t kind;
@@ -97,7 +106,7 @@ struct PassOp {
     uint8_t hint;     // structure every parameter value keeps: K_D1 / K_D2 bit k (k < 4): diagonal
                       // entry k of the matrix is exactly 1 (and of dW/deta exactly 0); K_M1
                       // kHintX: the matrix is exactly X (a swap); kHintReal: it is real;
-                      // kHintRX (K_M1, K_F2) as above; K_F2 bit 0 / bit 3: the phase on
+                      // kHintRX (K_M1, K_F2, K_P2) as above; K_F2 bit 0 / bit 3: the phase on
                       // |00> / |11> is exactly 1
     int32_t mat;      // offset of the op's matrix (forward) or W^dagger (reverse)
     int32_t dmat[2];  // reverse: offsets of dW/deta_j
