@@ -252,7 +252,7 @@ template <int D> __device__ __forceinline__ void build_task_d(const BuildTask &b
             for (int i = 0; i < D; i++)
 #pragma unroll
                 for (int j = 0; j < D; j++) acc[i * D + j] = C(g[j * D + i].x, -g[j * D + i].y);
-        } else if (bt.kind == BT_DERIV) {
+        } else if (bt.kind == BT_DERIV || bt.mem_count == 1) {  // one member: its matrix itself
 #pragma unroll
             for (int i = 0; i < D * D; i++) acc[i] = g[i];
         } else {
