@@ -20,6 +20,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <cstring>
 #include <sstream>
 #include <vector>
 
@@ -655,6 +656,142 @@ uint32_t local_mask(const TileGeom &gm, uint64_t m)
 
 } // namespace
 
+namespace {
+
+// phi = g H psi over the tile of one pass: per thread 16 amplitudes (the top
+// four bits of the tile index) in four chunks of four; per chunk and term
+// group (same X mask on the tile) one partner read per amplitude, per term
+// two FMAs with the term's coefficient c' = coeff i^ny chi_z(x) signed by
+// chi_z of the output amplitude (fixed and thread bits: once per group and
+// chunk, register bits: at compile time).
+void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
+{
+    const TileGeom &gm = pp.geom;
+    const int t = gm.t, P = 16, RC = 4, tb = t - 4, NT = 1 << tb, NW = NT / 64;
+    struct TT {
+        uint32_t zlo, zhi;
+        uint64_t zF;
+        double C;  // c' = C (real) or i C (imaginary)
+        bool im;
+    };
+    std::map<uint32_t, std::vector<TT>> groups;
+    for (const SpecTerm &tm : pp.terms) {
+        const uint32_t xT = local_mask(gm, tm.x), zT = local_mask(gm, tm.z);
+        const int ny = tm.ny & 3;
+        const double chi = (__builtin_popcountll(tm.x & tm.z) & 1) ? -1.0 : 1.0;
+        const double C = tm.coeff * chi * (ny >= 2 ? -1.0 : 1.0);
+        groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, tm.z & gm.fixed_mask, C, (ny & 1) != 0});
+    }
+    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void tq_hphi_" << pi
+      << "(HPhiArgs a)\n{\n"
+         "    extern __shared__ __align__(16) unsigned char smem[];\n"
+         "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
+         "    uint64_t *hi_off = reinterpret_cast<uint64_t *>(la + "
+      << (1 << t)
+      << ");\n"
+         "    double *red = reinterpret_cast<double *>(hi_off + "
+      << (1 << gm.h)
+      << ");\n"
+         "    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;\n"
+         "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
+         "    const int64_t ro = (int64_t)cget(a.rows, row) * a.row_stride;\n"
+         "    float2 *ps = const_cast<float2 *>(a.psi) + ro;\n"
+         "    float2 *pf = a.phi + ro;\n"
+         "    const double gw = (double)a.upstream[(int64_t)cget(a.brows, row) * a.K];\n"
+         "    build_hi_off(a.g, hi_off);\n"
+         "    __syncthreads();\n"
+         "    const TileCtx tc{hi_off, "
+      << ((1u << gm.c) - 1) << "u, " << gm.c
+      << "};\n"
+         "    const uint32_t st = sw((uint32_t)tid);\n"
+         "    uint32_t tz = (uint32_t)tid;\n"
+         "    double e = 0.0;\n"
+         "    for (int64_t tile = w; tile < "
+      << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
+      << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
+      << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
+      << "    __syncthreads();\n";
+    std::vector<std::pair<uint32_t, const std::vector<TT> *>> gl;
+    for (auto &g : groups) gl.emplace_back(g.first, &g.second);
+    for (int ch = 0; ch < P / RC; ch++) {
+        // the thread index made opaque anew per chunk: what is derived from
+        // it (partner offsets, signed coefficients) is recomputed next to its
+        // use instead of being held across chunks and tiles
+        o << "    {\n    asm volatile(\"\" : \"+v\"(tz));\n"
+          // thread bits and the tile number side by side: a term's sign is
+          // the parity of one masked word
+          << "    const uint32_t vz = tz | ((uint32_t)tile << " << tb << ");\n"
+          << "    double2 acc[" << RC << "];\n"
+          << "#pragma unroll\n    for (int r = 0; r < " << RC << "; r++) acc[r] = make_double2(0.0, 0.0);\n";
+        for (size_t gi = 0; gi < gl.size(); gi++) {
+            const uint32_t xT = gl[gi].first, xhi = xT >> tb;
+            const std::vector<TT> &tts = *gl[gi].second;
+            o << "    {\n";
+            o << "        const uint32_t pt = sw(tz ^ " << (xT & (uint32_t)(NT - 1)) << "u);\n";
+            for (size_t j = 0; j < tts.size(); j++) {
+                const TT &tt = tts[j];
+                // the sign flips the coefficient's sign bit (integer ops: no
+                // per-term lane masks held in scalar registers)
+                uint64_t zt = 0;  // the term's Z bits among the fixed bits, as tile-number bits
+                for (int b = 0, k = 0; b < gm.n; b++)
+                    if ((gm.fixed_mask >> b) & 1) zt |= ((tt.zF >> b) & 1ull) << k++;
+                const uint64_t m = (uint64_t)tt.zlo | (zt << tb);
+                uint64_t cb;
+                std::memcpy(&cb, &tt.C, sizeof cb);
+                if (!m) o << "        const double k" << j << " = " << dbl(tt.C) << ";\n";
+                else
+                    o << "        const double k" << j << " = __longlong_as_double((long long)(" << cb
+                      << "ull ^ ((uint64_t)(__popc(vz & " << m << "u) & 1) << 63)));\n";
+            }
+            for (int rr = 0; rr < RC; rr++) {
+                const int r = ch * RC + rr;
+                o << "        { const double2 p = up2(la[pt ^ " << host_sw((uint32_t)NT * (r ^ xhi)) << "u]);";
+                for (size_t j = 0; j < tts.size(); j++) {
+                    const TT &tt = tts[j];
+                    const bool neg = __builtin_popcount(tt.zhi & (uint32_t)r) & 1;
+                    const std::string k = (neg ? "-k" : "k") + N((long)j);
+                    const std::string A = "acc[" + N(rr) + "]";
+                    if (!tt.im)
+                        o << " " << A << ".x = fma(" << k << ", p.x, " << A << ".x); " << A << ".y = fma(" << k << ", p.y, "
+                          << A << ".y);";
+                    else  // i k p = k (-p.y, p.x)
+                        o << " " << A << ".x = fma(" << k << ", -p.y, " << A << ".x); " << A << ".y = fma(" << k
+                          << ", p.x, " << A << ".y);";
+                }
+                o << " }\n";
+            }
+            // keep each group's coefficients and partner reads next to its FMAs
+            o << "    }\n    __builtin_amdgcn_sched_barrier(0);\n";
+        }
+        for (int rr = 0; rr < RC; rr++) {
+            const int r = ch * RC + rr;
+            o << "    {\n        const double2 ow = up2(la[st ^ " << host_sw((uint32_t)NT * r) << "u]);\n"
+              << "        e = fma(ow.x, acc[" << rr << "].x, fma(ow.y, acc[" << rr << "].y, e));\n"
+              << "        const uint64_t gix = tile_index(tc, fb, " << (uint32_t)NT * r << "u + (uint32_t)tid);\n"
+              << "        const float2 v = make_float2((float)(gw * acc[" << rr << "].x), (float)(gw * acc[" << rr
+              << "].y));\n";
+            if (pi == 0)
+                o << "        pf[gix] = v;\n";
+            else
+                o << "        const float2 q = pf[gix];\n        pf[gix] = make_float2(q.x + v.x, q.y + v.y);\n";
+            o << "    }\n";
+        }
+        o << "    }\n";
+    }
+    o << "    __syncthreads();\n"
+         "    }\n"
+         "    { const double v = wave_sum(e); if (lane == 0) red[wave] = v; }\n"
+         "    __syncthreads();\n"
+         "    if (tid == 0) {\n"
+         "        double v = red[0];\n";
+    for (int wv = 1; wv < NW; wv++) o << "        v += red[" << wv << "];\n";
+    o << "        a.partial[(int64_t)(row * a.npass + " << pi << ") * a.wg_per_row + w] = v;\n"
+         "    }\n"
+         "}\n";
+}
+
+} // namespace
+
 std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
 {
     std::ostringstream o;
@@ -960,6 +1097,25 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
+}
+
+std::string hphi_spec_source(const std::vector<PauliPass> &passes)
+{
+    std::ostringstream o;
+    o << kHead;
+    for (size_t pi = 0; pi < passes.size(); pi++) hphi_pass(o, passes[pi], (int)pi);
+    o << "} // namespace tq\n";
+    return o.str();
+}
+
+hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
+                            std::string *log, SpecMemo *memo)
+{
+    if (nrows <= 0) return hipSuccess;
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_hphi_" + N(pass), &fn, log);
+    if (e != hipSuccess) return e;
+    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
 }
 
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,

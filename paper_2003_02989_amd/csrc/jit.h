@@ -59,6 +59,13 @@ hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int 
 std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K);
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
                              std::string *log, SpecMemo *memo);
+// Kernels tq_hphi_<pass> computing phi = g H psi and <psi|H|psi> for one
+// observable H (the same on every row) pass by pass, each pass's tile
+// holding the X bits of its terms; partials of the expectation go to
+// partial[row][npass][wg_per_row].
+std::string hphi_spec_source(const std::vector<PauliPass> &passes);
+hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
+                            std::string *log, SpecMemo *memo);
 // Workgroups of a specialised Pauli pass that fit on the device at once (0 if unknown).
 int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo);
 

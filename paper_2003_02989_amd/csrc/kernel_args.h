@@ -105,6 +105,23 @@ struct PauliSpecArgs {
     double *partial;
 };
 
+// phi = g H psi for a single observable H (the same on every row) and its
+// expectation, pass by pass over tiles that hold the X bits of the pass's
+// terms (kernels tq_hphi_<pass> generated for the observable).
+struct HPhiArgs {
+    const float2 *psi;
+    float2 *phi;             // written by pass 0, accumulated by the others
+    int64_t row_stride;
+    const int32_t *rows;     // state rows
+    const int32_t *brows;    // batch index of each row (upstream)
+    const float *upstream;   // [B][K]: g = upstream[b][0]
+    int K;
+    TileGeom g;              // the pass's tile
+    int wg_per_row;
+    int npass, pass;         // partial slots: [nrows][npass][wg_per_row]
+    double *partial;
+};
+
 struct PauliReduceArgs {
     const int32_t *rows;     // batch index of each row
     const double *partial;

@@ -93,6 +93,11 @@ struct ObsGroupDev {
     std::vector<PauliPass> spec_passes;
     std::string spec_src;
     SpecMemo spec_memo;
+    // passes and source of the kernels computing phi = g H psi for a single
+    // observable the same on every row (specialize = 1)
+    std::vector<PauliPass> phi_passes;
+    std::string phi_src;
+    SpecMemo phi_memo;
     void release()
     {
         for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
@@ -100,6 +105,9 @@ struct ObsGroupDev {
             b->release();
     }
 };
+
+// Largest observable (terms) whose phi = g H psi kernels are generated.
+constexpr size_t kMaxPhiTerms = 1024;
 
 // Tile size of the Pauli kernel (log2 amplitudes): 2048 amplitudes, eight
 // per thread.
@@ -431,6 +439,17 @@ void ensure_obs(tq_program p, tq_observables o)
                 }
             if (!og->spec_passes.empty()) og->spec_src = pauli_spec_source(og->spec_passes, od.K);
         }
+        if (p->pd->opt.specialize && uniform && od.K == 1 && nterms > 0 && nterms <= kMaxPhiTerms && n > 12) {
+            // the fewest passes (each reads psi and updates phi), smaller
+            // tiles and longer runs on ties
+            for (int t = 12; t <= 13 && t < n; t++)
+                for (int c = 6; c >= 5; c--) {
+                    std::vector<PauliPass> pp;
+                    if (!pauli_spec_plan(n, t, c, per_row[0], &pp)) continue;
+                    if (og->phi_passes.empty() || pp.size() < og->phi_passes.size()) og->phi_passes = std::move(pp);
+                }
+            if (!og->phi_passes.empty()) og->phi_src = hphi_spec_source(og->phi_passes);
+        }
         if (diag) {
             DiagTables dt = diag_tables(per_row, uniform);
             og->diag = true;
@@ -537,6 +556,47 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
 // (when out is not NULL) and, when phi is not NULL, phi = sum_k g_k h_k psi
 // with g = upstream.  Observables are split over launches so that the
 // per-workgroup partials stay within a bounded workspace.
+// phi = g H psi and <psi|H|psi> of a single observable (K = 1) with the
+// kernels generated for it: one read of psi and one update of phi per pass.
+void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, float *out,
+                    hipStream_t s)
+{
+    const Group &g = *p->pd->groups[gi];
+    GroupDev &gd = *p->gdev[gi];
+    ObsGroupDev &og = *p->obs_dev[gi];
+    const int nrows = (int)g.rows.size();
+    const int npass = (int)og.phi_passes.size();
+    HPhiArgs a{};
+    a.psi = psi;
+    a.phi = phi;
+    a.row_stride = (int64_t)1 << g.n;
+    a.rows = (const int32_t *)gd.ident.p;
+    a.brows = (const int32_t *)gd.rows.p;
+    a.upstream = upstream;
+    a.K = 1;
+    a.wg_per_row = wg_for(nrows, g.n - og.phi_passes[0].geom.t);
+    a.npass = npass;
+    a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)nrows * npass * a.wg_per_row);
+    std::string log;
+    for (int pi = 0; pi < npass; pi++) {
+        a.g = og.phi_passes[pi].geom;
+        a.pass = pi;
+        const hipError_t e = launch_hphi_spec(og.phi_src, pi, a, nrows, s, &log, &og.phi_memo);
+        if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+        hip_check(e, "specialised H_g launch");
+    }
+    if (!out) return;
+    PauliReduceArgs r{};
+    r.rows = (const int32_t *)gd.rows.p;
+    r.partial = a.partial;
+    r.wg_per_row = npass * a.wg_per_row;  // the passes' workgroups side by side
+    r.K = 1;
+    r.k_begin = 0;
+    r.k_count = 1;
+    r.out = out;
+    hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
+}
+
 void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, int K, float *out,
                  hipStream_t s)
 {
@@ -551,6 +611,10 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     }
     if (!phi && !og.spec_passes.empty()) {
         spec_pauli_group(p, gi, psi, K, out, s);
+        return;
+    }
+    if (phi && upstream && K == 1 && !og.phi_passes.empty()) {
+        spec_phi_group(p, gi, psi, phi, upstream, out, s);
         return;
     }
     PauliArgs a{};

@@ -219,3 +219,15 @@ def test_specialized_resident_random(seed):
     w = wl.random_batch(6600 + seed, B=4, n=9 + seed, n_gates=60, n_symbols=5, K=3, hetero=True)
     say("specialised resident", seed)
     compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("n,max_terms,seed", [(13, 40, 0), (15, 150, 1)])
+def test_specialized_hphi(n, max_terms, seed):
+    # phi = g H psi from the kernels generated for one observable that is the
+    # same on every row: partners across the tile's high bits, Y phases,
+    # Z-only and identity terms, several passes
+    w = wl.random_batch(7100 + seed, B=3, n=n, n_gates=50, n_symbols=5, K=1)
+    obs = wl.random_observables(wl.rng_for(7200 + seed), n, 1, max_terms=max_terms, max_weight=4)
+    w.observables = [obs for _ in range(w.B)]
+    say("specialised H_g", n, len(obs[0]))
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
