@@ -313,21 +313,18 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     if (a.phase_out < 0 || blockIdx.x != 0) return;
     // the row's global phase (block 0 of the row; its thread 0 built the
     // product-init matrix at phase_out), reduced in a fixed order
-    __shared__ double part[256];
+    __shared__ double part[4];
     double ph = 0.0;
     for (int j = threadIdx.x; j < a.n_phase; j += blockDim.x) {
         const PhaseTerm pt = a.phase_terms[j];
         ph += pt.slot >= 0 ? pt.c * slot_value(c, pt.slot) : pt.c;
     }
-    part[threadIdx.x] = ph;
+    ph = wave_sum(ph);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ph;
     __syncthreads();
-    for (int h = blockDim.x / 2; h > 0; h >>= 1) {
-        if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
-        __syncthreads();
-    }
     if (threadIdx.x == 0) {
         double s, co;
-        sincos(part[0], &s, &co);
+        sincos(part[0] + part[1] + part[2] + part[3], &s, &co);
         double2 *out = a.mats + (int64_t)row * a.mat_stride + a.phase_out;
         for (int i = 0; i < 4; i++) {
             const double2 v = out[i];
