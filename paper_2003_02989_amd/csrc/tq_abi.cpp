@@ -439,6 +439,7 @@ void ensure_obs(tq_program p, tq_observables o)
                 }
             if (!og->spec_passes.empty()) og->spec_src = pauli_spec_source(og->spec_passes, od.K);
         }
+        // (states of at most 12 qubits run resident: their phi is formed on chip)
         if (p->pd->opt.specialize && uniform && od.K == 1 && nterms > 0 && nterms <= kMaxPhiTerms && n > 12) {
             // the fewest passes (each reads psi and updates phi), smaller
             // tiles and longer runs on ties
