@@ -65,6 +65,10 @@ struct Env {
     std::string acc_shift;
     int nt = kThreads;  // threads of the workgroup
     const Group *grp = nullptr;  // reverse stages: gradients from gate generators where known
+    // keep each op's matrix reads next to the op (opaque per-item offset,
+    // scheduling barriers between reverse ops): needed where registers are
+    // short (tile passes, four waves per SIMD)
+    bool pin = true;
 };
 
 // An op bit at tile position l (global position p): from the item's base
@@ -393,7 +397,7 @@ void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint
     // matrix reads offset by it stay inside the item loop instead of being
     // hoisted above it, where every matrix of the stage would be live at once
     o << "        int z_ = 0;\n";
-    o << "        asm volatile(\"\" : \"+s\"(z_));\n";
+    if (e.pin) o << "        asm volatile(\"\" : \"+s\"(z_));\n";
 }
 
 // A forward stage on the tile lp.
@@ -481,7 +485,7 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
             if (!c.empty()) {
                 for (const std::string &d : dots) o << "        " << d << "\n";
                 o << "        " << c << "\n";
-                o << "        __builtin_amdgcn_sched_barrier(0);\n";
+                if (e.pin) o << "        __builtin_amdgcn_sched_barrier(0);\n";
                 gk = gkr;
                 oi = oi + (int)run.size() - 1;
                 continue;
@@ -508,7 +512,7 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
         o << "        " << apply(e, op, R, op.mat - e.mbase, "f") << "\n";
         // keep each op's matrix reads next to the op: scheduled ahead they
         // would hold every matrix of the stage in registers at once
-        o << "        __builtin_amdgcn_sched_barrier(0);\n";
+        if (e.pin) o << "        __builtin_amdgcn_sched_barrier(0);\n";
     }
     for (int k = 0; k < NR; k++)
         o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]); lf[sb ^ " << off[k] << "u] = down2(f[" << k
@@ -555,6 +559,7 @@ std::string resident_source(const Group &g)
          "    const int tid = threadIdx.x;\n"
          "    resident_begin(a, M, acc, lp, tid, " << nt << ");\n";
     Env e{n, 0, "M", false, "a.nacc", "a.gacc"};
+    e.pin = false;  // two waves per SIMD: registers to spare, latency to hide
     e.nt = nt;
     e.grp = &g;
     for (const Pass &ps : g.fwd)
