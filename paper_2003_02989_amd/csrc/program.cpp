@@ -758,6 +758,20 @@ bool gate_phase(int op, double *c, bool *constant)
     }
 }
 
+// Arithmetic per amplitude (fp64 instructions) of a single-qubit op fusing
+// `mem` in a generated kernel: diagonal 2 per entry that is not exactly 1,
+// dense 4 when real or RX-form, else 8.
+int one_qubit_cost(const Group &g, const std::vector<Member> &mem)
+{
+    bool diag = true;
+    for (const Member &m : mem) diag = diag && classify(g.gates[m.gate].op) == C_1D;
+    PassOp t{};
+    t.kind = diag ? K_D1 : K_M1;
+    const uint8_t h = op_hint(g, t, mem);
+    if (diag) return 2 * (2 - __builtin_popcount(h & 3u));
+    return (h & (kHintReal | kHintRX)) ? 4 : 8;
+}
+
 void plan_group(Group &g, const Options &opt, int S)
 {
     const int n = g.n;
@@ -828,8 +842,19 @@ void plan_group(Group &g, const Options &opt, int S)
             int q0 = g.gate_q0[gi], q1 = g.gate_q1[gi];
             if (opt.fuse && (cls == C_1D || cls == C_1M)) {
                 int o = last[q0];
-                if (o >= 0 && ops[o].qb == -1 && ops[o].qa == q0) {
-                    ops[o].mem.push_back(Member{gi, 0, FORM_FULL, {0, 0}});
+                const Member mg{gi, 0, FORM_FULL, {0, 0}};
+                // generated kernels spend nothing per op, so a product that
+                // loses its factors' structure (RY RZ: real and diagonal with
+                // a unit entry, dense and complex together) is kept apart when
+                // the factors are cheaper one by one
+                bool merge = o >= 0 && ops[o].qb == -1 && ops[o].qa == q0;
+                if (merge && opt.specialize) {
+                    std::vector<Member> both = ops[o].mem;
+                    both.push_back(mg);
+                    merge = one_qubit_cost(g, both) <= one_qubit_cost(g, ops[o].mem) + one_qubit_cost(g, {mg});
+                }
+                if (merge) {
+                    ops[o].mem.push_back(mg);
                     if (cls == C_1M) ops[o].op.kind = K_M1;
                     continue;
                 }
