@@ -323,7 +323,12 @@ bool uniform(const PassOp &op, const std::vector<int> &bits)
 // fp64-instruction equivalents per amplitude of one op in a register stage
 int op_cost(const PassOp &op, int dispatch)
 {
+    // a diagonal op's entries that are exactly 1 cost nothing in generated
+    // kernels (the table-driven ones multiply every entry)
+    const bool generated = dispatch == kOpDispatchCostSpec;
     int c = 4;
+    if (generated && op.kind == K_D1) c = 2 * (2 - __builtin_popcount(op.hint & 3u));
+    if (generated && op.kind == K_D2) c = 4 - __builtin_popcount(op.hint & 15u);
     if (op.kind == K_M1) c = op.ctrl || (op.hint & (kHintReal | kHintRX)) ? 4 : 8;
     if (op.kind == K_M2) c = 16;
     if (op.kind == K_F2) c = (op.hint & kHintRX) ? 4 : 6;
