@@ -1032,7 +1032,10 @@ std::string pass_unit(const Group &g)
 {
     std::string body = kHead;
     for (int pi = 0; pi < (int)g.fwd.size(); pi++) body += pass_kernel_source(g, pi);
-    for (int pi = 0; pi < (int)g.rev.size(); pi++) body += rev_pass_kernel_source(g, pi);
+    // reverse passes only run for gradients: a structure without symbolic
+    // parameters never launches them
+    if (g.n_gslots > 0)
+        for (int pi = 0; pi < (int)g.rev.size(); pi++) body += rev_pass_kernel_source(g, pi);
     return body + "} // namespace tq\n";
 }
 

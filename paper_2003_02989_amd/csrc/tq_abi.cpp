@@ -1016,7 +1016,9 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
                 r.mat_begin = ps.mat_begin;
                 r.mat_end = ps.mat_end;
                 gbase += gc;
-                if (pd.opt.specialize) {
+                // (a structure without symbolic parameters has no generated
+                // reverse passes: it takes the precompiled kernel)
+                if (pd.opt.specialize && g.n_gslots > 0) {
                     std::string log;
                     const hipError_t e = launch_rev_pass_spec(g, (int)pi, r, nrows, s, &log, &gd.pass_memo);
                     if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);

@@ -231,3 +231,13 @@ def test_specialized_hphi(n, max_terms, seed):
     w.observables = [obs for _ in range(w.B)]
     say("specialised H_g", n, len(obs[0]))
     compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+
+
+def test_specialized_group_without_symbols():
+    # adjoint over a batch whose first structure has no symbolic parameter
+    # (no generated reverse passes: it takes the precompiled ones) next to one
+    # with symbols, both run as tile passes
+    w = wl.random_batch(7300, B=2, n=13, n_gates=40, n_symbols=3, K=2)
+    w.circuits[0] = wl.random_circuit(wl.rng_for(7301), 13, 40, 3, p_symbolic=0.0)
+    say("specialised group without symbols")
+    compare(gpu_outputs(w, max_tile_qubits=10, specialize=True), oracle_outputs(w))
