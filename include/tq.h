@@ -73,8 +73,13 @@ typedef enum {
  *                    written in as constants; likewise an observable set that
  *                    is the same on every row (at most 16 observables and 64
  *                    terms, some with X or Y factors) gets expectation passes
- *                    generated for its terms.  0 = the precompiled kernels
- *                    that read the plan from tables (default). */
+ *                    generated for its terms, and a single observable that is
+ *                    the same on every row (at most 1024 terms, states of more
+ *                    than 12 qubits) gets passes generated for the adjoint's
+ *                    phi = g H psi and its expectation.  Structures without
+ *                    symbolic parameters get no generated reverse passes.
+ *                    0 = the precompiled kernels that read the plan from
+ *                    tables (default). */
 typedef struct {
     int32_t max_tile_qubits;
     int32_t low_qubits;
