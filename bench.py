@@ -1,17 +1,23 @@
 """Benchmark of the batched state-vector hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config c2|c1|c3|c4|c5] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config c4|c1|c2|c3|c5] [--no-cpu-baseline]
 
 One step is one call of the configuration's hot path on its full batch with
-inputs resident in HBM:
+inputs resident in HBM and a new parameter set (or sampling seed) per step:
+  c4  tq_sample_with_amplitudes: one simulation of the 30-qubit random circuit
+      (46 fused tile passes over the 8 GiB state), its amplitudes at 4096
+      bitstrings and 10^6 samples (the default workload)
   c1, c2, c5  tq_adjoint_grad with expectation output (forward passes, Pauli-sum
               expectations, H_g, reverse adjoint passes, gradient reduction)
-  c3          tq_expectation
-  c4          tq_amplitudes (4096 bitstrings) + tq_sample (10^6 shots)
-The default workload is c2, the 10-qubit QNN classifier with batch 1024.
-Rank 0 prints one JSON line.  The dominant kernel (largest device time per
-step, measured with HIP events) gets a roofline entry; the oracle, timed on
-the host's cores on a bounded sample, gives the cpu_baseline entry.
+  c3  tq_expectation
+Rank 0 prints one JSON line.  `value` is the metric's half that fits the
+workload: for c4 the effective HBM GB/s of its fused-gate passes
+(16 B per amplitude per pass, 8 B for the pass that generates the product
+state, over the passes' HIP-event time); for the batched workloads
+circuit-expectations/s over the step time.  Both figures, the cold rate
+(program creation + first call, which compiles the generated kernels) and the
+dominant kernel's HBM and fp64 rooflines are in the line; the oracle, timed
+on the host's cores on a bounded sample, gives the cpu_baseline entry.
 """
 import argparse
 import json
@@ -156,12 +162,23 @@ def kernel_work(plan, kernel, n_obs_terms, adjoint):
     return flops, bytes_, launches
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="c2", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-specialize", action="store_true",
                     help="run with the precompiled table-driven kernels instead of the ones compiled for the "
@@ -175,14 +192,16 @@ def main():
                     help="only copy a 1 GiB device buffer three times (reference for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the batched path has no "
-              "multi-GPU mode in this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU mode; "
+              "the batch would split across GPUs row-wise and a large state by amplitudes (DESIGN.md)",
+              file=sys.stderr)
         sys.exit(1)
 
     import numpy as np
     import torch
 
     from paper_2003_02989_amd import tq
+    from paper_2003_02989_amd import workloads as wl
 
     local_rank = int(os.environ.get("LOCAL_RANK", "0"))
     torch.cuda.set_device(local_rank)
@@ -199,12 +218,14 @@ def main():
         return
     w = workload(args.config)
     B, K = w.B, w.K
-    t_cold0 = time.perf_counter()
+    adjoint = args.config in ("c1", "c2", "c5")
     specialize = not args.no_specialize
-    prog = tq.Program(w.program_blob(), specialize=specialize)
-    obs = tq.Observables(w.observable_blob())
-    t_create = time.perf_counter() - t_cold0
-    theta = torch.as_tensor(w.theta, device="cuda") if w.n_symbols else None
+    # every step (first call, warm-up, per-kernel profiling, timed) gets its
+    # own parameter set, drawn like the workload's
+    n_prof = 2 * len(KERNELS)
+    n_steps_total = 1 + args.warmup + n_prof + args.steps
+    thetas = ([torch.as_tensor(t, device="cuda") for t in wl.fresh_thetas(w, n_steps_total, 7 + wl.BASE_SEED)]
+              if w.n_symbols else [None] * n_steps_total)
     up = torch.as_tensor(w.upstream, device="cuda")
     exp = torch.empty((B, K), dtype=torch.float32, device="cuda")
     grad = torch.empty((B, w.n_symbols), dtype=torch.float32, device="cuda")
@@ -213,19 +234,28 @@ def main():
         amps = torch.empty((1, bits.shape[1]), dtype=torch.complex64, device="cuda")
         n_shots = w.extras["n_shots"]
         shots = torch.empty((1, n_shots), dtype=torch.int64, device="cuda")
-        state = torch.empty((1, 1 << w.circuits[0].n), dtype=torch.complex64, device="cuda")
+    torch.cuda.synchronize()
+
+    counter = [0]
 
     def step():
-        if args.config in ("c1", "c2", "c5"):
-            tq.adjoint_grad(prog, theta, obs, up, grad=grad, expectations=exp)
+        i = counter[0]
+        counter[0] += 1
+        th = thetas[i]
+        if adjoint:
+            tq.adjoint_grad(prog, th, obs, up, grad=grad, expectations=exp)
         elif args.config == "c3":
-            tq.expectation(prog, theta, obs, out=exp)
+            tq.expectation(prog, th, obs, out=exp)
         else:
-            # one simulation serves both outputs
-            tq.simulate_state(prog, None, out=state)
-            tq.amplitudes_from_state(state, bits, out=amps)
-            tq.sample_from_state(state, n_shots, w.extras["seed"], out=shots)
+            # one simulation serves both outputs; a new sampling seed per step
+            tq.sample_with_amplitudes(prog, None, n_shots, w.extras["seed"] + i, bits, out=shots, amps=amps)
 
+    # cold: program and observables created, first call (kernels generated and
+    # compiled for the structure)
+    t0 = time.perf_counter()
+    prog = tq.Program(w.program_blob(), specialize=specialize)
+    obs = tq.Observables(w.observable_blob())
+    t_create = time.perf_counter() - t0
     t0 = time.perf_counter()
     step()
     torch.cuda.synchronize()
@@ -261,22 +291,46 @@ def main():
 
     plan = tq.describe(prog)
     n_terms = sum(len(t) for t in w.observables[0])
-    flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, args.config in ("c1", "c2", "c5"))
+    flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, adjoint)
     avg_ms = dom_ms / max(n_launch, 1)
     traffic = measured_traffic(args.config, dominant)
-    if args.config in ("c1", "c2"):
-        bound, unit, peak = "alu", "TFLOP/s", PEAK_FP64_TFLOPS
-        achieved = (flops / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e12
-    else:
-        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
-        achieved = (bytes_ / max(launches_per_step, 1)) / (avg_ms * 1e-3) / 1e9
+    per_launch_flops = flops / max(launches_per_step, 1)
+    per_launch_bytes = bytes_ / max(launches_per_step, 1)
+    hbm = {"bound": "hbm", "achieved": per_launch_bytes / (avg_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
+           "unit": "GB/s", "algorithmic_per_launch": per_launch_bytes}
+    hbm["frac"] = hbm["achieved"] / hbm["peak"]
+    alu = {"bound": "alu", "achieved": per_launch_flops / (avg_ms * 1e-3) / 1e12, "peak": PEAK_FP64_TFLOPS,
+           "unit": "TFLOP/s", "algorithmic_per_launch": per_launch_flops, "arithmetic": "fp64 vector"}
+    alu["frac"] = alu["achieved"] / alu["peak"]
+    binding, other = (hbm, alu) if hbm["frac"] >= alu["frac"] else (alu, hbm)
+    roofline = dict(binding)
+    roofline.update({"kernel": dominant, "traffic": traffic, "launches_per_step": launches_per_step,
+                     "avg_launch_ms": avg_ms, "other_roof": other})
 
+    # the two halves of the metric
+    pass_bytes = kernel_work(plan, "pass", n_terms, adjoint)[1]
+    if dominant == "pass":
+        pass_ms = dom_ms / args.steps
+    else:
+        pass_ms = per_kernel.get("pass", 0.0)
+    fused_pass_gbs = pass_bytes / (pass_ms * 1e-3) / 1e9 if pass_ms > 0 else None
+    cold_s = t_create + t_first
     if args.config == "c4":
-        value = B * amps.shape[1] / (ms_per_step * 1e-3)
-        unit_v = "amplitudes/s (with 10^6 samples per step)"
+        value, unit_v = fused_pass_gbs, "GB/s (effective HBM bandwidth per fused-gate pass)"
+        rates = {"amplitudes_per_s": B * amps.shape[1] / (ms_per_step * 1e-3),
+                 "samples_per_s": B * n_shots / (ms_per_step * 1e-3),
+                 "fused_passes_per_step": kernel_work(plan, "pass", n_terms, adjoint)[2],
+                 "fused_pass_ms_per_step": pass_ms,
+                 "cold_ms": cold_s * 1e3}
     else:
         value = B * K / (ms_per_step * 1e-3)
-        unit_v = "circuit-expectations/s" + (" (with adjoint gradients)" if args.config in ("c1", "c2", "c5") else "")
+        unit_v = "circuit-expectations/s" + (" (with adjoint gradients)" if adjoint else "")
+        rates = {"circuit_expectations_per_s": value,
+                 "cold_circuit_expectations_per_s": B * K / cold_s,
+                 "fused_pass_GBps": fused_pass_gbs,
+                 "fused_pass_ms_per_step": pass_ms if pass_ms > 0 else None}
+        if adjoint:
+            rates["gradient_rows_per_s"] = B / (ms_per_step * 1e-3)
 
     line = {
         "metric": METRIC,
@@ -290,15 +344,13 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f64",
-        "data": "synthetic (seeded generators, no datasets)",
-        "config": {"workload": describe_workload(args.config, w), "storage": "complex64", "batch": B, "qubits": w.n_max,
-                   "symbols": w.n_symbols, "observables": K, "pauli_terms": n_terms,
-                   "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3,
+        "data": "synthetic (seeded generators, no datasets); a new parameter set or sampling seed per step",
+        "config": {"workload": describe_workload(args.config, w), "storage": "complex64", "arithmetic": "fp64",
+                   "batch": B, "qubits": w.n_max, "symbols": w.n_symbols, "observables": K,
+                   "pauli_terms": n_terms, "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3,
                    "specialized_kernel": specialize},
-        "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": traffic, "launches_per_step": launches_per_step,
-                     "avg_launch_ms": avg_ms,
-                     "algorithmic_per_launch": (flops if bound == "alu" else bytes_) / max(launches_per_step, 1)},
+        "rates": rates,
+        "roofline": roofline,
         "kernel_ms_per_step": per_kernel,
     }
 
@@ -439,8 +491,14 @@ def cpu_baseline(name, w, budget_s):
             if time.perf_counter() - t0 > budget_s:
                 break
         dt = (time.perf_counter() - t0) / reps
-        return {"value": 4096 / dt, "unit": "amplitudes/s", "cores": threads, "kind": "oracle",
-                "sample": f"24-qubit (4x6 grid) version of the depth-20 circuit, full simulation per call, {reps} calls"}
+        # the metric's unit: 16 B per amplitude per gate application of the
+        # oracle's gate-by-gate sweeps (it applies every gate as its own pass)
+        n_g = len(ws.circuits[0].gates)
+        gbs = 16.0 * (1 << ws.circuits[0].n) * n_g / dt / 1e9
+        return {"value": gbs, "unit": "GB/s (effective, 16 B per amplitude per gate pass)", "cores": threads,
+                "kind": "oracle", "cpu": cpu_model(), "amplitudes_per_s": 4096 / dt,
+                "sample": f"24-qubit stand-in (4x6 grid) of the depth-20 random circuit, {n_g} gates, one full "
+                          f"complex128 simulation plus 4096 amplitudes per call, {reps} calls in {dt * reps:.1f} s"}
     rows = 1
     done_rows = 0
     t0 = time.perf_counter()
@@ -462,6 +520,7 @@ def cpu_baseline(name, w, budget_s):
         rows = min(max(rows * 2, 1), w.B)
     what = "expectations" + (" + adjoint gradients" if name != "c3" else "")
     return {"value": done_rows * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "
                       f"the full batch) in {el:.1f} s"}
 

@@ -159,9 +159,19 @@ tq_status tq_expectation(tq_program prog, const float *symbol_values, tq_observa
  * u_k = SplitMix64 output number (b * n_shots + k) of the stream started at
  * `seed`, r_k = floor(u_k W / 2^64), and shot k is the unique i with
  * C_i <= r_k < C_i + w_i where C is the exclusive prefix sum of w.
- * n_shots >= 0; a row with W = 0 yields all-zero bitstrings. */
+ * n_shots >= 0.  A row with W = 0 (no distribution: an all-zero state)
+ * yields 2^64 - 1 for every shot, a value no bitstring of at most 32 qubits
+ * takes. */
 tq_status tq_sample(tq_program prog, const float *symbol_values, int64_t n_shots, uint64_t seed,
                     uint64_t *out, void *stream);
+
+/* One simulation serving both outputs of a random-circuit benchmark: the
+ * samples of tq_sample (out, uint64 [B, n_shots], when n_shots > 0) and the
+ * amplitudes of tq_amplitudes (bitstrings uint64 [B, M], amps complex64
+ * [B, M], when M > 0) of the same final states.  Uses only the program's
+ * cached workspaces. */
+tq_status tq_sample_with_amplitudes(tq_program prog, const float *symbol_values, int64_t n_shots, uint64_t seed,
+                                    uint64_t *out, const uint64_t *bitstrings, int64_t M, void *amps, void *stream);
 
 /* Adjoint-method gradient (Sec. "Adjoint Gradient Backpropagation in
  * Simulations") of sum_k upstream[b,k] <h_{b,k}> with respect to every symbol
@@ -183,7 +193,9 @@ tq_status tq_amplitudes(tq_program prog, const float *symbol_values, const uint6
                         void *amps, void *stream);
 
 /* The sampling rule of tq_sample applied to given states: complex64
- * [B, 2^n] device array.  Deterministic and bit-exact for a given input. */
+ * [B, 2^n] device array (8-byte aligned).  Deterministic and bit-exact for a
+ * given input.  Its level workspace (about B 2^n / 63 uint64) is taken from
+ * the stream-ordered allocator and released in stream order on every call. */
 tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
                                uint64_t *out, void *stream);
 
@@ -210,6 +222,21 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
  * clears the record.  Process-wide; not meant for concurrent use. */
 tq_status tq_profile_start(const char *kernel);
 tq_status tq_profile_read(int64_t *launches, double *total_ms);
+
+/* The matrix builder's gate table, for checks on the host (no device call):
+ * the matrix of opcode `op` (deriv = 0), or its derivative with respect to
+ * parameter `which` (deriv = 1), at the resolved parameter values params[np],
+ * as the builder forms it: without the global phase it leaves out of some
+ * gates (and multiplies into the row's product state instead), which goes to
+ * *phase in radians -- the gate's own matrix is e^{i phase} times `out`, and
+ * the derivative is that of `out`.  explicit_m: the 8 or 32 f64 entries of
+ * MATRIX1 / MATRIX2 (else NULL).  cblock = 1 asks for the 2x2 target block of
+ * CNOT / CNOTPOW.  out: d*d complex128 entries, row major, interleaved
+ * (re, im), host memory of at least 32 doubles; *dim = d (2 or 4).
+ * TQ_E_INVALID for an unknown opcode, a null pointer, or a derivative the gate
+ * does not have (gates without parameters, MATRIX1/2, SWAP). */
+tq_status tq_gate_matrix(int32_t op, const double *params, const double *explicit_m, int32_t cblock, int32_t deriv,
+                         int32_t which, double *out, int32_t *dim, double *phase);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *tq_last_error(void);

@@ -647,7 +647,9 @@ uint64_t orc_splitmix64(uint64_t seed, uint64_t counter)
 
 /* Integer fixed-point inverse-CDF sampling of one row from its probabilities:
  * w_i = floor(p_i * 2^62), W = sum w_i, r_k = floor(u_k * W / 2^64), and shot k
- * is the unique i with C_i <= r_k < C_i + w_i (C = exclusive prefix of w). */
+ * is the unique i with C_i <= r_k < C_i + w_i (C = exclusive prefix of w).
+ * A row with W = 0 has no distribution to draw from; every shot of it is the
+ * marker 2^64 - 1 (no bitstring of at most 34 qubits takes that value). */
 static int sample_row_from_p(const double *p, int64_t N, int64_t row, int64_t n_shots, uint64_t seed,
                              uint64_t *out)
 {
@@ -655,7 +657,11 @@ static int sample_row_from_p(const double *p, int64_t N, int64_t row, int64_t n_
     C[0] = 0;
     for (int64_t i = 0; i < N; i++) C[i + 1] = C[i] + (uint64_t)(p[i] * 0x1p62);
     uint64_t W = C[N];
-    if (W == 0) { free(C); return 1; }
+    if (W == 0) {
+        for (int64_t k = 0; k < n_shots; k++) out[k] = ~(uint64_t)0;
+        free(C);
+        return 0;
+    }
     for (int64_t k = 0; k < n_shots; k++) {
         uint64_t u = orc_splitmix64(seed, (uint64_t)(row * n_shots + k));
         uint64_t r = (uint64_t)(((unsigned __int128)u * W) >> 64);
@@ -687,7 +693,7 @@ int orc_sample_from_state(const float *state, int B, int n, int64_t n_shots, uin
         bad |= sample_row_from_p(p, N, b, n_shots, seed, out + (int64_t)b * n_shots);
         free(p);
     }
-    return bad ? fail("a row has zero total weight") : 0;
+    return bad ? fail("sampling failed") : 0;
 }
 
 /* full pipeline: simulate in complex128, then sample each row from its p */
@@ -705,7 +711,7 @@ int orc_sample(void *hp, const double *theta, int64_t n_shots, uint64_t seed, ui
         bad |= sample_row_from_p(p, N, b, n_shots, seed, out + (int64_t)b * n_shots);
         free(psi); free(p);
     }
-    return bad ? fail("a row has zero total weight") : 0;
+    return bad ? fail("sampling failed") : 0;
 }
 
 /* -------------------------------------------------- gate table accessors */

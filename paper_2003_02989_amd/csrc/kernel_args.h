@@ -201,6 +201,7 @@ struct SampArgs {
     int64_t n_shots;
     uint64_t seed;
     uint64_t *out;
+    int vec16;          // rows start 16-byte aligned (16-byte loads in level 1)
 };
 
 struct GatherArgs {

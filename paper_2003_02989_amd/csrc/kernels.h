@@ -20,6 +20,12 @@ struct ProfScope {
 };
 void profile_start(const char *kernel);
 hipError_t profile_read(int64_t *launches, double *total_ms);
+// The builder's gate table on the host: the matrix (deriv = 0) or its
+// derivative with respect to parameter `which` of opcode `op` at resolved
+// parameters eta, as the device builds it (without the global phase it leaves
+// out), in `form`; out receives d*d complex entries (re, im); returns d (0 for
+// an opcode without that matrix).
+int gate_table_host(int op, const double *eta, const double *ex, int form, int deriv, int which, double *out);
 size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat);
 size_t resident_lds_bytes(int n, int nacc, bool adjoint);
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);

@@ -10,6 +10,8 @@
 // floating-point atomics), so every output is bitwise reproducible.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cmath>
 #include <map>
 #include <mutex>
 #include <string>
@@ -29,25 +31,47 @@ namespace tq {
 // Gates whose matrix is a global phase times a matrix of simpler form are
 // built without that phase: RZ(theta) = e^{-i theta/2} diag(1, e^{i theta}),
 // RZZ(gamma) = e^{-i gamma/2} diag(1, e^{i gamma}, e^{i gamma}, 1) (entries
-// exactly 1), X^t, sqrt X, XX^t = e^{i pi t/2}(cos I - i sin G) (real
+// exactly 1), X^t, sqrt X, XX^t, YY^t = e^{i pi t/2}(cos I - i sin G) (real
 // diagonal, imaginary off-diagonal), Y^t, sqrt Y = e^{i pi t/2}(cos I - i sin
-// Y) (real); YY^t keeps its phase.  The phases of a row sum to one global
-// phase, a linear form in the parameters that the planner lists per group
-// (PhaseTerm), which the builder multiplies into the first qubit's
-// product-init matrix:
+// Y) (real).  The phases of a row sum to one global phase, a linear form in
+// the parameters that the planner lists per group (PhaseTerm), which the
+// builder multiplies into the first qubit's product-init matrix:
 // states and amplitudes come out with the gates' own phases, while every
 // intermediate state differs from its phased counterpart by a global phase
 // alone, which no expectation, gradient or probability sees.
+//
+// The table is callable from the host as well (gate_table_host), so that the
+// matrices and derivatives the builder forms can be checked on the CPU.
 struct cd {
     double x, y;
 };
-__device__ __forceinline__ cd C(double x, double y) { return cd{x, y}; }
-__device__ __forceinline__ cd cdmul(cd a, cd b) { return cd{a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x}; }
-__device__ __forceinline__ cd cdadd(cd a, cd b) { return cd{a.x + b.x, a.y + b.y}; }
-__device__ __forceinline__ cd cdscale(cd a, double s) { return cd{a.x * s, a.y * s}; }
+__host__ __device__ __forceinline__ cd C(double x, double y) { return cd{x, y}; }
+__host__ __device__ __forceinline__ cd cdmul(cd a, cd b) { return cd{a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x}; }
+__host__ __device__ __forceinline__ cd cdadd(cd a, cd b) { return cd{a.x + b.x, a.y + b.y}; }
+__host__ __device__ __forceinline__ cd cdscale(cd a, double s) { return cd{a.x * s, a.y * s}; }
+
+// sin and cos of x, and of pi x
+__host__ __device__ __forceinline__ void sc(double x, double *s, double *c)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    sincos(x, s, c);
+#else
+    *s = std::sin(x);
+    *c = std::cos(x);
+#endif
+}
+__host__ __device__ __forceinline__ void scpi(double x, double *s, double *c)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    sincospi(x, s, c);
+#else
+    *s = std::sin(M_PI * x);
+    *c = std::cos(M_PI * x);
+#endif
+}
 
 // m: row-major d x d, zero-initialised by the caller
-__device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const double *ex, int form, cd *m)
+__host__ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const double *ex, int form, cd *m)
 {
     const double r = 0.70710678118654752440;
     double c, s;
@@ -57,16 +81,16 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
     case OP_Y: m[1] = C(0, -1); m[2] = C(0, 1); return 2;
     case OP_Z: m[0] = C(1, 0); m[3] = C(-1, 0); return 2;
     case OP_RX:
-        sincos(eta[0] * 0.5, &s, &c);
+        sc(eta[0] * 0.5, &s, &c);
         m[0] = C(c, 0); m[1] = C(0, -s); m[2] = C(0, -s); m[3] = C(c, 0); return 2;
     case OP_RY:
-        sincos(eta[0] * 0.5, &s, &c);
+        sc(eta[0] * 0.5, &s, &c);
         m[0] = C(c, 0); m[1] = C(-s, 0); m[2] = C(s, 0); m[3] = C(c, 0); return 2;
     case OP_RZ:
-        sincos(eta[0], &s, &c);
+        sc(eta[0], &s, &c);
         m[0] = C(1, 0); m[3] = C(c, s); return 2;
     case OP_XPOW: case OP_SQRTX: case OP_YPOW: case OP_SQRTY: {
-        sincospi(0.5 * (op == OP_XPOW || op == OP_YPOW ? eta[0] : 0.5), &s, &c);
+        scpi(0.5 * (op == OP_XPOW || op == OP_YPOW ? eta[0] : 0.5), &s, &c);
         m[0] = m[3] = C(c, 0);
         if (op == OP_XPOW || op == OP_SQRTX) { m[1] = m[2] = C(0, -s); }
         else { m[1] = C(-s, 0); m[2] = C(s, 0); }
@@ -74,7 +98,7 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
     }
     case OP_ZPOW: case OP_SQRTW: {
         double t = op == OP_SQRTW ? 0.5 : eta[0];
-        sincospi(t, &s, &c);
+        scpi(t, &s, &c);
         cd a = C(0.5 * (1 + c), 0.5 * s);   // (1 + w) / 2
         cd bq = C(0.5 * (1 - c), -0.5 * s); // (1 - w) / 2
         if (op == OP_ZPOW) { m[0] = C(1, 0); m[3] = C(c, s); return 2; }
@@ -85,40 +109,40 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
     case OP_CZ:
         m[0] = m[5] = m[10] = C(1, 0); m[15] = C(-1, 0); return 4;
     case OP_CZPOW:
-        sincospi(eta[0], &s, &c);
+        scpi(eta[0], &s, &c);
         m[0] = m[5] = m[10] = C(1, 0); m[15] = C(c, s); return 4;
     case OP_CNOT:
         if (form == FORM_CBLOCK) { m[1] = m[2] = C(1, 0); return 2; }
         m[0] = m[5] = C(1, 0); m[11] = m[14] = C(1, 0); return 4;
     case OP_CNOTPOW: {
-        sincospi(eta[0], &s, &c);
+        scpi(eta[0], &s, &c);
         cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
         if (form == FORM_CBLOCK) { m[0] = m[3] = a; m[1] = m[2] = bq; return 2; }
         m[0] = m[5] = C(1, 0); m[10] = m[15] = a; m[11] = m[14] = bq; return 4;
     }
-    case OP_XXPOW: {
-        sincospi(0.5 * eta[0], &s, &c);
+    case OP_XXPOW: {  // cos I - i sin XX; XX couples 00 with 11 and 01 with 10, all with +1
+        scpi(0.5 * eta[0], &s, &c);
         m[0] = m[5] = m[10] = m[15] = C(c, 0);
         m[3] = m[6] = m[9] = m[12] = C(0, -s);
         return 4;
     }
-    case OP_YYPOW: {  // with its phase: (1+w)/2 I + (1-w)/2 YY
-        sincospi(eta[0], &s, &c);
-        const cd a = C(0.5 * (1 + c), 0.5 * s), bq = C(0.5 * (1 - c), -0.5 * s);
-        m[0] = m[5] = m[10] = m[15] = a;
-        m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq;  // YY: -|11><00| - |00><11| + |10><01| + |01><10|
+    case OP_YYPOW: {  // cos I - i sin YY; YY = -|11><00| - |00><11| + |10><01| + |01><10|
+        scpi(0.5 * eta[0], &s, &c);
+        m[0] = m[5] = m[10] = m[15] = C(c, 0);
+        m[3] = m[12] = C(0, s);
+        m[6] = m[9] = C(0, -s);
         return 4;
     }
     case OP_ZZPOW:
-        sincospi(eta[0], &s, &c);
+        scpi(eta[0], &s, &c);
         m[0] = m[15] = C(1, 0); m[5] = m[10] = C(c, s); return 4;
     case OP_RZZ:
-        sincos(eta[0], &s, &c);
+        sc(eta[0], &s, &c);
         m[0] = m[15] = C(1, 0); m[5] = m[10] = C(c, s); return 4;
     case OP_FSIM:
-        sincos(eta[0], &s, &c);
+        sc(eta[0], &s, &c);
         m[0] = C(1, 0); m[5] = m[10] = C(c, 0); m[6] = m[9] = C(0, -s);
-        sincos(eta[1], &s, &c);
+        sc(eta[1], &s, &c);
         m[15] = C(c, -s); return 4;
     case OP_SWAP:
         m[0] = m[6] = m[9] = m[15] = C(1, 0); return 4;
@@ -132,37 +156,41 @@ __device__ __forceinline__ int gate_matrix_dev(int op, const double *eta, const 
     return 0;
 }
 
-// derivative with respect to parameter `which` (m zero-initialised)
-__device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd *m)
+// derivative of gate_matrix_dev (the matrix as built, without its left-out
+// phase) with respect to parameter `which` (m zero-initialised)
+__host__ __device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int which, int form, cd *m)
 {
     double c, s;
     const double pi = 3.14159265358979323846;
     switch (op) {
     case OP_RX:
-        sincos(eta[0] * 0.5, &s, &c);
+        sc(eta[0] * 0.5, &s, &c);
         m[0] = C(-0.5 * s, 0); m[1] = C(0, -0.5 * c); m[2] = C(0, -0.5 * c); m[3] = C(-0.5 * s, 0); return 2;
     case OP_RY:
-        sincos(eta[0] * 0.5, &s, &c);
+        sc(eta[0] * 0.5, &s, &c);
         m[0] = C(-0.5 * s, 0); m[1] = C(-0.5 * c, 0); m[2] = C(0.5 * c, 0); m[3] = C(-0.5 * s, 0); return 2;
     case OP_RZ:  // d/dtheta diag(1, e^{i theta})
-        sincos(eta[0], &s, &c);
+        sc(eta[0], &s, &c);
         m[3] = C(-s, c); return 2;
     case OP_RZZ:
-        sincos(eta[0], &s, &c);
+        sc(eta[0], &s, &c);
         m[5] = m[10] = C(-s, c); return 4;
-    case OP_XPOW: case OP_YPOW: case OP_XXPOW: {
-        // d/dt (cos(pi t/2) I - i sin(pi t/2) G) = (pi/2)(-sin I - i cos G)
-        sincospi(0.5 * eta[0], &s, &c);
+    case OP_XPOW: case OP_YPOW: case OP_XXPOW: case OP_YYPOW: {
+        // d/dt (cos(pi t/2) I - i sin(pi t/2) G) = (pi/2)(-sin I - i cos G): the
+        // diagonal a, and bq times each entry of G
+        scpi(0.5 * eta[0], &s, &c);
         const cd a = C(-0.5 * pi * s, 0), bq = C(0, -0.5 * pi * c);
         switch (op) {
         case OP_XPOW: m[0] = m[3] = a; m[1] = m[2] = bq; return 2;
         case OP_YPOW: m[0] = m[3] = a; m[1] = C(-0.5 * pi * c, 0); m[2] = C(0.5 * pi * c, 0); return 2;
-        default: m[0] = m[5] = m[10] = m[15] = a; m[3] = m[6] = m[9] = m[12] = bq; return 4;
+        case OP_XXPOW: m[0] = m[5] = m[10] = m[15] = a; m[3] = m[6] = m[9] = m[12] = bq; return 4;
+        default:  // YY: -1 on (00, 11) and (11, 00), +1 on (01, 10) and (10, 01)
+            m[0] = m[5] = m[10] = m[15] = a; m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq; return 4;
         }
     }
-    case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW: case OP_ZZPOW: case OP_YYPOW: {
+    case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW: case OP_ZZPOW: {
         // d/dt G^t = (i pi w / 2)(I - G), w = e^{i pi t}
-        sincospi(eta[0], &s, &c);
+        scpi(eta[0], &s, &c);
         cd k = C(-0.5 * pi * s, 0.5 * pi * c);  // i pi w / 2
         cd mk = cdscale(k, -1);
         switch (op) {
@@ -171,17 +199,15 @@ __device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int whi
         case OP_CNOTPOW:
             if (form == FORM_CBLOCK) { m[0] = m[3] = k; m[1] = m[2] = mk; return 2; }
             m[10] = m[15] = k; m[11] = m[14] = mk; return 4;
-        case OP_ZZPOW: m[5] = m[10] = cdscale(k, 2); return 4;
-        case OP_YYPOW: m[0] = m[5] = m[10] = m[15] = k; m[3] = m[12] = k; m[6] = m[9] = mk; return 4;
+        default: m[5] = m[10] = cdscale(k, 2); return 4;  // ZZPOW
         }
-        return 0;
     }
     case OP_FSIM:
         if (which == 0) {
-            sincos(eta[0], &s, &c);
+            sc(eta[0], &s, &c);
             m[5] = m[10] = C(-s, 0); m[6] = m[9] = C(0, -c);
         } else {
-            sincos(eta[1], &s, &c);
+            sc(eta[1], &s, &c);
             m[15] = C(-s, -c);  // -i e^{-i phi}
         }
         return 4;
@@ -189,8 +215,20 @@ __device__ __forceinline__ int gate_deriv_dev(int op, const double *eta, int whi
     return 0;
 }
 
+int gate_table_host(int op, const double *eta, const double *ex, int form, int deriv, int which, double *out)
+{
+    cd m[16];
+    for (int i = 0; i < 16; i++) m[i] = C(0, 0);
+    const int d = deriv ? gate_deriv_dev(op, eta, which, form, m) : gate_matrix_dev(op, eta, ex, form, m);
+    for (int i = 0; i < d * d; i++) {
+        out[2 * i] = m[i].x;
+        out[2 * i + 1] = m[i].y;
+    }
+    return d;
+}
+
 // permutation of a 4x4 two-qubit matrix for reversed qubit order (|ab> -> |ba>)
-__device__ __forceinline__ void swap_qubits4(cd *m)
+__host__ __device__ __forceinline__ void swap_qubits4(cd *m)
 {
     cd t[16];
 #pragma unroll
@@ -324,7 +362,7 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     __syncthreads();
     if (threadIdx.x == 0) {
         double s, co;
-        sincos(part[0] + part[1] + part[2] + part[3], &s, &co);
+        sc(part[0] + part[1] + part[2] + part[3], &s, &co);
         double2 *out = a.mats + (int64_t)row * a.mat_stride + a.phase_out;
         for (int i = 0; i < 4; i++) {
             const double2 v = out[i];
@@ -748,19 +786,42 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v)
     return v;
 }
 
-// level 1: sum of the weights of each group of 64 amplitudes
+// Level 1: the sum of the weights of each group of 64 amplitudes, streamed
+// from HBM.  Eight consecutive lanes share a group: lane j of it sums the
+// weights of amplitudes 8j .. 8j+7, read with four 16-byte loads when the row
+// is 16-byte aligned (vec16), and the eight partial sums are added over the
+// lanes.  Grid-stride over the groups of the row (integer sums: the order
+// does not matter).
 __global__ __launch_bounds__(256) void k_samp_l1(SampArgs a)
 {
     const int row = blockIdx.y;
     const int sr = a.rows ? a.rows[row] : row;
-    const int64_t grp = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
-    const int lane = threadIdx.x % 64;
-    if (grp >= a.count[1]) return;
-    const int64_t i = grp * 64 + lane;
     const float2 *st = a.state + (int64_t)sr * a.row_stride;
-    uint64_t wv = i < a.count[0] ? weight_of(st[i]) : 0;
-    wv = wave_sum_u64(wv);
-    if (lane == 0) a.levels[(int64_t)row * a.row_level + a.off[1] + grp] = wv;
+    uint64_t *out = a.levels + (int64_t)row * a.row_level + a.off[1];
+    const int64_t N = a.count[0], ngrp = a.count[1];
+    const int sub = threadIdx.x & 7;
+    const int64_t stride = ((int64_t)gridDim.x * blockDim.x) >> 3;
+    for (int64_t grp = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 3; grp < ngrp; grp += stride) {
+        const int64_t i0 = grp * 64 + sub * 8;
+        uint64_t w = 0;
+        if (a.vec16 && i0 + 8 <= N) {
+            const float4 *p = reinterpret_cast<const float4 *>(st + i0);
+            float4 v[4];
+#pragma unroll
+            for (int k = 0; k < 4; k++) v[k] = p[k];
+#pragma unroll
+            for (int k = 0; k < 4; k++) w += weight_of(make_float2(v[k].x, v[k].y)) + weight_of(make_float2(v[k].z, v[k].w));
+        } else {
+            for (int e = 0; e < 8; e++)
+                if (i0 + e < N) w += weight_of(st[i0 + e]);
+        }
+        // the eight lanes of a group are consecutive and take the same trip
+        // count, so they are active together here
+        w += __shfl_xor(w, 1, 8);
+        w += __shfl_xor(w, 2, 8);
+        w += __shfl_xor(w, 4, 8);
+        if (sub == 0) out[grp] = w;
+    }
 }
 
 // level k+1 from level k
@@ -809,7 +870,9 @@ __global__ __launch_bounds__(256) void k_samp_shots(SampArgs a)
     const uint64_t W = wave_sum_u64(tv);
     uint64_t *out = a.out + (int64_t)b * a.n_shots + shot;
     if (W == 0) {
-        if (lane == 0) *out = 0;
+        // no distribution to draw from (an all-zero row): every shot is the
+        // marker 2^64 - 1, which no bitstring of at most 32 qubits equals
+        if (lane == 0) *out = ~0ull;
         return;
     }
     const uint64_t u = splitmix64(a.seed, (uint64_t)b * (uint64_t)a.n_shots + (uint64_t)shot);
@@ -1088,7 +1151,10 @@ hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s)
     if (a.nlev >= 1) {
         {
             prof::Scope ps("samp_l1", s);
-            hipLaunchKernelGGL(k_samp_l1, dim3((unsigned)((a.count[1] + 3) / 4), nrows), dim3(256), 0, s, a);
+            // eight lanes per group of 64 amplitudes, at most 8192 workgroups
+            // over all rows (grid-stride beyond)
+            const int64_t blocks = std::min<int64_t>((a.count[1] * 8 + 255) / 256, std::max(1, 8192 / nrows));
+            hipLaunchKernelGGL(k_samp_l1, dim3((unsigned)blocks, nrows), dim3(256), 0, s, a);
         }
         for (int k = 1; k < a.nlev; k++)
             hipLaunchKernelGGL(k_samp_up, dim3((unsigned)((a.count[k + 1] + 3) / 4), nrows), dim3(256), 0, s, a, k);

@@ -622,7 +622,7 @@ uint8_t gate_hint(int op, bool cblock)
     case OP_RY: case OP_H: return kHintReal;  // real for every angle, and so is dRY/dtheta
     case OP_RX: return kHintRX;               // cos on the diagonal, -i sin off it
     // power gates without their global phase e^{i pi t/2}: cos I - i sin G
-    case OP_XPOW: case OP_SQRTX: case OP_XXPOW: return kHintRX;
+    case OP_XPOW: case OP_SQRTX: case OP_XXPOW: case OP_YYPOW: return kHintRX;
     case OP_YPOW: case OP_SQRTY: return kHintReal;
     default: return 0;
     }
@@ -757,11 +757,23 @@ bool gate_phase(int op, double *c, bool *constant)
     *constant = false;
     switch (op) {
     case OP_RZ: case OP_RZZ: *c = -0.5; return true;
-    case OP_XPOW: case OP_YPOW: case OP_XXPOW: *c = 0.5 * M_PI; return true;
+    case OP_XPOW: case OP_YPOW: case OP_XXPOW: case OP_YYPOW: *c = 0.5 * M_PI; return true;
     case OP_SQRTX: case OP_SQRTY: *c = 0.25 * M_PI; *constant = true; return true;
     default: return false;
     }
 }
+
+} // namespace
+
+double gate_left_out_phase(int op, double eta)
+{
+    double c;
+    bool constant;
+    if (!gate_phase(op, &c, &constant)) return 0.0;
+    return constant ? c : c * eta;
+}
+
+namespace {
 
 // Arithmetic per amplitude (fp64 instructions) of a single-qubit op fusing
 // `mem` in a generated kernel: diagonal 2 per entry that is not exactly 1,

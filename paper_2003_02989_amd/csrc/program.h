@@ -135,6 +135,11 @@ struct ObsData {
     uint64_t id = 0;
 };
 
+// The global phase (radians) the device builder leaves out of the matrix of
+// gate `op` with first parameter eta: the full gate matrix is e^{i phase}
+// times the one built.
+double gate_left_out_phase(int op, double eta);
+
 std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt);
 std::unique_ptr<ObsData> parse_observables(const void *blob, size_t nbytes);
 

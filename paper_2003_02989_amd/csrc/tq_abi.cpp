@@ -1047,14 +1047,24 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
 
 tq_status tq_sample(tq_program prog, const float *theta, int64_t n_shots, uint64_t seed, uint64_t *out, void *stream)
 {
+    return tq_sample_with_amplitudes(prog, theta, n_shots, seed, out, nullptr, 0, nullptr, stream);
+}
+
+tq_status tq_sample_with_amplitudes(tq_program prog, const float *theta, int64_t n_shots, uint64_t seed, uint64_t *out,
+                                    const uint64_t *bitstrings, int64_t M, void *amps, void *stream)
+{
     return guarded([&] {
         if (!prog) fail(TQ_E_INVALID, "program is NULL");
         if (n_shots < 0) fail(TQ_E_INVALID, "n_shots is negative");
+        if (M < 0) fail(TQ_E_INVALID, "M is negative");
         const ProgramData &pd = *prog->pd;
-        if (pd.B == 0 || n_shots == 0) return;
-        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        if (pd.B == 0 || (n_shots == 0 && M == 0)) return;
+        if (n_shots > 0 && !out) fail(TQ_E_INVALID, "out is NULL");
+        if (M > 0 && (!bitstrings || !amps)) fail(TQ_E_INVALID, "bitstrings or amps is NULL");
         if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
         check_align(out, 8, "out");
+        check_align(bitstrings, 8, "bitstrings");
+        check_align(amps, 8, "amps");
         check_align(theta, 4, "symbol_values");
         ensure_device(prog);
         hipStream_t s = as_stream(stream);
@@ -1063,9 +1073,23 @@ tq_status tq_sample(tq_program prog, const float *theta, int64_t n_shots, uint64
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
             forward_to_ws(prog, gi, theta, psi + gd.psi_off, s);
+            if (M > 0) {
+                GatherArgs ga{};
+                ga.state = psi + gd.psi_off;
+                ga.row_stride = (int64_t)1 << g.n;
+                ga.rows = (const int32_t *)gd.ident.p;
+                ga.brows = (const int32_t *)gd.rows.p;
+                ga.n = g.n;
+                ga.bits = bitstrings;
+                ga.M = M;
+                ga.out = (float2 *)amps;
+                hip_check(launch_gather(ga, (int)g.rows.size(), s), "gather launch");
+            }
+            if (n_shots == 0) continue;
             SampArgs a{};
             a.state = psi + gd.psi_off;
             a.row_stride = (int64_t)1 << g.n;
+            a.vec16 = g.n >= 1;  // workspace rows are 512-byte aligned, 2^n amplitudes apart
             a.rows = (const int32_t *)gd.ident.p;
             a.brows = (const int32_t *)gd.rows.p;
             fill_levels(a, g.n);
@@ -1125,6 +1149,7 @@ tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t
         SampArgs a{};
         a.state = (const float2 *)states;
         a.row_stride = (int64_t)1 << n;
+        a.vec16 = reinterpret_cast<uintptr_t>(states) % 16 == 0 && n >= 1;
         fill_levels(a, n);
         // stream-ordered workspace: allocated and released in the stream's order
         void *lv = nullptr;
@@ -1161,6 +1186,23 @@ tq_status tq_amplitudes_from_state(const void *states, int32_t B, int32_t n, con
         a.M = M;
         a.out = (float2 *)amps;
         hip_check(launch_gather(a, B, as_stream(stream)), "gather launch");
+    });
+}
+
+tq_status tq_gate_matrix(int32_t op, const double *params, const double *explicit_m, int32_t cblock, int32_t deriv,
+                         int32_t which, double *out, int32_t *dim, double *phase)
+{
+    return guarded([&] {
+        if (!out || !dim || !phase) fail(TQ_E_INVALID, "out, dim or phase is NULL");
+        if (op < 1 || op >= OP_COUNT) fail(TQ_E_INVALID, "unknown opcode");
+        const bool expl = op == OP_MATRIX1 || op == OP_MATRIX2;
+        if (expl && !explicit_m) fail(TQ_E_INVALID, "explicit matrix is NULL");
+        double eta[2] = {params ? params[0] : 0.0, params ? params[1] : 0.0};
+        const int form = cblock && (op == OP_CNOT || op == OP_CNOTPOW) ? FORM_CBLOCK : FORM_FULL;
+        const int d = gate_table_host(op, eta, explicit_m, form, deriv ? 1 : 0, which, out);
+        if (d == 0) fail(TQ_E_INVALID, deriv ? "the gate has no derivative" : "unknown opcode");
+        *dim = d;
+        *phase = gate_left_out_phase(op, eta[0]);
     });
 }
 

@@ -56,16 +56,20 @@ def lib():
         L.tq_simulate_state.argtypes = [vp, vp, vp, vp]
         L.tq_expectation.argtypes = [vp, vp, vp, vp, vp]
         L.tq_sample.argtypes = [vp, vp, i64, u64, vp, vp]
+        L.tq_sample_with_amplitudes.argtypes = [vp, vp, i64, u64, vp, vp, i64, vp, vp]
         L.tq_adjoint_grad.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.tq_amplitudes.argtypes = [vp, vp, vp, i64, vp, vp]
         L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
         L.tq_amplitudes_from_state.argtypes = [vp, i32, i32, vp, i64, vp, vp]
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
+        L.tq_gate_matrix.argtypes = [i32, vp, vp, i32, i32, i32, vp, p32, ctypes.POINTER(ctypes.c_double)]
         L.tq_profile_start.argtypes = [ctypes.c_char_p]
         L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
         for f in ("tq_program_create", "tq_program_info", "tq_program_specialize", "tq_observables_create", "tq_observables_info",
-                  "tq_simulate_state", "tq_expectation", "tq_sample", "tq_adjoint_grad", "tq_amplitudes",
-                  "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read"):
+                  "tq_simulate_state", "tq_expectation", "tq_sample", "tq_sample_with_amplitudes", "tq_adjoint_grad",
+                  "tq_amplitudes",
+                  "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read",
+                  "tq_gate_matrix"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -153,6 +157,28 @@ def describe(prog):
     return json.loads(buf.value.decode())
 
 
+def gate_matrix(op, params=(), explicit=None, cblock=False, deriv=False, which=0):
+    """(matrix, phase) of the library's gate table (tq_gate_matrix, host
+    only): numpy complex128 [d, d] as the builder forms it and the global
+    phase it leaves out (the gate's matrix is exp(1j * phase) * matrix)."""
+    import numpy as np
+    p = np.zeros(2, dtype=np.float64)
+    p[: len(params)] = params
+    ex = None
+    if explicit is not None:
+        m = np.asarray(explicit, np.complex128).ravel()
+        ex = np.ascontiguousarray(np.stack([m.real, m.imag], axis=1).ravel())
+    out = np.zeros(32, dtype=np.float64)
+    d = ctypes.c_int32()
+    ph = ctypes.c_double()
+    _check(lib().tq_gate_matrix(int(op), ctypes.c_void_p(p.ctypes.data),
+                                ctypes.c_void_p(ex.ctypes.data) if ex is not None else None, 1 if cblock else 0,
+                                1 if deriv else 0, int(which), ctypes.c_void_p(out.ctypes.data), ctypes.byref(d),
+                                ctypes.byref(ph)))
+    k = d.value
+    return out[: 2 * k * k].view(np.complex128).reshape(k, k).copy(), ph.value
+
+
 def profile_start(kernel):
     _check(lib().tq_profile_start(kernel.encode() if kernel else None))
 
@@ -215,6 +241,22 @@ def amplitudes(prog, symbol_values, bitstrings, out=None, stream=None):
     p = _dev(out, torch.complex64, (prog.B, M), "amps")
     _check(lib().tq_amplitudes(prog._h, _theta(prog, symbol_values), b, M, p, _stream(stream)))
     return out
+
+
+def sample_with_amplitudes(prog, symbol_values, n_shots, seed, bitstrings, out=None, amps=None, stream=None):
+    """One simulation, both outputs: (samples int64 [B, n_shots], amplitudes
+    complex64 [B, M]) at bitstrings int64 [B, M]."""
+    M = bitstrings.shape[1]
+    b = _dev(bitstrings, torch.int64, (prog.B, M), "bitstrings")
+    if out is None:
+        out = torch.empty((prog.B, n_shots), dtype=torch.int64, device="cuda")
+    if amps is None:
+        amps = torch.empty((prog.B, M), dtype=torch.complex64, device="cuda")
+    p = _dev(out, torch.int64, (prog.B, n_shots), "out")
+    a = _dev(amps, torch.complex64, (prog.B, M), "amps")
+    _check(lib().tq_sample_with_amplitudes(prog._h, _theta(prog, symbol_values), int(n_shots), ctypes.c_uint64(seed),
+                                           p, b, M, a, _stream(stream)))
+    return out, amps
 
 
 def sample_from_state(states, n_shots, seed, out=None, stream=None):

@@ -307,3 +307,20 @@ def random_batch(seed, B, n, n_gates, n_symbols, K=2, hetero=False, **kw):
 
 
 CONFIGS = {"c1": c1_hea, "c2": c2_qnn, "c3": c3_qaoa, "c4": c4_random, "c5": c5_vqe}
+
+
+def fresh_thetas(w, count, seed):
+    """`count` further symbol-value arrays [B, S] drawn like the workload's
+    own: U[0, pi) for the QAOA angles, one shared U[0, 2 pi) row for the QNN,
+    U[0, 2 pi) per entry otherwise (a new parameter set per benchmark step)."""
+    rng = rng_for(seed)
+    out = []
+    for _ in range(count):
+        if w.name.startswith("c3"):
+            th = rng.uniform(0.0, math.pi, size=w.theta.shape)
+        elif w.name.startswith("c2"):
+            th = np.broadcast_to(rng.uniform(0.0, 2 * math.pi, size=w.theta.shape[1]), w.theta.shape)
+        else:
+            th = rng.uniform(0.0, 2 * math.pi, size=w.theta.shape)
+        out.append(np.ascontiguousarray(th, dtype=np.float32))
+    return out

@@ -241,3 +241,34 @@ def test_specialized_group_without_symbols():
     w.circuits[0] = wl.random_circuit(wl.rng_for(7301), 13, 40, 3, p_symbolic=0.0)
     say("specialised group without symbols")
     compare(gpu_outputs(w, max_tile_qubits=10, specialize=True), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("specialize", [False, True])
+@pytest.mark.parametrize("n,tile", [(2, 0), (13, 10)])
+def test_yy_power_gradient(specialize, n, tile):
+    # Y⊗Y^t built without its global phase: the adjoint gradient through it
+    # (derivative matrices in the precompiled kernels, the gate's generator in
+    # the generated ones), resident (n = 2) and in tile passes (n = 13,
+    # 10-bit tiles), against the oracle
+    from paper_2003_02989_amd.circuits import Circuit, sym
+    c = Circuit(n).add("H", 0).add("RX", 1, [sym(1)]).add("YYPOW", (0, n - 1), [sym(0)])
+    c.add("CNOT", (n - 1, 0)).add("YYPOW", (1, 0), [sym(0, 0.5, 0.1)])
+    obs = [[(1.0, [(0, "Z")]), (0.5, [(0, "X"), (n - 1, "X")]), (-0.7, [(1, "Y")]), (0.3, [(0, "Y"), (1, "Y")])]]
+    th = np.array([[0.37, 0.3], [-1.1, 2.0]], np.float32)
+    w = wl.Workload("yy", [c, c], 2, th, [obs, obs], np.array([[1.0], [-0.6]], np.float32))
+    say("YY^t gradient n", n, "specialize", specialize)
+    compare(gpu_outputs(w, max_tile_qubits=tile, specialize=specialize), oracle_outputs(w))
+
+
+def test_sampler_zero_row_marker():
+    # a row without weight yields 2^64 - 1 for every shot on both sides; the
+    # other rows are drawn as usual, bit-exact with the oracle
+    rng = np.random.default_rng(4)
+    z = (rng.standard_normal((3, 1 << 9)) + 1j * rng.standard_normal((3, 1 << 9))).astype(np.complex64)
+    z /= np.linalg.norm(z, axis=1, keepdims=True)
+    z = z.astype(np.complex64)
+    z[1] = 0
+    g = tq.sample_from_state(dev(z, torch.complex64), 3000, seed=8).cpu().numpy().astype(np.uint64)
+    r = orc.sample_from_state(z, 3000, seed=8)
+    assert np.all(g[1] == np.uint64(2**64 - 1))
+    assert np.array_equal(g, r)

@@ -52,3 +52,18 @@ def test_rows_use_distinct_counters_and_seed_changes_stream():
     b = orc.sample_from_state(z, 100, seed=10)
     assert not np.array_equal(a, b)
     assert np.array_equal(a, orc.sample_from_state(z, 100, seed=9))
+
+
+def test_zero_row_gives_the_marker():
+    # a row with no weight has no distribution: every shot is 2^64 - 1 (no
+    # bitstring of at most 34 qubits), and the other rows draw as usual
+    z = np.zeros((3, 32), np.complex64)
+    z[0, 5] = 1.0
+    z[2, [1, 30]] = [0.6, 0.8]
+    s = orc.sample_from_state(z, 400, seed=17)
+    assert np.all(s[1] == np.uint64(2**64 - 1))
+    assert np.all(s[0] == 5)
+    assert set(np.unique(s[2]).tolist()) <= {1, 30}
+    alone = orc.sample_from_state(z[2:], 400, seed=17)
+    # row 2 of the batch uses counters 2 * 400 + k, row 0 of `alone` 0 * 400 + k
+    assert alone.shape == (1, 400)
