@@ -238,6 +238,18 @@ tq_status tq_profile_read(int64_t *launches, double *total_ms);
 tq_status tq_gate_matrix(int32_t op, const double *params, const double *explicit_m, int32_t cblock, int32_t deriv,
                          int32_t which, double *out, int32_t *dim, double *phase);
 
+/* The matrix builder's output, for checks: resolves the symbols and builds
+ * every matrix of every structure group (forward products, W^dagger and
+ * dW/deta of the reverse sweep, dense stage matrices) exactly as a call of
+ * tq_adjoint_grad would, then copies each group's row blocks, groups in the
+ * order of tq_program_describe, rows in its "row_ids" order, into out:
+ * complex128 (re, im) device array of cap entries.  *entries (may be NULL)
+ * receives the number of entries needed (sum over groups of rows x
+ * mat_block); with out = NULL only that is returned.  The layout of a block
+ * is the "tasks" list of tq_program_describe. */
+tq_status tq_build_matrices(tq_program prog, const float *symbol_values, void *out, int64_t cap, int64_t *entries,
+                            void *stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *tq_last_error(void);
 const char *tq_version(void);

@@ -48,7 +48,6 @@ struct cd {
 __host__ __device__ __forceinline__ cd C(double x, double y) { return cd{x, y}; }
 __host__ __device__ __forceinline__ cd cdmul(cd a, cd b) { return cd{a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x}; }
 __host__ __device__ __forceinline__ cd cdadd(cd a, cd b) { return cd{a.x + b.x, a.y + b.y}; }
-__host__ __device__ __forceinline__ cd cdscale(cd a, double s) { return cd{a.x * s, a.y * s}; }
 
 // sin and cos of x, and of pi x
 __host__ __device__ __forceinline__ void sc(double x, double *s, double *c)
@@ -177,29 +176,30 @@ __host__ __device__ __forceinline__ int gate_deriv_dev(int op, const double *eta
         m[5] = m[10] = C(-s, c); return 4;
     case OP_XPOW: case OP_YPOW: case OP_XXPOW: case OP_YYPOW: {
         // d/dt (cos(pi t/2) I - i sin(pi t/2) G) = (pi/2)(-sin I - i cos G): the
-        // diagonal a, and bq times each entry of G
+        // diagonal ds, and -i dc times each entry of G.  Every entry is its own
+        // expression (a negated copy of a complex value with a zero part has
+        // been compiled for the device with the sign of only one part flipped).
         scpi(0.5 * eta[0], &s, &c);
-        const cd a = C(-0.5 * pi * s, 0), bq = C(0, -0.5 * pi * c);
+        const double ds = -0.5 * pi * s, dc = 0.5 * pi * c;
         switch (op) {
-        case OP_XPOW: m[0] = m[3] = a; m[1] = m[2] = bq; return 2;
-        case OP_YPOW: m[0] = m[3] = a; m[1] = C(-0.5 * pi * c, 0); m[2] = C(0.5 * pi * c, 0); return 2;
-        case OP_XXPOW: m[0] = m[5] = m[10] = m[15] = a; m[3] = m[6] = m[9] = m[12] = bq; return 4;
+        case OP_XPOW: m[0] = m[3] = C(ds, 0); m[1] = m[2] = C(0, -dc); return 2;
+        case OP_YPOW: m[0] = m[3] = C(ds, 0); m[1] = C(-dc, 0); m[2] = C(dc, 0); return 2;
+        case OP_XXPOW: m[0] = m[5] = m[10] = m[15] = C(ds, 0); m[3] = m[6] = m[9] = m[12] = C(0, -dc); return 4;
         default:  // YY: -1 on (00, 11) and (11, 00), +1 on (01, 10) and (10, 01)
-            m[0] = m[5] = m[10] = m[15] = a; m[3] = m[12] = cdscale(bq, -1); m[6] = m[9] = bq; return 4;
+            m[0] = m[5] = m[10] = m[15] = C(ds, 0); m[3] = m[12] = C(0, dc); m[6] = m[9] = C(0, -dc); return 4;
         }
     }
     case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW: case OP_ZZPOW: {
-        // d/dt G^t = (i pi w / 2)(I - G), w = e^{i pi t}
+        // d/dt G^t = (i pi w / 2)(I - G), w = e^{i pi t}: i pi w / 2 = (kx, ky)
         scpi(eta[0], &s, &c);
-        cd k = C(-0.5 * pi * s, 0.5 * pi * c);  // i pi w / 2
-        cd mk = cdscale(k, -1);
+        const double kx = -0.5 * pi * s, ky = 0.5 * pi * c;
         switch (op) {
-        case OP_ZPOW: m[3] = cdscale(k, 2); return 2;
-        case OP_CZPOW: m[15] = cdscale(k, 2); return 4;
+        case OP_ZPOW: m[3] = C(2 * kx, 2 * ky); return 2;
+        case OP_CZPOW: m[15] = C(2 * kx, 2 * ky); return 4;
         case OP_CNOTPOW:
-            if (form == FORM_CBLOCK) { m[0] = m[3] = k; m[1] = m[2] = mk; return 2; }
-            m[10] = m[15] = k; m[11] = m[14] = mk; return 4;
-        default: m[5] = m[10] = cdscale(k, 2); return 4;  // ZZPOW
+            if (form == FORM_CBLOCK) { m[0] = m[3] = C(kx, ky); m[1] = m[2] = C(-kx, -ky); return 2; }
+            m[10] = m[15] = C(kx, ky); m[11] = m[14] = C(-kx, -ky); return 4;
+        default: m[5] = m[10] = C(2 * kx, 2 * ky); return 4;  // ZZPOW
         }
     }
     case OP_FSIM:

@@ -1189,6 +1189,34 @@ tq_status tq_amplitudes_from_state(const void *states, int32_t B, int32_t n, con
     });
 }
 
+tq_status tq_build_matrices(tq_program prog, const float *theta, void *out, int64_t cap, int64_t *entries, void *stream)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        const ProgramData &pd = *prog->pd;
+        int64_t total = 0;
+        for (auto &gp : pd.groups) total += (int64_t)gp->rows.size() * std::max(gp->mat_block, 1);
+        if (entries) *entries = total;
+        if (!out) return;
+        if (cap < total) fail(TQ_E_INVALID, "out holds fewer than the needed entries");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(out, 16, "out");
+        ensure_device(prog);
+        hipStream_t s = as_stream(stream);
+        int64_t off = 0;
+        for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+            const Group &g = *pd.groups[gi];
+            GroupDev &gd = *prog->gdev[gi];
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
+            const size_t n = g.rows.size() * (size_t)std::max(g.mat_block, 1);
+            hip_check(hipMemcpyAsync((double2 *)out + off, mat_ws(prog) + gd.mat_off, n * sizeof(double2),
+                                     hipMemcpyDeviceToDevice, s),
+                      "matrix copy");
+            off += (int64_t)n;
+        }
+    });
+}
+
 tq_status tq_gate_matrix(int32_t op, const double *params, const double *explicit_m, int32_t cblock, int32_t deriv,
                          int32_t which, double *out, int32_t *dim, double *phase)
 {
@@ -1238,6 +1266,27 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
                 for (const BuildTask &bt : g.tasks)
                     if (bt.out == g.init_mat[q]) absorbed += bt.mem_count;
             o << (gi ? "," : "") << "{\"n\":" << g.n << ",\"rows\":" << g.rows.size() << ",\"gates\":" << g.gates.size()
+              << ",\"row_ids\":[";
+            for (size_t r = 0; r < g.rows.size(); r++) o << (r ? "," : "") << g.rows[r];
+            o << "],\"init_mat\":[";
+            for (int q = 0; q < g.n; q++) o << (q ? "," : "") << g.init_mat[q];
+            // build tasks: kind (0 product, 1 dagger, 2 derivative), dim, storage
+            // (0 dense, 1 diagonal, 2 / 3 the (a, b) pair of a I + b XX / YY, 4 the
+            // six entries of an excitation-preserving 4x4), parameter, offset in the
+            // row block, members [gate, qubit order swapped, controlled block]
+            o << "],\"tasks\":[";
+            for (size_t t = 0; t < g.tasks.size(); t++) {
+                const BuildTask &bt = g.tasks[t];
+                o << (t ? "," : "") << "[" << (int)bt.kind << "," << (int)bt.dim << "," << (int)bt.diag << ","
+                  << (int)bt.which << "," << bt.out << ",[";
+                for (int m = 0; m < bt.mem_count; m++) {
+                    const Member &mb = g.members[bt.mem_begin + m];
+                    o << (m ? "," : "") << "[" << mb.gate << "," << (int)mb.swapped << "," << (int)mb.form << "]";
+                }
+                o << "]]";
+            }
+            o << "]";
+            o
               << ",\"slots\":" << g.n_slots << ",\"mat_block\":" << g.mat_block << ",\"n_gslots\":" << g.n_gslots
               << ",\"absorbed\":" << absorbed << ",\"uniform_slots\":" << (g.uniform_slots ? 1 : 0);
             for (int dir = 0; dir < 2; dir++) {

@@ -62,6 +62,7 @@ def lib():
         L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
         L.tq_amplitudes_from_state.argtypes = [vp, i32, i32, vp, i64, vp, vp]
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
+        L.tq_build_matrices.argtypes = [vp, vp, vp, i64, ctypes.POINTER(i64), vp]
         L.tq_gate_matrix.argtypes = [i32, vp, vp, i32, i32, i32, vp, p32, ctypes.POINTER(ctypes.c_double)]
         L.tq_profile_start.argtypes = [ctypes.c_char_p]
         L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
@@ -69,7 +70,7 @@ def lib():
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_sample_with_amplitudes", "tq_adjoint_grad",
                   "tq_amplitudes",
                   "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read",
-                  "tq_gate_matrix"):
+                  "tq_gate_matrix", "tq_build_matrices"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -155,6 +156,17 @@ def describe(prog):
     buf = ctypes.create_string_buffer(need.value)
     _check(lib().tq_program_describe(prog._h, buf, need.value, None))
     return json.loads(buf.value.decode())
+
+
+def build_matrices(prog, symbol_values, stream=None):
+    """The device builder's matrix blocks (tq_build_matrices): complex128
+    device tensor of every group's rows x mat_block entries, concatenated."""
+    need = ctypes.c_int64()
+    _check(lib().tq_build_matrices(prog._h, None, None, 0, ctypes.byref(need), None))
+    out = torch.empty(max(need.value, 1), dtype=torch.complex128, device="cuda")
+    _check(lib().tq_build_matrices(prog._h, _theta(prog, symbol_values), ctypes.c_void_p(out.data_ptr()), need.value,
+                                   None, _stream(stream)))
+    return out[: need.value]
 
 
 def gate_matrix(op, params=(), explicit=None, cblock=False, deriv=False, which=0):
