@@ -199,6 +199,18 @@ tq_status tq_amplitudes(tq_program prog, const float *symbol_values, const uint6
 tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
                                uint64_t *out, void *stream);
 
+/* tq_sample_from_state for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same rule and kernels, bit-identical output, but no
+ * allocation of any kind.  The level workspace is a static device array of
+ * 2^22 uint64 (32 MiB) per GPU, held until the process ends; inputs with
+ * B * (level entries per row, about 2^n / 63) above 2^22 -- e.g. B = 1 with
+ * n >= 28 -- are rejected with TQ_E_UNSUPPORTED before anything is enqueued.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (other streams, other threads) race and must be serialised by the caller. */
+tq_status tq_sample_from_state_noalloc(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
+                                       uint64_t *out, void *stream);
+
 /* The amplitude lookup of tq_amplitudes applied to given states: states
  * complex64 [B, 2^n] device array, bitstrings uint64 [B, M] (an entry >= 2^n
  * yields a zero amplitude), amps complex64 [B, M].  With tq_simulate_state

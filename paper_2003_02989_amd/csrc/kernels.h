@@ -45,6 +45,11 @@ size_t rev_pass_lds_bytes(const RevArgs &a);
 hipError_t launch_rev_pass(const RevArgs &a, int nrows, hipStream_t s);
 hipError_t launch_grad_reduce(const GradReduceArgs &a, int nrows, hipStream_t s);
 hipError_t launch_sample(const SampArgs &a, int nrows, hipStream_t s);
+// The static sampler workspace: kStaticLevelEntries uint64 per device (32 MiB),
+// its device address on the current device (looked up on the first call per
+// device).
+constexpr int64_t kStaticLevelEntries = (int64_t)1 << 22;
+hipError_t static_levels(uint64_t **ptr);
 hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s);
 hipError_t launch_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int nrows, int64_t from,
                             int64_t to, hipStream_t s);

@@ -896,6 +896,33 @@ __global__ __launch_bounds__(256) void k_samp_shots(SampArgs a)
     if (lane == 0) *out = (uint64_t)base;
 }
 
+// ---------------------------------------------- static sampler workspace
+// The level workspace of the sampler for callers that cannot allocate device
+// memory (tq_sample_from_state_noalloc): a file-scope device array, one copy
+// per GPU, held until the process ends.  In host code its name is only a
+// stand-in: kernels get the device address that hipGetSymbolAddress returns
+// for the current device, looked up once per device.
+static __device__ __align__(256) uint64_t scratch[kStaticLevelEntries];
+
+hipError_t static_levels(uint64_t **ptr)
+{
+    static std::mutex mu;
+    static std::map<int, uint64_t *> addr;  // device -> address of its copy
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> l(mu);
+    auto it = addr.find(dev);
+    if (it == addr.end()) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        it = addr.emplace(dev, static_cast<uint64_t *>(p)).first;
+    }
+    *ptr = it->second;
+    return hipSuccess;
+}
+
 // ------------------------------------------------------- gather, padding
 __global__ void k_gather(GatherArgs a)
 {

@@ -1168,6 +1168,36 @@ tq_status tq_sample_from_state(const void *states, int32_t B, int32_t n, int64_t
     });
 }
 
+tq_status tq_sample_from_state_noalloc(const void *states, int32_t B, int32_t n, int64_t n_shots, uint64_t seed,
+                                       uint64_t *out, void *stream)
+{
+    return guarded([&] {
+        if (B < 0 || n < 0 || n > kMaxQubits || n_shots < 0) fail(TQ_E_INVALID, "bad B, n or n_shots");
+        if (B == 0 || n_shots == 0) return;
+        if (!states || !out) fail(TQ_E_INVALID, "states or out is NULL");
+        check_align(states, 8, "states");
+        check_align(out, 8, "out");
+        SampArgs a{};
+        a.state = (const float2 *)states;
+        a.row_stride = (int64_t)1 << n;
+        a.vec16 = reinterpret_cast<uintptr_t>(states) % 16 == 0 && n >= 1;
+        fill_levels(a, n);
+        if ((int64_t)B * a.row_level > kStaticLevelEntries)
+            fail(TQ_E_UNSUPPORTED, "tq_sample_from_state_noalloc: B * (level entries per row) = " +
+                                       std::to_string((int64_t)B * a.row_level) + " exceeds its static workspace of " +
+                                       std::to_string(kStaticLevelEntries) + " entries (about B 2^n / 63 <= 2^22)");
+        uint64_t *lv = nullptr;
+        hip_check(static_levels(&lv), "static sampler workspace lookup");
+        // every level entry is written (level 1 from the state, the others
+        // from the level below) before it is read: nothing to clear
+        a.levels = lv;
+        a.n_shots = n_shots;
+        a.seed = seed;
+        a.out = out;
+        hip_check(launch_sample(a, B, as_stream(stream)), "sampler launch");
+    });
+}
+
 tq_status tq_amplitudes_from_state(const void *states, int32_t B, int32_t n, const uint64_t *bitstrings, int64_t M,
                                    void *amps, void *stream)
 {

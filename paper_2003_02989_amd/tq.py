@@ -60,6 +60,7 @@ def lib():
         L.tq_adjoint_grad.argtypes = [vp, vp, vp, vp, vp, vp, vp]
         L.tq_amplitudes.argtypes = [vp, vp, vp, i64, vp, vp]
         L.tq_sample_from_state.argtypes = [vp, i32, i32, i64, u64, vp, vp]
+        L.tq_sample_from_state_noalloc.argtypes = [vp, i32, i32, i64, u64, vp, vp]
         L.tq_amplitudes_from_state.argtypes = [vp, i32, i32, vp, i64, vp, vp]
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
         L.tq_build_matrices.argtypes = [vp, vp, vp, i64, ctypes.POINTER(i64), vp]
@@ -69,7 +70,7 @@ def lib():
         for f in ("tq_program_create", "tq_program_info", "tq_program_specialize", "tq_observables_create", "tq_observables_info",
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_sample_with_amplitudes", "tq_adjoint_grad",
                   "tq_amplitudes",
-                  "tq_sample_from_state", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read",
+                  "tq_sample_from_state", "tq_sample_from_state_noalloc", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read",
                   "tq_gate_matrix", "tq_build_matrices"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -281,6 +282,19 @@ def sample_from_state(states, n_shots, seed, out=None, stream=None):
         out = torch.empty((B, n_shots), dtype=torch.int64, device="cuda")
     p = _dev(out, torch.int64, (B, n_shots), "out")
     _check(lib().tq_sample_from_state(s, B, n, int(n_shots), ctypes.c_uint64(seed), p, _stream(stream)))
+    return out
+
+
+def sample_from_state_noalloc(states, n_shots, seed, out, stream=None):
+    """sample_from_state without any allocation (tq_sample_from_state_noalloc):
+    `out` int64 [B, n_shots] is required."""
+    B, N = states.shape
+    n = N.bit_length() - 1
+    if (1 << n) != N:
+        raise ValueError("state length must be a power of two")
+    s = _dev(states, torch.complex64, (B, N), "states")
+    p = _dev(out, torch.int64, (B, n_shots), "out")
+    _check(lib().tq_sample_from_state_noalloc(s, B, n, int(n_shots), ctypes.c_uint64(seed), p, _stream(stream)))
     return out
 
 
