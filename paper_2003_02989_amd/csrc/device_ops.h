@@ -541,6 +541,22 @@ template <int R, int LO, int HI, int U, bool RX, class MT> __device__ __forceinl
         if (!(U & 8)) a[k11] = zmul(m[5], a[k11]);
     }
 }
+// rf2 for an op whose (|01>, |10>) block is -i SWAP (kHintSwap: fSim(pi/2,
+// phi)): the pair trades places with a factor -i, (x, y) -> (y, -x), and only
+// the |00> / |11> phases that are not exactly 1 (U as in rf2x) are multiplied
+template <int R, int LO, int HI, int U, class MT> __device__ __forceinline__ void rf2s(double2 *a, MT m)
+{
+#pragma unroll
+    for (int k = 0; k < (1 << R); k++) {
+        if (((k >> LO) & 1) || ((k >> HI) & 1)) continue;
+        const int k10 = k | (1 << LO), k01 = k | (1 << HI), k11 = k10 | k01;
+        const double2 x = a[k01], y = a[k10];
+        a[k01] = make_double2(y.y, -y.x);
+        a[k10] = make_double2(x.y, -x.x);
+        if (!(U & 1)) a[k] = zmul(m[0], a[k]);
+        if (!(U & 8)) a[k11] = zmul(m[5], a[k11]);
+    }
+}
 template <int R, int LO, int HI, class MT> __device__ __forceinline__ double rf2_dot(const double2 *a, const double2 *f, MT m)
 {
     const double2 p00 = m[0], b00 = m[1], b01 = m[2], b10 = m[3], b11 = m[4], p11 = m[5];

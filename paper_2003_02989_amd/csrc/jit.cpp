@@ -143,6 +143,8 @@ std::string apply(const Env &e, const PassOp &op, int R, int mat, const std::str
                N(op.cval) + "u);";
     case K_M2: return "rm2<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ">(" + v + ", " + m + ");";
     case K_F2:
+        if (op.hint & kHintSwap)
+            return "rf2s<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ", " + N(op.hint & 9) + ">(" + v + ", " + m + ");";
         if (op.hint & (9 | kHintRX))
             return "rf2x<" + Rs + ", " + N(op.s0) + ", " + N(op.s1) + ", " + N(op.hint & 9) + ", " +
                    ((op.hint & kHintRX) ? "true" : "false") + ">(" + v + ", " + m + ");";
@@ -575,36 +577,145 @@ std::string resident_source(const Group &g)
     return o.str();
 }
 
+namespace {
+
+// Tile loads and stores of a generated forward pass with the tile's geometry
+// written in (every pass but the first, which generates the product state):
+// thread tid holds the pairs l = 2 tid + 512 k (k < 2^t / 512) of the tile.
+// The global offset of l is a per-thread part -- the tid bits deposited at
+// their global positions -- plus a constant per k, and its LDS position sw(l)
+// is one of two per-thread values (by the parity of k) plus 512 k, an
+// immediate offset: no table lookups and no guards, all loads of a tile
+// issued back to back.
+bool direct_io(const Pass &ps) { return !ps.product_init && ps.geom.t >= 9 && ps.geom.c >= 1; }
+
+// global index bit of tile-local bit b
+int gpos(const TileGeom &gm, int b) { return b < gm.c ? b : gm.hb[b - gm.c]; }
+
+// With kFwdPrefetch the next tile's loads are issued right after the current
+// tile is in LDS, into registers held over its stages, so that every
+// workgroup streams its next tile while it computes; the registers this takes
+// leave three workgroups per CU instead of four.
+constexpr bool kFwdPrefetch = true;
+
+void direct_io_setup(std::ostream &o, const TileGeom &gm)
+{
+    o << "    const uint32_t tb_ = (uint32_t)tid << 1;\n"
+         "    const uint32_t la0_ = tb_ ^ ((tb_ >> 5) & 15u), la1_ = la0_ ^ 16u, lb0_ = la0_ ^ 1u, lb1_ = la1_ ^ 1u;\n"
+         "    uint64_t toff_ = 0;\n";
+    for (int j = 0; j < 8; j++)
+        o << "    toff_ |= (uint64_t)(((uint32_t)tid >> " << j << ") & 1u) << " << gpos(gm, j + 1) << ";\n";
+}
+
+uint64_t chunk_offset(const TileGeom &gm, int k)
+{
+    uint64_t o = 0;
+    for (int m = 0; 9 + m < gm.t; m++)
+        if ((k >> m) & 1) o |= 1ull << gpos(gm, 9 + m);
+    return o;
+}
+
+void direct_load(std::ostream &o, const TileGeom &gm, const std::string &fb, const std::string &dst,
+                 const std::string &row = "c.st")
+{
+    const int K = 1 << (gm.t - 9);
+    o << "    { const float2 *src_ = " << row << " + (" << fb << " | toff_);\n";
+    for (int k = 0; k < K; k++)
+        o << "      " << dst << "[" << k << "] = *reinterpret_cast<const float4 *>(src_ + " << chunk_offset(gm, k)
+          << "ull);\n";
+    o << "    }\n";
+}
+
+void direct_to_lds(std::ostream &o, const TileGeom &gm, const std::string &srcv, const std::string &lds = "lp")
+{
+    const int K = 1 << (gm.t - 9);
+    for (int k = 0; k < K; k++) {
+        const std::string p = (k & 1) ? "1_" : "0_";
+        o << "    " << lds << "[la" << p << " + " << 512 * k << "u] = make_float2(" << srcv << "[" << k << "].x, " << srcv << "[" << k
+          << "].y); " << lds << "[lb" << p << " + " << 512 * k << "u] = make_float2(" << srcv << "[" << k << "].z, " << srcv << "["
+          << k << "].w);\n";
+    }
+}
+
+void direct_store(std::ostream &o, const TileGeom &gm, const std::string &fb, const std::string &row = "c.st",
+                  const std::string &lds = "lp")
+{
+    const int K = 1 << (gm.t - 9);
+    o << "    { float2 *dst_ = " << row << " + (" << fb << " | toff_);\n";
+    for (int k = 0; k < K; k++) {
+        const std::string p = (k & 1) ? "1_" : "0_";
+        o << "      { const float2 u0 = " << lds << "[la" << p << " + " << 512 * k << "u], u1 = " << lds << "[lb" << p
+          << " + " << 512 * k
+          << "u]; *reinterpret_cast<float4 *>(dst_ + " << chunk_offset(gm, k)
+          << "ull) = make_float4(u0.x, u0.y, u1.x, u1.y); }\n";
+    }
+    o << "    }\n";
+}
+
+} // namespace
+
 std::string pass_kernel_source(const Group &g, int pass)
 {
     std::ostringstream o;
-    {
-        const Pass &ps = g.fwd[pass];
-        const TileGeom &gm = ps.geom;
-        // at most 128 registers: four workgroups of the tile's LDS share a CU
-        o << "extern \"C\" __global__ __launch_bounds__(256, 4) void tq_fwd_" << pass
-          << "(PassArgs a)\n{\n"
-             "    extern __shared__ __align__(16) unsigned char smem[];\n"
-             "    const PassCtx c = pass_setup(a, smem);\n"
-             "    const double2 *M = c.lm;\n"
-             "    const SMat G = smat(a.mats + (int64_t)c.row * a.mat_stride);\n";
-        o << "    float2 *lp = c.lds;\n"
-             "    const int tid = threadIdx.x;\n"
-             "    for (int64_t tile = c.w; tile < "
-          << (1ll << (gm.n - gm.t))
-          << "ll; tile += a.wg_per_row) {\n"
-             "    const uint64_t fb = pdep64((uint64_t)tile, "
-          << gm.fixed_mask
-          << "ull);\n"
+    const Pass &ps = g.fwd[pass];
+    const TileGeom &gm = ps.geom;
+    const bool dio = direct_io(ps), pre = dio && kFwdPrefetch;
+    const int64_t NT = 1ll << (gm.n - gm.t);
+    // at most 128 registers (four workgroups of the tile's LDS share a CU), or
+    // 168 with the prefetch registers (three); a pass with four-bit stages
+    // (16 amplitudes and up to 16 diagonal entries per thread) may take 256,
+    // so that it never spills -- the waves per SIMD follow what it uses
+    int maxr = 0;
+    for (const Stage &st : ps.stages) maxr = std::max(maxr, (int)st.r);
+    const int minwg = maxr >= 4 ? 2 : pre ? 3 : 4;
+    o << "extern \"C\" __global__ __launch_bounds__(256, " << minwg << ") void tq_fwd_" << pass
+      << "(PassArgs a)\n{\n"
+         "    extern __shared__ __align__(16) unsigned char smem[];\n"
+         "    const PassCtx c = pass_setup(a, smem);\n"
+         // op matrices through the scalar cache (SGPR operands of the FMAs),
+         // not from the LDS copy: the stages' LDS traffic is the tile alone
+         "    const SMat M = smat(a.mats + (int64_t)c.row * a.mat_stride + a.mat_begin);\n"
+         "    const SMat G = smat(a.mats + (int64_t)c.row * a.mat_stride);\n"
+         "    float2 *lp = c.lds;\n"
+         "    const int tid = threadIdx.x;\n";
+    const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
+    if (!dio) {
+        o << "    for (int64_t tile = c.w; tile < " << NT << "ll; tile += a.wg_per_row) {\n"
+          << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
              "    pass_load(a, c, fb);\n"
              "    __syncthreads();\n";
-        const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
         for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
         o << "    pass_store(a, c, fb);\n"
              "    __syncthreads();\n"
              "    }\n"
              "}\n";
+        return o.str();
     }
+    direct_io_setup(o, gm);
+    const int K = 1 << (gm.t - 9);
+    o << "    float4 nx_[" << K << "];\n";
+    if (pre) {
+        o << "    if (c.w < " << NT << "ll) {\n";
+        direct_load(o, gm, "pdep64((uint64_t)c.w, " + std::to_string(gm.fixed_mask) + "ull)", "nx_");
+        o << "    }\n";
+    }
+    o << "    for (int64_t tile = c.w; tile < " << NT << "ll; tile += a.wg_per_row) {\n"
+      << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n";
+    if (!pre) direct_load(o, gm, "fb", "nx_");
+    direct_to_lds(o, gm, "nx_");
+    o << "    __syncthreads();\n";
+    if (pre) {
+        // the next tile's loads, in flight during this tile's stages
+        o << "    if (tile + a.wg_per_row < " << NT << "ll) {\n"
+          << "    const uint64_t fbn_ = pdep64((uint64_t)(tile + a.wg_per_row), " << gm.fixed_mask << "ull);\n";
+        direct_load(o, gm, "fbn_", "nx_");
+        o << "    }\n";
+    }
+    for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
+    direct_store(o, gm, "fb");
+    o << "    __syncthreads();\n"
+         "    }\n"
+         "}\n";
     return o.str();
 }
 
@@ -618,28 +729,44 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
     const TileGeom &gm = ps.geom;
     int gcount = 0;
     for (const PassOp &op : ps.ops) gcount += op.ngrad;
+    const bool dio = gm.t >= 9 && gm.c >= 1;
     o << "extern \"C\" __global__ __launch_bounds__(256, 2) void tq_rev_" << pass
       << "(RevArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    const RevCtx c = rev_setup(a, smem);\n"
-         "    const double2 *M = c.lm;\n"
+         // matrices through the scalar cache, as in the forward passes
+         "    const SMat M = smat(a.mats + (int64_t)c.row * a.mat_stride + a.mat_begin);\n"
          "    float2 *lp = c.lp, *lf = c.lf;\n"
          "    double *acc = c.acc;\n"
-         "    const int tid = threadIdx.x;\n"
-         "    for (int64_t tile = c.w; tile < "
-      << (1ll << (gm.n - gm.t))
-      << "ll; tile += a.wg_per_row) {\n"
-         "    const uint64_t fb = pdep64((uint64_t)tile, "
-      << gm.fixed_mask
-      << "ull);\n"
-         "    rev_load(a, c, fb);\n"
-         "    __syncthreads();\n";
+         "    const int tid = threadIdx.x;\n";
+    if (dio) direct_io_setup(o, gm);
+    o << "    for (int64_t tile = c.w; tile < " << (1ll << (gm.n - gm.t)) << "ll; tile += a.wg_per_row) {\n"
+      << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n";
+    if (dio) {
+        const int K = 1 << (gm.t - 9);
+        o << "    { float4 xp_[" << K << "], xf_[" << K << "];\n";
+        direct_load(o, gm, "fb", "xp_", "c.sp");
+        direct_load(o, gm, "fb", "xf_", "c.sf");
+        direct_to_lds(o, gm, "xp_", "lp");
+        direct_to_lds(o, gm, "xf_", "lf");
+        o << "    }\n";
+    } else {
+        o << "    rev_load(a, c, fb);\n";
+    }
+    o << "    __syncthreads();\n";
     // accumulator rows of gcount slots, the pass's first slot at column 0
     Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
     e.grp = &g;
     for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
-    o << "    rev_store(a, c, fb);\n"
-         "    __syncthreads();\n"
+    if (dio) {
+        o << "    if (a.store) {\n";
+        direct_store(o, gm, "fb", "c.sp", "lp");
+        direct_store(o, gm, "fb", "c.sf", "lf");
+        o << "    }\n";
+    } else {
+        o << "    rev_store(a, c, fb);\n";
+    }
+    o << "    __syncthreads();\n"
          "    }\n"
          "    rev_finish(a, c);\n"
          "}\n";

@@ -331,7 +331,16 @@ int op_cost(const PassOp &op, int dispatch)
     if (generated && op.kind == K_D2) c = 4 - __builtin_popcount(op.hint & 15u);
     if (op.kind == K_M1) c = op.ctrl || (op.hint & (kHintReal | kHintRX)) ? 4 : 8;
     if (op.kind == K_M2) c = 16;
-    if (op.kind == K_F2) c = (op.hint & kHintRX) ? 4 : 6;
+    if (op.kind == K_F2) {
+        c = (op.hint & kHintRX) ? 4 : 6;
+        if (generated) {
+            // per four amplitudes: 4 for each |00>, |11> phase that is not 1,
+            // and the block: 0 as -i SWAP, 8 in RX form, 16 dense
+            const int ph = 4 * (!(op.hint & 1) + !(op.hint & 8));
+            const int blk = (op.hint & kHintSwap) ? 2 : (op.hint & kHintRX) ? 8 : 16;
+            c = (ph + blk + 3) / 4;
+        }
+    }
     if (op.kind == K_P2) c = 8;
     return c + dispatch;
 }
@@ -471,7 +480,8 @@ Packing pack(const Pass &ps, int rmax, int rdense, bool commute, bool soft_first
             ops += op_cost(ps.ops[P.order[i]], dispatch);
             uni = uni && uniform(ps.ops[P.order[i]], st.bits);
         }
-        P.cost += kStageCost + (uni ? std::min(ops, 4 << (int)st.bits.size()) : ops);
+        const int dense_cost = (4 << (int)st.bits.size()) + (dispatch == kOpDispatchCostSpec ? 2 : 0);
+        P.cost += kStageCost + (uni ? std::min(ops, dense_cost) : ops);
         P.st.push_back(st);
     }
     if ((int)P.order.size() != nops) fail(TQ_E_UNSUPPORTED, "internal planner error: op dependency cycle");
@@ -561,7 +571,9 @@ bool dense_pays(const Pass &ps, const Stage &st, int dispatch)
     int ops = 0;
     for (int k = st.op_begin - ps.op_offset; k < st.op_end - ps.op_offset; k++)
         ops += stages::op_cost(ps.ops[k], dispatch);
-    return (4 << st.r) < ops;
+    // a dense stage: 4 per entry of a matrix row, plus (generated kernels)
+    // reading its 2^(2r) entries through the scalar cache per item
+    return (4 << st.r) + (dispatch == kOpDispatchCostSpec ? 2 : 0) < ops;
 }
 
 // Append a pass, split into consecutive passes over the same tile when its
@@ -775,6 +787,23 @@ double gate_left_out_phase(int op, double eta)
 
 namespace {
 
+// A single fSim gate whose (|01>, |10>) block is -i SWAP in every row: theta a
+// constant with |cos theta| <= 1e-15 and |sin theta - 1| <= 1e-15 (theta =
+// pi/2, the random-circuit coupler): the generated kernels then move the pair
+// instead of multiplying it by entries of ~6e-17 and ~1.
+bool fsim_swap_block(const Group &g, int gi)
+{
+    if (g.gates[gi].op != OP_FSIM) return false;
+    const int slot = g.gates[gi].slot0;
+    if (g.slot_sym[slot] >= 0) return false;
+    const size_t rows = g.uniform_slots ? 1 : g.rows.size();
+    for (size_t r = 0; r < rows; r++) {
+        const double th = g.slot_off[r * (size_t)g.n_slots + slot];
+        if (!(std::fabs(std::cos(th)) <= 1e-15 && std::fabs(std::sin(th) - 1.0) <= 1e-15)) return false;
+    }
+    return true;
+}
+
 // Arithmetic per amplitude (fp64 instructions) of a single-qubit op fusing
 // `mem` in a generated kernel: diagonal 2 per entry that is not exactly 1,
 // dense 4 when real or RX-form, else 8.
@@ -911,6 +940,8 @@ void plan_group(Group &g, const Options &opt, int S)
             int ti = P.add_task(BT_PRODUCT, op_dim(ob.op), storage_of(ob.op), 0, ob.mem);
             ob.op.mat = g.tasks[ti].out;
             ob.op.hint = op_hint(g, ob.op, ob.mem);
+            if (ob.op.kind == K_F2 && ob.mem.size() == 1 && fsim_swap_block(g, ob.mem[0].gate))
+                ob.op.hint |= kHintSwap;
             ps.ops.push_back(ob.op);
         }
         ps.mat_end = g.mat_block;
@@ -982,13 +1013,19 @@ void plan_group(Group &g, const Options &opt, int S)
     const int dispatch = opt.specialize ? kOpDispatchCostSpec : kOpDispatchCost;
     for (Pass &ps : g.fwd) {
         ps.op_offset = off;
-        make_stages(ps, kStageBitsFwd, kStageBitsFwd, g, task_at, true, dispatch);
+        // generated tile passes (states too large to run resident) hold
+        // four-bit stages, 16 amplitudes per thread in registers: fewer LDS
+        // round trips per pass; the precompiled kernels and the resident
+        // ones keep kStageBitsFwd, and only stages of at most kStageBitsFwd
+        // bits become dense (the stage-matrix builder's limit)
+        const int rf = (opt.specialize && n > 12) ? 4 : kStageBitsFwd;
+        make_stages(ps, rf, rf, g, task_at, true, dispatch);
         off += (int)ps.ops.size();
         // forward stages whose ops act alike on every item become one dense
         // matrix when that is cheaper than the ops one by one (matrix
         // entries appended to the row block, built after the op matrices)
         for (Stage &st : ps.stages) {
-            if (!stage_fusable(ps, st) || !dense_pays(ps, st, dispatch)) continue;
+            if (st.r > kStageBitsFwd || !stage_fusable(ps, st) || !dense_pays(ps, st, dispatch)) continue;
             st.dense = 1;
             st.mat = g.mat_block;
             g.mat_block += 1 << (2 * st.r);

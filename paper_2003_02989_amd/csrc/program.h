@@ -85,7 +85,7 @@ struct Group {
 constexpr int kOpDispatchCost = 6;
 // The same for kernels generated for the circuit structure, whose ops are
 // straight-line code (no table reads or dispatch; a register move or two).
-constexpr int kOpDispatchCostSpec = 1;
+constexpr int kOpDispatchCostSpec = 0;
 // One register stage's LDS round trip in the same units (measured: ~0.29 ms
 // per stage of a 2^30-amplitude pass).
 constexpr int kStageCost = 11;

@@ -94,6 +94,11 @@ constexpr uint8_t kHintReal = 32;  // K_M1: the matrix and its derivatives are r
 // so are the derivatives); K_F2: the (|01>, |10>) block has that form (fSim);
 // K_P2: a real and b imaginary
 constexpr uint8_t kHintRX = 64;
+// K_F2, forward ops of generated kernels: the (|01>, |10>) block is -i SWAP
+// (fSim(theta, phi) with a constant theta whose cosine is below 1e-15 and
+// sine within 1e-15 of 1 in every row: its diagonal entries, ~6e-17, are
+// taken as 0 and the off-diagonal ones as exactly -i)
+constexpr uint8_t kHintSwap = 128;
 struct PassOp {
     uint8_t kind;
     uint8_t l0, l1;   // local bit of q0 / q1 in the tile, kFixed if outside
