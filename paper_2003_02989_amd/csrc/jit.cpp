@@ -65,6 +65,7 @@ struct Env {
     std::string acc_shift;
     int nt = kThreads;  // threads of the workgroup
     const Group *grp = nullptr;  // reverse stages: gradients from gate generators where known
+    const Group *fgrp = nullptr; // forward stages: constant single-qubit ops written out (const_m1)
     // keep each op's matrix reads next to the op (opaque per-item offset,
     // scheduling barriers between reverse ops): needed where registers are
     // short (tile passes, four waves per SIMD)
@@ -402,8 +403,126 @@ void stage_head(std::ostream &o, const Env &e, const Stage &st, std::vector<uint
     if (e.pin) o << "        asm volatile(\"\" : \"+s\"(z_));\n";
 }
 
-// A forward stage on the tile lp.
-void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &st)
+// Constant single-qubit ops.  A forward op on one qubit whose member gates
+// all have constant parameters, the same in every row, has a matrix known on
+// the host (the builder's gate table, gate_table_host); when its diagonal is
+// d = M00 = M11, real and positive, it is M = d U with U's diagonal exactly 1
+// (sqrt X, sqrt Y and sqrt W without their global phases: U off-diagonal in
+// {-i, -1, 1, (-1 -/+ i)/sqrt 2}).  Such an op is written out as U's products
+// with every entry that is 0 or +-1 or +-i folded in (entries below 1e-15 of
+// the largest taken as 0, within 1e-15 of +-1 as +-1: the rounding of the
+// closed forms is removed, not added), and the pass multiplies its registers
+// once by the product of the d's at the end of its last stage.
+struct ConstM1 {
+    double u[8];  // U row major, (re, im)
+    double d;     // the factor taken out (1 when none)
+};
+bool const_m1(const Group &g, const PassOp &op, ConstM1 *out)
+{
+    if (op.kind != K_M1 || op.ctrl) return false;
+    if (!g.uniform_slots && g.rows.size() > 1) return false;
+    const BuildTask *bt = nullptr;
+    for (int k = g.fwd_tasks.begin; k < g.fwd_tasks.end && !bt; k++)
+        if (g.tasks[k].out == op.mat && g.tasks[k].kind == BT_PRODUCT) bt = &g.tasks[k];
+    if (!bt || bt->dim != 2 || bt->diag != 0) return false;
+    double acc[8] = {1, 0, 0, 0, 0, 0, 1, 0};
+    for (int mi = 0; mi < bt->mem_count; mi++) {
+        const GateDev &gd = g.gates[g.members[bt->mem_begin + mi].gate];
+        double eta[2] = {0, 0};
+        for (int j = 0; j < gd.np; j++) {
+            if (g.slot_sym[gd.slot0 + j] >= 0) return false;
+            eta[j] = g.slot_off[gd.slot0 + j];
+        }
+        double m[32];
+        const double *ex = gd.explicit_ >= 0 ? &g.explicit_mats[32 * (size_t)gd.explicit_] : nullptr;
+        if (gate_table_host(gd.op, eta, ex, g.members[bt->mem_begin + mi].form, 0, 0, m) != 2) return false;
+        double t[8];
+        for (int i = 0; i < 2; i++)
+            for (int j = 0; j < 2; j++) {
+                double re = 0, im = 0;
+                for (int k = 0; k < 2; k++) {
+                    const double ar = m[2 * (2 * i + k)], ai = m[2 * (2 * i + k) + 1];
+                    const double br = acc[2 * (2 * k + j)], bi = acc[2 * (2 * k + j) + 1];
+                    re += ar * br - ai * bi;
+                    im += ar * bi + ai * br;
+                }
+                t[2 * (2 * i + j)] = re;
+                t[2 * (2 * i + j) + 1] = im;
+            }
+        std::copy(t, t + 8, acc);
+    }
+    double big = 0;
+    for (double v : acc) big = std::max(big, std::fabs(v));
+    for (double &v : acc)
+        if (std::fabs(v) <= 1e-15 * big) v = 0.0;
+    out->d = 1.0;
+    if (acc[1] == 0.0 && acc[7] == 0.0 && acc[0] == acc[6] && acc[0] >= 0.25) out->d = acc[0];
+    for (int i = 0; i < 8; i++) out->u[i] = acc[i] / out->d;
+    if (out->d != 1.0) out->u[0] = out->u[6] = 1.0;
+    // entries within 1e-15 of +-1 are the unit values they stand for (cos and
+    // sin of pi/4 differ in their last bit)
+    for (double &v : out->u)
+        if (std::fabs(std::fabs(v) - 1.0) <= 1e-15) v = v > 0 ? 1.0 : -1.0;
+    return true;
+}
+
+// One component of c0 x + c1 y (c complex literals, x y register names):
+// re: sum c.x w.x - c.y w.y, im: sum c.x w.y + c.y w.x, with zero terms left
+// out and unit factors as additions.
+std::string cterm_sum(const std::vector<std::pair<const double *, std::string>> &terms, bool im)
+{
+    std::vector<std::pair<double, std::string>> t;  // coefficient, operand
+    for (auto &tm : terms) {
+        const double cx = tm.first[0], cy = tm.first[1];
+        const std::string &w = tm.second;
+        if (!im) {
+            if (cx != 0) t.emplace_back(cx, w + ".x");
+            if (cy != 0) t.emplace_back(-cy, w + ".y");
+        } else {
+            if (cx != 0) t.emplace_back(cx, w + ".y");
+            if (cy != 0) t.emplace_back(cy, w + ".x");
+        }
+    }
+    if (t.empty()) return "0.0";
+    // unit terms first (additions), then the others as an fma chain on them
+    std::stable_sort(t.begin(), t.end(), [](const std::pair<double, std::string> &a, const std::pair<double, std::string> &b) {
+        return (std::fabs(a.first) == 1.0) > (std::fabs(b.first) == 1.0);
+    });
+    std::string acc;
+    for (auto &tm : t) {
+        const double c = tm.first;
+        if (acc.empty()) {
+            acc = c == 1.0 ? tm.second : c == -1.0 ? "(-" + tm.second + ")" : "(" + dbl(c) + " * " + tm.second + ")";
+        } else if (c == 1.0) {
+            acc = "(" + acc + " + " + tm.second + ")";
+        } else if (c == -1.0) {
+            acc = "(" + acc + " - " + tm.second + ")";
+        } else {
+            acc = "fma(" + dbl(c) + ", " + tm.second + ", " + acc + ")";
+        }
+    }
+    return acc;
+}
+
+std::string const_m1_code(const ConstM1 &cm, const PassOp &op, int R)
+{
+    std::ostringstream o;
+    const int J = op.s0;
+    for (int k = 0; k < (1 << R); k++) {
+        if ((k >> J) & 1) continue;
+        const int kk = k | (1 << J);
+        o << "{ const double2 x_ = v[" << k << "], y_ = v[" << kk << "]; ";
+        o << "v[" << k << "] = make_double2(" << cterm_sum({{cm.u + 0, "x_"}, {cm.u + 2, "y_"}}, false) << ", "
+          << cterm_sum({{cm.u + 0, "x_"}, {cm.u + 2, "y_"}}, true) << "); ";
+        o << "v[" << kk << "] = make_double2(" << cterm_sum({{cm.u + 4, "x_"}, {cm.u + 6, "y_"}}, false) << ", "
+          << cterm_sum({{cm.u + 4, "x_"}, {cm.u + 6, "y_"}}, true) << "); } ";
+    }
+    return o.str();
+}
+
+// A forward stage on the tile lp.  scale: the factor the pass's constant ops
+// left out, multiplied into the registers at the end of the stage ("" = none).
+void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &st, const std::string &scale = "")
 {
     const int R = st.r, NR = 1 << R;
     std::vector<uint32_t> off;
@@ -428,11 +547,34 @@ void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
                     continue;
                 }
             }
+            ConstM1 cm;
+            if (e.fgrp && const_m1(*e.fgrp, op, &cm)) {
+                o << "        " << const_m1_code(cm, op, R) << "\n";
+                continue;
+            }
             o << "        " << apply(e, op, R, op.mat - e.mbase, "v") << "\n";
         }
     }
+    if (!scale.empty())
+        for (int k = 0; k < NR; k++) o << "        v[" << k << "].x *= " << scale << "; v[" << k << "].y *= " << scale << ";\n";
     for (int k = 0; k < NR; k++) o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]);\n";
     o << "    }\n    }\n    __syncthreads();\n";
+}
+
+// The product of the factors the constant ops of a pass's stages leave out
+// ("" when it is 1), written in where the last stage applies it.
+std::string pass_scale(const Env &e, const Pass &ps)
+{
+    if (!e.fgrp) return "";
+    double s = 1.0;
+    for (const Stage &st : ps.stages) {
+        if (st.dense) continue;
+        for (int oi = st.op_begin; oi < st.op_end; oi++) {
+            ConstM1 cm;
+            if (const_m1(*e.fgrp, ps.ops[oi - ps.op_offset], &cm)) s *= cm.d;
+        }
+    }
+    return s == 1.0 ? "" : dbl(s);
 }
 
 // A reverse stage on the tiles lp (psi) and lf (phi); the gradient partials
@@ -564,8 +706,12 @@ std::string resident_source(const Group &g)
     e.pin = false;  // two waves per SIMD: registers to spare, latency to hide
     e.nt = nt;
     e.grp = &g;
-    for (const Pass &ps : g.fwd)
-        for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
+    e.fgrp = &g;
+    for (const Pass &ps : g.fwd) {
+        const std::string scale = pass_scale(e, ps);
+        for (size_t si = 0; si < ps.stages.size(); si++)
+            forward_stage(o, e, ps, ps.stages[si], si + 1 == ps.stages.size() ? scale : "");
+    }
     o << "    resident_middle(a, acc, lp, lf, blockIdx.x, tid, " << nt << ");\n"
          "    if (a.grad) {\n";
     for (const Pass &ps : g.rev)
@@ -678,13 +824,19 @@ std::string pass_kernel_source(const Group &g, int pass)
          "    const SMat G = smat(a.mats + (int64_t)c.row * a.mat_stride);\n"
          "    float2 *lp = c.lds;\n"
          "    const int tid = threadIdx.x;\n";
-    const Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
+    Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
+    e.fgrp = &g;
+    const std::string scale = pass_scale(e, ps);
+    auto stages = [&]() {
+        for (size_t si = 0; si < ps.stages.size(); si++)
+            forward_stage(o, e, ps, ps.stages[si], si + 1 == ps.stages.size() ? scale : "");
+    };
     if (!dio) {
         o << "    for (int64_t tile = c.w; tile < " << NT << "ll; tile += a.wg_per_row) {\n"
           << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
              "    pass_load(a, c, fb);\n"
              "    __syncthreads();\n";
-        for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
+        stages();
         o << "    pass_store(a, c, fb);\n"
              "    __syncthreads();\n"
              "    }\n"
@@ -711,7 +863,7 @@ std::string pass_kernel_source(const Group &g, int pass)
         direct_load(o, gm, "fbn_", "nx_");
         o << "    }\n";
     }
-    for (const Stage &st : ps.stages) forward_stage(o, e, ps, st);
+    stages();
     direct_store(o, gm, "fb");
     o << "    __syncthreads();\n"
          "    }\n"

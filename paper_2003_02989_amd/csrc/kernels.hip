@@ -33,7 +33,7 @@ namespace tq {
 // RZZ(gamma) = e^{-i gamma/2} diag(1, e^{i gamma}, e^{i gamma}, 1) (entries
 // exactly 1), X^t, sqrt X, XX^t, YY^t = e^{i pi t/2}(cos I - i sin G) (real
 // diagonal, imaginary off-diagonal), Y^t, sqrt Y = e^{i pi t/2}(cos I - i sin
-// Y) (real).  The phases of a row sum to one global phase, a linear form in
+// Y) (real), sqrt W = e^{i pi/4}(cos(pi/4) I - i sin(pi/4) W) (real diagonal).  The phases of a row sum to one global phase, a linear form in
 // the parameters that the planner lists per group (PhaseTerm), which the
 // builder multiplies into the first qubit's product-init matrix:
 // states and amplitudes come out with the gates' own phases, while every
@@ -95,16 +95,15 @@ __host__ __device__ __forceinline__ int gate_matrix_dev(int op, const double *et
         else { m[1] = C(-s, 0); m[2] = C(s, 0); }
         return 2;
     }
-    case OP_ZPOW: case OP_SQRTW: {
-        double t = op == OP_SQRTW ? 0.5 : eta[0];
-        scpi(t, &s, &c);
-        cd a = C(0.5 * (1 + c), 0.5 * s);   // (1 + w) / 2
-        cd bq = C(0.5 * (1 - c), -0.5 * s); // (1 - w) / 2
-        if (op == OP_ZPOW) { m[0] = C(1, 0); m[3] = C(c, s); return 2; }
-        m[0] = a; m[3] = a;
-        m[1] = cdmul(bq, C(r, -r)); m[2] = cdmul(bq, C(r, r)); // W = [[0, e^{-i pi/4}], [e^{i pi/4}, 0]]
+    case OP_ZPOW:
+        scpi(eta[0], &s, &c);
+        m[0] = C(1, 0); m[3] = C(c, s); return 2;
+    case OP_SQRTW:
+        // W^{1/2} = e^{i pi/4} (cos(pi/4) I - i sin(pi/4) W) with W = [[0, e^{-i pi/4}],
+        // [e^{i pi/4}, 0]]: without the phase, r I - i r W with r = 1/sqrt(2)
+        // (real diagonal; -i r e^{-/+ i pi/4} = (-1 -/+ i)/2 off it)
+        m[0] = m[3] = C(r, 0); m[1] = C(-0.5, -0.5); m[2] = C(0.5, -0.5);
         return 2;
-    }
     case OP_CZ:
         m[0] = m[5] = m[10] = C(1, 0); m[15] = C(-1, 0); return 4;
     case OP_CZPOW:

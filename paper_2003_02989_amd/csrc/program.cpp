@@ -763,14 +763,14 @@ PassOp base_op(const Group &g, const TileGeom &gm, int gi, int n)
 // The global phase the builder leaves out of a gate's matrix (the matrix is
 // e^{i phase} times the one built), linear in its parameter: phase = c eta,
 // or the constant c.  Rotations about Z and ZZ: e^{-i eta/2}; power gates of
-// X, Y and XX: e^{i pi t/2}; sqrt X and sqrt Y: e^{i pi/4}.
+// X, Y, XX and YY: e^{i pi t/2}; sqrt X, sqrt Y and sqrt W: e^{i pi/4}.
 bool gate_phase(int op, double *c, bool *constant)
 {
     *constant = false;
     switch (op) {
     case OP_RZ: case OP_RZZ: *c = -0.5; return true;
     case OP_XPOW: case OP_YPOW: case OP_XXPOW: case OP_YYPOW: *c = 0.5 * M_PI; return true;
-    case OP_SQRTX: case OP_SQRTY: *c = 0.25 * M_PI; *constant = true; return true;
+    case OP_SQRTX: case OP_SQRTY: case OP_SQRTW: *c = 0.25 * M_PI; *constant = true; return true;
     default: return false;
     }
 }
