@@ -87,18 +87,38 @@ def describe_workload(name, w):
     return f"c5 VQE ansatz n={n} B={w.B} 10 layers RY,RZ + CNOT ring, 200 Pauli strings, expectations+adjoint grads"
 
 
-# algorithmic work of one op applied to one amplitude (complex mul = 6 flops,
-# complex add = 2): dense 2x2 matvec 14, dense 4x4 30, diagonal 6; a
-# controlled 2x2 touches half the amplitudes
+# Algorithmic work of one op applied to one amplitude, in the form the plan
+# gives the op (its structure hints, PassOp::hint): complex mul = 6 flops,
+# complex add = 2, a real times a complex = 2.  2x2: dense 14, real or
+# "RX form" (real diagonal, imaginary off-diagonal) 6, exactly X 0; a
+# controlled 2x2 touches half the amplitudes.  Diagonal: 6 per entry that is
+# not exactly 1, over the entries' share of amplitudes.  Excitation
+# preserving (fSim-like): the |00>, |11> phases that are not 1 (6 on a quarter
+# each) and the (|01>, |10>) block on half (dense 14, RX form 6, -i SWAP 0).
+# Pauli pair 14 (6 in RX form), dense 4x4 30.  Constant single-qubit gates
+# the generated kernels write out with unit entries folded (sqrt X: 2) are
+# still counted by their hint, so the count is an upper bound of the
+# arithmetic done.
+H_X, H_REAL, H_RX, H_SWAP = 16, 32, 64, 128
+
+
 def op_flops(op, n_local_ctrl):
-    k = op["kind"]
+    k, h = op["kind"], op.get("hint", 0)
     if k == "M1":
-        return 7.0 if (op["ctrl"] and n_local_ctrl) else 14.0
+        f = 0.0 if h & H_X else 6.0 if h & (H_REAL | H_RX) else 14.0
+        return f / 2 if (op["ctrl"] and n_local_ctrl) else f
     if k == "M2":
         return 30.0
     if k == "P2":
-        return 14.0
-    return 6.0
+        return 6.0 if h & H_RX else 14.0
+    if k == "F2":
+        ph = 1.5 * ((0 if h & 1 else 1) + (0 if h & 8 else 1))
+        blk = 0.0 if h & H_SWAP else 3.0 if h & H_RX else 7.0
+        return ph + blk
+    # diagonal: D1 has 2 entries (half the amplitudes each), D2 4 (a quarter)
+    units = bin(h & (3 if k == "D1" else 15)).count("1")
+    n_ent = 2 if k == "D1" else 4
+    return 6.0 * (n_ent - units) / n_ent
 
 
 def fwd_flops(g):

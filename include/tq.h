@@ -57,7 +57,8 @@ typedef enum {
 
 /* Planner options; a zero field selects the default.
  *   max_tile_qubits: log2 of the amplitudes one workgroup stages in LDS per
- *                    forward pass (default 12, allowed 8..13);
+ *                    forward pass (default 12, or 13 with specialize = 1;
+ *                    allowed 8..13);
  *   low_qubits:      contiguous low index bits every tile keeps, so that each
  *                    wavefront reads runs of 2^low_qubits amplitudes
  *                    (default 6, allowed 3..8);

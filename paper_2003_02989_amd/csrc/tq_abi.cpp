@@ -813,6 +813,10 @@ tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *o
             if (opt->specialize < 0 || opt->specialize > 1) fail(TQ_E_INVALID, "specialize must be 0 or 1");
             o.specialize = opt->specialize == 1;
         }
+        // generated passes default to tiles of 2^13 amplitudes: fewer passes
+        // for the same gates (measured: the 30-qubit random circuit 46 -> 40
+        // passes, 181 -> 163 ms; QAOA 9.9 -> 8.7 ms; VQE 85 -> 83 ms)
+        if (o.specialize && !(opt && opt->max_tile_qubits)) o.tile = 13;
         if (o.low > o.tile - 2) o.low = o.tile - 2;
         auto p = std::make_unique<tq_program_s>();
         p->pd = parse_program(blob, nbytes, o);
@@ -1332,6 +1336,7 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
                         const PassOp &op = ps.ops[k];
                         o << (k ? "," : "") << "{\"kind\":\"" << kinds[op.kind] << "\",\"p\":[" << (int)op.p0 << ","
                           << (int)op.p1 << "],\"l\":[" << (int)op.l0 << "," << (int)op.l1 << "],\"ctrl\":" << (int)op.ctrl
+                          << ",\"hint\":" << (int)op.hint
                           << ",\"ngrad\":" << (int)op.ngrad << ",\"members\":"
                           << (members_at.count(op.mat) ? members_at[op.mat] : 0);
                         if (dir == 1) {  // generator terms [x, z, ny, c] of each gradient parameter
