@@ -23,6 +23,13 @@
 #include <cstring>
 #include <sstream>
 #include <vector>
+#include <atomic>
+#include <cstdlib>
+#include <fstream>
+#include <iterator>
+#include <thread>
+#include <sys/stat.h>
+#include <unistd.h>
 
 namespace tq {
 namespace {
@@ -1234,22 +1241,94 @@ std::mutex g_mu;
 std::map<std::pair<int, std::string>, Module> g_cache;
 int g_compiled = 0;
 
+// ---------------------------------------------------------- code cache
+// Compiled code objects are kept on disk, keyed by a 128-bit hash of
+// everything that determines them (the shared device code, the kernel
+// source, the offload target and the compiler options), so that a circuit
+// structure compiles once per machine.  Directory: $TQ_CACHE_DIR, else
+// $XDG_CACHE_HOME/tq-kernels, else $HOME/.cache/tq-kernels; TQ_CACHE_DIR=""
+// (empty) turns the cache off.  Files are written under a temporary name
+// and renamed, so that concurrent processes never read a partial file.
+constexpr int kCompileOpts = 7;
+const char *const kOptsTail[] = {"-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"};
+
+std::string cache_dir()
+{
+    const char *d = std::getenv("TQ_CACHE_DIR");
+    if (d) return d;
+    if ((d = std::getenv("XDG_CACHE_HOME")) && *d) return std::string(d) + "/tq-kernels";
+    if ((d = std::getenv("HOME")) && *d) return std::string(d) + "/.cache/tq-kernels";
+    return "";
+}
+
+// FNV-1a over the bytes, in two independent 64-bit lanes
+std::string hash128(const std::string &text)
+{
+    uint64_t a = 1469598103934665603ull, b = 0x9e3779b97f4a7c15ull;
+    for (unsigned char ch : text) {
+        a = (a ^ ch) * 1099511628211ull;
+        b = (b ^ ch) * 0x100000001b3ull ^ (b >> 29);
+    }
+    char buf[40];
+    snprintf(buf, sizeof buf, "%016llx%016llx", (unsigned long long)a, (unsigned long long)b);
+    return buf;
+}
+
+bool cache_read(const std::string &path, std::vector<char> *code)
+{
+    std::ifstream f(path, std::ios::binary);
+    if (!f) return false;
+    std::vector<char> v((std::istreambuf_iterator<char>(f)), std::istreambuf_iterator<char>());
+    if (v.empty()) return false;
+    code->swap(v);
+    return true;
+}
+
+void cache_write(const std::string &dir, const std::string &path, const std::vector<char> &code)
+{
+    // mkdir -p
+    for (size_t i = 1; i <= dir.size(); i++)
+        if (i == dir.size() || dir[i] == '/') mkdir(dir.substr(0, i).c_str(), 0755);
+    const std::string tmp = path + ".tmp" + std::to_string((long)getpid()) + "_" +
+                            std::to_string((unsigned long long)std::hash<std::thread::id>()(std::this_thread::get_id()));
+    {
+        std::ofstream f(tmp, std::ios::binary);
+        if (!f) return;
+        f.write(code.data(), (std::streamsize)code.size());
+        if (!f) {
+            std::remove(tmp.c_str());
+            return;
+        }
+    }
+    if (std::rename(tmp.c_str(), path.c_str()) != 0) std::remove(tmp.c_str());
+}
+
+std::atomic<int> g_disk_hits{0};
+
 // Compile the kernel source `body` for offload target `target` into a code
-// object.
+// object (or read it from the code cache).
 hipError_t compile_code(const std::string &body, const std::string &target, std::vector<char> *code,
                         std::string *log)
 {
     const std::string src = std::string(kPrelude) + "\n" + body;
+    const std::string arch = "--offload-arch=" + target;
+    std::string key = src + "\n//" + arch;
+    for (const char *o : kOptsTail) key += std::string(" ") + o;
+    const std::string dir = cache_dir();
+    const std::string path = dir.empty() ? "" : dir + "/" + hash128(key) + "_" + target + ".co";
+    if (!path.empty() && cache_read(path, code)) {
+        g_disk_hits++;
+        return hipSuccess;
+    }
     hiprtcProgram prog;
     if (hiprtcCreateProgram(&prog, src.c_str(), "tq_spec.hip", 0, nullptr, nullptr) != HIPRTC_SUCCESS) {
         *log = "hiprtcCreateProgram failed";
         return hipErrorInvalidSource;
     }
-    const std::string arch = "--offload-arch=" + target;
     // the same code generation flags as the precompiled kernels
-    const char *opts[] = {arch.c_str(), "-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang",
-                          "-packed-fp32-ops"};
-    const hiprtcResult r = hiprtcCompileProgram(prog, 7, opts);
+    const char *opts[kCompileOpts] = {arch.c_str()};
+    for (int i = 1; i < kCompileOpts; i++) opts[i] = kOptsTail[i - 1];
+    const hiprtcResult r = hiprtcCompileProgram(prog, kCompileOpts, opts);
     if (r != HIPRTC_SUCCESS) {
         size_t n = 0;
         hiprtcGetProgramLogSize(prog, &n);
@@ -1264,6 +1343,30 @@ hipError_t compile_code(const std::string &body, const std::string &target, std:
     code->resize(size);
     hiprtcGetCode(prog, code->data());
     hiprtcDestroyProgram(&prog);
+    if (!path.empty()) cache_write(dir, path, *code);
+    return hipSuccess;
+}
+
+// Compile several sources for one target at once, one thread each (at most
+// the host's hardware threads, up to 16, at a time).
+hipError_t compile_many(const std::vector<const std::string *> &bodies, const std::string &target,
+                        std::vector<std::vector<char>> *codes, std::string *log)
+{
+    codes->assign(bodies.size(), {});
+    std::vector<hipError_t> err(bodies.size(), hipSuccess);
+    std::vector<std::string> logs(bodies.size());
+    const size_t width = std::max<size_t>(1, std::min<size_t>(16, std::thread::hardware_concurrency()));
+    for (size_t b0 = 0; b0 < bodies.size(); b0 += width) {
+        std::vector<std::thread> th;
+        for (size_t i = b0; i < std::min(bodies.size(), b0 + width); i++)
+            th.emplace_back([&, i] { err[i] = compile_code(*bodies[i], target, &(*codes)[i], &logs[i]); });
+        for (auto &t : th) t.join();
+    }
+    for (size_t i = 0; i < bodies.size(); i++)
+        if (err[i] != hipSuccess) {
+            *log = logs[i];
+            return err[i];
+        }
     return hipSuccess;
 }
 
@@ -1305,17 +1408,67 @@ hipError_t get_kernels(const std::string &body, const std::vector<std::string> &
     return hipSuccess;
 }
 
-// every pass kernel of group g in one source (one compilation: the run-time
-// compiler does not gain from several programs at once)
-std::string pass_unit(const Group &g)
+// Load the sources `bodies` on the current device, compiling (in parallel)
+// those not loaded yet.
+hipError_t load_all(const std::vector<std::string> &bodies, std::string *log)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::vector<const std::string *> missing;
+    {
+        std::lock_guard<std::mutex> l(g_mu);
+        for (const std::string &b : bodies)
+            if (!g_cache.count(std::make_pair(dev, b))) missing.push_back(&b);
+    }
+    if (missing.empty()) return hipSuccess;
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return e;
+    std::vector<std::vector<char>> codes;
+    e = compile_many(missing, prop.gcnArchName, &codes, log);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> l(g_mu);
+    for (size_t i = 0; i < missing.size(); i++) {
+        auto key = std::make_pair(dev, *missing[i]);
+        if (g_cache.count(key)) continue;
+        Module m;
+        e = hipModuleLoadData(&m.mod, codes[i].data());
+        if (e != hipSuccess) return e;
+        g_cache.emplace(std::move(key), std::move(m));
+        g_compiled++;
+    }
+    return hipSuccess;
+}
+
+// The pass kernels of group g are compiled as programs of up to
+// kChunkPasses passes each (forward and reverse separately).  The run-time
+// compiler serialises compilations within a process (measured: 16 threads
+// take as long as one), so a structure's passes form one program each way,
+// which parses the shared device code once.  Reverse passes only run for
+// gradients: a structure without symbolic parameters never launches them,
+// and gets none.
+constexpr int kChunkPasses = 256;
+int fwd_chunks(const Group &g) { return ((int)g.fwd.size() + kChunkPasses - 1) / kChunkPasses; }
+int rev_chunks(const Group &g) { return g.n_gslots > 0 ? ((int)g.rev.size() + kChunkPasses - 1) / kChunkPasses : 0; }
+
+std::string pass_chunk(const Group &g, int chunk)
 {
     std::string body = kHead;
-    for (int pi = 0; pi < (int)g.fwd.size(); pi++) body += pass_kernel_source(g, pi);
-    // reverse passes only run for gradients: a structure without symbolic
-    // parameters never launches them
-    if (g.n_gslots > 0)
-        for (int pi = 0; pi < (int)g.rev.size(); pi++) body += rev_pass_kernel_source(g, pi);
+    const int nf = fwd_chunks(g);
+    const bool rev = chunk >= nf;
+    const int c = rev ? chunk - nf : chunk;
+    const int np = rev ? (int)g.rev.size() : (int)g.fwd.size();
+    for (int pi = c * kChunkPasses; pi < std::min(np, (c + 1) * kChunkPasses); pi++)
+        body += rev ? rev_pass_kernel_source(g, pi) : pass_kernel_source(g, pi);
     return body + "} // namespace tq\n";
+}
+
+std::vector<std::string> pass_chunks(const Group &g)
+{
+    std::vector<std::string> v;
+    for (int c = 0; c < fwd_chunks(g) + rev_chunks(g); c++) v.push_back(pass_chunk(g, c));
+    return v;
 }
 
 template <class Args>
@@ -1362,6 +1515,23 @@ hipError_t memo_kernel(SpecMemo *memo, size_t slot, size_t nslots, Src &&src, co
     return hipSuccess;
 }
 
+// Forward or reverse pass kernel `pass` of group g: on the first request on
+// a device every chunk of the group is compiled (in parallel) and loaded.
+hipError_t pass_kernel(const Group &g, bool rev, int pass, hipFunction_t *fn, std::string *log, SpecMemo *memo)
+{
+    const size_t slot = (rev ? g.fwd.size() : 0) + (size_t)pass, nslots = g.fwd.size() + g.rev.size();
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (!(memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot])) {
+        e = load_all(pass_chunks(g), log);
+        if (e != hipSuccess) return e;
+    }
+    const int chunk = rev ? fwd_chunks(g) + pass / kChunkPasses : pass / kChunkPasses;
+    return memo_kernel(memo, slot, nslots, [&] { return pass_chunk(g, chunk); },
+                       (rev ? "tq_rev_" : "tq_fwd_") + N(pass), fn, log);
+}
+
 } // namespace
 
 hipError_t launch_resident_spec(const Group &g, const ResArgs &a, int nrows, size_t lds, hipStream_t s,
@@ -1379,8 +1549,7 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
 {
     if (nrows <= 0) return hipSuccess;
     hipFunction_t fn;
-    hipError_t e = memo_kernel(memo, (size_t)pass, g.fwd.size() + g.rev.size(), [&] { return pass_unit(g); },
-                               "tq_fwd_" + N(pass), &fn, log);
+    hipError_t e = pass_kernel(g, false, pass, &fn, log, memo);
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
@@ -1441,22 +1610,24 @@ hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int 
 {
     if (nrows <= 0) return hipSuccess;
     hipFunction_t fn;
-    hipError_t e = memo_kernel(memo, g.fwd.size() + (size_t)pass, g.fwd.size() + g.rev.size(),
-                               [&] { return pass_unit(g); }, "tq_rev_" + N(pass), &fn, log);
+    hipError_t e = pass_kernel(g, true, pass, &fn, log, memo);
     if (e != hipSuccess) return e;
     return launch(fn, a, nrows * a.wg_per_row, rev_pass_lds_bytes(a), s, "rev_pass");
 }
 
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log)
 {
-    const std::string body = resident ? resident_source(g) : pass_unit(g);
+    const std::vector<std::string> bodies = resident ? std::vector<std::string>{resident_source(g)} : pass_chunks(g);
     if (target) {
-        std::vector<char> code;
-        return compile_code(body, target, &code, log);
+        std::vector<const std::string *> ptrs;
+        for (const std::string &b : bodies) ptrs.push_back(&b);
+        std::vector<std::vector<char>> codes;
+        return compile_many(ptrs, target, &codes, log);
     }
-    std::vector<hipFunction_t> fn;
-    return get_kernels(body, {}, &fn, log);
+    return load_all(bodies, log);
 }
+
+int spec_disk_cache_hits() { return g_disk_hits.load(); }
 
 int spec_kernels_compiled()
 {

@@ -75,7 +75,9 @@ int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log
 // compile for the offload target (e.g. "gfx950"), which needs no device.
 hipError_t prepare_spec(const Group &g, bool resident, const char *target, std::string *log);
 
-// Specialised kernels compiled so far in this process (all devices).
+// Specialised kernel programs loaded so far in this process (all devices),
+// and how many of their code objects came from the on-disk code cache.
 int spec_kernels_compiled();
+int spec_disk_cache_hits();
 
 } // namespace tq

@@ -1330,6 +1330,12 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
     pd->S = (int)S;
     pd->opt = opt;
     pd->circuits.resize(B);
+    // Each circuit is parsed into one reused scratch list; only the first
+    // circuit of a structure keeps its gates (in its group), the others add
+    // their scales and offsets to that group's parameter tables.
+    std::vector<HGate> gates;
+    std::map<std::string, int> key_to_group;
+    std::string key;
     for (uint32_t b = 0; b < B; b++) {
         uint32_t n = r.get<uint32_t>(), ng = r.get<uint32_t>();
         if (r.bad) fail(TQ_E_INVALID, "program blob: truncated circuit header");
@@ -1339,13 +1345,15 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
         HCircuit &c = pd->circuits[b];
         c.n = (int)n;
         pd->nmax = std::max(pd->nmax, (int)n);
-        c.gates.resize(ng);
+        if (gates.size() < ng) gates.resize(ng);
         for (uint32_t i = 0; i < ng; i++) {
-            HGate &g = c.gates[i];
-            std::memset(&g, 0, sizeof g);
+            HGate &g = gates[i];
             g.op = r.get<uint16_t>();
             g.nq = r.get<uint8_t>();
             g.np = r.get<uint8_t>();
+            g.q[0] = g.q[1] = 0;
+            g.sym[0] = g.sym[1] = 0;
+            g.scale[0] = g.scale[1] = g.offset[0] = g.offset[1] = 0.0;
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
             int enq, enp;
             if (!op_shape(g.op, enq, enp))
@@ -1371,34 +1379,33 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
                     fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
                                            ": symbol column out of range");
             }
-            int nm = g.op == OP_MATRIX1 ? 8 : g.op == OP_MATRIX2 ? 32 : 0;
+            const int nm = g.op == OP_MATRIX1 ? 8 : g.op == OP_MATRIX2 ? 32 : 0;
             for (int j = 0; j < nm; j++) g.mat[j] = r.get<double>();
+            if (nm)
+                for (int j = nm; j < 32; j++) g.mat[j] = 0.0;
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
         }
-    }
-    if (r.p != r.end) fail(TQ_E_INVALID, "program blob: trailing bytes");
-
-    // structure dedupe: same qubit count, opcodes, qubits, symbol wiring and
-    // explicit matrices; scales and offsets may differ per row
-    std::map<std::string, int> key_to_group;
-    for (uint32_t b = 0; b < B; b++) {
-        const HCircuit &c = pd->circuits[b];
-        std::string key;
+        // structure dedupe: same qubit count, opcodes, qubits, symbol wiring
+        // and explicit matrices; scales and offsets may differ per row
+        key.clear();
         key.append((const char *)&c.n, sizeof c.n);
-        for (const HGate &g : c.gates) {
+        for (uint32_t i = 0; i < ng; i++) {
+            const HGate &g = gates[i];
             key.append((const char *)&g.op, 2);
             key.append((const char *)g.q, 8);
             key.append((const char *)g.sym, 8);
-            if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2) key.append((const char *)g.mat, sizeof g.mat);
+            if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2)
+                key.append((const char *)g.mat, sizeof(double) * (g.op == OP_MATRIX1 ? 8 : 32));
         }
         auto it = key_to_group.find(key);
         Group *grp;
         if (it == key_to_group.end()) {
-            key_to_group[key] = (int)pd->groups.size();
+            key_to_group.emplace(key, (int)pd->groups.size());
             pd->groups.push_back(std::make_unique<Group>());
             grp = pd->groups.back().get();
             grp->n = c.n;
-            for (const HGate &g : c.gates) {
+            for (uint32_t i = 0; i < ng; i++) {
+                const HGate &g = gates[i];
                 GateDev gd{};
                 gd.op = g.op;
                 gd.nq = g.nq;
@@ -1419,12 +1426,14 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             grp = pd->groups[it->second].get();
         }
         grp->rows.push_back((int32_t)b);
-        for (const HGate &g : c.gates)
-            for (int j = 0; j < g.np; j++) {
-                grp->slot_scale.push_back(g.scale[j]);
-                grp->slot_off.push_back(g.offset[j]);
+        for (uint32_t i = 0; i < ng; i++)
+            for (int j = 0; j < gates[i].np; j++) {
+                grp->slot_scale.push_back(gates[i].scale[j]);
+                grp->slot_off.push_back(gates[i].offset[j]);
             }
     }
+    if (r.p != r.end) fail(TQ_E_INVALID, "program blob: trailing bytes");
+
     for (auto &gp : pd->groups) {
         Group &g = *gp;
         // rows that share every scale and offset keep one table row

@@ -34,8 +34,7 @@ struct HGate {
 };
 
 struct HCircuit {
-    int n = 0;
-    std::vector<HGate> gates;
+    int n = 0;  // (gates live in the circuit's structure group)
 };
 
 struct Pass {
