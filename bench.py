@@ -1,14 +1,16 @@
 """Benchmark of the batched state-vector hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config c4|c1|c2|c3|c5] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config c4|c1|c2|c3|c5] [--expectation-only]
+                    [--no-cpu-baseline]
 
 One step is one call of the configuration's hot path on its full batch with
 inputs resident in HBM and a new parameter set (or sampling seed) per step:
   c4  tq_sample_with_amplitudes: one simulation of the 30-qubit random circuit
-      (46 fused tile passes over the 8 GiB state), its amplitudes at 4096
+      (40 fused tile passes over the 8 GiB state), its amplitudes at 4096
       bitstrings and 10^6 samples (the default workload)
   c1, c2, c5  tq_adjoint_grad with expectation output (forward passes, Pauli-sum
-              expectations, H_g, reverse adjoint passes, gradient reduction)
+              expectations, H_g, reverse adjoint passes, gradient reduction);
+              with --expectation-only tq_expectation
   c3  tq_expectation
 Rank 0 prints one JSON line.  `value` is the metric's half that fits the
 workload: for c4 the effective HBM GB/s of its fused-gate passes
@@ -74,7 +76,14 @@ def workload(name):
     return wl.CONFIGS[name]()
 
 
-def describe_workload(name, w):
+def describe_workload(name, w, adjoint=True):
+    d = describe_config(name, w)
+    if name in ("c1", "c2", "c5") and not adjoint:
+        d = d.replace("expectations+adjoint grads", "expectations only")
+    return d
+
+
+def describe_config(name, w):
     n = w.n_max
     if name == "c1":
         return f"c1 hardware-efficient ansatz n={n} B={w.B} 2 layers RX,RY,RZ + CZ ladder, sum Z, expectations+adjoint grads"
@@ -174,11 +183,21 @@ def kernel_work(plan, kernel, n_obs_terms, adjoint):
                 flops += f * amps
                 bytes_ += (32.0 if i + 1 < len(g["rev"]) else 16.0) * amps
         elif kernel == "pauli":
-            # one sweep: expectations (4 flops per term and amplitude), and
-            # with the adjoint also phi = H_g psi (4 more, and phi written)
-            launches += 1
-            flops += (8.0 if adjoint else 4.0) * n_obs_terms * amps
-            bytes_ += (16.0 if adjoint else 8.0) * amps
+            # expectations: 4 flops per term and amplitude, psi read; with the
+            # adjoint also phi = H_g psi (4 more, phi written, and read back by
+            # every pass after the first).  The generated passes split the
+            # terms over several launches (the plan's "obs" entry).
+            ob = g.get("obs", {})
+            passes = ob.get("phi_passes") if adjoint else (ob.get("exp_passes") or ob.get("phi_passes"))
+            if passes and not (ob.get("diag") and not adjoint):
+                for i, nt in enumerate(passes):
+                    launches += 1
+                    flops += (8.0 if adjoint else 4.0) * nt * amps
+                    bytes_ += ((16.0 if i == 0 else 24.0) if adjoint else 8.0) * amps
+            else:
+                launches += 1
+                flops += (8.0 if adjoint else 4.0) * n_obs_terms * amps
+                bytes_ += (16.0 if adjoint else 8.0) * amps
     return flops, bytes_, launches
 
 
@@ -200,6 +219,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--expectation-only", action="store_true",
+                    help="c1, c2, c5: time tq_expectation (no adjoint gradients)")
     ap.add_argument("--no-specialize", action="store_true",
                     help="run with the precompiled table-driven kernels instead of the ones compiled for the "
                          "circuit structure on the first call")
@@ -238,7 +259,7 @@ def main():
         return
     w = workload(args.config)
     B, K = w.B, w.K
-    adjoint = args.config in ("c1", "c2", "c5")
+    adjoint = args.config in ("c1", "c2", "c5") and not args.expectation_only
     specialize = not args.no_specialize
     # every step (first call, warm-up, per-kernel profiling, timed) gets its
     # own parameter set, drawn like the workload's
@@ -264,7 +285,7 @@ def main():
         th = thetas[i]
         if adjoint:
             tq.adjoint_grad(prog, th, obs, up, grad=grad, expectations=exp)
-        elif args.config == "c3":
+        elif args.config != "c4":
             tq.expectation(prog, th, obs, out=exp)
         else:
             # one simulation serves both outputs; a new sampling seed per step
@@ -365,7 +386,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic (seeded generators, no datasets); a new parameter set or sampling seed per step",
-        "config": {"workload": describe_workload(args.config, w), "storage": "complex64", "arithmetic": "fp64",
+        "config": {"workload": describe_workload(args.config, w, adjoint), "storage": "complex64", "arithmetic": "fp64",
                    "batch": B, "qubits": w.n_max, "symbols": w.n_symbols, "observables": K,
                    "pauli_terms": n_terms, "program_create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3,
                    "specialized_kernel": specialize},
@@ -375,7 +396,7 @@ def main():
     }
 
     if not args.no_cpu_baseline and local_rank == 0:
-        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds, adjoint)
     print(json.dumps(line), flush=True)
 
 
@@ -492,7 +513,7 @@ def sweep(steps, cases="all", specialize=True):
         del prog
 
 
-def cpu_baseline(name, w, budget_s):
+def cpu_baseline(name, w, budget_s, adjoint=True):
     """The oracle on the host cores, on a bounded sample of the same workload."""
     import numpy as np
 
@@ -531,14 +552,14 @@ def cpu_baseline(name, w, budget_s):
         o = orc.Observables(sub.observable_blob())
         th = sub.theta.astype(np.float64)
         orc.expectation(p, th, o)
-        if name != "c3":
+        if adjoint:
             orc.adjoint_grad(p, th, o, sub.upstream.astype(np.float64))
         done_rows += len(r)
         el = time.perf_counter() - t0
         if el > budget_s:
             break
         rows = min(max(rows * 2, 1), w.B)
-    what = "expectations" + (" + adjoint gradients" if name != "c3" else "")
+    what = "expectations" + (" + adjoint gradients" if adjoint else "")
     return {"value": done_rows * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
             "cpu": cpu_model(),
             "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "

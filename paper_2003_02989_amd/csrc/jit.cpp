@@ -955,7 +955,9 @@ namespace {
 // two FMAs with the term's coefficient c' = coeff i^ny chi_z(x) signed by
 // chi_z of the output amplitude (fixed and thread bits: once per group and
 // chunk, register bits: at compile time).
-void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
+// With write_phi false the same passes only form the expectation
+// <psi|H|psi> (kernels tq_hexp_<pass>: no phi, no upstream weight).
+void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = true)
 {
     const TileGeom &gm = pp.geom;
     const int t = gm.t, P = 16, RC = 4, tb = t - 4, NT = 1 << tb, NW = NT / 64;
@@ -973,7 +975,7 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
         const double C = tm.coeff * chi * (ny >= 2 ? -1.0 : 1.0);
         groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, tm.z & gm.fixed_mask, C, (ny & 1) != 0});
     }
-    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void tq_hphi_" << pi
+    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void " << (write_phi ? "tq_hphi_" : "tq_hexp_") << pi
       << "(HPhiArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
@@ -987,8 +989,9 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
          "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
          "    const int64_t ro = (int64_t)cget(a.rows, row) * a.row_stride;\n"
          "    float2 *ps = const_cast<float2 *>(a.psi) + ro;\n"
-         "    float2 *pf = a.phi + ro;\n"
-         "    const double gw = (double)a.upstream[(int64_t)cget(a.brows, row) * a.K];\n"
+         << (write_phi ? "    float2 *pf = a.phi + ro;\n"
+                         "    const double gw = (double)a.upstream[(int64_t)cget(a.brows, row) * a.K];\n"
+                       : "") <<
          "    build_hi_off(a.g, hi_off);\n"
          "    __syncthreads();\n"
          "    const TileCtx tc{hi_off, "
@@ -1057,14 +1060,16 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
         for (int rr = 0; rr < RC; rr++) {
             const int r = ch * RC + rr;
             o << "    {\n        const double2 ow = up2(la[st ^ " << host_sw((uint32_t)NT * r) << "u]);\n"
-              << "        e = fma(ow.x, acc[" << rr << "].x, fma(ow.y, acc[" << rr << "].y, e));\n"
-              << "        const uint64_t gix = tile_index(tc, fb, " << (uint32_t)NT * r << "u + (uint32_t)tid);\n"
-              << "        const float2 v = make_float2((float)(gw * acc[" << rr << "].x), (float)(gw * acc[" << rr
-              << "].y));\n";
-            if (pi == 0)
-                o << "        pf[gix] = v;\n";
-            else
-                o << "        const float2 q = pf[gix];\n        pf[gix] = make_float2(q.x + v.x, q.y + v.y);\n";
+              << "        e = fma(ow.x, acc[" << rr << "].x, fma(ow.y, acc[" << rr << "].y, e));\n";
+            if (write_phi) {
+                o << "        const uint64_t gix = tile_index(tc, fb, " << (uint32_t)NT * r << "u + (uint32_t)tid);\n"
+                  << "        const float2 v = make_float2((float)(gw * acc[" << rr << "].x), (float)(gw * acc[" << rr
+                  << "].y));\n";
+                if (pi == 0)
+                    o << "        pf[gix] = v;\n";
+                else
+                    o << "        const float2 q = pf[gix];\n        pf[gix] = make_float2(q.x + v.x, q.y + v.y);\n";
+            }
             o << "    }\n";
         }
         o << "    }\n";
@@ -1555,13 +1560,24 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
 }
 
-std::string hphi_spec_source(const std::vector<PauliPass> &passes)
+std::string hphi_spec_source(const std::vector<PauliPass> &passes, bool write_phi)
 {
     std::ostringstream o;
     o << kHead;
-    for (size_t pi = 0; pi < passes.size(); pi++) hphi_pass(o, passes[pi], (int)pi);
+    for (size_t pi = 0; pi < passes.size(); pi++) hphi_pass(o, passes[pi], (int)pi, write_phi);
     o << "} // namespace tq\n";
     return o.str();
+}
+
+hipError_t launch_hexp_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
+                            std::string *log, SpecMemo *memo)
+{
+    if (nrows <= 0) return hipSuccess;
+    hipFunction_t fn;
+    hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_hexp_" + N(pass), &fn,
+                               log);
+    if (e != hipSuccess) return e;
+    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
 }
 
 hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,

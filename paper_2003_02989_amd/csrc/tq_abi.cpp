@@ -94,10 +94,11 @@ struct ObsGroupDev {
     std::string spec_src;
     SpecMemo spec_memo;
     // passes and source of the kernels computing phi = g H psi for a single
-    // observable the same on every row (specialize = 1)
+    // observable the same on every row (specialize = 1), and of their variant
+    // forming only <psi|H|psi> (expectations of more than 64 terms)
     std::vector<PauliPass> phi_passes;
-    std::string phi_src;
-    SpecMemo phi_memo;
+    std::string phi_src, hexp_src;
+    SpecMemo phi_memo, hexp_memo;
     void release()
     {
         for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
@@ -449,7 +450,10 @@ void ensure_obs(tq_program p, tq_observables o)
                     if (!pauli_spec_plan(n, t, c, per_row[0], &pp)) continue;
                     if (og->phi_passes.empty() || pp.size() < og->phi_passes.size()) og->phi_passes = std::move(pp);
                 }
-            if (!og->phi_passes.empty()) og->phi_src = hphi_spec_source(og->phi_passes);
+            if (!og->phi_passes.empty()) {
+                og->phi_src = hphi_spec_source(og->phi_passes, true);
+                og->hexp_src = hphi_spec_source(og->phi_passes, false);
+            }
         }
         if (diag) {
             DiagTables dt = diag_tables(per_row, uniform);
@@ -559,6 +563,9 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
 // per-workgroup partials stay within a bounded workspace.
 // phi = g H psi and <psi|H|psi> of a single observable (K = 1) with the
 // kernels generated for it: one read of psi and one update of phi per pass.
+// phi = g H psi and <psi|H|psi> of a single observable (K = 1) with the
+// kernels generated for it (phi = NULL: the expectation alone, by the
+// passes' variant that writes no phi).
 void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, float *out,
                     hipStream_t s)
 {
@@ -582,7 +589,8 @@ void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, con
     for (int pi = 0; pi < npass; pi++) {
         a.g = og.phi_passes[pi].geom;
         a.pass = pi;
-        const hipError_t e = launch_hphi_spec(og.phi_src, pi, a, nrows, s, &log, &og.phi_memo);
+        const hipError_t e = phi ? launch_hphi_spec(og.phi_src, pi, a, nrows, s, &log, &og.phi_memo)
+                                 : launch_hexp_spec(og.hexp_src, pi, a, nrows, s, &log, &og.hexp_memo);
         if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
         hip_check(e, "specialised H_g launch");
     }
@@ -612,6 +620,12 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     }
     if (!phi && !og.spec_passes.empty()) {
         spec_pauli_group(p, gi, psi, K, out, s);
+        return;
+    }
+    // a single observable beyond the generated expectation passes' 64 terms:
+    // the H_g passes without their phi output
+    if (!phi && K == 1 && !og.phi_passes.empty()) {
+        spec_phi_group(p, gi, psi, nullptr, nullptr, out, s);
         return;
     }
     if (phi && upstream && K == 1 && !og.phi_passes.empty()) {
@@ -1323,6 +1337,19 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
             o
               << ",\"slots\":" << g.n_slots << ",\"mat_block\":" << g.mat_block << ",\"n_gslots\":" << g.n_gslots
               << ",\"absorbed\":" << absorbed << ",\"uniform_slots\":" << (g.uniform_slots ? 1 : 0);
+            // the observables last used with the program: Z-only stream, and the
+            // terms of each generated expectation pass and H_g pass
+            if (gi < prog->obs_dev.size()) {
+                const ObsGroupDev &og = *prog->obs_dev[gi];
+                o << ",\"obs\":{\"diag\":" << (og.diag ? 1 : 0);
+                for (int v = 0; v < 2; v++) {
+                    const std::vector<PauliPass> &pp = v == 0 ? og.spec_passes : og.phi_passes;
+                    o << (v == 0 ? ",\"exp_passes\":[" : ",\"phi_passes\":[");
+                    for (size_t k = 0; k < pp.size(); k++) o << (k ? "," : "") << pp[k].terms.size();
+                    o << "]";
+                }
+                o << "}";
+            }
             for (int dir = 0; dir < 2; dir++) {
                 const std::vector<Pass> &pv = dir == 0 ? g.fwd : g.rev;
                 o << (dir == 0 ? ",\"fwd\":[" : ",\"rev\":[");
