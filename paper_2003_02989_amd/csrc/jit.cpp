@@ -20,6 +20,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <set>
 #include <cstring>
 #include <sstream>
 #include <vector>
@@ -934,6 +935,19 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
 
 namespace {
 
+// Partner reads la[b ^ host_sw(NT q)] with b < NT a swizzled thread index:
+// the swizzle only moves bits below NT, so the xor splits into b ^ low (a
+// base pointer per distinct low part) plus a multiple of NT that the LDS read
+// takes as an immediate offset.
+struct LdsSplit {
+    uint32_t low, high;
+};
+LdsSplit lds_split(uint32_t NT, uint32_t q)
+{
+    const uint32_t v = host_sw(NT * q);
+    return LdsSplit{v & (NT - 1), v & ~(NT - 1)};
+}
+
 // A mask in global index bits as tile-local bits of geometry gm.
 uint32_t local_mask(const TileGeom &gm, uint64_t m)
 {
@@ -955,9 +969,7 @@ namespace {
 // two FMAs with the term's coefficient c' = coeff i^ny chi_z(x) signed by
 // chi_z of the output amplitude (fixed and thread bits: once per group and
 // chunk, register bits: at compile time).
-// With write_phi false the same passes only form the expectation
-// <psi|H|psi> (kernels tq_hexp_<pass>: no phi, no upstream weight).
-void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = true)
+void hphi_pass(std::ostream &o, const PauliPass &pp, int pi)
 {
     const TileGeom &gm = pp.geom;
     const int t = gm.t, P = 16, RC = 4, tb = t - 4, NT = 1 << tb, NW = NT / 64;
@@ -975,7 +987,7 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
         const double C = tm.coeff * chi * (ny >= 2 ? -1.0 : 1.0);
         groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, tm.z & gm.fixed_mask, C, (ny & 1) != 0});
     }
-    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void " << (write_phi ? "tq_hphi_" : "tq_hexp_") << pi
+    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void tq_hphi_" << pi
       << "(HPhiArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
@@ -989,9 +1001,8 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
          "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
          "    const int64_t ro = (int64_t)cget(a.rows, row) * a.row_stride;\n"
          "    float2 *ps = const_cast<float2 *>(a.psi) + ro;\n"
-         << (write_phi ? "    float2 *pf = a.phi + ro;\n"
-                         "    const double gw = (double)a.upstream[(int64_t)cget(a.brows, row) * a.K];\n"
-                       : "") <<
+         "    float2 *pf = a.phi + ro;\n"
+         "    const double gw = (double)a.upstream[(int64_t)cget(a.brows, row) * a.K];\n"
          "    build_hi_off(a.g, hi_off);\n"
          "    __syncthreads();\n"
          "    const TileCtx tc{hi_off, "
@@ -1011,7 +1022,12 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
         // the thread index made opaque anew per chunk: what is derived from
         // it (partner offsets, signed coefficients) is recomputed next to its
         // use instead of being held across chunks and tiles
+        // zc: a zero the compiler cannot see through, xored into each
+        // coefficient's words so that they are formed next to their use
+        // (hoisted out of the tile loop, hundreds of them would be held in
+        // registers and spilled)
         o << "    {\n    asm volatile(\"\" : \"+v\"(tz));\n"
+          << "    uint32_t zc = 0u;\n    asm volatile(\"\" : \"+v\"(zc));\n"
           // thread bits and the tile number side by side: a term's sign is
           // the parity of one masked word
           << "    const uint32_t vz = tz | ((uint32_t)tile << " << tb << ");\n"
@@ -1022,6 +1038,9 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
             const std::vector<TT> &tts = *gl[gi].second;
             o << "    {\n";
             o << "        const uint32_t pt = sw(tz ^ " << (xT & (uint32_t)(NT - 1)) << "u);\n";
+            std::set<uint32_t> lows;
+            for (int rr = 0; rr < RC; rr++) lows.insert(lds_split(NT, (ch * RC + rr) ^ xhi).low);
+            for (uint32_t L : lows) o << "        const float2 *lp" << L << " = la + (pt ^ " << L << "u);\n";
             for (size_t j = 0; j < tts.size(); j++) {
                 const TT &tt = tts[j];
                 // the sign flips the coefficient's sign bit (integer ops: no
@@ -1032,14 +1051,16 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
                 const uint64_t m = (uint64_t)tt.zlo | (zt << tb);
                 uint64_t cb;
                 std::memcpy(&cb, &tt.C, sizeof cb);
-                if (!m) o << "        const double k" << j << " = " << dbl(tt.C) << ";\n";
-                else
-                    o << "        const double k" << j << " = __longlong_as_double((long long)(" << cb
-                      << "ull ^ ((uint64_t)(__popc(vz & " << m << "u) & 1) << 63)));\n";
+                const uint32_t chi = (uint32_t)(cb >> 32), clo = (uint32_t)cb;
+                o << "        const double k" << j << " = __hiloint2double((int)(" << chi << "u ^ ";
+                if (!m) o << "zc";
+                else o << "((uint32_t)(__popc(vz & " << m << "u) & 1) << 31)";
+                o << "), (int)(" << clo << "u ^ zc));\n";
             }
             for (int rr = 0; rr < RC; rr++) {
                 const int r = ch * RC + rr;
-                o << "        { const double2 p = up2(la[pt ^ " << host_sw((uint32_t)NT * (r ^ xhi)) << "u]);";
+                const LdsSplit pw = lds_split(NT, r ^ xhi);
+                o << "        { const double2 p = up2(lp" << pw.low << "[" << pw.high << "]);";
                 for (size_t j = 0; j < tts.size(); j++) {
                     const TT &tt = tts[j];
                     const bool neg = __builtin_popcount(tt.zhi & (uint32_t)r) & 1;
@@ -1059,17 +1080,16 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
         }
         for (int rr = 0; rr < RC; rr++) {
             const int r = ch * RC + rr;
-            o << "    {\n        const double2 ow = up2(la[st ^ " << host_sw((uint32_t)NT * r) << "u]);\n"
+            const LdsSplit sp = lds_split(NT, r);
+            o << "    {\n        const double2 ow = up2(la[(st ^ " << sp.low << "u) + " << sp.high << "u]);\n"
               << "        e = fma(ow.x, acc[" << rr << "].x, fma(ow.y, acc[" << rr << "].y, e));\n";
-            if (write_phi) {
-                o << "        const uint64_t gix = tile_index(tc, fb, " << (uint32_t)NT * r << "u + (uint32_t)tid);\n"
-                  << "        const float2 v = make_float2((float)(gw * acc[" << rr << "].x), (float)(gw * acc[" << rr
-                  << "].y));\n";
-                if (pi == 0)
-                    o << "        pf[gix] = v;\n";
-                else
-                    o << "        const float2 q = pf[gix];\n        pf[gix] = make_float2(q.x + v.x, q.y + v.y);\n";
-            }
+            o << "        const uint64_t gix = tile_index(tc, fb, " << (uint32_t)NT * r << "u + (uint32_t)tid);\n"
+              << "        const float2 v = make_float2((float)(gw * acc[" << rr << "].x), (float)(gw * acc[" << rr
+              << "].y));\n";
+            if (pi == 0)
+                o << "        pf[gix] = v;\n";
+            else
+                o << "        const float2 q = pf[gix];\n        pf[gix] = make_float2(q.x + v.x, q.y + v.y);\n";
             o << "    }\n";
         }
         o << "    }\n";
@@ -1088,148 +1108,214 @@ void hphi_pass(std::ostream &o, const PauliPass &pp, int pi, bool write_phi = tr
 
 } // namespace
 
+namespace {
+
+// Terms per block of the expectation passes: one running sum (two VGPRs) per
+// term of the block.
+constexpr int kExpBlock = 16;
+
+// <psi|P|psi> of the pass's terms, for up to 16 observables: per thread 16
+// amplitudes (the top four bits of the tile index).  The terms, grouped by
+// their X mask on the tile, are taken in blocks; a block sweeps the 16
+// registers with one running sum per term (s += Re or Im of
+// conj(psi_l) psi_{l^x}, one partner read per group, the sign of the
+// register bits of the term's Z mask written in) and then folds each sum into
+// its observable's accumulator with the term's coefficient signed by the
+// thread and tile bits of its Z mask.  A term whose X mask has a register bit
+// visits each pair {l, l^x} once, with twice the coefficient.
+void pauli_exp_pass(std::ostream &o, const PauliPass &pp, int pi)
+{
+    const TileGeom &gm = pp.geom;
+    const int t = gm.t, P = 16, tb = t - 4, NT = 1 << tb, NW = NT / 64;
+    // observables of the pass, and the register accumulator of each
+    std::vector<int> ks;
+    for (const SpecTerm &tm : pp.terms)
+        if (std::find(ks.begin(), ks.end(), tm.k) == ks.end()) ks.push_back(tm.k);
+    std::sort(ks.begin(), ks.end());
+    auto slot = [&](int k) { return (int)(std::find(ks.begin(), ks.end(), k) - ks.begin()); };
+    const int NK = (int)ks.size();
+    struct TT {
+        uint32_t zlo, zhi;
+        uint64_t zt;  // Z bits among the fixed bits, as tile-number bits
+        double C;
+        bool im;
+        int kk;
+    };
+    std::map<uint32_t, std::vector<TT>> groups;
+    for (const SpecTerm &tm : pp.terms) {
+        const uint32_t xT = local_mask(gm, tm.x), zT = local_mask(gm, tm.z);
+        const int ny = tm.ny & 3;
+        const double chi = (__builtin_popcountll(tm.x & tm.z) & 1) ? -1.0 : 1.0;
+        // <P> = Re(c' sum_l chi_z(l) conj(psi_l) psi_{l^x}), c' = coeff i^ny chi_z(x):
+        // ny even: c' real, Re part; ny odd: c' = i b, -b times the Im part
+        double C = (ny & 1) ? -(tm.coeff * (ny == 1 ? 1.0 : -1.0) * chi) : tm.coeff * (ny == 2 ? -1.0 : 1.0) * chi;
+        // pairs {l, l^x} summed once when x has a register bit: twice the half
+        if (xT >> tb) C *= 2.0;
+        uint64_t zt = 0;
+        for (int bb = 0, k = 0; bb < gm.n; bb++)
+            if ((gm.fixed_mask >> bb) & 1) zt |= ((tm.z >> bb) & 1ull) << k++;
+        groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, zt, C, (ny & 1) != 0, slot(tm.k)});
+    }
+    // blocks of at most kExpBlock terms; a group larger than what is left of
+    // a block continues in the next one (its partner read again)
+    struct Slice {
+        uint32_t xT;
+        std::vector<const TT *> tts;
+        int first;  // running-sum index of its first term in the block
+    };
+    std::vector<std::vector<Slice>> blocks;
+    {
+        std::vector<Slice> cur;
+        int cnt = 0;
+        for (auto &g : groups)
+            for (size_t i = 0; i < g.second.size();) {
+                if (cnt == kExpBlock) {
+                    blocks.push_back(std::move(cur));
+                    cur.clear();
+                    cnt = 0;
+                }
+                const size_t take = std::min(g.second.size() - i, (size_t)(kExpBlock - cnt));
+                Slice sl{g.first, {}, cnt};
+                for (size_t j = 0; j < take; j++) sl.tts.push_back(&g.second[i + j]);
+                cur.push_back(std::move(sl));
+                cnt += (int)take;
+                i += take;
+            }
+        if (!cur.empty()) blocks.push_back(std::move(cur));
+    }
+    o << "extern \"C\" __global__ __launch_bounds__(" << NT << ", 4) void tq_pauli_" << pi
+      << "(PauliSpecArgs a)\n{\n"
+         "    extern __shared__ __align__(16) unsigned char smem[];\n"
+         "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
+         "    uint64_t *hi_off = reinterpret_cast<uint64_t *>(la + "
+      << (1 << t)
+      << ");\n"
+         "    double *red = reinterpret_cast<double *>(hi_off + "
+      << (1 << gm.h)
+      << ");\n"
+         "    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;\n"
+         "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
+         "    float2 *ps = const_cast<float2 *>(a.psi) + (int64_t)cget(a.rows, row) * a.row_stride;\n"
+         "    build_hi_off(a.g, hi_off);\n"
+         "    __syncthreads();  // hi_off complete before the first tile load\n"
+         "    const TileCtx tc{hi_off, "
+      << ((1u << gm.c) - 1) << "u, " << gm.c
+      << "};\n"
+         "    uint32_t tz = (uint32_t)tid;\n";
+    for (int j = 0; j < NK; j++) o << "    double e" << j << " = 0.0;\n";
+    o << "    for (int64_t tile = w; tile < " << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
+      << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
+      << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
+      << "    __syncthreads();\n";
+    auto skipped = [&](uint32_t xT, int r) {
+        const uint32_t xhi = xT >> tb;
+        const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
+        return pivot >= 0 && ((r >> pivot) & 1);
+    };
+    for (const std::vector<Slice> &blk : blocks) {
+        // the thread index and a zero made opaque anew per block: addresses
+        // and signed coefficients are formed next to their use
+        o << "    {\n    asm volatile(\"\" : \"+v\"(tz));\n"
+          << "    uint32_t zc = 0u;\n    asm volatile(\"\" : \"+v\"(zc));\n"
+          << "    const uint32_t vz = tz | ((uint32_t)tile << " << tb << ");\n"
+          << "    const uint32_t st = sw(tz);\n";
+        int nb = 0;
+        for (const Slice &sl : blk) nb += (int)sl.tts.size();
+        for (int j = 0; j < nb; j++) o << "    double s" << j << " = 0.0;\n";
+        // rows by the low part of their swizzled offset: within a phase every
+        // read of a slice goes through one base pointer, st ^ sw(x_lo) ^ low
+        // (sw is linear over xor), with the rest of the offset immediate
+        std::map<uint32_t, std::vector<int>> phases;
+        for (int r = 0; r < P; r++) phases[lds_split(NT, r).low].push_back(r);
+        for (auto &ph : phases) {
+            const uint32_t lowr = ph.first;
+            o << "    {\n    const float2 *lo = la + (st ^ " << lowr << "u);\n";
+            for (size_t si = 0; si < blk.size(); si++) {
+                const uint32_t xT = blk[si].xT, xhi = xT >> tb;
+                if (!xT) continue;
+                bool used = false;
+                for (int r : ph.second) used |= !skipped(xT, r);
+                if (!used) continue;
+                const uint32_t c = host_sw(xT & (uint32_t)(NT - 1)) ^ lowr ^ lds_split(NT, xhi).low;
+                o << "    const float2 *lp" << si << " = la + (st ^ " << c << "u);\n";
+            }
+            for (int r : ph.second) {
+                o << "    {\n        const double2 o = up2(lo[" << lds_split(NT, r).high << "]);\n";
+                for (size_t si = 0; si < blk.size(); si++) {
+                    const Slice &sl = blk[si];
+                    if (skipped(sl.xT, r)) continue;
+                    bool any_re = false, any_im = false;
+                    for (const TT *tt : sl.tts) (tt->im ? any_im : any_re) = true;
+                    o << "        {\n";
+                    if (sl.xT) {
+                        o << "        const double2 p = up2(lp" << si << "[" << lds_split(NT, r ^ (sl.xT >> tb)).high
+                          << "]);\n";
+                        if (any_re) o << "        const double re = fma(o.x, p.x, o.y * p.y);\n";
+                        if (any_im) o << "        const double im = fma(o.x, p.y, -o.y * p.x);\n";
+                    } else {
+                        o << "        const double re = fma(o.x, o.x, o.y * o.y);\n";
+                    }
+                    for (size_t j = 0; j < sl.tts.size(); j++) {
+                        const TT &tt = *sl.tts[j];
+                        const bool neg = __builtin_popcount(tt.zhi & (uint32_t)r) & 1;
+                        o << "        s" << sl.first + (int)j << (neg ? " -= " : " += ") << (tt.im ? "im" : "re")
+                          << ";\n";
+                    }
+                    o << "        }\n";
+                }
+                o << "    }\n";
+            }
+            o << "    }\n";
+        }
+        // fold: the coefficient's sign bit flipped by the parity of the
+        // thread and tile bits of the term's Z mask
+        for (const Slice &sl : blk)
+            for (size_t j = 0; j < sl.tts.size(); j++) {
+                const TT &tt = *sl.tts[j];
+                const uint64_t m = (uint64_t)tt.zlo | (tt.zt << tb);
+                uint64_t cb;
+                std::memcpy(&cb, &tt.C, sizeof cb);
+                o << "    e" << tt.kk << " = fma(__hiloint2double((int)(" << (uint32_t)(cb >> 32) << "u ^ ";
+                if (!m) o << "zc";
+                else o << "((uint32_t)(__popc(vz & " << m << "u) & 1) << 31)";
+                o << "), (int)(" << (uint32_t)cb << "u ^ zc)), s" << sl.first + (int)j << ", e" << tt.kk << ");\n";
+            }
+        o << "    }\n    __builtin_amdgcn_sched_barrier(0);\n";
+    }
+    o << "    __syncthreads();\n"
+         "    }\n";
+    // fixed-order reduction: waves, then the wave sums
+    for (int j = 0; j < NK; j++)
+        o << "    { const double v = wave_sum(e" << j << "); if (lane == 0) red[wave * " << NK << " + " << j << "] = v; }\n";
+    o << "    __syncthreads();\n"
+         "    double *out = a.partial + ((int64_t)(row * a.npass + "
+      << pi
+      << ") * a.wg_per_row + w) * a.k_count;\n"
+         "    for (int k = tid; k < a.k_count; k += "
+      << NT
+      << ") {\n"
+         "        double v = 0.0;\n"
+         "        switch (k) {\n";
+    for (int j = 0; j < NK; j++) {
+        o << "        case " << ks[j] << ": v = red[" << j << "]";
+        for (int wv = 1; wv < NW; wv++) o << "; v += red[" << wv * NK + j << "]";
+        o << "; break;\n";
+    }
+    o << "        default: break;\n"
+         "        }\n"
+         "        out[k] = v;\n"
+         "    }\n"
+         "}\n";
+}
+
+} // namespace
+
 std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
 {
     std::ostringstream o;
     o << kHead;
-    for (size_t pi = 0; pi < passes.size(); pi++) {
-        const PauliPass &pp = passes[pi];
-        const TileGeom &gm = pp.geom;
-        // 16 amplitudes per thread: a tile of 2^t amplitudes takes 2^(t-4)
-        // threads (tb bits of the tile index select the thread)
-        const int t = gm.t, P = 16, tb = t - 4, NT = 1 << tb, NW = NT / 64;
-        // observables of the pass, and the register accumulator of each
-        std::vector<int> ks;
-        for (const SpecTerm &tm : pp.terms)
-            if (std::find(ks.begin(), ks.end(), tm.k) == ks.end()) ks.push_back(tm.k);
-        std::sort(ks.begin(), ks.end());
-        auto slot = [&](int k) { return (int)(std::find(ks.begin(), ks.end(), k) - ks.begin()); };
-        const int NK = (int)ks.size();
-        o << "extern \"C\" __global__ __launch_bounds__(" << NT << ") void tq_pauli_" << pi
-          << "(PauliSpecArgs a)\n{\n"
-             "    extern __shared__ __align__(16) unsigned char smem[];\n"
-             "    float2 *la = reinterpret_cast<float2 *>(smem);\n"
-             "    uint64_t *hi_off = reinterpret_cast<uint64_t *>(la + "
-          << (1 << t)
-          << ");\n"
-             "    double *red = reinterpret_cast<double *>(hi_off + "
-          << (1 << gm.h)
-          << ");\n"
-             "    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;\n"
-             "    const int row = blockIdx.x / a.wg_per_row, w = blockIdx.x % a.wg_per_row;\n"
-             "    float2 *ps = const_cast<float2 *>(a.psi) + (int64_t)cget(a.rows, row) * a.row_stride;\n"
-             "    build_hi_off(a.g, hi_off);\n"
-             "    __syncthreads();  // hi_off complete before the first tile load\n"
-             "    const TileCtx tc{hi_off, "
-          << ((1u << gm.c) - 1) << "u, " << gm.c
-          << "};\n"
-             "    const uint32_t st = sw((uint32_t)tid);\n";
-        // group terms by their tile X mask; per term its real coefficient,
-        // its real/imaginary part and its sign pattern
-        struct TT {
-            uint32_t zlo, zhi;
-            uint64_t zF;
-            double C;
-            bool im;
-            int kk;
-        };
-        std::map<uint32_t, std::vector<TT>> groups;
-        for (const SpecTerm &tm : pp.terms) {
-            const uint32_t xT = local_mask(gm, tm.x), zT = local_mask(gm, tm.z);
-            const int ny = tm.ny & 3;
-            const double chi = (__builtin_popcountll(tm.x & tm.z) & 1) ? -1.0 : 1.0;
-            // <P> = Re(c' sum_l chi_z(l) conj(psi_l) psi_{l^x}), c' = coeff i^ny chi_z(x):
-            // ny even: c' real, Re part; ny odd: c' = i b, -b times the Im part
-            double C = (ny & 1) ? -(tm.coeff * (ny == 1 ? 1.0 : -1.0) * chi) : tm.coeff * (ny == 2 ? -1.0 : 1.0) * chi;
-            // pairs {l, l^x} summed once when x has a register bit: twice the half
-            if (xT >> tb) C *= 2.0;
-            groups[xT].push_back(TT{zT & (uint32_t)(NT - 1), zT >> tb, tm.z & gm.fixed_mask, C, (ny & 1) != 0, slot(tm.k)});
-        }
-        int ti = 0;
-        for (auto &g : groups)
-            for (const TT &tt : g.second)
-                o << "    const double L" << ti++ << " = par32((uint32_t)tid & " << tt.zlo << "u) ? " << dbl(-tt.C) << " : "
-                  << dbl(tt.C) << ";\n";
-        for (int j = 0; j < NK; j++) o << "    double e" << j << " = 0.0;\n";
-        o << "    for (int64_t tile = w; tile < " << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
-          << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
-          << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
-          << "    __syncthreads();\n";
-        // register by register: the own amplitude, then every term group's
-        // partner; one running sum per term
-        std::vector<std::pair<uint32_t, const std::vector<TT> *>> gl;
-        for (auto &g : groups) gl.emplace_back(g.first, &g.second);
-        for (size_t gi = 0; gi < gl.size(); gi++) {
-            const uint32_t xT = gl[gi].first;
-            if (xT) o << "    const uint32_t pt" << gi << " = sw((uint32_t)tid ^ " << (xT & (uint32_t)(NT - 1)) << "u);\n";
-        }
-        ti = 0;
-        for (size_t gi = 0; gi < gl.size(); gi++)
-            for (size_t j = 0; j < gl[gi].second->size(); j++) o << "    double s" << ti++ << " = 0.0;\n";
-        for (int r = 0; r < P; r++) {
-            o << "    {\n        const double2 o = up2(la[st ^ " << host_sw((uint32_t)NT * r) << "u]);\n";
-            int tj = 0;
-            for (size_t gi = 0; gi < gl.size(); gi++) {
-                const uint32_t xT = gl[gi].first, xhi = xT >> tb;
-                const std::vector<TT> &tts = *gl[gi].second;
-                const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
-                if (pivot >= 0 && ((r >> pivot) & 1)) {  // the other half of the pairs
-                    tj += (int)tts.size();
-                    continue;
-                }
-                bool any_re = false, any_im = false;
-                for (const TT &tt : tts) (tt.im ? any_im : any_re) = true;
-                o << "        {\n";
-                if (xT) {
-                    o << "        const double2 p = up2(la[pt" << gi << " ^ " << host_sw((uint32_t)NT * (r ^ xhi))
-                      << "u]);\n";
-                    if (any_re) o << "        const double re = fma(o.x, p.x, o.y * p.y);\n";
-                    if (any_im) o << "        const double im = fma(o.x, p.y, -o.y * p.x);\n";
-                } else {
-                    o << "        const double re = fma(o.x, o.x, o.y * o.y);\n";
-                }
-                for (const TT &tt : tts) {
-                    const bool neg = __builtin_popcount(tt.zhi & (uint32_t)r) & 1;
-                    o << "        s" << tj++ << (neg ? " -= " : " += ") << (tt.im ? "im" : "re") << ";\n";
-                }
-                o << "        }\n";
-            }
-            o << "    }\n";
-        }
-        ti = 0;
-        for (size_t gi = 0; gi < gl.size(); gi++)
-            for (const TT &tt : *gl[gi].second) {
-                o << "    e" << tt.kk << " = fma(par64(fb & " << tt.zF << "ull) ? -L" << ti << " : L" << ti << ", s" << ti
-                  << ", e" << tt.kk << ");\n";
-                ti++;
-            }
-        o << "    __syncthreads();\n"
-             "    }\n";
-        // fixed-order reduction: waves, then the four wave sums
-        for (int j = 0; j < NK; j++)
-            o << "    { const double v = wave_sum(e" << j << "); if (lane == 0) red[wave * " << NK << " + " << j
-              << "] = v; }\n";
-        o << "    __syncthreads();\n"
-             "    double *out = a.partial + ((int64_t)(row * a.npass + "
-          << pi
-          << ") * a.wg_per_row + w) * a.k_count;\n"
-             "    for (int k = tid; k < a.k_count; k += "
-          << NT
-          << ") {\n"
-             "        double v = 0.0;\n"
-             "        switch (k) {\n";
-        for (int j = 0; j < NK; j++) {
-            o << "        case " << ks[j] << ": v = red[" << j << "]";
-            for (int wv = 1; wv < NW; wv++) o << "; v += red[" << wv * NK + j << "]";
-            o << "; break;\n";
-        }
-        o << "        default: break;\n"
-             "        }\n"
-             "        out[k] = v;\n"
-             "    }\n"
-             "}\n";
-        (void)K;
-    }
+    for (size_t pi = 0; pi < passes.size(); pi++) pauli_exp_pass(o, passes[pi], (int)pi);
+    (void)K;
     o << "} // namespace tq\n";
     return o.str();
 }
@@ -1560,24 +1646,13 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
 }
 
-std::string hphi_spec_source(const std::vector<PauliPass> &passes, bool write_phi)
+std::string hphi_spec_source(const std::vector<PauliPass> &passes)
 {
     std::ostringstream o;
     o << kHead;
-    for (size_t pi = 0; pi < passes.size(); pi++) hphi_pass(o, passes[pi], (int)pi, write_phi);
+    for (size_t pi = 0; pi < passes.size(); pi++) hphi_pass(o, passes[pi], (int)pi);
     o << "} // namespace tq\n";
     return o.str();
-}
-
-hipError_t launch_hexp_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
-                            std::string *log, SpecMemo *memo)
-{
-    if (nrows <= 0) return hipSuccess;
-    hipFunction_t fn;
-    hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_hexp_" + N(pass), &fn,
-                               log);
-    if (e != hipSuccess) return e;
-    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
 }
 
 hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,

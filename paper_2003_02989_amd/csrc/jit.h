@@ -63,13 +63,8 @@ hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecAr
 // observable H (the same on every row) pass by pass, each pass's tile
 // holding the X bits of its terms; partials of the expectation go to
 // partial[row][npass][wg_per_row].
-std::string hphi_spec_source(const std::vector<PauliPass> &passes, bool write_phi = true);
+std::string hphi_spec_source(const std::vector<PauliPass> &passes);
 hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
-                            std::string *log, SpecMemo *memo);
-// The same passes forming only <psi|H|psi> (kernels tq_hexp_<pass>, source
-// from hphi_spec_source(passes, false)): no phi written, a.phi and
-// a.upstream unused.
-hipError_t launch_hexp_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
                             std::string *log, SpecMemo *memo);
 // Workgroups of a specialised Pauli pass that fit on the device at once (0 if unknown).
 int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo);

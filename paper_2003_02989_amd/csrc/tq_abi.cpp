@@ -94,11 +94,10 @@ struct ObsGroupDev {
     std::string spec_src;
     SpecMemo spec_memo;
     // passes and source of the kernels computing phi = g H psi for a single
-    // observable the same on every row (specialize = 1), and of their variant
-    // forming only <psi|H|psi> (expectations of more than 64 terms)
+    // observable the same on every row (specialize = 1)
     std::vector<PauliPass> phi_passes;
-    std::string phi_src, hexp_src;
-    SpecMemo phi_memo, hexp_memo;
+    std::string phi_src;
+    SpecMemo phi_memo;
     void release()
     {
         for (DevBuf *b : {&terms, &begin, &count, &chunks, &cbegin, &ccount, &xfg, &xg, &us, &pterms, &dchunks,
@@ -107,8 +106,11 @@ struct ObsGroupDev {
     }
 };
 
-// Largest observable (terms) whose phi = g H psi kernels are generated.
+// Largest observable (terms) whose phi = g H psi kernels are generated, and
+// largest observable set (terms over all its observables) whose expectation
+// kernels are.
 constexpr size_t kMaxPhiTerms = 1024;
+constexpr size_t kMaxSpecTerms = 1024;
 
 // Tile size of the Pauli kernel (log2 amplitudes): 2048 amplitudes, eight
 // per thread.
@@ -421,7 +423,7 @@ void ensure_obs(tq_program p, tq_observables o)
             for (auto &td : row) diag = diag && td.x == 0;
         size_t nterms = 0;
         for (auto &row : per_row) nterms = std::max(nterms, row.size());
-        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= 64) {
+        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= kMaxSpecTerms) {
             // tiles of 2^12 or 2^13 amplitudes (16 per thread) with runs of
             // 2^5 or 2^6 contiguous amplitudes: the fewest passes weighted by
             // what a pass costs (measured on 2^24..2^30 amplitudes: a 2^13
@@ -450,10 +452,7 @@ void ensure_obs(tq_program p, tq_observables o)
                     if (!pauli_spec_plan(n, t, c, per_row[0], &pp)) continue;
                     if (og->phi_passes.empty() || pp.size() < og->phi_passes.size()) og->phi_passes = std::move(pp);
                 }
-            if (!og->phi_passes.empty()) {
-                og->phi_src = hphi_spec_source(og->phi_passes, true);
-                og->hexp_src = hphi_spec_source(og->phi_passes, false);
-            }
+            if (!og->phi_passes.empty()) og->phi_src = hphi_spec_source(og->phi_passes);
         }
         if (diag) {
             DiagTables dt = diag_tables(per_row, uniform);
@@ -564,8 +563,7 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
 // phi = g H psi and <psi|H|psi> of a single observable (K = 1) with the
 // kernels generated for it: one read of psi and one update of phi per pass.
 // phi = g H psi and <psi|H|psi> of a single observable (K = 1) with the
-// kernels generated for it (phi = NULL: the expectation alone, by the
-// passes' variant that writes no phi).
+// kernels generated for it.
 void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, float *out,
                     hipStream_t s)
 {
@@ -589,8 +587,7 @@ void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, con
     for (int pi = 0; pi < npass; pi++) {
         a.g = og.phi_passes[pi].geom;
         a.pass = pi;
-        const hipError_t e = phi ? launch_hphi_spec(og.phi_src, pi, a, nrows, s, &log, &og.phi_memo)
-                                 : launch_hexp_spec(og.hexp_src, pi, a, nrows, s, &log, &og.hexp_memo);
+        const hipError_t e = launch_hphi_spec(og.phi_src, pi, a, nrows, s, &log, &og.phi_memo);
         if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
         hip_check(e, "specialised H_g launch");
     }
@@ -620,12 +617,6 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     }
     if (!phi && !og.spec_passes.empty()) {
         spec_pauli_group(p, gi, psi, K, out, s);
-        return;
-    }
-    // a single observable beyond the generated expectation passes' 64 terms:
-    // the H_g passes without their phi output
-    if (!phi && K == 1 && !og.phi_passes.empty()) {
-        spec_phi_group(p, gi, psi, nullptr, nullptr, out, s);
         return;
     }
     if (phi && upstream && K == 1 && !og.phi_passes.empty()) {

@@ -190,18 +190,19 @@ def test_c4_full_against_golden(specialize):
 @pytest.mark.parametrize("n,n_terms", [(14, 150), (16, 200), (13, 1000)])
 def test_specialized_expectation_many_terms(n, n_terms):
     # one observable of more than 64 Pauli strings, the same on every row:
-    # tq_expectation runs the generated H_g passes in their form without phi
-    # (up to 1024 terms); the plan shows the passes, the oracle the values
+    # tq_expectation runs the expectation passes generated for its terms (in
+    # blocks of running sums, up to 1024 terms); the plan shows the passes,
+    # the oracle the values
     w = wl.c5_vqe(B=8, n=n, layers=3, n_terms=n_terms)
-    say("expectation-only H passes n", n, "terms", n_terms)
+    say("generated expectation passes n", n, "terms", n_terms)
     p = tq.Program(w.program_blob(), specialize=True)
     o = tq.Observables(w.observable_blob())
     th = dev(w.theta, torch.float32)
     e = tq.expectation(p, th, o).cpu().numpy()
     plan = tq.describe(p)
     ob = plan["groups"][0]["obs"]
-    say("exp passes", ob["exp_passes"], "H_g passes", ob["phi_passes"])
-    assert not ob["exp_passes"] and sum(ob["phi_passes"]) == len(w.observables[0][0])
+    say("expectation passes", ob["exp_passes"], "H_g passes", ob["phi_passes"])
+    assert sum(ob["exp_passes"]) == len(w.observables[0][0])
     ref = orc.expectation(orc.Program(w.program_blob()), w.theta.astype(np.float64), orc.Observables(w.observable_blob()))
     say("max |d exp|", float(np.abs(e - ref).max()))
     assert np.abs(e - ref).max() <= TOL_EXP * max(1.0, float(np.abs(ref).max()))

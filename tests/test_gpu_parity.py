@@ -185,6 +185,24 @@ def test_specialized_pauli_passes(n, B):
     compare(gpu_outputs(w, want=("exp",), specialize=True), oracle_outputs(w, want=("exp",)))
 
 
+@pytest.mark.parametrize("n,K,max_terms", [(15, 16, 60), (14, 2, 400)])
+def test_specialized_pauli_passes_many(n, K, max_terms):
+    # the generated expectation passes with their terms in several blocks:
+    # sixteen observables (one accumulator each), and two observables of a few
+    # hundred terms (groups split across blocks)
+    w = wl.random_batch(5500 + n, B=2, n=n, n_gates=60, n_symbols=4, K=K)
+    shared = wl.random_observables(wl.rng_for(5600 + n), n, K, max_terms=max_terms, max_weight=5)
+    for b in range(w.B):
+        w.observables[b] = shared
+    say("specialised Pauli passes", n, "K", K, "terms", sum(len(o) for o in shared))
+    p = tq.Program(w.program_blob(), specialize=True)
+    e = tq.expectation(p, dev(w.theta), tq.Observables(w.observable_blob())).cpu().numpy()
+    ob = tq.describe(p)["groups"][0]["obs"]
+    say("generated expectation passes (terms per pass)", ob["exp_passes"])
+    assert sum(ob["exp_passes"]) == sum(len(o) for o in shared)
+    compare({"exp": e}, oracle_outputs(w, want=("exp",)))
+
+
 @pytest.mark.gpu
 def test_amplitudes_from_state_matches_amplitudes():
     # the state-based lookup returns what tq_amplitudes returns, bit for bit,
