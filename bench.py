@@ -528,26 +528,42 @@ def sweep(steps, cases="all", specialize=True):
                               "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
         if cases not in ("all", "expectation"):
             continue
-        # expectation kernels: sum_i Z_i, 30 random Z_i Z_j plus a constant
-        # (the QAOA cost's shape), and 16 random X/Y/Z strings
+        # expectation kernels on a product state (RY, RZ on every qubit: one
+        # fused pass) whose expectations have a closed form, checked on every
+        # row: sum_i Z_i, 30 random Z_i Z_j plus a constant (the QAOA cost's
+        # shape), 16 random X/Y/Z strings, 200 (the VQE Hamiltonian's shape)
+        # and sixteen observables of 650 strings over all
+        from paper_2003_02989_amd.workloads import random_pauli_strings
         rng = np.random.default_rng(n)
-        obs_sets = {"sum Z_i": [(1.0, [(i, "Z")]) for i in range(n)],
-                    "16 XYZ strings": [(float(rng.standard_normal()),
-                                        [(int(x), "XYZ"[int(rng.integers(0, 3))])
-                                         for x in rng.choice(n, size=int(rng.integers(1, 5)), replace=False)])
-                                       for _ in range(16)],
-                    "30 ZZ + constant": [(-0.5, [(int(a), "Z"), (int(b), "Z")])
-                                         for a, b in (rng.choice(n, size=2, replace=False) for _ in range(30))]
-                                        + [(15.0, [])]}
+        obs_sets = {"sum Z_i": [[(1.0, [(i, "Z")]) for i in range(n)]],
+                    "16 XYZ strings": [[(float(rng.standard_normal()),
+                                         [(int(x), "XYZ"[int(rng.integers(0, 3))])
+                                          for x in rng.choice(n, size=int(rng.integers(1, 5)), replace=False)])
+                                        for _ in range(16)]],
+                    "30 ZZ + constant": [[(-0.5, [(int(a), "Z"), (int(b), "Z")])
+                                          for a, b in (rng.choice(n, size=2, replace=False) for _ in range(30))]
+                                         + [(15.0, [])]],
+                    "200 XYZ strings": [random_pauli_strings(rng, n, 200)],
+                    "16 observables, 650 strings": [random_pauli_strings(rng, n, 200)]
+                    + [random_pauli_strings(rng, n, 30) for _ in range(15)]}
+        ang_t = rng.uniform(0.0, 2 * np.pi, size=n)
+        ang_f = rng.uniform(0.0, 2 * np.pi, size=n)
         c = Circuit(n)
-        for i in range(n - 1):
-            c.add("CZ", (i, i + 1))
+        for i in range(n):
+            c.add("RY", i, [const(float(ang_t[i]))])
+            c.add("RZ", i, [const(float(ang_f[i]))])
+        comp = [{"X": np.sin(ang_t[q]) * np.cos(ang_f[q]), "Y": np.sin(ang_t[q]) * np.sin(ang_f[q]),
+                 "Z": np.cos(ang_t[q])} for q in range(n)]
         prog = tq.Program(program_blob([c] * B, 0), specialize=specialize)
-        for oname, terms in obs_sets.items():
-            obs = tq.Observables(observable_blob([[terms]] * B))
-            out = torch.empty((B, 1), dtype=torch.float32, device="cuda")
+        for oname, sums in obs_sets.items():
+            K = len(sums)
+            obs = tq.Observables(observable_blob([sums] * B))
+            out = torch.empty((B, K), dtype=torch.float32, device="cuda")
             tq.expectation(prog, None, obs, out=out)
             torch.cuda.synchronize()
+            ref = np.array([sum(cf * np.prod([comp[q][p] for q, p in fac]) for cf, fac in terms) for terms in sums])
+            err = float(np.abs(out.cpu().numpy() - ref[None, :]).max())
+            tol = float((1e-6 * np.array([sum(abs(cf) for cf, _ in t) for t in sums]) + 1e-6).min())
             tq.profile_start("pauli")
             for _ in range(steps):
                 tq.expectation(prog, None, obs, out=out)
@@ -555,10 +571,14 @@ def sweep(steps, cases="all", specialize=True):
             nl, ms = tq.profile_read()
             tq.profile_start(None)
             ms /= steps  # every launch of the call (one per pass of the plan)
+            n_terms = sum(len(t) for t in sums)
             gbs = 8.0 * (1 << n) * B / (ms * 1e-3) / 1e9
-            print(json.dumps({"sweep": "expectation", "n": n, "batch": B, "case": oname, "ms": ms,
-                              "launches_per_call": nl // steps,
-                              "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
+            tfs = 4.0 * n_terms * (1 << n) * B / (ms * 1e-3) / 1e12
+            print(json.dumps({"sweep": "expectation", "n": n, "batch": B, "case": oname, "terms": n_terms,
+                              "ms": ms, "launches_per_call": nl // steps,
+                              "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS,
+                              "fp64_TFLOP_per_s": tfs, "frac_of_fp64_peak": tfs / PEAK_FP64_TFLOPS,
+                              "closed_form_max_error": err, "closed_form_ok": err <= tol}), flush=True)
         del prog
 
 

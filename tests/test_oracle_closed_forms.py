@@ -147,3 +147,26 @@ def test_identity_term_and_empty_circuit():
     c = Circuit(3)
     e, _ = run([c], 0, np.zeros((1, 0)), [[[(2.5, []), (1.0, [(2, "Z")]), (1.0, [(1, "X")])]]])
     assert abs(e[0, 0] - 3.5) < 1e-15
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_product_state_pauli_strings(seed):
+    # RY(t) then RZ(f) on every qubit: a product state whose Bloch vectors are
+    # (sin t cos f, sin t sin f, cos t); a Pauli string's expectation is its
+    # coefficient times the product of its factors' components (X/Y/Z strings
+    # of any weight, several observables, identity terms)
+    rng = np.random.default_rng(70 + seed)
+    n, B = 6, 3
+    c = Circuit(n)
+    for q in range(n):
+        c.add("RY", q, [sym(q)]).add("RZ", q, [sym(n + q)])
+    obs = [wl.random_pauli_strings(rng, n, 25, max_weight=n) + [(0.3, [])] for _ in range(3)]
+    theta = rng.uniform(0.0, 2 * math.pi, size=(B, 2 * n))
+    e, im = run([c] * B, 2 * n, theta, [obs] * B)
+    for b in range(B):
+        t, f = theta[b, :n], theta[b, n:]
+        comp = [{"X": math.sin(t[q]) * math.cos(f[q]), "Y": math.sin(t[q]) * math.sin(f[q]), "Z": math.cos(t[q])}
+                for q in range(n)]
+        for k, terms in enumerate(obs):
+            ref = sum(cf * np.prod([comp[q][p] for q, p in fac]) for cf, fac in terms)
+            assert abs(e[b, k] - ref) < 1e-13 and abs(im[b, k]) < 1e-13
