@@ -3,7 +3,8 @@
 TEST INFRASTRUCTURE ONLY.  Independent of tq_oracle.c: every gate is built
 here from its generator with a matrix exponential (a rotation is
 exp(-i theta G / 2), a power gate is G^t = exp(i pi t (I - G) / 2), fSim is
-exp(-i theta (XX + YY) / 2) times a controlled phase), embedded in the full
+exp(-i theta (XX + YY) / 2) times a controlled phase, a Pauli-string
+exponential is exp(-i eta P)), embedded in the full
 2^n x 2^n space by index arithmetic, and the circuit unitary is the plain
 matrix product (Sec. "Quantum Neural Networks", eq. full_par_circ).  Pauli
 sums are Kronecker products of 2x2 Paulis (eq. cost_lincomb).
@@ -71,6 +72,11 @@ def gate(name, eta=(), matrix=None):
         return expm(-1j * eta[0] / 2 * (XX + YY)) @ np.diag([1, 1, 1, np.exp(-1j * eta[1])])
     if name in ("MATRIX1", "MATRIX2"):
         return np.asarray(matrix, dtype=complex)
+    if name == "PAULIEXP":  # the letters of the string ride in the matrix slot
+        P = np.array([[1.0 + 0j]])
+        for p in matrix:
+            P = np.kron(P, PAULI[p])
+        return expm(-1j * eta[0] * P)
     raise ValueError(name)
 
 

@@ -12,7 +12,9 @@
  *  - the final state of each circuit of the batch, psi_b = W_G ... W_1 |0..0>,
  *    with every parameter resolved from the symbol values (Sec. "Cirq",
  *    ParamResolver semantics; Sec. "Quantum Neural Networks",
- *    eqs. full_par_circ, layer_blocks, Pauli_decomp);
+ *    eqs. full_par_circ, layer_blocks, Pauli_decomp); the gates include the
+ *    exponential exp(-i eta P) of a Pauli string of any weight, applied as
+ *    cos(eta) psi - i sin(eta) P psi (eq. cs_decomp);
  *  - expectation values <psi_b| h_{b,k} |psi_b> of Pauli sums
  *    h = sum_t c_t P_t (Sec. "Sampling and Expectations",
  *    eqs. cost_lincomb and qee_lincomb);
@@ -69,7 +71,9 @@ enum {
     OP_H = 1, OP_X, OP_Y, OP_Z, OP_RX, OP_RY, OP_RZ, OP_XPOW, OP_YPOW, OP_ZPOW,
     OP_CZ, OP_CNOT, OP_CZPOW, OP_CNOTPOW, OP_XXPOW, OP_YYPOW, OP_ZZPOW, OP_RZZ,
     OP_SQRTX, OP_SQRTY, OP_SQRTW, OP_FSIM, OP_MATRIX1, OP_MATRIX2, OP_SWAP,
-    OP_LAST = OP_SWAP
+    OP_LAST = OP_SWAP,
+    /* exp(-i eta P) of a Pauli string P of any weight (variable qubit count) */
+    OP_PAULIEXP = 26
 };
 
 /* qubit count and parameter count of every opcode */
@@ -255,6 +259,7 @@ typedef struct {
     int sym[2];
     double scale[2], offset[2];
     double mat[32];
+    int *pq, *pp; /* OP_PAULIEXP: its nq qubits and their Paulis (1=X, 2=Y, 3=Z) */
 } OGate;
 
 typedef struct {
@@ -312,7 +317,13 @@ void orc_program_free(void *h)
 {
     OProgram *pr = (OProgram *)h;
     if (!pr) return;
-    for (int b = 0; b < pr->B; b++) free(pr->c[b].g);
+    for (int b = 0; b < pr->B; b++) {
+        for (int i = 0; i < pr->c[b].ngates; i++) {
+            free(pr->c[b].g[i].pq);
+            free(pr->c[b].g[i].pp);
+        }
+        free(pr->c[b].g);
+    }
     free(pr->c);
     free(pr);
 }
@@ -338,6 +349,28 @@ int orc_program_parse(const void *blob, size_t nbytes, void **out)
         for (uint32_t i = 0; i < ng; i++) {
             OGate *g = &c->g[i];
             g->op = rd_u16(&r); g->nq = rd_u8(&r); g->np = rd_u8(&r);
+            if (!r.bad && g->op == OP_PAULIEXP) {
+                /* w qubits (distinct), one parameter, then w Pauli codes */
+                if (g->np != 1 || g->nq > (int)n) { orc_program_free(pr); return fail("bad Pauli exponential"); }
+                g->pq = calloc(g->nq ? g->nq : 1, sizeof(int));
+                g->pp = calloc(g->nq ? g->nq : 1, sizeof(int));
+                for (int j = 0; j < g->nq; j++) {
+                    uint32_t q = rd_u32(&r);
+                    if (q >= n) { orc_program_free(pr); return fail("qubit out of range"); }
+                    for (int k = 0; k < j; k++)
+                        if (g->pq[k] == (int)q) { orc_program_free(pr); return fail("duplicate qubit"); }
+                    g->pq[j] = (int)q;
+                }
+                int32_t s = (int32_t)rd_u32(&r);
+                g->sym[0] = s; g->scale[0] = rd_f64(&r); g->offset[0] = rd_f64(&r);
+                if (s < -1 || s >= (int32_t)S) { orc_program_free(pr); return fail("symbol out of range"); }
+                for (int j = 0; j < g->nq; j++) {
+                    g->pp[j] = rd_u8(&r);
+                    if (g->pp[j] < 1 || g->pp[j] > 3) { orc_program_free(pr); return fail("bad Pauli code"); }
+                }
+                if (r.bad) { orc_program_free(pr); return fail("truncated program"); }
+                continue;
+            }
             int enq, enp;
             if (r.bad || op_arity(g->op, &enq, &enp) || enq != g->nq || enp != g->np) {
                 orc_program_free(pr); return fail("bad gate opcode/arity");
@@ -460,6 +493,29 @@ static void apply_matrix(cplx *psi, int n, int nq, const int *qs, const cplx *m,
     }
 }
 
+/* psi <- a psi + b P psi for the Pauli string of an OP_PAULIEXP gate: with
+ * (a, b) = (cos eta, -i sin eta) the gate exp(-i eta P) = cos(eta) I -
+ * i sin(eta) P (Sec. "Quantum Neural Networks", eqs. Pauli_decomp and
+ * cs_decomp), (cos eta, i sin eta) its inverse and (-sin eta, -i cos eta)
+ * its derivative.  P psi: the string's 2x2 Paulis applied one by one. */
+static void apply_pauli_exp(cplx *psi, int n, const OGate *g, cplx a, cplx b, int par)
+{
+    const int64_t N = (int64_t)1 << n;
+    cplx *tmp = malloc(sizeof(cplx) * N);
+    memcpy(tmp, psi, sizeof(cplx) * N);
+    for (int f = 0; f < g->nq; f++) {
+        cplx m[4];
+        pauli2(g->pp[f], m);
+        apply_matrix(tmp, n, 1, &g->pq[f], m, par);
+    }
+    for (int64_t i = 0; i < N; i++) {
+        cplx w = a * psi[i] + b * tmp[i];
+        if (g_c64_storage) w = (float)creal(w) + I * (float)cimag(w);
+        psi[i] = w;
+    }
+    free(tmp);
+}
+
 static void dagger(int d, const cplx *m, cplx *out)
 {
     for (int i = 0; i < d; i++)
@@ -484,6 +540,10 @@ static void simulate_row(const OCircuit *c, const double *theta_row, cplx *psi, 
         cplx m[16];
         int d;
         resolve(g, theta_row, eta);
+        if (g->op == OP_PAULIEXP) {
+            apply_pauli_exp(psi, c->n, g, cos(eta[0]), -I * sin(eta[0]), par);
+            continue;
+        }
         gate_matrix(g->op, eta, g->mat, m, &d);
         apply_matrix(psi, c->n, g->nq, g->q, m, par);
     }
@@ -592,6 +652,17 @@ int orc_adjoint_grad(void *hp, const double *theta, void *ho, const double *upst
             cplx m[16], md[16];
             int d;
             resolve(g, th, eta);
+            if (g->op == OP_PAULIEXP) {
+                const double cs = cos(eta[0]), sn = sin(eta[0]);
+                apply_pauli_exp(psi, c->n, g, cs, I * sn, par);
+                if (g->sym[0] >= 0) {
+                    memcpy(dpsi, psi, sizeof(cplx) * N);
+                    apply_pauli_exp(dpsi, c->n, g, -sn, -I * cs, par);
+                    gr[g->sym[0]] += g->scale[0] * 2.0 * creal(inner(phi, dpsi, N));
+                }
+                apply_pauli_exp(phi, c->n, g, cs, I * sn, par);
+                continue;
+            }
             gate_matrix(g->op, eta, g->mat, m, &d);
             dagger(d, m, md);
             apply_matrix(psi, c->n, g->nq, g->q, md, par);

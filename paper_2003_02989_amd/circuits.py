@@ -14,6 +14,13 @@ Program blob::
       per gate:   u16 opcode  u8 nq  u8 np  u32 qubit[nq]
                   np x { i32 symbol (-1 = constant)  f64 scale  f64 offset }
                   MATRIX1: 8 f64, MATRIX2: 32 f64 (re, im interleaved, row major)
+                  PAULIEXP: nq u8 Pauli codes (1=X 2=Y 3=Z), one per qubit
+
+PAULIEXP (opcode 26) is exp(-i eta P) for the Pauli string P over its nq
+qubits (any weight, nq = 0 being a global phase), the exponentials of the
+Pauli decomposition of a generator (Sec. "Quantum Neural Networks",
+eqs. Pauli_decomp and cs_decomp) that the paper's exponential utility builds
+from a Pauli sum term by term.
 
 Each parameter resolves to eta = scale * symbol_values[b, symbol] + offset
 (or eta = offset for a constant), the affine symbol expressions of the
@@ -43,6 +50,7 @@ OPS = {
     "XXPOW": (15, 2, 1), "YYPOW": (16, 2, 1), "ZZPOW": (17, 2, 1), "RZZ": (18, 2, 1),
     "SQRTX": (19, 1, 0), "SQRTY": (20, 1, 0), "SQRTW": (21, 1, 0),
     "FSIM": (22, 2, 2), "MATRIX1": (23, 1, 0), "MATRIX2": (24, 2, 0), "SWAP": (25, 2, 0),
+    "PAULIEXP": (26, None, 1),
 }
 OPCODE_NAMES = {v[0]: k for k, v in OPS.items()}
 PAULI_CODES = {"X": 1, "Y": 2, "Z": 3}
@@ -66,8 +74,21 @@ class Circuit:
         self.n = int(n_qubits)
         self.gates = []
 
+    def add_pauli_exp(self, factors, param):
+        """exp(-i eta P) for the Pauli string ``factors`` = [(qubit, 'X'|'Y'|'Z'), ...]
+        (distinct qubits; an empty list is the global phase exp(-i eta)); the
+        string's letters ride in the gate's matrix slot."""
+        qubits = tuple(int(q) for q, _ in factors)
+        letters = "".join(p for _, p in factors)
+        if any(p not in PAULI_CODES for p in letters):
+            raise ValueError("Pauli factors are X, Y or Z")
+        self.gates.append(("PAULIEXP", qubits, (param if isinstance(param, tuple) else const(param),), letters))
+        return self
+
     def add(self, name, qubits, params=(), matrix=None):
         code, nq, npar = OPS[name]
+        if nq is None:
+            raise ValueError(f"{name} is added with add_pauli_exp")
         qubits = tuple(int(q) for q in (qubits if isinstance(qubits, (tuple, list)) else (qubits,)))
         if len(qubits) != nq:
             raise ValueError(f"{name} takes {nq} qubits")
@@ -89,10 +110,13 @@ def program_blob(circuits, n_symbols):
         out.append(struct.pack("<II", c.n, len(c.gates)))
         for name, qubits, params, matrix in c.gates:
             code, nq, npar = OPS[name]
+            nq = len(qubits)
             out.append(struct.pack("<HBB", code, nq, npar))
             out.append(struct.pack(f"<{nq}I", *qubits))
             for s, scale, offset in params:
                 out.append(struct.pack("<idd", s, scale, offset))
+            if name == "PAULIEXP":
+                out.append(bytes(PAULI_CODES[p] for p in matrix))
             if name in ("MATRIX1", "MATRIX2"):
                 d = 2 if name == "MATRIX1" else 4
                 m = np.asarray(matrix, np.complex128).reshape(d, d)
