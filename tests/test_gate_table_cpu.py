@@ -11,7 +11,10 @@ from oracle import oracle as orc
 from paper_2003_02989_amd import tq
 from paper_2003_02989_amd.circuits import OPS
 
-PARAM_OPS = [name for name, (code, nq, npar) in OPS.items() if npar > 0]
+# gates with a fixed matrix size (the Pauli-string exponential has none: it is
+# lowered to these gates when a program is parsed)
+GATES = sorted(name for name, (code, nq, npar) in OPS.items() if nq is not None)
+PARAM_OPS = [name for name in GATES if OPS[name][2] > 0]
 VALUES = [0.0, 0.37, -1.3, 2.9]
 
 
@@ -19,7 +22,7 @@ def lib_matrix(op, p, **kw):
     return tq.gate_matrix(op, p, **kw)
 
 
-@pytest.mark.parametrize("name", sorted(OPS))
+@pytest.mark.parametrize("name", GATES)
 def test_phase_times_built_matrix_is_the_gate(name):
     code, nq, npar = OPS[name]
     rng = np.random.default_rng(code)
