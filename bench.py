@@ -92,7 +92,8 @@ def describe_config(name, w):
     if name == "c2":
         return f"c2 QNN classifier n={n} B={w.B} RX(pi x) encoding + 4 layers ZZ^t, XX^t to readout, Z_9, expectations+adjoint grads"
     if name == "c3":
-        return f"c3 QAOA MaxCut n={n} B={w.B} p=4 random 3-regular graph, cut observable, expectations"
+        how = " layers from Pauli-string exponentials of H_C, H_M," if w.name == "c3_qaoa_exp" else ""
+        return f"c3 QAOA MaxCut n={n} B={w.B} p=4 random 3-regular graph,{how} cut observable, expectations"
     if name == "c4":
         return f"c4 random circuit n={n} B=1 depth 20 sqrtX/Y/W + fSim 5x6 grid, 4096 amplitudes + 10^6 samples"
     return f"c5 VQE ansatz n={n} B={w.B} 10 layers RY,RZ + CNOT ring, 200 Pauli strings, expectations+adjoint grads"
@@ -223,6 +224,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--expectation-only", action="store_true",
                     help="c1, c2, c5: time tq_expectation (no adjoint gradients)")
+    ap.add_argument("--pauli-exp", action="store_true",
+                    help="c3: the QAOA layers built from Pauli-string exponentials of the cost and mixer "
+                         "Hamiltonians")
     ap.add_argument("--no-specialize", action="store_true",
                     help="run with the precompiled table-driven kernels instead of the ones compiled for the "
                          "circuit structure on the first call")
@@ -257,6 +261,8 @@ def main():
         cmd = [sys.executable, os.path.abspath(__file__), "--cold-probe", "--config", args.config]
         if args.expectation_only:
             cmd.append("--expectation-only")
+        if args.pauli_exp:
+            cmd.append("--pauli-exp")
         cold = {}
         for key in ("empty_cache", "filled_cache"):
             r = subprocess.run(cmd, env=env, capture_output=True, text=True, timeout=900)
@@ -285,7 +291,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes_read": 8 << 27, "bytes_written": 8 << 27, "copies": 3}))
         return
-    w = workload(args.config)
+    if args.pauli_exp and args.config != "c3":
+        print("--pauli-exp applies to c3 only", file=sys.stderr)
+        sys.exit(1)
+    w = wl.c3_qaoa(exponentials=True) if args.pauli_exp else workload(args.config)
     B, K = w.B, w.K
     adjoint = args.config in ("c1", "c2", "c5") and not args.expectation_only
     specialize = not args.no_specialize
@@ -372,7 +381,8 @@ def main():
     n_terms = sum(len(t) for t in w.observables[0])
     flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, adjoint)
     avg_ms = dom_ms / max(n_launch, 1)
-    traffic = measured_traffic(args.config, dominant)
+    traffic = measured_traffic(args.config + ("_expectation" if args.expectation_only else "")
+                               + ("_pauli_exp" if args.pauli_exp else ""), dominant)
     per_launch_flops = flops / max(launches_per_step, 1)
     per_launch_bytes = bytes_ / max(launches_per_step, 1)
     hbm = {"bound": "hbm", "achieved": per_launch_bytes / (avg_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,

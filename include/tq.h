@@ -95,7 +95,8 @@ typedef struct {
  *     per circuit: u32 n_qubits u32 n_gates
  *       per gate:  u16 opcode u8 nq u8 np u32 qubit[nq]
  *                  np x { i32 symbol (-1 = constant) f64 scale f64 offset }
- *                  then 8 f64 for MATRIX1, 32 f64 for MATRIX2 (re, im, row major)
+ *                  then 8 f64 for MATRIX1, 32 f64 for MATRIX2 (re, im, row major),
+ *                  nq u8 Pauli codes (1 X, 2 Y, 3 Z) for PAULIEXP
  * A parameter resolves to eta = scale * symbol_values[b, symbol] + offset, the
  * affine symbol maps of the paper's chain rule (Sec. "Parameter shift
  * methods", eq. chain_rule); constants take eta = offset.
@@ -106,6 +107,13 @@ typedef struct {
  *     16 YYPOW(t)  17 ZZPOW(t)  18 RZZ(gamma) = exp(-i gamma Z Z / 2)
  *     19 SQRTX  20 SQRTY  21 SQRTW  22 FSIM(theta, phi)  23 MATRIX1
  *     24 MATRIX2  25 SWAP
+ *     26 PAULIEXP(eta) = exp(-i eta P) = cos(eta) I - i sin(eta) P for the
+ *        Pauli string P over its nq distinct qubits, any weight (nq = 0: the
+ *        global phase exp(-i eta)); the exponentials of a generator's Pauli
+ *        decomposition (Sec. "Quantum Neural Networks", eqs. Pauli_decomp and
+ *        cs_decomp).  It is lowered to the gates above when the program is
+ *        parsed (basis changes, a CNOT ladder around RZ / RZZ(2 eta)), so
+ *        tq_program_describe counts the lowered gates.
  * A two-qubit gate on (a, b) uses the local index 2*bit(a) + bit(b).
  * Circuits may have 0..32 qubits and any number of gates.  `opt` may be NULL.
  * On success *out owns the parsed program; release it with

@@ -1316,6 +1316,87 @@ DiagTables diag_tables(const std::vector<std::vector<TermDev>> &per_row, bool un
     return dt;
 }
 
+// exp(-i eta P) for a Pauli string P (Sec. "Quantum Neural Networks",
+// eqs. Pauli_decomp and cs_decomp), read from the blob after its header
+// (nq = the string's weight w, np = 1: w qubits, the parameter, w Pauli
+// codes) and written as gates of the fixed table, which the planner fuses:
+// each X factor turned into Z by H on both sides, each Y by RX(pi/2) before
+// and RX(-pi/2) after (RX(t)^dag Z RX(t) = cos t Z + sin t Y); the Z string
+// by RZZ(2 eta) for weight two, and for more by a CNOT ladder that gathers
+// the parity of the first w - 1 qubits into the (w-1)-th, RZZ(2 eta) with
+// the last, and the ladder undone.  Weight one is RX, RY or RZ(2 eta)
+// itself; weight zero is the global phase exp(-i eta) = RZ(2 eta)
+// ZPOW(-2 eta / pi) on qubit 0.
+// The parameter keeps its symbol: the emitted rotations scale it by 2 (or
+// -2/pi), so the chain rule sums their gradients back onto the symbol.
+template <class Emit>
+void lower_pauli_exp(Reader &r, const HGate &head, int n, int32_t S, uint32_t b, uint32_t i, Emit &&emit)
+{
+    const std::string where = "circuit " + std::to_string(b) + " gate " + std::to_string(i);
+    const int w = head.nq;
+    if (head.np != 1) fail(TQ_E_INVALID, where + ": a Pauli exponential takes one parameter");
+    if (w > n) fail(TQ_E_INVALID, where + ": Pauli string longer than the circuit");
+    std::vector<uint32_t> qs(w);
+    for (int j = 0; j < w; j++) {
+        qs[j] = r.get<uint32_t>();
+        if (!r.bad && qs[j] >= (uint32_t)n) fail(TQ_E_INVALID, where + ": qubit out of range");
+        for (int k = 0; k < j; k++)
+            if (qs[k] == qs[j]) fail(TQ_E_INVALID, where + ": repeated qubit");
+    }
+    const int32_t sym = r.get<int32_t>();
+    const double scale = r.get<double>(), offset = r.get<double>();
+    if (!r.bad && (sym < -1 || sym >= S)) fail(TQ_E_INVALID, where + ": symbol column out of range");
+    std::vector<uint8_t> ps(w);
+    for (int j = 0; j < w; j++) {
+        ps[j] = r.get<uint8_t>();
+        if (!r.bad && (ps[j] < 1 || ps[j] > 3)) fail(TQ_E_INVALID, where + ": Pauli code must be 1 (X), 2 (Y) or 3 (Z)");
+    }
+    if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+    auto gate = [](int op, uint32_t q0, uint32_t q1 = 0) {
+        HGate h{};
+        h.op = (uint16_t)op;
+        int nq, np;
+        op_shape(op, nq, np);
+        h.nq = (uint8_t)nq;
+        h.np = (uint8_t)np;
+        h.q[0] = q0;
+        h.q[1] = q1;
+        return h;
+    };
+    auto param = [&](HGate h, double f) {  // the exponential's parameter times f
+        h.sym[0] = sym;
+        h.scale[0] = f * scale;
+        h.offset[0] = f * offset;
+        return h;
+    };
+    auto constant = [](HGate h, double v) {
+        h.sym[0] = -1;
+        h.offset[0] = v;
+        return h;
+    };
+    if (w == 0) {
+        if (n == 0) return;  // no qubit to carry the phase: a circuit without amplitudes to scale
+        emit(param(gate(OP_RZ, 0), 2.0));
+        emit(param(gate(OP_ZPOW, 0), -2.0 / M_PI));
+        return;
+    }
+    auto basis = [&](bool before) {
+        for (int j = 0; j < w; j++) {
+            if (ps[j] == 1) emit(gate(OP_H, qs[j]));
+            else if (ps[j] == 2) emit(constant(gate(OP_RX, qs[j]), before ? M_PI / 2 : -M_PI / 2));
+        }
+    };
+    if (w == 1) {  // exp(-i eta X) = RX(2 eta), likewise Y and Z: no basis change
+        emit(param(gate(ps[0] == 1 ? OP_RX : ps[0] == 2 ? OP_RY : OP_RZ, qs[0]), 2.0));
+        return;
+    }
+    basis(true);
+    for (int j = 0; j + 2 < w; j++) emit(gate(OP_CNOT, qs[j], qs[j + 1]));
+    emit(param(gate(OP_RZZ, qs[w - 2], qs[w - 1]), 2.0));
+    for (int j = w - 3; j >= 0; j--) emit(gate(OP_CNOT, qs[j], qs[j + 1]));
+    basis(false);
+}
+
 std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt)
 {
     if (!blob) fail(TQ_E_INVALID, "program blob is NULL");
@@ -1345,9 +1426,16 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
         HCircuit &c = pd->circuits[b];
         c.n = (int)n;
         pd->nmax = std::max(pd->nmax, (int)n);
-        if (gates.size() < ng) gates.resize(ng);
+        // m: gates of the circuit after lowering (a Pauli-string exponential
+        // becomes several gates)
+        size_t m = 0;
+        auto emit = [&](const HGate &h) {
+            if (m == gates.size()) gates.push_back(h);
+            else gates[m] = h;
+            m++;
+        };
+        HGate g{};
         for (uint32_t i = 0; i < ng; i++) {
-            HGate &g = gates[i];
             g.op = r.get<uint16_t>();
             g.nq = r.get<uint8_t>();
             g.np = r.get<uint8_t>();
@@ -1355,6 +1443,10 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             g.sym[0] = g.sym[1] = 0;
             g.scale[0] = g.scale[1] = g.offset[0] = g.offset[1] = 0.0;
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+            if (g.op == OP_PAULIEXP) {
+                lower_pauli_exp(r, g, (int)n, (int32_t)S, b, i, emit);
+                continue;
+            }
             int enq, enp;
             if (!op_shape(g.op, enq, enp))
                 fail(TQ_E_UNSUPPORTED, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
@@ -1384,7 +1476,10 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             if (nm)
                 for (int j = nm; j < 32; j++) g.mat[j] = 0.0;
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+            emit(g);
         }
+        if (m > (size_t)1 << 24) fail(TQ_E_INVALID, "program blob: gate count too large");
+        ng = (uint32_t)m;
         // structure dedupe: same qubit count, opcodes, qubits, symbol wiring
         // and explicit matrices; scales and offsets may differ per row
         key.clear();

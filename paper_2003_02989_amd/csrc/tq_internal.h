@@ -22,6 +22,9 @@ enum Opcode : uint16_t {
     OP_SQRTX, OP_SQRTY, OP_SQRTW, OP_FSIM, OP_MATRIX1, OP_MATRIX2, OP_SWAP,
     OP_COUNT
 };
+// exp(-i eta P) of a Pauli string: a blob opcode only, lowered to the gates
+// above when a program is parsed
+constexpr uint16_t OP_PAULIEXP = 26;
 
 constexpr int kMaxQubits = 32;
 constexpr int kThreads = 256;  // threads per workgroup of every tile kernel

@@ -137,25 +137,37 @@ def random_regular3(rng, n):
             return sorted(edges)
 
 
-def c3_qaoa(B=256, n=20, p=4, seed=BASE_SEED + 3):
+def c3_qaoa(B=256, n=20, p=4, seed=BASE_SEED + 3, exponentials=False):
     """H on every qubit, then per layer l: RZZ(gamma_l) on every edge and
     RX(beta_l) on every qubit; symbols gamma_1..p = 0..p-1, beta = p..2p-1,
     (gamma, beta) ~ U[0, pi).  Observable sum_edges 0.5 (1 - Z_i Z_j) =
-    |E|/2 * I - 0.5 sum_edges Z_i Z_j."""
+    |E|/2 * I - 0.5 sum_edges Z_i Z_j.
+
+    exponentials=True builds the layers as the paper's QAOA example does,
+    from the exponentials of the two Hamiltonians: exp(-i gamma_l H_C) as the
+    product of its terms' exponentials (the constant one a global phase, each
+    -0.5 Z_i Z_j one Pauli-string exponential), then exp(-i beta_l sum X_i)
+    as one exponential per qubit."""
     rng = rng_for(seed)
     edges = random_regular3(rng, n)
     theta = rng.uniform(0.0, math.pi, size=(B, 2 * p)).astype(np.float32)
+    obs = [(0.5 * len(edges), [])] + [(-0.5, [(a, "Z"), (b, "Z")]) for a, b in edges]
     c = Circuit(n)
     for q in range(n):
         c.add("H", q)
     for l in range(p):
+        if exponentials:
+            for coeff, factors in obs:
+                c.add_pauli_exp(factors, sym(l, coeff))
+            for q in range(n):
+                c.add_pauli_exp([(q, "X")], sym(p + l))
+            continue
         for a, b in edges:
             c.add("RZZ", (a, b), [sym(l)])
         for q in range(n):
             c.add("RX", q, [sym(p + l)])
-    obs = [(0.5 * len(edges), [])] + [(-0.5, [(a, "Z"), (b, "Z")]) for a, b in edges]
-    return Workload("c3_qaoa", [c] * B, 2 * p, theta, _repeat_obs(obs, B), np.ones((B, 1), np.float32),
-                    {"edges": edges})
+    return Workload("c3_qaoa_exp" if exponentials else "c3_qaoa", [c] * B, 2 * p, theta, _repeat_obs(obs, B),
+                    np.ones((B, 1), np.float32), {"edges": edges})
 
 
 # ----------------------------------------------------------------------- c4

@@ -125,3 +125,32 @@ def test_specialize_option_is_validated():
     opt = tq._Options(0, 0, 1, 0, 2)
     h = ctypes.c_void_p()
     assert tq.lib().tq_program_create(blob, len(blob), ctypes.byref(opt), ctypes.byref(h)) == tq.TQ_E_INVALID
+
+
+def test_pauli_exponential_is_lowered_and_validated():
+    # exp(-i eta P) becomes gates of the fixed table: X -> H, Y -> RX(pi/2) on
+    # both sides, weight 3 -> one CNOT each side of RZZ; weight 1 -> RX, RY or
+    # RZ; weight 0 -> RZ and ZPOW on qubit 0
+    c = Circuit(4).add_pauli_exp([(0, "X"), (2, "Y"), (3, "Z")], sym(0, 0.5))
+    d = tq.describe(create(program_blob([c], 1)))
+    assert d["groups"][0]["gates"] == 2 + 1 + 1 + 1 + 2
+    for fac, ng in (([(1, "Z")], 1), ([(1, "X")], 1), ([(2, "Y")], 1), ([], 2), ([(0, "Z"), (3, "Z")], 1),
+                    ([(0, "X"), (3, "Y")], 5),
+                    ([(q, "Z") for q in range(4)], 5)):
+        d = tq.describe(create(program_blob([Circuit(4).add_pauli_exp(fac, sym(0))], 1)))
+        assert d["groups"][0]["gates"] == ng, fac
+    # same structure for rows that differ only in the exponential's scale
+    rows = [Circuit(3).add_pauli_exp([(0, "X"), (1, "Z")], sym(0, s)) for s in (0.3, -1.0)]
+    assert len(tq.describe(create(program_blob(rows, 1)))["groups"]) == 1
+
+    def blob(qubits, codes, np_=1, n=4):
+        return (b"TQP1" + struct.pack("<III", 1, 1, 1) + struct.pack("<II", n, 1)
+                + struct.pack("<HBB", 26, len(qubits), np_) + struct.pack(f"<{len(qubits)}I", *qubits)
+                + b"".join(struct.pack("<idd", 0, 1.0, 0.0) for _ in range(np_)) + bytes(codes))
+    create(blob([0, 1], [1, 3]))
+    assert status_of(lambda: create(blob([0, 0], [1, 3]))) == tq.TQ_E_INVALID  # repeated qubit
+    assert status_of(lambda: create(blob([0, 4], [1, 3]))) == tq.TQ_E_INVALID  # qubit >= n
+    assert status_of(lambda: create(blob([0, 1], [1, 4]))) == tq.TQ_E_INVALID  # Pauli code
+    assert status_of(lambda: create(blob([0, 1], [1, 3], np_=2))) == tq.TQ_E_INVALID  # parameters
+    assert status_of(lambda: create(blob([0, 1], [1, 3])[:-1])) == tq.TQ_E_INVALID  # truncated
+    assert status_of(lambda: create(blob([0, 1, 2, 3, 0], [1, 1, 1, 1, 1]))) == tq.TQ_E_INVALID  # longer than n

@@ -69,6 +69,32 @@ def test_c3_full_sampled_rows(specialize):
     assert np.all(g["exp"] >= -TOL_EXP) and np.all(g["exp"] <= 30 + TOL_EXP)
 
 
+def test_c3_exponentials_reduced():
+    # the QAOA layers built from the exponentials of the cost and mixer
+    # Hamiltonians (the paper's QAOA example), every output against the oracle
+    w = wl.c3_qaoa(B=16, n=14, exponentials=True)
+    say("c3 by exponentials, reduced n=14 B=16")
+    compare(gpu_outputs(w), oracle_outputs(w))
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("specialize", [False, True])
+def test_c3_exponentials_full_sampled_rows(specialize):
+    w = wl.c3_qaoa(exponentials=True)
+    say("c3 by exponentials, full n=20 B=256 specialize", specialize)
+    g = gpu_outputs(w, want=("exp", "grad"), specialize=specialize)
+    rows = [0, 128, 255]
+    ref = oracle_outputs(sub_workload(w, rows), want=("exp", "grad"))
+    gs = {"exp": g["exp"][rows], "grad": g["grad"][rows], "grad_exp": g["grad_exp"][rows]}
+    compare(gs, ref)
+    # the same circuits as the RZZ / RX layers up to the parametrization:
+    # exp(-i gamma (-1/2) Z Z) = RZZ(-gamma), exp(-i beta X) = RX(2 beta)
+    v = wl.c3_qaoa()
+    v.theta = w.theta * np.array([-1.0] * 4 + [2.0] * 4, np.float32)
+    e2 = gpu_outputs(v, want=("exp",), specialize=specialize)["exp"]
+    assert np.abs(e2 - g["exp"]).max() <= 2 * TOL_EXP
+
+
 def test_c5_reduced():
     w = wl.c5_vqe(B=24, n=12, layers=10, n_terms=200)
     say("c5 reduced n=12 B=24")

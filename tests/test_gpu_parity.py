@@ -290,3 +290,25 @@ def test_sampler_zero_row_marker():
     r = orc.sample_from_state(z, 3000, seed=8)
     assert np.all(g[1] == np.uint64(2**64 - 1))
     assert np.array_equal(g, r)
+
+
+@pytest.mark.parametrize("specialize", [False, True])
+@pytest.mark.parametrize("n,seed", [(9, 0), (13, 1), (15, 2)])
+def test_pauli_exponentials_random(n, seed, specialize):
+    # Pauli-string exponentials of every weight (0 to n, X/Y/Z letters,
+    # symbolic with shared symbols, or constant) interleaved with random
+    # gates: states, expectations and adjoint gradients against the oracle
+    # (resident states, and tile passes of 13 and 15 qubits)
+    from paper_2003_02989_amd.circuits import Circuit, const, sym
+    rng = wl.rng_for(8100 + seed)
+    w = wl.random_batch(8200 + seed, B=3, n=n, n_gates=30, n_symbols=4, K=2)
+    for c in w.circuits:
+        for _ in range(8):
+            wt = int(rng.integers(0, n + 1))
+            fac = [(int(q), "XYZ"[int(rng.integers(0, 3))]) for q in rng.choice(n, size=wt, replace=False)]
+            par = (sym(int(rng.integers(0, 4)), float(rng.normal()), float(rng.normal())) if rng.random() < 0.75
+                   else const(float(rng.normal())))
+            e = Circuit(n).add_pauli_exp(fac, par).gates[0]
+            c.gates.insert(int(rng.integers(0, len(c.gates) + 1)), e)
+    say("Pauli exponentials", n, seed, "specialize", specialize)
+    compare(gpu_outputs(w, specialize=specialize), oracle_outputs(w))
