@@ -126,3 +126,24 @@ def pauli_sum(terms, n):
 def expectation(gates, n, theta_row, terms):
     psi = state(gates, n, theta_row)
     return np.vdot(psi, pauli_sum(terms, n) @ psi)
+
+
+def density_expectation(gates, n, theta_row, terms):
+    """tr(H rho) with rho evolved as a density matrix: unitaries as U rho U^dag,
+    a Pauli channel (p_x, p_y, p_z) as (1 - p) rho + sum_k p_k P_k rho P_k
+    (Sec. "Noise in qsim", the full-density-matrix alternative to trajectories)."""
+    N = 1 << n
+    rho = np.zeros((N, N), dtype=complex)
+    rho[0, 0] = 1.0
+    for name, qubits, params, matrix in gates:
+        eta = resolve(params, theta_row)
+        if name == "PCHAN":
+            out = (1.0 - sum(eta)) * rho
+            for p, P in zip(eta, (PX, PY, PZ)):
+                E = embed(P, qubits, n)
+                out = out + p * (E @ rho @ E.conj().T)
+            rho = out
+            continue
+        U = embed(gate(name, eta, matrix), qubits, n)
+        rho = U @ rho @ U.conj().T
+    return np.trace(pauli_sum(terms, n) @ rho)

@@ -58,6 +58,9 @@ def lib():
         L.orc_set_c64_storage.argtypes = [i32]
         L.orc_num_threads.restype = i32
         L.orc_op_arity.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.orc_set_noise_seed.argtypes = [u64]
+        L.orc_channel_pick.argtypes = [u64, i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double]
+        L.orc_channel_pick.restype = i32
         _lib = L
     return _lib
 
@@ -190,3 +193,14 @@ def set_c64_storage(on):
 
 def num_threads():
     return int(lib().orc_num_threads())
+
+
+def set_noise_seed(seed):
+    """Seed of the channels' Kraus draws in every later call (trajectory rows)."""
+    lib().orc_set_noise_seed(int(seed) & 0xFFFFFFFFFFFFFFFF)
+
+
+def channel_pick(seed, row, chan, px, py, pz):
+    """The Pauli (0 = I, 1 = X, 2 = Y, 3 = Z) channel `chan` of batch row `row` applies."""
+    return int(lib().orc_channel_pick(int(seed) & 0xFFFFFFFFFFFFFFFF, int(row), int(chan), float(px), float(py),
+                                      float(pz)))

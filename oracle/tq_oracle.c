@@ -23,6 +23,8 @@
  *    the effective Hamiltonian H_g of Sec. "Autodifferentiation through
  *    hybrid quantum-classical backpropagation"; shared symbols add up over
  *    their occurrences by the chain rule, eq. chain_rule);
+ *  - noisy circuits by trajectories (Sec. "Noise in qsim"): each row draws
+ *    one Pauli per channel from a counter stream and is then a pure circuit;
  *  - bitstring samples drawn from |psi_i|^2 (Sec. "Sampling and Expectation
  *    Values") with the integer fixed-point rule and the SplitMix64 counter
  *    stream fixed in the design doc (the paper leaves both open).
@@ -73,7 +75,10 @@ enum {
     OP_SQRTX, OP_SQRTY, OP_SQRTW, OP_FSIM, OP_MATRIX1, OP_MATRIX2, OP_SWAP,
     OP_LAST = OP_SWAP,
     /* exp(-i eta P) of a Pauli string P of any weight (variable qubit count) */
-    OP_PAULIEXP = 26
+    OP_PAULIEXP = 26,
+    /* Pauli channel on one qubit: X, Y, Z with probabilities p_x, p_y, p_z
+     * (three constant parameters), one Kraus operator drawn per trajectory */
+    OP_PCHAN = 27
 };
 
 /* qubit count and parameter count of every opcode */
@@ -91,6 +96,8 @@ static int op_arity(int op, int *nq, int *np)
         *nq = 2; *np = 1; return 0;
     case OP_FSIM:
         *nq = 2; *np = 2; return 0;
+    case OP_PCHAN:
+        *nq = 1; *np = 3; return 0;
     default:
         return 1;
     }
@@ -256,8 +263,9 @@ static int gate_dmatrix(int op, const double *p, int which, cplx *dm, int *d)
 typedef struct {
     int op, nq, np;
     int q[2];
-    int sym[2];
-    double scale[2], offset[2];
+    int sym[3];
+    double scale[3], offset[3];
+    int chan; /* OP_PCHAN: its ordinal among the circuit's channels */
     double mat[32];
     int *pq, *pp; /* OP_PAULIEXP: its nq qubits and their Paulis (1=X, 2=Y, 3=Z) */
 } OGate;
@@ -343,6 +351,7 @@ int orc_program_parse(const void *blob, size_t nbytes, void **out)
         uint32_t n = rd_u32(&r), ng = rd_u32(&r);
         if (r.bad || n > 34 || ng > (1u << 24)) { orc_program_free(pr); return fail("bad circuit header"); }
         OCircuit *c = &pr->c[b];
+        int nchan = 0;
         c->n = (int)n; c->ngates = (int)ng;
         c->g = calloc(ng ? ng : 1, sizeof(OGate));
         if ((int)n > pr->nmax) pr->nmax = (int)n;
@@ -387,6 +396,17 @@ int orc_program_parse(const void *blob, size_t nbytes, void **out)
                 g->scale[j] = rd_f64(&r);
                 g->offset[j] = rd_f64(&r);
                 if (s < -1 || s >= (int32_t)S) { orc_program_free(pr); return fail("symbol out of range"); }
+            }
+            if (g->op == OP_PCHAN) {
+                double tot = 0;
+                for (int j = 0; j < 3; j++) {
+                    if (g->sym[j] != -1 || !(g->offset[j] >= 0.0)) {
+                        orc_program_free(pr); return fail("channel probabilities must be constants >= 0");
+                    }
+                    tot += g->offset[j];
+                }
+                if (!(tot <= 1.0)) { orc_program_free(pr); return fail("channel probabilities sum above 1"); }
+                g->chan = nchan++;
             }
             int nm = g->op == OP_MATRIX1 ? 8 : g->op == OP_MATRIX2 ? 32 : 0;
             for (int j = 0; j < nm; j++) g->mat[j] = rd_f64(&r);
@@ -529,19 +549,56 @@ static void resolve(const OGate *g, const double *theta_row, double *eta)
         eta[j] = g->sym[j] >= 0 ? g->scale[j] * theta_row[g->sym[j]] + g->offset[j] : g->offset[j];
 }
 
-static void simulate_row(const OCircuit *c, const double *theta_row, cplx *psi, int par)
+/* ------------------------------------------------------------------ noise */
+/* Trajectory simulation of noisy circuits (Sec. "Noise in qsim"): every row
+ * is one trajectory; at each channel one Kraus operator is drawn and
+ * applied.  For a Pauli channel (X, Y, Z with probabilities p_x, p_y, p_z,
+ * else the identity) the draw of channel k of batch row b is
+ * r = (u >> 11) 2^-53 with u = output number (b 2^32 + k) of SplitMix64 from
+ * the noise seed: X if r < p_x, Y if r < p_x + p_y, Z if r < p_x + p_y + p_z
+ * (sums in that order, in fp64), else I. */
+static uint64_t g_noise_seed = 0;
+void orc_set_noise_seed(uint64_t seed) { g_noise_seed = seed; }
+
+uint64_t orc_splitmix64(uint64_t seed, uint64_t counter);
+
+/* 0 = I, 1 = X, 2 = Y, 3 = Z */
+int orc_channel_pick(uint64_t seed, int64_t row, int chan, double px, double py, double pz)
+{
+    const uint64_t u = orc_splitmix64(seed, ((uint64_t)row << 32) | (uint64_t)chan);
+    const double r = (double)(u >> 11) * 0x1.0p-53;
+    if (r < px) return 1;
+    if (r < px + py) return 2;
+    if (r < px + py + pz) return 3;
+    return 0;
+}
+
+/* the Pauli a channel gate applies in row `row` (the identity as I) */
+static void channel_matrix(const OGate *g, int64_t row, cplx *m)
+{
+    const int k = orc_channel_pick(g_noise_seed, row, g->chan, g->offset[0], g->offset[1], g->offset[2]);
+    if (k == 0) mat_eye(2, m);
+    else pauli2(k, m);
+}
+
+static void simulate_row(const OCircuit *c, const double *theta_row, int64_t row, cplx *psi, int par)
 {
     const int64_t N = (int64_t)1 << c->n;
     for (int64_t i = 0; i < N; i++) psi[i] = 0;
     psi[0] = 1;
     for (int i = 0; i < c->ngates; i++) {
         const OGate *g = &c->g[i];
-        double eta[2];
+        double eta[3];
         cplx m[16];
         int d;
         resolve(g, theta_row, eta);
         if (g->op == OP_PAULIEXP) {
             apply_pauli_exp(psi, c->n, g, cos(eta[0]), -I * sin(eta[0]), par);
+            continue;
+        }
+        if (g->op == OP_PCHAN) {
+            channel_matrix(g, row, m);
+            apply_matrix(psi, c->n, 1, g->q, m, par);
             continue;
         }
         gate_matrix(g->op, eta, g->mat, m, &d);
@@ -589,7 +646,7 @@ int orc_simulate_state(void *hp, const double *theta, double *out)
     for (int b = 0; b < pr->B; b++) {
         cplx *row = (cplx *)out + (int64_t)b * stride;
         for (int64_t i = 0; i < stride; i++) row[i] = 0;
-        simulate_row(&pr->c[b], theta + (int64_t)b * pr->S, row, par);
+        simulate_row(&pr->c[b], theta + (int64_t)b * pr->S, b, row, par);
     }
     return 0;
 }
@@ -607,7 +664,7 @@ int orc_expectation(void *hp, const double *theta, void *ho, double *out, double
         const OCircuit *c = &pr->c[b];
         const int64_t N = (int64_t)1 << c->n;
         cplx *psi = malloc(sizeof(cplx) * N), *tmp = malloc(sizeof(cplx) * N), *hp_ = malloc(sizeof(cplx) * N);
-        simulate_row(c, theta + (int64_t)b * pr->S, psi, par);
+        simulate_row(c, theta + (int64_t)b * pr->S, b, psi, par);
         for (int k = 0; k < o->K; k++) {
             for (int64_t i = 0; i < N; i++) hp_[i] = 0;
             for (int t = o->start[b * o->K + k]; t < o->start[b * o->K + k + 1]; t++)
@@ -639,7 +696,7 @@ int orc_adjoint_grad(void *hp, const double *theta, void *ho, const double *upst
         cplx *psi = malloc(sizeof(cplx) * N), *phi = malloc(sizeof(cplx) * N);
         cplx *tmp = malloc(sizeof(cplx) * N), *dpsi = malloc(sizeof(cplx) * N);
         for (int s = 0; s < pr->S; s++) gr[s] = 0;
-        simulate_row(c, th, psi, par);
+        simulate_row(c, th, b, psi, par);
         for (int64_t i = 0; i < N; i++) phi[i] = 0;
         for (int k = 0; k < o->K; k++) {
             double gk = upstream[(int64_t)b * o->K + k];
@@ -648,10 +705,16 @@ int orc_adjoint_grad(void *hp, const double *theta, void *ho, const double *upst
         }
         for (int i = c->ngates - 1; i >= 0; i--) {
             const OGate *g = &c->g[i];
-            double eta[2];
+            double eta[3];
             cplx m[16], md[16];
             int d;
             resolve(g, th, eta);
+            if (g->op == OP_PCHAN) { /* the trajectory's Pauli: its own inverse, no parameter */
+                channel_matrix(g, b, m);
+                apply_matrix(psi, c->n, 1, g->q, m, par);
+                apply_matrix(phi, c->n, 1, g->q, m, par);
+                continue;
+            }
             if (g->op == OP_PAULIEXP) {
                 const double cs = cos(eta[0]), sn = sin(eta[0]);
                 apply_pauli_exp(psi, c->n, g, cs, I * sn, par);
@@ -693,7 +756,7 @@ int orc_amplitudes(void *hp, const double *theta, const uint64_t *bits, int64_t 
     for (int b = 0; b < pr->B; b++) {
         const OCircuit *c = &pr->c[b];
         cplx *psi = malloc(sizeof(cplx) * ((int64_t)1 << c->n));
-        simulate_row(c, theta + (int64_t)b * pr->S, psi, par);
+        simulate_row(c, theta + (int64_t)b * pr->S, b, psi, par);
         for (int64_t m = 0; m < M; m++) {
             cplx a = psi[bits[b * M + m]];
             out[2 * (b * M + m)] = creal(a);
@@ -777,7 +840,7 @@ int orc_sample(void *hp, const double *theta, int64_t n_shots, uint64_t seed, ui
         const int64_t N = (int64_t)1 << c->n;
         cplx *psi = malloc(sizeof(cplx) * N);
         double *p = malloc(sizeof(double) * N);
-        simulate_row(c, theta + (int64_t)b * pr->S, psi, par);
+        simulate_row(c, theta + (int64_t)b * pr->S, b, psi, par);
         for (int64_t i = 0; i < N; i++) p[i] = creal(psi[i]) * creal(psi[i]) + cimag(psi[i]) * cimag(psi[i]);
         bad |= sample_row_from_p(p, N, b, n_shots, seed, out + (int64_t)b * n_shots);
         free(psi); free(p);

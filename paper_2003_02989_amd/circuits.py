@@ -16,6 +16,12 @@ Program blob::
                   MATRIX1: 8 f64, MATRIX2: 32 f64 (re, im interleaved, row major)
                   PAULIEXP: nq u8 Pauli codes (1=X 2=Y 3=Z), one per qubit
 
+PCHAN (opcode 27) is a Pauli channel on one qubit: X, Y or Z with the
+constant probabilities (p_x, p_y, p_z) of its three parameters, else the
+identity.  Noisy circuits run as trajectories (Sec. "Noise in qsim"): every
+batch row draws one Pauli per channel from a counter stream seeded per call,
+so R rows holding the same circuit are R trajectories of it.
+
 PAULIEXP (opcode 26) is exp(-i eta P) for the Pauli string P over its nq
 qubits (any weight, nq = 0 being a global phase), the exponentials of the
 Pauli decomposition of a generator (Sec. "Quantum Neural Networks",
@@ -51,6 +57,7 @@ OPS = {
     "SQRTX": (19, 1, 0), "SQRTY": (20, 1, 0), "SQRTW": (21, 1, 0),
     "FSIM": (22, 2, 2), "MATRIX1": (23, 1, 0), "MATRIX2": (24, 2, 0), "SWAP": (25, 2, 0),
     "PAULIEXP": (26, None, 1),
+    "PCHAN": (27, 1, 3),
 }
 OPCODE_NAMES = {v[0]: k for k, v in OPS.items()}
 PAULI_CODES = {"X": 1, "Y": 2, "Z": 3}
@@ -84,6 +91,16 @@ class Circuit:
             raise ValueError("Pauli factors are X, Y or Z")
         self.gates.append(("PAULIEXP", qubits, (param if isinstance(param, tuple) else const(param),), letters))
         return self
+
+    def depolarize(self, qubit, p):
+        """Depolarizing channel: X, Y or Z each with probability p / 3."""
+        return self.add("PCHAN", qubit, [p / 3.0, p / 3.0, p / 3.0])
+
+    def bit_flip(self, qubit, p):
+        return self.add("PCHAN", qubit, [p, 0.0, 0.0])
+
+    def phase_flip(self, qubit, p):
+        return self.add("PCHAN", qubit, [0.0, 0.0, p])
 
     def add(self, name, qubits, params=(), matrix=None):
         code, nq, npar = OPS[name]

@@ -11,9 +11,10 @@ from oracle import oracle as orc
 from paper_2003_02989_amd import tq
 from paper_2003_02989_amd.circuits import OPS
 
-# gates with a fixed matrix size (the Pauli-string exponential has none: it is
-# lowered to these gates when a program is parsed)
-GATES = sorted(name for name, (code, nq, npar) in OPS.items() if nq is not None)
+# gates with a fixed matrix (the Pauli-string exponential has no fixed size:
+# it is lowered to these gates when a program is parsed; a channel's matrix
+# is drawn per trajectory)
+GATES = sorted(name for name, (code, nq, npar) in OPS.items() if nq is not None and name != "PCHAN")
 PARAM_OPS = [name for name in GATES if OPS[name][2] > 0]
 VALUES = [0.0, 0.37, -1.3, 2.9]
 

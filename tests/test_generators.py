@@ -16,7 +16,7 @@ from oracle import oracle as orc
 from paper_2003_02989_amd import tq
 from paper_2003_02989_amd.circuits import OPS, Circuit, program_blob, sym
 
-PARAM_GATES = sorted(name for name, (_, nq, npar) in OPS.items() if npar > 0 and nq is not None)
+PARAM_GATES = sorted(name for name, (_, nq, npar) in OPS.items() if npar > 0 and nq is not None and name != "PCHAN")
 
 X = np.array([[0, 1], [1, 0]], dtype=complex)
 Z = np.diag([1.0, -1.0]).astype(complex)
