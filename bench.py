@@ -79,24 +79,27 @@ def workload(name):
 
 
 def describe_workload(name, w, adjoint=True):
-    d = describe_config(name, w)
+    d = describe_config(name, w, w.B // w.extras.get("trajectories", 1))
+    if "trajectories" in w.extras:
+        d += (f", depolarizing noise p={w.extras['noise_p']} after every gate, "
+              f"{w.extras['trajectories']} trajectories per circuit (B={w.B} trajectory rows)")
     if name in ("c1", "c2", "c5") and not adjoint:
         d = d.replace("expectations+adjoint grads", "expectations only")
     return d
 
 
-def describe_config(name, w):
+def describe_config(name, w, B):
     n = w.n_max
     if name == "c1":
-        return f"c1 hardware-efficient ansatz n={n} B={w.B} 2 layers RX,RY,RZ + CZ ladder, sum Z, expectations+adjoint grads"
+        return f"c1 hardware-efficient ansatz n={n} B={B} 2 layers RX,RY,RZ + CZ ladder, sum Z, expectations+adjoint grads"
     if name == "c2":
-        return f"c2 QNN classifier n={n} B={w.B} RX(pi x) encoding + 4 layers ZZ^t, XX^t to readout, Z_9, expectations+adjoint grads"
+        return f"c2 QNN classifier n={n} B={B} RX(pi x) encoding + 4 layers ZZ^t, XX^t to readout, Z_9, expectations+adjoint grads"
     if name == "c3":
-        how = " layers from Pauli-string exponentials of H_C, H_M," if w.name == "c3_qaoa_exp" else ""
-        return f"c3 QAOA MaxCut n={n} B={w.B} p=4 random 3-regular graph,{how} cut observable, expectations"
+        how = " layers from Pauli-string exponentials of H_C, H_M," if w.name.startswith("c3_qaoa_exp") else ""
+        return f"c3 QAOA MaxCut n={n} B={B} p=4 random 3-regular graph,{how} cut observable, expectations"
     if name == "c4":
         return f"c4 random circuit n={n} B=1 depth 20 sqrtX/Y/W + fSim 5x6 grid, 4096 amplitudes + 10^6 samples"
-    return f"c5 VQE ansatz n={n} B={w.B} 10 layers RY,RZ + CNOT ring, 200 Pauli strings, expectations+adjoint grads"
+    return f"c5 VQE ansatz n={n} B={B} 10 layers RY,RZ + CNOT ring, 200 Pauli strings, expectations+adjoint grads"
 
 
 # Algorithmic work of one op applied to one amplitude, in the form the plan
@@ -224,6 +227,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--expectation-only", action="store_true",
                     help="c1, c2, c5: time tq_expectation (no adjoint gradients)")
+    ap.add_argument("--noise", type=float, default=0.0,
+                    help="c1, c2, c3, c5: depolarizing channel of this probability after every gate on its qubits, "
+                         "simulated as --trajectories trajectories per circuit (averaged)")
+    ap.add_argument("--trajectories", type=int, default=10)
     ap.add_argument("--pauli-exp", action="store_true",
                     help="c3: the QAOA layers built from Pauli-string exponentials of the cost and mixer "
                          "Hamiltonians")
@@ -263,6 +270,8 @@ def main():
             cmd.append("--expectation-only")
         if args.pauli_exp:
             cmd.append("--pauli-exp")
+        if args.noise > 0:
+            cmd += ["--noise", str(args.noise), "--trajectories", str(args.trajectories)]
         cold = {}
         for key in ("empty_cache", "filled_cache"):
             r = subprocess.run(cmd, env=env, capture_output=True, text=True, timeout=900)
@@ -295,6 +304,14 @@ def main():
         print("--pauli-exp applies to c3 only", file=sys.stderr)
         sys.exit(1)
     w = wl.c3_qaoa(exponentials=True) if args.pauli_exp else workload(args.config)
+    noisy = args.noise > 0
+    if noisy and args.config == "c4":
+        print("--noise applies to c1, c2, c3, c5", file=sys.stderr)
+        sys.exit(1)
+    R = args.trajectories if noisy else 1
+    w_base = w
+    if noisy:
+        w = wl.with_noise(w_base, args.noise, R)
     B, K = w.B, w.K
     adjoint = args.config in ("c1", "c2", "c5") and not args.expectation_only
     specialize = not args.no_specialize
@@ -302,11 +319,15 @@ def main():
     # own parameter set, drawn like the workload's
     n_prof = 2 * len(KERNELS)
     n_steps_total = 1 + args.warmup + n_prof + args.steps
-    thetas = ([torch.as_tensor(t, device="cuda") for t in wl.fresh_thetas(w, n_steps_total, 7 + wl.BASE_SEED)]
+    # (the trajectories of a noisy circuit share its parameters)
+    thetas = ([torch.as_tensor(np.repeat(t, R, axis=0), device="cuda")
+               for t in wl.fresh_thetas(w_base, n_steps_total, 7 + wl.BASE_SEED)]
               if w.n_symbols else [None] * n_steps_total)
     up = torch.as_tensor(w.upstream, device="cuda")
     exp = torch.empty((B, K), dtype=torch.float32, device="cuda")
     grad = torch.empty((B, w.n_symbols), dtype=torch.float32, device="cuda")
+    exp_mean = torch.empty((B // R, K), dtype=torch.float32, device="cuda")
+    grad_mean = torch.empty((B // R, w.n_symbols), dtype=torch.float32, device="cuda")
     if args.config == "c4":
         bits = torch.as_tensor(w.extras["bitstrings"].astype(np.int64), device="cuda")
         amps = torch.empty((1, bits.shape[1]), dtype=torch.complex64, device="cuda")
@@ -320,10 +341,17 @@ def main():
         i = counter[0]
         counter[0] += 1
         th = thetas[i]
+        if noisy:  # new trajectories every step
+            tq.set_noise_seed(prog, 1000 + i)
         if adjoint:
             tq.adjoint_grad(prog, th, obs, up, grad=grad, expectations=exp)
+            if noisy:
+                tq.row_mean(grad, R, out=grad_mean)
+                tq.row_mean(exp, R, out=exp_mean)
         elif args.config != "c4":
             tq.expectation(prog, th, obs, out=exp)
+            if noisy:
+                tq.row_mean(exp, R, out=exp_mean)
         else:
             # one simulation serves both outputs; a new sampling seed per step
             tq.sample_with_amplitudes(prog, None, n_shots, w.extras["seed"] + i, bits, out=shots, amps=amps)
@@ -418,15 +446,21 @@ def main():
                  "cold_ms": cold_s * 1e3,
                  "cold_cached_ms": cached_s * 1e3 if cached_s else None}
     else:
-        value = B * K / (ms_per_step * 1e-3)
+        # noisy: one circuit-expectation is the mean over its R trajectories
+        Bc = B // R
+        value = Bc * K / (ms_per_step * 1e-3)
         unit_v = "circuit-expectations/s" + (" (with adjoint gradients)" if adjoint else "")
+        if noisy:
+            unit_v += f" (noisy: mean of {R} trajectories each)"
         rates = {"circuit_expectations_per_s": value,
-                 "cold_circuit_expectations_per_s": B * K / cold_s,
-                 "cold_cached_circuit_expectations_per_s": B * K / cached_s if cached_s else None,
+                 "cold_circuit_expectations_per_s": Bc * K / cold_s,
+                 "cold_cached_circuit_expectations_per_s": Bc * K / cached_s if cached_s else None,
                  "fused_pass_GBps": fused_pass_gbs,
                  "fused_pass_ms_per_step": pass_ms if pass_ms > 0 else None}
+        if noisy:
+            rates["trajectory_rows_per_s"] = B / (ms_per_step * 1e-3)
         if adjoint:
-            rates["gradient_rows_per_s"] = B / (ms_per_step * 1e-3)
+            rates["gradient_rows_per_s"] = Bc / (ms_per_step * 1e-3)
 
     line = {
         "metric": METRIC,
@@ -443,7 +477,8 @@ def main():
         "data": "synthetic (seeded generators, no datasets); a new parameter set or sampling seed per step",
         "config": {"workload": describe_workload(args.config, w, adjoint), "storage": "complex64", "arithmetic": "fp64",
                    "batch": B, "qubits": w.n_max, "symbols": w.n_symbols, "observables": K,
-                   "pauli_terms": n_terms, "specialized_kernel": specialize},
+                   "pauli_terms": n_terms, "specialized_kernel": specialize,
+                   "noise": {"depolarizing_p": args.noise, "trajectories": R} if noisy else None},
         "cold_start": {"fresh_process_empty_code_cache": cold["empty_cache"] if cold else None,
                        "fresh_process_filled_code_cache": cold["filled_cache"] if cold else None,
                        "this_process": here},
@@ -453,7 +488,7 @@ def main():
     }
 
     if not args.no_cpu_baseline and local_rank == 0:
-        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds, adjoint)
+        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds, adjoint, R)
     print(json.dumps(line), flush=True)
     if cache_tmp:
         shutil.rmtree(cache_tmp, ignore_errors=True)
@@ -592,7 +627,7 @@ def sweep(steps, cases="all", specialize=True):
         del prog
 
 
-def cpu_baseline(name, w, budget_s, adjoint=True):
+def cpu_baseline(name, w, budget_s, adjoint=True, R=1):
     """The oracle on the host cores, on a bounded sample of the same workload."""
     import numpy as np
 
@@ -639,7 +674,7 @@ def cpu_baseline(name, w, budget_s, adjoint=True):
             break
         rows = min(max(rows * 2, 1), w.B)
     what = "expectations" + (" + adjoint gradients" if adjoint else "")
-    return {"value": done_rows * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
+    return {"value": done_rows / R * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
             "cpu": cpu_model(),
             "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "
                       f"the full batch) in {el:.1f} s"}

@@ -114,12 +114,34 @@ typedef struct {
  *        cs_decomp).  It is lowered to the gates above when the program is
  *        parsed (basis changes, a CNOT ladder around RZ / RZZ(2 eta)), so
  *        tq_program_describe counts the lowered gates.
+ *     27 PCHAN(p_x, p_y, p_z), one qubit: a Pauli channel, X, Y or Z with these
+ *        probabilities (constant parameters, each >= 0, sum <= 1), else the
+ *        identity.  Noisy circuits run as trajectories (Sec. "Noise in
+ *        qsim"): in every call each batch row draws one Pauli per channel and
+ *        is then a pure circuit, so R rows holding the same circuit are R
+ *        trajectories of it; tq_row_mean averages their outputs.  The draw of
+ *        channel k (its ordinal among the circuit's channels) in batch row b:
+ *        r = (u >> 11) 2^-53 with u the output number (b 2^32 + k) of
+ *        SplitMix64 started at the program's noise seed
+ *        (tq_program_set_noise_seed, default 0); X if r < p_x, Y if
+ *        r < p_x + p_y, Z if r < p_x + p_y + p_z (fp64, in that order).
  * A two-qubit gate on (a, b) uses the local index 2*bit(a) + bit(b).
  * Circuits may have 0..32 qubits and any number of gates.  `opt` may be NULL.
  * On success *out owns the parsed program; release it with
  * tq_program_destroy. */
 tq_status tq_program_create(const void *blob, size_t nbytes, const tq_options *opt, tq_program *out);
 void tq_program_destroy(tq_program prog);
+
+/* Seed of the channels' Kraus draws (opcode 27) in the program's later calls;
+ * a new seed per call gives new trajectories.  Host only. */
+tq_status tq_program_set_noise_seed(tq_program prog, uint64_t seed);
+
+/* out[g, k] = (1/R) sum_{r < R} in[g R + r, k] for g < groups, k < K: the
+ * average over R consecutive rows (the trajectories of one noisy circuit),
+ * summed in fp64 in row order.  in: device float[groups R, K]; out: device
+ * float[groups, K]; both caller-owned; enqueued on `stream`.  TQ_E_INVALID
+ * for R < 1, negative sizes or NULL pointers with work to do. */
+tq_status tq_row_mean(const float *in, int64_t groups, int32_t R, int32_t K, float *out, void *stream);
 
 /* Compile the kernels a program created with specialize = 1 generates for
  * its circuit structures (per structure: the resident kernel when its

@@ -59,6 +59,7 @@ def lib():
         L.orc_num_threads.restype = i32
         L.orc_op_arity.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.orc_set_noise_seed.argtypes = [u64]
+        L.orc_set_row_offset.argtypes = [i64]
         L.orc_channel_pick.argtypes = [u64, i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double]
         L.orc_channel_pick.restype = i32
         _lib = L
@@ -204,3 +205,8 @@ def channel_pick(seed, row, chan, px, py, pz):
     """The Pauli (0 = I, 1 = X, 2 = Y, 3 = Z) channel `chan` of batch row `row` applies."""
     return int(lib().orc_channel_pick(int(seed) & 0xFFFFFFFFFFFFFFFF, int(row), int(chan), float(px), float(py),
                                       float(pz)))
+
+
+def set_row_offset(offset):
+    """Rows of a program draw their channels as rows offset + b of a larger batch."""
+    lib().orc_set_row_offset(int(offset))

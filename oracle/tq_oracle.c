@@ -559,6 +559,10 @@ static void resolve(const OGate *g, const double *theta_row, double *eta)
  * (sums in that order, in fp64), else I. */
 static uint64_t g_noise_seed = 0;
 void orc_set_noise_seed(uint64_t seed) { g_noise_seed = seed; }
+/* added to a program row's index in the draws: rows of a larger batch
+ * simulated one by one keep their own draws */
+static int64_t g_row_offset = 0;
+void orc_set_row_offset(int64_t off) { g_row_offset = off; }
 
 uint64_t orc_splitmix64(uint64_t seed, uint64_t counter);
 
@@ -576,7 +580,7 @@ int orc_channel_pick(uint64_t seed, int64_t row, int chan, double px, double py,
 /* the Pauli a channel gate applies in row `row` (the identity as I) */
 static void channel_matrix(const OGate *g, int64_t row, cplx *m)
 {
-    const int k = orc_channel_pick(g_noise_seed, row, g->chan, g->offset[0], g->offset[1], g->offset[2]);
+    const int k = orc_channel_pick(g_noise_seed, row + g_row_offset, g->chan, g->offset[0], g->offset[1], g->offset[2]);
     if (k == 0) mat_eye(2, m);
     else pauli2(k, m);
 }

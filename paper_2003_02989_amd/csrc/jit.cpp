@@ -436,7 +436,7 @@ bool const_m1(const Group &g, const PassOp &op, ConstM1 *out)
     double acc[8] = {1, 0, 0, 0, 0, 0, 1, 0};
     for (int mi = 0; mi < bt->mem_count; mi++) {
         const GateDev &gd = g.gates[g.members[bt->mem_begin + mi].gate];
-        double eta[2] = {0, 0};
+        double eta[3] = {0, 0, 0};
         for (int j = 0; j < gd.np; j++) {
             if (g.slot_sym[gd.slot0 + j] >= 0) return false;
             eta[j] = g.slot_off[gd.slot0 + j];

@@ -31,6 +31,8 @@ struct BuildArgs {
     int32_t phase_out;
     int32_t n_phase;
     const PhaseTerm *phase_terms;
+    // seed of the channels' per-row Kraus draws
+    uint64_t noise_seed;
 };
 
 struct StageBuildArgs {

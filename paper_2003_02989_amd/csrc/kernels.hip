@@ -249,7 +249,27 @@ struct BuildCtx {
     const double *scale, *off;  // this row's scale and offset per slot
     const double *explicit_mats;
     const float *theta;         // this row's symbol values
+    uint64_t noise_seed;        // channels: the row's trajectory draws
+    int64_t b;                  // batch row
 };
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t seed, uint64_t counter);
+
+// The Pauli (0 = I, 1 = X, 2 = Y, 3 = Z) a Pauli channel applies in batch row
+// b, one trajectory of the noisy circuit (Sec. "Noise in qsim": one Kraus
+// operator drawn per channel): r = (u >> 11) 2^-53 with u the output number
+// (b 2^32 + k) of SplitMix64 from the noise seed, k the channel's ordinal in
+// the circuit; X if r < p_x, Y if r < p_x + p_y, Z if r < p_x + p_y + p_z
+// (fp64, in that order), else I.
+__device__ __forceinline__ int channel_pick(uint64_t seed, int64_t b, int k, const double *p)
+{
+    const uint64_t u = splitmix64(seed, ((uint64_t)b << 32) | (uint64_t)(uint32_t)k);
+    const double r = (double)(u >> 11) * 0x1.0p-53;
+    if (r < p[0]) return 1;
+    if (r < p[0] + p[1]) return 2;
+    if (r < p[0] + p[1] + p[2]) return 3;
+    return 0;
+}
 
 // symbol resolution eta = scale*theta + offset (or the constant) of a parameter slot
 __device__ __forceinline__ double slot_value(const BuildCtx &c, int slot)
@@ -275,13 +295,23 @@ template <int D> __device__ __forceinline__ void build_task_d(const BuildTask &b
     for (int mi = 0; mi < bt.mem_count; mi++) {
         const Member mem = c.members[bt.mem_begin + mi];
         const GateDev gd = c.gates[mem.gate];
-        double eta[2] = {0, 0};
+        double eta[3] = {0, 0, 0};
         resolve(c, gd, eta);
         const double *ex = gd.explicit_ >= 0 ? c.explicit_mats + 32 * gd.explicit_ : nullptr;
 #pragma unroll
         for (int i = 0; i < 16; i++) g[i] = C(0, 0);
-        const int gdim = bt.kind == BT_DERIV ? gate_deriv_dev(gd.op, eta, bt.which, mem.form, g)
-                                             : gate_matrix_dev(gd.op, eta, ex, mem.form, g);
+        int gdim;
+        if (gd.op == OP_PCHAN) {  // this row's Pauli (never a derivative: no symbols)
+            const int k = channel_pick(c.noise_seed, c.b, gd.chan, eta);
+            if (k == 0) { g[0] = g[3] = C(1, 0); }
+            else if (k == 1) { g[1] = g[2] = C(1, 0); }
+            else if (k == 2) { g[1] = C(0, -1); g[2] = C(0, 1); }
+            else { g[0] = C(1, 0); g[3] = C(-1, 0); }
+            gdim = 2;
+        } else {
+            gdim = bt.kind == BT_DERIV ? gate_deriv_dev(gd.op, eta, bt.which, mem.form, g)
+                                       : gate_matrix_dev(gd.op, eta, ex, mem.form, g);
+        }
         if (gdim != D) continue;  // the planner never mixes dimensions
         if (D == 4 && mem.swapped) swap_qubits4(g);
         if (bt.kind == BT_DAGGER) {
@@ -342,7 +372,7 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     BuildCtx c{a.members, a.gates, a.slot_sym,
                a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots),
                a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots), a.explicit_mats,
-               a.theta + (int64_t)b * a.S};
+               a.theta + (int64_t)b * a.S, a.noise_seed, b};
     if (ti < a.task_end) {
         const BuildTask bt = a.tasks[ti];
         build_task(bt, c, a.mats + (int64_t)row * a.mat_stride + bt.out);
@@ -935,6 +965,19 @@ __global__ void k_gather(GatherArgs a)
     a.out[(int64_t)b * a.M + m] = v;
 }
 
+// out[g, k] = the mean of in[g R + r, k] over r < R (trajectory rows of one
+// circuit), summed in fp64 in row order
+__global__ void k_row_mean(const float *in, int64_t groups, int32_t R, int32_t K, float *out)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= groups * K) return;
+    const int64_t g = i / K, k = i - g * K;
+    const float *p = in + g * R * K + k;
+    double s = 0.0;
+    for (int32_t r = 0; r < R; r++) s += (double)p[(int64_t)r * K];
+    out[i] = (float)(s / R);
+}
+
 __global__ void k_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int64_t from, int64_t to)
 {
     const int row = blockIdx.y;
@@ -1197,6 +1240,15 @@ hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s)
     if (a.M <= 0 || nrows <= 0) return hipSuccess;
     prof::Scope ps("gather", s);
     hipLaunchKernelGGL(k_gather, dim3((unsigned)((a.M + 255) / 256), nrows), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_row_mean(const float *in, int64_t groups, int32_t R, int32_t K, float *out, hipStream_t s)
+{
+    const int64_t n = groups * K;
+    if (n <= 0) return hipSuccess;
+    prof::Scope ps("row_mean", s);
+    hipLaunchKernelGGL(k_row_mean, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, in, groups, R, K, out);
     return hipGetLastError();
 }
 

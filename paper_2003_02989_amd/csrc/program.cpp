@@ -55,6 +55,8 @@ bool op_shape(int op, int &nq, int &np)
         nq = 2; np = 1; return true;
     case OP_FSIM:
         nq = 2; np = 2; return true;
+    case OP_PCHAN:
+        nq = 1; np = 3; return true;
     default:
         return false;
     }
@@ -1440,8 +1442,10 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             g.nq = r.get<uint8_t>();
             g.np = r.get<uint8_t>();
             g.q[0] = g.q[1] = 0;
-            g.sym[0] = g.sym[1] = 0;
-            g.scale[0] = g.scale[1] = g.offset[0] = g.offset[1] = 0.0;
+            for (int j = 0; j < 3; j++) {
+                g.sym[j] = 0;
+                g.scale[j] = g.offset[j] = 0.0;
+            }
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
             if (g.op == OP_PAULIEXP) {
                 lower_pauli_exp(r, g, (int)n, (int32_t)S, b, i, emit);
@@ -1471,6 +1475,18 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
                     fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
                                            ": symbol column out of range");
             }
+            if (g.op == OP_PCHAN && !r.bad) {  // constant probabilities >= 0, summing to <= 1
+                double tot = 0.0;
+                for (int j = 0; j < 3; j++) {
+                    if (g.sym[j] != -1 || !(g.offset[j] >= 0.0))
+                        fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                               ": channel probabilities must be constants >= 0");
+                    tot += g.offset[j];
+                }
+                if (!(tot <= 1.0))
+                    fail(TQ_E_INVALID, "circuit " + std::to_string(b) + " gate " + std::to_string(i) +
+                                           ": channel probabilities sum above 1");
+            }
             const int nm = g.op == OP_MATRIX1 ? 8 : g.op == OP_MATRIX2 ? 32 : 0;
             for (int j = 0; j < nm; j++) g.mat[j] = r.get<double>();
             if (nm)
@@ -1488,7 +1504,7 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             const HGate &g = gates[i];
             key.append((const char *)&g.op, 2);
             key.append((const char *)g.q, 8);
-            key.append((const char *)g.sym, 8);
+            key.append((const char *)g.sym, sizeof g.sym);
             if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2)
                 key.append((const char *)g.mat, sizeof(double) * (g.op == OP_MATRIX1 ? 8 : 32));
         }
@@ -1499,6 +1515,7 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             pd->groups.push_back(std::make_unique<Group>());
             grp = pd->groups.back().get();
             grp->n = c.n;
+            int nchan = 0;
             for (uint32_t i = 0; i < ng; i++) {
                 const HGate &g = gates[i];
                 GateDev gd{};
@@ -1507,6 +1524,7 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
                 gd.np = g.np;
                 gd.slot0 = grp->n_slots;
                 gd.explicit_ = -1;
+                gd.chan = g.op == OP_PCHAN ? nchan++ : -1;
                 if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2) {
                     gd.explicit_ = (int32_t)(grp->explicit_mats.size() / 32);
                     grp->explicit_mats.insert(grp->explicit_mats.end(), g.mat, g.mat + 32);

@@ -28,8 +28,8 @@ struct HGate {
     uint16_t op;
     uint8_t nq, np;
     uint32_t q[2];
-    int32_t sym[2];
-    double scale[2], offset[2];
+    int32_t sym[3];
+    double scale[3], offset[3];
     double mat[32];
 };
 

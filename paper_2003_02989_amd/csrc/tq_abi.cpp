@@ -141,6 +141,7 @@ struct tq_program_s {
     size_t psi_total = 0, mat_total = 0;
     uint64_t obs_id = 0;
     std::vector<std::unique_ptr<ObsGroupDev>> obs_dev;
+    uint64_t noise_seed = 0;  // seed of the channels' per-row draws
 
     ~tq_program_s()
     {
@@ -276,6 +277,7 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.phase_out = init ? g.init_mat[0] : -1;
     a.n_phase = (int32_t)g.phase_terms.size();
     a.phase_terms = (const PhaseTerm *)gd.phase_terms.p;
+    a.noise_seed = p->noise_seed;
     hip_check(launch_build(a, (int)g.rows.size(), s), "matrix build launch");
     if (begin <= g.fwd_tasks.begin && end >= g.fwd_tasks.end && gd.n_dense > 0) {
         // dense forward stages, from the op matrices just built
@@ -843,6 +845,26 @@ tq_status tq_program_info(tq_program prog, int32_t *B, int32_t *S, int32_t *max_
     });
 }
 
+tq_status tq_program_set_noise_seed(tq_program prog, uint64_t seed)
+{
+    return guarded([&] {
+        if (!prog) fail(TQ_E_INVALID, "program is NULL");
+        prog->noise_seed = seed;
+    });
+}
+
+tq_status tq_row_mean(const float *in, int64_t groups, int32_t R, int32_t K, float *out, void *stream)
+{
+    return guarded([&] {
+        if (groups < 0 || R < 1 || K < 0) fail(TQ_E_INVALID, "row_mean: groups >= 0, R >= 1 and K >= 0 required");
+        if (groups == 0 || K == 0) return;
+        if (!in || !out) fail(TQ_E_INVALID, "row_mean: in and out must not be NULL");
+        check_align(in, 4, "in");
+        check_align(out, 4, "out");
+        hip_check(launch_row_mean(in, groups, R, K, out, as_stream(stream)), "row mean launch");
+    });
+}
+
 tq_status tq_program_specialize(tq_program prog, const char *target)
 {
     return guarded([&] {
@@ -1264,7 +1286,7 @@ tq_status tq_gate_matrix(int32_t op, const double *params, const double *explici
         if (op < 1 || op >= OP_COUNT) fail(TQ_E_INVALID, "unknown opcode");
         const bool expl = op == OP_MATRIX1 || op == OP_MATRIX2;
         if (expl && !explicit_m) fail(TQ_E_INVALID, "explicit matrix is NULL");
-        double eta[2] = {params ? params[0] : 0.0, params ? params[1] : 0.0};
+        double eta[3] = {params ? params[0] : 0.0, params ? params[1] : 0.0, 0.0};
         const int form = cblock && (op == OP_CNOT || op == OP_CNOTPOW) ? FORM_CBLOCK : FORM_FULL;
         const int d = gate_table_host(op, eta, explicit_m, form, deriv ? 1 : 0, which, out);
         if (d == 0) fail(TQ_E_INVALID, deriv ? "the gate has no derivative" : "unknown opcode");

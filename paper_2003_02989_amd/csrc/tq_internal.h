@@ -20,6 +20,9 @@ enum Opcode : uint16_t {
     OP_H = 1, OP_X, OP_Y, OP_Z, OP_RX, OP_RY, OP_RZ, OP_XPOW, OP_YPOW, OP_ZPOW,
     OP_CZ, OP_CNOT, OP_CZPOW, OP_CNOTPOW, OP_XXPOW, OP_YYPOW, OP_ZZPOW, OP_RZZ,
     OP_SQRTX, OP_SQRTY, OP_SQRTW, OP_FSIM, OP_MATRIX1, OP_MATRIX2, OP_SWAP,
+    // Pauli channel on one qubit (X, Y, Z with the constant probabilities of
+    // its three parameters): each row, one trajectory, draws its Pauli
+    OP_PCHAN = 27,
     OP_COUNT
 };
 // exp(-i eta P) of a Pauli string: a blob opcode only, lowered to the gates
@@ -38,6 +41,7 @@ struct GateDev {
     uint8_t nq, np;
     int32_t slot0;     // first of its np parameter slots
     int32_t explicit_; // index of its explicit matrix (MATRIX1/2) or -1
+    int32_t chan;      // OP_PCHAN: its ordinal among the circuit's channels, else -1
 };
 
 // How a matrix is rendered by the builder.

@@ -49,6 +49,8 @@ def lib():
         L.tq_program_destroy.restype = None
         L.tq_program_info.argtypes = [vp, p32, p32, p32, p32]
         L.tq_program_specialize.argtypes = [vp, ctypes.c_char_p]
+        L.tq_program_set_noise_seed.argtypes = [vp, u64]
+        L.tq_row_mean.argtypes = [vp, i64, i32, i32, vp, vp]
         L.tq_observables_create.argtypes = [ctypes.c_char_p, sz, ctypes.POINTER(vp)]
         L.tq_observables_destroy.argtypes = [vp]
         L.tq_observables_destroy.restype = None
@@ -214,6 +216,26 @@ def simulate_state(prog, symbol_values, out=None, stream=None):
         out = torch.empty((prog.B, 1 << prog.max_qubits), dtype=torch.complex64, device="cuda")
     p = _dev(out, torch.complex64, (prog.B, 1 << prog.max_qubits), "states")
     _check(lib().tq_simulate_state(prog._h, _theta(prog, symbol_values), p, _stream(stream)))
+    return out
+
+
+def set_noise_seed(prog, seed):
+    """Seed of the channels' per-row Kraus draws in the program's later calls."""
+    _check(lib().tq_program_set_noise_seed(prog._h, int(seed) & 0xFFFFFFFFFFFFFFFF))
+
+
+def row_mean(x, R, out=None, stream=None):
+    """[G R, K] float32 -> [G, K]: the mean over each R consecutive rows (the
+    trajectories of one noisy circuit)."""
+    G = x.shape[0] // R
+    if x.shape[0] != G * R:
+        raise ValueError("rows must be a multiple of R")
+    K = x.shape[1]
+    if out is None:
+        out = torch.empty((G, K), dtype=torch.float32, device="cuda")
+    i = _dev(x, torch.float32, (G * R, K), "in")
+    o = _dev(out, torch.float32, (G, K), "out")
+    _check(lib().tq_row_mean(i, G, R, K, o, _stream(stream)))
     return out
 
 

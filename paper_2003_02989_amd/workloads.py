@@ -318,6 +318,27 @@ def random_batch(seed, B, n, n_gates, n_symbols, K=2, hetero=False, **kw):
     return Workload(f"random_n{n}", circuits, n_symbols, theta, obs, upstream)
 
 
+def with_noise(w, p, R):
+    """The noisy version of workload w as trajectories: after every gate a
+    depolarizing channel of probability p on each qubit the gate acts on (the
+    paper's circuit-wide depolarizing model: the channel after each
+    operation, Sec. "Training Models with Noise"), and every row repeated R
+    times (rows b R .. b R + R - 1 are the trajectories of circuit b; their
+    outputs average with tq_row_mean)."""
+    circuits = []
+    for c in w.circuits:
+        nc = Circuit(c.n)
+        for g in c.gates:
+            nc.gates.append(g)
+            for q in g[1]:
+                nc.depolarize(q, p)
+        circuits += [nc] * R
+    rep = lambda a: np.repeat(a, R, axis=0)
+    return Workload(w.name + f"_noisy{R}", circuits, w.n_symbols, rep(w.theta),
+                    [o for o in w.observables for _ in range(R)], rep(w.upstream),
+                    dict(w.extras, noise_p=p, trajectories=R))
+
+
 CONFIGS = {"c1": c1_hea, "c2": c2_qnn, "c3": c3_qaoa, "c4": c4_random, "c5": c5_vqe}
 
 

@@ -154,3 +154,23 @@ def test_pauli_exponential_is_lowered_and_validated():
     assert status_of(lambda: create(blob([0, 1], [1, 3], np_=2))) == tq.TQ_E_INVALID  # parameters
     assert status_of(lambda: create(blob([0, 1], [1, 3])[:-1])) == tq.TQ_E_INVALID  # truncated
     assert status_of(lambda: create(blob([0, 1, 2, 3, 0], [1, 1, 1, 1, 1]))) == tq.TQ_E_INVALID  # longer than n
+
+
+def test_channels_validated_and_seed_entry_points():
+    from paper_2003_02989_amd.circuits import const
+    create(program_blob([Circuit(2).add("PCHAN", 1, [0.1, 0.2, 0.3])], 0))
+    for params in ([0.5, 0.6, 0.0], [-0.1, 0.0, 0.0]):
+        assert status_of(lambda: create(program_blob([Circuit(2).add("PCHAN", 0, params)], 0))) == tq.TQ_E_INVALID
+    assert status_of(lambda: create(program_blob([Circuit(2).add("PCHAN", 0, [sym(0), 0.0, 0.0])], 1))) \
+        == tq.TQ_E_INVALID
+    L = tq.lib()
+    assert L.tq_program_set_noise_seed(None, 1) == tq.TQ_E_INVALID
+    p = create(program_blob([Circuit(2).add("PCHAN", 1, [0.1, 0.2, 0.3])], 0))
+    assert L.tq_program_set_noise_seed(p._h, 77) == tq.TQ_OK
+    fake = ctypes.c_void_p(16)
+    assert L.tq_row_mean(fake, 2, 0, 1, fake, None) == tq.TQ_E_INVALID  # R < 1
+    assert L.tq_row_mean(None, 2, 3, 1, fake, None) == tq.TQ_E_INVALID  # in NULL
+    assert L.tq_row_mean(None, 0, 3, 1, None, None) == tq.TQ_OK  # no work
+    # a noisy structure's generated kernels compile for gfx950
+    w = wl.with_noise(wl.random_batch(1413, B=2, n=14, n_gates=30, n_symbols=3, K=1), 0.05, 2)
+    tq.specialize(create(w.program_blob(), specialize=True), "gfx950")

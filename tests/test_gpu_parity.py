@@ -312,3 +312,37 @@ def test_pauli_exponentials_random(n, seed, specialize):
             c.gates.insert(int(rng.integers(0, len(c.gates) + 1)), e)
     say("Pauli exponentials", n, seed, "specialize", specialize)
     compare(gpu_outputs(w, specialize=specialize), oracle_outputs(w))
+
+
+@pytest.mark.parametrize("specialize", [False, True])
+@pytest.mark.parametrize("n,seed", [(8, 0), (13, 1)])
+def test_noisy_trajectories(n, seed, specialize):
+    # Pauli channels (depolarizing after every gate, plus asymmetric ones):
+    # every row a trajectory whose Paulis are drawn from the noise seed; the
+    # draws are bit-exact between the two sides, so states, expectations and
+    # adjoint gradients match the oracle row by row; tq_row_mean averages the
+    # trajectories of each circuit
+    from paper_2003_02989_amd.circuits import Circuit
+    base = wl.random_batch(8300 + seed, B=2, n=n, n_gates=25, n_symbols=3, K=2)
+    for c in base.circuits:
+        c.add("PCHAN", 0, [0.2, 0.05, 0.3])
+        c.add("PCHAN", n - 1, [0.0, 0.0, 0.5])
+    R = 6
+    w = wl.with_noise(base, 0.08, R)
+    for noise_seed in (11, 12):
+        say("noisy trajectories n", n, "seed", noise_seed, "specialize", specialize)
+        orc.set_noise_seed(noise_seed)
+        orc.set_row_offset(0)
+        p = tq.Program(w.program_blob(), specialize=specialize)
+        tq.set_noise_seed(p, noise_seed)
+        o = tq.Observables(w.observable_blob())
+        th = dev(w.theta)
+        st = tq.simulate_state(p, th).cpu().numpy()
+        e = tq.expectation(p, th, o)
+        ge = torch.empty((w.B, w.K), dtype=torch.float32, device="cuda")
+        g = tq.adjoint_grad(p, th, o, dev(w.upstream), expectations=ge).cpu().numpy()
+        compare({"state": st, "exp": e.cpu().numpy(), "grad": g, "grad_exp": ge.cpu().numpy()}, oracle_outputs(w))
+        m = tq.row_mean(e, R).cpu().numpy()
+        assert np.abs(m - e.cpu().numpy().reshape(base.B, R, w.K).astype(np.float64).mean(1)).max() < 1e-6
+    # the trajectories differ from row to row (the noise is applied)
+    assert np.abs(st[0] - st[1]).max() > 1e-3 or np.abs(st[1] - st[2]).max() > 1e-3
