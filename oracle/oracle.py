@@ -60,6 +60,8 @@ def lib():
         L.orc_op_arity.argtypes = [i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.orc_set_noise_seed.argtypes = [u64]
         L.orc_set_row_offset.argtypes = [i64]
+        L.orc_sampled_expectation.argtypes = [vp, vp, vp, i32, u64, vp]
+        L.orc_sampled_from_terms.argtypes = [vp, vp, i32, i32, u64, vp]
         L.orc_channel_pick.argtypes = [u64, i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double]
         L.orc_channel_pick.restype = i32
         _lib = L
@@ -210,3 +212,21 @@ def channel_pick(seed, row, chan, px, py, pz):
 def set_row_offset(offset):
     """Rows of a program draw their channels as rows offset + b of a larger batch."""
     lib().orc_set_row_offset(int(offset))
+
+
+def sampled_expectation(prog: Program, theta, obs: Observables, reps, seed):
+    """[B, K] expectations estimated from `reps` shots per non-identity term."""
+    out = np.zeros((prog.B, obs.K), dtype=np.float64)
+    _check(lib().orc_sampled_expectation(prog._h, _ptr(prog._theta(theta)), obs._h, int(reps),
+                                         int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(out)))
+    return out
+
+
+def sampled_from_terms(obs: Observables, term_exp, reps, seed):
+    """The same estimate from given float32 term expectations [B, Kt] (the
+    j-th non-identity term of each row over (k, t) in order)."""
+    te = np.ascontiguousarray(np.asarray(term_exp, dtype=np.float32))
+    out = np.zeros((obs.B, obs.K), dtype=np.float64)
+    _check(lib().orc_sampled_from_terms(obs._h, _ptr(te), te.shape[1], int(reps), int(seed) & 0xFFFFFFFFFFFFFFFF,
+                                        _ptr(out)))
+    return out

@@ -25,6 +25,8 @@
  *    their occurrences by the chain rule, eq. chain_rule);
  *  - noisy circuits by trajectories (Sec. "Noise in qsim"): each row draws
  *    one Pauli per channel from a counter stream and is then a pure circuit;
+ *  - expectations estimated from a finite number of measurement shots per
+ *    term (SampledExpectation);
  *  - bitstring samples drawn from |psi_i|^2 (Sec. "Sampling and Expectation
  *    Values") with the integer fixed-point rule and the SplitMix64 counter
  *    stream fixed in the design doc (the paper leaves both open).
@@ -678,6 +680,96 @@ int orc_expectation(void *hp, const double *theta, void *ho, double *out, double
             if (imag) imag[(int64_t)b * o->K + k] = cimag(e);
         }
         free(psi); free(tmp); free(hp_);
+    }
+    return 0;
+}
+
+/* ------------------------------------------------- sampled expectations */
+/* Expectation estimated from samples (Sec. "Sampling and Expectation
+ * Values": sample bitstrings in the measurement basis, apply the measurement
+ * to each, average).  For h = sum_t c_t P_t each non-identity term is
+ * measured `reps` times on its own: a shot of P_t yields +1 with probability
+ * (1 + <P_t>)/2, else -1 (the parity of the term's qubits after rotating them
+ * to the Z basis), and the estimate is sum_t c_t (2 n_t / reps - 1) plus the
+ * identity terms' coefficients, n_t the number of +1 shots.  Shot s of term
+ * t of observable k in batch row b is +1 when (u >> 11) 2^-53 < q with
+ * q = (1 + e_t)/2 in fp64 (e_t clamped to [-1, 1]) and u the output number
+ * ((b K + k) 2^40 + t 2^24 + s) of SplitMix64 started at `seed`. */
+static uint64_t sampled_count(uint64_t seed, int64_t bk, int t, int reps, double e)
+{
+    if (e > 1.0) e = 1.0;
+    if (e < -1.0) e = -1.0;
+    const double q = 0.5 * (1.0 + e);
+    uint64_t n = 0;
+    for (int s = 0; s < reps; s++) {
+        const uint64_t u = orc_splitmix64(seed, ((uint64_t)bk << 40) | ((uint64_t)t << 24) | (uint64_t)s);
+        n += ((double)(u >> 11) * 0x1.0p-53 < q);
+    }
+    return n;
+}
+
+static int check_sampled(const OObs *o, int reps)
+{
+    if (reps < 1 || reps >= (1 << 24)) return fail("repetitions must be in [1, 2^24)");
+    if ((int64_t)o->B * o->K >= ((int64_t)1 << 24)) return fail("too many (row, observable) pairs for the shot counter");
+    for (int i = 0; i < o->B * o->K; i++)
+        if (o->start[i + 1] - o->start[i] >= (1 << 16)) return fail("too many terms in one observable");
+    return 0;
+}
+
+/* full pipeline: exact term expectations from the complex128 state */
+int orc_sampled_expectation(void *hp, const double *theta, void *ho, int reps, uint64_t seed, double *out)
+{
+    OProgram *pr = (OProgram *)hp;
+    OObs *o = (OObs *)ho;
+    if (check_obs(pr, o) || check_sampled(o, reps)) return 1;
+    int par = pr->B == 1;
+#pragma omp parallel for if (!par) schedule(dynamic)
+    for (int b = 0; b < pr->B; b++) {
+        const OCircuit *c = &pr->c[b];
+        const int64_t N = (int64_t)1 << c->n;
+        cplx *psi = malloc(sizeof(cplx) * N), *tmp = malloc(sizeof(cplx) * N), *hp_ = malloc(sizeof(cplx) * N);
+        simulate_row(c, theta + (int64_t)b * pr->S, b, psi, par);
+        for (int k = 0; k < o->K; k++) {
+            double est = 0.0;
+            const int t0 = o->start[b * o->K + k], t1 = o->start[b * o->K + k + 1];
+            for (int t = t0; t < t1; t++) {
+                const OTerm *tm = &o->t[t];
+                if (tm->nf == 0) { est += tm->coeff; continue; }
+                for (int64_t i = 0; i < N; i++) hp_[i] = 0;
+                add_pauli_term(tm, c->n, psi, tmp, hp_, 1.0, par);
+                const double e = creal(inner(psi, hp_, N));
+                const uint64_t n = sampled_count(seed, (int64_t)b * o->K + k, t - t0, reps, e);
+                est += tm->coeff * (2.0 * (double)n / reps - 1.0);
+            }
+            out[(int64_t)b * o->K + k] = est;
+        }
+        free(psi); free(tmp); free(hp_);
+    }
+    return 0;
+}
+
+/* the same estimate from given term expectations: term_exp[b, j] for the
+ * j-th non-identity term of row b over (k, t) in order, Kt per row */
+int orc_sampled_from_terms(void *ho, const float *term_exp, int Kt, int reps, uint64_t seed, double *out)
+{
+    OObs *o = (OObs *)ho;
+    if (check_sampled(o, reps)) return 1;
+    for (int b = 0; b < o->B; b++) {
+        int j = 0;
+        for (int k = 0; k < o->K; k++) {
+            double est = 0.0;
+            const int t0 = o->start[b * o->K + k], t1 = o->start[b * o->K + k + 1];
+            for (int t = t0; t < t1; t++) {
+                const OTerm *tm = &o->t[t];
+                if (tm->nf == 0) { est += tm->coeff; continue; }
+                if (j >= Kt) return fail("term_exp has fewer terms than the observables");
+                const uint64_t n = sampled_count(seed, (int64_t)b * o->K + k, t - t0, reps,
+                                                 (double)term_exp[(int64_t)b * Kt + j++]);
+                est += tm->coeff * (2.0 * (double)n / reps - 1.0);
+            }
+            out[(int64_t)b * o->K + k] = est;
+        }
     }
     return 0;
 }
