@@ -64,6 +64,8 @@ def lib():
         L.orc_sampled_from_terms.argtypes = [vp, vp, i32, i32, u64, vp]
         L.orc_channel_pick.argtypes = [u64, i64, i32, ctypes.c_double, ctypes.c_double, ctypes.c_double]
         L.orc_channel_pick.restype = i32
+        L.orc_param_shift_grad.argtypes = [vp, vp, vp, vp, i32, u64, vp]
+        L.orc_finite_diff_grad.argtypes = [vp, vp, vp, vp, ctypes.c_double, vp]
         _lib = L
     return _lib
 
@@ -230,3 +232,22 @@ def sampled_from_terms(obs: Observables, term_exp, reps, seed):
     _check(lib().orc_sampled_from_terms(obs._h, _ptr(te), te.shape[1], int(reps), int(seed) & 0xFFFFFFFFFFFFFFFF,
                                         _ptr(out)))
     return out
+
+
+def param_shift_grad(prog: Program, theta, obs: Observables, upstream, reps=0, seed=0):
+    """[B, S] gradients of sum_k g_k <h_k> by the parameter-shift rule, every
+    symbolic parameter shifted alone; reps > 0 estimates each shifted
+    circuit's expectations from that many shots per term."""
+    up = np.ascontiguousarray(np.asarray(upstream, dtype=np.float64))
+    g = np.zeros((prog.B, prog.S), dtype=np.float64)
+    _check(lib().orc_param_shift_grad(prog._h, _ptr(prog._theta(theta)), obs._h, _ptr(up), int(reps),
+                                      int(seed) & 0xFFFFFFFFFFFFFFFF, _ptr(g)))
+    return g
+
+
+def finite_diff_grad(prog: Program, theta, obs: Observables, upstream, eps):
+    """[B, S] gradients by central differences of step eps in each symbol."""
+    up = np.ascontiguousarray(np.asarray(upstream, dtype=np.float64))
+    g = np.zeros((prog.B, prog.S), dtype=np.float64)
+    _check(lib().orc_finite_diff_grad(prog._h, _ptr(prog._theta(theta)), obs._h, _ptr(up), float(eps), _ptr(g)))
+    return g

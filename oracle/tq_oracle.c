@@ -27,6 +27,9 @@
  *    one Pauli per channel from a counter stream and is then a pure circuit;
  *  - expectations estimated from a finite number of measurement shots per
  *    term (SampledExpectation);
+ *  - gradients by the parameter-shift rule (exact or from sampled
+ *    expectations) and by central finite differences (Sec. "Parameter shift
+ *    methods", Sec. "Finite difference methods");
  *  - bitstring samples drawn from |psi_i|^2 (Sec. "Sampling and Expectation
  *    Values") with the integer fixed-point rule and the SplitMix64 counter
  *    stream fixed in the design doc (the paper leaves both open).
@@ -587,7 +590,11 @@ static void channel_matrix(const OGate *g, int64_t row, cplx *m)
     else pauli2(k, m);
 }
 
-static void simulate_row(const OCircuit *c, const double *theta_row, int64_t row, cplx *psi, int par)
+/* psi = W_G ... W_1 |0..0> for one row; parameter `shift_param` of gate
+ * `shift_gate` (none when negative) is taken at its resolved value plus
+ * `delta` (the shifted circuits of the parameter-shift rule) */
+static void simulate_row_shifted(const OCircuit *c, const double *theta_row, int64_t row, int shift_gate,
+                                 int shift_param, double delta, cplx *psi, int par)
 {
     const int64_t N = (int64_t)1 << c->n;
     for (int64_t i = 0; i < N; i++) psi[i] = 0;
@@ -598,6 +605,7 @@ static void simulate_row(const OCircuit *c, const double *theta_row, int64_t row
         cplx m[16];
         int d;
         resolve(g, theta_row, eta);
+        if (i == shift_gate) eta[shift_param] += delta;
         if (g->op == OP_PAULIEXP) {
             apply_pauli_exp(psi, c->n, g, cos(eta[0]), -I * sin(eta[0]), par);
             continue;
@@ -610,6 +618,11 @@ static void simulate_row(const OCircuit *c, const double *theta_row, int64_t row
         gate_matrix(g->op, eta, g->mat, m, &d);
         apply_matrix(psi, c->n, g->nq, g->q, m, par);
     }
+}
+
+static void simulate_row(const OCircuit *c, const double *theta_row, int64_t row, cplx *psi, int par)
+{
+    simulate_row_shifted(c, theta_row, row, -1, 0, 0.0, psi, par);
 }
 
 /* out += coeff * P psi for one Pauli string term */
@@ -770,6 +783,177 @@ int orc_sampled_from_terms(void *ho, const float *term_exp, int Kt, int reps, ui
             }
             out[(int64_t)b * o->K + k] = est;
         }
+    }
+    return 0;
+}
+
+/* ------------------------------------------ shift and difference rules */
+/* The two-term parameter-shift rule of parameter j of a gate (Sec.
+ * "Parameter shift methods", eq. parshift_grad): when the parameter enters
+ * as exp(-i eta G) with G of two distinct eigenvalues e0 < e1, every
+ * expectation is a + b cos(r eta) + c sin(r eta) with r = e1 - e0, so
+ * f'(eta) = (r / 2) (f(eta + pi / (2 r)) - f(eta - pi / (2 r))).
+ *   RX, RY, RZ, RZZ = exp(-i eta G / 2), G involutory: r = 1.
+ *   pow gates G^t = e^{i pi t / 2} exp(-i (pi t / 2) G): r = pi (in t).
+ *   exp(-i eta P) of a Pauli string: r = 2, the printed rule with pi / 4.
+ *   fSim's phi, exp(-i phi |11><11|): r = 1.
+ * fSim's theta, exp(-i theta (XX + YY) / 2), has three eigenvalues and no
+ * two-term rule; it returns 1. */
+static int shift_rule(int op, int j, double *delta, double *factor)
+{
+    switch (op) {
+    case OP_RX: case OP_RY: case OP_RZ: case OP_RZZ:
+        *delta = M_PI / 2.0; *factor = 0.5; return 0;
+    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW:
+    case OP_XXPOW: case OP_YYPOW: case OP_ZZPOW:
+        *delta = 0.5; *factor = M_PI / 2.0; return 0;
+    case OP_PAULIEXP:
+        *delta = M_PI / 4.0; *factor = 1.0; return 0;
+    case OP_FSIM:
+        if (j == 1) { *delta = M_PI / 2.0; *factor = 0.5; return 0; }
+        return 1;
+    default:
+        return 1;
+    }
+}
+
+/* number of symbolic parameters (shift-rule occurrences) of a circuit */
+static int count_occurrences(const OCircuit *c)
+{
+    int n = 0;
+    for (int i = 0; i < c->ngates; i++)
+        for (int j = 0; j < c->g[i].np; j++) n += c->g[i].sym[j] >= 0;
+    return n;
+}
+
+/* The K values of row b's observables on state psi: exact (reps = 0), or
+ * estimated from reps shots per non-identity term with the shot counter of
+ * (row e, observable k) as in the sampled expectation above. */
+static void observable_values(const OObs *o, int b, int n, const cplx *psi, cplx *tmp, cplx *hp_, int reps,
+                              uint64_t seed, int64_t e, double *out, int par)
+{
+    const int64_t N = (int64_t)1 << n;
+    for (int k = 0; k < o->K; k++) {
+        double v = 0.0;
+        const int t0 = o->start[b * o->K + k], t1 = o->start[b * o->K + k + 1];
+        for (int t = t0; t < t1; t++) {
+            const OTerm *tm = &o->t[t];
+            if (tm->nf == 0) { v += tm->coeff; continue; }
+            for (int64_t i = 0; i < N; i++) hp_[i] = 0;
+            add_pauli_term(tm, n, psi, tmp, hp_, 1.0, par);
+            const double pe = creal(inner(psi, hp_, N));
+            if (reps == 0) v += tm->coeff * pe;
+            else v += tm->coeff * (2.0 * (double)sampled_count(seed, e * o->K + k, t - t0, reps, pe) / reps - 1.0);
+        }
+        out[k] = v;
+    }
+}
+
+/* Gradients of sum_k g_{b,k} <h_{b,k}> by the parameter-shift rule: every
+ * symbolic parameter (occurrence) of a circuit is shifted by +-delta alone,
+ * the circuit re-simulated, and grad[b, sym] += scale * factor *
+ * sum_k g_k (f_k(+) - f_k(-)) (shared symbols add over their occurrences,
+ * eq. chain_rule).  With reps > 0 each shifted circuit's expectations are
+ * sampled estimates: the shifted circuits form a batch of sum_b 2 O_b rows
+ * (O_b the occurrences of row b) in the order (row, occurrence in gate and
+ * parameter order, + before -), and shifted circuit e draws its shots with
+ * the counter of row e. */
+int orc_param_shift_grad(void *hp, const double *theta, void *ho, const double *upstream, int reps, uint64_t seed,
+                         double *grad)
+{
+    OProgram *pr = (OProgram *)hp;
+    OObs *o = (OObs *)ho;
+    if (check_obs(pr, o)) return 1;
+    if (reps < 0) return fail("repetitions must be >= 0");
+    int64_t *ebase = malloc(sizeof(int64_t) * (pr->B + 1));
+    ebase[0] = 0;
+    for (int b = 0; b < pr->B; b++) {
+        const OCircuit *c = &pr->c[b];
+        for (int i = 0; i < c->ngates; i++)
+            for (int j = 0; j < c->g[i].np; j++) {
+                double dl, fc;
+                if (c->g[i].sym[j] >= 0 && shift_rule(c->g[i].op, j, &dl, &fc)) {
+                    free(ebase);
+                    return fail("a symbolic parameter has no two-term shift rule (fSim theta)");
+                }
+            }
+        ebase[b + 1] = ebase[b] + 2 * (int64_t)count_occurrences(c);
+    }
+    if (reps > 0) {
+        if (reps >= (1 << 24)) { free(ebase); return fail("repetitions must be in [1, 2^24)"); }
+        if (ebase[pr->B] * o->K >= ((int64_t)1 << 24)) {
+            free(ebase);
+            return fail("too many (shifted circuit, observable) pairs for the shot counter");
+        }
+        if (check_sampled(o, reps)) { free(ebase); return 1; }
+    }
+    int par = pr->B == 1;
+#pragma omp parallel for if (!par) schedule(dynamic)
+    for (int b = 0; b < pr->B; b++) {
+        const OCircuit *c = &pr->c[b];
+        const double *th = theta + (int64_t)b * pr->S;
+        double *gr = grad + (int64_t)b * pr->S;
+        const int64_t N = (int64_t)1 << c->n;
+        cplx *psi = malloc(sizeof(cplx) * N), *tmp = malloc(sizeof(cplx) * N), *hp_ = malloc(sizeof(cplx) * N);
+        double *fp = malloc(sizeof(double) * (o->K + 1)), *fm = malloc(sizeof(double) * (o->K + 1));
+        for (int s = 0; s < pr->S; s++) gr[s] = 0;
+        int64_t occ = 0;
+        for (int i = 0; i < c->ngates; i++) {
+            const OGate *g = &c->g[i];
+            for (int j = 0; j < g->np; j++) {
+                if (g->sym[j] < 0) continue;
+                double dl, fc;
+                shift_rule(g->op, j, &dl, &fc);
+                const int64_t e = ebase[b] + 2 * occ++;
+                simulate_row_shifted(c, th, b, i, j, dl, psi, par);
+                observable_values(o, b, c->n, psi, tmp, hp_, reps, seed, e, fp, par);
+                simulate_row_shifted(c, th, b, i, j, -dl, psi, par);
+                observable_values(o, b, c->n, psi, tmp, hp_, reps, seed, e + 1, fm, par);
+                double d = 0.0;
+                for (int k = 0; k < o->K; k++) d += upstream[(int64_t)b * o->K + k] * (fp[k] - fm[k]);
+                gr[g->sym[j]] += g->scale[j] * fc * d;
+            }
+        }
+        free(psi); free(tmp); free(hp_); free(fp); free(fm);
+    }
+    free(ebase);
+    return 0;
+}
+
+/* Gradients by central finite differences in the symbol values (Sec.
+ * "Finite difference methods", eq. central_diff):
+ * grad[b, s] = sum_k g_{b,k} (f_k(theta + eps e_s) - f_k(theta - eps e_s)) / (2 eps),
+ * the shifted symbol value formed in fp64.  Every symbol is shifted; one no
+ * gate of the row uses gets exactly 0. */
+int orc_finite_diff_grad(void *hp, const double *theta, void *ho, const double *upstream, double eps, double *grad)
+{
+    OProgram *pr = (OProgram *)hp;
+    OObs *o = (OObs *)ho;
+    if (check_obs(pr, o)) return 1;
+    if (!(eps > 0.0)) return fail("eps must be > 0");
+    int par = pr->B == 1;
+#pragma omp parallel for if (!par) schedule(dynamic)
+    for (int b = 0; b < pr->B; b++) {
+        const OCircuit *c = &pr->c[b];
+        const int64_t N = (int64_t)1 << c->n;
+        cplx *psi = malloc(sizeof(cplx) * N), *tmp = malloc(sizeof(cplx) * N), *hp_ = malloc(sizeof(cplx) * N);
+        double *fp = malloc(sizeof(double) * (o->K + 1)), *fm = malloc(sizeof(double) * (o->K + 1));
+        double *th = malloc(sizeof(double) * (pr->S + 1));
+        for (int s = 0; s < pr->S; s++) th[s] = theta[(int64_t)b * pr->S + s];
+        for (int s = 0; s < pr->S; s++) {
+            const double t0 = th[s];
+            th[s] = t0 + eps;
+            simulate_row(c, th, b, psi, par);
+            observable_values(o, b, c->n, psi, tmp, hp_, 0, 0, 0, fp, par);
+            th[s] = t0 - eps;
+            simulate_row(c, th, b, psi, par);
+            observable_values(o, b, c->n, psi, tmp, hp_, 0, 0, 0, fm, par);
+            th[s] = t0;
+            double d = 0.0;
+            for (int k = 0; k < o->K; k++) d += upstream[(int64_t)b * o->K + k] * (fp[k] - fm[k]);
+            grad[(int64_t)b * pr->S + s] = d / (2.0 * eps);
+        }
+        free(psi); free(tmp); free(hp_); free(fp); free(fm); free(th);
     }
     return 0;
 }
