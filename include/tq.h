@@ -217,6 +217,60 @@ tq_status tq_sample_with_amplitudes(tq_program prog, const float *symbol_values,
 tq_status tq_adjoint_grad(tq_program prog, const float *symbol_values, tq_observables obs,
                           const float *upstream, float *grad, float *expectations, void *stream);
 
+/* Number of non-identity terms of the row with the most (the term values
+ * of tq_sampled_expectation have this many columns). */
+tq_status tq_observables_terms(tq_observables obs, int32_t *Kt);
+
+/* Expectations estimated from measurement shots (SampledExpectation; Sec.
+ * "Sampling and Expectation Values": a Pauli term is measured by sampling
+ * its qubits in its eigenbasis, each shot giving the parity +1 or -1).  Each
+ * non-identity term t of h_{b,k} = sum_t c_t P_t is measured `reps` times on
+ * its own: shot s is +1 when (u >> 11) 2^-53 < (1 + e_t) / 2, fp64, with e_t
+ * the term's exact expectation as float32 clamped to [-1, 1] and u the
+ * SplitMix64 output number ((b K + k) 2^40 + t 2^24 + s) of the stream
+ * started at `seed` (t: the term's index in the observable, identity terms
+ * counted); then out[b, k] = sum_t c_t (2 n_t / reps - 1) + the identity
+ * terms' coefficients, in term order in fp64 (n_t: +1 shots), as float32.
+ * The shots are drawn from exact term expectations, which gives each term's
+ * shot count the distribution that sampling bitstrings would give.
+ * reps in [1, 2^24); B K < 2^24; at most 65535 terms per observable
+ * (TQ_E_UNSUPPORTED beyond).  out: float32 [B, K].  term_out: float32
+ * [B, Kt] (tq_observables_terms) or NULL; when given it receives the term
+ * expectations the shots were drawn from: row b's j-th non-identity term over
+ * (k, t) in order, zero beyond the row's own. */
+tq_status tq_sampled_expectation(tq_program prog, const float *symbol_values, tq_observables obs, int32_t reps,
+                                 uint64_t seed, float *out, float *term_out, void *stream);
+
+/* Gradient of sum_k upstream[b,k] <h_{b,k}> by the parameter-shift rule
+ * (Sec. "Parameter shift methods", eq. parshift_grad), as batched launches:
+ * every symbolic parameter of a blob gate whose generator has two
+ * eigenvalues a gap r apart is moved alone by +-pi/(2r) (rotations RX, RY,
+ * RZ, RZZ: +-pi/2; power gates: +-1/2 in the exponent; Pauli-string
+ * exponentials: +-pi/4; fSim's phi: +-pi/2) and
+ * grad[b, s] += scale x (r/2) x sum_k g_k (<h_k>(+) - <h_k>(-)) (shared
+ * symbols add up, eq. chain_rule).  The shifted circuits run as derived rows
+ * through the same kernels as plain rows, in chunks within fixed
+ * workspaces.  reps = 0: exact expectations; reps > 0: each shifted
+ * circuit's expectations are the estimates of tq_sampled_expectation, the
+ * shifted circuits of all rows forming one batch of sum_b 2 O_b rows (O_b:
+ * row b's symbolic parameters) in the order (row, parameter in gate and
+ * parameter order, + then -), shifted circuit e taking the shot counters of
+ * row e.  Noisy rows keep their trajectory.  upstream float32 [B, K], grad
+ * float32 [B, S] (overwritten).  TQ_E_UNSUPPORTED for a symbolic fSim theta
+ * (three generator eigenvalues: no two-term rule) or, with reps > 0, more
+ * than 2^24 (shifted circuit, observable) pairs. */
+tq_status tq_param_shift_grad(tq_program prog, const float *symbol_values, tq_observables obs, const float *upstream,
+                              int32_t reps, uint64_t seed, float *grad, void *stream);
+
+/* Gradient by central differences in the symbol values (Sec. "Finite
+ * difference methods", eq. central_diff): grad[b, s] = sum_k g_k
+ * (<h_k>(theta + eps e_s) - <h_k>(theta - eps e_s)) / (2 eps), the moved
+ * symbol value formed in fp64 (theta_s + eps); symbols no gate of the row
+ * uses get 0.  Batched like tq_param_shift_grad (two derived rows per symbol
+ * a row uses).  eps > 0. */
+tq_status tq_finite_diff_grad(tq_program prog, const float *symbol_values, tq_observables obs, const float *upstream,
+                              double eps, float *grad, void *stream);
+
 /* Amplitudes <x_{b,m}|psi_b> at M bitstrings per circuit: bitstrings uint64
  * [B, M] (each < 2^{n_b}, checked on the device: an out-of-range entry yields
  * a zero amplitude), amps complex64 [B, M]. */

@@ -11,6 +11,18 @@ namespace tq {
 
 constexpr int kMaxLevels = 8;    // sampler levels (64-ary), enough for 2^48 amplitudes
 
+// The parameter moves of one derived row of the batched shift rules: the
+// parameter-shift rule moves eta of one or two slots (a Pauli-string
+// exponential's lowered gates move together), central differences move one
+// symbol value.
+struct ShiftDev {
+    int32_t slot[2];   // slots whose eta moves by delta (-1: none)
+    int32_t sym;       // symbol whose value moves by dtheta x eps (-1: none)
+    int32_t pad;
+    double delta[2];
+    double dtheta;
+};
+
 struct BuildArgs {
     const BuildTask *tasks;
     int task_begin, task_end;
@@ -33,6 +45,14 @@ struct BuildArgs {
     const PhaseTerm *phase_terms;
     // seed of the channels' per-row Kraus draws
     uint64_t noise_seed;
+    // derived rows of the batched shift rules (x_period = 0: the rows
+    // themselves): launch row r is row L = x_begin + r of the group's
+    // expansion, a copy of group row L / x_period with the parameter moves of
+    // x_shift[L % x_period]
+    int64_t x_begin;
+    int32_t x_period;
+    const ShiftDev *x_shift;
+    double x_eps;            // symbol moves are dtheta x x_eps
 };
 
 struct StageBuildArgs {
@@ -204,6 +224,69 @@ struct SampArgs {
     uint64_t seed;
     uint64_t *out;
     int vec16;          // rows start 16-byte aligned (16-byte loads in level 1)
+};
+
+// Per-row table offsets of derived rows: out[j][r] = in[j][(x_begin + r) / x_period].
+constexpr int kRowGatherArrays = 6;
+struct RowGatherArgs {
+    const int32_t *in[kRowGatherArrays];
+    int32_t *out[kRowGatherArrays];
+    int narrays;
+    int64_t x_begin;
+    int32_t x_period;
+    int32_t count;
+};
+
+// Expectations estimated from measurement shots (SampledExpectation): each
+// non-identity term of an observable measured `reps` times from its exact
+// expectation.  Launch row r is a row of term values tv[r][Kt]; its
+// observable tables are those of batch row b and its shot counters those of
+// row e: plain rows (x_period = 0) have b = e = r; derived rows of a group
+// have source group row s = (x_begin + r) / x_period, b = rows[s] and
+// e = ebase[s] + (x_begin + r) % x_period.
+struct SampledArgs {
+    const float *tv;         // [nrows][Kt] term expectations
+    int Kt;
+    int K;
+    int reps;
+    uint64_t seed;
+    // tables (row stride 0 when every row has the same terms)
+    const int32_t *slot_k, *slot_t;  // [.][Kt]: observable and term index of term slot j (t < 0: none)
+    int64_t slot_stride;
+    const int32_t *obs_begin;        // [.][K + 1]: CSR of each observable's terms
+    int64_t obs_stride;
+    const int32_t *term_slot;        // term -> its slot j (-1: identity term)
+    const double *term_coeff;
+    int64_t term_stride;             // terms per table row
+    // derived rows
+    const int32_t *rows;
+    const int64_t *ebase;
+    int64_t x_begin;
+    int32_t x_period;
+    int32_t nrows;
+    int64_t w_begin;         // first (row, term slot) pair of a counts launch
+    uint32_t *counts;        // [nrows][Kt]
+    float *out;              // [nrows][K]
+};
+
+// Gradients of the batched shift rules from the expectations of the derived
+// rows: per group row s and symbol, the sum over the symbol's move pairs p
+// (rows 2p and 2p + 1 of s's expansion, moved + and -) of
+// coef_p x scale x sum_k g_k (f_k(+) - f_k(-)), in pair order; scale is the
+// row's scale of slot_p (1 when slot_p < 0).
+struct ShiftGradArgs {
+    const float *f;          // [group rows x period][K], row s x period + j
+    int K, S;
+    int32_t period;
+    const int32_t *rows;     // group row -> batch row
+    const float *upstream;   // [B][K]
+    const int32_t *sym_begin, *sym_pairs;  // CSR symbol -> pairs
+    const int32_t *pair_slot;
+    const double *pair_coef;
+    double coef_mul;         // every coefficient times this
+    const double *slot_scale;
+    int uniform, n_slots;
+    float *grad;             // [B][S]
 };
 
 struct GatherArgs {

@@ -52,6 +52,10 @@ constexpr int64_t kStaticLevelEntries = (int64_t)1 << 22;
 hipError_t static_levels(uint64_t **ptr);
 hipError_t launch_gather(const GatherArgs &a, int nrows, hipStream_t s);
 hipError_t launch_row_mean(const float *in, int64_t groups, int32_t R, int32_t K, float *out, hipStream_t s);
+hipError_t launch_row_gather(const RowGatherArgs &a, hipStream_t s);
+// shot counts and estimates of the sampled expectation (a.nrows rows)
+hipError_t launch_sampled(const SampledArgs &a, hipStream_t s);
+hipError_t launch_shift_grad(const ShiftGradArgs &a, int nrows, hipStream_t s);
 hipError_t launch_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int nrows, int64_t from,
                             int64_t to, hipStream_t s);
 

@@ -251,6 +251,8 @@ struct BuildCtx {
     const float *theta;         // this row's symbol values
     uint64_t noise_seed;        // channels: the row's trajectory draws
     int64_t b;                  // batch row
+    const ShiftDev *shift;      // derived rows: the row's parameter moves (else NULL)
+    double eps;                 // symbol moves are dtheta x eps
 };
 
 __device__ __forceinline__ uint64_t splitmix64(uint64_t seed, uint64_t counter);
@@ -272,10 +274,16 @@ __device__ __forceinline__ int channel_pick(uint64_t seed, int64_t b, int k, con
 }
 
 // symbol resolution eta = scale*theta + offset (or the constant) of a parameter slot
+// (derived rows: the symbol value moved by dtheta, eta moved by delta)
 __device__ __forceinline__ double slot_value(const BuildCtx &c, int slot)
 {
     const int sy = c.slot_sym[slot];
-    return sy >= 0 ? c.scale[slot] * (double)c.theta[sy] + c.off[slot] : c.off[slot];
+    if (!c.shift) return sy >= 0 ? c.scale[slot] * (double)c.theta[sy] + c.off[slot] : c.off[slot];
+    const ShiftDev &x = *c.shift;
+    if (sy < 0) return c.off[slot];
+    const double th = sy == x.sym ? (double)c.theta[sy] + x.dtheta * c.eps : (double)c.theta[sy];
+    const double eta = c.scale[slot] * th + c.off[slot];
+    return slot == x.slot[0] ? eta + x.delta[0] : slot == x.slot[1] ? eta + x.delta[1] : eta;
 }
 __device__ __forceinline__ void resolve(const BuildCtx &c, const GateDev &gd, double *eta)
 {
@@ -368,11 +376,20 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
 {
     const int row = blockIdx.y;
     const int ti = blockIdx.x * blockDim.x + threadIdx.x + a.task_begin;
-    const int b = cget(a.rows, row);
+    // derived rows take the symbols, parameter tables and trajectory of
+    // their source row, plus their parameter moves
+    int src = row;
+    const ShiftDev *shift = nullptr;
+    if (a.x_period > 0) {
+        const int64_t L = a.x_begin + row;
+        src = (int)(L / a.x_period);
+        shift = a.x_shift + (L - (int64_t)src * a.x_period);
+    }
+    const int b = cget(a.rows, src);
     BuildCtx c{a.members, a.gates, a.slot_sym,
-               a.slot_scale + (a.uniform ? 0 : (int64_t)row * a.n_slots),
-               a.slot_off + (a.uniform ? 0 : (int64_t)row * a.n_slots), a.explicit_mats,
-               a.theta + (int64_t)b * a.S, a.noise_seed, b};
+               a.slot_scale + (a.uniform ? 0 : (int64_t)src * a.n_slots),
+               a.slot_off + (a.uniform ? 0 : (int64_t)src * a.n_slots), a.explicit_mats,
+               a.theta + (int64_t)b * a.S, a.noise_seed, b, shift, a.x_eps};
     if (ti < a.task_end) {
         const BuildTask bt = a.tasks[ti];
         build_task(bt, c, a.mats + (int64_t)row * a.mat_stride + bt.out);
@@ -978,6 +995,103 @@ __global__ void k_row_mean(const float *in, int64_t groups, int32_t R, int32_t K
     out[i] = (float)(s / R);
 }
 
+// ------------------------------------------- batched shift rules
+__global__ void k_row_gather(RowGatherArgs a)
+{
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.count) return;
+    const int64_t src = (a.x_begin + r) / a.x_period;
+    for (int j = 0; j < a.narrays; j++) a.out[j][r] = a.in[j][src];
+}
+
+// Shot counts of the sampled expectation: one wavefront per (launch row,
+// term slot), lanes over the shots.  Shot s of term t of observable k in
+// counter row e is +1 when (u >> 11) 2^-53 < (1 + e_t) / 2 (fp64, e_t the
+// float term expectation clamped to [-1, 1]), u the output number
+// ((e K + k) 2^40 + t 2^24 + s) of SplitMix64 from the seed (Sec. "Sampling
+// and Expectation Values": a term's shot is the parity of its qubits
+// measured in its eigenbasis, +1 with that probability).
+__global__ __launch_bounds__(64) void k_sampled_counts(SampledArgs a)
+{
+    const int64_t w = (int64_t)blockIdx.x + a.w_begin;
+    const int r = (int)(w / a.Kt), j = (int)(w - (int64_t)r * a.Kt), lane = threadIdx.x;
+    int64_t b = r, e = r;
+    if (a.x_period > 0) {
+        const int64_t L = a.x_begin + r, src = L / a.x_period;
+        b = a.rows[src];
+        e = a.ebase[src] + (L - src * a.x_period);
+    }
+    const int t = a.slot_t[b * a.slot_stride + j];
+    if (t < 0) {
+        if (lane == 0) a.counts[(int64_t)r * a.Kt + j] = 0;
+        return;
+    }
+    const int k = a.slot_k[b * a.slot_stride + j];
+    double ev = (double)a.tv[(int64_t)r * a.Kt + j];
+    ev = ev > 1.0 ? 1.0 : ev < -1.0 ? -1.0 : ev;
+    const double q = 0.5 * (1.0 + ev);
+    const uint64_t base = ((uint64_t)(e * a.K + k) << 40) | ((uint64_t)t << 24);
+    uint32_t n = 0;
+    for (int sh = lane; sh < a.reps; sh += 64) {
+        const uint64_t u = splitmix64(a.seed, base | (uint64_t)sh);
+        n += (double)(u >> 11) * 0x1.0p-53 < q;
+    }
+    for (int d = 32; d >= 1; d >>= 1) n += __shfl_xor(n, d, 64);
+    if (lane == 0) a.counts[(int64_t)r * a.Kt + j] = n;
+}
+
+// est = sum over the observable's terms in order of c (identity terms) or
+// c (2 n / reps - 1), in fp64 without contractions (the rounding of a plain
+// evaluation of that sum), stored as float.
+__global__ void k_sampled_combine(SampledArgs a)
+{
+#pragma clang fp contract(off)
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)a.nrows * a.K) return;
+    const int64_t r = i / a.K;
+    const int k = (int)(i - r * a.K);
+    int64_t b = r;
+    if (a.x_period > 0) b = a.rows[(a.x_begin + r) / a.x_period];
+    const int32_t *ob = a.obs_begin + b * a.obs_stride;
+    const int32_t *ts = a.term_slot + b * a.term_stride;
+    const double *tc = a.term_coeff + b * a.term_stride;
+    const double reps = (double)a.reps;
+    double est = 0.0;
+    for (int t = ob[k]; t < ob[k + 1]; t++) {
+        const int j = ts[t];
+        if (j < 0) {
+            est += tc[t];
+            continue;
+        }
+        const double n = (double)a.counts[r * a.Kt + j];
+        est += tc[t] * (2.0 * n / reps - 1.0);
+    }
+    a.out[i] = (float)est;
+}
+
+// Gradients of the batched shift rules (one thread per (group row, symbol)).
+__global__ void k_shift_grad(ShiftGradArgs a)
+{
+    const int srow = blockIdx.x;
+    const int s = blockIdx.y * blockDim.x + threadIdx.x;
+    if (s >= a.S) return;
+    const int64_t b = a.rows[srow];
+    const double *scale = a.slot_scale + (a.uniform ? 0 : (int64_t)srow * a.n_slots);
+    const float *g = a.upstream + b * a.K;
+    double sum = 0.0;
+    for (int pi = a.sym_begin[s]; pi < a.sym_begin[s + 1]; pi++) {
+        const int p = a.sym_pairs[pi];
+        const float *fp = a.f + ((int64_t)srow * a.period + 2 * p) * a.K;
+        const float *fm = fp + a.K;
+        double d = 0.0;
+        for (int k = 0; k < a.K; k++) d += (double)g[k] * ((double)fp[k] - (double)fm[k]);
+        const int sl = a.pair_slot[p];
+        sum += a.pair_coef[p] * (sl >= 0 ? scale[sl] : 1.0) * d;
+    }
+    sum *= a.coef_mul;
+    a.grad[b * a.S + s] = (float)sum;
+}
+
 __global__ void k_zero_tail(float2 *state, int64_t row_stride, const int32_t *rows, int64_t from, int64_t to)
 {
     const int row = blockIdx.y;
@@ -1249,6 +1363,39 @@ hipError_t launch_row_mean(const float *in, int64_t groups, int32_t R, int32_t K
     if (n <= 0) return hipSuccess;
     prof::Scope ps("row_mean", s);
     hipLaunchKernelGGL(k_row_mean, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, in, groups, R, K, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_row_gather(const RowGatherArgs &a, hipStream_t s)
+{
+    if (a.count <= 0 || a.narrays <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_row_gather, dim3((unsigned)((a.count + 255) / 256)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_sampled(const SampledArgs &a, hipStream_t s)
+{
+    if (a.nrows <= 0 || a.K <= 0) return hipSuccess;
+    if (a.Kt > 0) {
+        prof::Scope ps("sampled_counts", s);
+        // one wavefront per (row, term slot), at most 2^30 per launch
+        const int64_t waves = (int64_t)a.nrows * a.Kt;
+        for (int64_t w0 = 0; w0 < waves; w0 += (int64_t)1 << 30) {
+            SampledArgs c = a;
+            c.w_begin = w0;
+            hipLaunchKernelGGL(k_sampled_counts, dim3((unsigned)std::min<int64_t>(waves - w0, (int64_t)1 << 30)),
+                               dim3(64), 0, s, c);
+        }
+    }
+    const int64_t n = (int64_t)a.nrows * a.K;
+    hipLaunchKernelGGL(k_sampled_combine, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_shift_grad(const ShiftGradArgs &a, int nrows, hipStream_t s)
+{
+    if (nrows <= 0 || a.S <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_shift_grad, dim3((unsigned)nrows, (unsigned)((a.S + 63) / 64)), dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

@@ -1369,6 +1369,7 @@ void lower_pauli_exp(Reader &r, const HGate &head, int n, int32_t S, uint32_t b,
         h.sym[0] = sym;
         h.scale[0] = f * scale;
         h.offset[0] = f * offset;
+        h.mult = f;
         return h;
     };
     auto constant = [](HGate h, double v) {
@@ -1397,6 +1398,36 @@ void lower_pauli_exp(Reader &r, const HGate &head, int n, int32_t S, uint32_t b,
     emit(param(gate(OP_RZZ, qs[w - 2], qs[w - 1]), 2.0));
     for (int j = w - 3; j >= 0; j--) emit(gate(OP_CNOT, qs[j], qs[j + 1]));
     basis(false);
+}
+
+bool shift_rule(int op, int param, double *delta, double *factor)
+{
+    switch (op) {
+    case OP_RX: case OP_RY: case OP_RZ: case OP_RZZ:
+        // exp(-i eta G / 2), G^2 = I: eigenvalues +-1/2, gap 1
+        *delta = M_PI / 2;
+        *factor = 0.5;
+        return true;
+    case OP_XPOW: case OP_YPOW: case OP_ZPOW: case OP_CZPOW: case OP_CNOTPOW: case OP_XXPOW: case OP_YYPOW:
+    case OP_ZZPOW:
+        // G^t = e^{i pi t / 2} exp(-i (pi t / 2) G): gap pi in t
+        *delta = 0.5;
+        *factor = M_PI / 2;
+        return true;
+    case OP_PAULIEXP:
+        // exp(-i eta P): eigenvalues +-1, gap 2 (the rule as the paper prints it)
+        *delta = M_PI / 4;
+        *factor = 1.0;
+        return true;
+    case OP_FSIM:
+        if (param != 1) return false;  // theta: (XX + YY) / 2 has eigenvalues -1, 0, 1
+        // phi: exp(-i phi |11><11|), gap 1
+        *delta = M_PI / 2;
+        *factor = 0.5;
+        return true;
+    default:
+        return false;
+    }
 }
 
 std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, const Options &opt)
@@ -1448,7 +1479,11 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             }
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
             if (g.op == OP_PAULIEXP) {
-                lower_pauli_exp(r, g, (int)n, (int32_t)S, b, i, emit);
+                lower_pauli_exp(r, g, (int)n, (int32_t)S, b, i, [&](HGate h) {
+                    h.origin = (int32_t)i;
+                    h.blob_op = OP_PAULIEXP;
+                    emit(h);
+                });
                 continue;
             }
             int enq, enp;
@@ -1492,6 +1527,9 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             if (nm)
                 for (int j = nm; j < 32; j++) g.mat[j] = 0.0;
             if (r.bad) fail(TQ_E_INVALID, "program blob: truncated gate");
+            g.origin = (int32_t)i;
+            g.blob_op = g.op;
+            g.mult = 1.0;
             emit(g);
         }
         if (m > (size_t)1 << 24) fail(TQ_E_INVALID, "program blob: gate count too large");
@@ -1505,6 +1543,7 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             key.append((const char *)&g.op, 2);
             key.append((const char *)g.q, 8);
             key.append((const char *)g.sym, sizeof g.sym);
+            key.append((const char *)&g.origin, sizeof g.origin);
             if (g.op == OP_MATRIX1 || g.op == OP_MATRIX2)
                 key.append((const char *)g.mat, sizeof(double) * (g.op == OP_MATRIX1 ? 8 : 32));
         }
@@ -1516,6 +1555,7 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
             grp = pd->groups.back().get();
             grp->n = c.n;
             int nchan = 0;
+            std::vector<int32_t> occ_origin;  // blob gate of each occurrence
             for (uint32_t i = 0; i < ng; i++) {
                 const HGate &g = gates[i];
                 GateDev gd{};
@@ -1529,7 +1569,24 @@ std::unique_ptr<ProgramData> parse_program(const void *blob, size_t nbytes, cons
                     gd.explicit_ = (int32_t)(grp->explicit_mats.size() / 32);
                     grp->explicit_mats.insert(grp->explicit_mats.end(), g.mat, g.mat + 32);
                 }
-                for (int j = 0; j < g.np; j++) grp->slot_sym.push_back(g.sym[j]);
+                for (int j = 0; j < g.np; j++) {
+                    if (g.sym[j] >= 0) {
+                        // a blob gate's parameter: lowered gates of one
+                        // exponential share it (parameter 0)
+                        const int bj = g.blob_op == OP_PAULIEXP ? 0 : j;
+                        auto &oc = grp->occurrences;
+                        if (!oc.empty() && oc.back().slot[1] < 0 && g.blob_op == OP_PAULIEXP &&
+                            oc.back().blob_op == OP_PAULIEXP && occ_origin.back() == g.origin) {
+                            oc.back().slot[1] = grp->n_slots + j;
+                            oc.back().mult[1] = g.mult;
+                        } else {
+                            oc.push_back(Occurrence{{grp->n_slots + j, -1}, {g.mult, 0.0}, g.sym[j], g.blob_op,
+                                                    (uint8_t)bj});
+                            occ_origin.push_back(g.origin);
+                        }
+                    }
+                    grp->slot_sym.push_back(g.sym[j]);
+                }
                 grp->n_slots += g.np;
                 grp->gates.push_back(gd);
                 grp->gate_q0.push_back((int32_t)g.q[0]);

@@ -31,7 +31,34 @@ struct HGate {
     int32_t sym[3];
     double scale[3], offset[3];
     double mat[32];
+    // the blob gate it comes from (its index in the circuit and opcode) and,
+    // for gates lowered from a Pauli-string exponential, the factor its
+    // parameter carries (parameter = mult x the exponential's eta)
+    int32_t origin;
+    uint16_t blob_op;
+    double mult;
 };
+
+// A symbolic parameter of a blob gate (what the parameter-shift rule shifts
+// one at a time), in gate and parameter order.  The gates lowered from a
+// Pauli-string exponential carry its parameter in one slot (two for the
+// global phase of weight zero), each as mult x eta.
+struct Occurrence {
+    int32_t slot[2];   // the parameter slots it drives (slot[1] = -1: one)
+    double mult[2];
+    int32_t sym;
+    uint16_t blob_op;  // opcode of the blob gate
+    uint8_t param;     // its parameter index in the blob gate
+};
+
+// The two-term shift rule of parameter `param` of blob opcode `op` (Sec.
+// "Parameter shift methods", eq. parshift_grad): when the parameter eta
+// enters as exp(-i eta G) and G has two distinct eigenvalues a gap r apart,
+// every expectation is c0 + c1 cos(r eta) + c2 sin(r eta), and
+// df/deta = (r/2) (f(eta + pi/(2r)) - f(eta - pi/(2r))).  Gives delta =
+// pi/(2r) and factor = r/2; false for a parameter without such a rule
+// (fSim's theta: three eigenvalues).
+bool shift_rule(int op, int param, double *delta, double *factor);
 
 struct HCircuit {
     int n = 0;  // (gates live in the circuit's structure group)
@@ -77,6 +104,7 @@ struct Group {
     int32_t fwd_mat_end = 0;                    // forward matrices (with the product init) end here
     std::vector<std::pair<int, int>> dense_stages;  // (forward pass, stage) with a stage matrix
     std::vector<PhaseTerm> phase_terms;         // the row's global phase, linear in the parameters
+    std::vector<Occurrence> occurrences;        // symbolic blob parameters, in gate and parameter order
 };
 
 // Per-op dispatch overhead of the register ops, in fp64-instruction

@@ -125,12 +125,39 @@ struct GroupDev {
     size_t mat_off = 0;  // offset in the matrix workspace
     // specialised kernels of the group: the resident kernel, the tile passes
     SpecMemo res_memo, pass_memo;
+    // the batched shift rules: per kind (0 parameter shift, 1 central
+    // differences) the moves of the derived rows, their pairs and the CSR
+    // symbol -> pairs; the parameter-shift rows' shot-counter bases
+    bool x_ready[2] = {false, false};
+    int x_period[2] = {0, 0};
+    DevBuf x_shift[2], x_pair_slot[2], x_pair_coef[2], x_sym_begin[2], x_sym_pairs[2], x_ebase;
+    void release_x()
+    {
+        for (int k = 0; k < 2; k++)
+            for (DevBuf *b : {&x_shift[k], &x_pair_slot[k], &x_pair_coef[k], &x_sym_begin[k], &x_sym_pairs[k]})
+                b->release();
+        x_ebase.release();
+    }
 };
 
 } // namespace
 
 struct tq_observables_s {
     std::unique_ptr<ObsData> od;
+    // Sampled expectations: the non-identity terms as observables of their
+    // own with coefficient 1 (row b's observable j is its j-th non-identity
+    // term over (k, t); Kt the most any row has), and the shot tables on the
+    // device `dev` (one table row when every row has the same terms).
+    std::unique_ptr<ObsData> terms;
+    int Kt = 0;
+    bool uniform = true;
+    int dev = -1;
+    DevBuf slot_k, slot_t, obs_begin, term_slot, term_coeff;
+    int64_t term_stride = 0;
+    ~tq_observables_s()
+    {
+        for (DevBuf *b : {&slot_k, &slot_t, &obs_begin, &term_slot, &term_coeff}) b->release();
+    }
 };
 
 struct tq_program_s {
@@ -138,21 +165,35 @@ struct tq_program_s {
     int device = -1;
     std::vector<std::unique_ptr<GroupDev>> gdev;
     DevBuf psi, phi, mats, partial, gpart, levels;
+    // workspaces of the derived rows (batched shift rules) and of the
+    // sampled expectations
+    DevBuf xpsi, xmats, xout, xident, xtab[kRowGatherArrays], xterm, xcounts;
+    int xident_n = 0;
     size_t psi_total = 0, mat_total = 0;
     uint64_t obs_id = 0;
     std::vector<std::unique_ptr<ObsGroupDev>> obs_dev;
+    // tables of the observable sets used before the current one (most
+    // recent last), kept so that calls alternating between a few sets do
+    // not rebuild them
+    std::vector<std::pair<uint64_t, std::vector<std::unique_ptr<ObsGroupDev>>>> obs_kept;
     uint64_t noise_seed = 0;  // seed of the channels' per-row draws
 
     ~tq_program_s()
     {
         for (auto &g : gdev) {
+            g->release_x();
             for (DevBuf *b : {&g->rows, &g->ident, &g->gates, &g->slot_sym, &g->scale, &g->off, &g->explicit_,
                               &g->tasks, &g->members, &g->fwd_ops, &g->rev_ops, &g->sym_begin, &g->sym_gslots,
                               &g->gslot_slot, &g->fwd_stages, &g->rev_stages, &g->dense_list, &g->phase_terms})
                 b->release();
         }
         for (auto &o : obs_dev) o->release();
-        for (DevBuf *b : {&psi, &phi, &mats, &partial, &gpart, &levels}) b->release();
+        for (auto &k : obs_kept)
+            for (auto &o : k.second) o->release();
+        for (DevBuf *b : {&psi, &phi, &mats, &partial, &gpart, &levels, &xpsi, &xmats, &xout, &xident, &xterm,
+                          &xcounts})
+            b->release();
+        for (DevBuf &b : xtab) b.release();
     }
 };
 
@@ -249,8 +290,43 @@ float2 *psi_ws(tq_program p) { return (float2 *)p->psi.ensure(p->psi_total * siz
 float2 *phi_ws(tq_program p) { return (float2 *)p->phi.ensure(p->psi_total * sizeof(float2)); }
 double2 *mat_ws(tq_program p) { return (double2 *)p->mats.ensure(p->mat_total * sizeof(double2)); }
 
+// The rows one launch sequence over a group runs.  Plain calls run the
+// group's own rows (own_rows).  The batched shift rules run derived rows:
+// launch row r is row begin + r of the group's expansion, a copy of group row
+// (begin + r) / period with the parameter moves of shift[(begin + r) % period],
+// its matrices in a workspace of its own, its state at row r of the state
+// array and its outputs at row r of the output array.
+struct RunRows {
+    int n = 0;
+    int64_t begin = 0;
+    int period = 0;                      // 0: the group's own rows
+    const ShiftDev *shift = nullptr;
+    double eps = 0.0;                    // central differences: the symbol moves are +-eps
+    double2 *mats = nullptr;
+    const int32_t *ident = nullptr;      // 0 .. n-1 (state rows of the workspaces)
+    const int32_t *out_rows = nullptr;   // output row of each launch row
+    // observable tables of each launch row (NULL: the group's own, by group row)
+    const int32_t *term_begin = nullptr, *term_count = nullptr, *cbegin = nullptr, *ccount = nullptr,
+                  *dcbegin = nullptr, *dccount = nullptr;
+};
+
+RunRows own_rows(tq_program p, size_t gi)
+{
+    RunRows r;
+    r.n = (int)p->pd->groups[gi]->rows.size();
+    r.mats = mat_ws(p) + p->gdev[gi]->mat_off;
+    r.ident = (const int32_t *)p->gdev[gi]->ident.p;
+    r.out_rows = (const int32_t *)p->gdev[gi]->rows.p;
+    return r;
+}
+
+template <class T> const T *or_own(const int32_t *derived, const DevBuf &own)
+{
+    return derived ? derived : (const T *)own.p;
+}
+
 // Symbol resolution + fused matrices for the task range [begin, end).
-void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end, hipStream_t s)
+void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end, hipStream_t s, const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
     GroupDev &gd = *p->gdev[gi];
@@ -269,8 +345,12 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.theta = theta;
     a.S = p->pd->S;
     a.rows = (const int32_t *)gd.rows.p;
-    a.mats = mat_ws(p) + gd.mat_off;
+    a.mats = rr.mats;
     a.mat_stride = std::max(g.mat_block, 1);
+    a.x_begin = rr.begin;
+    a.x_period = rr.period;
+    a.x_shift = rr.shift;
+    a.x_eps = rr.eps;
     // the first qubit's product-init matrix (built by the range's first
     // task) carries the row's global phase
     const bool init = g.n > 0 && begin == g.fwd_tasks.begin && end > begin && !g.phase_terms.empty();
@@ -278,7 +358,7 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.n_phase = (int32_t)g.phase_terms.size();
     a.phase_terms = (const PhaseTerm *)gd.phase_terms.p;
     a.noise_seed = p->noise_seed;
-    hip_check(launch_build(a, (int)g.rows.size(), s), "matrix build launch");
+    hip_check(launch_build(a, rr.n, s), "matrix build launch");
     if (begin <= g.fwd_tasks.begin && end >= g.fwd_tasks.end && gd.n_dense > 0) {
         // dense forward stages, from the op matrices just built
         StageBuildArgs sb{};
@@ -288,24 +368,25 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
         sb.ops = (const PassOp *)gd.fwd_ops.p;
         sb.mats = a.mats;
         sb.mat_stride = a.mat_stride;
-        hip_check(launch_build_stage(sb, (int)g.rows.size(), s), "stage matrix build launch");
+        hip_check(launch_build_stage(sb, rr.n, s), "stage matrix build launch");
     }
 }
 
 // Forward passes of group gi into `state` (row r of the group at
 // srows[r] * row_stride).
-void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const int32_t *srows, hipStream_t s)
+void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const int32_t *srows, hipStream_t s,
+             const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
     GroupDev &gd = *p->gdev[gi];
-    const int nrows = (int)g.rows.size();
+    const int nrows = rr.n;
     for (size_t pi = 0; pi < g.fwd.size(); pi++) {
         const Pass &ps = g.fwd[pi];
         PassArgs a{};
         a.state = state;
         a.row_stride = row_stride;
         a.rows = srows;
-        a.mats = mat_ws(p) + gd.mat_off;
+        a.mats = rr.mats;
         a.mat_stride = std::max(g.mat_block, 1);
         a.ops = (const PassOp *)gd.fwd_ops.p;
         a.stages = (const Stage *)gd.fwd_stages.p + gd.fwd_stage_off[pi];
@@ -344,11 +425,21 @@ void check_obs_fit(tq_program p, tq_observables o)
 
 // Per-group term tables of an observables handle, in the group's
 // expectation tile geometry.
-void ensure_obs(tq_program p, tq_observables o)
+constexpr size_t kObsKept = 3;
+
+void ensure_obs(tq_program p, const ObsData &od)
 {
-    if (p->obs_id == o->od->id) return;
+    if (p->obs_id == od.id) return;
+    for (size_t i = 0; i < p->obs_kept.size(); i++)
+        if (p->obs_kept[i].first == od.id) {
+            auto tables = std::move(p->obs_kept[i].second);
+            p->obs_kept.erase(p->obs_kept.begin() + i);
+            if (p->obs_id) p->obs_kept.emplace_back(p->obs_id, std::move(p->obs_dev));
+            p->obs_dev = std::move(tables);
+            p->obs_id = od.id;
+            return;
+        }
     const ProgramData &pd = *p->pd;
-    const ObsData &od = *o->od;
     std::vector<std::unique_ptr<ObsGroupDev>> out;
     for (auto &gp : pd.groups) {
         const Group &g = *gp;
@@ -468,26 +559,31 @@ void ensure_obs(tq_program p, tq_observables o)
         }
         out.push_back(std::move(og));
     }
-    for (auto &old : p->obs_dev) old->release();
+    if (p->obs_id) {
+        p->obs_kept.emplace_back(p->obs_id, std::move(p->obs_dev));
+        if (p->obs_kept.size() > kObsKept) {
+            for (auto &old : p->obs_kept.front().second) old->release();
+            p->obs_kept.erase(p->obs_kept.begin());
+        }
+    }
     p->obs_dev = std::move(out);
-    p->obs_id = o->od->id;
+    p->obs_id = od.id;
 }
 
 // Expectations of Z-only Pauli sums over group gi's rows (n >= 12), streamed
 // from HBM by the diagonal kernel.
-void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s, const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
-    GroupDev &gd = *p->gdev[gi];
     ObsGroupDev &og = *p->obs_dev[gi];
-    const int nrows = (int)g.rows.size();
+    const int nrows = rr.n;
     DiagArgs a{};
     a.psi = psi;
     a.row_stride = (int64_t)1 << g.n;
-    a.rows = (const int32_t *)gd.ident.p;
+    a.rows = rr.ident;
     a.chunks = (const DChunk *)og.dchunks.p;
-    a.row_chunk_begin = (const int32_t *)og.dcbegin.p;
-    a.row_chunk_count = (const int32_t *)og.dccount.p;
+    a.row_chunk_begin = or_own<int32_t>(rr.dcbegin, og.dcbegin);
+    a.row_chunk_count = or_own<int32_t>(rr.dccount, og.dccount);
     a.classes = (const DClass *)og.dclasses.p;
     a.terms = (const DTerm *)og.dterms.p;
     a.blocks_log2 = g.n - kDiagBlockBits;
@@ -505,7 +601,7 @@ void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, h
         a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)slots * a.k_count);
         hip_check(launch_pauli_diag(a, nrows, og.damax, s), "diagonal Pauli kernel launch");
         PauliReduceArgs r{};
-        r.rows = (const int32_t *)gd.rows.p;
+        r.rows = rr.out_rows;
         r.partial = a.partial;
         r.wg_per_row = a.wg_per_row;
         r.K = K;
@@ -518,12 +614,12 @@ void diag_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, h
 
 // Expectations of an observable set the same on every row of group gi, by
 // the kernels specialised for it: one state read per pass of the plan.
-void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s)
+void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *out, hipStream_t s,
+                      const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
-    GroupDev &gd = *p->gdev[gi];
     ObsGroupDev &og = *p->obs_dev[gi];
-    const int nrows = (int)g.rows.size();
+    const int nrows = rr.n;
     const int npass = (int)og.spec_passes.size();
     std::string log;
     int fit = pauli_spec_slots(og.spec_src, og.spec_passes[0].geom, &log, &og.spec_memo);
@@ -535,7 +631,7 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
     PauliSpecArgs a{};
     a.psi = psi;
     a.row_stride = (int64_t)1 << g.n;
-    a.rows = (const int32_t *)gd.ident.p;
+    a.rows = rr.ident;
     a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
     a.npass = npass;
     a.k_count = K;
@@ -548,7 +644,7 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
         hip_check(e, "specialised Pauli launch");
     }
     PauliReduceArgs r{};
-    r.rows = (const int32_t *)gd.rows.p;
+    r.rows = rr.out_rows;
     r.partial = a.partial;
     r.wg_per_row = npass * a.wg_per_row;  // the passes' workgroups side by side
     r.K = K;
@@ -606,22 +702,21 @@ void spec_phi_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, con
 }
 
 void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const float *upstream, int K, float *out,
-                 hipStream_t s)
+                 hipStream_t s, const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
-    GroupDev &gd = *p->gdev[gi];
     ObsGroupDev &og = *p->obs_dev[gi];
-    const int nrows = (int)g.rows.size();
+    const int nrows = rr.n;
     if (K == 0 || nrows == 0) return;
     if (!phi && og.diag) {
-        diag_group(p, gi, psi, K, out, s);
+        diag_group(p, gi, psi, K, out, s, rr);
         return;
     }
     if (!phi && !og.spec_passes.empty()) {
-        spec_pauli_group(p, gi, psi, K, out, s);
+        spec_pauli_group(p, gi, psi, K, out, s, rr);
         return;
     }
-    if (phi && upstream && K == 1 && !og.phi_passes.empty()) {
+    if (phi && upstream && K == 1 && !og.phi_passes.empty() && rr.period == 0) {
         spec_phi_group(p, gi, psi, phi, upstream, out, s);
         return;
     }
@@ -629,11 +724,11 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
     a.psi = psi;
     a.phi = phi;
     a.row_stride = (int64_t)1 << g.n;
-    a.rows = (const int32_t *)gd.ident.p;
-    a.brows = (const int32_t *)gd.rows.p;
+    a.rows = rr.ident;
+    a.brows = rr.out_rows;
     a.chunks = (const PChunk *)og.chunks.p;
-    a.row_chunk_begin = (const int32_t *)og.cbegin.p;
-    a.row_chunk_count = (const int32_t *)og.ccount.p;
+    a.row_chunk_begin = or_own<int32_t>(rr.cbegin, og.cbegin);
+    a.row_chunk_count = or_own<int32_t>(rr.ccount, og.ccount);
     a.xfg = (const PXfGroup *)og.xfg.p;
     a.xg = (const PXGroup *)og.xg.p;
     a.us = (const PUSub *)og.us.p;
@@ -695,10 +790,9 @@ bool resident(tq_program p, size_t gi, bool adjoint, int tmax)
 // Launch the resident kernel of group gi: the one specialised for the
 // group's structure when the program asks for it and its LDS fits the
 // default window, else the precompiled one.
-void run_resident(tq_program p, size_t gi, const ResArgs &a, hipStream_t s)
+void run_resident(tq_program p, size_t gi, const ResArgs &a, int nrows, hipStream_t s)
 {
     const Group &g = *p->pd->groups[gi];
-    const int nrows = (int)g.rows.size();
     const size_t lds = resident_lds_bytes(a.n, a.nacc, a.grad != nullptr);
     if (p->pd->opt.specialize && lds <= kResidentSpecLds) {
         std::string log;
@@ -710,19 +804,19 @@ void run_resident(tq_program p, size_t gi, const ResArgs &a, hipStream_t s)
     hip_check(launch_resident(a, nrows, s), "resident launch");
 }
 
-ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint, hipStream_t s)
+ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint, hipStream_t s, const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
     GroupDev &gd = *p->gdev[gi];
-    build_mats(p, gi, theta, g.fwd_tasks.begin, adjoint ? g.rev_tasks.end : g.fwd_tasks.end, s);
+    build_mats(p, gi, theta, g.fwd_tasks.begin, adjoint ? g.rev_tasks.end : g.fwd_tasks.end, s, rr);
     ResArgs a{};
-    a.mats = mat_ws(p) + gd.mat_off;
+    a.mats = rr.mats;
     a.mat_stride = std::max(g.mat_block, 1);
     a.slot_scale = (const double *)gd.scale.p;
     a.uniform = g.uniform_slots;
     a.n_slots = g.n_slots;
     a.S = p->pd->S;
-    a.rows = (const int32_t *)gd.rows.p;
+    a.rows = rr.out_rows;
     a.n = g.n;
     a.fops = (const PassOp *)gd.fwd_ops.p;
     a.fstages = (const Stage *)gd.fwd_stages.p;
@@ -738,12 +832,12 @@ ResArgs resident_args(tq_program p, size_t gi, const float *theta, bool adjoint,
     return a;
 }
 
-void resident_terms(tq_program p, size_t gi, ResArgs &a, int K, float *exp_out)
+void resident_terms(tq_program p, size_t gi, ResArgs &a, int K, float *exp_out, const RunRows &rr)
 {
     ObsGroupDev &og = *p->obs_dev[gi];
     a.terms = (const TermDev *)og.terms.p;
-    a.row_term_begin = (const int32_t *)og.begin.p;
-    a.row_term_count = (const int32_t *)og.count.p;
+    a.row_term_begin = or_own<int32_t>(rr.term_begin, og.begin);
+    a.row_term_count = or_own<int32_t>(rr.term_count, og.count);
     a.K = K;
     a.exp_out = exp_out;
     a.gacc = og.tmax;
@@ -751,20 +845,19 @@ void resident_terms(tq_program p, size_t gi, ResArgs &a, int K, float *exp_out)
 }
 
 // the final states of group gi into its rows of the state workspace
-void forward_to_ws(tq_program p, size_t gi, const float *theta, float2 *psi, hipStream_t s)
+void forward_to_ws(tq_program p, size_t gi, const float *theta, float2 *psi, hipStream_t s, const RunRows &rr)
 {
     const Group &g = *p->pd->groups[gi];
-    GroupDev &gd = *p->gdev[gi];
     if (resident(p, gi, false, 0)) {
-        ResArgs a = resident_args(p, gi, theta, false, s);
+        ResArgs a = resident_args(p, gi, theta, false, s, rr);
         a.state_out = psi;
         a.out_stride = (int64_t)1 << g.n;
-        a.out_rows = (const int32_t *)gd.ident.p;
-        run_resident(p, gi, a, s);
+        a.out_rows = rr.ident;
+        run_resident(p, gi, a, rr.n, s);
         return;
     }
-    build_mats(p, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-    forward(p, gi, psi, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
+    build_mats(p, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, rr);
+    forward(p, gi, psi, (int64_t)1 << g.n, rr.ident, s, rr);
 }
 
 
@@ -788,6 +881,377 @@ void fill_levels(SampArgs &a, int n)
     }
     a.nlev = k;
     a.row_level = std::max<int64_t>(total, 1);
+}
+
+// ---------------------------------------------- sampled expectations
+// Limits of the shot counter ((e K + k) 2^40 + t 2^24 + s): e K + k < 2^24,
+// t < 2^16, s < 2^24.
+constexpr int64_t kMaxCounterRows = (int64_t)1 << 24;
+
+// The term observables and shot tables of an observables handle, built on
+// first use (tables on the current device).
+void prepare_terms(tq_observables o)
+{
+    int dev = -1;
+    hip_check(hipGetDevice(&dev), "hipGetDevice");
+    if (o->terms) {
+        if (dev != o->dev) fail(TQ_E_INVALID, "observables were first used on another device");
+        return;
+    }
+    const ObsData &od = *o->od;
+    auto t = std::make_unique<ObsData>();
+    t->B = od.B;
+    int Kt = 0;
+    for (int b = 0; b < od.B; b++) {
+        int n = 0;
+        for (int k = 0; k < od.K; k++) {
+            const auto &sum = od.sums[(size_t)b * od.K + k];
+            if (sum.size() >= ((size_t)1 << 16)) fail(TQ_E_UNSUPPORTED, "sampled expectation: more than 65535 terms in one observable");
+            for (const HTerm &h : sum) n += !h.factors.empty();
+        }
+        Kt = std::max(Kt, n);
+    }
+    t->K = Kt;
+    t->sums.resize((size_t)od.B * Kt);
+    // tables: per row the (k, t) of each slot and per observable its terms
+    bool uniform = true;
+    for (int b = 1; b < od.B && uniform; b++)
+        for (int k = 0; k < od.K && uniform; k++) {
+            const auto &x = od.sums[k], &y = od.sums[(size_t)b * od.K + k];
+            uniform = x.size() == y.size();
+            for (size_t i = 0; i < x.size() && uniform; i++)
+                uniform = x[i].coeff == y[i].coeff && x[i].factors == y[i].factors;
+        }
+    const int tb = uniform ? std::min(od.B, 1) : od.B;  // table rows
+    size_t tmax = 0;
+    for (int b = 0; b < tb; b++) {
+        size_t n = 0;
+        for (int k = 0; k < od.K; k++) n += od.sums[(size_t)b * od.K + k].size();
+        tmax = std::max(tmax, n);
+    }
+    std::vector<int32_t> slot_k((size_t)tb * Kt, 0), slot_t((size_t)tb * Kt, -1), obs_begin((size_t)tb * (od.K + 1));
+    std::vector<int32_t> term_slot(std::max<size_t>((size_t)tb * tmax, 1), -1);
+    std::vector<double> term_coeff(term_slot.size(), 0.0);
+    for (int b = 0; b < od.B; b++) {
+        int j = 0;
+        size_t ti = 0;
+        for (int k = 0; k < od.K; k++) {
+            const auto &sum = od.sums[(size_t)b * od.K + k];
+            if (b < tb) obs_begin[(size_t)b * (od.K + 1) + k] = (int32_t)ti;
+            for (size_t tt = 0; tt < sum.size(); tt++, ti++) {
+                const HTerm &h = sum[tt];
+                if (b < tb) term_coeff[(size_t)b * tmax + ti] = h.coeff;
+                if (h.factors.empty()) continue;
+                t->sums[(size_t)b * Kt + j].push_back(HTerm{1.0, h.factors});
+                if (b < tb) {
+                    slot_k[(size_t)b * Kt + j] = k;
+                    slot_t[(size_t)b * Kt + j] = (int32_t)tt;
+                    term_slot[(size_t)b * tmax + ti] = j;
+                }
+                j++;
+            }
+        }
+        if (b < tb) obs_begin[(size_t)b * (od.K + 1) + od.K] = (int32_t)ti;
+    }
+    t->id = g_obs_counter.fetch_add(1);
+    upload(o->slot_k, slot_k);
+    upload(o->slot_t, slot_t);
+    upload(o->obs_begin, obs_begin);
+    upload(o->term_slot, term_slot);
+    upload(o->term_coeff, term_coeff);
+    o->term_stride = (int64_t)tmax;
+    o->uniform = uniform;
+    o->Kt = Kt;
+    o->dev = dev;
+    o->terms = std::move(t);
+}
+
+SampledArgs sampled_args(tq_observables o, int reps, uint64_t seed)
+{
+    SampledArgs a{};
+    a.Kt = o->Kt;
+    a.K = o->od->K;
+    a.reps = reps;
+    a.seed = seed;
+    a.slot_k = (const int32_t *)o->slot_k.p;
+    a.slot_t = (const int32_t *)o->slot_t.p;
+    a.slot_stride = o->uniform ? 0 : o->Kt;
+    a.obs_begin = (const int32_t *)o->obs_begin.p;
+    a.obs_stride = o->uniform ? 0 : o->od->K + 1;
+    a.term_slot = (const int32_t *)o->term_slot.p;
+    a.term_coeff = (const double *)o->term_coeff.p;
+    a.term_stride = o->uniform ? 0 : o->term_stride;
+    return a;
+}
+
+// Expectations of every group's rows (the body of tq_expectation).
+void expectations_all(tq_program prog, const float *theta, const ObsData &od, float *out, hipStream_t s)
+{
+    const ProgramData &pd = *prog->pd;
+    ensure_obs(prog, od);
+    float2 *psi = psi_ws(prog);
+    for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+        const Group &g = *pd.groups[gi];
+        GroupDev &gd = *prog->gdev[gi];
+        const RunRows rr = own_rows(prog, gi);
+        if (resident(prog, gi, false, prog->obs_dev[gi]->tmax)) {
+            ResArgs a = resident_args(prog, gi, theta, false, s, rr);
+            resident_terms(prog, gi, a, od.K, out, rr);
+            run_resident(prog, gi, a, rr.n, s);
+            continue;
+        }
+        build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, rr);
+        forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, rr.ident, s, rr);
+        pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, od.K, out, s, rr);
+    }
+}
+
+// ------------------------------------------------ batched shift rules
+enum ShiftKind { kParamShift = 0, kFiniteDiff = 1 };
+
+// The derived rows of group gi for one kind: parameter shift, pair p = the
+// p-th symbolic blob parameter moved by +delta (row 2p) and -delta (row
+// 2p + 1), gradient coefficient factor / mult x the row's scale of its
+// first slot; central differences, pair p = the p-th symbol the group uses
+// moved by +-eps (the moves are +-1 times eps), coefficient 1 / (2 eps)
+// applied at the reduction.
+void ensure_x(tq_program p, size_t gi, int kind)
+{
+    GroupDev &gd = *p->gdev[gi];
+    if (gd.x_ready[kind]) return;
+    const Group &g = *p->pd->groups[gi];
+    const int S = p->pd->S;
+    std::vector<ShiftDev> sh;
+    std::vector<int32_t> pslot, psym;
+    std::vector<double> pcoef;
+    if (kind == kParamShift) {
+        for (const Occurrence &oc : g.occurrences) {
+            double delta, factor;
+            if (!shift_rule(oc.blob_op, oc.param, &delta, &factor))
+                fail(TQ_E_UNSUPPORTED, "parameter shift: a symbolic parameter has no two-term shift rule "
+                                       "(fSim theta; use the adjoint or finite differences)");
+            for (int sg : {1, -1}) {
+                ShiftDev d{};
+                d.slot[0] = oc.slot[0];
+                d.slot[1] = oc.slot[1];
+                d.sym = -1;
+                d.delta[0] = sg * oc.mult[0] * delta;
+                d.delta[1] = oc.slot[1] >= 0 ? sg * oc.mult[1] * delta : 0.0;
+                sh.push_back(d);
+            }
+            pslot.push_back(oc.slot[0]);
+            pcoef.push_back(factor / oc.mult[0]);
+            psym.push_back(oc.sym);
+        }
+    } else {
+        std::vector<char> used(S, 0);
+        for (int32_t sy : g.slot_sym)
+            if (sy >= 0) used[sy] = 1;
+        for (int sy = 0; sy < S; sy++) {
+            if (!used[sy]) continue;
+            for (int sg : {1, -1}) {
+                ShiftDev d{};
+                d.slot[0] = d.slot[1] = -1;
+                d.sym = sy;
+                d.dtheta = sg;
+                sh.push_back(d);
+            }
+            pslot.push_back(-1);
+            pcoef.push_back(1.0);
+            psym.push_back(sy);
+        }
+    }
+    std::vector<int32_t> begin(S + 1, 0), pairs(psym.size());
+    for (int32_t sy : psym) begin[sy + 1]++;
+    for (int i = 0; i < S; i++) begin[i + 1] += begin[i];
+    std::vector<int32_t> fill(begin.begin(), begin.end() - 1);
+    for (size_t pi = 0; pi < psym.size(); pi++) pairs[fill[psym[pi]]++] = (int32_t)pi;
+    upload(gd.x_shift[kind], sh);
+    upload(gd.x_pair_slot[kind], pslot);
+    upload(gd.x_pair_coef[kind], pcoef);
+    upload(gd.x_sym_begin[kind], begin);
+    upload(gd.x_sym_pairs[kind], pairs);
+    gd.x_period[kind] = (int)sh.size();
+    gd.x_ready[kind] = true;
+}
+
+// Shot-counter rows of the parameter-shift rows: the shifted circuits of all
+// rows as one batch in row order, each row's 2 x (its occurrences) in
+// (occurrence, +/-) order; per group row the first of its row.
+int64_t ensure_ebase(tq_program p)
+{
+    const ProgramData &pd = *p->pd;
+    std::vector<int64_t> per_row(pd.B, 0);
+    for (size_t gi = 0; gi < pd.groups.size(); gi++)
+        for (int32_t b : pd.groups[gi]->rows) per_row[b] = 2 * (int64_t)pd.groups[gi]->occurrences.size();
+    std::vector<int64_t> start(pd.B + 1, 0);
+    for (int b = 0; b < pd.B; b++) start[b + 1] = start[b] + per_row[b];
+    for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+        GroupDev &gd = *p->gdev[gi];
+        if (gd.x_ebase.p) continue;
+        std::vector<int64_t> e;
+        for (int32_t b : pd.groups[gi]->rows) e.push_back(start[b]);
+        upload(gd.x_ebase, e);
+    }
+    return start[pd.B];
+}
+
+const int32_t *ident_rows(tq_program p, int n)
+{
+    if (p->xident_n < n) {
+        std::vector<int32_t> v(n);
+        for (int i = 0; i < n; i++) v[i] = i;
+        upload(p->xident, v);
+        p->xident_n = n;
+    }
+    return (const int32_t *)p->xident.p;
+}
+
+// Derived rows per launch: at most 65535 (one grid row each in the builder),
+// states within 4 GiB and matrices within 1 GiB.
+int derived_chunk(tq_program p, size_t gi, int64_t total, bool on_chip)
+{
+    const Group &g = *p->pd->groups[gi];
+    int64_t c = std::min<int64_t>(total, 65535);
+    c = std::min<int64_t>(c, std::max<int64_t>(1, ((int64_t)1 << 30) / (16 * (int64_t)std::max(g.mat_block, 1))));
+    if (!on_chip) c = std::min<int64_t>(c, std::max<int64_t>(1, ((int64_t)1 << 32) / ((int64_t)8 << g.n)));
+    return (int)std::max<int64_t>(c, 1);
+}
+
+// Gradients of sum_k g_k <h_k> of every row by a batched shift rule: the
+// derived rows of each group run chunk by chunk through the same build,
+// forward and expectation kernels as plain rows (reps > 0: their sampled
+// expectations), then one reduction per group forms the gradients.
+void shift_grad(tq_program prog, const float *theta, tq_observables obs, const float *upstream, int kind, int reps,
+                uint64_t seed, double eps, float *grad, hipStream_t s)
+{
+    const ProgramData &pd = *prog->pd;
+    const ObsData &od = *obs->od;
+    const int K = od.K;
+    for (size_t gi = 0; gi < pd.groups.size(); gi++) ensure_x(prog, gi, kind);
+    if (reps > 0) {
+        prepare_terms(obs);
+        const int64_t total = ensure_ebase(prog);
+        if (total * (int64_t)std::max(K, 1) >= kMaxCounterRows)
+            fail(TQ_E_UNSUPPORTED, "sampled parameter shift: too many (shifted circuit, observable) pairs for the "
+                                   "shot counter (2^24)");
+    }
+    const ObsData &eod = reps > 0 ? *obs->terms : od;  // observables the derived rows evaluate
+    const int Ke = eod.K;
+    ensure_obs(prog, eod);
+    // workspaces sized for the largest group first (none is reallocated
+    // while work of an earlier group may still read it)
+    size_t need_out = 1, need_mats = 1, need_psi = 1, need_chunk = 1;
+    std::vector<int> chunks(pd.groups.size(), 0);
+    std::vector<char> on_chip(pd.groups.size(), 0);
+    for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+        const Group &g = *pd.groups[gi];
+        const int64_t total = (int64_t)g.rows.size() * prog->gdev[gi]->x_period[kind];
+        if (total == 0 || K == 0) continue;
+        on_chip[gi] = resident(prog, gi, false, prog->obs_dev[gi]->tmax);
+        chunks[gi] = derived_chunk(prog, gi, total, on_chip[gi]);
+        need_out = std::max(need_out, (size_t)total * K);
+        need_mats = std::max(need_mats, (size_t)chunks[gi] * std::max(g.mat_block, 1));
+        if (!on_chip[gi]) need_psi = std::max(need_psi, (size_t)chunks[gi] << g.n);
+        need_chunk = std::max(need_chunk, (size_t)chunks[gi]);
+    }
+    float *f_all = (float *)prog->xout.ensure(sizeof(float) * need_out);
+    double2 *mats = (double2 *)prog->xmats.ensure(sizeof(double2) * need_mats);
+    float2 *psi = need_psi > 1 ? (float2 *)prog->xpsi.ensure(sizeof(float2) * need_psi) : nullptr;
+    const int32_t *ident = ident_rows(prog, (int)need_chunk);
+    float *tv = reps > 0 ? (float *)prog->xterm.ensure(sizeof(float) * need_chunk * std::max(Ke, 1)) : nullptr;
+    uint32_t *counts = reps > 0 ? (uint32_t *)prog->xcounts.ensure(sizeof(uint32_t) * need_chunk * std::max(Ke, 1))
+                                : nullptr;
+    int32_t *tab_buf[kRowGatherArrays];
+    for (int j = 0; j < kRowGatherArrays; j++) tab_buf[j] = (int32_t *)prog->xtab[j].ensure(sizeof(int32_t) * need_chunk);
+    for (size_t gi = 0; gi < pd.groups.size(); gi++) {
+        const Group &g = *pd.groups[gi];
+        GroupDev &gd = *prog->gdev[gi];
+        ObsGroupDev &og = *prog->obs_dev[gi];
+        const int nrows = (int)g.rows.size();
+        const int period = gd.x_period[kind];
+        const int64_t total = (int64_t)nrows * period;
+        float *f = nullptr;
+        if (total > 0 && K > 0) {
+            f = f_all;
+            const int chunk = chunks[gi];
+            // per-row observable tables, gathered from the source rows
+            const DevBuf *tab_in[kRowGatherArrays] = {&og.begin, &og.count, &og.cbegin, &og.ccount, &og.dcbegin,
+                                                      &og.dccount};
+            int32_t *tab_out[kRowGatherArrays];
+            for (int j = 0; j < kRowGatherArrays; j++) tab_out[j] = tab_in[j]->p ? tab_buf[j] : nullptr;
+            for (int64_t begin = 0; begin < total; begin += chunk) {
+                const int c = (int)std::min<int64_t>(chunk, total - begin);
+                RunRows rr;
+                rr.n = c;
+                rr.begin = begin;
+                rr.period = period;
+                rr.shift = (const ShiftDev *)gd.x_shift[kind].p;
+                rr.eps = eps;
+                rr.mats = mats;
+                rr.ident = ident;
+                rr.out_rows = ident;
+                RowGatherArgs ra{};
+                for (int j = 0; j < kRowGatherArrays; j++)
+                    if (tab_out[j]) {
+                        ra.in[ra.narrays] = (const int32_t *)tab_in[j]->p;
+                        ra.out[ra.narrays] = tab_out[j];
+                        ra.narrays++;
+                    }
+                ra.x_begin = begin;
+                ra.x_period = period;
+                ra.count = c;
+                hip_check(launch_row_gather(ra, s), "row table gather launch");
+                rr.term_begin = tab_out[0];
+                rr.term_count = tab_out[1];
+                rr.cbegin = tab_out[2];
+                rr.ccount = tab_out[3];
+                rr.dcbegin = tab_out[4];
+                rr.dccount = tab_out[5];
+                float *vals = reps > 0 ? tv : f + begin * K;
+                if (Ke > 0) {
+                    if (on_chip[gi]) {
+                        ResArgs a = resident_args(prog, gi, theta, false, s, rr);
+                        resident_terms(prog, gi, a, Ke, vals, rr);
+                        run_resident(prog, gi, a, c, s);
+                    } else {
+                        build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, rr);
+                        forward(prog, gi, psi, (int64_t)1 << g.n, ident, s, rr);
+                        pauli_group(prog, gi, psi, nullptr, nullptr, Ke, vals, s, rr);
+                    }
+                }
+                if (reps > 0) {
+                    SampledArgs sa = sampled_args(obs, reps, seed);
+                    sa.tv = tv;
+                    sa.rows = (const int32_t *)gd.rows.p;
+                    sa.ebase = (const int64_t *)gd.x_ebase.p;
+                    sa.x_begin = begin;
+                    sa.x_period = period;
+                    sa.nrows = c;
+                    sa.counts = counts;
+                    sa.out = f + begin * K;
+                    hip_check(launch_sampled(sa, s), "sampled expectation launch");
+                }
+            }
+        }
+        ShiftGradArgs ga{};
+        ga.f = f;
+        ga.K = K;
+        ga.S = pd.S;
+        ga.period = period;
+        ga.rows = (const int32_t *)gd.rows.p;
+        ga.upstream = upstream;
+        ga.sym_begin = (const int32_t *)gd.x_sym_begin[kind].p;
+        ga.sym_pairs = (const int32_t *)gd.x_sym_pairs[kind].p;
+        ga.pair_slot = (const int32_t *)gd.x_pair_slot[kind].p;
+        ga.pair_coef = (const double *)gd.x_pair_coef[kind].p;
+        ga.coef_mul = kind == kFiniteDiff ? 1.0 / (2.0 * eps) : 1.0;
+        ga.slot_scale = (const double *)gd.scale.p;
+        ga.uniform = g.uniform_slots;
+        ga.n_slots = g.n_slots;
+        ga.grad = grad;
+        hip_check(launch_shift_grad(ga, nrows, s), "shift-rule gradient launch");
+    }
 }
 
 } // namespace
@@ -918,15 +1382,16 @@ tq_status tq_simulate_state(tq_program prog, const float *theta, void *states, v
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
+            const RunRows rr = own_rows(prog, gi);
             if (resident(prog, gi, false, 0)) {
-                ResArgs a = resident_args(prog, gi, theta, false, s);
+                ResArgs a = resident_args(prog, gi, theta, false, s, rr);
                 a.state_out = (float2 *)states;
                 a.out_stride = stride;
                 a.out_rows = (const int32_t *)gd.rows.p;
-                run_resident(prog, gi, a, s);
+                run_resident(prog, gi, a, rr.n, s);
             } else {
-                build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-                forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s);
+                build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, rr);
+                forward(prog, gi, (float2 *)states, stride, (const int32_t *)gd.rows.p, s, rr);
             }
             if (g.n < pd.nmax)
                 hip_check(launch_zero_tail((float2 *)states, stride, (const int32_t *)gd.rows.p, (int)g.rows.size(),
@@ -948,21 +1413,22 @@ tq_status tq_expectation(tq_program prog, const float *theta, tq_observables obs
         check_align(out, 4, "out");
         check_align(theta, 4, "symbol_values");
         ensure_device(prog);
-        ensure_obs(prog, obs);
+        ensure_obs(prog, *obs->od);
         hipStream_t s = as_stream(stream);
         float2 *psi = psi_ws(prog);
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
+            const RunRows rr = own_rows(prog, gi);
             if (resident(prog, gi, false, prog->obs_dev[gi]->tmax)) {
-                ResArgs a = resident_args(prog, gi, theta, false, s);
-                resident_terms(prog, gi, a, obs->od->K, out);
-                run_resident(prog, gi, a, s);
+                ResArgs a = resident_args(prog, gi, theta, false, s, rr);
+                resident_terms(prog, gi, a, obs->od->K, out, rr);
+                run_resident(prog, gi, a, rr.n, s);
                 continue;
             }
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s);
-            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, (const int32_t *)gd.ident.p, s);
-            pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, obs->od->K, out, s);
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, rr);
+            forward(prog, gi, psi + gd.psi_off, (int64_t)1 << g.n, rr.ident, s, rr);
+            pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, obs->od->K, out, s, rr);
         }
     });
 }
@@ -982,7 +1448,7 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
         check_align(upstream, 4, "upstream");
         check_align(expectations, 4, "expectations");
         ensure_device(prog);
-        ensure_obs(prog, obs);
+        ensure_obs(prog, *obs->od);
         hipStream_t s = as_stream(stream);
         float2 *psi = psi_ws(prog), *phi = phi_ws(prog);
         const int K = obs->od->K;
@@ -992,27 +1458,29 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
             ObsGroupDev &og = *prog->obs_dev[gi];
             const int nrows = (int)g.rows.size();
             const int64_t stride = (int64_t)1 << g.n;
+            const RunRows rr = own_rows(prog, gi);
             if (resident(prog, gi, true, og.tmax)) {
-                ResArgs a = resident_args(prog, gi, theta, pd.S > 0, s);
-                resident_terms(prog, gi, a, K, expectations);
+                ResArgs a = resident_args(prog, gi, theta, pd.S > 0, s, rr);
+                resident_terms(prog, gi, a, K, expectations, rr);
                 if (pd.S > 0) {
                     a.upstream = upstream;
                     a.grad = grad;
                     a.nacc = og.tmax + g.n_gslots;
                 }
                 a.nacc = std::max(a.nacc, 1);
-                run_resident(prog, gi, a, s);
+                run_resident(prog, gi, a, rr.n, s);
                 continue;
             }
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
-            forward(prog, gi, psi + gd.psi_off, stride, (const int32_t *)gd.ident.p, s);
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s, rr);
+            forward(prog, gi, psi + gd.psi_off, stride, rr.ident, s, rr);
             if (pd.S == 0) {
-                if (expectations && K > 0) pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, K, expectations, s);
+                if (expectations && K > 0)
+                    pauli_group(prog, gi, psi + gd.psi_off, nullptr, nullptr, K, expectations, s, rr);
                 continue;
             }
             // phi = H_g psi, with the expectations from the same sweep
             if (K > 0)
-                pauli_group(prog, gi, psi + gd.psi_off, phi + gd.psi_off, upstream, K, expectations, s);
+                pauli_group(prog, gi, psi + gd.psi_off, phi + gd.psi_off, upstream, K, expectations, s, rr);
             else
                 hip_check(launch_zero_tail(phi + gd.psi_off, stride, (const int32_t *)gd.ident.p, nrows, 0, stride, s),
                           "phi clear");
@@ -1076,6 +1544,102 @@ tq_status tq_adjoint_grad(tq_program prog, const float *theta, tq_observables ob
     });
 }
 
+tq_status tq_observables_terms(tq_observables obs, int32_t *Kt)
+{
+    return guarded([&] {
+        if (!obs || !Kt) fail(TQ_E_INVALID, "observables handle or Kt is NULL");
+        int most = 0;
+        const ObsData &od = *obs->od;
+        for (int b = 0; b < od.B; b++) {
+            int n = 0;
+            for (int k = 0; k < od.K; k++)
+                for (const HTerm &h : od.sums[(size_t)b * od.K + k]) n += !h.factors.empty();
+            most = std::max(most, n);
+        }
+        *Kt = most;
+    });
+}
+
+tq_status tq_sampled_expectation(tq_program prog, const float *theta, tq_observables obs, int32_t reps, uint64_t seed,
+                                 float *out, float *term_out, void *stream)
+{
+    return guarded([&] {
+        if (!prog || !obs) fail(TQ_E_INVALID, "program or observables is NULL");
+        const ProgramData &pd = *prog->pd;
+        check_obs_fit(prog, obs);
+        if (reps < 1 || reps >= (1 << 24)) fail(TQ_E_INVALID, "repetitions must be in [1, 2^24)");
+        const int K = obs->od->K;
+        if ((int64_t)pd.B * K >= kMaxCounterRows)
+            fail(TQ_E_UNSUPPORTED, "sampled expectation: B x K must be below 2^24 (the shot counter)");
+        if (pd.B == 0 || K == 0) return;
+        if (!out) fail(TQ_E_INVALID, "out is NULL");
+        if (pd.S > 0 && !theta) fail(TQ_E_INVALID, "symbol_values is NULL");
+        check_align(out, 4, "out");
+        check_align(term_out, 4, "term_out");
+        check_align(theta, 4, "symbol_values");
+        ensure_device(prog);
+        prepare_terms(obs);
+        hipStream_t s = as_stream(stream);
+        const int Kt = obs->Kt;
+        float *tv = (float *)prog->xterm.ensure(sizeof(float) * (size_t)pd.B * std::max(Kt, 1));
+        if (Kt > 0) expectations_all(prog, theta, *obs->terms, tv, s);
+        SampledArgs a = sampled_args(obs, reps, seed);
+        a.tv = tv;
+        a.nrows = pd.B;
+        a.counts = (uint32_t *)prog->xcounts.ensure(sizeof(uint32_t) * (size_t)pd.B * std::max(Kt, 1));
+        a.out = out;
+        hip_check(launch_sampled(a, s), "sampled expectation launch");
+        if (term_out && Kt > 0)
+            hip_check(hipMemcpyAsync(term_out, tv, sizeof(float) * (size_t)pd.B * Kt, hipMemcpyDeviceToDevice, s),
+                      "term values copy");
+    });
+}
+
+tq_status tq_param_shift_grad(tq_program prog, const float *theta, tq_observables obs, const float *upstream,
+                              int32_t reps, uint64_t seed, float *grad, void *stream)
+{
+    return guarded([&] {
+        if (!prog || !obs) fail(TQ_E_INVALID, "program or observables is NULL");
+        const ProgramData &pd = *prog->pd;
+        check_obs_fit(prog, obs);
+        if (reps < 0 || reps >= (1 << 24)) fail(TQ_E_INVALID, "repetitions must be in [0, 2^24)");
+        if (pd.B == 0 || pd.S == 0) return;
+        if (!theta || !grad) fail(TQ_E_INVALID, "symbol_values or grad is NULL");
+        if (obs->od->K > 0 && !upstream) fail(TQ_E_INVALID, "upstream is NULL");
+        check_align(theta, 4, "symbol_values");
+        check_align(grad, 4, "grad");
+        check_align(upstream, 4, "upstream");
+        for (auto &gp : pd.groups)
+            for (const Occurrence &oc : gp->occurrences) {
+                double delta, factor;
+                if (!shift_rule(oc.blob_op, oc.param, &delta, &factor))
+                    fail(TQ_E_UNSUPPORTED, "parameter shift: a symbolic parameter has no two-term shift rule "
+                                           "(fSim theta; use the adjoint or finite differences)");
+            }
+        ensure_device(prog);
+        shift_grad(prog, theta, obs, upstream, kParamShift, reps, seed, 0.0, grad, as_stream(stream));
+    });
+}
+
+tq_status tq_finite_diff_grad(tq_program prog, const float *theta, tq_observables obs, const float *upstream,
+                              double eps, float *grad, void *stream)
+{
+    return guarded([&] {
+        if (!prog || !obs) fail(TQ_E_INVALID, "program or observables is NULL");
+        const ProgramData &pd = *prog->pd;
+        check_obs_fit(prog, obs);
+        if (!(eps > 0.0) || !(eps < 1e300)) fail(TQ_E_INVALID, "eps must be a finite number > 0");
+        if (pd.B == 0 || pd.S == 0) return;
+        if (!theta || !grad) fail(TQ_E_INVALID, "symbol_values or grad is NULL");
+        if (obs->od->K > 0 && !upstream) fail(TQ_E_INVALID, "upstream is NULL");
+        check_align(theta, 4, "symbol_values");
+        check_align(grad, 4, "grad");
+        check_align(upstream, 4, "upstream");
+        ensure_device(prog);
+        shift_grad(prog, theta, obs, upstream, kFiniteDiff, 0, 0, eps, grad, as_stream(stream));
+    });
+}
+
 tq_status tq_sample(tq_program prog, const float *theta, int64_t n_shots, uint64_t seed, uint64_t *out, void *stream)
 {
     return tq_sample_with_amplitudes(prog, theta, n_shots, seed, out, nullptr, 0, nullptr, stream);
@@ -1103,7 +1667,7 @@ tq_status tq_sample_with_amplitudes(tq_program prog, const float *theta, int64_t
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s);
+            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s, own_rows(prog, gi));
             if (M > 0) {
                 GatherArgs ga{};
                 ga.state = psi + gd.psi_off;
@@ -1152,7 +1716,7 @@ tq_status tq_amplitudes(tq_program prog, const float *theta, const uint64_t *bit
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s);
+            forward_to_ws(prog, gi, theta, psi + gd.psi_off, s, own_rows(prog, gi));
             GatherArgs a{};
             a.state = psi + gd.psi_off;
             a.row_stride = (int64_t)1 << g.n;
@@ -1268,7 +1832,7 @@ tq_status tq_build_matrices(tq_program prog, const float *theta, void *out, int6
         for (size_t gi = 0; gi < pd.groups.size(); gi++) {
             const Group &g = *pd.groups[gi];
             GroupDev &gd = *prog->gdev[gi];
-            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s);
+            build_mats(prog, gi, theta, g.fwd_tasks.begin, g.rev_tasks.end, s, own_rows(prog, gi));
             const size_t n = g.rows.size() * (size_t)std::max(g.mat_block, 1);
             hip_check(hipMemcpyAsync((double2 *)out + off, mat_ws(prog) + gd.mat_off, n * sizeof(double2),
                                      hipMemcpyDeviceToDevice, s),
@@ -1350,6 +1914,15 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
             o
               << ",\"slots\":" << g.n_slots << ",\"mat_block\":" << g.mat_block << ",\"n_gslots\":" << g.n_gslots
               << ",\"absorbed\":" << absorbed << ",\"uniform_slots\":" << (g.uniform_slots ? 1 : 0);
+            // symbolic blob parameters (what the parameter-shift rule moves):
+            // [slot, second slot or -1, symbol, blob opcode, parameter index]
+            o << ",\"occurrences\":[";
+            for (size_t k = 0; k < g.occurrences.size(); k++) {
+                const Occurrence &oc = g.occurrences[k];
+                o << (k ? "," : "") << "[" << oc.slot[0] << "," << oc.slot[1] << "," << oc.sym << ","
+                  << oc.blob_op << "," << (int)oc.param << "]";
+            }
+            o << "]";
             // the observables last used with the program: Z-only stream, and the
             // terms of each generated expectation pass and H_g pass
             if (gi < prog->obs_dev.size()) {

@@ -67,13 +67,18 @@ def lib():
         L.tq_program_describe.argtypes = [vp, ctypes.c_char_p, sz, ctypes.POINTER(sz)]
         L.tq_build_matrices.argtypes = [vp, vp, vp, i64, ctypes.POINTER(i64), vp]
         L.tq_gate_matrix.argtypes = [i32, vp, vp, i32, i32, i32, vp, p32, ctypes.POINTER(ctypes.c_double)]
+        L.tq_observables_terms.argtypes = [vp, p32]
+        L.tq_sampled_expectation.argtypes = [vp, vp, vp, i32, u64, vp, vp, vp]
+        L.tq_param_shift_grad.argtypes = [vp, vp, vp, vp, i32, u64, vp, vp]
+        L.tq_finite_diff_grad.argtypes = [vp, vp, vp, vp, ctypes.c_double, vp, vp]
         L.tq_profile_start.argtypes = [ctypes.c_char_p]
         L.tq_profile_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
         for f in ("tq_program_create", "tq_program_info", "tq_program_specialize", "tq_observables_create", "tq_observables_info",
                   "tq_simulate_state", "tq_expectation", "tq_sample", "tq_sample_with_amplitudes", "tq_adjoint_grad",
                   "tq_amplitudes",
                   "tq_sample_from_state", "tq_sample_from_state_noalloc", "tq_amplitudes_from_state", "tq_program_describe", "tq_profile_start", "tq_profile_read",
-                  "tq_gate_matrix", "tq_build_matrices"):
+                  "tq_gate_matrix", "tq_build_matrices", "tq_observables_terms", "tq_sampled_expectation",
+                  "tq_param_shift_grad", "tq_finite_diff_grad"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -255,6 +260,50 @@ def adjoint_grad(prog, symbol_values, obs, upstream, grad=None, expectations=Non
     u = _dev(upstream, torch.float32, (prog.B, obs.K), "upstream")
     e = _dev(expectations, torch.float32, (prog.B, obs.K), "expectations")
     _check(lib().tq_adjoint_grad(prog._h, _theta(prog, symbol_values), obs._h, u, g, e, _stream(stream)))
+    return grad
+
+
+def observables_terms(obs):
+    """Kt: the most non-identity terms any row of `obs` has."""
+    kt = ctypes.c_int32()
+    _check(lib().tq_observables_terms(obs._h, ctypes.byref(kt)))
+    return kt.value
+
+
+def sampled_expectation(prog, symbol_values, obs, reps, seed, out=None, term_out=None, stream=None):
+    """[B, K] expectations estimated from `reps` shots per non-identity term
+    (tq_sampled_expectation); `term_out` [B, Kt] receives the term values the
+    shots were drawn from when given."""
+    if out is None:
+        out = torch.empty((prog.B, obs.K), dtype=torch.float32, device="cuda")
+    p = _dev(out, torch.float32, (prog.B, obs.K), "out")
+    t = _dev(term_out, torch.float32, (prog.B, observables_terms(obs)), "term_out") if term_out is not None else None
+    _check(lib().tq_sampled_expectation(prog._h, _theta(prog, symbol_values), obs._h, int(reps),
+                                        ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), p, t, _stream(stream)))
+    return out
+
+
+def param_shift_grad(prog, symbol_values, obs, upstream, reps=0, seed=0, grad=None, stream=None):
+    """[B, S] gradients by the parameter-shift rule (tq_param_shift_grad);
+    reps > 0 takes each shifted circuit's expectations from that many shots
+    per term."""
+    if grad is None:
+        grad = torch.empty((prog.B, prog.S), dtype=torch.float32, device="cuda")
+    g = _dev(grad, torch.float32, (prog.B, prog.S), "grad") if prog.S else None
+    u = _dev(upstream, torch.float32, (prog.B, obs.K), "upstream")
+    _check(lib().tq_param_shift_grad(prog._h, _theta(prog, symbol_values), obs._h, u, int(reps),
+                                     ctypes.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF), g, _stream(stream)))
+    return grad
+
+
+def finite_diff_grad(prog, symbol_values, obs, upstream, eps, grad=None, stream=None):
+    """[B, S] gradients by central differences of step eps (tq_finite_diff_grad)."""
+    if grad is None:
+        grad = torch.empty((prog.B, prog.S), dtype=torch.float32, device="cuda")
+    g = _dev(grad, torch.float32, (prog.B, prog.S), "grad") if prog.S else None
+    u = _dev(upstream, torch.float32, (prog.B, obs.K), "upstream")
+    _check(lib().tq_finite_diff_grad(prog._h, _theta(prog, symbol_values), obs._h, u, float(eps), g,
+                                     _stream(stream)))
     return grad
 
 

@@ -174,3 +174,40 @@ def test_channels_validated_and_seed_entry_points():
     # a noisy structure's generated kernels compile for gfx950
     w = wl.with_noise(wl.random_batch(1413, B=2, n=14, n_gates=30, n_symbols=3, K=1), 0.05, 2)
     tq.specialize(create(w.program_blob(), specialize=True), "gfx950")
+
+
+def test_shift_rule_occurrences_and_validation():
+    # every symbolic blob parameter is one occurrence; the global phase of a
+    # weight-0 Pauli exponential drives two lowered slots as one occurrence,
+    # and the same lowered gates written out by hand stay two occurrences
+    # (a structure of its own)
+    from paper_2003_02989_amd.circuits import const
+    c1 = Circuit(2).add("RX", 0, [sym(0)]).add_pauli_exp([], sym(1, 0.5)).add("FSIM", (0, 1), [const(0.2), sym(0)])
+    c2 = Circuit(2).add("RX", 0, [sym(0)]).add("RZ", 0, [sym(1, 1.0)]).add("ZPOW", 0, [sym(1, -2 / 3.141592653589793)])
+    c2.add("FSIM", (0, 1), [const(0.2), sym(0)])
+    p = create(program_blob([c1, c2], 2))
+    d = tq.describe(p)
+    assert len(d["groups"]) == 2
+    occ = [[o[:3] + [o[3], o[4]] for o in g["occurrences"]] for g in d["groups"]]
+    assert [len(o) for o in occ] == [3, 4]
+    g0 = occ[0]
+    assert g0[0][1] == -1 and g0[0][2] == 0 and g0[0][3] == 5            # RX
+    assert g0[1][1] >= 0 and g0[1][2] == 1 and g0[1][3] == 26           # exp(-i eta I): two slots
+    assert g0[2][2] == 0 and g0[2][3] == 22 and g0[2][4] == 1            # fSim phi
+    L = tq.lib()
+    o = tq.Observables(observable_blob([[[(1.0, [(0, "Z")]), (0.5, [])]]] * 2))
+    assert tq.observables_terms(o) == 1
+    fake = ctypes.c_void_p(16)
+    assert L.tq_sampled_expectation(p._h, fake, o._h, 0, 0, fake, None, None) == tq.TQ_E_INVALID  # reps 0
+    assert L.tq_sampled_expectation(p._h, fake, o._h, 1 << 24, 0, fake, None, None) == tq.TQ_E_INVALID
+    assert L.tq_sampled_expectation(p._h, fake, o._h, 10, 0, None, None, None) == tq.TQ_E_INVALID  # out NULL
+    assert L.tq_param_shift_grad(p._h, fake, o._h, fake, -1, 0, fake, None) == tq.TQ_E_INVALID
+    assert L.tq_param_shift_grad(p._h, fake, o._h, fake, 0, 0, None, None) == tq.TQ_E_INVALID  # grad NULL
+    assert L.tq_finite_diff_grad(p._h, fake, o._h, fake, ctypes.c_double(0.0), fake, None) == tq.TQ_E_INVALID
+    assert L.tq_finite_diff_grad(p._h, fake, o._h, fake, ctypes.c_double(float("nan")), fake, None) == tq.TQ_E_INVALID
+    # fSim theta has no two-term rule: rejected before any device call
+    c3 = Circuit(2).add("FSIM", (0, 1), [sym(0), const(0.1)])
+    p3 = create(program_blob([c3], 1))
+    o3 = tq.Observables(observable_blob([[[(1.0, [(0, "Z")])]]]))
+    assert L.tq_param_shift_grad(p3._h, fake, o3._h, fake, 0, 0, fake, None) == tq.TQ_E_UNSUPPORTED
+    assert b"shift" in L.tq_last_error()
