@@ -33,7 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "effective HBM GB/s per fused-gate pass; circuit-expectations/sec at batch"
-KERNELS = ("build", "resident", "pass", "pauli", "pauli_reduce", "rev_pass", "grad_reduce",
+KERNELS = ("build", "resident", "pass", "pauli", "pauli_reduce", "rev_pass", "grad_reduce", "sampled_counts",
            "samp_l1", "samp_shots", "gather")
 PEAK_HBM_GBS = 8000.0
 PEAK_FP64_TFLOPS = 78.6  # fp64 vector: 256 CUs x 2.4 GHz x 128 flop/clk
@@ -78,12 +78,19 @@ def workload(name):
     return wl.CONFIGS[name]()
 
 
-def describe_workload(name, w, adjoint=True):
+def describe_workload(name, w, adjoint=True, mode="plain", reps=0, eps=0.0):
     d = describe_config(name, w, w.B // w.extras.get("trajectories", 1))
+    if mode == "sampled":
+        d = d.replace("expectations+adjoint grads", "expectations") + f", sampled expectations ({reps} shots per term)"
+    elif mode == "param-shift":
+        d = d.replace("expectations+adjoint grads", "expectations") + ", parameter-shift gradients" + (
+            f" from sampled expectations ({reps} shots per term)" if reps else "")
+    elif mode == "finite-diff":
+        d = d.replace("expectations+adjoint grads", "expectations") + f", central-difference gradients (eps {eps})"
     if "trajectories" in w.extras:
         d += (f", depolarizing noise p={w.extras['noise_p']} after every gate, "
               f"{w.extras['trajectories']} trajectories per circuit (B={w.B} trajectory rows)")
-    if name in ("c1", "c2", "c5") and not adjoint:
+    if name in ("c1", "c2", "c5") and not adjoint and mode == "plain":
         d = d.replace("expectations+adjoint grads", "expectations only")
     return d
 
@@ -207,6 +214,22 @@ def kernel_work(plan, kernel, n_obs_terms, adjoint):
     return flops, bytes_, launches
 
 
+def expansion(plan, w, mode):
+    """Rows the step runs per row of the batch: 1, or for the shift rules the
+    shifted circuits (2 per symbolic blob parameter; central differences: 2
+    per symbol a row uses), averaged over the batch."""
+    if mode == "param-shift":
+        tot = sum(g["rows"] * 2 * len(g["occurrences"]) for g in plan["groups"])
+    elif mode == "finite-diff":
+        tot = 0
+        for c in w.circuits:
+            used = {p[0] for _, _, params, _ in c.gates for p in params if p[0] >= 0}
+            tot += 2 * len(used)
+    else:
+        return 1.0
+    return tot / max(w.B, 1)
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as fh:
@@ -216,6 +239,12 @@ def cpu_model():
     except OSError:
         pass
     return "unknown"
+
+
+def progress(msg):
+    """One line per finished phase on stderr (the JSON line is the only
+    stdout output)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
 def main():
@@ -234,6 +263,14 @@ def main():
     ap.add_argument("--pauli-exp", action="store_true",
                     help="c3: the QAOA layers built from Pauli-string exponentials of the cost and mixer "
                          "Hamiltonians")
+    ap.add_argument("--mode", default="plain", choices=["plain", "sampled", "param-shift", "finite-diff"],
+                    help="c1, c2, c3, c5: plain = adjoint gradients (c1, c2, c5) or expectations (c3); "
+                         "sampled = tq_sampled_expectation with --reps shots per term; param-shift = "
+                         "tq_param_shift_grad (--reps > 0: from sampled expectations); finite-diff = "
+                         "tq_finite_diff_grad with step --eps")
+    ap.add_argument("--reps", type=int, default=None,
+                    help="shots per term (sampled: default 1000; param-shift: default 0 = exact)")
+    ap.add_argument("--eps", type=float, default=1e-2)
     ap.add_argument("--no-specialize", action="store_true",
                     help="run with the precompiled table-driven kernels instead of the ones compiled for the "
                          "circuit structure on the first call")
@@ -272,6 +309,9 @@ def main():
             cmd.append("--pauli-exp")
         if args.noise > 0:
             cmd += ["--noise", str(args.noise), "--trajectories", str(args.trajectories)]
+        cmd += ["--mode", args.mode, "--eps", str(args.eps)]
+        if args.reps is not None:
+            cmd += ["--reps", str(args.reps)]
         cold = {}
         for key in ("empty_cache", "filled_cache"):
             r = subprocess.run(cmd, env=env, capture_output=True, text=True, timeout=900)
@@ -279,6 +319,7 @@ def main():
                 print(r.stdout[-2000:], r.stderr[-4000:], file=sys.stderr)
                 sys.exit(r.returncode)
             cold[key] = json.loads(r.stdout.strip().splitlines()[-1])
+            progress(f"cold start ({key.replace('_', ' ')}) {cold[key]['cold_ms']:.0f} ms")
         os.environ["TQ_CACHE_DIR"] = cache_tmp
 
     import numpy as np
@@ -305,6 +346,11 @@ def main():
         sys.exit(1)
     w = wl.c3_qaoa(exponentials=True) if args.pauli_exp else workload(args.config)
     noisy = args.noise > 0
+    mode = args.mode
+    if mode != "plain" and (args.config == "c4" or args.expectation_only):
+        print("--mode applies to c1, c2, c3, c5 (without --expectation-only)", file=sys.stderr)
+        sys.exit(1)
+    reps = args.reps if args.reps is not None else (1000 if mode == "sampled" else 0)
     if noisy and args.config == "c4":
         print("--noise applies to c1, c2, c3, c5", file=sys.stderr)
         sys.exit(1)
@@ -313,11 +359,12 @@ def main():
     if noisy:
         w = wl.with_noise(w_base, args.noise, R)
     B, K = w.B, w.K
-    adjoint = args.config in ("c1", "c2", "c5") and not args.expectation_only
+    adjoint = args.config in ("c1", "c2", "c5") and not args.expectation_only and mode == "plain"
     specialize = not args.no_specialize
     # every step (first call, warm-up, per-kernel profiling, timed) gets its
     # own parameter set, drawn like the workload's
-    n_prof = 2 * len(KERNELS)
+    prof_steps = 1 if mode in ("param-shift", "finite-diff") else 2
+    n_prof = prof_steps * len(KERNELS)
     n_steps_total = 1 + args.warmup + n_prof + args.steps
     # (the trajectories of a noisy circuit share its parameters)
     thetas = ([torch.as_tensor(np.repeat(t, R, axis=0), device="cuda")
@@ -343,7 +390,18 @@ def main():
         th = thetas[i]
         if noisy:  # new trajectories every step
             tq.set_noise_seed(prog, 1000 + i)
-        if adjoint:
+        if mode == "sampled":
+            tq.sampled_expectation(prog, th, obs, reps, 5000 + i, out=exp)
+            if noisy:
+                tq.row_mean(exp, R, out=exp_mean)
+        elif mode in ("param-shift", "finite-diff"):
+            if mode == "param-shift":
+                tq.param_shift_grad(prog, th, obs, up, reps=reps, seed=5000 + i, grad=grad)
+            else:
+                tq.finite_diff_grad(prog, th, obs, up, args.eps, grad=grad)
+            if noisy:
+                tq.row_mean(grad, R, out=grad_mean)
+        elif adjoint:
             tq.adjoint_grad(prog, th, obs, up, grad=grad, expectations=exp)
             if noisy:
                 tq.row_mean(grad, R, out=grad_mean)
@@ -376,21 +434,24 @@ def main():
         print(json.dumps({"load_ms": t_load * 1e3, "create_ms": t_create * 1e3, "first_call_ms": t_first * 1e3,
                           "cold_ms": (t_load + t_create + t_first) * 1e3}), flush=True)
         return
+    progress(f"first call {t_first * 1e3:.0f} ms")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    progress("warm-up done")
 
     # dominant kernel: device time per step of every kernel, from HIP events
     per_kernel = {}
     for kname in KERNELS:
         tq.profile_start(kname)
-        for _ in range(2):
+        for _ in range(prof_steps):
             step()
         torch.cuda.synchronize()
         n_l, ms = tq.profile_read()
         tq.profile_start(None)
         if n_l:
-            per_kernel[kname] = ms / 2
+            per_kernel[kname] = ms / prof_steps
+            progress(f"kernel {kname}: {ms / prof_steps:.3f} ms per step")
     dominant = max(per_kernel, key=per_kernel.get)
 
     # timed region; the dominant kernel's launches are bracketed by events
@@ -404,10 +465,18 @@ def main():
     n_launch, dom_ms = tq.profile_read()
     tq.profile_start(None)
     ms_per_step = elapsed * 1e3 / args.steps
+    progress(f"timed {args.steps} steps: {ms_per_step:.3f} ms per step")
 
     plan = tq.describe(prog)
     n_terms = sum(len(t) for t in w.observables[0])
     flops, bytes_, launches_per_step = kernel_work(plan, dominant, n_terms, adjoint)
+    # the shift rules run every row's shifted circuits (derived rows) through
+    # the same kernels: the work of a plain step times the rows per row
+    expand = expansion(plan, w, mode)
+    flops *= expand
+    bytes_ *= expand
+    if mode in ("param-shift", "finite-diff"):  # launches are per chunk of derived rows: count them
+        launches_per_step = n_launch / args.steps
     avg_ms = dom_ms / max(n_launch, 1)
     traffic = measured_traffic(args.config + ("_expectation" if args.expectation_only else "")
                                + ("_pauli_exp" if args.pauli_exp else ""), dominant)
@@ -425,7 +494,7 @@ def main():
                      "avg_launch_ms": avg_ms, "other_roof": other})
 
     # the two halves of the metric
-    pass_bytes = kernel_work(plan, "pass", n_terms, adjoint)[1]
+    pass_bytes = kernel_work(plan, "pass", n_terms, adjoint)[1] * expand
     if dominant == "pass":
         pass_ms = dom_ms / args.steps
     else:
@@ -450,13 +519,24 @@ def main():
         Bc = B // R
         value = Bc * K / (ms_per_step * 1e-3)
         unit_v = "circuit-expectations/s" + (" (with adjoint gradients)" if adjoint else "")
+        if mode == "sampled":
+            unit_v = f"circuit-expectations/s (sampled, {reps} shots per term)"
+        if mode in ("param-shift", "finite-diff"):
+            value = Bc / (ms_per_step * 1e-3)
+            unit_v = ("gradient rows/s (" + ("parameter shift" if mode == "param-shift" else
+                                             f"central differences, eps {args.eps}")
+                      + f", {expand:g} shifted circuits per row" + (f", {reps} shots per term" if reps else "") + ")")
         if noisy:
             unit_v += f" (noisy: mean of {R} trajectories each)"
-        rates = {"circuit_expectations_per_s": value,
+        rates = {"circuit_expectations_per_s": Bc * K / (ms_per_step * 1e-3),
                  "cold_circuit_expectations_per_s": Bc * K / cold_s,
                  "cold_cached_circuit_expectations_per_s": Bc * K / cached_s if cached_s else None,
                  "fused_pass_GBps": fused_pass_gbs,
                  "fused_pass_ms_per_step": pass_ms if pass_ms > 0 else None}
+        if mode in ("param-shift", "finite-diff"):
+            rates["gradient_rows_per_s"] = value
+            rates["shifted_circuits_per_step"] = expand * B
+            rates["shifted_circuit_expectations_per_s"] = expand * B * K / (ms_per_step * 1e-3)
         if noisy:
             rates["trajectory_rows_per_s"] = B / (ms_per_step * 1e-3)
         if adjoint:
@@ -475,7 +555,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic (seeded generators, no datasets); a new parameter set or sampling seed per step",
-        "config": {"workload": describe_workload(args.config, w, adjoint), "storage": "complex64", "arithmetic": "fp64",
+        "config": {"workload": describe_workload(args.config, w, adjoint, mode, reps, args.eps), "storage": "complex64",
+                   "arithmetic": "fp64",
                    "batch": B, "qubits": w.n_max, "symbols": w.n_symbols, "observables": K,
                    "pauli_terms": n_terms, "specialized_kernel": specialize,
                    "noise": {"depolarizing_p": args.noise, "trajectories": R} if noisy else None},
@@ -488,7 +569,7 @@ def main():
     }
 
     if not args.no_cpu_baseline and local_rank == 0:
-        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds, adjoint, R)
+        line["cpu_baseline"] = cpu_baseline(args.config, w, args.cpu_seconds, adjoint, R, mode, reps, args.eps)
     print(json.dumps(line), flush=True)
     if cache_tmp:
         shutil.rmtree(cache_tmp, ignore_errors=True)
@@ -627,7 +708,7 @@ def sweep(steps, cases="all", specialize=True):
         del prog
 
 
-def cpu_baseline(name, w, budget_s, adjoint=True, R=1):
+def cpu_baseline(name, w, budget_s, adjoint=True, R=1, mode="plain", reps=0, eps=1e-2):
     """The oracle on the host cores, on a bounded sample of the same workload."""
     import numpy as np
 
@@ -654,6 +735,36 @@ def cpu_baseline(name, w, budget_s, adjoint=True, R=1):
                 "kind": "oracle", "cpu": cpu_model(), "amplitudes_per_s": 4096 / dt,
                 "sample": f"24-qubit stand-in (4x6 grid) of the depth-20 random circuit, {n_g} gates, one full "
                           f"complex128 simulation plus 4096 amplitudes per call, {reps} calls in {dt * reps:.1f} s"}
+    if mode in ("param-shift", "finite-diff"):
+        # the oracle simulates every shifted circuit in full: one row costs
+        # `expand` expectation evaluations.  Rows are timed directly when one
+        # fits the budget; otherwise the expectation of sampled rows is timed
+        # and scaled by the shifted circuits per row (what the oracle's
+        # shift rule runs for each row).
+        from paper_2003_02989_amd.workloads import Workload
+        sub = Workload(w.name, [w.circuits[0]], w.n_symbols, w.theta[:1], [w.observables[0]], w.upstream[:1])
+        p = orc.Program(sub.program_blob())
+        o = orc.Observables(sub.observable_blob())
+        th = sub.theta.astype(np.float64)
+        t0 = time.perf_counter()
+        orc.expectation(p, th, o)
+        t_exp = time.perf_counter() - t0
+        n_shift = 2 * (sum(1 for _, _, params, _ in w.circuits[0].gates for q in params if q[0] >= 0)
+                       if mode == "param-shift" else
+                       len({q[0] for _, _, params, _ in w.circuits[0].gates for q in params if q[0] >= 0}))
+        if t_exp * n_shift > budget_s:
+            n_e = 1
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < budget_s:
+                orc.expectation(p, th, o)
+                n_e += 1
+            dt = (time.perf_counter() - t0 + t_exp) / n_e
+            return {"value": 1.0 / (dt * n_shift) / R, "unit": "gradient rows/s", "cores": threads,
+                    "kind": "oracle", "cpu": cpu_model(),
+                    "sample": f"{n_e} complex128 expectation evaluations of row 0 in {dt * n_e:.1f} s, scaled by the "
+                              f"{n_shift} shifted circuits the oracle's "
+                              + ("parameter-shift" if mode == "param-shift" else "central-difference")
+                              + " rule simulates per row"}
     rows = 1
     done_rows = 0
     t0 = time.perf_counter()
@@ -665,15 +776,31 @@ def cpu_baseline(name, w, budget_s, adjoint=True, R=1):
         p = orc.Program(sub.program_blob())
         o = orc.Observables(sub.observable_blob())
         th = sub.theta.astype(np.float64)
-        orc.expectation(p, th, o)
-        if adjoint:
-            orc.adjoint_grad(p, th, o, sub.upstream.astype(np.float64))
+        if mode == "sampled":
+            orc.sampled_expectation(p, th, o, reps, 1)
+        elif mode == "param-shift":
+            orc.param_shift_grad(p, th, o, sub.upstream.astype(np.float64), reps, 1)
+        elif mode == "finite-diff":
+            orc.finite_diff_grad(p, th, o, sub.upstream.astype(np.float64), eps)
+        else:
+            orc.expectation(p, th, o)
+            if adjoint:
+                orc.adjoint_grad(p, th, o, sub.upstream.astype(np.float64))
         done_rows += len(r)
         el = time.perf_counter() - t0
         if el > budget_s:
             break
         rows = min(max(rows * 2, 1), w.B)
     what = "expectations" + (" + adjoint gradients" if adjoint else "")
+    if mode != "plain":
+        what = {"sampled": f"sampled expectations, {reps} shots per term",
+                "param-shift": "parameter-shift gradients" + (f" from {reps} shots per term" if reps else ""),
+                "finite-diff": f"central-difference gradients, eps {eps}"}[mode]
+    if mode in ("param-shift", "finite-diff"):
+        return {"value": done_rows / R / el, "unit": "gradient rows/s", "cores": threads, "kind": "oracle",
+                "cpu": cpu_model(),
+                "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "
+                          f"the full batch) in {el:.1f} s"}
     return {"value": done_rows / R * w.K / el, "unit": "circuit-expectations/s", "cores": threads, "kind": "oracle",
             "cpu": cpu_model(),
             "sample": f"{done_rows} rows of the same batch ({what}, rows repeated in doubling chunks up to "

@@ -312,7 +312,7 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
 
 /* Kernel timing for benchmarks.  After tq_profile_start(name) every launch of
  * the named kernel ("build", "resident", "pass", "pauli", "pauli_reduce",
- * "rev_pass", "grad_reduce", "samp_l1", "samp_shots", "gather") is bracketed
+ * "rev_pass", "grad_reduce", "samp_l1", "samp_shots", "gather", "sampled_counts") is bracketed
  * by a pair of HIP events recorded on its launch stream; NULL or "" stops
  * recording.  tq_profile_read waits for the recorded events, returns the
  * number of bracketed launches and their total duration in milliseconds, and

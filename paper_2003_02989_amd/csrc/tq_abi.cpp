@@ -90,9 +90,14 @@ struct ObsGroupDev {
     DevBuf dchunks, dcbegin, dccount, dclasses, dterms;
     // passes and source of the kernels specialised for the observable set
     // (specialize = 1, every row the same terms, tiles that hold every X mask)
-    std::vector<PauliPass> spec_passes;
-    std::string spec_src;
-    SpecMemo spec_memo;
+    // sets of at most 16 observables, each with passes of its own
+    struct SpecSet {
+        int k0 = 0, kc = 0;  // observables [k0, k0 + kc)
+        std::vector<PauliPass> passes;
+        std::string src;
+        SpecMemo memo;
+    };
+    std::vector<SpecSet> spec_sets;
     // passes and source of the kernels computing phi = g H psi for a single
     // observable the same on every row (specialize = 1)
     std::vector<PauliPass> phi_passes;
@@ -111,6 +116,10 @@ struct ObsGroupDev {
 // kernels are.
 constexpr size_t kMaxPhiTerms = 1024;
 constexpr size_t kMaxSpecTerms = 1024;
+// observables per set of generated expectation passes, and the most terms
+// (over all observables) whose passes are generated
+constexpr int kSpecSetObs = 16;
+constexpr size_t kMaxSpecTermsAll = 4096;
 
 // Tile size of the Pauli kernel (log2 amplitudes): 2048 amplitudes, eight
 // per thread.
@@ -516,24 +525,43 @@ void ensure_obs(tq_program p, const ObsData &od)
             for (auto &td : row) diag = diag && td.x == 0;
         size_t nterms = 0;
         for (auto &row : per_row) nterms = std::max(nterms, row.size());
-        if (!diag && p->pd->opt.specialize && uniform && od.K <= 16 && nterms <= kMaxSpecTerms) {
-            // tiles of 2^12 or 2^13 amplitudes (16 per thread) with runs of
-            // 2^5 or 2^6 contiguous amplitudes: the fewest passes weighted by
-            // what a pass costs (measured on 2^24..2^30 amplitudes: a 2^13
-            // tile streams ~15-20% slower than a 2^12 one, 2^14 tiles and
-            // runs of 2^4 much slower)
-            double best = 0;
-            for (int t = 12; t <= 13 && t < n; t++)
-                for (int c = 6; c >= 5; c--) {
-                    std::vector<PauliPass> pp;
-                    if (!pauli_spec_plan(n, t, c, per_row[0], &pp)) continue;
-                    const double cost = pp.size() * (1.0 + 0.2 * (t - 12)) * (1.0 + 0.05 * (6 - c));
-                    if (og->spec_passes.empty() || cost < best) {
-                        best = cost;
-                        og->spec_passes = std::move(pp);
+        if (!diag && p->pd->opt.specialize && uniform && nterms <= kMaxSpecTermsAll) {
+            // observables in sets of at most 16 (the pass kernels keep one
+            // accumulator per observable in registers), each set's terms in
+            // passes over tiles of 2^12 or 2^13 amplitudes (16 per thread)
+            // with runs of 2^5 or 2^6 contiguous amplitudes: the fewest
+            // passes weighted by what a pass costs (measured on 2^24..2^30
+            // amplitudes: a 2^13 tile streams ~15-20% slower than a 2^12 one,
+            // 2^14 tiles and runs of 2^4 much slower)
+            bool ok = true;
+            for (int k0 = 0; k0 < od.K && ok; k0 += kSpecSetObs) {
+                ObsGroupDev::SpecSet set;
+                set.k0 = k0;
+                set.kc = std::min(kSpecSetObs, od.K - k0);
+                std::vector<TermDev> terms;
+                for (const TermDev &td : per_row[0])
+                    if (td.k >= k0 && td.k < k0 + set.kc) {
+                        terms.push_back(td);
+                        terms.back().k -= k0;
                     }
-                }
-            if (!og->spec_passes.empty()) og->spec_src = pauli_spec_source(og->spec_passes, od.K);
+                if (terms.size() > kMaxSpecTerms) ok = false;
+                double best = 0;
+                for (int t = 12; t <= 13 && t < n && ok; t++)
+                    for (int c = 6; c >= 5; c--) {
+                        std::vector<PauliPass> pp;
+                        if (!pauli_spec_plan(n, t, c, terms, &pp)) continue;
+                        const double cost = pp.size() * (1.0 + 0.2 * (t - 12)) * (1.0 + 0.05 * (6 - c));
+                        if (set.passes.empty() || cost < best) {
+                            best = cost;
+                            set.passes = std::move(pp);
+                        }
+                    }
+                if (set.passes.empty()) ok = false;
+                if (!ok) break;
+                set.src = pauli_spec_source(set.passes, set.kc);
+                og->spec_sets.push_back(std::move(set));
+            }
+            if (!ok) og->spec_sets.clear();
         }
         // (states of at most 12 qubits run resident: their phi is formed on chip)
         if (p->pd->opt.specialize && uniform && od.K == 1 && nterms > 0 && nterms <= kMaxPhiTerms && n > 12) {
@@ -620,38 +648,51 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
     const Group &g = *p->pd->groups[gi];
     ObsGroupDev &og = *p->obs_dev[gi];
     const int nrows = rr.n;
-    const int npass = (int)og.spec_passes.size();
     std::string log;
-    int fit = pauli_spec_slots(og.spec_src, og.spec_passes[0].geom, &log, &og.spec_memo);
-    if (fit <= 0) {
-        if (!log.empty()) fail(TQ_E_DEVICE, log);
-        fit = 2048;
+    // launch shapes of every set first: the partial workspace is sized once
+    // for the largest (no reallocation while an earlier set's work runs)
+    std::vector<int> wg(og.spec_sets.size());
+    size_t need = 1;
+    for (size_t si = 0; si < og.spec_sets.size(); si++) {
+        ObsGroupDev::SpecSet &set = og.spec_sets[si];
+        int fit = pauli_spec_slots(set.src, set.passes[0].geom, &log, &set.memo);
+        if (fit <= 0) {
+            if (!log.empty()) fail(TQ_E_DEVICE, log);
+            fit = 2048;
+        }
+        const int64_t ntiles = (int64_t)1 << (g.n - set.passes[0].geom.t);
+        wg[si] = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
+        need = std::max(need, (size_t)nrows * set.passes.size() * wg[si] * set.kc);
     }
-    const int64_t ntiles = (int64_t)1 << (g.n - og.spec_passes[0].geom.t);
-    PauliSpecArgs a{};
-    a.psi = psi;
-    a.row_stride = (int64_t)1 << g.n;
-    a.rows = rr.ident;
-    a.wg_per_row = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
-    a.npass = npass;
-    a.k_count = K;
-    a.partial = (double *)p->partial.ensure(sizeof(double) * (size_t)nrows * npass * a.wg_per_row * K);
-    for (int pi = 0; pi < npass; pi++) {
-        a.g = og.spec_passes[pi].geom;
-        a.pass = pi;
-        const hipError_t e = launch_pauli_spec(og.spec_src, pi, a, nrows, s, &log, &og.spec_memo);
-        if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
-        hip_check(e, "specialised Pauli launch");
+    double *partial = (double *)p->partial.ensure(sizeof(double) * need);
+    for (size_t si = 0; si < og.spec_sets.size(); si++) {
+        ObsGroupDev::SpecSet &set = og.spec_sets[si];
+        const int npass = (int)set.passes.size();
+        PauliSpecArgs a{};
+        a.psi = psi;
+        a.row_stride = (int64_t)1 << g.n;
+        a.rows = rr.ident;
+        a.wg_per_row = wg[si];
+        a.npass = npass;
+        a.k_count = set.kc;
+        a.partial = partial;
+        for (int pi = 0; pi < npass; pi++) {
+            a.g = set.passes[pi].geom;
+            a.pass = pi;
+            const hipError_t e = launch_pauli_spec(set.src, pi, a, nrows, s, &log, &set.memo);
+            if (e == hipErrorInvalidSource) fail(TQ_E_DEVICE, log);
+            hip_check(e, "specialised Pauli launch");
+        }
+        PauliReduceArgs r{};
+        r.rows = rr.out_rows;
+        r.partial = partial;
+        r.wg_per_row = npass * a.wg_per_row;  // the passes' workgroups side by side
+        r.K = K;
+        r.k_begin = set.k0;
+        r.k_count = set.kc;
+        r.out = out;
+        hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
     }
-    PauliReduceArgs r{};
-    r.rows = rr.out_rows;
-    r.partial = a.partial;
-    r.wg_per_row = npass * a.wg_per_row;  // the passes' workgroups side by side
-    r.K = K;
-    r.k_begin = 0;
-    r.k_count = K;
-    r.out = out;
-    hip_check(launch_pauli_reduce(r, nrows, s), "Pauli reduce launch");
 }
 
 // Run the Pauli kernel over group gi's rows: expectations into out[b, k]
@@ -712,7 +753,7 @@ void pauli_group(tq_program p, size_t gi, const float2 *psi, float2 *phi, const 
         diag_group(p, gi, psi, K, out, s, rr);
         return;
     }
-    if (!phi && !og.spec_passes.empty()) {
+    if (!phi && !og.spec_sets.empty()) {
         spec_pauli_group(p, gi, psi, K, out, s, rr);
         return;
     }
@@ -1928,12 +1969,18 @@ tq_status tq_program_describe(tq_program prog, char *buf, size_t cap, size_t *ne
             if (gi < prog->obs_dev.size()) {
                 const ObsGroupDev &og = *prog->obs_dev[gi];
                 o << ",\"obs\":{\"diag\":" << (og.diag ? 1 : 0);
+                // (expectation passes of every observable set, in order)
+                std::vector<size_t> exp_terms, phi_terms;
+                for (const ObsGroupDev::SpecSet &set : og.spec_sets)
+                    for (const PauliPass &pp : set.passes) exp_terms.push_back(pp.terms.size());
+                for (const PauliPass &pp : og.phi_passes) phi_terms.push_back(pp.terms.size());
                 for (int v = 0; v < 2; v++) {
-                    const std::vector<PauliPass> &pp = v == 0 ? og.spec_passes : og.phi_passes;
+                    const std::vector<size_t> &pt = v == 0 ? exp_terms : phi_terms;
                     o << (v == 0 ? ",\"exp_passes\":[" : ",\"phi_passes\":[");
-                    for (size_t k = 0; k < pp.size(); k++) o << (k ? "," : "") << pp[k].terms.size();
+                    for (size_t k = 0; k < pt.size(); k++) o << (k ? "," : "") << pt[k];
                     o << "]";
                 }
+                o << ",\"exp_sets\":" << og.spec_sets.size();
                 o << "}";
             }
             for (int dir = 0; dir < 2; dir++) {

@@ -185,11 +185,13 @@ def test_specialized_pauli_passes(n, B):
     compare(gpu_outputs(w, want=("exp",), specialize=True), oracle_outputs(w, want=("exp",)))
 
 
-@pytest.mark.parametrize("n,K,max_terms", [(15, 16, 60), (14, 2, 400)])
+@pytest.mark.parametrize("n,K,max_terms", [(15, 16, 60), (14, 2, 400), (14, 45, 8), (13, 200, 1)])
 def test_specialized_pauli_passes_many(n, K, max_terms):
     # the generated expectation passes with their terms in several blocks:
-    # sixteen observables (one accumulator each), and two observables of a few
-    # hundred terms (groups split across blocks)
+    # sixteen observables (one accumulator each), two observables of a few
+    # hundred terms (groups split across blocks), and more than sixteen
+    # observables (sets of sixteen, each with passes of its own; 200
+    # single-term observables as the sampled expectations' term values)
     w = wl.random_batch(5500 + n, B=2, n=n, n_gates=60, n_symbols=4, K=K)
     shared = wl.random_observables(wl.rng_for(5600 + n), n, K, max_terms=max_terms, max_weight=5)
     for b in range(w.B):
@@ -198,8 +200,9 @@ def test_specialized_pauli_passes_many(n, K, max_terms):
     p = tq.Program(w.program_blob(), specialize=True)
     e = tq.expectation(p, dev(w.theta), tq.Observables(w.observable_blob())).cpu().numpy()
     ob = tq.describe(p)["groups"][0]["obs"]
-    say("generated expectation passes (terms per pass)", ob["exp_passes"])
+    say("generated expectation passes (terms per pass)", ob["exp_passes"], "sets", ob["exp_sets"])
     assert sum(ob["exp_passes"]) == sum(len(o) for o in shared)
+    assert ob["exp_sets"] == (K + 15) // 16
     compare({"exp": e}, oracle_outputs(w, want=("exp",)))
 
 
