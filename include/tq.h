@@ -4,7 +4,10 @@
  * The library runs the circuit-execution hot path of TensorFlow Quantum
  * (arXiv:2003.02989) on one AMD Instinct MI355X: batched state-vector
  * simulation of parameterized circuits in complex64, Pauli-sum expectation
- * values, bitstring sampling and adjoint-method gradients.
+ * values, bitstring sampling and adjoint-method gradients; noisy circuits as
+ * trajectories (Pauli channels), expectations estimated from measurement
+ * shots, and parameter-shift and finite-difference gradients as batched
+ * launches.
  *
  * Conventions shared by every call
  * --------------------------------
