@@ -107,6 +107,9 @@ int qubits_of(const Group &g, int gi, int *out)
     return 1;
 }
 
+// Tile-bit swaps the pass scheduler tries per pass (each one places more gates).
+constexpr int kTileSearchSteps = 64;
+
 struct Sched {
     std::vector<int> bits;   // tile bit positions
     std::vector<int> items;  // gate indices in application order
@@ -171,25 +174,66 @@ std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n
             for (int b = n - 1; b >= 0 && used < t; b--)
                 if (!in_tile[b]) in_tile[b] = 1, used++;
         }
-        // phase 3: schedule with the tile fixed
+        // phase 3: schedule with the tile fixed -- every gate in order whose
+        // target bits are in the tile and whose qubits no earlier deferred
+        // gate blocks
+        auto place = [&](const std::vector<char> &tile, std::vector<int> *items, std::vector<int> *deferred,
+                         int *first_deferred) {
+            std::vector<char> blocked(n, 0);
+            int count = 0;
+            *first_deferred = (int)g.gates.size();
+            for (int gi : remaining) {
+                int qs[2], ts[2];
+                int nq = qubits_of(g, gi, qs), nt = targets(g, gi, ts);
+                bool ok = true;
+                for (int j = 0; j < nq; j++) ok &= !blocked[qs[j]];
+                for (int j = 0; j < nt; j++) ok &= tile[pos(ts[j])] != 0;
+                if (ok) {
+                    count++;
+                    if (items) items->push_back(gi);
+                } else {
+                    if (*first_deferred == (int)g.gates.size()) *first_deferred = gi;
+                    if (deferred) deferred->push_back(gi);
+                    for (int j = 0; j < nq; j++) blocked[qs[j]] = 1;
+                }
+            }
+            return count;
+        };
+        // local search over the tile's free bits: swap one in-tile bit above
+        // the low ones for one outside while that places more gates (ties:
+        // the first deferred gate comes later), at most kTileSearchSteps
+        // swaps (the 30-qubit random circuit: 40 -> 29 passes of 2^13)
+        if (cap <= 0) {
+            int fd;
+            int best = place(in_tile, nullptr, nullptr, &fd), best_fd = fd;
+            for (int step = 0; step < kTileSearchSteps; step++) {
+                bool found = false;
+                for (int bi = c; bi < n && !found; bi++) {
+                    if (!in_tile[bi]) continue;
+                    for (int bo = c; bo < n && !found; bo++) {
+                        if (in_tile[bo]) continue;
+                        in_tile[bi] = 0;
+                        in_tile[bo] = 1;
+                        const int cnt = place(in_tile, nullptr, nullptr, &fd);
+                        if (cnt > best || (cnt == best && fd > best_fd)) {
+                            best = cnt;
+                            best_fd = fd;
+                            found = true;
+                        } else {
+                            in_tile[bi] = 1;
+                            in_tile[bo] = 0;
+                        }
+                    }
+                }
+                if (!found) break;
+            }
+        }
         Sched s;
         for (int b = 0; b < n; b++)
             if (in_tile[b]) s.bits.push_back(b);
         std::vector<int> deferred;
-        std::vector<char> blocked(n, 0);
-        for (int gi : remaining) {
-            int qs[2], ts[2];
-            int nq = qubits_of(g, gi, qs), nt = targets(g, gi, ts);
-            bool ok = true;
-            for (int j = 0; j < nq; j++) ok &= !blocked[qs[j]];
-            for (int j = 0; j < nt; j++) ok &= in_tile[pos(ts[j])] != 0;
-            if (ok) {
-                s.items.push_back(gi);
-            } else {
-                deferred.push_back(gi);
-                for (int j = 0; j < nq; j++) blocked[qs[j]] = 1;
-            }
-        }
+        int fd_unused;
+        place(in_tile, &s.items, &deferred, &fd_unused);
         if (s.items.empty()) fail(TQ_E_UNSUPPORTED, "planner made no progress");
         if (cap > 0 && (int)s.items.size() > cap) {
             // keep the first `cap` gates; everything else stays in order
