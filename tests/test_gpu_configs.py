@@ -203,7 +203,7 @@ def test_specialized_passes_configs():
 
 @pytest.mark.parametrize("specialize", [False, True])
 def test_c4_full_against_golden(specialize):
-    # specialize=True is the benchmark's path: 40 generated forward passes
+    # specialize=True is the benchmark's path: 30 generated forward passes
     # over the 2^30-amplitude state (17 fixed bits per 2^13-amplitude tile)
     path = os.path.join(GOLDEN, "c4_n30.npz")
     g = np.load(path)
