@@ -53,6 +53,14 @@ struct BuildArgs {
     int32_t x_period;
     const ShiftDev *x_shift;
     double x_eps;            // symbol moves are dtheta x x_eps
+    // derived rows built from their source row's block: the block's first
+    // x_copy entries are copied from x_src (the source rows' blocks), then
+    // only the tasks task_list[list_begin[m] .. list_begin[m + 1]) of the
+    // row's move m are built again (the first of them the task of phase_out
+    // when the row carries a global phase)
+    const double2 *x_src;
+    int32_t x_copy;
+    const int32_t *list_begin, *task_list;
 };
 
 struct StageBuildArgs {

@@ -30,6 +30,9 @@ size_t pass_lds_bytes(const TileGeom &g, bool product_init, int nmat);
 size_t resident_lds_bytes(int n, int nacc, bool adjoint);
 hipError_t launch_resident(const ResArgs &a, int nrows, hipStream_t s);
 hipError_t launch_build(const BuildArgs &a, int nrows, hipStream_t s);
+// derived rows: the source rows' blocks copied, then the listed tasks of each
+// row's move rebuilt (max_list: the longest list)
+hipError_t launch_build_derived(const BuildArgs &a, int nrows, int max_list, hipStream_t s);
 hipError_t launch_build_stage(const StageBuildArgs &a, int nrows, hipStream_t s);
 hipError_t launch_pass(const PassArgs &a, int nrows, hipStream_t s);
 // Tiles of the Pauli kernel: 2^t amplitudes with t <= kPauliTileMax.

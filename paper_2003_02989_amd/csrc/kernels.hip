@@ -417,6 +417,59 @@ __global__ __launch_bounds__(256) void k_build_mats(BuildArgs a)
     }
 }
 
+// Derived rows of the batched shift rules, one wavefront per row (four rows
+// per workgroup): the source row's matrices (x_copy entries of its block)
+// copied into the derived row's block ...
+__global__ __launch_bounds__(256) void k_copy_source(BuildArgs a, int nrows)
+{
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= nrows) return;
+    const int64_t L = a.x_begin + row;
+    const int src = (int)(L / a.x_period);
+    const double2 *from = a.x_src + (int64_t)src * a.mat_stride;
+    double2 *to = a.mats + (int64_t)row * a.mat_stride;
+    for (int e = lane; e < a.x_copy; e += 64) to[e] = from[e];
+}
+
+// ... then the tasks that read a moved parameter built again, lane by lane;
+// the row's global phase, as in k_build_mats, multiplied into the
+// product-init task that heads the list by the lane that built it.
+__global__ __launch_bounds__(256) void k_build_list(BuildArgs a, int nrows)
+{
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (row >= nrows) return;
+    const int64_t L = a.x_begin + row;
+    const int src = (int)(L / a.x_period);
+    const int m = (int)(L - (int64_t)src * a.x_period);
+    const ShiftDev *shift = a.x_shift + m;
+    const int b = cget(a.rows, src);
+    BuildCtx c{a.members, a.gates, a.slot_sym,
+               a.slot_scale + (a.uniform ? 0 : (int64_t)src * a.n_slots),
+               a.slot_off + (a.uniform ? 0 : (int64_t)src * a.n_slots), a.explicit_mats,
+               a.theta + (int64_t)b * a.S, a.noise_seed, b, shift, a.x_eps};
+    double2 *block = a.mats + (int64_t)row * a.mat_stride;
+    for (int li = a.list_begin[m] + lane; li < a.list_begin[m + 1]; li += 64) {
+        const BuildTask bt = a.tasks[a.task_list[li]];
+        build_task(bt, c, block + bt.out);
+    }
+    if (a.phase_out < 0) return;
+    double ph = 0.0;
+    for (int j = lane; j < a.n_phase; j += 64) {
+        const PhaseTerm pt = a.phase_terms[j];
+        ph += pt.slot >= 0 ? pt.c * slot_value(c, pt.slot) : pt.c;
+    }
+    ph = wave_sum(ph);
+    if (lane == 0) {
+        double sn, co;
+        sc(ph, &sn, &co);
+        double2 *out = block + a.phase_out;
+        for (int i = 0; i < 4; i++) {
+            const double2 v = out[i];
+            out[i] = make_double2(co * v.x - sn * v.y, co * v.y + sn * v.x);
+        }
+    }
+}
+
 __global__ __launch_bounds__(64) void k_build_stage(StageBuildArgs a)
 {
     const int si = blockIdx.x, row = blockIdx.y, j = threadIdx.x;
@@ -1171,6 +1224,16 @@ hipError_t launch_build_stage(const StageBuildArgs &a, int nrows, hipStream_t s)
     if (a.nlist <= 0 || nrows <= 0) return hipSuccess;
     prof::Scope ps("build", s);
     hipLaunchKernelGGL(k_build_stage, dim3(a.nlist, nrows), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_derived(const BuildArgs &a, int nrows, int max_list, hipStream_t s)
+{
+    if (nrows <= 0) return hipSuccess;
+    prof::Scope ps("build", s);
+    const unsigned blocks = (unsigned)((nrows + 3) / 4);
+    if (a.x_copy > 0) hipLaunchKernelGGL(k_copy_source, dim3(blocks), dim3(256), 0, s, a, nrows);
+    if (max_list > 0 || a.phase_out >= 0) hipLaunchKernelGGL(k_build_list, dim3(blocks), dim3(256), 0, s, a, nrows);
     return hipGetLastError();
 }
 

@@ -139,11 +139,14 @@ struct GroupDev {
     // symbol -> pairs; the parameter-shift rows' shot-counter bases
     bool x_ready[2] = {false, false};
     int x_period[2] = {0, 0};
-    DevBuf x_shift[2], x_pair_slot[2], x_pair_coef[2], x_sym_begin[2], x_sym_pairs[2], x_ebase;
+    int x_max_list[2] = {0, 0};  // the longest task list of a move
+    DevBuf x_shift[2], x_pair_slot[2], x_pair_coef[2], x_sym_begin[2], x_sym_pairs[2], x_ebase, x_list_begin[2],
+        x_list[2];
     void release_x()
     {
         for (int k = 0; k < 2; k++)
-            for (DevBuf *b : {&x_shift[k], &x_pair_slot[k], &x_pair_coef[k], &x_sym_begin[k], &x_sym_pairs[k]})
+            for (DevBuf *b : {&x_shift[k], &x_pair_slot[k], &x_pair_coef[k], &x_sym_begin[k], &x_sym_pairs[k],
+                              &x_list_begin[k], &x_list[k]})
                 b->release();
         x_ebase.release();
     }
@@ -311,6 +314,11 @@ struct RunRows {
     int period = 0;                      // 0: the group's own rows
     const ShiftDev *shift = nullptr;
     double eps = 0.0;                    // central differences: the symbol moves are +-eps
+    // derived rows built from their source rows' matrices (x_src): copied,
+    // then only the tasks of each move's list built again
+    const double2 *x_src = nullptr;
+    const int32_t *list_begin = nullptr, *task_list = nullptr;
+    int max_list = 0;
     double2 *mats = nullptr;
     const int32_t *ident = nullptr;      // 0 .. n-1 (state rows of the workspaces)
     const int32_t *out_rows = nullptr;   // output row of each launch row
@@ -360,6 +368,10 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.x_period = rr.period;
     a.x_shift = rr.shift;
     a.x_eps = rr.eps;
+    a.x_src = rr.x_src;
+    a.x_copy = g.fwd_mat_end;
+    a.list_begin = rr.list_begin;
+    a.task_list = rr.task_list;
     // the first qubit's product-init matrix (built by the range's first
     // task) carries the row's global phase
     const bool init = g.n > 0 && begin == g.fwd_tasks.begin && end > begin && !g.phase_terms.empty();
@@ -367,7 +379,13 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.n_phase = (int32_t)g.phase_terms.size();
     a.phase_terms = (const PhaseTerm *)gd.phase_terms.p;
     a.noise_seed = p->noise_seed;
-    hip_check(launch_build(a, rr.n, s), "matrix build launch");
+    if (rr.x_src) {
+        if (begin != g.fwd_tasks.begin || end != g.fwd_tasks.end)
+            fail(TQ_E_INVALID, "derived rows build the forward matrices only");
+        hip_check(launch_build_derived(a, rr.n, rr.max_list, s), "derived matrix build launch");
+    } else {
+        hip_check(launch_build(a, rr.n, s), "matrix build launch");
+    }
     if (begin <= g.fwd_tasks.begin && end >= g.fwd_tasks.end && gd.n_dense > 0) {
         // dense forward stages, from the op matrices just built
         StageBuildArgs sb{};
@@ -1049,6 +1067,9 @@ void expectations_all(tq_program prog, const float *theta, const ObsData &od, fl
 
 // ------------------------------------------------ batched shift rules
 enum ShiftKind { kParamShift = 0, kFiniteDiff = 1 };
+// derived rows copy their source row's matrices (and rebuild only the moved
+// tasks) when the expansion would otherwise build at least this many tasks
+constexpr int64_t kDerivedCopyTasks = (int64_t)1 << 20;
 
 // The derived rows of group gi for one kind: parameter shift, pair p = the
 // p-th symbolic blob parameter moved by +delta (row 2p) and -delta (row
@@ -1102,6 +1123,37 @@ void ensure_x(tq_program p, size_t gi, int kind)
             psym.push_back(sy);
         }
     }
+    // per move the forward build tasks that read a moved parameter (any
+    // member gate with a moved slot, or a slot of the moved symbol), headed
+    // by the first qubit's product-init task when the row carries a global
+    // phase (that task is rebuilt and takes the moved row's phase)
+    std::vector<int32_t> lbegin(1, 0), list;
+    int init_task = -1;
+    for (int ti = g.fwd_tasks.begin; ti < g.fwd_tasks.end; ti++)
+        if (g.n > 0 && g.tasks[ti].out == g.init_mat[0]) init_task = ti;
+    int max_list = 0;
+    for (const ShiftDev &d : sh) {
+        const size_t at = list.size();
+        if (!g.phase_terms.empty() && init_task >= 0) list.push_back(init_task);
+        for (int ti = g.fwd_tasks.begin; ti < g.fwd_tasks.end; ti++) {
+            if (ti == init_task && !g.phase_terms.empty()) continue;
+            const BuildTask &bt = g.tasks[ti];
+            bool moved = false;
+            for (int mi = 0; mi < bt.mem_count && !moved; mi++) {
+                const GateDev &gd0 = g.gates[g.members[bt.mem_begin + mi].gate];
+                for (int j = 0; j < gd0.np && !moved; j++) {
+                    const int sl = gd0.slot0 + j;
+                    moved = sl == d.slot[0] || sl == d.slot[1] || (d.sym >= 0 && g.slot_sym[sl] == d.sym);
+                }
+            }
+            if (moved) list.push_back(ti);
+        }
+        max_list = std::max(max_list, (int)(list.size() - at));
+        lbegin.push_back((int32_t)list.size());
+    }
+    upload(gd.x_list_begin[kind], lbegin);
+    upload(gd.x_list[kind], list);
+    gd.x_max_list[kind] = max_list;
     std::vector<int32_t> begin(S + 1, 0), pairs(psym.size());
     for (int32_t sy : psym) begin[sy + 1]++;
     for (int i = 0; i < S; i++) begin[i + 1] += begin[i];
@@ -1216,6 +1268,12 @@ void shift_grad(tq_program prog, const float *theta, tq_observables obs, const f
         if (total > 0 && K > 0) {
             f = f_all;
             const int chunk = chunks[gi];
+            // large expansions: the source rows' forward matrices, which
+            // every derived row copies before its moved tasks are built again
+            // (small ones build every task, in fewer launches)
+            const bool copy_build =
+                (int64_t)total * (g.fwd_tasks.end - g.fwd_tasks.begin) >= kDerivedCopyTasks;
+            if (copy_build) build_mats(prog, gi, theta, g.fwd_tasks.begin, g.fwd_tasks.end, s, own_rows(prog, gi));
             // per-row observable tables, gathered from the source rows
             const DevBuf *tab_in[kRowGatherArrays] = {&og.begin, &og.count, &og.cbegin, &og.ccount, &og.dcbegin,
                                                       &og.dccount};
@@ -1229,6 +1287,12 @@ void shift_grad(tq_program prog, const float *theta, tq_observables obs, const f
                 rr.period = period;
                 rr.shift = (const ShiftDev *)gd.x_shift[kind].p;
                 rr.eps = eps;
+                if (copy_build) {
+                    rr.x_src = mat_ws(prog) + gd.mat_off;
+                    rr.list_begin = (const int32_t *)gd.x_list_begin[kind].p;
+                    rr.task_list = (const int32_t *)gd.x_list[kind].p;
+                    rr.max_list = gd.x_max_list[kind];
+                }
                 rr.mats = mats;
                 rr.ident = ident;
                 rr.out_rows = ident;
