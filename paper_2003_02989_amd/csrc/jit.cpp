@@ -52,13 +52,15 @@ std::string dbl(double v)
 
 // LDS of a specialised Pauli pass: the tile, its high-bit offsets and the
 // per-wave sums of at most `nk` observables (every pass has at most 16)
-size_t pauli_spec_lds_bytes(const TileGeom &g)
-{
-    // the tile, its high-bit offsets, and per-wave sums of at most 16
-    // observables for at most 16 waves
-    return sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) + sizeof(double) * 16 * 16;
-}
 int pauli_spec_threads(const TileGeom &g) { return 1 << (g.t - 4); }
+size_t pauli_spec_lds_bytes(const TileGeom &g, int K)
+{
+    // the tile, its high-bit offsets, and per-wave sums of the observables
+    // (at least 16 x 16 slots)
+    const size_t waves = (size_t)pauli_spec_threads(g) / 64;
+    return sizeof(float2) * ((size_t)1 << g.t) + sizeof(uint64_t) * ((size_t)1 << g.h) +
+           sizeof(double) * std::max<size_t>(16 * 16, waves * (size_t)K);
+}
 
 uint32_t host_sw(uint32_t i) { return i ^ ((i >> 5) & 31u); }
 
@@ -1113,6 +1115,8 @@ namespace {
 // Terms per block of the expectation passes: one running sum (two VGPRs) per
 // term of the block.
 constexpr int kExpBlock = 16;
+// observables of a generated expectation pass that keep register accumulators
+constexpr int kSpecRegObs = 16;
 
 // <psi|P|psi> of the pass's terms, for up to 16 observables: per thread 16
 // amplitudes (the top four bits of the tile index).  The terms, grouped by
@@ -1123,10 +1127,17 @@ constexpr int kExpBlock = 16;
 // its observable's accumulator with the term's coefficient signed by the
 // thread and tile bits of its Z mask.  A term whose X mask has a register bit
 // visits each pair {l, l^x} once, with twice the coefficient.
-void pauli_exp_pass(std::ostream &o, const PauliPass &pp, int pi)
+// K: the set's observables.  Up to kSpecRegObs of them each keep an fp64
+// accumulator in registers over the tile loop.  Larger sets run one tile per
+// workgroup (the host launches one workgroup per tile) and keep per-wave
+// sums in LDS: each block stores, per observable it touches, the wavefront
+// sum of its terms' contributions in the wave's slot (lane 0; an observable
+// met again in a later block of the pass is added to its slot).
+void pauli_exp_pass(std::ostream &o, const PauliPass &pp, int pi, int K)
 {
     const TileGeom &gm = pp.geom;
     const int t = gm.t, P = 16, tb = t - 4, NT = 1 << tb, NW = NT / 64;
+    const bool lds_acc = K > kSpecRegObs;
     // observables of the pass, and the register accumulator of each
     std::vector<int> ks;
     for (const SpecTerm &tm : pp.terms)
@@ -1202,11 +1213,17 @@ void pauli_exp_pass(std::ostream &o, const PauliPass &pp, int pi)
       << ((1u << gm.c) - 1) << "u, " << gm.c
       << "};\n"
          "    uint32_t tz = (uint32_t)tid;\n";
-    for (int j = 0; j < NK; j++) o << "    double e" << j << " = 0.0;\n";
+    if (lds_acc) {
+        o << "    for (int i_ = tid; i_ < " << NW * K << "; i_ += " << NT << ") red[i_] = 0.0;\n"
+             "    __syncthreads();\n";
+    } else {
+        for (int j = 0; j < NK; j++) o << "    double e" << j << " = 0.0;\n";
+    }
     o << "    for (int64_t tile = w; tile < " << (1ll << (gm.n - t)) << "ll; tile += a.wg_per_row) {\n"
       << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n"
       << "    tile_copy<true>(tc, la, ps, fb, " << (1 << t) << ");\n"
       << "    __syncthreads();\n";
+    std::set<int> seen_k;  // LDS sums: observables already stored in this pass
     auto skipped = [&](uint32_t xT, int r) {
         const uint32_t xhi = xT >> tb;
         const int pivot = xhi ? 31 - __builtin_clz(xhi) : -1;
@@ -1269,21 +1286,77 @@ void pauli_exp_pass(std::ostream &o, const PauliPass &pp, int pi)
         }
         // fold: the coefficient's sign bit flipped by the parity of the
         // thread and tile bits of the term's Z mask
-        for (const Slice &sl : blk)
-            for (size_t j = 0; j < sl.tts.size(); j++) {
-                const TT &tt = *sl.tts[j];
-                const uint64_t m = (uint64_t)tt.zlo | (tt.zt << tb);
-                uint64_t cb;
-                std::memcpy(&cb, &tt.C, sizeof cb);
-                o << "    e" << tt.kk << " = fma(__hiloint2double((int)(" << (uint32_t)(cb >> 32) << "u ^ ";
-                if (!m) o << "zc";
-                else o << "((uint32_t)(__popc(vz & " << m << "u) & 1) << 31)";
-                o << "), (int)(" << (uint32_t)cb << "u ^ zc)), s" << sl.first + (int)j << ", e" << tt.kk << ");\n";
+        auto coef = [&](const TT &tt) {
+            const uint64_t m = (uint64_t)tt.zlo | (tt.zt << tb);
+            uint64_t cb;
+            std::memcpy(&cb, &tt.C, sizeof cb);
+            std::string c = "__hiloint2double((int)(" + std::to_string((uint32_t)(cb >> 32)) + "u ^ ";
+            if (!m) c += "zc";
+            else c += "((uint32_t)(__popc(vz & " + std::to_string(m) + "u) & 1) << 31)";
+            return c + "), (int)(" + std::to_string((uint32_t)cb) + "u ^ zc))";
+        };
+        if (!lds_acc) {
+            for (const Slice &sl : blk)
+                for (size_t j = 0; j < sl.tts.size(); j++) {
+                    const TT &tt = *sl.tts[j];
+                    o << "    e" << tt.kk << " = fma(" << coef(tt) << ", s" << sl.first + (int)j << ", e" << tt.kk
+                      << ");\n";
+                }
+        } else {
+            // per observable of the block (at most 16): its terms'
+            // contributions summed into u_m; then a reduce-scatter over the
+            // lane bits 0..3 (lane l keeps u_{T(l)}, T(l) = 8 l0 + 4 l1 +
+            // 2 l2 + l3, the sum over its 16 lanes) and the two row
+            // exchanges leave the wavefront sum of u_m in lanes l < 16 with
+            // T(l) = m, which store it in (or, met before, add it to) the
+            // wave's slot of that observable
+            std::map<int, std::vector<std::pair<const TT *, int>>> by_k;
+            for (const Slice &sl : blk)
+                for (size_t j = 0; j < sl.tts.size(); j++) by_k[ks[sl.tts[j]->kk]].push_back({sl.tts[j], sl.first + (int)j});
+            std::vector<int> kms;
+            o << "    {\n";
+            for (auto &kv : by_k) {
+                const int m = (int)kms.size();
+                kms.push_back(kv.first);
+                o << "      double u" << m << " = 0.0;\n";
+                for (auto &tj : kv.second) o << "      u" << m << " = fma(" << coef(*tj.first) << ", s" << tj.second << ", u" << m << ");\n";
             }
+            int M = (int)kms.size();  // entries u_0 .. u_{M-1} not known to be zero
+            for (int step = 0, half = 8; step < 4; step++, half /= 2) {
+                const int bitv = 1 << step;
+                auto u = [&](int q) { return q < M ? "u" + std::to_string(q) : std::string("0.0"); };
+                for (int i = 0; i < std::min(M, half); i++)
+                    o << "      { const bool h_ = (lane & " << bitv << ") != 0; const double k_ = h_ ? " << u(i + half)
+                      << " : " << u(i) << ", x_ = h_ ? " << u(i) << " : " << u(i + half) << "; u" << i
+                      << " = k_ + __shfl_xor(x_, " << bitv << ", 64); }\n";
+                M = std::min(M, half);
+            }
+            o << "      u0 += __shfl_xor(u0, 16, 64);\n"
+                 "      u0 += __shfl_xor(u0, 32, 64);\n"
+                 "      const int t_ = ((lane & 1) << 3) | ((lane & 2) << 1) | ((lane >> 1) & 2) | ((lane >> 3) & 1);\n"
+                 "      if (lane < 16) {\n"
+                 "        switch (t_) {\n";
+            for (int m = 0; m < (int)kms.size(); m++) {
+                o << "        case " << m << ": red[wave * " << K << " + " << kms[m] << "] "
+                  << (seen_k.count(kms[m]) ? "+=" : "=") << " u0; break;\n";
+                seen_k.insert(kms[m]);
+            }
+            o << "        default: break;\n        }\n      }\n    }\n";
+        }
         o << "    }\n    __builtin_amdgcn_sched_barrier(0);\n";
     }
     o << "    __syncthreads();\n"
          "    }\n";
+    if (lds_acc) {
+        // the per-wave sums, in wave order
+        o << "    double *out = a.partial + ((int64_t)(row * a.npass + " << pi
+          << ") * a.wg_per_row + w) * a.k_count;\n"
+             "    for (int k = tid; k < a.k_count; k += "
+          << NT << ") {\n        double v = red[k];\n";
+        for (int wv = 1; wv < NW; wv++) o << "        v += red[" << wv * K << " + k];\n";
+        o << "        out[k] = v;\n    }\n}\n";
+        return;
+    }
     // fixed-order reduction: waves, then the wave sums
     for (int j = 0; j < NK; j++)
         o << "    { const double v = wave_sum(e" << j << "); if (lane == 0) red[wave * " << NK << " + " << j << "] = v; }\n";
@@ -1314,8 +1387,7 @@ std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K)
 {
     std::ostringstream o;
     o << kHead;
-    for (size_t pi = 0; pi < passes.size(); pi++) pauli_exp_pass(o, passes[pi], (int)pi);
-    (void)K;
+    for (size_t pi = 0; pi < passes.size(); pi++) pauli_exp_pass(o, passes[pi], (int)pi, K);
     o << "} // namespace tq\n";
     return o.str();
 }
@@ -1662,7 +1734,7 @@ hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a,
     hipFunction_t fn;
     hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_hphi_" + N(pass), &fn, log);
     if (e != hipSuccess) return e;
-    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
+    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g, 16), s, "pauli", pauli_spec_threads(a.g));
 }
 
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
@@ -1673,10 +1745,11 @@ hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecAr
     hipError_t e = memo_kernel(memo, (size_t)pass, (size_t)a.npass, [&] { return src; }, "tq_pauli_" + N(pass), &fn,
                                log);
     if (e != hipSuccess) return e;
-    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g), s, "pauli", pauli_spec_threads(a.g));
+    return launch(fn, a, nrows * a.wg_per_row, pauli_spec_lds_bytes(a.g, a.k_count), s, "pauli",
+                  pauli_spec_threads(a.g));
 }
 
-int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo)
+int pauli_spec_slots(const std::string &src, const TileGeom &g, int K, std::string *log, SpecMemo *memo)
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
@@ -1685,12 +1758,12 @@ int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log
     if (get_kernels(src, {"tq_pauli_0"}, &fn, log) != hipSuccess) return 0;
     int per_cu = 0, cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (pauli_spec_lds_bytes(g) > 65536 &&
+    if (pauli_spec_lds_bytes(g, K) > 65536 &&
         hipFuncSetAttribute(reinterpret_cast<const void *>(fn[0]), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)pauli_spec_lds_bytes(g)) != hipSuccess)
+                            (int)pauli_spec_lds_bytes(g, K)) != hipSuccess)
         return 0;
     if (hipModuleOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn[0], pauli_spec_threads(g),
-                                                           pauli_spec_lds_bytes(g)) != hipSuccess)
+                                                           pauli_spec_lds_bytes(g, K)) != hipSuccess)
         return 0;
     if (memo && memo->dev == dev) memo->slots = per_cu * cus;
     return per_cu * cus;

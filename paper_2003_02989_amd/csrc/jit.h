@@ -53,9 +53,11 @@ hipError_t launch_rev_pass_spec(const Group &g, int pass, const RevArgs &a, int 
                                 std::string *log, SpecMemo *memo);
 
 // Kernels tq_pauli_<pass> computing the expectations of one observable set
-// (the same on every row, at most 16 observables) pass by pass: each pass's
-// tile holds the X bits of its terms; partials go to
-// partial[row][npass][wg_per_row][k_count].
+// of K observables (the same on every row) pass by pass: each pass's tile
+// holds the X bits of its terms; partials go to
+// partial[row][npass][wg_per_row][k_count].  Up to 16 observables keep
+// register accumulators; larger sets per-wave sums in LDS (K doubles per
+// wave).
 std::string pauli_spec_source(const std::vector<PauliPass> &passes, int K);
 hipError_t launch_pauli_spec(const std::string &src, int pass, const PauliSpecArgs &a, int nrows, hipStream_t s,
                              std::string *log, SpecMemo *memo);
@@ -67,7 +69,7 @@ std::string hphi_spec_source(const std::vector<PauliPass> &passes);
 hipError_t launch_hphi_spec(const std::string &src, int pass, const HPhiArgs &a, int nrows, hipStream_t s,
                             std::string *log, SpecMemo *memo);
 // Workgroups of a specialised Pauli pass that fit on the device at once (0 if unknown).
-int pauli_spec_slots(const std::string &src, const TileGeom &g, std::string *log, SpecMemo *memo);
+int pauli_spec_slots(const std::string &src, const TileGeom &g, int K, std::string *log, SpecMemo *memo);
 
 // Compile the specialised kernels of group g (the resident kernel, or the
 // forward and reverse pass kernels) ahead of their first launch: for the current device when

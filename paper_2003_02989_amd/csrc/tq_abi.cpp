@@ -116,9 +116,13 @@ struct ObsGroupDev {
 // kernels are.
 constexpr size_t kMaxPhiTerms = 1024;
 constexpr size_t kMaxSpecTerms = 1024;
-// observables per set of generated expectation passes, and the most terms
-// (over all observables) whose passes are generated
+// observables per set of generated expectation passes: up to 16 keep
+// register accumulators (one set); more are split into sets of up to 200
+// with per-wave sums in LDS (8 waves x 200 doubles beside a 2^13-amplitude
+// tile still leave two workgroups per CU); and the most terms (over all
+// observables) whose passes are generated
 constexpr int kSpecSetObs = 16;
+constexpr int kSpecSetObsLds = 200;
 constexpr size_t kMaxSpecTermsAll = 4096;
 
 // Tile size of the Pauli kernel (log2 amplitudes): 2048 amplitudes, eight
@@ -544,18 +548,19 @@ void ensure_obs(tq_program p, const ObsData &od)
         size_t nterms = 0;
         for (auto &row : per_row) nterms = std::max(nterms, row.size());
         if (!diag && p->pd->opt.specialize && uniform && nterms <= kMaxSpecTermsAll) {
-            // observables in sets of at most 16 (the pass kernels keep one
-            // accumulator per observable in registers), each set's terms in
+            // observables in sets (at most 16 with one register accumulator
+            // each, else up to 200 summed per wave in LDS), each set's terms in
             // passes over tiles of 2^12 or 2^13 amplitudes (16 per thread)
             // with runs of 2^5 or 2^6 contiguous amplitudes: the fewest
             // passes weighted by what a pass costs (measured on 2^24..2^30
             // amplitudes: a 2^13 tile streams ~15-20% slower than a 2^12 one,
             // 2^14 tiles and runs of 2^4 much slower)
             bool ok = true;
-            for (int k0 = 0; k0 < od.K && ok; k0 += kSpecSetObs) {
+            const int per_set = od.K <= kSpecSetObs ? kSpecSetObs : kSpecSetObsLds;
+            for (int k0 = 0; k0 < od.K && ok; k0 += per_set) {
                 ObsGroupDev::SpecSet set;
                 set.k0 = k0;
-                set.kc = std::min(kSpecSetObs, od.K - k0);
+                set.kc = std::min(per_set, od.K - k0);
                 std::vector<TermDev> terms;
                 for (const TermDev &td : per_row[0])
                     if (td.k >= k0 && td.k < k0 + set.kc) {
@@ -673,13 +678,15 @@ void spec_pauli_group(tq_program p, size_t gi, const float2 *psi, int K, float *
     size_t need = 1;
     for (size_t si = 0; si < og.spec_sets.size(); si++) {
         ObsGroupDev::SpecSet &set = og.spec_sets[si];
-        int fit = pauli_spec_slots(set.src, set.passes[0].geom, &log, &set.memo);
+        int fit = pauli_spec_slots(set.src, set.passes[0].geom, set.kc, &log, &set.memo);
         if (fit <= 0) {
             if (!log.empty()) fail(TQ_E_DEVICE, log);
             fit = 2048;
         }
         const int64_t ntiles = (int64_t)1 << (g.n - set.passes[0].geom.t);
-        wg[si] = (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
+        // sets beyond kSpecSetObs observables: one workgroup per tile (their
+        // kernels store per-tile sums)
+        wg[si] = set.kc > kSpecSetObs ? (int)ntiles : (int)std::max<int64_t>(1, std::min<int64_t>(ntiles, fit / nrows));
         need = std::max(need, (size_t)nrows * set.passes.size() * wg[si] * set.kc);
     }
     double *partial = (double *)p->partial.ensure(sizeof(double) * need);

@@ -202,7 +202,7 @@ def test_specialized_pauli_passes_many(n, K, max_terms):
     ob = tq.describe(p)["groups"][0]["obs"]
     say("generated expectation passes (terms per pass)", ob["exp_passes"], "sets", ob["exp_sets"])
     assert sum(ob["exp_passes"]) == sum(len(o) for o in shared)
-    assert ob["exp_sets"] == (K + 15) // 16
+    assert ob["exp_sets"] == (1 if K <= 16 else (K + 199) // 200)
     compare({"exp": e}, oracle_outputs(w, want=("exp",)))
 
 
