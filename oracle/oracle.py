@@ -14,7 +14,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# TQ_ORACLE_LIB: another build of the same source (the sanitizer test loads one)
+_LIB_PATH = os.environ.get("TQ_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _SRC = os.path.join(_HERE, "tq_oracle.c")
 
 

@@ -13,7 +13,8 @@ import struct
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtq.so")
+# TQ_LIB_PATH: another build of the same sources (the sanitizer test loads one)
+LIB_PATH = os.environ.get("TQ_LIB_PATH") or os.path.join(_HERE, "libtq.so")
 
 TQ_OK, TQ_E_INVALID, TQ_E_UNSUPPORTED, TQ_E_NOMEM, TQ_E_DEVICE = range(5)
 _STATUS = {1: "TQ_E_INVALID", 2: "TQ_E_UNSUPPORTED", 3: "TQ_E_NOMEM", 4: "TQ_E_DEVICE"}
