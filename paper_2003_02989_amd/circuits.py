@@ -121,23 +121,34 @@ class Circuit:
         return len(self.gates)
 
 
+def _circuit_bytes(c):
+    out = [struct.pack("<II", c.n, len(c.gates))]
+    for name, qubits, params, matrix in c.gates:
+        code, nq, npar = OPS[name]
+        nq = len(qubits)
+        out.append(struct.pack("<HBB", code, nq, npar))
+        out.append(struct.pack(f"<{nq}I", *qubits))
+        for s, scale, offset in params:
+            out.append(struct.pack("<idd", s, scale, offset))
+        if name == "PAULIEXP":
+            out.append(bytes(PAULI_CODES[p] for p in matrix))
+        if name in ("MATRIX1", "MATRIX2"):
+            d = 2 if name == "MATRIX1" else 4
+            m = np.asarray(matrix, np.complex128).reshape(d, d)
+            out.append(np.stack([m.real.ravel(), m.imag.ravel()], axis=1).astype("<f8").tobytes())
+    return b"".join(out)
+
+
 def program_blob(circuits, n_symbols):
+    # a circuit object repeated in the batch (trajectories, uniform batches)
+    # is encoded once
+    memo = {}
     out = [b"TQP1", struct.pack("<III", 1, len(circuits), int(n_symbols))]
     for c in circuits:
-        out.append(struct.pack("<II", c.n, len(c.gates)))
-        for name, qubits, params, matrix in c.gates:
-            code, nq, npar = OPS[name]
-            nq = len(qubits)
-            out.append(struct.pack("<HBB", code, nq, npar))
-            out.append(struct.pack(f"<{nq}I", *qubits))
-            for s, scale, offset in params:
-                out.append(struct.pack("<idd", s, scale, offset))
-            if name == "PAULIEXP":
-                out.append(bytes(PAULI_CODES[p] for p in matrix))
-            if name in ("MATRIX1", "MATRIX2"):
-                d = 2 if name == "MATRIX1" else 4
-                m = np.asarray(matrix, np.complex128).reshape(d, d)
-                out.append(np.stack([m.real.ravel(), m.imag.ravel()], axis=1).astype("<f8").tobytes())
+        b = memo.get(id(c))
+        if b is None:
+            b = memo[id(c)] = _circuit_bytes(c)
+        out.append(b)
     return b"".join(out)
 
 
@@ -146,13 +157,19 @@ def observable_blob(sums):
     B = len(sums)
     K = len(sums[0]) if B else 0
     out = [b"TQO1", struct.pack("<III", 1, B, K)]
+    memo = {}  # a row object repeated in the batch is encoded once
     for row in sums:
         if len(row) != K:
             raise ValueError("every batch row needs the same number of observables")
-        for terms in row:
-            out.append(struct.pack("<I", len(terms)))
-            for coeff, factors in terms:
-                out.append(struct.pack("<dI", float(coeff), len(factors)))
-                for q, p in factors:
-                    out.append(struct.pack("<IB", int(q), PAULI_CODES[p]))
+        b = memo.get(id(row))
+        if b is None:
+            enc = []
+            for terms in row:
+                enc.append(struct.pack("<I", len(terms)))
+                for coeff, factors in terms:
+                    enc.append(struct.pack("<dI", float(coeff), len(factors)))
+                    for q, p in factors:
+                        enc.append(struct.pack("<IB", int(q), PAULI_CODES[p]))
+            b = memo[id(row)] = b"".join(enc)
+        out.append(b)
     return b"".join(out)

@@ -325,13 +325,15 @@ def with_noise(w, p, R):
     operation, Sec. "Training Models with Noise"), and every row repeated R
     times (rows b R .. b R + R - 1 are the trajectories of circuit b; their
     outputs average with tq_row_mean)."""
-    circuits = []
+    circuits, memo = [], {}
     for c in w.circuits:
-        nc = Circuit(c.n)
-        for g in c.gates:
-            nc.gates.append(g)
-            for q in g[1]:
-                nc.depolarize(q, p)
+        nc = memo.get(id(c))  # one noisy circuit per distinct circuit object
+        if nc is None:
+            nc = memo[id(c)] = Circuit(c.n)
+            for g in c.gates:
+                nc.gates.append(g)
+                for q in g[1]:
+                    nc.depolarize(q, p)
         circuits += [nc] * R
     rep = lambda a: np.repeat(a, R, axis=0)
     return Workload(w.name + f"_noisy{R}", circuits, w.n_symbols, rep(w.theta),

@@ -121,6 +121,41 @@ def test_c5_full_sampled_rows(specialize):
     assert np.abs(g["grad_exp"] - g["exp"]).max() <= 2 * TOL_EXP
 
 
+def test_c5_noisy_full_sampled_rows():
+    # the noisy VQE as benchmarked: depolarizing p = 0.01 after every gate,
+    # 10 trajectories per circuit (40960 rows of 16 qubits), generated
+    # kernels; the oracle draws the same channels for the sampled rows (rows
+    # offset into the full batch)
+    R = 10
+    w = wl.with_noise(wl.c5_vqe(), 0.01, R)
+    seed = 1000
+    say("c5 noisy full n=16 rows", w.B)
+    p = tq.Program(w.program_blob(), specialize=True)
+    tq.set_noise_seed(p, seed)
+    o = tq.Observables(w.observable_blob())
+    th = dev(w.theta)
+    e = tq.expectation(p, th, o).cpu().numpy()
+    ge = torch.empty((w.B, w.K), dtype=torch.float32, device="cuda")
+    g = tq.adjoint_grad(p, th, o, dev(w.upstream), expectations=ge).cpu().numpy()
+    ge = ge.cpu().numpy()
+    orc.set_noise_seed(seed)
+    try:
+        for r in (0, 7, 20479, 40959):
+            orc.set_row_offset(r)
+            ref = oracle_outputs(sub_workload(w, [r]), want=("exp", "grad"))
+            say("  row", r, "exp error", float(np.abs(e[r] - ref["exp"][0]).max()),
+                "grad error", float(np.abs(g[r] - ref["grad"][0]).max()))
+            compare({"exp": e[[r]], "grad": g[[r]], "grad_exp": ge[[r]]}, ref)
+    finally:
+        orc.set_row_offset(0)
+        orc.set_noise_seed(0)
+    # trajectories of one circuit differ (channels applied) and their mean is
+    # what tq_row_mean returns
+    assert np.abs(e[0] - e[1]).max() > 0 or np.abs(e[1] - e[2]).max() > 0
+    m = tq.row_mean(dev(e), R).cpu().numpy()
+    assert np.abs(m - e.reshape(-1, R, w.K).astype(np.float64).mean(1)).max() < 1e-6
+
+
 def _norm2_f64(st):
     # sum |psi|^2 in float64, in chunks (the n = 30 state holds 2^31 floats)
     x = st.reshape(-1).view(torch.float32)

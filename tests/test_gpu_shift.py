@@ -234,6 +234,28 @@ def test_shift_rules_c2_full_sampled_rows():
     assert np.abs(g - ga).max() <= 2 * TOL_GRAD
 
 
+def test_shift_rules_c3_full_sampled_rows():
+    # QAOA at full size as benchmarked: 256 rows x 400 shifted circuits =
+    # 102400 derived rows of 2^20 amplitudes in chunks through the generated
+    # forward passes; the exact gradient of sampled rows from the oracle's
+    # adjoint (the shift rule is exact for these gates), every row against
+    # the library's adjoint gradient
+    w = wl.c3_qaoa()
+    say("c3 full parameter shift, derived rows", w.B * 400)
+    p = tq.Program(w.program_blob(), specialize=True)
+    o = tq.Observables(w.observable_blob())
+    th, up = dev(w.theta), dev(w.upstream)
+    g = tq.param_shift_grad(p, th, o, up).cpu().numpy()
+    rows = [0, 255]
+    sub = sub_workload(w, rows)
+    ref = orc.adjoint_grad(orc.Program(sub.program_blob()), sub.theta.astype(np.float64),
+                           orc.Observables(sub.observable_blob()), sub.upstream.astype(np.float64))
+    say("  max error against the oracle", float(np.abs(g[rows] - ref).max()))
+    assert np.abs(g[rows] - ref).max() <= TOL_GRAD
+    ga = tq.adjoint_grad(p, th, o, up).cpu().numpy()
+    assert np.abs(g - ga).max() <= 2 * TOL_GRAD
+
+
 def test_shift_rules_in_several_launches():
     # 16-qubit rows (512 KiB states): 8192 derived rows per launch, so 70
     # rows x 2 x 60 parameters run in two launches; the oracle checks
