@@ -584,12 +584,15 @@ def sweep(steps, cases="all", specialize=True):
     kernel for n = 24..30 with batches sized so the states span >= 1 GiB (the
     256 MB last-level cache cannot hold them).  A pass time is the difference
     of two programs with max_pass_gates = 1 (every gate its own pass) that
-    differ by G test gates, divided by G.  One JSON line per case."""
+    differ by G test gates (or G fused blocks of gates, max_pass_gates = the
+    block's size), divided by the difference of their pass counts.  One JSON
+    line per case."""
     import numpy as np
     import torch
 
     from paper_2003_02989_amd import tq
     from paper_2003_02989_amd.circuits import Circuit, const, observable_blob, program_blob
+    from paper_2003_02989_amd.workloads import random_unitary
 
     G = 8
     tile = int(os.environ.get("TQ_SWEEP_TILE", "0"))
@@ -611,8 +614,12 @@ def sweep(steps, cases="all", specialize=True):
                           "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
         del src, dst
 
-    def pass_ms(n, B, prefix, gate):
-        times = []
+    def pass_ms(n, B, prefix, gate, block=None):
+        # block: the test gates as a list applied G times, with max_pass_gates
+        # equal to its length, so that each test pass applies one block's
+        # worth of gates on its qubits, fused
+        block = block or [gate]
+        times, passes = [], []
         for with_test in (True, False):
             circuits = []
             for _ in range(B):
@@ -621,10 +628,12 @@ def sweep(steps, cases="all", specialize=True):
                     c.add(*g)
                 if with_test:
                     for _ in range(G):
-                        c.add(*gate)
+                        for g in block:
+                            c.add(*g)
                 circuits.append(c)
-            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=1,
+            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=len(block),
                               specialize=specialize)
+            passes.append(sum(len(g["fwd"]) for g in tq.describe(prog)["groups"]))
             st = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
             tq.simulate_state(prog, None, out=st)
             torch.cuda.synchronize()
@@ -636,7 +645,7 @@ def sweep(steps, cases="all", specialize=True):
             tq.profile_start(None)
             times.append(ms / steps)
             del st, prog
-        return (times[0] - times[1]) / G
+        return (times[0] - times[1]) / (passes[0] - passes[1])
 
     for n in (24, 26, 28, 30):
         B = max(1, (1 << 27) >> n)
@@ -651,8 +660,19 @@ def sweep(steps, cases="all", specialize=True):
                       ("XXPOW", (q(n - 1), q(n - 2)), [const(0.3)])))
         gate_cases.append((f"CNOT control bit {n-1}, target bit 0", [("CZ", (q(n - 1), q(0)))], ("CNOT", (q(n - 1), q(0)))))
         gate_cases.append((f"RZZ on bits {n-1},0 (diagonal)", [("CZ", (q(n - 1), q(0)))], ("RZZ", (q(n - 1), q(0)), [const(0.3)])))
-        for name, prefix, gate in (gate_cases if cases in ("all", "gates") else []):
-            ms = pass_ms(n, B, prefix, gate)
+        # fused k-qubit windows on the top bits: a random unitary on each of
+        # the k qubits and on each neighbouring pair (2k - 1 dense gates, one
+        # pass per block)
+        urng = np.random.default_rng(1000 + n)
+        for k in (2, 3, 4, 5):
+            qs = [q(n - 1 - j) for j in range(k)]
+            blk = [("MATRIX1", qs[j], [], random_unitary(urng, 2)) for j in range(k)]
+            blk += [("MATRIX2", (qs[j], qs[j + 1]), [], random_unitary(urng, 4)) for j in range(k - 1)]
+            gate_cases.append((f"fused k={k} window on bits {n-1}..{n-k} ({2 * k - 1} dense gates)",
+                               [("CZ", (qs[0], qs[1]))], None, blk))
+        for case in (gate_cases if cases in ("all", "gates") else []):
+            name, prefix, gate = case[:3]
+            ms = pass_ms(n, B, prefix, gate, case[3] if len(case) > 3 else None)
             gbs = 16.0 * (1 << n) * B / (ms * 1e-3) / 1e9
             print(json.dumps({"sweep": "gate_pass", "n": n, "batch": B, "case": name, "ms_per_pass": ms,
                               "GB_per_s": gbs, "frac_of_8TBps": gbs / PEAK_HBM_GBS}), flush=True)
