@@ -275,6 +275,8 @@ def main():
     ap.add_argument("--no-specialize", action="store_true",
                     help="run with the precompiled table-driven kernels instead of the ones compiled for the "
                          "circuit structure on the first call")
+    ap.add_argument("--low-qubits", type=int, default=0,
+                    help="contiguous low index bits of every tile (0: the library's default)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the workload step: HBM sweep of single-gate passes and expectation kernels")
@@ -424,7 +426,7 @@ def main():
     tq.lib()
     t_load = time.perf_counter() - t0
     t0 = time.perf_counter()
-    prog = tq.Program(pblob, specialize=specialize)
+    prog = tq.Program(pblob, specialize=specialize, low_qubits=args.low_qubits)
     obs = tq.Observables(oblob)
     t_create = time.perf_counter() - t0
     t0 = time.perf_counter()
@@ -596,6 +598,7 @@ def sweep(steps, cases="all", specialize=True):
 
     G = 8
     tile = int(os.environ.get("TQ_SWEEP_TILE", "0"))
+    low = int(os.environ.get("TQ_SWEEP_LOW", "0"))
 
     # plain device copy of the same footprint: the practical HBM ceiling
     for n in ((26, 30) if cases in ("all", "gates") else ()):
@@ -631,8 +634,8 @@ def sweep(steps, cases="all", specialize=True):
                         for g in block:
                             c.add(*g)
                 circuits.append(c)
-            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, max_pass_gates=len(block),
-                              specialize=specialize)
+            prog = tq.Program(program_blob(circuits, 0), max_tile_qubits=tile, low_qubits=low,
+                              max_pass_gates=len(block), specialize=specialize)
             passes.append(sum(len(g["fwd"]) for g in tq.describe(prog)["groups"]))
             st = torch.empty((B, 1 << n), dtype=torch.complex64, device="cuda")
             tq.simulate_state(prog, None, out=st)

@@ -121,7 +121,8 @@ struct Sched {
 // deferred and blocks its qubits.  The free tile bits are then filled with
 // the targets of the earliest deferred gates and the scan is repeated with
 // the tile fixed, so that the pass takes every gate that became possible.
-std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n, int t, int c, int cap)
+std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n, int t, int c, int cap,
+                            bool earlier_tie)
 {
     std::vector<Sched> out;
     if (n <= t) {
@@ -201,8 +202,8 @@ std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n
         };
         // local search over the tile's free bits: swap one in-tile bit above
         // the low ones for one outside while that places more gates (ties:
-        // the first deferred gate comes later), at most kTileSearchSteps
-        // swaps (the 30-qubit random circuit: 40 -> 29 passes of 2^13)
+        // the first deferred gate comes later, or with earlier_tie earlier),
+        // at most kTileSearchSteps swaps
         if (cap <= 0) {
             int fd;
             int best = place(in_tile, nullptr, nullptr, &fd), best_fd = fd;
@@ -215,7 +216,7 @@ std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n
                         in_tile[bi] = 0;
                         in_tile[bo] = 1;
                         const int cnt = place(in_tile, nullptr, nullptr, &fd);
-                        if (cnt > best || (cnt == best && fd > best_fd)) {
+                        if (cnt > best || (cnt == best && (earlier_tie ? fd < best_fd : fd > best_fd))) {
                             best = cnt;
                             best_fd = fd;
                             found = true;
@@ -248,6 +249,39 @@ std::vector<Sched> schedule(const Group &g, const std::vector<int> &items, int n
         remaining.swap(deferred);
     }
     return out;
+}
+
+// The schedule with the fewest passes of both tie rules of the tile search;
+// and for c >= 6 the same with one low bit fewer forced into every tile, which
+// frees a tile bit for the search (a pass whose tile holds the bit anyway
+// keeps c contiguous low bits, pass_low).  Contiguous runs of 2^5 complex64
+// (256 bytes) stream about as fast as runs of 2^6 (gate passes at 24-30
+// qubits: within 3%), runs of 2^4 lose 8-15%, so c - 1 stops at 5; and it is
+// taken only when it saves at least two passes and a tenth of them, since a
+// heavier pass of fp64-bound ops gains little from a sweep fewer (the
+// 30-qubit random circuit: 29 -> 22 passes).
+std::vector<Sched> schedule_best(const Group &g, const std::vector<int> &items, int n, int t, int c, int cap)
+{
+    auto best_of_ties = [&](int cc) {
+        std::vector<Sched> a = schedule(g, items, n, t, cc, cap, false);
+        std::vector<Sched> b = schedule(g, items, n, t, cc, cap, true);
+        return b.size() < a.size() ? b : a;
+    };
+    std::vector<Sched> best = best_of_ties(c);
+    if (c - 1 >= 5 && n > t) {
+        std::vector<Sched> fewer = best_of_ties(c - 1);
+        const size_t save = std::max<size_t>(2, (best.size() + 9) / 10);
+        if (fewer.size() + save <= best.size()) best = std::move(fewer);
+    }
+    return best;
+}
+
+// Contiguous low bits of a pass: the run of tile bits from bit 0, at most c.
+int pass_low(const std::vector<int> &bits, int c)
+{
+    int k = 0;
+    while (k < c && std::find(bits.begin(), bits.end(), k) != bits.end()) k++;
+    return k;
 }
 
 TileGeom geom_from_bits(int n, int c, const std::vector<int> &bits)
@@ -908,7 +942,7 @@ void plan_group(Group &g, const Options &opt, int S)
     std::vector<int> fitems;
     for (int gi = 0; gi < G; gi++)
         if (!is_absorbed[gi]) fitems.push_back(gi);
-    auto fs = schedule(g, fitems, n, opt.tile, opt.low, opt.max_pass_gates);
+    auto fs = schedule_best(g, fitems, n, opt.tile, opt.low, opt.max_pass_gates);
     if (fs.empty()) {  // nothing beyond the product state: one generating pass
         Sched s;
         for (int b = 0; b < std::min(n, opt.tile); b++) s.bits.push_back(b);
@@ -920,7 +954,7 @@ void plan_group(Group &g, const Options &opt, int S)
     }
     for (size_t pi = 0; pi < fs.size(); pi++) {
         Pass ps;
-        ps.geom = geom_from_bits(n, opt.low, fs[pi].bits);
+        ps.geom = geom_from_bits(n, pass_low(fs[pi].bits, opt.low), fs[pi].bits);
         ps.product_init = pi == 0;
         struct OpB {
             PassOp op;
@@ -1002,7 +1036,8 @@ void plan_group(Group &g, const Options &opt, int S)
     std::vector<int> ritems;
     for (int gi = G - 1; gi >= 0; gi--) ritems.push_back(gi);
     int trev = std::min(opt.tile, 12);
-    auto rs0 = schedule(g, ritems, n, trev, std::min(opt.low, trev - 2), opt.max_pass_gates);
+    const int crev = std::min(opt.low, trev - 2);
+    auto rs0 = schedule_best(g, ritems, n, trev, crev, opt.max_pass_gates);
     // the reverse kernel keeps per-wave accumulators of every gradient slot of
     // a pass in LDS: split passes that would hold too many
     std::vector<Sched> rs;
@@ -1025,7 +1060,7 @@ void plan_group(Group &g, const Options &opt, int S)
     }
     for (auto &s : rs) {
         Pass ps;
-        ps.geom = geom_from_bits(n, std::min(opt.low, trev - 2), s.bits);
+        ps.geom = geom_from_bits(n, pass_low(s.bits, crev), s.bits);
         ps.mat_begin = g.mat_block;
         for (int gi : s.items) {
             int cls = classify(g.gates[gi].op);
