@@ -1037,7 +1037,13 @@ void plan_group(Group &g, const Options &opt, int S)
     for (int gi = G - 1; gi >= 0; gi--) ritems.push_back(gi);
     int trev = std::min(opt.tile, 12);
     const int crev = std::min(opt.low, trev - 2);
-    auto rs0 = schedule_best(g, ritems, n, trev, crev, opt.max_pass_gates);
+    // (a group without symbolic parameters never runs its reverse passes:
+    // one schedule is enough)
+    bool symbolic = false;
+    for (int gi = 0; gi < G && !symbolic; gi++)
+        for (int j = 0; j < g.gates[gi].np; j++) symbolic |= g.slot_sym[g.gates[gi].slot0 + j] >= 0;
+    auto rs0 = symbolic ? schedule_best(g, ritems, n, trev, crev, opt.max_pass_gates)
+                        : schedule(g, ritems, n, trev, crev, opt.max_pass_gates, false);
     // the reverse kernel keeps per-wave accumulators of every gradient slot of
     // a pass in LDS: split passes that would hold too many
     std::vector<Sched> rs;
