@@ -289,7 +289,7 @@ def main():
                     help="only copy a 1 GiB device buffer three times (reference for the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no multi-GPU mode; "
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU mode; "
               "the batch would split across GPUs row-wise and a large state by amplitudes (DESIGN.md)",
               file=sys.stderr)
         sys.exit(1)
