@@ -290,7 +290,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no multi-GPU mode; "
-              "the batch would split across GPUs row-wise and a large state by amplitudes (DESIGN.md)",
+              "the batch would split across GPUs row-wise and a large state by amplitudes",
               file=sys.stderr)
         sys.exit(1)
 
