@@ -32,7 +32,7 @@
  *    methods", Sec. "Finite difference methods");
  *  - bitstring samples drawn from |psi_i|^2 (Sec. "Sampling and Expectation
  *    Values") with the integer fixed-point rule and the SplitMix64 counter
- *    stream fixed in the design doc (the paper leaves both open).
+ *    stream stated at the sampler below (the paper leaves both open).
  *
  * Every step is done gate by gate, on the full 2^n vector, with no fusion,
  * blocking or reordering.  Qubit q of an n-qubit circuit is bit (n-1-q) of an
