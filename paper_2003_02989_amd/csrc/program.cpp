@@ -1282,39 +1282,84 @@ PauliTables pauli_tables(int n, int t, int c, int K, const std::vector<std::vect
     return pt;
 }
 
+// Covers tried besides the greedy one when planning the passes of an
+// observable set (each a greedy fill of the tile bits in a shuffled term
+// order); the plan with the fewest passes is kept.
+constexpr int kCoverTrials = 256;
+
 bool pauli_spec_plan(int n, int t, int c, const std::vector<TermDev> &terms, std::vector<PauliPass> *passes)
 {
     passes->clear();
     const int h = t - c;
     const uint64_t low = (1ull << c) - 1;
-    std::vector<const TermDev *> left;
+    std::vector<uint64_t> xs;  // the terms' X bits above the low ones
     for (const TermDev &td : terms) {
         if (__builtin_popcountll(td.x & ~low) > h) return false;
-        left.push_back(&td);
+        xs.push_back(td.x & ~low);
     }
-    while (!left.empty()) {
-        // grow the set S of high tile bits greedily: each step adds the X
-        // mask that keeps S within h bits and covers the most terms
-        uint64_t S = 0;
-        for (;;) {
-            uint64_t best = 0;
-            size_t best_cov = 0;
-            int best_size = 0;
-            for (const TermDev *td : left) {
-                const uint64_t U = S | (td->x & ~low);
-                if (U == S || __builtin_popcountll(U) > h) continue;
-                size_t cov = 0;
-                for (const TermDev *o : left) cov += ((o->x & ~low) & ~U) == 0;
-                const int size = __builtin_popcountll(U);
-                if (cov > best_cov || (cov == best_cov && size < best_size)) {
-                    best = U;
-                    best_cov = cov;
-                    best_size = size;
+    // greedy: grow the set S of high tile bits one X mask at a time, the one
+    // that keeps S within h bits and covers the most terms left
+    std::vector<uint64_t> cover;
+    {
+        std::vector<uint64_t> left = xs;
+        while (!left.empty()) {
+            uint64_t S = 0;
+            for (;;) {
+                uint64_t best = 0;
+                size_t best_cov = 0;
+                int best_size = 0;
+                for (uint64_t x : left) {
+                    const uint64_t U = S | x;
+                    if (U == S || __builtin_popcountll(U) > h) continue;
+                    size_t cov = 0;
+                    for (uint64_t o : left) cov += (o & ~U) == 0;
+                    const int size = __builtin_popcountll(U);
+                    if (cov > best_cov || (cov == best_cov && size < best_size)) {
+                        best = U;
+                        best_cov = cov;
+                        best_size = size;
+                    }
                 }
+                if (!best) break;
+                S = best;
             }
-            if (!best) break;
-            S = best;
+            cover.push_back(S);
+            std::vector<uint64_t> rest;
+            for (uint64_t x : left)
+                if (x & ~S) rest.push_back(x);
+            left.swap(rest);
         }
+    }
+    // shuffled fills (a fixed counter-based shuffle per trial): keep one
+    // with fewer passes
+    for (int trial = 0; trial < kCoverTrials && cover.size() > 1; trial++) {
+        std::vector<uint64_t> left = xs, cv;
+        uint64_t st = 0x9E3779B97F4A7C15ull * (uint64_t)(trial + 1);
+        while (!left.empty() && cv.size() + 1 < cover.size()) {
+            for (size_t i = left.size(); i > 1; i--) {  // Fisher-Yates with SplitMix64 draws
+                st += 0x9E3779B97F4A7C15ull;
+                uint64_t z = st;
+                z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+                z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+                z ^= z >> 31;
+                std::swap(left[i - 1], left[z % i]);
+            }
+            uint64_t S = 0;
+            for (uint64_t x : left)
+                if (__builtin_popcountll(S | x) <= h) S |= x;
+            cv.push_back(S);
+            std::vector<uint64_t> rest;
+            for (uint64_t x : left)
+                if (x & ~S) rest.push_back(x);
+            left.swap(rest);
+        }
+        if (left.empty() && cv.size() < cover.size()) cover = cv;
+    }
+    // the passes: each tile the low bits, the cover's bits and filler bits;
+    // each term in the first pass whose tile holds its X bits
+    std::vector<const TermDev *> left;
+    for (const TermDev &td : terms) left.push_back(&td);
+    for (uint64_t S : cover) {
         std::vector<int> bits;
         for (int b = 0; b < c; b++) bits.push_back(b);
         for (int b = c; b < n; b++)
@@ -1331,10 +1376,10 @@ bool pauli_spec_plan(int n, int t, int c, const std::vector<TermDev> &terms, std
             else
                 rest.push_back(td);
         }
-        passes->push_back(std::move(ps));
+        if (!ps.terms.empty()) passes->push_back(std::move(ps));
         left.swap(rest);
     }
-    return true;
+    return left.empty();
 }
 
 DiagTables diag_tables(const std::vector<std::vector<TermDev>> &per_row, bool uniform)
