@@ -484,8 +484,12 @@ def main():
     if mode in ("param-shift", "finite-diff"):  # launches are per chunk of derived rows: count them
         launches_per_step = n_launch / args.steps
     avg_ms = dom_ms / max(n_launch, 1)
+    # (the stored counters are per workload: noisy rows, shift-rule expansions
+    # and sampled modes launch other sizes and have entries of their own)
     traffic = measured_traffic(args.config + ("_expectation" if args.expectation_only else "")
-                               + ("_pauli_exp" if args.pauli_exp else ""), dominant)
+                               + ("_pauli_exp" if args.pauli_exp else "")
+                               + (f"_noisy{R}" if noisy else "")
+                               + ("" if mode == "plain" else "_" + mode), dominant)
     per_launch_flops = flops / max(launches_per_step, 1)
     per_launch_bytes = bytes_ / max(launches_per_step, 1)
     hbm = {"bound": "hbm", "achieved": per_launch_bytes / (avg_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBS,
