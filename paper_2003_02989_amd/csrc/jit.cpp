@@ -73,6 +73,12 @@ struct Env {
     // reverse stages: accumulator of gradient slot s is acc[(tid >> 6) * stride + s + shift]
     std::string acc_stride;
     std::string acc_shift;
+    // reverse tile passes with few gradient slots: each thread's partial sum
+    // of slot s stays in register gacc_[s + gshift] over all its tiles (one
+    // wavefront sum per slot at the end of the kernel instead of one per
+    // stage and tile)
+    bool gacc_reg = false;
+    int gshift = 0;
     int nt = kThreads;  // threads of the workgroup
     const Group *grp = nullptr;  // reverse stages: gradients from gate generators where known
     const Group *fgrp = nullptr; // forward stages: constant single-qubit ops written out (const_m1)
@@ -672,11 +678,19 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
         o << "        lp[sb ^ " << off[k] << "u] = down2(v[" << k << "]); lf[sb ^ " << off[k] << "u] = down2(f[" << k
           << "]);\n";
     o << "    }\n";
-    for (auto &gs : grads)
-        o << "    { const double s_ = wave_sum(g[" << gs.first << "]); if ((tid & 63) == 0) acc[(tid >> 6) * "
-          << e.acc_stride << " + " << gs.second << " + " << e.acc_shift << "] += s_; }\n";
+    for (auto &gs : grads) {
+        if (e.gacc_reg)
+            o << "    gacc_[" << gs.second + e.gshift << "] += g[" << gs.first << "];\n";
+        else
+            o << "    { const double s_ = wave_sum(g[" << gs.first << "]); if ((tid & 63) == 0) acc[(tid >> 6) * "
+              << e.acc_stride << " + " << gs.second << " + " << e.acc_shift << "] += s_; }\n";
+    }
     o << "    }\n    __syncthreads();\n";
 }
+
+// Gradient slots of a reverse tile pass that keep per-thread register sums
+// over the workgroup's tiles (two VGPRs each).
+constexpr int kRevRegGrads = 32;
 
 const char kHead[] =
     "namespace tq {\n"
@@ -902,6 +916,8 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
          "    double *acc = c.acc;\n"
          "    const int tid = threadIdx.x;\n";
     if (dio) direct_io_setup(o, gm);
+    const bool greg = gcount > 0 && gcount <= kRevRegGrads;
+    if (greg) o << "    double gacc_[" << gcount << "] = {};\n";
     o << "    for (int64_t tile = c.w; tile < " << (1ll << (gm.n - gm.t)) << "ll; tile += a.wg_per_row) {\n"
       << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n";
     if (dio) {
@@ -919,6 +935,8 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
     // accumulator rows of gcount slots, the pass's first slot at column 0
     Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
     e.grp = &g;
+    e.gacc_reg = greg;
+    e.gshift = -gbase;
     for (const Stage &st : ps.stages) reverse_stage(o, e, ps, st);
     if (dio) {
         o << "    if (a.store) {\n";
@@ -929,8 +947,14 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
         o << "    rev_store(a, c, fb);\n";
     }
     o << "    __syncthreads();\n"
-         "    }\n"
-         "    rev_finish(a, c);\n"
+         "    }\n";
+    if (greg) {
+        for (int i = 0; i < gcount; i++)
+            o << "    { const double s_ = wave_sum(gacc_[" << i << "]); if ((tid & 63) == 0) acc[(tid >> 6) * " << gcount
+              << " + " << i << "] += s_; }\n";
+        o << "    __syncthreads();\n";
+    }
+    o << "    rev_finish(a, c);\n"
          "}\n";
     return o.str();
 }
