@@ -691,6 +691,12 @@ void reverse_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
 // Gradient slots of a reverse tile pass that keep per-thread register sums
 // over the workgroup's tiles (two VGPRs each).
 constexpr int kRevRegGrads = 32;
+// With kRevPrefetch the reverse tile passes load the next tile's psi and phi
+// into registers while the current tile's stages run, as the forward passes
+// do.  Off: the 64 VGPRs it takes leave no room for the register gradient
+// sums, and either way it measured slower (VQE reverse passes 47.5-48.5 ms
+// per step with it, 45.7 ms without it and with the register sums).
+constexpr bool kRevPrefetch = false;
 
 const char kHead[] =
     "namespace tq {\n"
@@ -918,20 +924,39 @@ std::string rev_pass_kernel_source(const Group &g, int pass)
     if (dio) direct_io_setup(o, gm);
     const bool greg = gcount > 0 && gcount <= kRevRegGrads;
     if (greg) o << "    double gacc_[" << gcount << "] = {};\n";
-    o << "    for (int64_t tile = c.w; tile < " << (1ll << (gm.n - gm.t)) << "ll; tile += a.wg_per_row) {\n"
+    const long long NT = 1ll << (gm.n - gm.t);
+    const int K = dio ? 1 << (gm.t - 9) : 0;
+    const bool pre = dio && kRevPrefetch;
+    if (pre) {
+        o << "    float4 xp_[" << K << "], xf_[" << K << "];\n"
+          << "    if (c.w < " << NT << "ll) {\n";
+        const std::string f0 = "pdep64((uint64_t)c.w, " + std::to_string(gm.fixed_mask) + "ull)";
+        direct_load(o, gm, f0, "xp_", "c.sp");
+        direct_load(o, gm, f0, "xf_", "c.sf");
+        o << "    }\n";
+    }
+    o << "    for (int64_t tile = c.w; tile < " << NT << "ll; tile += a.wg_per_row) {\n"
       << "    const uint64_t fb = pdep64((uint64_t)tile, " << gm.fixed_mask << "ull);\n";
-    if (dio) {
-        const int K = 1 << (gm.t - 9);
+    if (pre) {
+        direct_to_lds(o, gm, "xp_", "lp");
+        direct_to_lds(o, gm, "xf_", "lf");
+        o << "    __syncthreads();\n";
+        // the next tile's loads, in flight during this tile's stages
+        o << "    if (tile + a.wg_per_row < " << NT << "ll) {\n"
+          << "    const uint64_t fbn_ = pdep64((uint64_t)(tile + a.wg_per_row), " << gm.fixed_mask << "ull);\n";
+        direct_load(o, gm, "fbn_", "xp_", "c.sp");
+        direct_load(o, gm, "fbn_", "xf_", "c.sf");
+        o << "    }\n";
+    } else if (dio) {
         o << "    { float4 xp_[" << K << "], xf_[" << K << "];\n";
         direct_load(o, gm, "fb", "xp_", "c.sp");
         direct_load(o, gm, "fb", "xf_", "c.sf");
         direct_to_lds(o, gm, "xp_", "lp");
         direct_to_lds(o, gm, "xf_", "lf");
-        o << "    }\n";
+        o << "    }\n    __syncthreads();\n";
     } else {
-        o << "    rev_load(a, c, fb);\n";
+        o << "    rev_load(a, c, fb);\n    __syncthreads();\n";
     }
-    o << "    __syncthreads();\n";
     // accumulator rows of gcount slots, the pass's first slot at column 0
     Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, N(gcount), N(-gbase)};
     e.grp = &g;
