@@ -56,11 +56,17 @@ struct BuildArgs {
     // derived rows built from their source row's block: the block's first
     // x_copy entries are copied from x_src (the source rows' blocks), then
     // only the tasks task_list[list_begin[m] .. list_begin[m + 1]) of the
-    // row's move m are built again (the first of them the task of phase_out
-    // when the row carries a global phase)
+    // row's move m are built again.  When the row carries a global phase,
+    // either the list starts with the task of phase_out (its members have a
+    // moved parameter), which takes the derived row's whole phase, or the
+    // copied phase_out matrix, holding the source row's phase, is multiplied
+    // by the change of the phase terms phase_list[phase_begin[m] ..
+    // phase_begin[m + 1]) (the terms of a moved parameter); phase_full[m]
+    // says which
     const double2 *x_src;
     int32_t x_copy;
     const int32_t *list_begin, *task_list;
+    const int32_t *phase_full, *phase_begin, *phase_list;
 };
 
 struct StageBuildArgs {

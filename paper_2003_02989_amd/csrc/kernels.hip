@@ -431,12 +431,14 @@ __global__ __launch_bounds__(256) void k_copy_source(BuildArgs a, int nrows)
     for (int e = lane; e < a.x_copy; e += 64) to[e] = from[e];
 }
 
-// ... then the tasks that read a moved parameter built again, lane by lane;
-// the row's global phase, as in k_build_mats, multiplied into the
-// product-init task that heads the list by the lane that built it.
+// ... then the tasks that read a moved parameter built again, one thread per
+// row (a move's list holds a task or two); the row's global phase, as in
+// k_build_mats, multiplied into the product-init task when it heads the
+// list, else the change of the moved parameters' phase terms multiplied into
+// the copied product-init matrix.
 __global__ __launch_bounds__(256) void k_build_list(BuildArgs a, int nrows)
 {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int row = blockIdx.x * blockDim.x + threadIdx.x;
     if (row >= nrows) return;
     const int64_t L = a.x_begin + row;
     const int src = (int)(L / a.x_period);
@@ -448,25 +450,32 @@ __global__ __launch_bounds__(256) void k_build_list(BuildArgs a, int nrows)
                a.slot_off + (a.uniform ? 0 : (int64_t)src * a.n_slots), a.explicit_mats,
                a.theta + (int64_t)b * a.S, a.noise_seed, b, shift, a.x_eps};
     double2 *block = a.mats + (int64_t)row * a.mat_stride;
-    for (int li = a.list_begin[m] + lane; li < a.list_begin[m + 1]; li += 64) {
+    for (int li = a.list_begin[m]; li < a.list_begin[m + 1]; li++) {
         const BuildTask bt = a.tasks[a.task_list[li]];
         build_task(bt, c, block + bt.out);
     }
     if (a.phase_out < 0) return;
     double ph = 0.0;
-    for (int j = lane; j < a.n_phase; j += 64) {
-        const PhaseTerm pt = a.phase_terms[j];
-        ph += pt.slot >= 0 ? pt.c * slot_value(c, pt.slot) : pt.c;
-    }
-    ph = wave_sum(ph);
-    if (lane == 0) {
-        double sn, co;
-        sc(ph, &sn, &co);
-        double2 *out = block + a.phase_out;
-        for (int i = 0; i < 4; i++) {
-            const double2 v = out[i];
-            out[i] = make_double2(co * v.x - sn * v.y, co * v.y + sn * v.x);
+    if (a.phase_full[m]) {
+        for (int j = 0; j < a.n_phase; j++) {
+            const PhaseTerm pt = a.phase_terms[j];
+            ph += pt.slot >= 0 ? pt.c * slot_value(c, pt.slot) : pt.c;
         }
+    } else {
+        if (a.phase_begin[m] == a.phase_begin[m + 1]) return;
+        BuildCtx c0 = c;
+        c0.shift = nullptr;
+        for (int j = a.phase_begin[m]; j < a.phase_begin[m + 1]; j++) {
+            const PhaseTerm pt = a.phase_terms[a.phase_list[j]];
+            ph += pt.c * (slot_value(c, pt.slot) - slot_value(c0, pt.slot));
+        }
+    }
+    double sn, co;
+    sc(ph, &sn, &co);
+    double2 *out = block + a.phase_out;
+    for (int i = 0; i < 4; i++) {
+        const double2 v = out[i];
+        out[i] = make_double2(co * v.x - sn * v.y, co * v.y + sn * v.x);
     }
 }
 
@@ -1233,7 +1242,8 @@ hipError_t launch_build_derived(const BuildArgs &a, int nrows, int max_list, hip
     prof::Scope ps("build", s);
     const unsigned blocks = (unsigned)((nrows + 3) / 4);
     if (a.x_copy > 0) hipLaunchKernelGGL(k_copy_source, dim3(blocks), dim3(256), 0, s, a, nrows);
-    if (max_list > 0 || a.phase_out >= 0) hipLaunchKernelGGL(k_build_list, dim3(blocks), dim3(256), 0, s, a, nrows);
+    if (max_list > 0 || a.phase_out >= 0)
+        hipLaunchKernelGGL(k_build_list, dim3((unsigned)((nrows + 255) / 256)), dim3(256), 0, s, a, nrows);
     return hipGetLastError();
 }
 

@@ -145,12 +145,12 @@ struct GroupDev {
     int x_period[2] = {0, 0};
     int x_max_list[2] = {0, 0};  // the longest task list of a move
     DevBuf x_shift[2], x_pair_slot[2], x_pair_coef[2], x_sym_begin[2], x_sym_pairs[2], x_ebase, x_list_begin[2],
-        x_list[2];
+        x_list[2], x_phase_full[2], x_phase_begin[2], x_phase_list[2];
     void release_x()
     {
         for (int k = 0; k < 2; k++)
             for (DevBuf *b : {&x_shift[k], &x_pair_slot[k], &x_pair_coef[k], &x_sym_begin[k], &x_sym_pairs[k],
-                              &x_list_begin[k], &x_list[k]})
+                              &x_list_begin[k], &x_list[k], &x_phase_full[k], &x_phase_begin[k], &x_phase_list[k]})
                 b->release();
         x_ebase.release();
     }
@@ -322,6 +322,7 @@ struct RunRows {
     // then only the tasks of each move's list built again
     const double2 *x_src = nullptr;
     const int32_t *list_begin = nullptr, *task_list = nullptr;
+    const int32_t *phase_full = nullptr, *phase_begin = nullptr, *phase_list = nullptr;
     int max_list = 0;
     double2 *mats = nullptr;
     const int32_t *ident = nullptr;      // 0 .. n-1 (state rows of the workspaces)
@@ -376,6 +377,9 @@ void build_mats(tq_program p, size_t gi, const float *theta, int begin, int end,
     a.x_copy = g.fwd_mat_end;
     a.list_begin = rr.list_begin;
     a.task_list = rr.task_list;
+    a.phase_full = rr.phase_full;
+    a.phase_begin = rr.phase_begin;
+    a.phase_list = rr.phase_list;
     // the first qubit's product-init matrix (built by the range's first
     // task) carries the row's global phase
     const bool init = g.n > 0 && begin == g.fwd_tasks.begin && end > begin && !g.phase_terms.empty();
@@ -1131,35 +1135,47 @@ void ensure_x(tq_program p, size_t gi, int kind)
         }
     }
     // per move the forward build tasks that read a moved parameter (any
-    // member gate with a moved slot, or a slot of the moved symbol), headed
-    // by the first qubit's product-init task when the row carries a global
-    // phase (that task is rebuilt and takes the moved row's phase)
-    std::vector<int32_t> lbegin(1, 0), list;
+    // member gate with a moved slot, or a slot of the moved symbol).  When
+    // the row carries a global phase: if the first qubit's product-init task
+    // is among them it heads the list and takes the moved row's whole phase;
+    // else its copied matrix keeps the source row's phase times the change
+    // of the phase terms of the moved parameters (listed per move)
+    auto slot_moved = [&](const ShiftDev &d, int sl) {
+        return sl >= 0 && (sl == d.slot[0] || sl == d.slot[1] || (d.sym >= 0 && g.slot_sym[sl] == d.sym));
+    };
+    auto task_moved = [&](const ShiftDev &d, int ti) {
+        const BuildTask &bt = g.tasks[ti];
+        for (int mi = 0; mi < bt.mem_count; mi++) {
+            const GateDev &gd0 = g.gates[g.members[bt.mem_begin + mi].gate];
+            for (int j = 0; j < gd0.np; j++)
+                if (slot_moved(d, gd0.slot0 + j)) return true;
+        }
+        return false;
+    };
+    std::vector<int32_t> lbegin(1, 0), list, pfull, pbegin(1, 0), plist;
     int init_task = -1;
     for (int ti = g.fwd_tasks.begin; ti < g.fwd_tasks.end; ti++)
         if (g.n > 0 && g.tasks[ti].out == g.init_mat[0]) init_task = ti;
     int max_list = 0;
     for (const ShiftDev &d : sh) {
         const size_t at = list.size();
-        if (!g.phase_terms.empty() && init_task >= 0) list.push_back(init_task);
-        for (int ti = g.fwd_tasks.begin; ti < g.fwd_tasks.end; ti++) {
-            if (ti == init_task && !g.phase_terms.empty()) continue;
-            const BuildTask &bt = g.tasks[ti];
-            bool moved = false;
-            for (int mi = 0; mi < bt.mem_count && !moved; mi++) {
-                const GateDev &gd0 = g.gates[g.members[bt.mem_begin + mi].gate];
-                for (int j = 0; j < gd0.np && !moved; j++) {
-                    const int sl = gd0.slot0 + j;
-                    moved = sl == d.slot[0] || sl == d.slot[1] || (d.sym >= 0 && g.slot_sym[sl] == d.sym);
-                }
-            }
-            if (moved) list.push_back(ti);
-        }
+        const bool full = !g.phase_terms.empty() && init_task >= 0 && task_moved(d, init_task);
+        if (full) list.push_back(init_task);
+        for (int ti = g.fwd_tasks.begin; ti < g.fwd_tasks.end; ti++)
+            if (!(full && ti == init_task) && task_moved(d, ti)) list.push_back(ti);
         max_list = std::max(max_list, (int)(list.size() - at));
         lbegin.push_back((int32_t)list.size());
+        pfull.push_back(full ? 1 : 0);
+        if (!full)
+            for (size_t j = 0; j < g.phase_terms.size(); j++)
+                if (slot_moved(d, g.phase_terms[j].slot)) plist.push_back((int32_t)j);
+        pbegin.push_back((int32_t)plist.size());
     }
     upload(gd.x_list_begin[kind], lbegin);
     upload(gd.x_list[kind], list);
+    upload(gd.x_phase_full[kind], pfull);
+    upload(gd.x_phase_begin[kind], pbegin);
+    upload(gd.x_phase_list[kind], plist);
     gd.x_max_list[kind] = max_list;
     std::vector<int32_t> begin(S + 1, 0), pairs(psym.size());
     for (int32_t sy : psym) begin[sy + 1]++;
@@ -1298,6 +1314,9 @@ void shift_grad(tq_program prog, const float *theta, tq_observables obs, const f
                     rr.x_src = mat_ws(prog) + gd.mat_off;
                     rr.list_begin = (const int32_t *)gd.x_list_begin[kind].p;
                     rr.task_list = (const int32_t *)gd.x_list[kind].p;
+                    rr.phase_full = (const int32_t *)gd.x_phase_full[kind].p;
+                    rr.phase_begin = (const int32_t *)gd.x_phase_begin[kind].p;
+                    rr.phase_list = (const int32_t *)gd.x_phase_list[kind].p;
                     rr.max_list = gd.x_max_list[kind];
                 }
                 rr.mats = mats;
