@@ -52,3 +52,18 @@ def test_structure_dedupe_keeps_per_row_constants():
     assert len(d["groups"]) == 1 and d["groups"][0]["rows"] == 8 and d["groups"][0]["uniform_slots"] == 0
     d = tq.describe(tq.Program(wl.c5_vqe(B=8, n=6, layers=2, n_terms=5).program_blob()))
     assert d["groups"][0]["uniform_slots"] == 1
+
+
+def test_scheduler_variants():
+    # the 30-qubit random circuit: the best of the schedule variants (both
+    # tie rules, five or six low bits forced into the tiles) takes 22 forward
+    # passes instead of 30, its tiles holding five or six contiguous low bits
+    d = check_plan(wl.c4_random(n_shots=1), specialize=True)
+    g = d["groups"][0]
+    assert len(g["fwd"]) <= 22
+    assert all(ps["c"] in (5, 6) for ps in g["fwd"]) and any(ps["c"] == 5 for ps in g["fwd"])
+    # the VQE ansatz would save one pass of 15 with five low bits: too little,
+    # it keeps six
+    d = check_plan(wl.c5_vqe(B=2), specialize=True)
+    g = d["groups"][0]
+    assert len(g["fwd"]) == 15 and all(ps["c"] == 6 for ps in g["fwd"])
