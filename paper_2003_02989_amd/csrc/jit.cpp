@@ -79,6 +79,10 @@ struct Env {
     // stage and tile)
     bool gacc_reg = false;
     int gshift = 0;
+    // forward tile passes: the phase classes of the pass's diagonal runs, in
+    // the order the stages meet them (see cut_classes), and the next to use
+    const std::vector<struct CutClass> *cuts = nullptr;
+    mutable size_t cut_next = 0;
     int nt = kThreads;  // threads of the workgroup
     const Group *grp = nullptr;  // reverse stages: gradients from gate generators where known
     const Group *fgrp = nullptr; // forward stages: constant single-qubit ops written out (const_m1)
@@ -331,6 +335,130 @@ std::string diag_entry(const Env &e, const PassOp &op, int mat, int k)
            "))";
 }
 
+// Phase classes.  ZZ-type diagonal ops (a single RZZ or ZZ^t gate each:
+// diag(1, w, w, 1) once the left-out global phase is removed) that share
+// their parameter expression (opcode, symbol, scale, offset: the same w in a
+// row) multiply amplitude i by w^c(i), c(i) the number of the ops whose two
+// bits differ in i -- a QAOA layer's 30 edges are one class, c(i) its cut
+// size.  A class of at least kCutMin ops of a diagonal run is applied as one
+// lookup of w^c in a table of powers (LDS, built once per workgroup) and one
+// complex multiply per amplitude; c is summed from the item's bits once per
+// item plus, per register, the class's bits in the stage.  The derived rows
+// of the shift rules move single parameters, so that a class's members may
+// differ there: their launches take a variant of the pass (tq_fwx_<pass>,
+// compiled when first needed) that applies every op on its own.
+constexpr int kCutMin = 3;
+struct CutClass {
+    std::vector<const PassOp *> ops;
+    int rep = 0;  // pass-relative matrix offset of one member (its entry 1 is w)
+    int tab = 0;  // offset of its powers w^0 .. w^ops.size() in the table
+};
+bool cut_key(const Group &g, const PassOp &op, std::tuple<int, int, double, double> *key)
+{
+    if (op.kind != K_D2 || (op.hint & 0xf) != 9) return false;
+    if (!g.uniform_slots && g.rows.size() > 1) return false;
+    const BuildTask *bt = nullptr;
+    for (int k = g.fwd_tasks.begin; k < g.fwd_tasks.end && !bt; k++)
+        if (g.tasks[k].out == op.mat && g.tasks[k].kind == BT_PRODUCT) bt = &g.tasks[k];
+    if (!bt || bt->mem_count != 1 || bt->diag != 1 || bt->dim != 4) return false;
+    const Member &mb = g.members[bt->mem_begin];
+    const GateDev &gd = g.gates[mb.gate];
+    if ((gd.op != OP_RZZ && gd.op != OP_ZZPOW) || mb.form != FORM_FULL || gd.np != 1) return false;
+    const int sl = gd.slot0;
+    *key = std::make_tuple((int)gd.op, (int)g.slot_sym[sl], g.slot_scale[sl], g.slot_off[sl]);
+    return true;
+}
+// Splits a diagonal run into its phase classes of at least kCutMin ops (in
+// order of first appearance) and the ops left over.
+void split_run(const Group *g, const std::vector<const PassOp *> &run, std::vector<CutClass> *classes,
+               std::vector<const PassOp *> *rest)
+{
+    std::map<std::tuple<int, int, double, double>, std::vector<const PassOp *>> by;
+    std::vector<std::tuple<int, int, double, double>> order;
+    std::vector<char> keyed(run.size(), 0);
+    for (size_t i = 0; g && i < run.size(); i++) {
+        std::tuple<int, int, double, double> k;
+        if (!cut_key(*g, *run[i], &k)) continue;
+        if (!by.count(k)) order.push_back(k);
+        by[k].push_back(run[i]);
+        keyed[i] = 1;
+    }
+    std::set<const PassOp *> taken;
+    for (auto &k : order)
+        if ((int)by[k].size() >= kCutMin) {
+            CutClass c;
+            c.ops = by[k];
+            classes->push_back(c);
+            for (const PassOp *op : c.ops) taken.insert(op);
+        }
+    for (const PassOp *op : run)
+        if (!taken.count(op)) rest->push_back(op);
+}
+// The phase classes of a forward pass's stages, in emission order, with
+// their table offsets; total table entries in *ntab.
+std::vector<CutClass> cut_classes(const Group &g, const Pass &ps, int *ntab)
+{
+    std::vector<CutClass> all;
+    *ntab = 0;
+    for (const Stage &st : ps.stages) {
+        if (st.dense) continue;
+        for (int oi = st.op_begin; oi < st.op_end; oi++) {
+            if (!is_diag(ps.ops[oi - ps.op_offset])) continue;
+            std::vector<const PassOp *> run;
+            int oe = oi;
+            for (; oe < st.op_end && is_diag(ps.ops[oe - ps.op_offset]); oe++) run.push_back(&ps.ops[oe - ps.op_offset]);
+            std::vector<CutClass> cls;
+            std::vector<const PassOp *> rest;
+            split_run(&g, run, &cls, &rest);
+            for (CutClass &c : cls) {
+                c.rep = c.ops[0]->mat - ps.mat_begin;
+                c.tab = *ntab;
+                *ntab += (int)c.ops.size() + 1;
+                all.push_back(c);
+            }
+            oi = oe - 1;
+        }
+    }
+    return all;
+}
+// The code applying phase class c on the registers v of a stage of R bits.
+std::string cut_apply(const Env &e, const CutClass &c, int R)
+{
+    const int NR = 1 << R;
+    std::ostringstream o;
+    o << "{ uint32_t q_ = 0u";
+    std::vector<std::pair<int, std::string>> mixed;  // (register bit, item bit expression)
+    std::vector<int> stat(NR, 0);
+    for (const PassOp *op : c.ops) {
+        const bool r0 = op->s0 != kFixed, r1 = op->s1 != kFixed;
+        if (!r0 && !r1)
+            o << " + (" << bit(e, op->l0, op->p0) << " ^ " << bit(e, op->l1, op->p1) << ")";
+        else if (r0 && r1) {
+            for (int k = 0; k < NR; k++) stat[k] += ((k >> op->s0) ^ (k >> op->s1)) & 1;
+        } else {
+            mixed.emplace_back(r0 ? op->s0 : op->s1, r0 ? bit(e, op->l1, op->p1) : bit(e, op->l0, op->p0));
+        }
+    }
+    o << ";";
+    for (size_t j = 0; j < mixed.size(); j++) o << " const uint32_t m" << j << "_ = " << mixed[j].second << ";";
+    for (int k = 0; k < NR; k++) {
+        std::ostringstream cnt;
+        int cst = stat[k];
+        cnt << "q_";
+        for (size_t j = 0; j < mixed.size(); j++) {
+            if ((k >> mixed[j].first) & 1) {
+                cst += 1;
+                cnt << " - m" << j << "_";
+            } else {
+                cnt << " + m" << j << "_";
+            }
+        }
+        o << " v[" << k << "] = zmul(cutw_[" << c.tab + cst << "u + " << cnt.str() << "], v[" << k << "]);";
+    }
+    o << " }";
+    return o.str();
+}
+
 // A run of consecutive diagonal ops of a stage as one diagonal: its entries
 // are multiplied together over the register bits the run touches (per item,
 // with the out-of-stage bits), then each register of the arrays `arrs` is
@@ -556,6 +684,23 @@ void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
                 int oe = oi;
                 for (; oe < st.op_end && is_diag(ps.ops[oe - ps.op_offset]); oe++)
                     run.push_back(&ps.ops[oe - ps.op_offset]);
+                if (e.cuts) {
+                    // phase classes first (diagonal ops commute), then the rest
+                    std::vector<CutClass> cls;
+                    std::vector<const PassOp *> rest;
+                    split_run(e.fgrp, run, &cls, &rest);
+                    if (!cls.empty()) {
+                        for (size_t ci = 0; ci < cls.size(); ci++)
+                            o << "        " << cut_apply(e, (*e.cuts)[e.cut_next++], R) << "\n";
+                        const std::string c = rest.size() > 1 ? diag_run(e, rest, R, {"v"}) : "";
+                        if (!c.empty())
+                            o << "        " << c << "\n";
+                        else
+                            for (const PassOp *ro : rest) o << "        " << apply(e, *ro, R, ro->mat - e.mbase, "v") << "\n";
+                        oi = oe - 1;
+                        continue;
+                    }
+                }
                 const std::string c = run.size() > 1 ? diag_run(e, run, R, {"v"}) : "";
                 if (!c.empty()) {
                     o << "        " << c << "\n";
@@ -700,7 +845,9 @@ constexpr bool kRevPrefetch = false;
 
 const char kHead[] =
     "namespace tq {\n"
-    "__device__ __forceinline__ double2 zsel(uint32_t c, double2 a, double2 b) { return c ? b : a; }\n";
+    "__device__ __forceinline__ double2 zsel(uint32_t c, double2 a, double2 b) { return c ? b : a; }\n"
+    "__device__ __forceinline__ double2 zpow(double2 w, uint32_t n)\n"
+    "{ double2 r = make_double2(1.0, 0.0); while (n) { if (n & 1u) r = zmul(r, w); w = zmul(w, w); n >>= 1; } return r; }\n";
 
 } // namespace
 
@@ -830,7 +977,7 @@ void direct_store(std::ostream &o, const TileGeom &gm, const std::string &fb, co
 
 } // namespace
 
-std::string pass_kernel_source(const Group &g, int pass)
+std::string pass_kernel_source(const Group &g, int pass, bool exact)
 {
     std::ostringstream o;
     const Pass &ps = g.fwd[pass];
@@ -844,7 +991,7 @@ std::string pass_kernel_source(const Group &g, int pass)
     int maxr = 0;
     for (const Stage &st : ps.stages) maxr = std::max(maxr, (int)st.r);
     const int minwg = maxr >= 4 ? 2 : pre ? 3 : 4;
-    o << "extern \"C\" __global__ __launch_bounds__(256, " << minwg << ") void tq_fwd_" << pass
+    o << "extern \"C\" __global__ __launch_bounds__(256, " << minwg << ") void " << (exact ? "tq_fwx_" : "tq_fwd_") << pass
       << "(PassArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    const PassCtx c = pass_setup(a, smem);\n"
@@ -856,6 +1003,17 @@ std::string pass_kernel_source(const Group &g, int pass)
          "    const int tid = threadIdx.x;\n";
     Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
     e.fgrp = &g;
+    int ntab = 0;
+    const std::vector<CutClass> cuts = exact ? std::vector<CutClass>() : cut_classes(g, ps, &ntab);
+    if (!cuts.empty()) {
+        // the powers w^0 .. w^m of each phase class, once per workgroup
+        e.cuts = &cuts;
+        o << "    __shared__ double2 cutw_[" << ntab << "];\n";
+        for (const CutClass &c : cuts)
+            o << "    if (tid <= " << c.ops.size() << ") cutw_[" << c.tab << " + tid] = zpow(M[" << c.rep
+              << " + 1], (uint32_t)tid);\n";
+        o << "    __syncthreads();\n";
+    }
     const std::string scale = pass_scale(e, ps);
     auto stages = [&]() {
         for (size_t si = 0; si < ps.stages.size(); si++)
@@ -1672,7 +1830,22 @@ std::string pass_chunk(const Group &g, int chunk)
     const int c = rev ? chunk - nf : chunk;
     const int np = rev ? (int)g.rev.size() : (int)g.fwd.size();
     for (int pi = c * kChunkPasses; pi < std::min(np, (c + 1) * kChunkPasses); pi++)
-        body += rev ? rev_pass_kernel_source(g, pi) : pass_kernel_source(g, pi);
+        body += rev ? rev_pass_kernel_source(g, pi) : pass_kernel_source(g, pi, false);
+    return body + "} // namespace tq\n";
+}
+
+// The op-by-op variants (tq_fwx_<pass>) of the forward passes of a chunk
+// that have phase classes.
+bool pass_has_cuts(const Group &g, int pass)
+{
+    int ntab = 0;
+    return !cut_classes(g, g.fwd[pass], &ntab).empty();
+}
+std::string exact_chunk(const Group &g, int chunk)
+{
+    std::string body = kHead;
+    for (int pi = chunk * kChunkPasses; pi < std::min((int)g.fwd.size(), (chunk + 1) * kChunkPasses); pi++)
+        if (pass_has_cuts(g, pi)) body += pass_kernel_source(g, pi, true);
     return body + "} // namespace tq\n";
 }
 
@@ -1729,13 +1902,22 @@ hipError_t memo_kernel(SpecMemo *memo, size_t slot, size_t nslots, Src &&src, co
 
 // Forward or reverse pass kernel `pass` of group g: on the first request on
 // a device every chunk of the group is compiled (in parallel) and loaded.
-hipError_t pass_kernel(const Group &g, bool rev, int pass, hipFunction_t *fn, std::string *log, SpecMemo *memo)
+// exact: the pass's op-by-op variant (slots after the reverse passes; its
+// chunk is compiled when first asked for).
+hipError_t pass_kernel(const Group &g, bool rev, int pass, hipFunction_t *fn, std::string *log, SpecMemo *memo,
+                       bool exact = false)
 {
-    const size_t slot = (rev ? g.fwd.size() : 0) + (size_t)pass, nslots = g.fwd.size() + g.rev.size();
+    const size_t nslots = 2 * g.fwd.size() + g.rev.size();
+    const size_t slot = exact ? g.fwd.size() + g.rev.size() + (size_t)pass : (rev ? g.fwd.size() : 0) + (size_t)pass;
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    if (!(memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot])) {
+    const bool known = memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot];
+    if (exact) {
+        const int chunk = pass / kChunkPasses;
+        return memo_kernel(memo, slot, nslots, [&] { return exact_chunk(g, chunk); }, "tq_fwx_" + N(pass), fn, log);
+    }
+    if (!known) {
         e = load_all(pass_chunks(g), log);
         if (e != hipSuccess) return e;
     }
@@ -1761,7 +1943,14 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
 {
     if (nrows <= 0) return hipSuccess;
     hipFunction_t fn;
-    hipError_t e = pass_kernel(g, false, pass, &fn, log, memo);
+    bool exact = false;
+    if (a.op_by_op) {
+        // whether the pass has phase classes, asked once per pass
+        if (memo && memo->cuts.size() != g.fwd.size()) memo->cuts.assign(g.fwd.size(), -1);
+        if (memo && memo->cuts[pass] < 0) memo->cuts[pass] = pass_has_cuts(g, pass) ? 1 : 0;
+        exact = memo ? memo->cuts[pass] == 1 : pass_has_cuts(g, pass);
+    }
+    hipError_t e = pass_kernel(g, false, pass, &fn, log, memo, exact);
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");
