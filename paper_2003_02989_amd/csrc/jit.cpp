@@ -1010,8 +1010,8 @@ std::string pass_kernel_source(const Group &g, int pass, bool exact)
         e.cuts = &cuts;
         o << "    __shared__ double2 cutw_[" << ntab << "];\n";
         for (const CutClass &c : cuts)
-            o << "    if (tid <= " << c.ops.size() << ") cutw_[" << c.tab << " + tid] = zpow(M[" << c.rep
-              << " + 1], (uint32_t)tid);\n";
+            o << "    for (int j_ = tid; j_ <= " << c.ops.size() << "; j_ += 256) cutw_[" << c.tab << " + j_] = zpow(M["
+              << c.rep << " + 1], (uint32_t)j_);\n";
         o << "    __syncthreads();\n";
     }
     const std::string scale = pass_scale(e, ps);

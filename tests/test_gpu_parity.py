@@ -349,3 +349,47 @@ def test_noisy_trajectories(n, seed, specialize):
         assert np.abs(m - e.cpu().numpy().reshape(base.B, R, w.K).astype(np.float64).mean(1)).max() < 1e-6
     # the trajectories differ from row to row (the noise is applied)
     assert np.abs(st[0] - st[1]).max() > 1e-3 or np.abs(st[1] - st[2]).max() > 1e-3
+
+
+@pytest.mark.parametrize("n,seed", [(14, 0), (18, 1)])
+def test_phase_classes(n, seed):
+    # ZZ-type layers that the generated passes apply as phase classes (one
+    # table lookup of w^cut per amplitude): RZZ on a random graph with one
+    # symbol, ZZ^t with another symbol and scale, RZZ with a constant angle,
+    # and a ZZ^t layer whose symbols differ per edge (no class); states,
+    # expectations, adjoint and parameter-shift gradients against the oracle
+    from paper_2003_02989_amd.circuits import Circuit, const, observable_blob, program_blob, sym
+    rng = np.random.default_rng(4400 + seed)
+    edges = wl.random_regular3(rng, n)
+    dense = sorted({(int(a), int(b)) for a, b in (sorted(rng.choice(n, 2, replace=False)) for _ in range(3 * n))})
+    c = Circuit(n)
+    for q in range(n):
+        c.add("H", q)
+    for a, b in edges:
+        c.add("RZZ", (a, b), [sym(0)])
+    for q in range(n):
+        c.add("RX", q, [sym(1)])
+    for a, b in dense:
+        c.add("ZZPOW", (a, b), [sym(2, -0.7, 0.1)])
+    for a, b in edges:
+        c.add("RZZ", (a, b), [const(0.37)])
+    for q in range(n):
+        c.add("RY", q, [sym(3)])
+    for i, (a, b) in enumerate(edges):
+        c.add("ZZPOW", (a, b), [sym(4 + i % 3)])
+    for q in range(0, n, 2):
+        c.add("RX", q, [sym(1)])
+    B, S = 3, 7
+    theta = rng.uniform(-3, 3, size=(B, S)).astype(np.float32)
+    obs = [[[(0.5, [(a, "Z"), (b, "Z")]) for a, b in edges[:6]] + [(0.3, [(0, "X"), (n - 1, "Y")])]]] * B
+    from paper_2003_02989_amd.workloads import Workload
+    w = Workload("phase_classes", [c] * B, S, theta, obs, rng.standard_normal((B, 1)).astype(np.float32))
+    say("phase classes n", n, "edges", len(edges), "dense", len(dense))
+    compare(gpu_outputs(w, specialize=True), oracle_outputs(w))
+    p = tq.Program(w.program_blob(), specialize=True)
+    o = tq.Observables(w.observable_blob())
+    g = tq.param_shift_grad(p, dev(w.theta), o, dev(w.upstream)).cpu().numpy()
+    ref = orc.param_shift_grad(orc.Program(w.program_blob()), w.theta.astype(np.float64),
+                               orc.Observables(w.observable_blob()), w.upstream.astype(np.float64))
+    say("  parameter-shift error", float(np.abs(g - ref).max()))
+    assert np.abs(g - ref).max() <= 1e-4
