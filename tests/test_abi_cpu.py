@@ -211,3 +211,21 @@ def test_shift_rule_occurrences_and_validation():
     o3 = tq.Observables(observable_blob([[[(1.0, [(0, "Z")])]]]))
     assert L.tq_param_shift_grad(p3._h, fake, o3._h, fake, 0, 0, fake, None) == tq.TQ_E_UNSUPPORTED
     assert b"shift" in L.tq_last_error()
+
+
+def test_empty_batch_is_a_no_op_for_every_compute_call():
+    # a program of no circuits: every compute entry point returns OK without
+    # touching the device (there is none here) or its output pointers
+    L = tq.lib()
+    p = create(program_blob([], 2))
+    o = tq.Observables(observable_blob([]))
+    fake = ctypes.c_void_p(16)
+    assert L.tq_simulate_state(p._h, fake, fake, None) == tq.TQ_OK
+    assert L.tq_expectation(p._h, fake, o._h, fake, None) == tq.TQ_OK
+    assert L.tq_adjoint_grad(p._h, fake, o._h, fake, fake, None, None) == tq.TQ_OK
+    assert L.tq_sample(p._h, fake, 10, 1, fake, None) == tq.TQ_OK
+    assert L.tq_amplitudes(p._h, fake, fake, 4, fake, None) == tq.TQ_OK
+    assert L.tq_sampled_expectation(p._h, fake, o._h, 10, 1, fake, None, None) == tq.TQ_OK
+    assert L.tq_param_shift_grad(p._h, fake, o._h, fake, 0, 0, fake, None) == tq.TQ_OK
+    assert L.tq_param_shift_grad(p._h, fake, o._h, fake, 50, 3, fake, None) == tq.TQ_OK
+    assert L.tq_finite_diff_grad(p._h, fake, o._h, fake, 1e-2, fake, None) == tq.TQ_OK
