@@ -344,14 +344,13 @@ std::string diag_entry(const Env &e, const PassOp &op, int mat, int k)
 // lookup of w^c in a table of powers (LDS, built once per workgroup) and one
 // complex multiply per amplitude; c is summed from the item's bits once per
 // item plus, per register, the class's bits in the stage.  The derived rows
-// of the shift rules move single parameters, so that a class's members may
-// differ there: their launches take a variant of the pass (tq_fwx_<pass>,
-// compiled when first needed) that applies every op on its own.
+// of the parameter shift move one member's parameter: see cut_apply.
 constexpr int kCutMin = 3;
 struct CutClass {
     std::vector<const PassOp *> ops;
     int rep = 0;  // pass-relative matrix offset of one member (its entry 1 is w)
     int tab = 0;  // offset of its powers w^0 .. w^ops.size() in the table
+    int id = 0;   // its index among the pass's classes
 };
 bool cut_key(const Group &g, const PassOp &op, std::tuple<int, int, double, double> *key)
 {
@@ -413,6 +412,7 @@ std::vector<CutClass> cut_classes(const Group &g, const Pass &ps, int *ntab)
             for (CutClass &c : cls) {
                 c.rep = c.ops[0]->mat - ps.mat_begin;
                 c.tab = *ntab;
+                c.id = (int)all.size();
                 *ntab += (int)c.ops.size() + 1;
                 all.push_back(c);
             }
@@ -421,10 +421,13 @@ std::vector<CutClass> cut_classes(const Group &g, const Pass &ps, int *ntab)
     }
     return all;
 }
-// The code applying phase class c on the registers v of a stage of R bits.
-std::string cut_apply(const Env &e, const CutClass &c, int R)
+// The code applying phase class c on the registers v of stage st.  In the
+// derived rows of the parameter shift one member x of a class may hold
+// another w_x (its parameter moved): the workgroup's prologue finds it and the
+// amplitudes where its bits differ take the factor w_x / w as well.
+std::string cut_apply(const Env &e, const CutClass &c, const Stage &st)
 {
-    const int NR = 1 << R;
+    const int R = st.r, NR = 1 << R;
     std::ostringstream o;
     o << "{ uint32_t q_ = 0u";
     std::vector<std::pair<int, std::string>> mixed;  // (register bit, item bit expression)
@@ -454,6 +457,21 @@ std::string cut_apply(const Env &e, const CutClass &c, int R)
             }
         }
         o << " v[" << k << "] = zmul(cutw_[" << c.tab + cst << "u + " << cnt.str() << "], v[" << k << "]);";
+    }
+    o << " }\n";
+    // the moved member (uniform over the workgroup): endpoint s is tile bit s,
+    // or with bit 7 set global bit s & 127 of the tile's fixed bits
+    o << "        if (cutx_[" << c.id << "] != 0xffffffffu) { const uint32_t x_ = cutx_[" << c.id
+      << "], sa_ = x_ & 255u, sb_ = (x_ >> 8) & 255u; const double2 r_ = cutr_[" << c.id << "];";
+    for (int k = 0; k < NR; k++) {
+        uint32_t roff = 0;
+        for (int j = 0; j < R; j++)
+            if ((k >> j) & 1) roff |= 1u << st.bits[j];
+        o << " { const uint32_t i_ = base | " << roff
+          << "u; const uint32_t a_ = (sa_ & 128u) ? ((uint32_t)(fb >> (sa_ & 127u)) & 1u) : ((i_ >> sa_) & 1u);"
+             " const uint32_t b_ = (sb_ & 128u) ? ((uint32_t)(fb >> (sb_ & 127u)) & 1u) : ((i_ >> sb_) & 1u);"
+             " if (a_ ^ b_) v["
+          << k << "] = zmul(r_, v[" << k << "]); }";
     }
     o << " }";
     return o.str();
@@ -691,7 +709,7 @@ void forward_stage(std::ostream &o, const Env &e, const Pass &ps, const Stage &s
                     split_run(e.fgrp, run, &cls, &rest);
                     if (!cls.empty()) {
                         for (size_t ci = 0; ci < cls.size(); ci++)
-                            o << "        " << cut_apply(e, (*e.cuts)[e.cut_next++], R) << "\n";
+                            o << "        " << cut_apply(e, (*e.cuts)[e.cut_next++], st) << "\n";
                         const std::string c = rest.size() > 1 ? diag_run(e, rest, R, {"v"}) : "";
                         if (!c.empty())
                             o << "        " << c << "\n";
@@ -846,6 +864,7 @@ constexpr bool kRevPrefetch = false;
 const char kHead[] =
     "namespace tq {\n"
     "__device__ __forceinline__ double2 zsel(uint32_t c, double2 a, double2 b) { return c ? b : a; }\n"
+    "__device__ __forceinline__ bool zeq(double2 a, double2 b) { return a.x == b.x && a.y == b.y; }\n"
     "__device__ __forceinline__ double2 zpow(double2 w, uint32_t n)\n"
     "{ double2 r = make_double2(1.0, 0.0); while (n) { if (n & 1u) r = zmul(r, w); w = zmul(w, w); n >>= 1; } return r; }\n";
 
@@ -977,7 +996,7 @@ void direct_store(std::ostream &o, const TileGeom &gm, const std::string &fb, co
 
 } // namespace
 
-std::string pass_kernel_source(const Group &g, int pass, bool exact)
+std::string pass_kernel_source(const Group &g, int pass)
 {
     std::ostringstream o;
     const Pass &ps = g.fwd[pass];
@@ -991,7 +1010,7 @@ std::string pass_kernel_source(const Group &g, int pass, bool exact)
     int maxr = 0;
     for (const Stage &st : ps.stages) maxr = std::max(maxr, (int)st.r);
     const int minwg = maxr >= 4 ? 2 : pre ? 3 : 4;
-    o << "extern \"C\" __global__ __launch_bounds__(256, " << minwg << ") void " << (exact ? "tq_fwx_" : "tq_fwd_") << pass
+    o << "extern \"C\" __global__ __launch_bounds__(256, " << minwg << ") void tq_fwd_" << pass
       << "(PassArgs a)\n{\n"
          "    extern __shared__ __align__(16) unsigned char smem[];\n"
          "    const PassCtx c = pass_setup(a, smem);\n"
@@ -1004,14 +1023,34 @@ std::string pass_kernel_source(const Group &g, int pass, bool exact)
     Env e{gm.t, ps.mat_begin, "G", gm.fixed_mask != 0, "", ""};
     e.fgrp = &g;
     int ntab = 0;
-    const std::vector<CutClass> cuts = exact ? std::vector<CutClass>() : cut_classes(g, ps, &ntab);
+    const std::vector<CutClass> cuts = cut_classes(g, ps, &ntab);
     if (!cuts.empty()) {
-        // the powers w^0 .. w^m of each phase class, once per workgroup
+        // per phase class, once per workgroup: the w most members hold (the
+        // first three include two equal ones), the member that differs if
+        // any (a derived row's moved parameter; at most one per class: a move
+        // changes one parameter slot) with w_x / w, and the powers of w
         e.cuts = &cuts;
-        o << "    __shared__ double2 cutw_[" << ntab << "];\n";
+        const size_t nc = cuts.size();
+        o << "    __shared__ double2 cutw_[" << ntab << "], cutm_[" << nc << "], cutr_[" << nc << "];\n"
+          << "    __shared__ uint32_t cutx_[" << nc << "];\n"
+          << "    if (tid == 0) {\n";
+        auto endpoint = [](uint8_t l, uint8_t p) { return l != kFixed ? (uint32_t)l : (0x80u | p); };
+        for (const CutClass &c : cuts) {
+            const int b = ps.mat_begin;
+            o << "    { const double2 w0_ = M[" << c.ops[0]->mat - b << " + 1], w1_ = M[" << c.ops[1]->mat - b
+              << " + 1], w2_ = M[" << c.ops[2]->mat - b << " + 1];\n"
+              << "      const double2 wm_ = (zeq(w0_, w1_) || zeq(w0_, w2_)) ? w0_ : w1_;\n"
+              << "      uint32_t x_ = 0xffffffffu; double2 r_ = make_double2(1.0, 0.0);\n";
+            for (const PassOp *op : c.ops)
+                o << "      { const double2 u_ = M[" << op->mat - b << " + 1]; if (!zeq(u_, wm_)) { x_ = "
+                  << (endpoint(op->l0, op->p0) | (endpoint(op->l1, op->p1) << 8))
+                  << "u; r_ = zmul(u_, make_double2(wm_.x, -wm_.y)); } }\n";
+            o << "      cutm_[" << c.id << "] = wm_; cutr_[" << c.id << "] = r_; cutx_[" << c.id << "] = x_; }\n";
+        }
+        o << "    }\n    __syncthreads();\n";
         for (const CutClass &c : cuts)
-            o << "    for (int j_ = tid; j_ <= " << c.ops.size() << "; j_ += 256) cutw_[" << c.tab << " + j_] = zpow(M["
-              << c.rep << " + 1], (uint32_t)j_);\n";
+            o << "    for (int j_ = tid; j_ <= " << c.ops.size() << "; j_ += 256) cutw_[" << c.tab << " + j_] = zpow(cutm_["
+              << c.id << "], (uint32_t)j_);\n";
         o << "    __syncthreads();\n";
     }
     const std::string scale = pass_scale(e, ps);
@@ -1830,22 +1869,7 @@ std::string pass_chunk(const Group &g, int chunk)
     const int c = rev ? chunk - nf : chunk;
     const int np = rev ? (int)g.rev.size() : (int)g.fwd.size();
     for (int pi = c * kChunkPasses; pi < std::min(np, (c + 1) * kChunkPasses); pi++)
-        body += rev ? rev_pass_kernel_source(g, pi) : pass_kernel_source(g, pi, false);
-    return body + "} // namespace tq\n";
-}
-
-// The op-by-op variants (tq_fwx_<pass>) of the forward passes of a chunk
-// that have phase classes.
-bool pass_has_cuts(const Group &g, int pass)
-{
-    int ntab = 0;
-    return !cut_classes(g, g.fwd[pass], &ntab).empty();
-}
-std::string exact_chunk(const Group &g, int chunk)
-{
-    std::string body = kHead;
-    for (int pi = chunk * kChunkPasses; pi < std::min((int)g.fwd.size(), (chunk + 1) * kChunkPasses); pi++)
-        if (pass_has_cuts(g, pi)) body += pass_kernel_source(g, pi, true);
+        body += rev ? rev_pass_kernel_source(g, pi) : pass_kernel_source(g, pi);
     return body + "} // namespace tq\n";
 }
 
@@ -1902,22 +1926,13 @@ hipError_t memo_kernel(SpecMemo *memo, size_t slot, size_t nslots, Src &&src, co
 
 // Forward or reverse pass kernel `pass` of group g: on the first request on
 // a device every chunk of the group is compiled (in parallel) and loaded.
-// exact: the pass's op-by-op variant (slots after the reverse passes; its
-// chunk is compiled when first asked for).
-hipError_t pass_kernel(const Group &g, bool rev, int pass, hipFunction_t *fn, std::string *log, SpecMemo *memo,
-                       bool exact = false)
+hipError_t pass_kernel(const Group &g, bool rev, int pass, hipFunction_t *fn, std::string *log, SpecMemo *memo)
 {
-    const size_t nslots = 2 * g.fwd.size() + g.rev.size();
-    const size_t slot = exact ? g.fwd.size() + g.rev.size() + (size_t)pass : (rev ? g.fwd.size() : 0) + (size_t)pass;
+    const size_t slot = (rev ? g.fwd.size() : 0) + (size_t)pass, nslots = g.fwd.size() + g.rev.size();
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    const bool known = memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot];
-    if (exact) {
-        const int chunk = pass / kChunkPasses;
-        return memo_kernel(memo, slot, nslots, [&] { return exact_chunk(g, chunk); }, "tq_fwx_" + N(pass), fn, log);
-    }
-    if (!known) {
+    if (!(memo && memo->dev == dev && slot < memo->fn.size() && memo->fn[slot])) {
         e = load_all(pass_chunks(g), log);
         if (e != hipSuccess) return e;
     }
@@ -1943,14 +1958,7 @@ hipError_t launch_pass_spec(const Group &g, int pass, const PassArgs &a, int nro
 {
     if (nrows <= 0) return hipSuccess;
     hipFunction_t fn;
-    bool exact = false;
-    if (a.op_by_op) {
-        // whether the pass has phase classes, asked once per pass
-        if (memo && memo->cuts.size() != g.fwd.size()) memo->cuts.assign(g.fwd.size(), -1);
-        if (memo && memo->cuts[pass] < 0) memo->cuts[pass] = pass_has_cuts(g, pass) ? 1 : 0;
-        exact = memo ? memo->cuts[pass] == 1 : pass_has_cuts(g, pass);
-    }
-    hipError_t e = pass_kernel(g, false, pass, &fn, log, memo, exact);
+    hipError_t e = pass_kernel(g, false, pass, &fn, log, memo);
     if (e != hipSuccess) return e;
     const size_t lds = pass_lds_bytes(a.g, a.product_init != 0, a.mat_end - a.mat_begin);
     return launch(fn, a, nrows * a.wg_per_row, lds, s, "pass");

@@ -26,9 +26,7 @@ std::string resident_source(const Group &g);
 // The specialised forward (tq_fwd_<pass>) and reverse (tq_rev_<pass>) tile
 // pass kernels of group g, to be placed in namespace tq after the shared
 // device code (all passes of a group are compiled as one program).
-// exact: the variant that applies every op on its own (no phase classes),
-// for rows whose class members may differ (tq_fwx_<pass>).
-std::string pass_kernel_source(const Group &g, int pass, bool exact = false);
+std::string pass_kernel_source(const Group &g, int pass);
 std::string rev_pass_kernel_source(const Group &g, int pass);
 
 // Handles of one structure's specialised kernels on one device.  The caller
@@ -39,7 +37,6 @@ struct SpecMemo {
     int dev = -1;
     std::vector<hipFunction_t> fn;  // by kernel slot, null until looked up
     int slots = -1;                 // pauli_spec_slots' answer, -1 until asked
-    std::vector<signed char> cuts;  // forward passes: has phase classes (-1 until asked)
 };
 
 // Launch a specialised kernel of group g, compiled on first use on the

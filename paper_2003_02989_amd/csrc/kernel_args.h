@@ -93,9 +93,6 @@ struct PassArgs {
     int product_init;
     int32_t init_mat[kMaxQubits];
     int mat_begin, mat_end;  // the pass's matrices, staged in LDS
-    // rows whose phase-class members may differ (the derived rows of the
-    // shift rules): the launch takes the generated pass's op-by-op variant
-    int32_t op_by_op;
 };
 
 struct PauliArgs {

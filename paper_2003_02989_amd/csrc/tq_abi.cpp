@@ -433,7 +433,6 @@ void forward(tq_program p, size_t gi, float2 *state, int64_t row_stride, const i
         for (int q = 0; q < kMaxQubits; q++) a.init_mat[q] = g.init_mat[q];
         a.mat_begin = ps.mat_begin;
         a.mat_end = ps.mat_end;
-        a.op_by_op = rr.period > 0;  // a derived row moves single parameters of a class
         if (p->pd->opt.specialize) {
             std::string log;
             const hipError_t e = launch_pass_spec(g, (int)pi, a, nrows, s, &log, &gd.pass_memo);
