@@ -482,8 +482,87 @@ std::string cut_apply(const Env &e, const CutClass &c, const Stage &st)
 // with the out-of-stage bits), then each register of the arrays `arrs` is
 // multiplied once.  Returns "" when op by op is no more expensive (complex
 // multiplies counted).
+// A run of one-qubit diagonal ops on register bits: the diagonal is a tensor
+// product over the bits, so its 2^m entries are built by doubling (one
+// complex multiply per new entry), with the bits' own entries (the product
+// of the ops on each bit) as factors.  "" when op by op is no more expensive.
+std::string diag_run_tensor(const Env &e, const std::vector<const PassOp *> &run, int R,
+                            const std::vector<std::string> &arrs)
+{
+    std::vector<int> jb;                       // register bits, ascending
+    std::map<int, std::vector<const PassOp *>> on;
+    for (const PassOp *op : run) {
+        if (op->kind != K_D1 || op->s0 == kFixed) return "";
+        on[op->s0].push_back(op);
+    }
+    for (auto &kv : on) jb.push_back(kv.first);
+    const int NR = 1 << R;
+    std::ostringstream b;
+    int mults = 0, direct = 0, nv = 0;
+    auto fresh = [&]() { return "t" + N(nv++) + "_"; };
+    // per bit: its entries for bit value 0 and 1 ("" = exactly 1)
+    std::vector<std::array<std::string, 2>> eb;
+    for (int bit : jb) {
+        std::array<std::string, 2> v{"", ""};
+        for (int x = 0; x < 2; x++)
+            for (const PassOp *op : on[bit]) {
+                const std::string en = diag_entry(e, *op, op->mat - e.mbase, x << bit);
+                if (en.empty()) continue;
+                if (v[x].empty()) {
+                    v[x] = en;
+                } else {
+                    const std::string t = fresh();
+                    b << "const double2 " << t << " = zmul(" << v[x] << ", " << en << "); ";
+                    v[x] = t;
+                    mults++;
+                }
+            }
+        eb.push_back(v);
+    }
+    for (const PassOp *op : run)
+        for (int k = 0; k < NR; k++) direct += !diag_entry(e, *op, op->mat - e.mbase, k).empty();
+    // doubling over the bits: entry j of the table (bit i of j: bit jb[i])
+    std::vector<std::string> tab(1, "");
+    for (size_t i = 0; i < jb.size(); i++) {
+        std::vector<std::string> nt(tab.size() * 2);
+        for (size_t j = 0; j < tab.size(); j++)
+            for (int x = 0; x < 2; x++) {
+                const std::string &f = eb[i][x];
+                std::string r;
+                if (tab[j].empty()) r = f;
+                else if (f.empty()) r = tab[j];
+                else {
+                    r = fresh();
+                    b << "const double2 " << r << " = zmul(" << tab[j] << ", " << f << "); ";
+                    mults++;
+                }
+                nt[j | ((size_t)x << i)] = r;
+            }
+        tab.swap(nt);
+    }
+    auto proj = [&](int k) {
+        int j = 0;
+        for (size_t i = 0; i < jb.size(); i++)
+            if ((k >> jb[i]) & 1) j |= 1 << i;
+        return j;
+    };
+    std::ostringstream a;
+    for (const std::string &v : arrs)
+        for (int k = 0; k < NR; k++)
+            if (!tab[proj(k)].empty()) {
+                a << v << "[" << k << "] = zmul(" << tab[proj(k)] << ", " << v << "[" << k << "]); ";
+                mults++;
+            }
+    if (mults >= direct * (int)arrs.size()) return "";
+    return "{ " + b.str() + a.str() + "}";
+}
+
 std::string diag_run(const Env &e, const std::vector<const PassOp *> &run, int R, const std::vector<std::string> &arrs)
 {
+    {
+        const std::string t = diag_run_tensor(e, run, R, arrs);
+        if (!t.empty()) return t;
+    }
     int jm = 0;  // register bits the run touches
     for (const PassOp *op : run) {
         if (op->s0 != kFixed) jm |= 1 << op->s0;

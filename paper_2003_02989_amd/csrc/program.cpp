@@ -585,6 +585,41 @@ void make_stages(Pass &ps, int rmax, int rdense, Group &g, const std::map<int32_
     std::vector<PassOp> ops(nops);
     for (int k = 0; k < nops; k++) ops[k] = ps.ops[best.order[k]];
     ps.ops = std::move(ops);
+    // diagonal ops move past the non-diagonal ops of their stage that act on
+    // other qubits (the two commute, and so do their generators), so that a
+    // stage's diagonal ops form runs the kernels apply as one diagonal: later
+    // in forward stages (a layer's RZ after its RY), earlier in reverse ones
+    // (the layer's daggers come in the opposite order)
+    auto is_d = [](const PassOp &op) { return op.kind == K_D1 || op.kind == K_D2; };
+    auto disjoint = [](const PassOp &a, const PassOp &b) {
+        auto qs = [](const PassOp &op, int *q) {
+            int n = 0;
+            q[n++] = op.p0;
+            if (op.kind == K_M2 || op.kind == K_D2 || op.kind == K_P2 || op.kind == K_F2 || (op.kind == K_M1 && op.ctrl))
+                q[n++] = op.p1;
+            return n;
+        };
+        int qa[2], qb[2];
+        const int na = qs(a, qa), nb = qs(b, qb);
+        for (int i = 0; i < na; i++)
+            for (int j = 0; j < nb; j++)
+                if (qa[i] == qb[j]) return false;
+        return true;
+    };
+    for (const auto &sl : best.st) {
+        if (forward) {
+            for (int k = sl.end - 2; k >= sl.begin; k--)
+                for (int i = k; i + 1 < sl.end && is_d(ps.ops[i]) && !is_d(ps.ops[i + 1]) &&
+                                disjoint(ps.ops[i], ps.ops[i + 1]);
+                     i++)
+                    std::swap(ps.ops[i], ps.ops[i + 1]);
+        } else {
+            for (int k = sl.begin + 1; k < sl.end; k++)
+                for (int i = k; i > sl.begin && is_d(ps.ops[i]) && !is_d(ps.ops[i - 1]) && disjoint(ps.ops[i], ps.ops[i - 1]);
+                     i--)
+                    std::swap(ps.ops[i], ps.ops[i - 1]);
+        }
+    }
 
     for (auto &sl : best.st) {
         const std::vector<int> &bits = sl.bits;
