@@ -111,9 +111,11 @@ def test_specialized_kernels_compile_for_gfx950():
     # gfx950 (no device needed): the two resident configurations, random
     # resident structures over the whole opcode set, and the forward and
     # reverse tile passes of a 14-qubit random structure
+    # (and the QAOA and VQE structures: phase classes, diagonal runs)
     for w in (wl.c1_hea(), wl.c2_qnn(B=4),
               wl.random_batch(6601, B=3, n=10, n_gates=60, n_symbols=5, K=3, hetero=True),
-              wl.random_batch(1412, B=2, n=14, n_gates=60, n_symbols=5, K=2)):
+              wl.random_batch(1412, B=2, n=14, n_gates=60, n_symbols=5, K=2),
+              wl.c3_qaoa(B=2), wl.c5_vqe(B=2, layers=3)):
         p = create(w.program_blob(), specialize=True)
         tq.specialize(p, "gfx950")
     # a program without the option has nothing to compile
